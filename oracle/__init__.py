@@ -1,0 +1,187 @@
+"""LoGra float64 CPU oracle -- test infrastructure, not part of the product.
+
+Thin numpy wrappers over ``logra_oracle.c``: a plain, slow float64
+implementation of what the LoGra hot path computes (arXiv 2405.13954,
+Sec. 2 Eq. (2)-(3), Sec. 3.1 Eq. (4)-(5), App. C and App. D).  Only the test
+suite, the smoke check and the benchmark's CPU-baseline leg may import this
+package; the product path never does, and this package imports nothing from
+it.
+
+Array conventions: numpy arrays on the host; bf16 data is carried as uint16
+bit patterns, fp32 as float32, fp64 as float64.  Outputs are float64.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "logra_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liblogra_oracle.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_NOT_PD = -4
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (C99, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        cmd = ["gcc", "-std=c99", "-O2", "-fno-fast-math", "-fopenmp", "-fPIC", "-shared",
+               _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        # LOGRA_ORACLE_LIB points the tests at a deliberately broken build of
+        # this file (the mutation test); normally unset.
+        path = os.environ.get("LOGRA_ORACLE_LIB")
+        if not path:
+            path = _LIB_PATH
+            if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_SRC):
+                build(force=True)
+        L = ctypes.CDLL(path)
+        vp, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        proj = [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp]
+        L.oracle_project_factored.argtypes = proj
+        L.oracle_project_dense.argtypes = proj
+        L.oracle_cov_accumulate.argtypes = [vp, i32, i64, i32, i32, vp]
+        L.oracle_precondition.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp, i64, vp]
+        L.oracle_scores.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, vp, i64]
+        L.oracle_topk.argtypes = [vp, i64, i32, i64, i64, i32, vp, vp]
+        L.oracle_num_threads.argtypes = []
+        for name in ("oracle_project_factored", "oracle_project_dense", "oracle_cov_accumulate",
+                     "oracle_precondition", "oracle_scores", "oracle_topk", "oracle_num_threads"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _code(a: np.ndarray) -> int:
+    if a.dtype == np.float32:
+        return 0
+    if a.dtype == np.uint16:
+        return 1
+    if a.dtype == np.float64:
+        return 2
+    raise TypeError(f"oracle: unsupported dtype {a.dtype}")
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a):
+    return None if a is None else np.ascontiguousarray(a)
+
+
+def _check(rc: int, what: str):
+    if rc == ERR_NOT_PD:
+        raise np.linalg.LinAlgError(f"{what}: matrix is not positive definite")
+    if rc != OK:
+        raise ValueError(f"{what}: status {rc}")
+
+
+def _project(fn, x, dy, p_in, p_out, mask=None):
+    x, dy, p_in, p_out, mask = map(_c, (x, dy, p_in, p_out, mask))
+    B, T, n_in = x.shape
+    n_out = dy.shape[2]
+    k_in, k_out = p_in.shape[0], p_out.shape[0]
+    code = _code(x)
+    assert _code(dy) == code and _code(p_in) == code and _code(p_out) == code
+    assert dy.shape[:2] == (B, T) and p_in.shape[1] == n_in and p_out.shape[1] == n_out
+    if mask is not None:
+        mask = mask.astype(np.uint8, copy=False)
+        assert mask.shape == (B, T)
+    g = np.zeros((B, k_out * k_in), dtype=np.float64)
+    rc = fn(_ptr(x), _ptr(dy), code, B, T, n_in, n_out, _ptr(mask), _ptr(p_in), _ptr(p_out),
+            k_in, k_out, _ptr(g))
+    _check(rc, fn.__name__)
+    return g
+
+
+def project_factored(x, dy, p_in, p_out, mask=None) -> np.ndarray:
+    """Eq. (5) right side: G_b = sum_t (P_out dy_t)(P_in x_t)^T over unmasked tokens.
+    Returns [B, k_out*k_in] float64, flat index o*k_in + i."""
+    return _project(lib().oracle_project_factored, x, dy, p_in, p_out, mask)
+
+
+def project_dense(x, dy, p_in, p_out, mask=None) -> np.ndarray:
+    """Eq. (4) then Eq. (5) left side: P_out (sum_t dy_t x_t^T) P_in^T.  Small inputs only."""
+    return _project(lib().oracle_project_dense, x, dy, p_in, p_out, mask)
+
+
+def cov_accumulate(g, S=None) -> np.ndarray:
+    """S += sum_b g_b g_b^T (float64).  g: [B, D] (any oracle dtype)."""
+    g = _c(g)
+    B, D = g.shape
+    if S is None:
+        S = np.zeros((D, D), dtype=np.float64)
+    assert S.dtype == np.float64 and S.shape == (D, D) and S.flags.c_contiguous
+    rc = lib().oracle_cov_accumulate(_ptr(g), _code(g), D, B, D, _ptr(S))
+    _check(rc, "oracle_cov_accumulate")
+    return S
+
+
+def precondition(S, N: int, damp_ratio: float, g_test):
+    """(S/N + lambda I)^{-1} g_q for each row q, lambda = damp_ratio * tr(S/N) / D.
+    damp_ratio < 0: identity.  Returns (out [Q, D] float64, lambda)."""
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    g_test = _c(g_test)
+    Q, D = g_test.shape
+    assert S.shape == (D, D)
+    out = np.zeros((Q, D), dtype=np.float64)
+    lam = ctypes.c_double(0.0)
+    rc = lib().oracle_precondition(_ptr(S), D, int(N), float(damp_ratio), _ptr(g_test),
+                                   _code(g_test), D, Q, _ptr(out), D, ctypes.byref(lam))
+    _check(rc, "oracle_precondition")
+    return out, lam.value
+
+
+def precondition_status(S, N: int, damp_ratio: float, g_test) -> int:
+    """Status code of oracle_precondition (OK or ERR_NOT_PD) without raising."""
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    g_test = _c(g_test)
+    Q, D = g_test.shape
+    out = np.zeros((Q, D), dtype=np.float64)
+    return lib().oracle_precondition(_ptr(S), D, int(N), float(damp_ratio), _ptr(g_test),
+                                     _code(g_test), D, Q, _ptr(out), D, None)
+
+
+def scores(te, tr) -> np.ndarray:
+    """s[q, j] = <te_q, tr_j> in float64.  te: [Q, D], tr: [N, D]."""
+    te, tr = _c(te), _c(tr)
+    Q, D = te.shape
+    N = tr.shape[0]
+    assert tr.shape[1] == D
+    s = np.zeros((Q, N), dtype=np.float64)
+    rc = lib().oracle_scores(_ptr(te), _code(te), D, Q, _ptr(tr), _code(tr), D, N, D, _ptr(s),
+                             max(N, 1))
+    _check(rc, "oracle_scores")
+    return s
+
+
+def topk(s, k: int, base: int = 0):
+    """Top-k per row: largest values first, ties to the lower index; pads (-inf, -1).
+    Returns (val [Q, k] float64, idx [Q, k] int64)."""
+    s = np.ascontiguousarray(s, dtype=np.float64)
+    Q, N = s.shape
+    val = np.empty((Q, k), dtype=np.float64)
+    idx = np.empty((Q, k), dtype=np.int64)
+    rc = lib().oracle_topk(_ptr(s), max(N, 1), Q, N, int(base), int(k), _ptr(val), _ptr(idx))
+    _check(rc, "oracle_topk")
+    return val, idx
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())

@@ -1,0 +1,58 @@
+"""The oracle's pins must catch plausible slips in the oracle itself.
+
+Each case plants one mistake in a copy of the oracle's C source (CPU only),
+builds it, and runs the pin suite against it; the suite must fail.
+"""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "logra_oracle.c")
+
+MUTATIONS = {
+    "transposed_G_layout": ("gb[(int64_t)o * k_in + i] += dp[o] * xp[i]",
+                            "gb[(int64_t)i * k_out + o] += dp[o] * xp[i]"),
+    "mask_ignored": ("if (mask && mask[bt] == 0) continue; /* masked: never read */", ""),
+    "mask_multiply_not_select": ("if (mask && mask[bt] == 0) continue; /* masked: never read */",
+                                 "double mm = mask ? (double)mask[bt] : 1.0;"),
+    "mean_not_sum_over_tokens": ("gb[(int64_t)o * k_in + i] += dp[o] * xp[i];",
+                                 "gb[(int64_t)o * k_in + i] += dp[o] * xp[i] / (double)T;"),
+    "cov_missing_term": ("for (int b = 0; b < B; ++b)\n                s += widen(g",
+                         "for (int b = 1; b < B; ++b)\n                s += widen(g"),
+    "damping_uses_D_minus_1": ("double lambda = r * tr / (double)D;",
+                               "double lambda = r * tr / (double)(D - 1);"),
+    "damping_unnormalised_S": ("tr += S[(int64_t)d * D + d] / (double)N;",
+                               "tr += S[(int64_t)d * D + d];"),
+    "backsolve_wrong_index": ("s -= L[(int64_t)m * D + i] * z[m];",
+                              "s -= L[(int64_t)i * D + m] * z[m];"),
+    "scores_sign": ("acc += widen(te", "acc -= widen(te"),
+    "topk_ties_to_higher_index": ("return ia < ib;", "return ia > ib;"),
+    "bf16_widen_wrong_shift": ("<< 16;", "<< 15;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_catch_mutation(name):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert old in src, f"mutation anchor not found: {name}"
+    src = src.replace(old, new, 1)
+    if name == "mask_multiply_not_select":
+        # a multiply-by-mask version: reads masked tokens and scales them by 0
+        src = src.replace("gb[(int64_t)o * k_in + i] += dp[o] * xp[i];",
+                          "gb[(int64_t)o * k_in + i] += mm * dp[o] * xp[i];", 1)
+    with tempfile.TemporaryDirectory() as td:
+        c = os.path.join(td, "m.c")
+        so = os.path.join(td, "m.so")
+        open(c, "w").write(src)
+        subprocess.run(["gcc", "-std=c99", "-O2", "-fopenmp", "-fPIC", "-shared", c, "-o", so, "-lm"],
+                       check=True)
+        env = dict(os.environ, LOGRA_ORACLE_LIB=so)
+        r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                            os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                           env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
+        assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"
