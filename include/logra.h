@@ -1,0 +1,203 @@
+/*
+ * logra.h -- C ABI of the LoGra hot path on AMD Instinct MI355X (gfx950).
+ *
+ * LoGra (Choe et al., arXiv 2405.13954) values training data with influence
+ * functions computed in a low-dimensional gradient space.  This library
+ * implements the data-parallel hot path of that method:
+ *
+ *   logging   : per-example structured gradient projection (Sec. 3.1, Eq. (5))
+ *               and the projected Fisher covariance (Sec. 2 Eq. (3); App. D)
+ *   influence : damped inverse applied to test gradients (Sec. 2 Eq. (2),
+ *               step (1); damping of App. C), the score GEMM against stored
+ *               training gradients (Eq. (2), step (2)) and per-query top-k.
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are caller-owned DEVICE memory (hipMalloc or a framework
+ *     allocator).  Host pointers are rejected with LOGRA_ERR_INVALID_ARG.
+ *     The library allocates no device memory; scratch space ("workspace") is
+ *     passed in by the caller after a *_ws_size query.
+ *   - Arrays are row-major with the last index contiguous; a "leading
+ *     dimension" (ld) is a row stride in ELEMENTS.
+ *   - Base pointers and row strides in bytes must be multiples of 16 (the
+ *     kernels use 128-bit loads); otherwise LOGRA_ERR_INVALID_ARG.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *     on it and the call returns without waiting, except where stated.
+ *   - Calls return a logra_status and never abort; logra_last_error() gives a
+ *     thread-local message for the last non-OK return.  Kernel faults surface
+ *     as HIP errors at the caller's next synchronisation.
+ *   - bf16 outputs are rounded from fp32 to nearest, ties to even.
+ *   - All functions are reentrant; calls that share an output buffer must be
+ *     ordered by the caller (same stream or events).
+ */
+#ifndef LOGRA_H
+#define LOGRA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LOGRA_OK = 0,
+    LOGRA_ERR_INVALID_ARG = -1, /* bad pointer, size, stride, alignment or dtype */
+    LOGRA_ERR_UNSUPPORTED = -2, /* valid request beyond a compiled limit */
+    LOGRA_ERR_HIP = -3,         /* a HIP runtime call failed */
+    LOGRA_ERR_NOT_PD = -4,      /* damped covariance is not positive definite */
+    LOGRA_ERR_WORKSPACE = -5    /* workspace missing or smaller than *_ws_size */
+} logra_status;
+
+typedef enum { LOGRA_F32 = 0, LOGRA_BF16 = 1 } logra_dtype;
+
+/* Compiled limits. */
+#define LOGRA_MAX_K 128          /* k_in, k_out of one projection */
+#define LOGRA_MAX_GROUP 16       /* layers in one logra_project_layers call */
+#define LOGRA_MAX_PRECOND_D 8192 /* dimension of one preconditioner block */
+#define LOGRA_MAX_TOPK 1024
+
+const char *logra_last_error(void);
+const char *logra_version(void);
+
+/* ------------------------------------------------------------------------
+ * Per-example structured gradient projection of one linear layer
+ * (Sec. 3.1, Eq. (4)-(5)):
+ *
+ *     G_b = sum_{t : mask[b,t] != 0}  (P_out dy_{b,t}) (P_in x_{b,t})^T
+ *
+ * the k_out x k_in projected gradient of example b, formed from the
+ * projected activations without materialising the n_out x n_in gradient.
+ * The sum runs over tokens (summed, not averaged, loss).
+ *
+ *   x      [B][T][n_in]   layer inputs (forward activations), in_dtype
+ *   dy     [B][T][n_out]  gradients w.r.t. the layer outputs, in_dtype
+ *   mask   [B][T] uint8   token t of example b contributes iff mask != 0;
+ *                         NULL = every token contributes.  Masked tokens are
+ *                         never read: their contribution is exactly zero even
+ *                         if their slots hold NaN or Inf.
+ *   p_in   [k_in][n_in]   and p_out [k_out][n_out], in_dtype
+ *   g_out  row b of the result is written at g_out + b * g_ld (elements),
+ *          flattened out-major: element o * k_in + i holds G_b[o][i].
+ *          g_dtype F32 or BF16.  Rows may interleave with other layers'
+ *          columns of a gradient store (g_ld >= k_in * k_out).
+ *   ws     workspace of at least logra_project_ws_size(B, T, k_in, k_out)
+ *          bytes; contents on entry are ignored.
+ * Limits: n_in, n_out multiples of 8 (bf16) or 4 (fp32); 1 <= k <= LOGRA_MAX_K.
+ * B = 0 or T = 0 is a no-op.  Deterministic: reruns are bitwise identical.
+ * ---------------------------------------------------------------------- */
+size_t logra_project_ws_size(int B, int T, int k_in, int k_out);
+int logra_project_layer(const void *x, const void *dy, int in_dtype, int B, int T, int n_in,
+                        int n_out, const uint8_t *mask, const void *p_in, const void *p_out,
+                        int k_in, int k_out, void *g_out, int g_dtype, int64_t g_ld, void *ws,
+                        size_t ws_bytes, void *stream);
+
+/* The same projection for up to LOGRA_MAX_GROUP layers of one batch in one
+ * launch (the layers share B, T, mask, k_in, k_out, dtypes and g_ld; each has
+ * its own tensors and output base).  Results are identical to calling
+ * logra_project_layer once per layer. */
+typedef struct {
+    const void *x;
+    const void *dy;
+    const void *p_in;
+    const void *p_out;
+    void *g_out;
+    int n_in;
+    int n_out;
+} logra_layer_desc;
+
+size_t logra_project_layers_ws_size(int n_layers, int B, int T, int k_in, int k_out);
+int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
+                         const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Projected Fisher covariance (Sec. 2 Eq. (3) P H P^T; App. D Assumption 1:
+ * the empirical Fisher over training examples):
+ *
+ *     S += sum_{b < B} g_b g_b^T
+ *
+ *   g   B rows of D elements at row stride ld (elements), g_dtype F32/BF16
+ *   S   [D][D] fp32, caller-initialised (zero for a new statistic), updated
+ *       in place and kept exactly symmetric (the upper triangle is computed
+ *       and mirrored).  The caller tracks the example count N; S is not
+ *       normalised here.
+ * bf16 inputs use bf16 MFMA with fp32 accumulation; fp32 inputs use fp32
+ * arithmetic.  B = 0 is a no-op.  Deterministic.
+ * ---------------------------------------------------------------------- */
+int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, float *S,
+                         void *stream);
+
+/* Block-diagonal form for many layers at once: columns [l*D, (l+1)*D) of g
+ * update S + l*D*D, for l < n_blocks.  Same semantics per block. */
+int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, int D,
+                                int n_blocks, float *S, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Damped inverse applied to test gradients, for one layer block (the iHVP
+ * step (1) of Sec. 2 Eq. (2) in the projected space of Eq. (3)):
+ *
+ *     C = S / N,   lambda = damp_ratio * tr(C) / D   (damp_ratio x the mean
+ *                                                     eigenvalue, App. C)
+ *     g_out[q] = (C + lambda I)^{-1} g_test[q]        for q < Q
+ *
+ * computed by a float64 Cholesky factorisation and two triangular solves.
+ * damp_ratio < 0 selects the identity preconditioner (g_out = g_test).
+ *
+ *   S       [D][D] fp32 covariance from logra_cov_accumulate (lower triangle
+ *           is read); N > 0 the number of examples accumulated into it
+ *   g_test  Q rows of D at stride ld_in, in_dtype;  g_out Q rows of D at
+ *           stride ld_out, out_dtype (may not alias g_test)
+ *   ws      workspace of logra_precondition_ws_size(D, 1, Q) bytes
+ * SYNCHRONOUS: waits for `stream`, so that a non-positive pivot can be
+ * returned as LOGRA_ERR_NOT_PD (g_out is then unspecified).
+ * D <= LOGRA_MAX_PRECOND_D.
+ * ---------------------------------------------------------------------- */
+size_t logra_precondition_ws_size(int D, int n_blocks, int Q);
+int logra_precondition(const float *S, int D, int64_t N, double damp_ratio, const void *g_test,
+                       int in_dtype, int64_t ld_in, int Q, void *g_out, int out_dtype,
+                       int64_t ld_out, void *ws, size_t ws_bytes, void *stream);
+
+/* Block-diagonal form: block l uses S + l*D*D and columns [l*D, (l+1)*D) of
+ * g_test and g_out, each with its own lambda_l.  NOT_PD if any block fails
+ * (logra_last_error names the first). */
+int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                              const void *g_test, int in_dtype, int64_t ld_in, int Q, void *g_out,
+                              int out_dtype, int64_t ld_out, void *ws, size_t ws_bytes,
+                              void *stream);
+
+/* ------------------------------------------------------------------------
+ * Influence scores and per-query top-k (Sec. 2 Eq. (2) step (2): the dot
+ * product of each preconditioned test gradient with every stored training
+ * gradient; with a block-diagonal Hessian this is one dot product over the
+ * concatenated layer blocks; top-k of the most valuable data, Sec. 4.1):
+ *
+ *     s[q][j] = sum_{d < D} g_test_pre[q][d] * g_train[j][d]
+ *
+ *   g_test_pre  Q rows at stride ld_te;  g_train N_chunk rows at stride ld_tr.
+ *               Both BF16 (bf16 MFMA, fp32 accumulation) or both F32.
+ *   scores      optional [Q][ld_s] fp32 output (NULL = not materialised by
+ *               the caller; it then lives in the workspace).
+ *   topk        0 = no selection; else 1..LOGRA_MAX_TOPK entries per query
+ *               into topk_val [Q][topk] (fp32) and topk_idx [Q][topk]
+ *               (int64 global train index train_base + j), sorted by value
+ *               descending, ties to the lower index.  Slots beyond the
+ *               number of candidates hold (-inf, -1).
+ *   merge       0: the top-k buffers are overwritten with this chunk's top-k;
+ *               1: they hold a running top-k (from earlier chunks) that is
+ *               merged with this chunk's candidates.  Calling once per chunk
+ *               with merge=1 after the first gives the top-k of all chunks.
+ *   ws          workspace of logra_influence_ws_size(Q, N_chunk, topk,
+ *               scores != NULL) bytes.
+ * Scores of NaN order unspecified.
+ * ---------------------------------------------------------------------- */
+size_t logra_influence_ws_size(int Q, int64_t N_chunk, int topk, int scores_given);
+int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
+                           const void *g_train, int tr_dtype, int64_t ld_tr, int64_t N_chunk,
+                           int D, int64_t train_base, float *scores, int64_t ld_s, int topk,
+                           float *topk_val, int64_t *topk_idx, int merge, void *ws,
+                           size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LOGRA_H */

@@ -1,0 +1,248 @@
+"""LoGra hot path on MI355X: thin Python binding of ``libpaper_logra.so``.
+
+Each function has the name of the C entry point it calls (``include/logra.h``)
+and only marshals arguments: torch device tensors become raw pointers, the
+current torch stream becomes the HIP stream, and a non-OK status becomes a
+``LograError``.  All computation happens in the HIP kernels.  The library must
+have been built (``paper_2405_13954_amd.build.build()``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = [
+    "LograError", "lib", "F32", "BF16",
+    "logra_version", "logra_last_error",
+    "logra_project_ws_size", "logra_project_layer",
+    "logra_project_layers_ws_size", "logra_project_layers",
+    "logra_cov_accumulate", "logra_cov_accumulate_blocks",
+    "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
+    "logra_influence_ws_size", "logra_influence_scores",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpaper_logra.so")
+
+F32, BF16 = 0, 1
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NOT_PD, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
+MAX_GROUP = 16
+
+EXPORTED = (
+    "logra_last_error", "logra_version",
+    "logra_project_ws_size", "logra_project_layer",
+    "logra_project_layers_ws_size", "logra_project_layers",
+    "logra_cov_accumulate", "logra_cov_accumulate_blocks",
+    "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
+    "logra_influence_ws_size", "logra_influence_scores",
+)
+
+
+class LograError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"logra status {status}: {msg}")
+        self.status = status
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("dy", ctypes.c_void_p), ("p_in", ctypes.c_void_p),
+                ("p_out", ctypes.c_void_p), ("g_out", ctypes.c_void_p),
+                ("n_in", ctypes.c_int), ("n_out", ctypes.c_int)]
+
+
+_lib = None
+
+
+def lib():
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2405_13954_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, sz, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
+        L.logra_last_error.restype = ctypes.c_char_p
+        L.logra_version.restype = ctypes.c_char_p
+        L.logra_project_ws_size.argtypes = [i32, i32, i32, i32]
+        L.logra_project_ws_size.restype = sz
+        L.logra_project_layer.argtypes = [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp, i32,
+                                          i64, vp, sz, vp]
+        L.logra_project_layers_ws_size.argtypes = [i32, i32, i32, i32, i32]
+        L.logra_project_layers_ws_size.restype = sz
+        L.logra_project_layers.argtypes = [ctypes.POINTER(LayerDesc), i32, i32, i32, i32, vp, i32, i32,
+                                           i32, i64, vp, sz, vp]
+        L.logra_cov_accumulate.argtypes = [vp, i32, i64, i32, i32, vp, vp]
+        L.logra_cov_accumulate_blocks.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
+        L.logra_precondition_ws_size.argtypes = [i32, i32, i32]
+        L.logra_precondition_ws_size.restype = sz
+        L.logra_precondition.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp, i32, i64, vp, sz, vp]
+        L.logra_precondition_blocks.argtypes = [vp, i32, i32, i64, f64, vp, i32, i64, i32, vp, i32, i64,
+                                                vp, sz, vp]
+        L.logra_influence_ws_size.argtypes = [i32, i64, i32, i32]
+        L.logra_influence_ws_size.restype = sz
+        L.logra_influence_scores.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, vp, i64, i32,
+                                             vp, vp, i32, vp, sz, vp]
+        for name in ("logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
+                     "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
+                     "logra_influence_scores"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+# ------------------------------------------------------------------ helpers --
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise LograError(rc, lib().logra_last_error().decode())
+
+
+def _workspace(nbytes: int, device, ws=None):
+    if nbytes == 0:
+        return None, 0
+    if ws is None:
+        ws = _torch().empty(nbytes, dtype=_torch().uint8, device=device)
+    return ws, ws.numel() * ws.element_size()
+
+
+def _rows(t, width: int):
+    """Row stride (elements) of a 2-D view whose rows are contiguous."""
+    assert t.dim() == 2 and t.stride(1) == 1 and t.shape[1] >= width, "rows must be contiguous"
+    return t.stride(0)
+
+
+# --------------------------------------------------------------- entry points --
+def logra_version() -> str:
+    return lib().logra_version().decode()
+
+
+def logra_last_error() -> str:
+    return lib().logra_last_error().decode()
+
+
+def logra_project_ws_size(B, T, k_in, k_out) -> int:
+    return int(lib().logra_project_ws_size(B, T, k_in, k_out))
+
+
+def logra_project_layers_ws_size(n_layers, B, T, k_in, k_out) -> int:
+    return int(lib().logra_project_layers_ws_size(n_layers, B, T, k_in, k_out))
+
+
+def logra_project_layer(x, dy, p_in, p_out, g_out, mask=None, ws=None, stream=None):
+    """G_b = sum_t m (P_out dy_bt)(P_in x_bt)^T into g_out rows (Sec. 3.1, Eq. (5)).
+
+    x [B,T,n_in], dy [B,T,n_out], p_in [k_in,n_in], p_out [k_out,n_out] (same dtype),
+    mask [B,T] uint8 or None, g_out [B, >=k_out*k_in] (a column slice of a store is fine).
+    """
+    B, T, n_in = x.shape
+    n_out = dy.shape[2]
+    k_in, k_out = p_in.shape[0], p_out.shape[0]
+    g_ld = _rows(g_out, k_in * k_out) if B > 0 else k_in * k_out
+    ws, wsb = _workspace(logra_project_ws_size(B, T, k_in, k_out), x.device, ws)
+    _check(lib().logra_project_layer(_ptr(x), _ptr(dy), _dtype_code(x), B, T, n_in, n_out, _ptr(mask),
+                                     _ptr(p_in), _ptr(p_out), k_in, k_out, _ptr(g_out), _dtype_code(g_out),
+                                     g_ld, _ptr(ws), wsb, _stream(stream)))
+
+
+def logra_project_layers(layers, mask=None, ws=None, stream=None):
+    """Grouped projection of up to 16 layers of one batch.  layers: list of dicts with x, dy,
+    p_in, p_out, g_out (shared B, T, k, dtypes and g_out row stride)."""
+    n = len(layers)
+    arr = (LayerDesc * n)()
+    x0 = layers[0]["x"]
+    B, T, _ = x0.shape
+    k_in, k_out = layers[0]["p_in"].shape[0], layers[0]["p_out"].shape[0]
+    g0 = layers[0]["g_out"]
+    g_ld = _rows(g0, k_in * k_out) if B > 0 else k_in * k_out
+    for i, L in enumerate(layers):
+        arr[i] = LayerDesc(L["x"].data_ptr(), L["dy"].data_ptr(), L["p_in"].data_ptr(),
+                           L["p_out"].data_ptr(), L["g_out"].data_ptr(), L["x"].shape[2], L["dy"].shape[2])
+    ws, wsb = _workspace(logra_project_layers_ws_size(n, B, T, k_in, k_out), x0.device, ws)
+    _check(lib().logra_project_layers(arr, n, _dtype_code(x0), B, T, _ptr(mask), k_in, k_out,
+                                      _dtype_code(g0), g_ld, _ptr(ws), wsb, _stream(stream)))
+
+
+def logra_cov_accumulate(g, S, stream=None):
+    """S [D,D] fp32 += sum_b g_b g_b^T for g [B, D] (rows contiguous)."""
+    B, D = g.shape
+    ld = _rows(g, D) if B > 0 else D
+    _check(lib().logra_cov_accumulate(_ptr(g), _dtype_code(g), ld, B, D, _ptr(S), _stream(stream)))
+
+
+def logra_cov_accumulate_blocks(g, S, D: int, stream=None):
+    """S [n_blocks, D, D] fp32; block l += G[:, l*D:(l+1)*D]^T G[:, l*D:(l+1)*D]."""
+    B = g.shape[0]
+    n_blocks = S.shape[0]
+    ld = _rows(g, D * n_blocks) if B > 0 else D * n_blocks
+    _check(lib().logra_cov_accumulate_blocks(_ptr(g), _dtype_code(g), ld, B, D, n_blocks, _ptr(S),
+                                             _stream(stream)))
+
+
+def logra_precondition_ws_size(D, n_blocks, Q) -> int:
+    return int(lib().logra_precondition_ws_size(D, n_blocks, Q))
+
+
+def logra_precondition(S, N: int, damp_ratio: float, g_test, g_out, ws=None, stream=None):
+    """g_out[q] = (S/N + lambda I)^{-1} g_test[q], lambda = damp_ratio * tr(S/N)/D (synchronous)."""
+    D = S.shape[0]
+    Q = g_test.shape[0]
+    ld_in = _rows(g_test, D) if Q > 0 else D
+    ld_out = _rows(g_out, D) if Q > 0 else D
+    ws, wsb = _workspace(logra_precondition_ws_size(D, 1, Q) if damp_ratio >= 0 else 0, S.device, ws)
+    _check(lib().logra_precondition(_ptr(S), D, int(N), float(damp_ratio), _ptr(g_test), _dtype_code(g_test),
+                                    ld_in, Q, _ptr(g_out), _dtype_code(g_out), ld_out, _ptr(ws), wsb,
+                                    _stream(stream)))
+
+
+def logra_precondition_blocks(S, N: int, damp_ratio: float, g_test, g_out, ws=None, stream=None):
+    """Block-diagonal form: S [n_blocks, D, D]; g_test/g_out [Q, n_blocks*D]."""
+    n_blocks, D, _ = S.shape
+    Q = g_test.shape[0]
+    ld_in = _rows(g_test, D * n_blocks) if Q > 0 else D * n_blocks
+    ld_out = _rows(g_out, D * n_blocks) if Q > 0 else D * n_blocks
+    ws, wsb = _workspace(logra_precondition_ws_size(D, n_blocks, Q) if damp_ratio >= 0 else 0, S.device, ws)
+    _check(lib().logra_precondition_blocks(_ptr(S), D, n_blocks, int(N), float(damp_ratio), _ptr(g_test),
+                                           _dtype_code(g_test), ld_in, Q, _ptr(g_out), _dtype_code(g_out),
+                                           ld_out, _ptr(ws), wsb, _stream(stream)))
+
+
+def logra_influence_ws_size(Q, N_chunk, topk, scores_given) -> int:
+    return int(lib().logra_influence_ws_size(Q, N_chunk, topk, int(bool(scores_given))))
+
+
+def logra_influence_scores(g_test_pre, g_train, scores=None, topk: int = 0, topk_val=None,
+                           topk_idx=None, train_base: int = 0, merge: bool = False, ws=None, stream=None):
+    """s = g_test_pre @ g_train^T (fp32) and/or the running per-query top-k."""
+    Q, D = g_test_pre.shape
+    N = g_train.shape[0]
+    ld_te = _rows(g_test_pre, D) if Q > 0 else D
+    ld_tr = _rows(g_train, D) if N > 0 else D
+    ld_s = _rows(scores, N) if scores is not None and Q > 0 else max(N, 1)
+    ws, wsb = _workspace(logra_influence_ws_size(Q, N, topk, scores is not None), g_test_pre.device, ws)
+    _check(lib().logra_influence_scores(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q, _ptr(g_train),
+                                        _dtype_code(g_train), ld_tr, N, D, int(train_base), _ptr(scores), ld_s,
+                                        int(topk), _ptr(topk_val), _ptr(topk_idx), int(bool(merge)),
+                                        _ptr(ws), wsb, _stream(stream)))

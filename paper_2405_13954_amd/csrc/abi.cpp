@@ -1,0 +1,287 @@
+// C ABI of the LoGra hot path: argument validation, workspace carving and
+// dispatch to the HIP kernels.  Size, dtype and limit checks run before any
+// HIP call; pointer checks follow (hipPointerGetAttributes); then launches.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <vector>
+
+#include "internal.h"
+#include "logra.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_err[0] = '\0';
+    return LOGRA_OK;
+}
+
+bool valid_dtype(int d) { return d == LOGRA_F32 || d == LOGRA_BF16; }
+size_t esize(int d) { return d == LOGRA_BF16 ? 2 : 4; }
+bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Device-memory check; `align` is the required base alignment in bytes.
+int check_dev(const void *p, const char *name, size_t align) {
+    if (p == nullptr) return fail(LOGRA_ERR_INVALID_ARG, "%s is NULL", name);
+    if ((reinterpret_cast<uintptr_t>(p) & (align - 1)) != 0)
+        return fail(LOGRA_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, align);
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof attr);
+    const hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(LOGRA_ERR_INVALID_ARG, "%s is not device memory (%s)", name, hipGetErrorString(e));
+    }
+    if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
+        return fail(LOGRA_ERR_INVALID_ARG, "%s is not device memory", name);
+    return LOGRA_OK;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(LOGRA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define TRY(expr)                       \
+    do {                                \
+        const int rc_ = (expr);         \
+        if (rc_ != LOGRA_OK) return rc_; \
+    } while (0)
+
+int check_ws(void *ws, size_t ws_bytes, size_t need) {
+    if (need == 0) return LOGRA_OK;
+    if (ws == nullptr || ws_bytes < need)
+        return fail(LOGRA_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws ? ws_bytes : 0);
+    return check_dev(ws, "ws", 256);
+}
+
+size_t round256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+int check_proj_sizes(int in_dtype, int B, int T, int n_in, int n_out, int k_in, int k_out,
+                     int g_dtype, int64_t g_ld) {
+    if (!valid_dtype(in_dtype) || !valid_dtype(g_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (B < 0 || T < 0) return fail(LOGRA_ERR_INVALID_ARG, "B and T must be >= 0");
+    if (n_in <= 0 || n_out <= 0 || k_in <= 0 || k_out <= 0)
+        return fail(LOGRA_ERR_INVALID_ARG, "n_in, n_out, k_in, k_out must be > 0");
+    const int vec = in_dtype == LOGRA_BF16 ? 8 : 4;
+    if (n_in % vec || n_out % vec)
+        return fail(LOGRA_ERR_INVALID_ARG, "n_in and n_out must be multiples of %d", vec);
+    if (k_in > LOGRA_MAX_K || k_out > LOGRA_MAX_K)
+        return fail(LOGRA_ERR_UNSUPPORTED, "k_in, k_out must be <= %d", LOGRA_MAX_K);
+    if (g_ld < static_cast<int64_t>(k_in) * k_out)
+        return fail(LOGRA_ERR_INVALID_ARG, "g_ld must be >= k_in * k_out");
+    if (static_cast<int64_t>(B) * T * (n_in > n_out ? n_in : n_out) < 0)
+        return fail(LOGRA_ERR_INVALID_ARG, "size overflow");
+    return LOGRA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *logra_last_error(void) { return g_err; }
+const char *logra_version(void) { return "logra-mi355x 0.1.0 (gfx950)"; }
+
+size_t logra_project_ws_size(int B, int T, int k_in, int k_out) {
+    return logra_project_layers_ws_size(1, B, T, k_in, k_out);
+}
+
+size_t logra_project_layers_ws_size(int n_layers, int B, int T, int k_in, int k_out) {
+    if (n_layers <= 0 || B <= 0 || T <= 0 || k_in <= 0 || k_out <= 0) return 0;
+    return round256(logra::project_partial_bytes(n_layers, B, T, k_in, k_out));
+}
+
+int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
+                         const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
+                         void *ws, size_t ws_bytes, void *stream) {
+    if (layers == nullptr) return fail(LOGRA_ERR_INVALID_ARG, "layers is NULL");
+    if (n_layers < 1 || n_layers > LOGRA_MAX_GROUP)
+        return fail(n_layers > LOGRA_MAX_GROUP ? LOGRA_ERR_UNSUPPORTED : LOGRA_ERR_INVALID_ARG,
+                    "n_layers must be in 1..%d", LOGRA_MAX_GROUP);
+    for (int l = 0; l < n_layers; ++l)
+        TRY(check_proj_sizes(in_dtype, B, T, layers[l].n_in, layers[l].n_out, k_in, k_out, g_dtype, g_ld));
+    if (B == 0 || T == 0) return ok();
+    const size_t ein = esize(in_dtype);
+    logra::ProjGroup grp;
+    std::memset(&grp, 0, sizeof grp);
+    grp.n_layers = n_layers;
+    for (int l = 0; l < n_layers; ++l) {
+        const logra_layer_desc &d = layers[l];
+        TRY(check_dev(d.x, "x", 16));
+        TRY(check_dev(d.dy, "dy", 16));
+        TRY(check_dev(d.p_in, "p_in", 16));
+        TRY(check_dev(d.p_out, "p_out", 16));
+        TRY(check_dev(d.g_out, "g_out", esize(g_dtype)));
+        (void)ein;
+        grp.layer[l] = {d.x, d.dy, d.p_in, d.p_out, d.g_out, d.n_in, d.n_out};
+    }
+    if (mask) TRY(check_dev(mask, "mask", 1));
+    TRY(check_ws(ws, ws_bytes, logra_project_layers_ws_size(n_layers, B, T, k_in, k_out)));
+    const hipError_t e = logra::launch_project(grp, in_dtype == LOGRA_BF16, B, T, mask, k_in, k_out,
+                                               g_dtype == LOGRA_BF16, g_ld, static_cast<float *>(ws),
+                                               static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "projection launch");
+    return ok();
+}
+
+int logra_project_layer(const void *x, const void *dy, int in_dtype, int B, int T, int n_in,
+                        int n_out, const uint8_t *mask, const void *p_in, const void *p_out,
+                        int k_in, int k_out, void *g_out, int g_dtype, int64_t g_ld, void *ws,
+                        size_t ws_bytes, void *stream) {
+    logra_layer_desc d;
+    d.x = x;
+    d.dy = dy;
+    d.p_in = p_in;
+    d.p_out = p_out;
+    d.g_out = g_out;
+    d.n_in = n_in;
+    d.n_out = n_out;
+    return logra_project_layers(&d, 1, in_dtype, B, T, mask, k_in, k_out, g_dtype, g_ld, ws, ws_bytes,
+                                stream);
+}
+
+int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks,
+                                float *S, void *stream) {
+    if (!valid_dtype(g_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (B < 0 || D <= 0 || n_blocks <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need B >= 0, D > 0, n_blocks > 0");
+    if (n_blocks > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "n_blocks must be <= 65535");
+    if (ld < static_cast<int64_t>(D) * n_blocks) return fail(LOGRA_ERR_INVALID_ARG, "ld must be >= D * n_blocks");
+    if (g_dtype == LOGRA_BF16 && (D % 8 || ld % 8))
+        return fail(LOGRA_ERR_INVALID_ARG, "bf16 covariance needs D and ld multiples of 8");
+    if (B == 0) return ok();
+    TRY(check_dev(g, "g", g_dtype == LOGRA_BF16 ? 16 : 4));
+    TRY(check_dev(S, "S", 4));
+    const hipError_t e = logra::launch_cov(g, g_dtype == LOGRA_BF16, ld, B, D, n_blocks, S,
+                                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "covariance launch");
+    return ok();
+}
+
+int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, float *S, void *stream) {
+    return logra_cov_accumulate_blocks(g, g_dtype, ld, B, D, 1, S, stream);
+}
+
+size_t logra_precondition_ws_size(int D, int n_blocks, int Q) {
+    if (D <= 0 || n_blocks <= 0 || Q < 0) return 0;
+    return round256(logra::precond_ws_bytes(D, n_blocks, Q));
+}
+
+int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                              const void *g_test, int in_dtype, int64_t ld_in, int Q, void *g_out,
+                              int out_dtype, int64_t ld_out, void *ws, size_t ws_bytes,
+                              void *stream) {
+    if (!valid_dtype(in_dtype) || !valid_dtype(out_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (D <= 0 || n_blocks <= 0 || Q < 0) return fail(LOGRA_ERR_INVALID_ARG, "need D > 0, n_blocks > 0, Q >= 0");
+    if (D > LOGRA_MAX_PRECOND_D) return fail(LOGRA_ERR_UNSUPPORTED, "D must be <= %d", LOGRA_MAX_PRECOND_D);
+    if (n_blocks > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "n_blocks must be <= 65535");
+    const int64_t width = static_cast<int64_t>(D) * n_blocks;
+    if (ld_in < width || ld_out < width) return fail(LOGRA_ERR_INVALID_ARG, "ld_in and ld_out must be >= D * n_blocks");
+    if (damp_ratio >= 0.0 && N <= 0) return fail(LOGRA_ERR_INVALID_ARG, "N must be > 0");
+    if (damp_ratio != damp_ratio) return fail(LOGRA_ERR_INVALID_ARG, "damp_ratio is NaN");
+    if (Q == 0 && damp_ratio < 0.0) return ok();
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (Q > 0) {
+        TRY(check_dev(g_test, "g_test", esize(in_dtype)));
+        TRY(check_dev(g_out, "g_out", esize(out_dtype)));
+    }
+    if (damp_ratio < 0.0) {
+        hipError_t e = logra::launch_copy_rows(g_test, in_dtype == LOGRA_BF16, ld_in, Q, static_cast<int>(width),
+                                               g_out, out_dtype == LOGRA_BF16, ld_out, s);
+        if (e != hipSuccess) return hip_fail(e, "copy launch");
+        e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+        return ok();
+    }
+    TRY(check_dev(S, "S", 4));
+    TRY(check_ws(ws, ws_bytes, logra_precondition_ws_size(D, n_blocks, Q)));
+    hipError_t e = logra::launch_precondition(S, D, n_blocks, N, damp_ratio, g_test, in_dtype == LOGRA_BF16,
+                                              ld_in, Q, g_out, out_dtype == LOGRA_BF16, ld_out, ws, s);
+    if (e != hipSuccess) return hip_fail(e, "precondition launch");
+    std::vector<int> info(static_cast<size_t>(n_blocks), 0);
+    e = hipMemcpyAsync(info.data(), logra::precond_info_ptr(ws, D, n_blocks), sizeof(int) * n_blocks,
+                       hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_fail(e, "status copy");
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+    for (int b = 0; b < n_blocks; ++b)
+        if (info[b] != 0)
+            return fail(LOGRA_ERR_NOT_PD, "block %d: pivot %d of C + lambda I is not positive", b, info[b] - 1);
+    return ok();
+}
+
+int logra_precondition(const float *S, int D, int64_t N, double damp_ratio, const void *g_test,
+                       int in_dtype, int64_t ld_in, int Q, void *g_out, int out_dtype, int64_t ld_out,
+                       void *ws, size_t ws_bytes, void *stream) {
+    return logra_precondition_blocks(S, D, 1, N, damp_ratio, g_test, in_dtype, ld_in, Q, g_out, out_dtype,
+                                     ld_out, ws, ws_bytes, stream);
+}
+
+size_t logra_influence_ws_size(int Q, int64_t N_chunk, int topk, int scores_given) {
+    if (Q <= 0 || N_chunk <= 0 || scores_given || topk <= 0) return 0;
+    return round256(sizeof(float) * static_cast<size_t>(Q) * static_cast<size_t>(N_chunk));
+}
+
+int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
+                           const void *g_train, int tr_dtype, int64_t ld_tr, int64_t N_chunk, int D,
+                           int64_t train_base, float *scores, int64_t ld_s, int topk, float *topk_val,
+                           int64_t *topk_idx, int merge, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(te_dtype) || !valid_dtype(tr_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (te_dtype != tr_dtype) return fail(LOGRA_ERR_UNSUPPORTED, "test and train dtypes must match");
+    if (Q < 0 || N_chunk < 0 || D <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need Q >= 0, N_chunk >= 0, D > 0");
+    if (ld_te < D || ld_tr < D) return fail(LOGRA_ERR_INVALID_ARG, "ld_te and ld_tr must be >= D");
+    if (topk < 0 || topk > LOGRA_MAX_TOPK) return fail(topk < 0 ? LOGRA_ERR_INVALID_ARG : LOGRA_ERR_UNSUPPORTED,
+                                                     "topk must be in 0..%d", LOGRA_MAX_TOPK);
+    if (scores == nullptr && topk == 0) return fail(LOGRA_ERR_INVALID_ARG, "nothing to compute: scores is NULL and topk is 0");
+    if (scores != nullptr && ld_s < N_chunk) return fail(LOGRA_ERR_INVALID_ARG, "ld_s must be >= N_chunk");
+    if (train_base < 0) return fail(LOGRA_ERR_INVALID_ARG, "train_base must be >= 0");
+    if (merge != 0 && merge != 1) return fail(LOGRA_ERR_INVALID_ARG, "merge must be 0 or 1");
+    const bool bf16 = te_dtype == LOGRA_BF16;
+    if (bf16 && (D % 8 || ld_te % 8 || ld_tr % 8))
+        return fail(LOGRA_ERR_INVALID_ARG, "bf16 scores need D, ld_te, ld_tr multiples of 8");
+    if (!bf16 && Q > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "fp32 scores support Q <= 65535");
+    if (Q == 0) return ok();
+    if (topk > 0) {
+        TRY(check_dev(topk_val, "topk_val", 4));
+        TRY(check_dev(topk_idx, "topk_idx", 8));
+    }
+    if (N_chunk == 0) {
+        if (topk > 0 && !merge) {   // no candidates: every slot is padding
+            const hipError_t e = logra::launch_topk(nullptr, 0, Q, 0, train_base, topk, topk_val, topk_idx,
+                                                    false, static_cast<hipStream_t>(stream));
+            if (e != hipSuccess) return hip_fail(e, "top-k launch");
+        }
+        return ok();
+    }
+    TRY(check_dev(g_test_pre, "g_test_pre", bf16 ? 16 : 4));
+    TRY(check_dev(g_train, "g_train", bf16 ? 16 : 4));
+    float *s_buf = scores;
+    int64_t ld = ld_s;
+    if (scores != nullptr) {
+        TRY(check_dev(scores, "scores", 4));
+    } else {
+        TRY(check_ws(ws, ws_bytes, logra_influence_ws_size(Q, N_chunk, topk, 0)));
+        s_buf = static_cast<float *>(ws);
+        ld = N_chunk;
+    }
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, N_chunk, D, bf16, s_buf, ld, s);
+    if (e != hipSuccess) return hip_fail(e, "score launch");
+    if (topk > 0) {
+        e = logra::launch_topk(s_buf, ld, Q, N_chunk, train_base, topk, topk_val, topk_idx, merge != 0, s);
+        if (e != hipSuccess) return hip_fail(e, "top-k launch");
+    }
+    return ok();
+}
+
+}  // extern "C"

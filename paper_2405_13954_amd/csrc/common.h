@@ -1,0 +1,87 @@
+// Device-side helpers shared by the LoGra HIP kernels (gfx950 / CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace logra {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_bits;
+
+constexpr int kWave = 64;
+
+// 128-bit load as four dwords (the only global access width the streaming
+// kernels use).
+__device__ __forceinline__ u32x4 ld128(const void *p) {
+    return *reinterpret_cast<const u32x4 *>(p);
+}
+// Streaming 128-bit load of data read exactly once (non-temporal hint).
+__device__ __forceinline__ u32x4 ld128_nt(const void *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+    return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ f32x4 as_f32x4(u32x4 v) { return __builtin_bit_cast(f32x4, v); }
+
+__device__ __forceinline__ float bf16_to_f32(bf16_bits h) {
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// fp32 -> bf16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ bf16_bits f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_bits>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<bf16_bits>(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_out(T *p, float v);
+template <>
+__device__ __forceinline__ void store_out<float>(float *p, float v) { *p = v; }
+template <>
+__device__ __forceinline__ void store_out<bf16_bits>(bf16_bits *p, float v) {
+    *p = f32_to_bf16_rne(v);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_out_d(T *p, double v);
+template <>
+__device__ __forceinline__ void store_out_d<float>(float *p, double v) { *p = static_cast<float>(v); }
+template <>
+__device__ __forceinline__ void store_out_d<bf16_bits>(bf16_bits *p, double v) {
+    *p = f32_to_bf16_rne(static_cast<float>(v));
+}
+
+template <typename T>
+__device__ __forceinline__ double load_in_d(const T *p);
+template <>
+__device__ __forceinline__ double load_in_d<float>(const float *p) { return static_cast<double>(*p); }
+template <>
+__device__ __forceinline__ double load_in_d<bf16_bits>(const bf16_bits *p) {
+    return static_cast<double>(bf16_to_f32(*p));
+}
+
+// Matrix-core products.  Operand layouts of the 16x16 shapes: lane l holds
+// row (l % 16) of A and column (l % 16) of B, with the contraction slice
+// selected by l / 16; the result holds rows 4*(l/16) + r, r < 4, of column
+// l % 16.  Any assignment of contraction indices to (l/16, element) is valid
+// as long as A and B use the same one.
+__device__ __forceinline__ f32x4 mfma16_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16_f32(float a, float b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+// 32x32x16: lane l holds row (l % 32) of A / column (l % 32) of B; result
+// register r holds row 8*(r/4) + 4*(l/32) + (r%4) of column l % 32.
+__device__ __forceinline__ f32x16 mfma32_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+}  // namespace logra

@@ -1,0 +1,57 @@
+// Host-side launch interface between the C ABI and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace logra {
+
+constexpr int kMaxGroup = 16;   // layers per grouped projection launch
+constexpr int kProjTile = 64;   // tokens per projection workgroup
+constexpr int kMaxK = 128;
+constexpr int kMaxTopk = 1024;
+constexpr int kMaxPrecondD = 8192;
+
+struct ProjLayer {
+    const void *x;
+    const void *dy;
+    const void *p_in;
+    const void *p_out;
+    void *g_out;
+    int n_in;
+    int n_out;
+};
+
+struct ProjGroup {
+    ProjLayer layer[kMaxGroup];
+    int n_layers;
+};
+
+// Projection (Sec. 3.1 Eq. (5)): per-tile partials into `partial`, then a
+// fixed-order sum over tiles into each layer's g_out rows.
+size_t project_partial_bytes(int n_layers, int B, int T, int k_in, int k_out);
+hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
+                          int k_in, int k_out, bool bf16_out, int64_t g_ld, float *partial,
+                          hipStream_t s);
+
+// Covariance S_l += G_l^T G_l for n_blocks column blocks of width D.
+hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S,
+                      hipStream_t s);
+
+// Damped Cholesky preconditioning of n_blocks blocks.  Writes a per-block
+// status word into the workspace; precond_info_ptr() locates it.
+size_t precond_ws_bytes(int D, int n_blocks, int Q);
+int *precond_info_ptr(void *ws, int D, int n_blocks);
+hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                               const void *g_test, bool bf16_in, int64_t ld_in, int Q, void *g_out,
+                               bool bf16_out, int64_t ld_out, void *ws, hipStream_t s);
+hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int rows, int cols,
+                            void *dst, bool bf16_out, int64_t ld_out, hipStream_t s);
+
+// Score GEMM s = te * tr^T (fp32 result) and per-query top-k.
+hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
+                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, hipStream_t st);
+hipError_t launch_topk(const float *s, int64_t ld_s, int Q, int64_t N, int64_t base, int k,
+                       float *val, int64_t *idx, bool merge, hipStream_t st);
+
+}  // namespace logra

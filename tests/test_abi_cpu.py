@@ -1,0 +1,105 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU.  CPU only: every call here
+returns from host-side validation or is a pure size query."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2405_13954_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "logra.h")
+
+
+def declared_symbols():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(logra_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(P.LIB_PATH):
+        pytest.fail("libpaper_logra.so is not built (run __graft_entry__.build())")
+    return P.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    syms = declared_symbols()
+    assert len(syms) >= 13
+    for s in syms:
+        assert hasattr(L, s), f"missing export {s}"
+    assert set(syms) == set(P.EXPORTED)
+
+
+def test_version(L):
+    assert "gfx950" in P.logra_version()
+
+
+def test_workspace_sizes(L):
+    # per-tile fp32 partials: B * ceil(T/64) * k_in * k_out * 4, rounded to 256
+    assert P.logra_project_ws_size(2, 100, 8, 12) == 2 * 2 * 8 * 12 * 4 + (256 - (2 * 2 * 8 * 12 * 4) % 256) % 256
+    assert P.logra_project_ws_size(0, 100, 8, 8) == 0
+    assert P.logra_project_layers_ws_size(7, 16, 1024, 64, 64) == 7 * 16 * 16 * 4096 * 4
+    assert P.logra_precondition_ws_size(256, 224, 1024) >= 224 * 256 * 256 * 8
+    assert P.logra_influence_ws_size(4, 10, 3, 0) == 256
+    assert P.logra_influence_ws_size(4, 10, 3, 1) == 0
+
+
+NULL = None
+
+
+def proj(L, **kw):
+    a = dict(x=NULL, dy=NULL, in_dtype=1, B=2, T=8, n_in=64, n_out=64, mask=NULL, p_in=NULL, p_out=NULL,
+             k_in=8, k_out=8, g_out=NULL, g_dtype=0, g_ld=64, ws=NULL, ws_bytes=0, stream=NULL)
+    a.update(kw)
+    return L.logra_project_layer(*a.values())
+
+
+def test_project_validation(L):
+    assert proj(L, B=-1) == P.ERR_INVALID_ARG
+    assert proj(L, n_in=0) == P.ERR_INVALID_ARG
+    assert proj(L, n_in=60) == P.ERR_INVALID_ARG            # bf16 rows need multiples of 8
+    assert proj(L, in_dtype=0, n_in=62) == P.ERR_INVALID_ARG  # fp32 rows need multiples of 4
+    assert proj(L, in_dtype=7) == P.ERR_INVALID_ARG
+    assert proj(L, k_in=129) == P.ERR_UNSUPPORTED
+    assert proj(L, g_ld=63) == P.ERR_INVALID_ARG
+    assert "g_ld" in P.logra_last_error()
+    assert proj(L, B=0) == P.OK                              # no-op, no device access
+    assert proj(L, T=0) == P.OK
+    assert L.logra_project_layers(None, 1, 1, 2, 8, None, 8, 8, 0, 64, None, 0, None) == P.ERR_INVALID_ARG
+    descs = (P.LayerDesc * 17)()
+    assert L.logra_project_layers(descs, 17, 1, 2, 8, None, 8, 8, 0, 64, None, 0, None) == P.ERR_UNSUPPORTED
+
+
+def test_cov_validation(L):
+    assert L.logra_cov_accumulate(None, 1, 64, 4, 0, None, None) == P.ERR_INVALID_ARG
+    assert L.logra_cov_accumulate(None, 1, 60, 4, 60, None, None) == P.ERR_INVALID_ARG   # bf16 needs D%8==0
+    assert L.logra_cov_accumulate(None, 1, 32, 4, 64, None, None) == P.ERR_INVALID_ARG   # ld < D
+    assert L.logra_cov_accumulate(None, 1, 64, 0, 64, None, None) == P.OK                # B = 0 no-op
+    assert L.logra_cov_accumulate_blocks(None, 1, 512, 4, 256, 0, None, None) == P.ERR_INVALID_ARG
+
+
+def test_precondition_validation(L):
+    f = L.logra_precondition
+    assert f(None, 8193, 4, 0.1, None, 0, 8193, 1, None, 0, 8193, None, 0, None) == P.ERR_UNSUPPORTED
+    assert f(None, 64, 0, 0.1, None, 0, 64, 1, None, 0, 64, None, 0, None) == P.ERR_INVALID_ARG
+    assert f(None, 64, 4, float("nan"), None, 0, 64, 1, None, 0, 64, None, 0, None) == P.ERR_INVALID_ARG
+    assert f(None, 64, 4, 0.1, None, 0, 32, 1, None, 0, 64, None, 0, None) == P.ERR_INVALID_ARG
+    assert f(None, 64, 4, -1.0, None, 0, 64, 0, None, 0, 64, None, 0, None) == P.OK     # identity, Q=0
+
+
+def test_influence_validation(L):
+    f = L.logra_influence_scores
+    args = lambda **kw: [kw.get(k, v) for k, v in dict(
+        te=None, tdt=1, ld_te=64, Q=2, tr=None, rdt=1, ld_tr=64, N=10, D=64, base=0, s=None, ld_s=10,
+        topk=3, tv=None, ti=None, merge=0, ws=None, wsb=0, st=None).items()]
+    assert f(*args(rdt=0)) == P.ERR_UNSUPPORTED
+    assert f(*args(topk=1025)) == P.ERR_UNSUPPORTED
+    assert f(*args(topk=0)) == P.ERR_INVALID_ARG          # nothing requested
+    assert f(*args(D=60, ld_te=60, ld_tr=60)) == P.ERR_INVALID_ARG
+    assert f(*args(merge=2)) == P.ERR_INVALID_ARG
+    assert f(*args(base=-1)) == P.ERR_INVALID_ARG
+    assert f(*args(Q=0)) == P.OK

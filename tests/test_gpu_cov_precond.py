@@ -1,0 +1,128 @@
+"""GPU parity of the covariance (Eq. (3), App. D) and the damped-inverse
+preconditioner (Eq. (2) step (1), App. C) against the float64 oracle.
+
+Preconditioner inputs are spectral random SPD matrices from the input
+generator, so both sides consume the same fp32 bytes of S."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("dtype,B,D", [("bf16", 37, 200), ("bf16", 16, 512), ("f32", 5, 64),
+                                       ("f32", 9, 100), ("bf16", 300, 64)])
+def test_cov_parity_and_symmetry(dtype, B, D):
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, normwise, say
+    say(f"[cov parity] dtype={dtype} B={B} D={D}")
+    g = W.normal(W.rng(21, B, D), (B, D), 1.0, dtype)
+    S = torch.zeros((D, D), dtype=torch.float32, device="cuda")
+    P.logra_cov_accumulate(dev(g), S)
+    torch.cuda.synchronize()
+    got = host(S)
+    want = oracle.cov_accumulate(g)
+    assert np.array_equal(got, got.T)          # exactly symmetric
+    err = normwise(got, want)
+    say(f"  normwise err {err:.3e}")
+    assert err <= (1e-4 if dtype == "f32" else 2e-2)
+    assert err <= 1e-5
+
+
+def test_cov_integer_exact_blocks_and_chunks():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[cov] integer exact, blocks, chunked")
+    g = W.integer_array(W.rng(22), (40, 3 * 72), -3, 3, "bf16")
+    S = torch.zeros((3, 72, 72), dtype=torch.float32, device="cuda")
+    gd = dev(g)
+    P.logra_cov_accumulate_blocks(gd[:25], S, 72)      # chunked: 25 then 15 rows
+    P.logra_cov_accumulate_blocks(gd[25:], S, 72)
+    torch.cuda.synchronize()
+    got = host(S)
+    for l in range(3):
+        want = oracle.cov_accumulate(g[:, l * 72:(l + 1) * 72])
+        assert np.array_equal(got[l].astype(np.float64), want)
+
+
+def test_cov_deterministic():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[cov] determinism")
+    g = dev(W.normal(W.rng(23), (64, 256), 1.0, "bf16"))
+    outs = []
+    for _ in range(2):
+        S = torch.zeros((256, 256), dtype=torch.float32, device="cuda")
+        P.logra_cov_accumulate(g, S)
+        torch.cuda.synchronize()
+        outs.append(host(S))
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+
+
+PRE_CASES = {
+    # name: (D, rank, n_blocks, Q, damp, in_dtype, out_dtype)
+    "tiny_f32": (64, 4, 1, 2, 1e-3, "f32", "f32"),
+    "ragged_D": (200, 50, 1, 7, 0.1, "bf16", "f32"),
+    "blocks_bf16": (256, 256, 5, 37, 0.1, "bf16", "bf16"),
+    "blocks_many_q": (64, 30, 3, 70, 0.1, "f32", "f32"),
+    "D1000": (1000, 1000, 1, 5, 0.1, "f32", "f32"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PRE_CASES))
+def test_precondition_parity(name):
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, rowwise_normwise, say
+    D, rank, nb, Q, r, idt, odt = PRE_CASES[name]
+    say(f"[precondition parity] case={name}")
+    N = 4096
+    S = np.stack([W.spd_matrix(30 + l, D, rank, scale=float(N)) for l in range(nb)])
+    g = W.normal(W.rng(31, D), (Q, nb * D), 1.0, idt)
+    out = torch.zeros((Q, nb * D), dtype=torch.float32 if odt == "f32" else torch.bfloat16, device="cuda")
+    P.logra_precondition_blocks(dev(S), N, r, dev(g), out)
+    got = host(out)
+    want = np.concatenate([oracle.precondition(S[l].astype(np.float64), N, r, g[:, l * D:(l + 1) * D])[0]
+                           for l in range(nb)], axis=1)
+    tol = 1e-4 if odt == "f32" else 2e-2
+    for l in range(nb):
+        err = rowwise_normwise(got[:, l * D:(l + 1) * D], want[:, l * D:(l + 1) * D])
+        say(f"  block {l}: normwise err {err:.3e} (tol {tol})")
+        assert err <= tol
+
+
+def test_precondition_identity_and_single_api():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[precondition] identity mode, single-block API")
+    g = W.normal(W.rng(32), (3, 64), 1.0, "bf16")
+    out = torch.zeros((3, 64), dtype=torch.float32, device="cuda")
+    S = torch.zeros((64, 64), dtype=torch.float32, device="cuda")
+    P.logra_precondition(S, 1, -1.0, dev(g), out)
+    assert np.array_equal(host(out), W.bf16_bits_to_f32(g))
+
+
+def test_precondition_not_pd():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, say
+    say("[precondition] not positive definite")
+    v = np.zeros((1, 64), np.float32)
+    v[0, :2] = [1.0, 2.0]
+    S = np.outer(v[0], v[0]).astype(np.float32)   # rank one: second pivot is exactly zero
+    out = torch.zeros((1, 64), dtype=torch.float32, device="cuda")
+    with pytest.raises(P.LograError) as ei:
+        P.logra_precondition(dev(S), 1, 0.0, dev(v), out)
+    assert ei.value.status == P.ERR_NOT_PD
+    S2 = np.eye(64, dtype=np.float32)
+    S2[10, 10] = -1.0
+    with pytest.raises(P.LograError) as ei:
+        P.logra_precondition(dev(S2), 1, 0.0, dev(v), out)
+    assert ei.value.status == P.ERR_NOT_PD
+    assert "pivot 10" in P.logra_last_error()

@@ -1,0 +1,146 @@
+"""GPU parity of the fused projection (Sec. 3.1 Eq. (5)) against the float64 oracle.
+
+Every case runs the HIP kernels through the C ABI and compares each example's
+k_out x k_in gradient with the oracle's on the same input bytes.  Tolerances:
+1e-4 normwise for fp32 inputs and 2e-2 for bf16 inputs (fp32 accumulation);
+fp32 outputs of bf16 inputs are also held to 1e-3, what fp32 accumulation of
+exact bf16 products leaves.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # name: (dtype, B, T, n_in, n_out, k_in, k_out, x_std, dy_std, ragged, out_dtype)
+    "tiny_f32": ("f32", 4, 16, 64, 64, 8, 8, 1.0, 1e-2, False, "f32"),
+    "asym_bf16_ragged": ("bf16", 5, 150, 200, 328, 12, 20, 1.0, 0.5, True, "f32"),
+    "asym_bf16_out_bf16": ("bf16", 5, 150, 200, 328, 12, 20, 1.0, 0.5, True, "bf16"),
+    "f32_ragged_kt2": ("f32", 3, 77, 96, 52, 24, 7, 1.0, 1.0, True, "f32"),
+    "k64_bf16": ("bf16", 3, 130, 512, 1024, 64, 64, 1.0, 1e-4, True, "f32"),
+    "k128_bf16": ("bf16", 2, 70, 256, 136, 128, 100, 1.0, 1.0, True, "f32"),
+    "gpt2_qkv": ("bf16", 3, 200, 768, 2304, 16, 16, 1.0, 1e-3, True, "bf16"),
+    "llama_gate": ("bf16", 2, 96, 4096, 14336, 16, 16, 1.0, 1e-4, True, "bf16"),
+    "llama_down_k64": ("bf16", 2, 65, 14336, 4096, 64, 64, 1.0, 1e-4, False, "f32"),
+}
+
+
+def _inputs(name, seed=0):
+    dt, B, T, n_in, n_out, k_in, k_out, xs, dys, ragged, _ = CASES[name]
+    lens = None
+    if ragged:
+        lens = W.lengths(W.rng(seed, 7, B), B, 0, T)
+        lens[0] = T
+        if B > 2:
+            lens[1] = 0
+    return W.layer_inputs(seed, sorted(CASES).index(name), B, T, n_in, n_out, k_in, k_out, xs, dys, dt, lens)
+
+
+def _run(d, out_dtype, g_ld=None, poison=False):
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host
+    x, dy = d["x"].copy(), d["dy"].copy()
+    if poison and d["mask"] is not None:
+        m = d["mask"] == 0
+        if x.dtype == np.uint16:
+            x[m] = 0x7FC0      # NaN
+            dy[m] = 0xFF80     # -Inf
+        else:
+            x[m] = np.nan
+            dy[m] = np.inf
+    B = x.shape[0]
+    D = d["p_in"].shape[0] * d["p_out"].shape[0]
+    tdt = torch.float32 if out_dtype == "f32" else torch.bfloat16
+    store = torch.full((B, g_ld or D), 7.0, dtype=tdt, device="cuda")
+    g = store[:, :D]
+    P.logra_project_layer(dev(x), dev(dy), dev(d["p_in"]), dev(d["p_out"]), g,
+                          mask=None if d["mask"] is None else dev(d["mask"]))
+    torch.cuda.synchronize()
+    return host(store)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_project_parity(name):
+    from gpu_util import f64, rowwise_normwise, say
+    say(f"[project parity] case={name}")
+    d = _inputs(name)
+    out_dtype = CASES[name][-1]
+    got = _run(d, out_dtype)
+    want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], d["mask"])
+    err = rowwise_normwise(got, want)
+    tol = 1e-4 if CASES[name][0] == "f32" else 2e-2
+    say(f"  normwise err {err:.3e} (tol {tol})")
+    assert err <= tol
+    if out_dtype == "f32" and CASES[name][0] == "bf16":
+        assert err <= 1e-3
+    if d["mask"] is not None:
+        empty = d["mask"].sum(1) == 0
+        assert np.all(f64(got)[empty] == 0.0)
+
+
+def test_project_integer_exact():
+    """Small-integer inputs make every product and sum exact in fp32: the GPU
+    result must equal the oracle bit for bit (catches any index/layout slip)."""
+    from gpu_util import say
+    say("[project exact] integer inputs")
+    g = W.rng(3, 11)
+    B, T, n_in, n_out, k_in, k_out = 3, 100, 64, 48, 8, 16
+    d = {"x": W.integer_array(g, (B, T, n_in), -1, 1, "bf16", 0.5),
+         "dy": W.integer_array(g, (B, T, n_out), -1, 1, "bf16", 0.5),
+         "p_in": W.integer_array(g, (k_in, n_in), -1, 1, "bf16", 0.5),
+         "p_out": W.integer_array(g, (k_out, n_out), -1, 1, "bf16", 0.5),
+         "mask": W.mask_from_lengths(np.array([100, 37, 64]), T)}
+    got = _run(d, "f32")
+    want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], d["mask"])
+    assert np.abs(want).max() < 2 ** 24
+    assert np.array_equal(got.astype(np.float64), want)
+
+
+def test_project_masked_garbage_and_determinism():
+    from gpu_util import say
+    say("[project] NaN/Inf in masked slots; determinism")
+    d = _inputs("asym_bf16_ragged", seed=5)
+    a = _run(d, "f32")
+    b = _run(d, "f32", poison=True)
+    c = _run(d, "f32")
+    assert np.all(np.isfinite(b))
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert np.array_equal(a.view(np.uint32), c.view(np.uint32))
+
+
+def test_project_store_stride_untouched():
+    """Rows land at b * g_ld; the store's other columns are left alone."""
+    from gpu_util import say
+    say("[project] store stride")
+    d = _inputs("tiny_f32")
+    got = _run(d, "f32", g_ld=100)
+    assert np.all(got[:, 64:] == 7.0)
+    want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], d["mask"])
+    assert np.abs(got[:, :64] - want).max() <= 1e-4 * np.abs(want).max()
+
+
+def test_project_grouped_equals_single():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[project] grouped launch == per-layer launches")
+    shapes = [(256, 512), (512, 128), (128, 384)]
+    B, T, k = 4, 90, 16
+    lens = np.array([90, 3, 64, 0])
+    mask = dev(W.mask_from_lengths(lens, T))
+    layers = []
+    store_g = torch.zeros((B, 3 * k * k + 8), dtype=torch.bfloat16, device="cuda")
+    store_s = torch.zeros_like(store_g)
+    for i, (ni, no) in enumerate(shapes):
+        d = W.layer_inputs(9, i, B, T, ni, no, k, k, 1.0, 1.0, "bf16")
+        t = {key: dev(d[key]) for key in ("x", "dy", "p_in", "p_out")}
+        layers.append(dict(t, g_out=store_g[:, i * k * k:(i + 1) * k * k]))
+        P.logra_project_layer(t["x"], t["dy"], t["p_in"], t["p_out"], store_s[:, i * k * k:(i + 1) * k * k],
+                              mask=mask)
+    P.logra_project_layers(layers, mask=mask)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(store_g), host(store_s))

@@ -197,3 +197,22 @@ def device_scaled_rows_(out, scales, block: int, gen, rows_per_chunk: int = 4096
         tmp.mul_(sc[None, :, None])
         out[r0:r1].copy_(tmp.view(r1 - r0, D))
     return out
+
+
+def spd_matrix(seed: int, D: int, rank: int, scale: float = 1.0) -> np.ndarray:
+    """A random symmetric PSD fp32 matrix with `rank` nonzero eigenvalues (log-uniform in
+    [1e-2, 1] x scale) and uniformly random eigenvectors; exactly symmetric after rounding."""
+    g = rng(seed, 5, D, rank)
+    q, _ = np.linalg.qr(g.standard_normal((D, rank)))
+    ev = scale * np.exp(g.uniform(np.log(1e-2), 0.0, size=rank))
+    s = (q * ev) @ q.T
+    s = np.triu(s.astype(np.float32))
+    return s + np.triu(s, 1).T
+
+
+def integer_array(g: np.random.Generator, shape, lo: int, hi: int, dtype: str, density: float = 1.0):
+    """Small integers in [lo, hi] (exact in bf16/fp32), zeroed with probability 1 - density."""
+    a = g.integers(lo, hi + 1, size=shape).astype(np.float32)
+    if density < 1.0:
+        a *= (g.random(size=shape) < density)
+    return a if dtype == "f32" else f32_to_bf16_bits(a)
