@@ -1,0 +1,350 @@
+"""Benchmark of the LoGra hot path on one MI355X.
+
+Logging leg (the reported `value`, tokens/s): the 32-block Llama3-8B logging
+stream -- per step one batch of B=8 examples of T=2048 padded tokens, valid
+lengths uniform on 128..2048, through all 224 linear layers (k_in = k_out = 16,
+57,344 projected dims per example): fused projection into the bf16 gradient
+store (32 grouped launches of 7 layers) and the 224 per-layer covariance
+updates.
+
+Influence leg (reported under "influence", scores/s): 1,024 test gradients
+against 500,000 stored training gradients of 57,344 dims -- damped-Cholesky
+preconditioning of the test gradients over 224 blocks of 256 (covariances of
+4,096 gradients, damping 0.1 x mean eigenvalue), the score GEMM and the
+per-query top-100.
+
+All inputs are synthetic, drawn on the device before timing.  Each leg
+reports the roofline of its dominant kernel from HIP events recorded on the
+launch stream around every launch, and the float64 oracle timed on a bounded
+sample on the host (rank 0 only).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+METRIC = "projected per-example grads/sec (tokens/s) at Llama3-8B shapes; influence scores/sec"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class EventTimer:
+    """Pairs of HIP events on the launch stream; mean duration per launch in ms."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = []
+
+    def start(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+    def stop(self, s):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        self.pairs.append((s, e))
+
+    def mean_ms(self):
+        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else float("nan")
+
+
+# ------------------------------------------------------------------ logging --
+def logging_leg(args, torch, P):
+    w = W.WORKLOADS["llama3_8b_stream"]
+    B, T, k = w.B, w.T, w.k_in
+    D = w.D
+    layers = w.layers
+    nl_block = len(layers)
+    n_layers = w.n_layers
+    D_tot = n_layers * D
+    dev = "cuda"
+    n_buf = 4   # distinct x/dy buffer sets, cycled over the 32 blocks (each 2.7 GB >> the 256 MB MALL)
+    log(f"[log] allocating {n_buf} x/dy block buffers, projections for {n_layers} layers, store")
+    gen = W.torch_generator(args.seed, 100)
+    bufs = []
+    for i in range(n_buf):
+        blk = []
+        for (_, n_in, n_out) in layers:
+            x = torch.empty((B, T, n_in), dtype=torch.bfloat16, device=dev)
+            dy = torch.empty((B, T, n_out), dtype=torch.bfloat16, device=dev)
+            W.device_normal_(x, w.x_std, gen)
+            W.device_normal_(dy, w.dy_std, gen)
+            blk.append((x, dy))
+        bufs.append(blk)
+    projs = []
+    for l in range(n_layers):
+        _, n_in, n_out = layers[l % nl_block]
+        pi = torch.empty((k, n_in), dtype=torch.bfloat16, device=dev)
+        po = torch.empty((k, n_out), dtype=torch.bfloat16, device=dev)
+        W.device_normal_(pi, 1.0 / np.sqrt(k), gen)
+        W.device_normal_(po, 1.0 / np.sqrt(k), gen)
+        projs.append((pi, po))
+    n_steps = args.warmup + args.steps
+    n_rows = max(n_steps * B, B)
+    store = torch.empty((n_rows, D_tot), dtype=torch.bfloat16, device=dev)
+    S = torch.zeros((n_layers, D, D), dtype=torch.float32, device=dev)
+    lens = [W.lengths(W.rng(args.seed, 200, s), B, w.len_lo, w.len_hi) for s in range(n_steps)]
+    masks = [torch.from_numpy(W.mask_from_lengths(L, T)).to(dev) for L in lens]
+    ws_bytes = P.logra_project_layers_ws_size(nl_block, B, T, k, k)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    L = P.lib()
+    g_ld = store.stride(0)
+
+    # descriptor arrays per (step, block), built once
+    def descs(step, blk):
+        arr = (P.LayerDesc * nl_block)()
+        row0 = step * B
+        for j in range(nl_block):
+            l = blk * nl_block + j
+            x, dy = bufs[blk % n_buf][j]
+            pi, po = projs[l]
+            g = store[row0:row0 + B, l * D:(l + 1) * D]
+            arr[j] = P.LayerDesc(x.data_ptr(), dy.data_ptr(), pi.data_ptr(), po.data_ptr(), g.data_ptr(),
+                                 x.shape[2], dy.shape[2])
+        return arr
+
+    all_descs = [[descs(s, b) for b in range(w.blocks)] for s in range(n_steps)]
+    proj_timer = EventTimer(torch)
+    cov_timer = EventTimer(torch)
+
+    def step(s, timed):
+        m = masks[s]
+        for b in range(w.blocks):
+            e0 = proj_timer.start() if timed else None
+            rc = L.logra_project_layers(all_descs[s][b], nl_block, P.BF16, B, T, ctypes.c_void_p(m.data_ptr()),
+                                        k, k, P.BF16, g_ld, ctypes.c_void_p(ws.data_ptr()), ws_bytes, stream)
+            if rc != 0:
+                raise P.LograError(rc, P.logra_last_error())
+            if timed:
+                proj_timer.stop(e0)
+        rows = store[s * B:(s + 1) * B]
+        e0 = cov_timer.start() if timed else None
+        rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(rows.data_ptr()), P.BF16, g_ld, B, D, n_layers,
+                                           ctypes.c_void_p(S.data_ptr()), stream)
+        if rc != 0:
+            raise P.LograError(rc, P.logra_last_error())
+        if timed:
+            cov_timer.stop(e0)
+
+    log(f"[log] warmup {args.warmup} steps")
+    for s in range(args.warmup):
+        step(s, False)
+    torch.cuda.synchronize()
+    log(f"[log] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for s in range(args.warmup, n_steps):
+        step(s, True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    tokens = int(sum(int(L_.sum()) for L_ in lens[args.warmup:]))
+    examples = args.steps * B
+    # algorithmic bytes of one grouped launch (7 layers of a block), averaged over timed steps:
+    # valid tokens x 2 B x (n_in + n_out) summed over the block, plus the projections once.
+    per_tok = sum(2 * (ni + no) for _, ni, no in layers)
+    proj_bytes = sum(2 * k * (ni + no) for _, ni, no in layers)
+    bytes_per_launch = tokens / args.steps * per_tok + proj_bytes
+    proj_ms = proj_timer.mean_ms()
+    achieved = bytes_per_launch / (proj_ms * 1e-3) / 1e9
+    res = {
+        "tokens": tokens, "seconds": dt,
+        "tokens_per_s": tokens / dt, "examples_per_s": examples / dt,
+        "ms_per_step": dt * 1e3 / args.steps,
+        "proj_launch_ms": proj_ms, "cov_launch_ms": cov_timer.mean_ms(),
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "logra_project_layers (7 Llama3-8B layers, B=8 ragged, k=16)",
+                     "bytes_per_launch": bytes_per_launch},
+    }
+    sample = None
+    if args.cpu_baseline:
+        sample = {"x": [host_bf16(bufs[0][j][0][:, :args.cpu_tokens]) for j in range(nl_block)],
+                  "dy": [host_bf16(bufs[0][j][1][:, :args.cpu_tokens]) for j in range(nl_block)],
+                  "p_in": [host_bf16(projs[j][0]) for j in range(nl_block)],
+                  "p_out": [host_bf16(projs[j][1]) for j in range(nl_block)],
+                  "mask": W.mask_from_lengths(lens[0], T)[:, :args.cpu_tokens], "blocks": w.blocks}
+    del bufs, store, S, ws
+    torch.cuda.empty_cache()
+    return res, sample
+
+
+def host_bf16(t):
+    import torch
+    return t.contiguous().to("cpu").view(torch.int16).numpy().view(np.uint16)
+
+
+def cpu_logging_baseline(sample):
+    import oracle
+    t0 = time.perf_counter()
+    for j in range(len(sample["x"])):
+        oracle.project_factored(sample["x"][j], sample["dy"][j], sample["p_in"][j], sample["p_out"][j],
+                                sample["mask"])
+    dt = time.perf_counter() - t0
+    toks = int(sample["mask"].sum())
+    B, Ts = sample["mask"].shape
+    # the sample is one block of the 32 identical-shape blocks: model tokens/s
+    return {"value": toks / (dt * sample["blocks"]), "unit": "tokens/s",
+            "cores": min(oracle.num_threads(), B), "kind": "oracle",
+            "sample": f"{B} examples x first {Ts} token slots ({toks} valid) through the 7 layers of one "
+                      f"block, scaled to 32 blocks; {dt:.2f} s"}
+
+
+# ---------------------------------------------------------------- influence --
+def influence_leg(args, torch, P):
+    w = W.WORKLOADS["llama3_8b_scores"]
+    ex = w.extra
+    D = w.D
+    nb = w.n_layers
+    D_tot = nb * D
+    N, Q, Nc, topk = args.n_train or ex["N_train"], ex["Q"], ex["N_cov"], ex["topk"]
+    dev = "cuda"
+    scales = W.block_scales(args.seed, nb, ex["scale_lo"], ex["scale_hi"])
+    log(f"[inf] drawing train store {N} x {D_tot}, {Q} test and {Nc} covariance gradients")
+    gen = W.torch_generator(args.seed, 300)
+    train = torch.empty((N, D_tot), dtype=torch.bfloat16, device=dev)
+    W.device_scaled_rows_(train, scales, D, gen)
+    test = torch.empty((Q, D_tot), dtype=torch.bfloat16, device=dev)
+    W.device_scaled_rows_(test, scales, D, gen)
+    covg = torch.empty((Nc, D_tot), dtype=torch.bfloat16, device=dev)
+    W.device_scaled_rows_(covg, scales, D, gen)
+    S = torch.zeros((nb, D, D), dtype=torch.float32, device=dev)
+    P.logra_cov_accumulate_blocks(covg, S, D)
+    pre = torch.empty((Q, D_tot), dtype=torch.bfloat16, device=dev)
+    pws = torch.empty(P.logra_precondition_ws_size(D, nb, Q), dtype=torch.uint8, device=dev)
+    tv = torch.empty((Q, topk), dtype=torch.float32, device=dev)
+    ti = torch.empty((Q, topk), dtype=torch.int64, device=dev)
+    sws = torch.empty(P.logra_influence_ws_size(Q, N, topk, False), dtype=torch.uint8, device=dev)
+    pre_timer, gemm_timer = EventTimer(torch), EventTimer(torch)
+
+    def one_pass(timed):
+        e0 = pre_timer.start() if timed else None
+        P.logra_precondition_blocks(S, Nc, ex["damp"], test, pre, ws=pws)   # synchronous
+        if timed:
+            pre_timer.stop(e0)
+        e0 = gemm_timer.start() if timed else None
+        P.logra_influence_scores(pre, train, scores=None, topk=topk, topk_val=tv, topk_idx=ti, ws=sws)
+        if timed:
+            gemm_timer.stop(e0)
+
+    log("[inf] warmup pass")
+    one_pass(False)
+    torch.cuda.synchronize()
+    log(f"[inf] timing {args.inf_passes} passes")
+    t0 = time.perf_counter()
+    for _ in range(args.inf_passes):
+        one_pass(True)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / args.inf_passes
+    flops = 2.0 * Q * N * D_tot
+    # the GEMM alone, from events around a scores-only launch (top-k excluded)
+    s_full = sws.view(torch.float32)[: Q * N].view(Q, N)
+    only = EventTimer(torch)
+    for _ in range(args.inf_passes):
+        e0 = only.start()
+        P.logra_influence_scores(pre, train, scores=s_full, topk=0)
+        only.stop(e0)
+    torch.cuda.synchronize()
+    gemm_ms = only.mean_ms()
+    achieved = flops / (gemm_ms * 1e-3) / 1e12
+    res = {
+        "metric": "influence scores/sec (1,024 x 500,000 at 57,344 dims, top-100)",
+        "value": Q * N / dt, "unit": "scores/s", "ms_per_pass": dt * 1e3,
+        "precondition_ms": pre_timer.mean_ms(), "scores_topk_ms": gemm_timer.mean_ms(),
+        "gemm_ms": gemm_ms,
+        "config": {"workload": "llama3_8b_scores", "N_train": N, "Q": Q, "D": D_tot, "blocks": nb,
+                   "block": D, "N_cov": Nc, "damp": ex["damp"], "topk": topk},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / BF16_PEAK_TFLOPS, "traffic": None,
+                     "kernel": "score GEMM (bf16 MFMA, fp32 accumulation)", "flops_per_launch": flops},
+    }
+    sample = None
+    if args.cpu_baseline:
+        ns = args.cpu_train_rows
+        sample = {"S": S[:, :, :].to("cpu").numpy().astype(np.float64), "N": Nc, "damp": ex["damp"],
+                  "test": host_bf16(test[:16]), "train": host_bf16(train[:ns]), "D": D, "topk": topk}
+    del train, test, covg, sws
+    torch.cuda.empty_cache()
+    return res, sample
+
+
+def cpu_influence_baseline(sample):
+    import oracle
+    D = sample["D"]
+    nb = sample["S"].shape[0]
+    t0 = time.perf_counter()
+    pre = np.concatenate([oracle.precondition(sample["S"][l], sample["N"], sample["damp"],
+                                              sample["test"][:, l * D:(l + 1) * D])[0] for l in range(nb)], axis=1)
+    s = oracle.scores(pre, sample["train"])
+    oracle.topk(s, sample["topk"])
+    dt = time.perf_counter() - t0
+    q, n = s.shape
+    return {"value": q * n / dt, "unit": "scores/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{q} queries x {n} stored gradients (224 blocks preconditioned, scores, top-100); "
+                      f"{dt:.2f} s"}
+
+
+# --------------------------------------------------------------------- main --
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--inf-passes", type=int, default=3)
+    ap.add_argument("--n-train", type=int, default=0, help="override stored-gradient count (testing)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--leg", choices=["all", "log", "influence"], default="all")
+    ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--cpu-train-rows", type=int, default=20000)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md on sharding)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2405_13954_amd as P
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    P.lib()
+
+    out = {"metric": METRIC, "value": None, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": "llama3_8b_stream", "blocks": 32, "layers": 224, "B": 8, "T": 2048,
+                      "len_range": [128, 2048], "k_in": 16, "k_out": 16, "store": "bf16 rows of 57,344"}}
+    log_sample = inf_sample = None
+    if args.leg in ("all", "log"):
+        r, log_sample = logging_leg(args, torch, P)
+        out.update(value=r["tokens_per_s"], ms_per_step=r["ms_per_step"], examples_per_s=r["examples_per_s"],
+                   roofline=r["roofline"], proj_launch_ms=r["proj_launch_ms"], cov_launch_ms=r["cov_launch_ms"])
+    if args.leg in ("all", "influence"):
+        r, inf_sample = influence_leg(args, torch, P)
+        out["influence"] = r
+    if args.cpu_baseline:
+        if log_sample is not None:
+            log("[cpu] oracle on the logging sample")
+            out["cpu_baseline"] = cpu_logging_baseline(log_sample)
+        if inf_sample is not None:
+            log("[cpu] oracle on the influence sample")
+            out.setdefault("influence", {})["cpu_baseline"] = cpu_influence_baseline(inf_sample)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
