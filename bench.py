@@ -43,6 +43,24 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def measured_traffic(key, sources):
+    """HBM bytes per launch of a kernel from the committed counter summary
+    (profiles/traffic.json), or None when the kernel's sources changed since
+    the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))[key]
+    except (OSError, KeyError, ValueError):
+        return None, None
+    h = hashlib.sha256()
+    for f in sources:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if h.hexdigest()[:16] != rec.get("source_sha"):
+        return None, None
+    return rec["traffic_bytes"], rec["traffic_over_algorithmic"]
+
+
 class EventTimer:
     """Pairs of HIP events on the launch stream; mean duration per launch in ms."""
 
@@ -101,7 +119,8 @@ def logging_leg(args, torch, P):
     S = torch.zeros((n_layers, D, D), dtype=torch.float32, device=dev)
     lens = [W.lengths(W.rng(args.seed, 200, s), B, w.len_lo, w.len_hi) for s in range(n_steps)]
     masks = [torch.from_numpy(W.mask_from_lengths(L, T)).to(dev) for L in lens]
-    ws_bytes = P.logra_project_layers_ws_size(nl_block, B, T, k, k)
+    shape_descs = (P.LayerDesc * nl_block)(*[P.LayerDesc(0, 0, 0, 0, 0, ni, no) for _, ni, no in layers])
+    ws_bytes = P.logra_project_layers_ws_size(shape_descs, nl_block, B, T, k, k)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     L = P.lib()
@@ -162,13 +181,15 @@ def logging_leg(args, torch, P):
     bytes_per_launch = tokens / args.steps * per_tok + proj_bytes
     proj_ms = proj_timer.mean_ms()
     achieved = bytes_per_launch / (proj_ms * 1e-3) / 1e9
+    traffic, ratio = measured_traffic("projection", ["paper_2405_13954_amd/csrc/project.hip",
+                                                     "paper_2405_13954_amd/csrc/common.h"])
     res = {
         "tokens": tokens, "seconds": dt,
         "tokens_per_s": tokens / dt, "examples_per_s": examples / dt,
         "ms_per_step": dt * 1e3 / args.steps,
         "proj_launch_ms": proj_ms, "cov_launch_ms": cov_timer.mean_ms(),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "traffic_over_algorithmic": ratio,
                      "kernel": "logra_project_layers (7 Llama3-8B layers, B=8 ragged, k=16)",
                      "bytes_per_launch": bytes_per_launch},
     }
@@ -262,6 +283,8 @@ def influence_leg(args, torch, P):
     torch.cuda.synchronize()
     gemm_ms = only.mean_ms()
     achieved = flops / (gemm_ms * 1e-3) / 1e12
+    traffic, ratio = measured_traffic("scores", ["paper_2405_13954_amd/csrc/scores.hip",
+                                                 "paper_2405_13954_amd/csrc/common.h"])
     res = {
         "metric": "influence scores/sec (1,024 x 500,000 at 57,344 dims, top-100)",
         "value": Q * N / dt, "unit": "scores/s", "ms_per_pass": dt * 1e3,
@@ -270,7 +293,7 @@ def influence_leg(args, torch, P):
         "config": {"workload": "llama3_8b_scores", "N_train": N, "Q": Q, "D": D_tot, "blocks": nb,
                    "block": D, "N_cov": Nc, "damp": ex["damp"], "topk": topk},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / BF16_PEAK_TFLOPS, "traffic": None,
+                     "frac": achieved / BF16_PEAK_TFLOPS, "traffic": traffic, "traffic_over_algorithmic": ratio,
                      "kernel": "score GEMM (bf16 MFMA, fp32 accumulation)", "flops_per_launch": flops},
     }
     sample = None

@@ -80,12 +80,14 @@ const char *logra_version(void);
  *          flattened out-major: element o * k_in + i holds G_b[o][i].
  *          g_dtype F32 or BF16.  Rows may interleave with other layers'
  *          columns of a gradient store (g_ld >= k_in * k_out).
- *   ws     workspace of at least logra_project_ws_size(B, T, k_in, k_out)
- *          bytes; contents on entry are ignored.
+ *   ws     workspace of at least logra_project_ws_size(B, T, n_in, n_out,
+ *          k_in, k_out) bytes (fp32 partial sums, about
+ *          B * T * (n_in + n_out) / 2048 * 16 * ceil(k/16) * 4 bytes);
+ *          contents on entry are ignored.
  * Limits: n_in, n_out multiples of 8 (bf16) or 4 (fp32); 1 <= k <= LOGRA_MAX_K.
  * B = 0 or T = 0 is a no-op.  Deterministic: reruns are bitwise identical.
  * ---------------------------------------------------------------------- */
-size_t logra_project_ws_size(int B, int T, int k_in, int k_out);
+size_t logra_project_ws_size(int B, int T, int n_in, int n_out, int k_in, int k_out);
 int logra_project_layer(const void *x, const void *dy, int in_dtype, int B, int T, int n_in,
                         int n_out, const uint8_t *mask, const void *p_in, const void *p_out,
                         int k_in, int k_out, void *g_out, int g_dtype, int64_t g_ld, void *ws,
@@ -105,7 +107,8 @@ typedef struct {
     int n_out;
 } logra_layer_desc;
 
-size_t logra_project_layers_ws_size(int n_layers, int B, int T, int k_in, int k_out);
+size_t logra_project_layers_ws_size(const logra_layer_desc *layers, int n_layers, int B, int T,
+                                    int k_in, int k_out);
 int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
                          const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
                          void *ws, size_t ws_bytes, void *stream);

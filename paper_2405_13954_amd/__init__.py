@@ -63,11 +63,11 @@ def lib():
         vp, i32, i64, sz, f64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
         L.logra_last_error.restype = ctypes.c_char_p
         L.logra_version.restype = ctypes.c_char_p
-        L.logra_project_ws_size.argtypes = [i32, i32, i32, i32]
+        L.logra_project_ws_size.argtypes = [i32, i32, i32, i32, i32, i32]
         L.logra_project_ws_size.restype = sz
         L.logra_project_layer.argtypes = [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp, i32,
                                           i64, vp, sz, vp]
-        L.logra_project_layers_ws_size.argtypes = [i32, i32, i32, i32, i32]
+        L.logra_project_layers_ws_size.argtypes = [ctypes.POINTER(LayerDesc), i32, i32, i32, i32, i32]
         L.logra_project_layers_ws_size.restype = sz
         L.logra_project_layers.argtypes = [ctypes.POINTER(LayerDesc), i32, i32, i32, i32, vp, i32, i32,
                                            i32, i64, vp, sz, vp]
@@ -143,12 +143,13 @@ def logra_last_error() -> str:
     return lib().logra_last_error().decode()
 
 
-def logra_project_ws_size(B, T, k_in, k_out) -> int:
-    return int(lib().logra_project_ws_size(B, T, k_in, k_out))
+def logra_project_ws_size(B, T, n_in, n_out, k_in, k_out) -> int:
+    return int(lib().logra_project_ws_size(B, T, n_in, n_out, k_in, k_out))
 
 
-def logra_project_layers_ws_size(n_layers, B, T, k_in, k_out) -> int:
-    return int(lib().logra_project_layers_ws_size(n_layers, B, T, k_in, k_out))
+def logra_project_layers_ws_size(descs, n_layers, B, T, k_in, k_out) -> int:
+    """descs: a ctypes array of LayerDesc (only n_in and n_out are read)."""
+    return int(lib().logra_project_layers_ws_size(descs, n_layers, B, T, k_in, k_out))
 
 
 def logra_project_layer(x, dy, p_in, p_out, g_out, mask=None, ws=None, stream=None):
@@ -161,7 +162,7 @@ def logra_project_layer(x, dy, p_in, p_out, g_out, mask=None, ws=None, stream=No
     n_out = dy.shape[2]
     k_in, k_out = p_in.shape[0], p_out.shape[0]
     g_ld = _rows(g_out, k_in * k_out) if B > 0 else k_in * k_out
-    ws, wsb = _workspace(logra_project_ws_size(B, T, k_in, k_out), x.device, ws)
+    ws, wsb = _workspace(logra_project_ws_size(B, T, n_in, n_out, k_in, k_out), x.device, ws)
     _check(lib().logra_project_layer(_ptr(x), _ptr(dy), _dtype_code(x), B, T, n_in, n_out, _ptr(mask),
                                      _ptr(p_in), _ptr(p_out), k_in, k_out, _ptr(g_out), _dtype_code(g_out),
                                      g_ld, _ptr(ws), wsb, _stream(stream)))
@@ -180,7 +181,7 @@ def logra_project_layers(layers, mask=None, ws=None, stream=None):
     for i, L in enumerate(layers):
         arr[i] = LayerDesc(L["x"].data_ptr(), L["dy"].data_ptr(), L["p_in"].data_ptr(),
                            L["p_out"].data_ptr(), L["g_out"].data_ptr(), L["x"].shape[2], L["dy"].shape[2])
-    ws, wsb = _workspace(logra_project_layers_ws_size(n, B, T, k_in, k_out), x0.device, ws)
+    ws, wsb = _workspace(logra_project_layers_ws_size(arr, n, B, T, k_in, k_out), x0.device, ws)
     _check(lib().logra_project_layers(arr, n, _dtype_code(x0), B, T, _ptr(mask), k_in, k_out,
                                       _dtype_code(g0), g_ld, _ptr(ws), wsb, _stream(stream)))
 

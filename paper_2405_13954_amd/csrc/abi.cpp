@@ -93,13 +93,23 @@ extern "C" {
 const char *logra_last_error(void) { return g_err; }
 const char *logra_version(void) { return "logra-mi355x 0.1.0 (gfx950)"; }
 
-size_t logra_project_ws_size(int B, int T, int k_in, int k_out) {
-    return logra_project_layers_ws_size(1, B, T, k_in, k_out);
+size_t logra_project_ws_size(int B, int T, int n_in, int n_out, int k_in, int k_out) {
+    if (B <= 0 || T <= 0 || n_in <= 0 || n_out <= 0 || k_in <= 0 || k_out <= 0) return 0;
+    return round256(logra::project_ws_bytes(&n_in, &n_out, 1, B, T, k_in, k_out));
 }
 
-size_t logra_project_layers_ws_size(int n_layers, int B, int T, int k_in, int k_out) {
-    if (n_layers <= 0 || B <= 0 || T <= 0 || k_in <= 0 || k_out <= 0) return 0;
-    return round256(logra::project_partial_bytes(n_layers, B, T, k_in, k_out));
+size_t logra_project_layers_ws_size(const logra_layer_desc *layers, int n_layers, int B, int T,
+                                    int k_in, int k_out) {
+    if (layers == nullptr || n_layers <= 0 || n_layers > LOGRA_MAX_GROUP || B <= 0 || T <= 0 ||
+        k_in <= 0 || k_out <= 0)
+        return 0;
+    int n_in[LOGRA_MAX_GROUP], n_out[LOGRA_MAX_GROUP];
+    for (int l = 0; l < n_layers; ++l) {
+        if (layers[l].n_in <= 0 || layers[l].n_out <= 0) return 0;
+        n_in[l] = layers[l].n_in;
+        n_out[l] = layers[l].n_out;
+    }
+    return round256(logra::project_ws_bytes(n_in, n_out, n_layers, B, T, k_in, k_out));
 }
 
 int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
@@ -112,7 +122,6 @@ int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dt
     for (int l = 0; l < n_layers; ++l)
         TRY(check_proj_sizes(in_dtype, B, T, layers[l].n_in, layers[l].n_out, k_in, k_out, g_dtype, g_ld));
     if (B == 0 || T == 0) return ok();
-    const size_t ein = esize(in_dtype);
     logra::ProjGroup grp;
     std::memset(&grp, 0, sizeof grp);
     grp.n_layers = n_layers;
@@ -123,13 +132,12 @@ int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dt
         TRY(check_dev(d.p_in, "p_in", 16));
         TRY(check_dev(d.p_out, "p_out", 16));
         TRY(check_dev(d.g_out, "g_out", esize(g_dtype)));
-        (void)ein;
         grp.layer[l] = {d.x, d.dy, d.p_in, d.p_out, d.g_out, d.n_in, d.n_out};
     }
     if (mask) TRY(check_dev(mask, "mask", 1));
-    TRY(check_ws(ws, ws_bytes, logra_project_layers_ws_size(n_layers, B, T, k_in, k_out)));
+    TRY(check_ws(ws, ws_bytes, logra_project_layers_ws_size(layers, n_layers, B, T, k_in, k_out)));
     const hipError_t e = logra::launch_project(grp, in_dtype == LOGRA_BF16, B, T, mask, k_in, k_out,
-                                               g_dtype == LOGRA_BF16, g_ld, static_cast<float *>(ws),
+                                               g_dtype == LOGRA_BF16, g_ld, ws,
                                                static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "projection launch");
     return ok();

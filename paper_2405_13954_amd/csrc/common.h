@@ -23,6 +23,24 @@ __device__ __forceinline__ u32x4 ld128_nt(const void *p) {
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
 }
 
+// Raw buffer resource over [base, base + bytes): a lane whose byte offset is
+// at or beyond `bytes` reads zeros and touches no memory (the hardware range
+// check), which is how masked tokens and contraction tails are skipped
+// without branches.
+constexpr uint32_t kBufOOB = 0x80000000u;   // an offset beyond every range used here
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
+                                             static_cast<int>(bytes), 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0);
+}
+// Same, marked non-temporal (nt): for data streamed once, so that it does not
+// push reused data (projection matrices) out of L2.
+__device__ __forceinline__ u32x4 buf_ld128_nt(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 2);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
     return __builtin_bit_cast(bf16x8, v);
 }

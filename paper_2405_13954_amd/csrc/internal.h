@@ -7,7 +7,6 @@
 namespace logra {
 
 constexpr int kMaxGroup = 16;   // layers per grouped projection launch
-constexpr int kProjTile = 64;   // tokens per projection workgroup
 constexpr int kMaxK = 128;
 constexpr int kMaxTopk = 1024;
 constexpr int kMaxPrecondD = 8192;
@@ -27,12 +26,12 @@ struct ProjGroup {
     int n_layers;
 };
 
-// Projection (Sec. 3.1 Eq. (5)): per-tile partials into `partial`, then a
-// fixed-order sum over tiles into each layer's g_out rows.
-size_t project_partial_bytes(int n_layers, int B, int T, int k_in, int k_out);
+// Projection (Sec. 3.1 Eq. (5)): chunk partials and per-tile sums in the
+// workspace, then a fixed-order sum over tiles into each layer's g_out rows.
+size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, int T, int k_in,
+                        int k_out);
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
-                          int k_in, int k_out, bool bf16_out, int64_t g_ld, float *partial,
-                          hipStream_t s);
+                          int k_in, int k_out, bool bf16_out, int64_t g_ld, void *ws, hipStream_t s);
 
 // Covariance S_l += G_l^T G_l for n_blocks column blocks of width D.
 hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S,

@@ -2,37 +2,80 @@
 //
 //   G_b = sum_t m_bt (P_out dy_bt)(P_in x_bt)^T        (k_out x k_in, fp32)
 //
-// One workgroup (4 waves) owns a 64-token tile of one example of one layer.
-//  1. Projection: x'[64 x k_in] = X_tile P_in^T and dy'[64 x k_out] =
-//     dY_tile P_out^T on the matrix cores (16x16x32 bf16 or 16x16x4 fp32,
-//     fp32 accumulation).  The n-contraction is split into 32-wide steps
-//     dealt round-robin to the waves; each lane feeds a 128-bit global load
-//     straight into its MFMA operand (row = token for X, row = projection
-//     dimension for P), so x and dy are read from HBM once with no LDS
-//     staging.  Masked and out-of-range tokens are never loaded (their
-//     operand is zero), so NaN/Inf in padding cannot leak.
-//  2. The four waves' partial x'/dy' are folded in a fixed order through
-//     LDS (deterministic).
-//  3. The per-tile sum over tokens of dy'_t x'_t^T runs in fp32 from LDS,
-//     4x4 outputs per thread.
-// A second kernel adds the per-tile partials of each example in tile order
-// and writes G_b (fp32 or bf16) into the caller's store row.
+// The work of a layer group is cut into uniform items, so that every
+// workgroup streams about the same number of bytes whatever the layer widths
+// and the padding (layers differ up to 4x in bytes per token; half of the
+// tiles of a ragged batch are empty):
+//
+//  0. k_tile_list (masked inputs only): the ordered list of 64-token tiles
+//     holding at least one valid token.
+//  A. k_project_chunks (persistent, sized to the resident capacity): one item
+//     = one contraction chunk (<= 4096 columns) of one side (x or dy) of one
+//     listed tile.  The four waves deal the chunk's 32-wide steps
+//     round-robin; each lane feeds a 128-bit buffer load straight into its
+//     MFMA operand (row = token for x/dy, row = projection dimension for P;
+//     16x16x32 bf16 or 16x16x4 fp32, fp32 accumulation).  Masked tokens, rows
+//     of P beyond k and lanes past the chunk end get an out-of-range offset:
+//     they read zeros without a memory access or a branch, so NaN/Inf in
+//     padding cannot leak.  The waves' partial x'/dy' are folded in a fixed
+//     order and written, in the MFMA result layout, to the workspace.
+//  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
+//     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
+//     formed in fp32 from LDS (4x4 outputs per thread).  Empty tiles give 0.
+//  C. k_project_reduce: per example, the tile sums are added in tile order
+//     and G_b is written (fp32 or bf16, round to nearest even) to the
+//     caller's store row.
+// Every sum has a fixed order, so results are bitwise reproducible.
 #include "common.h"
 #include "internal.h"
 
 namespace logra {
 namespace {
 
-constexpr int TT = kProjTile;  // tokens per tile
-constexpr int NT = 256;        // threads per workgroup
-constexpr int NW = NT / kWave; // waves per workgroup
+#ifndef LOGRA_PROJ_STAGES
+#define LOGRA_PROJ_STAGES 3
+#endif
+#ifndef LOGRA_PROJ_ROWBLOCKS
+#define LOGRA_PROJ_ROWBLOCKS 4
+#endif
+#ifndef LOGRA_PROJ_CHUNK
+#define LOGRA_PROJ_CHUNK 4096
+#endif
+#ifndef LOGRA_PROJ_NT
+#define LOGRA_PROJ_NT 0
+#endif
+constexpr int MB = LOGRA_PROJ_ROWBLOCKS;  // 16-token row blocks per tile
+constexpr int TT = 16 * MB;               // tokens per tile
+constexpr int NW = 4;                     // waves per workgroup
+constexpr int NT = NW * kWave;            // threads per workgroup
+
+// Contraction columns per work item, and register pipeline depth, by
+// projection width (KT = ceil(k / 16)).
+__host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? 4096 : LOGRA_PROJ_CHUNK; }
+__host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGRA_PROJ_STAGES; }
+
+struct ChunkLayer {
+    const void *x;
+    const void *dy;
+    const void *p_in;
+    const void *p_out;
+    int64_t part_begin;  // first float of this layer's chunk partials
+    int n_in, n_out;
+    int c_in, c_out;     // chunks of the x side and of the dy side
+    int slot_begin;      // chunk slots of the layers before this one
+};
 
 struct ProjArgs {
-    ProjGroup grp;
+    ChunkLayer layer[kMaxGroup];
+    int n_layers;
+    int slots;      // chunk slots of all layers
     const uint8_t *mask;
-    float *partial;
+    const int *tiles;     // non-empty tiles (b * tpe + tile) in index order; NULL = all
+    const int *n_tiles;   // their count (device), read when tiles != NULL
+    float *part;    // chunk partials, MFMA result layout, TT x 16KT floats each
+    float *gpart;   // per-tile sums  [layer][b][tile][k_out * k_in]
     int B, T, tpe;  // tpe = tiles per example
-    int k_in, k_out;
+    int k_in, k_out, ck;
 };
 
 template <typename TIn>
@@ -49,164 +92,262 @@ struct InTraits<float> {
 };
 
 template <int KT>
-__device__ __forceinline__ void mma_step(f32x4 (&acc)[4][KT], const u32x4 (&xa)[4],
+__device__ __forceinline__ void mma_step(f32x4 (&acc)[MB][KT], const u32x4 (&xa)[MB],
                                          const u32x4 (&pb)[KT], bf16_bits) {
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < MB; ++m)
 #pragma unroll
         for (int j = 0; j < KT; ++j) acc[m][j] = mfma16_bf16(as_bf16x8(xa[m]), as_bf16x8(pb[j]), acc[m][j]);
 }
 
 template <int KT>
-__device__ __forceinline__ void mma_step(f32x4 (&acc)[4][KT], const u32x4 (&xa)[4],
+__device__ __forceinline__ void mma_step(f32x4 (&acc)[MB][KT], const u32x4 (&xa)[MB],
                                          const u32x4 (&pb)[KT], float) {
 #pragma unroll
     for (int e = 0; e < 4; ++e)
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
+        for (int m = 0; m < MB; ++m)
 #pragma unroll
             for (int j = 0; j < KT; ++j)
                 acc[m][j] = mfma16_f32(__uint_as_float(xa[m][e]), __uint_as_float(pb[j][e]), acc[m][j]);
 }
 
-// One wave's share of  A'[64 x 16KT] = A_tile[64 x n] * P^T  (P: k rows of n).
-// Contraction steps s = wave, wave + NW, ... ; two register stages so that
-// the next step's loads are in flight while the current step multiplies.
-template <int KT, typename TIn>
-__device__ __forceinline__ void project_part(f32x4 (&acc)[4][KT], const TIn *A, const TIn *P,
-                                             int n, int k, const bool (&tok_ok)[4], int wave,
+// One wave's share of  A'[TT x 16KT] = A[TT x nk] * P[k x nk]^T, A and P with
+// row strides lda and ldp.  Contraction steps s = wave, wave + NW, ... .
+// Every load is unconditional (out-of-range offsets read zeros), and the
+// ST-stage register pipeline keeps ST-1 steps in flight while a step
+// multiplies.  Each wave's step count is rounded up to a multiple of ST with
+// empty steps (no memory access, zero operands), so the loop body has no exits.
+template <int KT, typename TIn, int ST>
+__device__ __forceinline__ void project_part(f32x4 (&acc)[MB][KT], const TIn *A, int lda, const TIn *P,
+                                             int ldp, int nk, int k, const bool (&tok_ok)[MB], int wave,
                                              int lane) {
     constexpr int E = InTraits<TIn>::kElems;
     constexpr int S = InTraits<TIn>::kStep;
+    constexpr uint32_t ES = sizeof(TIn);
     const int row = lane & 15;
     const int kg = lane >> 4;
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < MB; ++m)
 #pragma unroll
         for (int j = 0; j < KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const TIn *arow[4];
-    const TIn *prow[KT];
-    bool p_ok[KT];
-#pragma unroll
-    for (int m = 0; m < 4; ++m) arow[m] = A + static_cast<size_t>(16 * m + row) * n + kg * E;
-#pragma unroll
-    for (int j = 0; j < KT; ++j) {
-        p_ok[j] = (16 * j + row) < k;
-        prow[j] = P + static_cast<size_t>(p_ok[j] ? 16 * j + row : 0) * n + kg * E;
-    }
-    const int nsteps = (n + S - 1) / S;
-
-    auto load = [&](int s, u32x4(&xa)[4], u32x4(&pb)[KT]) {
-        const int off = s * S;
-        const bool in_n = off + kg * E < n;
-        const u32x4 z = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int m = 0; m < 4; ++m) xa[m] = (tok_ok[m] && in_n) ? ld128_nt(arow[m] + off) : z;
-#pragma unroll
-        for (int j = 0; j < KT; ++j) pb[j] = (p_ok[j] && in_n) ? ld128(prow[j] + off) : z;
-    };
-
-    u32x4 xa0[4], pb0[KT], xa1[4], pb1[KT];
+    const int nsteps = (nk + S - 1) / S;
     int s = wave;
     if (s >= nsteps) return;
-    load(s, xa0, pb0);
-    while (true) {
-        if (s + NW < nsteps) load(s + NW, xa1, pb1);
-        mma_step<KT>(acc, xa0, pb0, TIn{});
-        s += NW;
-        if (s >= nsteps) break;
-        if (s + NW < nsteps) load(s + NW, xa0, pb0);
-        mma_step<KT>(acc, xa1, pb1, TIn{});
-        s += NW;
-        if (s >= nsteps) break;
+
+    const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * ES);
+    const auto rp = buf_rsrc(P, (static_cast<uint32_t>(k - 1) * ldp + nk) * ES);
+    uint32_t aoff[MB], poff[KT];
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+        aoff[m] = tok_ok[m] ? (static_cast<uint32_t>(16 * m + row) * lda + kg * E) * ES : kBufOOB;
+#pragma unroll
+    for (int j = 0; j < KT; ++j)
+        poff[j] = (16 * j + row < k) ? (static_cast<uint32_t>(16 * j + row) * ldp + kg * E) * ES : kBufOOB;
+
+    auto load = [&](int st, u32x4(&xa)[MB], u32x4(&pb)[KT]) {
+        const bool in_k = st * S + kg * E < nk;   // false past the last step: all lanes zero
+        const uint32_t koff = static_cast<uint32_t>(st * S) * ES;
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+            xa[m] = LOGRA_PROJ_NT ? buf_ld128_nt(ra, in_k ? aoff[m] + koff : kBufOOB)
+                                  : buf_ld128(ra, in_k ? aoff[m] + koff : kBufOOB);
+#pragma unroll
+        for (int j = 0; j < KT; ++j) pb[j] = buf_ld128(rp, in_k ? poff[j] + koff : kBufOOB);
+    };
+
+    const int iters = ((nsteps - wave + NW - 1) / NW + ST - 1) / ST;
+    u32x4 xa[ST][MB], pb[ST][KT];
+#pragma unroll
+    for (int i = 0; i < ST - 1; ++i) load(s + i * NW, xa[i], pb[i]);
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int i = 0; i < ST; ++i) {
+            load(s + (i + ST - 1) * NW, xa[(i + ST - 1) % ST], pb[(i + ST - 1) % ST]);
+            mma_step<KT>(acc, xa[i], pb[i], TIn{});
+        }
+        s += ST * NW;
     }
 }
 
-// Fold the four waves' accumulators (order ((w3 + w2) + w1) + w0) and write
-// the result as dst[token][16*KT] fp32.
-template <int KT>
-__device__ __forceinline__ void fold_waves(f32x4 (&acc)[4][KT], f32x4 *red, float *dst, int wave,
-                                           int lane) {
-    f32x4 *slot = red + lane;  // red[(m*KT + j) * 64 + lane]
+// Validity of the MB token rows a lane feeds (tokens t0 + 16m + lane%16):
+// each lane loads the flags of tokens t0 + lane and t0 + 64 + lane (one
+// coalesced load each), and the rows are gathered by lane shuffles.
+// Returns whether any of the lane's rows is valid.
+__device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, int lane, bool (&tok_ok)[MB]) {
+    int v[(TT + kWave - 1) / kWave];
+#pragma unroll
+    for (int h = 0; h < (TT + kWave - 1) / kWave; ++h) {
+        const int t = t0 + h * kWave + lane;
+        int ok = t < a.T && h * kWave + lane < TT;
+        if (a.mask && ok) ok = a.mask[static_cast<size_t>(b) * a.T + t] != 0;
+        v[h] = ok;
+    }
+    bool any = false;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+        const int r = 16 * m + (lane & 15);
+        tok_ok[m] = __shfl(v[r / kWave], r % kWave, kWave) != 0;
+        any |= tok_ok[m];
+    }
+    return any;
+}
+
+// One chunk item (see the file comment).  Returns without a barrier when the
+// tile is fully masked; every thread of the workgroup takes the same path.
+template <int KT, typename TIn>
+__device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int count, f32x4 *slot, int lane,
+                                           int wave) {
+    const int gslot = item / count;             // chunk slot over all layers
+    const int j = item - gslot * count;         // listed tile
+    int l = 0;
+    while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
+    const ChunkLayer &L = a.layer[l];
+    const int cs = gslot - L.slot_begin;        // chunk slot of the layer: x chunks, then dy chunks
+    const int bt = a.tiles ? a.tiles[j] : j;
+    const int b = bt / a.tpe, tile = bt - b * a.tpe;
+
+    bool tok_ok[MB];
+    lane_tokens(a, b, tile * TT, lane, tok_ok);  // listed tiles have at least one valid token
+    __syncthreads();   // the previous item's reads of `slot` are done
+
+    const bool xside = cs < L.c_in;
+    const int c = xside ? cs : cs - L.c_in;
+    const int n = xside ? L.n_in : L.n_out;
+    const int k = xside ? a.k_in : a.k_out;
+    const int col0 = c * a.ck;
+    const int nk = min(a.ck, n - col0);
+    const size_t tok0 = static_cast<size_t>(b) * a.T + static_cast<size_t>(tile) * TT;
+    const TIn *A = static_cast<const TIn *>(xside ? L.x : L.dy) + tok0 * n + col0;
+    const TIn *P = static_cast<const TIn *>(xside ? L.p_in : L.p_out) + col0;
+
+    f32x4 acc[MB][KT];
+    project_part<KT, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
+
+    // fold the waves in the order ((w3 + w2) + w1) + w0, then write the
+    // result in the MFMA layout: element (m, j) of lane l at [(m*KT + j)*64 + l]
+    f32x4 *my = slot + lane;
     if (wave == NW - 1) {
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
+        for (int m = 0; m < MB; ++m)
 #pragma unroll
-            for (int j = 0; j < KT; ++j) slot[(m * KT + j) * kWave] = acc[m][j];
+            for (int j = 0; j < KT; ++j) my[(m * KT + j) * kWave] = acc[m][j];
     }
     __syncthreads();
 #pragma unroll
     for (int w = NW - 2; w >= 1; --w) {
         if (wave == w) {
 #pragma unroll
-            for (int m = 0; m < 4; ++m)
+            for (int m = 0; m < MB; ++m)
 #pragma unroll
-                for (int j = 0; j < KT; ++j) slot[(m * KT + j) * kWave] = slot[(m * KT + j) * kWave] + acc[m][j];
+                for (int j = 0; j < KT; ++j) my[(m * KT + j) * kWave] = my[(m * KT + j) * kWave] + acc[m][j];
         }
         __syncthreads();
     }
     if (wave == 0) {
-        const int row = lane & 15, kg = lane >> 4;
+        f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + L.part_begin +
+                                               (static_cast<size_t>(bt) * (L.c_in + L.c_out) + cs) * (TT * 16 * KT));
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
+        for (int m = 0; m < MB; ++m)
 #pragma unroll
-            for (int j = 0; j < KT; ++j) {
-                const f32x4 v = slot[(m * KT + j) * kWave] + acc[m][j];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) dst[(16 * m + 4 * kg + r) * (16 * KT) + 16 * j + row] = v[r];
-            }
+            for (int j = 0; j < KT; ++j) dst[(m * KT + j) * kWave + lane] = my[(m * KT + j) * kWave] + acc[m][j];
     }
-    __syncthreads();
 }
 
+// Persistent: the grid is sized to the resident capacity of the GPU and each
+// workgroup strides over the items (chunk slot x non-empty tile), which all
+// carry the same work.  The loop bound is uniform and finite.
 template <int KT, typename TIn>
-__global__ __launch_bounds__(NT) void k_project_tiles(ProjArgs a) {
-    constexpr int KP = 16 * KT;              // padded projection width
+__global__ __launch_bounds__(NT) void k_project_chunks(ProjArgs a) {
+    __shared__ f32x4 slot[MB * KT * kWave];   // cross-wave fold
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int count = a.tiles ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : a.B * a.tpe;
+    const int items = count * a.slots;
+    for (int item = blockIdx.x; item < items; item += gridDim.x) chunk_item<KT, TIn>(a, item, count, slot, lane, wave);
+}
+
+// Ordered list of the tiles with at least one valid token (one workgroup;
+// block-wide prefix counts keep the list in tile order).
+__global__ __launch_bounds__(1024) void k_tile_list(const uint8_t *mask, int B, int T, int tpe, int *tiles,
+                                                     int *n_tiles) {
+    __shared__ int wsum[16];
+    __shared__ int base;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid == 0) base = 0;
+    __syncthreads();
+    const int total = B * tpe;
+    for (int t0 = 0; t0 < total; t0 += 1024) {
+        const int bt = t0 + tid;
+        int any = 0;
+        if (bt < total) {
+            const int b = bt / tpe, tile = bt - b * tpe;
+            const uint8_t *m = mask + static_cast<size_t>(b) * T + static_cast<size_t>(tile) * TT;
+            const int n = min(TT, T - tile * TT);
+            for (int i = 0; i < n && !any; ++i) any = m[i] != 0;
+        }
+        int x = any;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(x, o, 64);
+            if (lane >= o) x += y;
+        }
+        if (lane == 63) wsum[wave] = x;
+        __syncthreads();
+        int before = 0, all = 0;
+        for (int w = 0; w < 16; ++w) {
+            before += w < wave ? wsum[w] : 0;
+            all += wsum[w];
+        }
+        if (any) tiles[base + before + x - 1] = bt;
+        __syncthreads();
+        if (tid == 0) base += all;
+        __syncthreads();
+    }
+    if (tid == 0) *n_tiles = base;
+}
+
+template <int KT>
+__global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a) {
+    constexpr int KP = 16 * KT;
+    constexpr int NQ = MB * KT * kWave;     // f32x4 per chunk partial
     __shared__ float xs[TT * KP];            // x'  [token][i]
     __shared__ float ds[TT * KP];            // dy' [token][o]
-    __shared__ f32x4 red[4 * KT * kWave];    // cross-wave fold slot
-
     const int per_layer = a.B * a.tpe;
     const int l = blockIdx.x / per_layer;
-    const int rem = blockIdx.x - l * per_layer;
-    const int b = rem / a.tpe;
-    const int tile = rem - b * a.tpe;
-    const int t0 = tile * TT;
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int bt = blockIdx.x - l * per_layer;
+    const int b = bt / a.tpe, tile = bt - b * a.tpe;
+    const int tid = threadIdx.x;
     const int D = a.k_in * a.k_out;
-    float *part = a.partial + (static_cast<size_t>(l * a.B + b) * a.tpe + tile) * D;
+    float *gdst = a.gpart + static_cast<size_t>(blockIdx.x) * D;
 
-    // Token validity of the four rows this lane feeds (tokens t0 + 16m + lane%16).
-    bool tok_ok[4];
-    bool any = false;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const int t = t0 + 16 * m + (lane & 15);
-        bool ok = t < a.T;
-        if (ok && a.mask) ok = a.mask[static_cast<size_t>(b) * a.T + t] != 0;
-        tok_ok[m] = ok;
-        any |= ok;
-    }
-    if (!__syncthreads_or(any)) {  // fully masked tile: contributes zero
-        for (int i = tid; i < D; i += NT) part[i] = 0.f;
+    bool tok_ok[MB];
+    const bool any = lane_tokens(a, b, tile * TT, tid & (kWave - 1), tok_ok);
+    if (!__syncthreads_or(any)) {
+        for (int i = tid; i < D; i += 256) gdst[i] = 0.f;
         return;
     }
-
-    const ProjLayer &L = a.grp.layer[l];
-    const size_t tok0 = static_cast<size_t>(b) * a.T + t0;
-    f32x4 acc[4][KT];
-
-    project_part<KT>(acc, static_cast<const TIn *>(L.x) + tok0 * L.n_in,
-                     static_cast<const TIn *>(L.p_in), L.n_in, a.k_in, tok_ok, wave, lane);
-    fold_waves<KT>(acc, red, xs, wave, lane);
-    project_part<KT>(acc, static_cast<const TIn *>(L.dy) + tok0 * L.n_out,
-                     static_cast<const TIn *>(L.p_out), L.n_out, a.k_out, tok_ok, wave, lane);
-    fold_waves<KT>(acc, red, ds, wave, lane);
+    const ChunkLayer &L = a.layer[l];
+    const int C = L.c_in + L.c_out;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP));
+    for (int q = tid; q < NQ; q += 256) {
+        f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sd = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < L.c_in; ++c) sx += src[static_cast<size_t>(c) * NQ + q];
+        for (int c = L.c_in; c < C; ++c) sd += src[static_cast<size_t>(c) * NQ + q];
+        const int lane = q & (kWave - 1), mj = q / kWave;
+        const int m = mj / KT, j = mj - m * KT;
+        const int row = lane & 15, kg = lane >> 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            xs[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sx[r];
+            ds[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sd[r];
+        }
+    }
+    __syncthreads();
 
     // Sum over the tile's tokens of dy'_t x'_t^T; 4x4 outputs per thread.
-    constexpr int NB = 4 * KT;  // 4-wide blocks per side
-    for (int blk = tid; blk < NB * NB; blk += NT) {
+    constexpr int NB = 4 * KT;
+    for (int blk = tid; blk < NB * NB; blk += 256) {
         const int ob = blk / NB, ib = blk - (blk / NB) * NB;
         float c[4][4];
 #pragma unroll
@@ -228,18 +369,18 @@ __global__ __launch_bounds__(NT) void k_project_tiles(ProjArgs a) {
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int i = 4 * ib + v;
-                if (i < a.k_in) part[o * a.k_in + i] = c[u][v];
+                if (i < a.k_in) gdst[o * a.k_in + i] = c[u][v];
             }
         }
     }
 }
 
 template <typename TOut>
-__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *partial, int B,
+__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, int B,
                                                         int tpe, int D, int64_t g_ld) {
     const int l = blockIdx.x / B;
     const int b = blockIdx.x - l * B;
-    const float *p = partial + static_cast<size_t>(l * B + b) * tpe * D;
+    const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * D;
     TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
     for (int i = threadIdx.x; i < D; i += blockDim.x) {
         float s = 0.f;
@@ -248,59 +389,142 @@ __global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const flo
     }
 }
 
+inline int kt_for(int k_in, int k_out) {
+    const int kmax = k_in > k_out ? k_in : k_out;
+    return kmax <= 16 ? 1 : kmax <= 32 ? 2 : kmax <= 64 ? 4 : 8;
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+struct Plan {
+    size_t part_floats = 0, gpart_floats = 0;
+    int slots = 0;
+};
+
+// Work items and workspace of a group; fills the per-layer fields of `a` if given.
+Plan plan_group(const int *n_in, const int *n_out, int n_layers, int B, int T, int k_in, int k_out,
+                ProjArgs *a) {
+    const int KT = kt_for(k_in, k_out);
+    const int ck = chunk_cols(KT);
+    const int tpe = (T + TT - 1) / TT;
+    Plan p;
+    for (int l = 0; l < n_layers; ++l) {
+        const int ci = (n_in[l] + ck - 1) / ck, co = (n_out[l] + ck - 1) / ck;
+        if (a) {
+            a->layer[l].n_in = n_in[l];
+            a->layer[l].n_out = n_out[l];
+            a->layer[l].c_in = ci;
+            a->layer[l].c_out = co;
+            a->layer[l].slot_begin = p.slots;
+            a->layer[l].part_begin = static_cast<int64_t>(p.part_floats);
+        }
+        p.slots += ci + co;
+        p.part_floats += static_cast<size_t>(ci + co) * B * tpe * TT * 16 * KT;
+    }
+    p.gpart_floats = static_cast<size_t>(n_layers) * B * tpe * k_in * k_out;
+    return p;
+}
+
+// Resident workgroups of a kernel on the current device (computed once per
+// device and kernel).
 template <int KT, typename TIn>
-hipError_t launch_tiles(const ProjArgs &a, int n_layers, hipStream_t s) {
-    const unsigned grid = static_cast<unsigned>(n_layers) * a.B * a.tpe;
-    hipLaunchKernelGGL((k_project_tiles<KT, TIn>), dim3(grid), dim3(NT), 0, s, a);
-    return hipGetLastError();
+int resident_groups() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+    if (cache[dev] == 0) {
+        int cus = 0, per_cu = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            cus = 256;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void *>(k_project_chunks<KT, TIn>), NT, 0) != hipSuccess ||
+            per_cu <= 0)
+            per_cu = 1;
+        cache[dev] = cus * per_cu;
+    }
+    return cache[dev];
+}
+
+template <int KT, typename TIn>
+void launch_chunks(const ProjArgs &a, int max_items, hipStream_t s) {
+    const int grid = max_items < resident_groups<KT, TIn>() ? max_items : resident_groups<KT, TIn>();
+    hipLaunchKernelGGL((k_project_chunks<KT, TIn>), dim3(grid), dim3(NT), 0, s, a);
 }
 
 }  // namespace
 
-size_t project_partial_bytes(int n_layers, int B, int T, int k_in, int k_out) {
-    const size_t tpe = (static_cast<size_t>(T) + TT - 1) / TT;
-    return static_cast<size_t>(n_layers) * B * tpe * k_in * k_out * sizeof(float);
+size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, int T, int k_in,
+                        int k_out) {
+    if (n_layers <= 0 || B <= 0 || T <= 0) return 0;
+    const Plan p = plan_group(n_in, n_out, n_layers, B, T, k_in, k_out, nullptr);
+    const size_t tiles = static_cast<size_t>(B) * ((T + TT - 1) / TT);
+    return align256(p.part_floats * sizeof(float)) + align256(p.gpart_floats * sizeof(float)) +
+           align256((tiles + 1) * sizeof(int));
 }
 
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
-                          int k_in, int k_out, bool bf16_out, int64_t g_ld, float *partial,
-                          hipStream_t s) {
+                          int k_in, int k_out, bool bf16_out, int64_t g_ld, void *ws, hipStream_t s) {
     if (B == 0 || T == 0 || grp.n_layers == 0) return hipSuccess;
     ProjArgs a;
-    a.grp = grp;
+    int n_in[kMaxGroup], n_out[kMaxGroup];
+    for (int l = 0; l < grp.n_layers; ++l) {
+        n_in[l] = grp.layer[l].n_in;
+        n_out[l] = grp.layer[l].n_out;
+        a.layer[l].x = grp.layer[l].x;
+        a.layer[l].dy = grp.layer[l].dy;
+        a.layer[l].p_in = grp.layer[l].p_in;
+        a.layer[l].p_out = grp.layer[l].p_out;
+    }
+    const Plan p = plan_group(n_in, n_out, grp.n_layers, B, T, k_in, k_out, &a);
+    const int KT = kt_for(k_in, k_out);
+    a.n_layers = grp.n_layers;
+    a.slots = p.slots;
     a.mask = mask;
-    a.partial = partial;
+    char *w = static_cast<char *>(ws);
+    a.part = reinterpret_cast<float *>(w);
+    w += align256(p.part_floats * sizeof(float));
+    a.gpart = reinterpret_cast<float *>(w);
+    w += align256(p.gpart_floats * sizeof(float));
     a.B = B;
     a.T = T;
     a.tpe = (T + TT - 1) / TT;
     a.k_in = k_in;
     a.k_out = k_out;
-    const int kmax = k_in > k_out ? k_in : k_out;
-    const int kt = kmax <= 16 ? 1 : kmax <= 32 ? 2 : kmax <= 64 ? 4 : 8;
-    hipError_t e;
-    if (bf16_in) {
-        switch (kt) {
-            case 1: e = launch_tiles<1, bf16_bits>(a, grp.n_layers, s); break;
-            case 2: e = launch_tiles<2, bf16_bits>(a, grp.n_layers, s); break;
-            case 4: e = launch_tiles<4, bf16_bits>(a, grp.n_layers, s); break;
-            default: e = launch_tiles<8, bf16_bits>(a, grp.n_layers, s); break;
-        }
-    } else {
-        switch (kt) {
-            case 1: e = launch_tiles<1, float>(a, grp.n_layers, s); break;
-            case 2: e = launch_tiles<2, float>(a, grp.n_layers, s); break;
-            case 4: e = launch_tiles<4, float>(a, grp.n_layers, s); break;
-            default: e = launch_tiles<8, float>(a, grp.n_layers, s); break;
-        }
+    a.ck = chunk_cols(KT);
+    a.tiles = nullptr;
+    a.n_tiles = nullptr;
+    if (mask) {
+        int *list = reinterpret_cast<int *>(w);
+        int *count = list + static_cast<size_t>(B) * a.tpe;
+        hipLaunchKernelGGL(k_tile_list, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count);
+        a.tiles = list;
+        a.n_tiles = count;
     }
+    const int max_items = p.slots * B * a.tpe;
+    switch (KT) {
+        case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, s) : launch_chunks<1, float>(a, max_items, s); break;
+        case 2: bf16_in ? launch_chunks<2, bf16_bits>(a, max_items, s) : launch_chunks<2, float>(a, max_items, s); break;
+        case 4: bf16_in ? launch_chunks<4, bf16_bits>(a, max_items, s) : launch_chunks<4, float>(a, max_items, s); break;
+        default: bf16_in ? launch_chunks<8, bf16_bits>(a, max_items, s) : launch_chunks<8, float>(a, max_items, s); break;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const unsigned tiles = static_cast<unsigned>(grp.n_layers) * B * a.tpe;
+    switch (KT) {
+        case 1: hipLaunchKernelGGL((k_project_tile_finish<1>), dim3(tiles), dim3(256), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((k_project_tile_finish<2>), dim3(tiles), dim3(256), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_project_tile_finish<4>), dim3(tiles), dim3(256), 0, s, a); break;
+        default: hipLaunchKernelGGL((k_project_tile_finish<8>), dim3(tiles), dim3(256), 0, s, a); break;
+    }
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned grid = static_cast<unsigned>(grp.n_layers) * B;
     if (bf16_out)
-        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid), dim3(256), 0, s, grp, partial,
-                           B, a.tpe, k_in * k_out, g_ld);
+        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+                           k_in * k_out, g_ld);
     else
-        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid), dim3(256), 0, s, grp, partial, B,
-                           a.tpe, k_in * k_out, g_ld);
+        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+                           k_in * k_out, g_ld);
     return hipGetLastError();
 }
 
