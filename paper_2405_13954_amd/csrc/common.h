@@ -8,6 +8,7 @@ namespace logra {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_bits;
 
@@ -95,6 +96,11 @@ __device__ __forceinline__ f32x4 mfma16_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
 }
 __device__ __forceinline__ f32x4 mfma16_f32(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+// fp64 16x16x4: same operand layout, but result register r of lane l holds
+// row (l/16) + 4r of column l % 16 (rows interleaved, unlike the fp32 shapes).
+__device__ __forceinline__ f64x4 mfma16_f64(double a, double b, f64x4 c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 // 32x32x16: lane l holds row (l % 32) of A / column (l % 32) of B; result
 // register r holds row 8*(r/4) + 4*(l/32) + (r%4) of column l % 32.

@@ -11,10 +11,13 @@
 //   3. blocked right-looking Cholesky, 64-wide panels: factor the diagonal
 //      block in LDS, solve the panel below it, SYRK-update the trailing
 //      matrix;  a non-positive pivot sets the block's status word;
-//   4. forward and backward substitution for up to 16 right-hand sides per
-//      workgroup, the right-hand sides resident in LDS, L streamed through
-//      LDS in coalesced 64x64 tiles, the 64x64 triangles solved one row at a
-//      time with a fixed-order wavefront reduction.
+//   4. the inverse of each 64x64 diagonal tile of L;
+//   5. blocked forward and backward substitution for 64 right-hand sides per
+//      workgroup, every step a 64x64x64 product on the fp64 matrix cores:
+//        forward   R_i = G_i - sum_{j<i} L_ij Y_j,     Y_i = inv(L_ii) R_i
+//        backward  R_i = Y_i - sum_{j>i} L_ji^T Z_j,   Z_i = inv(L_ii)^T R_i
+//      (tiles staged through LDS with coalesced loads, Y and Z in the
+//      workspace), so no step is a row-by-row recurrence.
 #include "common.h"
 #include "internal.h"
 
@@ -25,21 +28,33 @@ constexpr int NB = 64;   // panel width / tile edge
 constexpr int LT = NB + 1;
 
 struct WsLayout {
-    double *A;
-    double *lam;
-    int *info;
+    double *A;      // [n_blocks][D][D], lower triangle: C + lambda I, then L
+    double *lam;    // [n_blocks]
+    int *info;      // [n_blocks] 0 or 1 + first non-positive pivot
+    double *Linv;   // [n_blocks][nbt][64][64] inverses of the diagonal tiles of L
+    double *Y;      // [n_blocks][D][Qp] forward solutions
+    double *Z;      // [n_blocks][D][Qp] backward solutions
 };
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+inline int tiles_of(int D) { return (D + NB - 1) / NB; }
+inline int padded_q(int Q) { return (Q + NB - 1) / NB * NB; }
 
-inline WsLayout ws_layout(void *ws, int D, int n_blocks) {
+inline WsLayout ws_layout(void *ws, int D, int n_blocks, int Q) {
     char *p = static_cast<char *>(ws);
+    const size_t nb = static_cast<size_t>(n_blocks);
     WsLayout w;
     w.A = reinterpret_cast<double *>(p);
-    p += align256(sizeof(double) * static_cast<size_t>(n_blocks) * D * D);
+    p += align256(sizeof(double) * nb * D * D);
     w.lam = reinterpret_cast<double *>(p);
-    p += align256(sizeof(double) * n_blocks);
+    p += align256(sizeof(double) * nb);
     w.info = reinterpret_cast<int *>(p);
+    p += align256(sizeof(int) * nb);
+    w.Linv = reinterpret_cast<double *>(p);
+    p += align256(sizeof(double) * nb * tiles_of(D) * NB * NB);
+    w.Y = reinterpret_cast<double *>(p);
+    p += align256(sizeof(double) * nb * D * padded_q(Q));
+    w.Z = reinterpret_cast<double *>(p);
     return w;
 }
 
@@ -178,121 +193,167 @@ __global__ __launch_bounds__(256) void k_syrk_update(double *A_all, int D, int k
     }
 }
 
-__device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+// Inverse of the lower-triangular 64x64 diagonal tile t of L (zero padded
+// past D): thread c computes column c by substitution, L_tt w = e_c.
+__global__ __launch_bounds__(64) void k_diag_inv(const double *A_all, int D, double *Linv_all) {
+    __shared__ double a[NB * LT];
+    __shared__ double wl[NB * LT];
+    const int t = blockIdx.x, blk = blockIdx.y, c = threadIdx.x;
+    const double *A = A_all + static_cast<size_t>(blk) * D * D;
+    const int r0 = t * NB, nb = min(NB, D - r0);
+    for (int i = 0; i < NB; ++i)
+        a[i * LT + c] = (i < nb && c <= i) ? A[static_cast<size_t>(r0 + i) * D + r0 + c] : 0.0;
+    __syncthreads();
+    double *W = Linv_all + (static_cast<size_t>(blk) * gridDim.x + t) * NB * NB;
+    for (int r = 0; r < NB; ++r) {
+        double v = 0.0;
+        if (c < nb && r < nb && r >= c) {
+            if (r == c) {
+                v = 1.0 / a[r * LT + r];
+            } else {
+                double s = 0.0;
+                for (int m = c; m < r; ++m) s = fma(a[r * LT + m], wl[m * LT + c], s);
+                v = -s / a[r * LT + r];
+            }
+        }
+        wl[r * LT + c] = v;   // only this thread reads column c
+        W[r * NB + c] = v;
+    }
 }
 
-// Forward (L y = g) and backward (L^T z = y) substitution for R right-hand
-// sides of one block; y lives in LDS as y[d * R + r].
+// Blocked substitution on the matrix cores for 64 right-hand sides (queries
+// q0 .. q0+63) of one layer block.  Wave w owns rows 16w..16w+15 of the
+// 64 x 64 (rows x queries) tile; acc[c] holds columns 16c..16c+15 in the
+// fp64 16x16 result layout (register r of lane l: row l/16 + 4r).
 template <typename TIn, typename TOut>
-__global__ __launch_bounds__(256) void k_solve(const double *A_all, int D, int R, const TIn *g,
-                                               int64_t ld_in, int Q, TOut *out, int64_t ld_out) {
-    extern __shared__ double smem[];
-    double *Lt = smem;              // [NB][LT]
-    double *y = smem + NB * LT;     // [D][R]
-    const int blk = blockIdx.y, q0 = blockIdx.x * R;
+__global__ __launch_bounds__(256) void k_trsm_f64(const double *A_all, const double *Linv_all, int D,
+                                                  const TIn *g, int64_t ld_in, int Q, int Qp, double *Y_all,
+                                                  double *Z_all, TOut *out, int64_t ld_out) {
+    __shared__ double La[NB * LT];   // A operand tile [row][k]
+    __shared__ double Yb[NB * LT];   // B operand tile [k][query]
+    const int blk = blockIdx.y, q0 = blockIdx.x * NB;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int row = lane & 15, kg = lane >> 4;
+    const int nbt = (D + NB - 1) / NB;
     const double *L = A_all + static_cast<size_t>(blk) * D * D;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nq = min(R, Q - q0);
+    const double *Li = Linv_all + static_cast<size_t>(blk) * nbt * NB * NB;
+    double *Y = Y_all + static_cast<size_t>(blk) * D * Qp;
+    double *Z = Z_all + static_cast<size_t>(blk) * D * Qp;
+    f64x4 acc[4];
 
-    for (int r = 0; r < R; ++r)
-        for (int d = tid; d < D; d += 256)
-            y[d * R + r] = (r < nq) ? load_in_d<TIn>(g + static_cast<int64_t>(q0 + r) * ld_in + static_cast<int64_t>(blk) * D + d) : 0.0;
-    __syncthreads();
-
-    const int nblk = (D + NB - 1) / NB;
-    // ---------------- forward ----------------
-    for (int bi = 0; bi < nblk; ++bi) {
-        const int i0 = bi * NB, nbi = min(NB, D - i0);
-        double acc[4] = {0.0, 0.0, 0.0, 0.0};
-        for (int m0 = 0; m0 < i0; m0 += NB) {
-            for (int e = tid; e < NB * NB; e += 256) {
-                const int r = e / NB, c = e - (e / NB) * NB;
-                Lt[r * LT + c] = (r < nbi) ? L[static_cast<size_t>(i0 + r) * D + m0 + c] : 0.0;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int p = tid + 256 * u;
-                const int i = p & 63, r = p >> 6;
-                if (r < R) {
-                    double s = acc[u];
-                    for (int m = 0; m < NB; ++m) s = fma(Lt[i * LT + m], y[(m0 + m) * R + r], s);
-                    acc[u] = s;
-                }
-            }
-            __syncthreads();
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int p = tid + 256 * u;
-            const int i = p & 63, r = p >> 6;
-            if (r < R && i < nbi) y[(i0 + i) * R + r] -= acc[u];
-        }
+    // La[rr][cc] = L[r0+rr][c0+cc] (strictly lower tiles only), or its transpose.
+    auto stage_L = [&](int r0, int c0, bool transpose) {
         for (int e = tid; e < NB * NB; e += 256) {
-            const int r = e / NB, c = e - (e / NB) * NB;
-            Lt[r * LT + c] = (r < nbi && c <= r) ? L[static_cast<size_t>(i0 + r) * D + i0 + c] : 0.0;
-        }
-        __syncthreads();
-        for (int r = wave; r < R; r += 4) {
-            double ym = (lane < nbi) ? y[(i0 + lane) * R + r] : 0.0;
-            for (int i = 0; i < nbi; ++i) {
-                const double s = wave_sum(lane < i ? Lt[i * LT + lane] * ym : 0.0);
-                if (lane == i) ym = (ym - s) / Lt[i * LT + i];
+            const int u = e / NB, v = e - (e / NB) * NB;   // consecutive threads: consecutive v
+            if (!transpose) {
+                La[u * LT + v] = (r0 + u < D && c0 + v < D) ? L[static_cast<size_t>(r0 + u) * D + c0 + v] : 0.0;
+            } else {   // La[v][u] = L[c0+u][r0+v]
+                La[v * LT + u] = (c0 + u < D && r0 + v < D) ? L[static_cast<size_t>(c0 + u) * D + r0 + v] : 0.0;
             }
-            if (lane < nbi) y[(i0 + lane) * R + r] = ym;
         }
+    };
+    auto stage_Linv = [&](int i, bool transpose) {
+        const double *T = Li + static_cast<size_t>(i) * NB * NB;
+        for (int e = tid; e < NB * NB; e += 256) {
+            const int u = e / NB, v = e - (e / NB) * NB;
+            if (!transpose) La[u * LT + v] = T[e];
+            else La[v * LT + u] = T[e];
+        }
+    };
+    auto stage_B = [&](const double *src, int j) {   // Yb[kk][qq] = src[j*64 + kk][q0 + qq]
+        for (int e = tid; e < NB * NB; e += 256) {
+            const int kk = e / NB, qq = e - (e / NB) * NB;
+            Yb[kk * LT + qq] = (j * NB + kk < D) ? src[static_cast<size_t>(j * NB + kk) * Qp + q0 + qq] : 0.0;
+        }
+    };
+    auto mma = [&](double sign) {
+#pragma unroll 4
+        for (int s4 = 0; s4 < NB / 4; ++s4) {
+            const double a = sign * La[(16 * w + row) * LT + 4 * s4 + kg];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[c] = mfma16_f64(a, Yb[(4 * s4 + kg) * LT + 16 * c + row], acc[c]);
+        }
+    };
+    auto acc_to_B = [&]() {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) Yb[(16 * w + kg + 4 * r) * LT + 16 * c + row] = acc[c][r];
+    };
+    auto zero = [&]() {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[c] = f64x4{0.0, 0.0, 0.0, 0.0};
+    };
+    auto store_ws = [&](double *dst, int i) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int d = i * NB + 16 * w + kg + 4 * r;
+                if (d < D) dst[static_cast<size_t>(d) * Qp + q0 + 16 * c + row] = acc[c][r];
+            }
+    };
+
+    // ---------------- forward: L Y = G ----------------
+    for (int i = 0; i < nbt; ++i) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int q = q0 + 16 * c + row, d = i * NB + 16 * w + kg + 4 * r;
+                acc[c][r] = (q < Q && d < D) ? load_in_d<TIn>(g + static_cast<int64_t>(q) * ld_in +
+                                                               static_cast<int64_t>(blk) * D + d)
+                                             : 0.0;
+            }
+        for (int j = 0; j < i; ++j) {
+            stage_L(i * NB, j * NB, false);
+            stage_B(Y, j);
+            __syncthreads();
+            mma(-1.0);
+            __syncthreads();
+        }
+        acc_to_B();
+        stage_Linv(i, false);
+        __syncthreads();
+        zero();
+        mma(1.0);
+        store_ws(Y, i);
         __syncthreads();
     }
-    // ---------------- backward ----------------
-    for (int bi = nblk - 1; bi >= 0; --bi) {
-        const int i0 = bi * NB, nbi = min(NB, D - i0);
-        double acc[4] = {0.0, 0.0, 0.0, 0.0};
-        for (int m0 = i0 + NB; m0 < D; m0 += NB) {
-            const int nm = min(NB, D - m0);
-            for (int e = tid; e < NB * NB; e += 256) {
-                const int r = e / NB, c = e - (e / NB) * NB;   // r: row m, c: column i
-                Lt[r * LT + c] = (r < nm && c < nbi) ? L[static_cast<size_t>(m0 + r) * D + i0 + c] : 0.0;
-            }
-            __syncthreads();
+    // ---------------- backward: L^T Z = Y ----------------
+    for (int i = nbt - 1; i >= 0; --i) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int p = tid + 256 * u;
-                const int i = p & 63, r = p >> 6;
-                if (r < R) {
-                    double s = acc[u];
-                    for (int m = 0; m < nm; ++m) s = fma(Lt[m * LT + i], y[(m0 + m) * R + r], s);
-                    acc[u] = s;
-                }
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int d = i * NB + 16 * w + kg + 4 * r;
+                acc[c][r] = d < D ? Y[static_cast<size_t>(d) * Qp + q0 + 16 * c + row] : 0.0;
             }
+        for (int j = i + 1; j < nbt; ++j) {
+            stage_L(i * NB, j * NB, true);
+            stage_B(Z, j);
+            __syncthreads();
+            mma(-1.0);
             __syncthreads();
         }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int p = tid + 256 * u;
-            const int i = p & 63, r = p >> 6;
-            if (r < R && i < nbi) y[(i0 + i) * R + r] -= acc[u];
-        }
-        for (int e = tid; e < NB * NB; e += 256) {
-            const int r = e / NB, c = e - (e / NB) * NB;
-            Lt[r * LT + c] = (r < nbi && c <= r) ? L[static_cast<size_t>(i0 + r) * D + i0 + c] : 0.0;
-        }
+        acc_to_B();
+        stage_Linv(i, true);
         __syncthreads();
-        for (int r = wave; r < R; r += 4) {
-            double zm = (lane < nbi) ? y[(i0 + lane) * R + r] : 0.0;
-            for (int i = nbi - 1; i >= 0; --i) {
-                const double s = wave_sum((lane > i && lane < nbi) ? Lt[lane * LT + i] * zm : 0.0);
-                if (lane == i) zm = (zm - s) / Lt[i * LT + i];
+        zero();
+        mma(1.0);
+        store_ws(Z, i);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int q = q0 + 16 * c + row, d = i * NB + 16 * w + kg + 4 * r;
+                if (q < Q && d < D)
+                    store_out_d<TOut>(out + static_cast<int64_t>(q) * ld_out + static_cast<int64_t>(blk) * D + d,
+                                      acc[c][r]);
             }
-            if (lane < nbi) y[(i0 + lane) * R + r] = zm;
-        }
         __syncthreads();
     }
-    for (int r = 0; r < nq; ++r)
-        for (int d = tid; d < D; d += 256)
-            store_out_d<TOut>(out + static_cast<int64_t>(q0 + r) * ld_out + static_cast<int64_t>(blk) * D + d, y[d * R + r]);
 }
 
 template <typename TIn, typename TOut>
@@ -303,36 +364,26 @@ __global__ __launch_bounds__(256) void k_copy_rows(const TIn *src, int64_t ld_in
         store_out_d<TOut>(dst + static_cast<int64_t>(r) * ld_out + c, load_in_d<TIn>(src + static_cast<int64_t>(r) * ld_in + c));
 }
 
-inline int rhs_per_group(int D) {
-    int R = 12288 / D;
-    if (R > 16) R = 16;
-    if (R < 1) R = 1;
-    return R;
-}
-
 template <typename TIn, typename TOut>
-hipError_t launch_solve(const double *A, int D, int n_blocks, const void *g, int64_t ld_in, int Q,
+hipError_t launch_solve(const WsLayout &w, int D, int n_blocks, const void *g, int64_t ld_in, int Q,
                         void *out, int64_t ld_out, hipStream_t s) {
-    const int R = rhs_per_group(D);
-    const size_t smem = sizeof(double) * (static_cast<size_t>(NB) * LT + static_cast<size_t>(D) * R);
-    const auto kern = k_solve<TIn, TOut>;
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(smem));
-    if (e != hipSuccess) return e;
-    const dim3 grid(static_cast<unsigned>((Q + R - 1) / R), static_cast<unsigned>(n_blocks));
-    hipLaunchKernelGGL(kern, grid, dim3(256), smem, s, A, D, R, static_cast<const TIn *>(g), ld_in, Q,
-                       static_cast<TOut *>(out), ld_out);
+    hipLaunchKernelGGL(k_diag_inv, dim3(tiles_of(D), n_blocks), dim3(64), 0, s, w.A, D, w.Linv);
+    const dim3 grid(static_cast<unsigned>(padded_q(Q) / NB), static_cast<unsigned>(n_blocks));
+    hipLaunchKernelGGL((k_trsm_f64<TIn, TOut>), grid, dim3(256), 0, s, w.A, w.Linv, D, static_cast<const TIn *>(g),
+                       ld_in, Q, padded_q(Q), w.Y, w.Z, static_cast<TOut *>(out), ld_out);
     return hipGetLastError();
 }
 
 }  // namespace
 
-size_t precond_ws_bytes(int D, int n_blocks, int /*Q*/) {
-    return align256(sizeof(double) * static_cast<size_t>(n_blocks) * D * D) +
-           align256(sizeof(double) * n_blocks) + align256(sizeof(int) * n_blocks);
+size_t precond_ws_bytes(int D, int n_blocks, int Q) {
+    const size_t nb = static_cast<size_t>(n_blocks);
+    return align256(sizeof(double) * nb * D * D) + align256(sizeof(double) * nb) + align256(sizeof(int) * nb) +
+           align256(sizeof(double) * nb * tiles_of(D) * NB * NB) +
+           2 * align256(sizeof(double) * nb * D * padded_q(Q));
 }
 
-int *precond_info_ptr(void *ws, int D, int n_blocks) { return ws_layout(ws, D, n_blocks).info; }
+int *precond_info_ptr(void *ws, int D, int n_blocks) { return ws_layout(ws, D, n_blocks, 0).info; }
 
 hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int rows, int cols,
                             void *dst, bool bf16_out, int64_t ld_out, hipStream_t s) {
@@ -352,7 +403,7 @@ hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int ro
 hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
                                const void *g_test, bool bf16_in, int64_t ld_in, int Q, void *g_out,
                                bool bf16_out, int64_t ld_out, void *ws, hipStream_t s) {
-    const WsLayout w = ws_layout(ws, D, n_blocks);
+    const WsLayout w = ws_layout(ws, D, n_blocks, Q);
     hipLaunchKernelGGL(k_lambda, dim3(n_blocks), dim3(256), 0, s, S, D, N, damp_ratio, w.lam);
     hipLaunchKernelGGL(k_form, dim3(D, n_blocks), dim3(256), 0, s, S, D, N, w.lam, w.A, w.info);
     hipError_t e = hipGetLastError();
@@ -369,10 +420,10 @@ hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, d
         if (e != hipSuccess) return e;
     }
     if (Q == 0) return hipSuccess;
-    if (bf16_in && bf16_out) return launch_solve<bf16_bits, bf16_bits>(w.A, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
-    if (bf16_in) return launch_solve<bf16_bits, float>(w.A, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
-    if (bf16_out) return launch_solve<float, bf16_bits>(w.A, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
-    return launch_solve<float, float>(w.A, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+    if (bf16_in && bf16_out) return launch_solve<bf16_bits, bf16_bits>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+    if (bf16_in) return launch_solve<bf16_bits, float>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+    if (bf16_out) return launch_solve<float, bf16_bits>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+    return launch_solve<float, float>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
 }
 
 }  // namespace logra
