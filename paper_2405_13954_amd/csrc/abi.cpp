@@ -257,6 +257,8 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     const bool bf16 = te_dtype == LOGRA_BF16;
     if (bf16 && (D % 8 || ld_te % 8 || ld_tr % 8))
         return fail(LOGRA_ERR_INVALID_ARG, "bf16 scores need D, ld_te, ld_tr multiples of 8");
+    if (bf16 && (ld_te >= (int64_t{1} << 22) || ld_tr >= (int64_t{1} << 22)))
+        return fail(LOGRA_ERR_UNSUPPORTED, "bf16 scores support ld_te, ld_tr < 4194304");
     if (!bf16 && Q > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "fp32 scores support Q <= 65535");
     if (Q == 0) return ok();
     if (topk > 0) {

@@ -33,6 +33,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base, uin
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), static_cast<short>(0),
                                              static_cast<int>(bytes), 0x00020000);
 }
+// The same, for a base and size the compiler cannot prove wave-uniform
+// although they are: both are taken from lane 0, so that the descriptor lives
+// in scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc_uniform(const void *base, uint32_t bytes) {
+    const uint64_t p = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(p >> 32));
+    const uint64_t q = (static_cast<uint64_t>(hi) << 32) | lo;
+    return buf_rsrc(reinterpret_cast<const void *>(q), __builtin_amdgcn_readfirstlane(bytes));
+}
 __device__ __forceinline__ u32x4 buf_ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
     return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0);
 }

@@ -27,10 +27,28 @@
 namespace logra {
 namespace {
 
+#ifndef LOGRA_SC_SCHED
+#define LOGRA_SC_SCHED 1   // interleave loads with the MFMA stream (scheduling hints)
+#endif
+#ifndef LOGRA_SC_NT
+#define LOGRA_SC_NT 0      // non-temporal hint on the train-operand loads
+#endif
+
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int LDR = BK + 8;       // padded LDS row (bf16 elements): 144 bytes
 constexpr int GT = 256;           // GEMM threads
+constexpr int kLoads = BM * BK / 8 / GT;   // 128-bit loads per operand and thread per slab
 constexpr int kXcd = 8;
+
+// One slab (BK columns) of both operands in flight, 128 bits per load.
+struct Slab {
+    u32x4 a[kLoads];
+    u32x4 b[kLoads];
+};
+
+// scheduling-group masks of __builtin_amdgcn_sched_group_barrier
+constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100,
+              kSchedDsWrite = 0x200;
 
 __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restrict__ te, int64_t ld_te,
                                                        int Q, const bf16_bits *__restrict__ tr,
@@ -48,40 +66,44 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
     if (nt >= n_tiles) return;
     const int m0 = mt * BM;
     const int64_t n0 = static_cast<int64_t>(nt) * BN;
+    const int rows_a = Q - m0 < BM ? Q - m0 : BM;
+    const int rows_b = N - n0 < BN ? static_cast<int>(N - n0) : BN;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // staging map: chunk c = tid + 256*i  -> row c/8, 8 elements at column 8*(c%8)
-    const bf16_bits *ag[8];
-    const bf16_bits *bg[8];
-    bool aok[8], bok[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int c = tid + GT * i;
-        const int r = c >> 3;
-        aok[i] = m0 + r < Q;
-        bok[i] = n0 + r < N;
-        ag[i] = te + static_cast<int64_t>(aok[i] ? m0 + r : 0) * ld_te + 8 * (c & 7);
-        bg[i] = tr + (bok[i] ? n0 + r : 0) * ld_tr + 8 * (c & 7);
-    }
+    // Buffer resources over this tile's rows (the host bounds rows * ld * 2 below
+    // 2^31).  Load i of a thread covers row srow + 32 i, columns scol..scol+7 of
+    // the slab; rows past the operand and columns past D read as zeros.
+    const auto rsa = buf_rsrc_uniform(te + static_cast<int64_t>(m0) * ld_te,
+                                      static_cast<uint32_t>(rows_a * ld_te * 2));
+    const auto rsb = buf_rsrc_uniform(tr + n0 * ld_tr, static_cast<uint32_t>(rows_b * ld_tr * 2));
     const int srow = tid >> 3, scol = 8 * (tid & 7);
-
-    u32x4 ra[8], rb[8];
-    auto gload = [&](int k0) {
-        const u32x4 z = {0u, 0u, 0u, 0u};
-        const bool kin = k0 + scol < D;
+    uint32_t oa[kLoads], ob[kLoads];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            ra[i] = (aok[i] && kin) ? ld128(ag[i] + k0) : z;
-            rb[i] = (bok[i] && kin) ? ld128_nt(bg[i] + k0) : z;
+    for (int i = 0; i < kLoads; ++i) {
+        const int r = srow + 32 * i;
+        oa[i] = r < rows_a ? static_cast<uint32_t>((r * ld_te + scol) * 2) : kBufOOB;
+        ob[i] = r < rows_b ? static_cast<uint32_t>((r * ld_tr + scol) * 2) : kBufOOB;
+    }
+    auto gload = [&](Slab &st, int k0) {
+        const bool kin = k0 + scol < D;
+        const uint32_t dk = static_cast<uint32_t>(k0) * 2u;
+#pragma unroll
+        for (int i = 0; i < kLoads; ++i) {
+            st.a[i] = buf_ld128(rsa, kin ? oa[i] + dk : kBufOOB);
+#if LOGRA_SC_NT
+            st.b[i] = buf_ld128_nt(rsb, kin ? ob[i] + dk : kBufOOB);
+#else
+            st.b[i] = buf_ld128(rsb, kin ? ob[i] + dk : kBufOOB);
+#endif
         }
     };
-    auto lstore = [&](int buf) {
+    auto lstore = [&](const Slab &st, int buf) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            *reinterpret_cast<u32x4 *>(&As[buf][(srow + 32 * i) * LDR + scol]) = ra[i];
-            *reinterpret_cast<u32x4 *>(&Bs[buf][(srow + 32 * i) * LDR + scol]) = rb[i];
+        for (int i = 0; i < kLoads; ++i) {
+            *reinterpret_cast<u32x4 *>(&As[buf][(srow + 32 * i) * LDR + scol]) = st.a[i];
+            *reinterpret_cast<u32x4 *>(&Bs[buf][(srow + 32 * i) * LDR + scol]) = st.b[i];
         }
     };
 
@@ -93,31 +115,77 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    const int nk = (D + BK - 1) / BK;
-    gload(0);
-    lstore(0);
-    __syncthreads();
+    // Operand fragments: lane l reads row l % 32, contraction columns
+    // 8 (l / 32) .. +8 of each 16-wide step.
     const int frow = lane & 31, fk = 8 * (lane >> 5);
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload((kt + 1) * BK);
-        const bf16_bits *Ab = &As[buf][(wm * 128 + frow) * LDR + fk];
-        const bf16_bits *Bb = &Bs[buf][(wn * 128 + frow) * LDR + fk];
+    bf16x8 fa[2][4], fb[2][4];
+    auto ldfrag = [&](int f, int buf, int ks) {
+        const bf16_bits *Ab = &As[buf][(wm * 128 + frow) * LDR + fk + 16 * ks];
+        const bf16_bits *Bb = &Bs[buf][(wn * 128 + frow) * LDR + fk + 16 * ks];
 #pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8 a[4], b[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                a[i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Ab + i * 32 * LDR + ks * 16));
-                b[i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Bb + i * 32 * LDR + ks * 16));
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma32_bf16(a[i], b[j], acc[i][j]);
+        for (int i = 0; i < 4; ++i) {
+            fa[f][i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Ab + i * 32 * LDR));
+            fb[f][i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Bb + i * 32 * LDR));
         }
-        if (kt + 1 < nk) lstore(buf ^ 1);
+    };
+    auto mfma_step = [&](int f) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = mfma32_bf16(fa[f][i], fb[f][j], acc[i][j]);
+    };
+
+    // One slab per half-step.  On entry LDS buffer `buf` holds slab kt and
+    // `next` holds slab kt+1 in flight.  The half-step starts the loads of slab
+    // kt+2 into `fill`, multiplies slab kt out of LDS (four 16-wide steps,
+    // each step's fragments read while the previous step multiplies), stores
+    // slab kt+1 into the other buffer and ends with the barrier.
+    auto half = [&](int buf, Slab &fill, int kfill, const Slab &next) {
+        gload(fill, kfill);
+        ldfrag(0, buf, 0);
+        ldfrag(1, buf, 1);
+        mfma_step(0);
+        ldfrag(0, buf, 2);
+        mfma_step(1);
+        ldfrag(1, buf, 3);
+        mfma_step(0);
+        lstore(next, buf ^ 1);
+        mfma_step(1);
+#if LOGRA_SC_SCHED
+        // first fragments, then the 16 global loads over the first 32 MFMAs,
+        // 8 fragment reads over each of the first three steps and the 16 LDS
+        // stores over the last
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 8, 0);
+#pragma unroll
+        for (int ks = 0; ks < 3; ++ks) {
+#pragma unroll
+            for (int g = 0; g < 8; ++g) {
+                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+                if (ks < 2) __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 8, 0);
+        }
+#pragma unroll
+        for (int g = 0; g < 16; ++g) {
+            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
+        }
+#endif
         __syncthreads();
+    };
+
+    // The slab count is rounded up to even; slabs past D load as zeros.
+    const int nk = (D + BK - 1) / BK;
+    const int nk2 = nk + (nk & 1);
+    Slab s0, s1;
+    gload(s0, 0);
+    gload(s1, BK);
+    lstore(s0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < nk2; kt += 2) {
+        half(0, s0, (kt + 2) * BK, s1);
+        half(1, s1, (kt + 3) * BK, s0);
     }
 
     // result register r of block (i, j): row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
@@ -125,13 +193,13 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            if (row >= Q) continue;
-            float *srow_p = s + static_cast<int64_t>(row) * ld_s;
+            const int row = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row >= rows_a) continue;
+            float *srow_p = s + static_cast<int64_t>(m0 + row) * ld_s + n0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int64_t col = n0 + wn * 128 + j * 32 + (lane & 31);
-                if (col < N) srow_p[col] = acc[i][j][r];
+                const int col = wn * 128 + j * 32 + (lane & 31);
+                if (col < rows_b) srow_p[col] = acc[i][j][r];
             }
         }
 }

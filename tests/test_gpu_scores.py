@@ -41,7 +41,8 @@ def _norm_err(got, want, te, tr):
 
 
 @pytest.mark.parametrize("dtype,Q,N,D", [("bf16", 37, 1000, 576), ("bf16", 300, 700, 192),
-                                         ("bf16", 1, 5, 8), ("f32", 2, 4, 64), ("f32", 9, 130, 36)])
+                                         ("bf16", 257, 300, 1000), ("bf16", 1, 5, 8),
+                                         ("f32", 2, 4, 64), ("f32", 9, 130, 36)])
 def test_scores_parity(dtype, Q, N, D):
     from gpu_util import say
     say(f"[scores parity] dtype={dtype} Q={Q} N={N} D={D}")
@@ -53,6 +54,29 @@ def test_scores_parity(dtype, Q, N, D):
     err = _norm_err(got, want, te, tr)
     say(f"  normalised err {err:.3e}")
     assert err <= (1e-4 if dtype == "f32" else 1e-3)
+    assert err <= 1e-5
+
+
+def test_scores_strided_operands():
+    """Test and train rows taken as column windows of wider stores (row strides
+    larger than D, as when scoring one block of a concatenated gradient)."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    Q, N, D, ld = 70, 520, 136, 264
+    say(f"[scores strided] Q={Q} N={N} D={D} ld={ld}")
+    g = W.rng(43, Q, N, D)
+    te_full = W.normal(g, (Q, ld), 1.0, "bf16")
+    tr_full = W.normal(g, (N, ld), 1.0, "bf16")
+    te, tr = te_full[:, 64:64 + D], tr_full[:, 64:64 + D]
+    ted, trd = dev(te_full)[:, 64:64 + D], dev(tr_full)[:, 64:64 + D]
+    s = torch.full((Q, N + 3), np.nan, dtype=torch.float32, device="cuda")
+    P.logra_influence_scores(ted, trd, scores=s[:, :N], topk=0)
+    torch.cuda.synchronize()
+    got = host(s)
+    assert np.isnan(got[:, N:]).all()     # nothing written past the N columns
+    err = _norm_err(got[:, :N], oracle.scores(te, tr), te, tr)
+    say(f"  normalised err {err:.3e}")
     assert err <= 1e-5
 
 
