@@ -190,7 +190,17 @@ int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, do
  *               merged with this chunk's candidates.  Calling once per chunk
  *               with merge=1 after the first gives the top-k of all chunks.
  *   ws          workspace of logra_influence_ws_size(Q, N_chunk, topk,
- *               scores != NULL) bytes.
+ *               scores != NULL) bytes (0 when scores are given and topk = 0):
+ *               the scores when not given, and for long bf16 chunks the
+ *               per-query top-k candidate lists described below.
+ * Long bf16 chunks (N_chunk at least twice a prefix of max(4096, about
+ * 2 * topk * N_chunk / 8192) rows) select in two stages: the exact top-k of
+ * the prefix gives each query a threshold (its k-th value, a lower bound on
+ * the chunk's k-th value), the GEMM keeps the later scores at or above it as
+ * candidates (up to 8192 per query), and the candidates are merged; a query
+ * whose candidates overflow is selected from its full score row.  The result
+ * is the same exact top-k in every case.
+ * N_chunk < 2^31; for bf16, ld_te and ld_tr < 2^22.
  * Scores of NaN order unspecified.
  * ---------------------------------------------------------------------- */
 size_t logra_influence_ws_size(int Q, int64_t N_chunk, int topk, int scores_given);

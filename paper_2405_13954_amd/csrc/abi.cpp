@@ -236,8 +236,12 @@ int logra_precondition(const float *S, int D, int64_t N, double damp_ratio, cons
 }
 
 size_t logra_influence_ws_size(int Q, int64_t N_chunk, int topk, int scores_given) {
-    if (Q <= 0 || N_chunk <= 0 || scores_given || topk <= 0) return 0;
-    return round256(sizeof(float) * static_cast<size_t>(Q) * static_cast<size_t>(N_chunk));
+    if (Q <= 0 || N_chunk <= 0 || topk <= 0 || topk > LOGRA_MAX_TOPK) return 0;
+    const size_t q = static_cast<size_t>(Q);
+    size_t b = scores_given ? 0 : round256(sizeof(float) * q * static_cast<size_t>(N_chunk));
+    if (logra::topk_prefix_rows(N_chunk, topk) > 0)   // thresholds, counts, candidate lists
+        b += 2 * round256(4 * q) + 2 * round256(4 * q * logra::kCandCap);
+    return b;
 }
 
 int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
@@ -253,6 +257,7 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     if (scores == nullptr && topk == 0) return fail(LOGRA_ERR_INVALID_ARG, "nothing to compute: scores is NULL and topk is 0");
     if (scores != nullptr && ld_s < N_chunk) return fail(LOGRA_ERR_INVALID_ARG, "ld_s must be >= N_chunk");
     if (train_base < 0) return fail(LOGRA_ERR_INVALID_ARG, "train_base must be >= 0");
+    if (N_chunk > INT32_MAX) return fail(LOGRA_ERR_UNSUPPORTED, "N_chunk must be < 2^31");
     if (merge != 0 && merge != 1) return fail(LOGRA_ERR_INVALID_ARG, "merge must be 0 or 1");
     const bool bf16 = te_dtype == LOGRA_BF16;
     if (bf16 && (D % 8 || ld_te % 8 || ld_tr % 8))
@@ -275,22 +280,52 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     }
     TRY(check_dev(g_test_pre, "g_test_pre", bf16 ? 16 : 4));
     TRY(check_dev(g_train, "g_train", bf16 ? 16 : 4));
+    const size_t need = logra_influence_ws_size(Q, N_chunk, topk, scores != nullptr);
+    if (need) TRY(check_ws(ws, ws_bytes, need));
+    char *wp = static_cast<char *>(ws);
     float *s_buf = scores;
     int64_t ld = ld_s;
     if (scores != nullptr) {
         TRY(check_dev(scores, "scores", 4));
     } else {
-        TRY(check_ws(ws, ws_bytes, logra_influence_ws_size(Q, N_chunk, topk, 0)));
-        s_buf = static_cast<float *>(ws);
+        s_buf = reinterpret_cast<float *>(wp);
         ld = N_chunk;
+        wp += round256(sizeof(float) * static_cast<size_t>(Q) * static_cast<size_t>(N_chunk));
     }
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, N_chunk, D, bf16, s_buf, ld, s);
-    if (e != hipSuccess) return hip_fail(e, "score launch");
-    if (topk > 0) {
-        e = logra::launch_topk(s_buf, ld, Q, N_chunk, train_base, topk, topk_val, topk_idx, merge != 0, s);
-        if (e != hipSuccess) return hip_fail(e, "top-k launch");
+    const int64_t pre = (bf16 && topk > 0) ? logra::topk_prefix_rows(N_chunk, topk) : 0;
+    if (pre == 0) {
+        hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, N_chunk, D, bf16, s_buf,
+                                            ld, nullptr, s);
+        if (e != hipSuccess) return hip_fail(e, "score launch");
+        if (topk > 0) {
+            e = logra::launch_topk(s_buf, ld, Q, N_chunk, train_base, topk, topk_val, topk_idx, merge != 0, s);
+            if (e != hipSuccess) return hip_fail(e, "top-k launch");
+        }
+        return ok();
     }
+    // Large chunk: exact top-k of the first `pre` rows, whose k-th values then
+    // filter the scores of the rest in the GEMM epilogue; the candidates (or,
+    // for a row whose candidates overflow, its full score row) are merged.
+    const size_t q4 = round256(4 * static_cast<size_t>(Q));
+    float *thr = reinterpret_cast<float *>(wp);
+    int *cnt = reinterpret_cast<int *>(wp + q4);
+    float *cval = reinterpret_cast<float *>(wp + 2 * q4);
+    int *cidx = reinterpret_cast<int *>(wp + 2 * q4 + round256(4 * static_cast<size_t>(Q) * logra::kCandCap));
+    hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, pre, D, true, s_buf, ld, nullptr, s);
+    if (e != hipSuccess) return hip_fail(e, "score launch");
+    e = logra::launch_topk(s_buf, ld, Q, pre, train_base, topk, topk_val, topk_idx, merge != 0, s);
+    if (e != hipSuccess) return hip_fail(e, "top-k launch");
+    e = logra::launch_topk_threshold(topk_val, topk_idx, Q, topk, thr, cnt, s);
+    if (e != hipSuccess) return hip_fail(e, "top-k threshold launch");
+    const logra::ScoreFilter filt{thr, cnt, cval, cidx, logra::kCandCap};
+    const void *tr_rest = static_cast<const uint16_t *>(g_train) + pre * ld_tr;
+    e = logra::launch_scores(g_test_pre, ld_te, Q, tr_rest, ld_tr, N_chunk - pre, D, true, s_buf + pre, ld,
+                             &filt, s);
+    if (e != hipSuccess) return hip_fail(e, "score launch");
+    e = logra::launch_topk_filtered(s_buf + pre, ld, Q, N_chunk - pre, train_base + pre, topk, topk_val, topk_idx,
+                                    cnt, cval, cidx, logra::kCandCap, s);
+    if (e != hipSuccess) return hip_fail(e, "top-k merge launch");
     return ok();
 }
 

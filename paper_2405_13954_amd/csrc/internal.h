@@ -47,10 +47,30 @@ hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, d
 hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int rows, int cols,
                             void *dst, bool bf16_out, int64_t ld_out, hipStream_t s);
 
-// Score GEMM s = te * tr^T (fp32 result) and per-query top-k.
+// Score GEMM s = te * tr^T (fp32 result) and per-query top-k.  With a
+// filter (bf16 only), scores at or above thr[q] are also appended to row q's
+// candidate list: cnt[q] counts them (past `cap` too), val/idx hold the
+// first `cap` of them (idx = column within this launch).
+constexpr int kCandCap = 8192;   // candidates kept per query row
+struct ScoreFilter {
+    const float *thr;
+    int *cnt;
+    float *val;
+    int *idx;
+    int cap;
+};
 hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
-                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, hipStream_t st);
+                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, const ScoreFilter *filt,
+                         hipStream_t st);
+// Rows of a chunk scored and selected exactly before candidate filtering
+// starts (their running top-k sets the thresholds); 0 = no filtering.
+int64_t topk_prefix_rows(int64_t N, int k);
 hipError_t launch_topk(const float *s, int64_t ld_s, int Q, int64_t N, int64_t base, int k,
                        float *val, int64_t *idx, bool merge, hipStream_t st);
+hipError_t launch_topk_threshold(const float *val, const int64_t *idx, int Q, int k, float *thr,
+                                 int *cnt, hipStream_t st);
+hipError_t launch_topk_filtered(const float *s, int64_t ld_s, int Q, int64_t N, int64_t base, int k,
+                                float *val, int64_t *idx, const int *cnt, const float *cval,
+                                const int *cidx, int cap, hipStream_t st);
 
 }  // namespace logra

@@ -5,22 +5,30 @@
 //
 // Score GEMM (bf16): one workgroup per 256 x 256 output tile; 4 waves, each
 // owning a 128 x 128 quadrant as 4 x 4 blocks of 32x32x16 bf16 MFMAs (256
-// fp32 accumulators per lane).  The contraction advances 64 at a time: the
-// next slab of both operands is fetched with coalesced 128-bit loads into
-// registers while the current slab is multiplied out of LDS, then stored
-// into the other LDS buffer (one barrier per step).  LDS rows are padded to
-// 144 bytes, which makes the lanes' 128-bit operand reads conflict-free.
-// Tiles are ordered so that the workgroups sharing one 256-row train slab
-// are dispatched together onto the same XCD (dispatch round-robins
-// workgroups over the 8 XCDs), so the slab is fetched from HBM once into
-// that XCD's L2.
+// fp32 accumulators per lane).  The contraction advances 64 columns (one
+// slab) per step.  Slabs are fetched two steps ahead with range-checked
+// 128-bit buffer loads into two register sets (rows past the operands and
+// columns past D read as zeros), stored into one of two LDS buffers one step
+// ahead, and multiplied out of LDS with each 16-wide step's fragments read
+// while the previous step multiplies; one barrier per slab.  Scheduling
+// groups spread the global loads, fragment reads and LDS stores over the
+// MFMA stream.  LDS rows are padded to 144 bytes, which makes the lanes'
+// 128-bit operand reads conflict-free.  Tiles are ordered so that the
+// workgroups sharing one 256-row train slab are dispatched together onto the
+// same XCD (dispatch round-robins workgroups over the 8 XCDs), so the slab
+// is fetched from HBM once into that XCD's L2.
 //
 // Top-k: one workgroup per query row.  An exact radix select (four 8-bit
-// passes over order-preserving keys) finds the k-th largest score; one more
-// pass collects the larger scores and the lowest-indexed ties in index order
-// (block-wide prefix counts), and a bitonic sort orders them by (value desc,
-// index asc).  With merge, the chunk's sorted list is merged with the
-// caller's running list.
+// passes over order-preserving keys) finds the k-th largest score; when more
+// scores tie at it than are needed, a second radix select over the
+// (complemented) indices keeps the lowest-indexed ones.  The selected
+// entries are sorted by (value desc, index asc) with a bitonic sort and, with
+// merge, merged with the caller's running list.  For long chunks the GEMM
+// epilogue filters: only scores at or above a per-query threshold (the k-th
+// value of a running list that already covers a prefix of the chunk, hence
+// a lower bound on the final k-th value) are appended to candidate lists, and
+// the selection runs over those; a list that overflows falls back to the
+// query's full score row.
 #include "common.h"
 #include "internal.h"
 
@@ -54,7 +62,7 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
                                                        int Q, const bf16_bits *__restrict__ tr,
                                                        int64_t ld_tr, int64_t N, int D,
                                                        float *__restrict__ s, int64_t ld_s,
-                                                       int m_tiles, int n_tiles) {
+                                                       int m_tiles, int n_tiles, ScoreFilter filt) {
     __shared__ __attribute__((aligned(16))) bf16_bits As[2][BM * LDR];
     __shared__ __attribute__((aligned(16))) bf16_bits Bs[2][BN * LDR];
 
@@ -188,6 +196,15 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
         half(1, s1, (kt + 3) * BK, s0);
     }
 
+    // Epilogue.  With a filter, scores at or above the row's threshold are
+    // also appended to the row's top-k candidate list (order arbitrary; the
+    // count keeps growing past the capacity so that an overflow is visible).
+    const bool filter = filt.thr != nullptr;
+    float *ths = reinterpret_cast<float *>(&As[0][0]);   // LDS is free after the last barrier
+    if (filter) {
+        ths[tid] = tid < rows_a ? filt.thr[m0 + tid] : __builtin_inff();
+        __syncthreads();
+    }
     // result register r of block (i, j): row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -195,11 +212,23 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
         for (int r = 0; r < 16; ++r) {
             const int row = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
             if (row >= rows_a) continue;
-            float *srow_p = s + static_cast<int64_t>(m0 + row) * ld_s + n0;
+            const int64_t q = m0 + row;
+            float *srow_p = s + q * ld_s + n0;
+            const float t = filter ? ths[row] : 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int col = wn * 128 + j * 32 + (lane & 31);
-                if (col < rows_b) srow_p[col] = acc[i][j][r];
+                const float v = acc[i][j][r];
+                if (col < rows_b) {
+                    srow_p[col] = v;
+                    if (filter && v >= t) {
+                        const int pos = atomicAdd(filt.cnt + q, 1);
+                        if (pos < filt.cap) {
+                            filt.val[q * filt.cap + pos] = v;
+                            filt.idx[q * filt.cap + pos] = static_cast<int>(n0) + col;
+                        }
+                    }
+                }
             }
         }
 }
@@ -240,128 +269,148 @@ __device__ __forceinline__ bool before(uint32_t ka, int64_t ia, uint32_t kb, int
     return ia < ib;
 }
 
-// Exclusive block-wide prefix sum of v (0/1 flags); returns the prefix and
-// writes the block total into *total.
-__device__ __forceinline__ int block_scan(int v, int *warp_sums, int *total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(x, o, 64);
-        if (lane >= o) x += y;
+// Sources of a selection: a row of scores (local index = column), or a
+// row's candidate list (local index = the candidate's column).  Global index
+// = base + local index.
+struct RowSrc {
+    const float *row;
+    int64_t n;
+    int64_t base;
+    __device__ int64_t size() const { return n; }
+    __device__ float value(int64_t j) const { return row[j]; }
+    __device__ uint32_t local(int64_t j) const { return static_cast<uint32_t>(j); }
+    __device__ int64_t global(int64_t j) const { return base + j; }
+};
+struct CandSrc {
+    const float *v;
+    const int *c;
+    int64_t n;
+    int64_t base;
+    __device__ int64_t size() const { return n; }
+    __device__ float value(int64_t j) const { return v[j]; }
+    __device__ uint32_t local(int64_t j) const { return static_cast<uint32_t>(c[j]); }
+    __device__ int64_t global(int64_t j) const { return base + c[j]; }
+};
+
+struct TopkShared {
+    uint32_t hist[256];
+    uint32_t ck[kMaxTopk];
+    int64_t ci[kMaxTopk];
+    uint32_t mk[kMaxTopk];
+    int64_t mi[kMaxTopk];
+    uint32_t prefix;
+    int rem;
+    uint32_t neq;
+    int count;
+};
+
+// Radix select (four 8-bit digits, most significant first) of the `want`-th
+// largest key(j) over the j < n with in(j).  Returns that key; *rem = how many
+// elements equal to it belong to the `want` largest, *neq = how many exist.
+template <class KeyFn, class InFn>
+__device__ uint32_t radix_select(int64_t n, KeyFn key, InFn in, int want, TopkShared &sh, int *rem,
+                                 uint32_t *neq) {
+    const int tid = threadIdx.x;
+    uint32_t prefix = 0, pmask = 0;
+    int r = want;
+    uint32_t eq = 0;
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        sh.hist[tid] = 0;
+        __syncthreads();
+        for (int64_t j = tid; j < n; j += KT_THREADS) {
+            if (!in(j)) continue;
+            const uint32_t kk = key(j);
+            if ((kk & pmask) == prefix) atomicAdd(&sh.hist[(kk >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int cum = 0, d = 255;
+            for (; d > 0; --d) {
+                if (cum + static_cast<int>(sh.hist[d]) >= r) break;
+                cum += static_cast<int>(sh.hist[d]);
+            }
+            sh.prefix = prefix | (static_cast<uint32_t>(d) << shift);
+            sh.rem = r - cum;
+            sh.neq = sh.hist[d];
+        }
+        __syncthreads();
+        prefix = sh.prefix;
+        r = sh.rem;
+        eq = sh.neq;
+        pmask |= 255u << shift;
+        __syncthreads();
     }
-    if (lane == 63) warp_sums[wave] = x;
-    __syncthreads();
-    int base = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < KT_THREADS / 64; ++w) {
-        const int ws = warp_sums[w];
-        if (w < wave) base += ws;
-        tot += ws;
-    }
-    __syncthreads();
-    *total = tot;
-    return base + x - v;
+    *rem = r;
+    *neq = eq;
+    return prefix;
 }
 
-__global__ __launch_bounds__(KT_THREADS) void k_topk(const float *__restrict__ S, int64_t ld_s,
-                                                     int64_t N, int64_t base, int k,
-                                                     float *__restrict__ val,
-                                                     int64_t *__restrict__ idx, int merge) {
-    __shared__ uint32_t hist[256];
-    __shared__ uint32_t ck[kMaxTopk];
-    __shared__ int64_t ci[kMaxTopk];
-    __shared__ int warp_sums[KT_THREADS / 64];
-    __shared__ uint32_t sh_prefix;
-    __shared__ int sh_krem;
-
-    const int q = blockIdx.x, tid = threadIdx.x;
-    const float *row = S + static_cast<int64_t>(q) * ld_s;
-    const int ksel = static_cast<int>(N < k ? N : k);   // candidates this chunk provides
-
-    // 1. radix select of the ksel-th largest key
-    uint32_t prefix = 0, pmask = 0;
-    int krem = ksel;
+// Top-k of one source, merged with the running list (vo, io) when `merge`.
+// The k-th largest key is found by radix select; when more elements tie at
+// it than are needed, a second radix select over the complemented local
+// index keeps the lowest-indexed ones.  Exactly min(n, k) elements are then
+// collected (in any order), padded to a power of two and sorted by (value
+// descending, index ascending).
+template <class Src>
+__device__ void topk_row(const Src &src, int k, float *vo, int64_t *io, bool merge, TopkShared &sh) {
+    const int tid = threadIdx.x;
+    const int64_t n = src.size();
+    const int ksel = static_cast<int>(n < k ? n : k);
+    uint32_t kth = 0, idx_limit = 0xffffffffu;
     if (ksel > 0) {
-        for (int pass = 0; pass < 4; ++pass) {
-            const int shift = 24 - 8 * pass;
-            hist[tid] = 0;
-            __syncthreads();
-            for (int64_t j = tid; j < N; j += KT_THREADS) {
-                const uint32_t key = fkey(row[j]);
-                if ((key & pmask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-            }
-            __syncthreads();
-            if (tid == 0) {
-                int cum = 0, d = 255;
-                for (; d > 0; --d) {
-                    if (cum + static_cast<int>(hist[d]) >= krem) break;
-                    cum += static_cast<int>(hist[d]);
-                }
-                sh_prefix = prefix | (static_cast<uint32_t>(d) << shift);
-                sh_krem = krem - cum;
-            }
-            __syncthreads();
-            prefix = sh_prefix;
-            krem = sh_krem;
-            pmask |= 255u << shift;
-            __syncthreads();
+        int rem;
+        uint32_t neq;
+        kth = radix_select(
+            n, [&](int64_t j) { return fkey(src.value(j)); }, [](int64_t) { return true; }, ksel, sh,
+            &rem, &neq);
+        if (neq > static_cast<uint32_t>(rem)) {
+            int rem2;
+            uint32_t neq2;
+            const uint32_t c = radix_select(
+                n, [&](int64_t j) { return ~src.local(j); },
+                [&](int64_t j) { return fkey(src.value(j)) == kth; }, rem, sh, &rem2, &neq2);
+            idx_limit = ~c;
         }
     }
-    // prefix is now the exact key of the ksel-th largest; krem ties of it are taken.
-    const int ngt = ksel - krem;
-
-    // 2. collect in index order: keys > prefix go to [0, ngt), the first krem
-    //    keys == prefix go to [ngt, ksel).
-    int seen_gt = 0, seen_eq = 0;
+    if (tid == 0) sh.count = 0;
+    __syncthreads();
     if (ksel > 0) {
-        for (int64_t j0 = 0; j0 < N; j0 += KT_THREADS) {
-            const int64_t j = j0 + tid;
-            uint32_t key = 0;
-            if (j < N) key = fkey(row[j]);
-            const int gt = (j < N && key > prefix) ? 1 : 0;
-            const int eq = (j < N && key == prefix) ? 1 : 0;
-            int tgt, teq;
-            const int pg = block_scan(gt, warp_sums, &tgt);
-            const int pe = block_scan(eq, warp_sums, &teq);
-            if (gt) {
-                ck[seen_gt + pg] = key;
-                ci[seen_gt + pg] = base + j;
+        for (int64_t j = tid; j < n; j += KT_THREADS) {
+            const uint32_t kk = fkey(src.value(j));
+            if (kk > kth || (kk == kth && src.local(j) <= idx_limit)) {
+                const int pos = atomicAdd(&sh.count, 1);
+                sh.ck[pos] = kk;
+                sh.ci[pos] = src.global(j);
             }
-            if (eq && seen_eq + pe < krem) {
-                ck[ngt + seen_eq + pe] = key;
-                ci[ngt + seen_eq + pe] = base + j;
-            }
-            seen_gt += tgt;
-            seen_eq += teq;
-            if (seen_gt >= ngt && seen_eq >= krem) break;   // uniform across the block
         }
     }
     // pad to a power of two >= k with (0, -1) entries (rank last)
     int P = 1;
     while (P < k) P <<= 1;
+    __syncthreads();
     for (int i = ksel + tid; i < P; i += KT_THREADS) {
-        ck[i] = 0u;
-        ci[i] = -1;
+        sh.ck[i] = 0u;
+        sh.ci[i] = -1;
     }
     __syncthreads();
 
-    // 3. bitonic sort by (key desc, index asc)
+    // bitonic sort by (key desc, index asc)
     for (int size = 2; size <= P; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
             for (int i = tid; i < P; i += KT_THREADS) {
                 const int jx = i ^ stride;
                 if (jx > i) {
                     const bool up = (i & size) == 0;   // this run sorts "before"-first
-                    const bool sw = up ? before(ck[jx], ci[jx], ck[i], ci[i])
-                                       : before(ck[i], ci[i], ck[jx], ci[jx]);
+                    const bool sw = up ? before(sh.ck[jx], sh.ci[jx], sh.ck[i], sh.ci[i])
+                                       : before(sh.ck[i], sh.ci[i], sh.ck[jx], sh.ci[jx]);
                     if (sw) {
-                        const uint32_t tk = ck[i];
-                        ck[i] = ck[jx];
-                        ck[jx] = tk;
-                        const int64_t ti = ci[i];
-                        ci[i] = ci[jx];
-                        ci[jx] = ti;
+                        const uint32_t tk = sh.ck[i];
+                        sh.ck[i] = sh.ck[jx];
+                        sh.ck[jx] = tk;
+                        const int64_t ti = sh.ci[i];
+                        sh.ci[i] = sh.ci[jx];
+                        sh.ci[jx] = ti;
                     }
                 }
             }
@@ -369,61 +418,106 @@ __global__ __launch_bounds__(KT_THREADS) void k_topk(const float *__restrict__ S
         }
     }
 
-    // 4. write, merging with the caller's running list if asked
-    float *vo = val + static_cast<int64_t>(q) * k;
-    int64_t *io = idx + static_cast<int64_t>(q) * k;
     if (!merge) {
         for (int r = tid; r < k; r += KT_THREADS) {
-            const bool ok = ci[r] >= 0;
-            vo[r] = ok ? unkey(ck[r]) : -__builtin_huge_valf();
-            io[r] = ok ? ci[r] : -1;
+            const bool ok = sh.ci[r] >= 0;
+            vo[r] = ok ? unkey(sh.ck[r]) : -__builtin_huge_valf();
+            io[r] = ok ? sh.ci[r] : -1;
         }
         return;
     }
     // merged[r] from the two sorted lists (old: vo/io, new: ck/ci), staged in
     // LDS so that the old list is read completely before it is overwritten.
-    __shared__ uint32_t mk[kMaxTopk];
-    __shared__ int64_t mi[kMaxTopk];
     if (tid == 0) {
         int a = 0, b = 0;
         for (int r = 0; r < k; ++r) {
             const int64_t ia = a < k ? io[a] : -1;
             const uint32_t ka = ia >= 0 ? fkey(vo[a]) : 0u;
-            const int64_t ib = b < k ? ci[b] : -1;
-            const uint32_t kb = ib >= 0 ? ck[b] : 0u;
+            const int64_t ib = b < k ? sh.ci[b] : -1;
+            const uint32_t kb = ib >= 0 ? sh.ck[b] : 0u;
             if (before(ka, ia, kb, ib)) {
-                mk[r] = ka;
-                mi[r] = ia;
+                sh.mk[r] = ka;
+                sh.mi[r] = ia;
                 ++a;
             } else {
-                mk[r] = kb;
-                mi[r] = ib;
+                sh.mk[r] = kb;
+                sh.mi[r] = ib;
                 ++b;
             }
         }
     }
     __syncthreads();
     for (int r = tid; r < k; r += KT_THREADS) {
-        const bool ok = mi[r] >= 0;
-        vo[r] = ok ? unkey(mk[r]) : -__builtin_huge_valf();
-        io[r] = ok ? mi[r] : -1;
+        const bool ok = sh.mi[r] >= 0;
+        vo[r] = ok ? unkey(sh.mk[r]) : -__builtin_huge_valf();
+        io[r] = ok ? sh.mi[r] : -1;
+    }
+}
+
+// One workgroup per query row over a full row of scores.
+__global__ __launch_bounds__(KT_THREADS) void k_topk(const float *__restrict__ S, int64_t ld_s,
+                                                     int64_t N, int64_t base, int k,
+                                                     float *__restrict__ val,
+                                                     int64_t *__restrict__ idx, int merge) {
+    __shared__ TopkShared sh;
+    const int q = blockIdx.x;
+    const RowSrc src{S + static_cast<int64_t>(q) * ld_s, N, base};
+    topk_row(src, k, val + static_cast<int64_t>(q) * k, idx + static_cast<int64_t>(q) * k, merge != 0,
+             sh);
+}
+
+// Threshold of each row for candidate filtering: the k-th value of the
+// running list (-inf while it holds fewer than k entries); clears the row's
+// candidate count.
+__global__ __launch_bounds__(256) void k_topk_threshold(const float *__restrict__ val,
+                                                        const int64_t *__restrict__ idx, int Q, int k,
+                                                        float *__restrict__ thr, int *__restrict__ cnt) {
+    const int q = blockIdx.x * 256 + threadIdx.x;
+    if (q >= Q) return;
+    const int64_t last = static_cast<int64_t>(q) * k + k - 1;
+    thr[q] = idx[last] >= 0 ? val[last] : -__builtin_huge_valf();
+    cnt[q] = 0;
+}
+
+// Merge of each row's candidates into its running list; a row whose
+// candidates overflowed the capacity is selected from its full score row.
+__global__ __launch_bounds__(KT_THREADS) void k_topk_filtered(
+    const float *__restrict__ S, int64_t ld_s, int64_t N, int64_t base, int k, float *__restrict__ val,
+    int64_t *__restrict__ idx, const int *__restrict__ cnt, const float *__restrict__ cval,
+    const int *__restrict__ cidx, int cap) {
+    __shared__ TopkShared sh;
+    const int q = blockIdx.x;
+    float *vo = val + static_cast<int64_t>(q) * k;
+    int64_t *io = idx + static_cast<int64_t>(q) * k;
+    const int c = cnt[q];
+    if (c <= cap) {
+        const CandSrc src{cval + static_cast<int64_t>(q) * cap, cidx + static_cast<int64_t>(q) * cap, c,
+                          base};
+        topk_row(src, k, vo, io, true, sh);
+    } else {
+        const RowSrc src{S + static_cast<int64_t>(q) * ld_s, N, base};
+        topk_row(src, k, vo, io, true, sh);
     }
 }
 
 }  // namespace
 
 hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
-                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, hipStream_t st) {
+                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, const ScoreFilter *filt,
+                         hipStream_t st) {
     if (Q == 0 || N == 0) return hipSuccess;
     if (bf16) {
         const int m_tiles = (Q + BM - 1) / BM;
         const int n_tiles = static_cast<int>((N + BN - 1) / BN);
         const int n_groups = (n_tiles + kXcd - 1) / kXcd;
         const unsigned grid = static_cast<unsigned>(kXcd) * n_groups * m_tiles;
+        const ScoreFilter none{nullptr, nullptr, nullptr, nullptr, 0};
         hipLaunchKernelGGL(k_scores_bf16, dim3(grid), dim3(GT), 0, st,
                            static_cast<const bf16_bits *>(te), ld_te, Q,
-                           static_cast<const bf16_bits *>(tr), ld_tr, N, D, s, ld_s, m_tiles, n_tiles);
+                           static_cast<const bf16_bits *>(tr), ld_tr, N, D, s, ld_s, m_tiles, n_tiles,
+                           filt ? *filt : none);
     } else {
+        if (filt) return hipErrorInvalidValue;   // candidate filtering is a bf16-path feature
         const dim3 grid(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(Q));
         hipLaunchKernelGGL(k_scores_f32, grid, dim3(256), 0, st, static_cast<const float *>(te), ld_te,
                            Q, static_cast<const float *>(tr), ld_tr, N, D, s, ld_s);
@@ -431,11 +525,37 @@ hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, i
     return hipGetLastError();
 }
 
+int64_t topk_prefix_rows(int64_t N, int k) {
+    // Expected candidates past a prefix of P rows: about k (N - P) / P; aim
+    // for at most half the capacity.
+    int64_t P = (2 * static_cast<int64_t>(k) * N + kCandCap - 1) / kCandCap;
+    if (P < 4096) P = 4096;
+    P = (P + 255) / 256 * 256;
+    return 2 * P <= N ? P : 0;
+}
+
 hipError_t launch_topk(const float *s, int64_t ld_s, int Q, int64_t N, int64_t base, int k,
                        float *val, int64_t *idx, bool merge, hipStream_t st) {
     if (Q == 0) return hipSuccess;
     hipLaunchKernelGGL(k_topk, dim3(Q), dim3(KT_THREADS), 0, st, s, ld_s, N, base, k, val, idx,
                        merge ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_threshold(const float *val, const int64_t *idx, int Q, int k, float *thr,
+                                 int *cnt, hipStream_t st) {
+    if (Q == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_topk_threshold, dim3((Q + 255) / 256), dim3(256), 0, st, val, idx, Q, k, thr,
+                       cnt);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_filtered(const float *s, int64_t ld_s, int Q, int64_t N, int64_t base, int k,
+                                float *val, int64_t *idx, const int *cnt, const float *cval,
+                                const int *cidx, int cap, hipStream_t st) {
+    if (Q == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_topk_filtered, dim3(Q), dim3(KT_THREADS), 0, st, s, ld_s, N, base, k, val, idx,
+                       cnt, cval, cidx, cap);
     return hipGetLastError();
 }
 

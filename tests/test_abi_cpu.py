@@ -52,6 +52,13 @@ def test_workspace_sizes(L):
     assert P.logra_precondition_ws_size(256, 224, 1024) >= 224 * 256 * 256 * 8
     assert P.logra_influence_ws_size(4, 10, 3, 0) == 256
     assert P.logra_influence_ws_size(4, 10, 3, 1) == 0
+    # large chunks add per-query thresholds, counts and candidate lists
+    # (8192 candidates of 4-byte value and 4-byte column)
+    Q, N = 1024, 500_000
+    cand = 2 * 4096 + 2 * 4 * Q * 8192
+    assert P.logra_influence_ws_size(Q, N, 100, 0) == 4 * Q * N + cand
+    assert P.logra_influence_ws_size(Q, N, 100, 1) == cand
+    assert P.logra_influence_ws_size(Q, N, 0, 1) == 0
 
 
 NULL = None

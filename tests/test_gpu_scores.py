@@ -100,6 +100,49 @@ def test_topk_integer_exact_with_ties_and_chunks():
     assert np.array_equal(tv2, tv)
 
 
+def test_topk_candidate_filter_exact():
+    """Chunks long enough for the filtered path (exact top-k of a prefix of the
+    chunk, then only scores at or above its k-th value kept as candidates):
+    integer scores with many exact ties must give the oracle's top-k bit for
+    bit, alone and merged over chunks."""
+    from gpu_util import f64, say
+    say("[top-k] candidate filtering, integer scores with ties")
+    g = W.rng(45)
+    Q, N, D, k = 9, 24_000, 64, 37
+    te = W.integer_array(g, (Q, D), -2, 2, "bf16", 0.5)
+    tr = W.integer_array(g, (N, D), -2, 2, "bf16", 0.5)
+    want = oracle.scores(te, tr)
+    wv, wi = oracle.topk(want, k)
+    s, tv, ti = _scores_gpu(te, tr, topk=k)
+    assert np.array_equal(f64(s), want)
+    assert np.array_equal(ti, wi)
+    assert np.array_equal(tv.astype(np.float64), wv)
+    _, tv2, ti2 = _scores_gpu(te, tr, topk=k, chunks=[(0, 9_000), (9_000, 24_000)], materialize=False)
+    assert np.array_equal(ti2, wi)
+    assert np.array_equal(tv2, tv)
+
+
+def test_topk_candidate_overflow_falls_back():
+    """Scores that grow along the chunk: the prefix holds the smallest values,
+    so nearly every later score passes its threshold and the candidate lists
+    overflow; those rows must be selected from their full score rows.  Rows
+    with decreasing scores keep few candidates (mostly ties at the
+    threshold).  Both must equal the oracle exactly."""
+    from gpu_util import f64, say
+    say("[top-k] candidate overflow fallback")
+    Q, N, D, k = 4, 30_000, 16, 100
+    te = np.zeros((Q, D), np.float32)
+    te[:, 0] = [1.0, -1.0, 2.0, 0.0]   # increasing, decreasing, increasing, all zero
+    tr = np.zeros((N, D), np.float32)
+    tr[:, 0] = np.arange(N) // 128      # 0..234, exact in bf16
+    te, tr = W.f32_to_bf16_bits(te), W.f32_to_bf16_bits(tr)
+    want = oracle.scores(te, tr)
+    wv, wi = oracle.topk(want, k)
+    _, tv, ti = _scores_gpu(te, tr, topk=k, materialize=False)
+    assert np.array_equal(ti, wi)
+    assert np.array_equal(tv.astype(np.float64), wv)
+
+
 def test_topk_padding_when_few_candidates():
     from gpu_util import say
     say("[top-k] fewer candidates than k")
