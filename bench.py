@@ -195,11 +195,13 @@ def logging_leg(args, torch, P):
     }
     sample = None
     if args.cpu_baseline:
-        sample = {"x": [host_bf16(bufs[0][j][0][:, :args.cpu_tokens]) for j in range(nl_block)],
-                  "dy": [host_bf16(bufs[0][j][1][:, :args.cpu_tokens]) for j in range(nl_block)],
+        n_b = min(args.cpu_batches, n_buf)
+        sample = {"batches": [{"x": [host_bf16(bufs[i][j][0]) for j in range(nl_block)],
+                               "dy": [host_bf16(bufs[i][j][1]) for j in range(nl_block)],
+                               "mask": W.mask_from_lengths(lens[i], T)} for i in range(n_b)],
                   "p_in": [host_bf16(projs[j][0]) for j in range(nl_block)],
                   "p_out": [host_bf16(projs[j][1]) for j in range(nl_block)],
-                  "mask": W.mask_from_lengths(lens[0], T)[:, :args.cpu_tokens], "blocks": w.blocks}
+                  "blocks": w.blocks, "seconds": args.cpu_seconds}
     del bufs, store, S, ws
     torch.cuda.empty_cache()
     return res, sample
@@ -211,19 +213,30 @@ def host_bf16(t):
 
 
 def cpu_logging_baseline(sample):
+    """The oracle on the logging step's work: per-example projection of the 7
+    layers of a block (Eq. (5)) and the covariance update of their blocks,
+    over the sampled batches, repeated until about `seconds` have passed."""
     import oracle
-    t0 = time.perf_counter()
-    for j in range(len(sample["x"])):
-        oracle.project_factored(sample["x"][j], sample["dy"][j], sample["p_in"][j], sample["p_out"][j],
-                                sample["mask"])
+    batches, target = sample["batches"], sample["seconds"]
+    toks, passes, t0 = 0, 0, time.perf_counter()
+    while True:
+        for b in batches:
+            for j in range(len(b["x"])):
+                g = oracle.project_factored(b["x"][j], b["dy"][j], sample["p_in"][j], sample["p_out"][j],
+                                            b["mask"])
+                oracle.cov_accumulate(g)
+            toks += int(b["mask"].sum())
+        passes += 1
+        if time.perf_counter() - t0 >= target:
+            break
     dt = time.perf_counter() - t0
-    toks = int(sample["mask"].sum())
-    B, Ts = sample["mask"].shape
-    # the sample is one block of the 32 identical-shape blocks: model tokens/s
+    B, T = batches[0]["mask"].shape
+    # each sampled batch goes through one block; the step runs 32 blocks
     return {"value": toks / (dt * sample["blocks"]), "unit": "tokens/s",
             "cores": min(oracle.num_threads(), B), "kind": "oracle",
-            "sample": f"{B} examples x first {Ts} token slots ({toks} valid) through the 7 layers of one "
-                      f"block, scaled to 32 blocks; {dt:.2f} s"}
+            "sample": f"{len(batches)} batches of {B} examples x {T} token slots through the 7 layers "
+                      f"(projection and covariance update) of one block, {passes} passes, {toks} valid "
+                      f"tokens in {dt:.1f} s, scaled to 32 blocks"}
 
 
 # ---------------------------------------------------------------- influence --
@@ -300,7 +313,8 @@ def influence_leg(args, torch, P):
     if args.cpu_baseline:
         ns = args.cpu_train_rows
         sample = {"S": S[:, :, :].to("cpu").numpy().astype(np.float64), "N": Nc, "damp": ex["damp"],
-                  "test": host_bf16(test[:16]), "train": host_bf16(train[:ns]), "D": D, "topk": topk}
+                  "test": host_bf16(test[:args.cpu_queries]), "train": host_bf16(train[:ns]), "D": D,
+                  "topk": topk}
     del train, test, covg, sws
     torch.cuda.empty_cache()
     return res, sample
@@ -319,7 +333,7 @@ def cpu_influence_baseline(sample):
     q, n = s.shape
     return {"value": q * n / dt, "unit": "scores/s", "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{q} queries x {n} stored gradients (224 blocks preconditioned, scores, top-100); "
-                      f"{dt:.2f} s"}
+                      f"{dt:.1f} s"}
 
 
 # --------------------------------------------------------------------- main --
@@ -333,8 +347,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--leg", choices=["all", "log", "influence"], default="all")
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
-    ap.add_argument("--cpu-tokens", type=int, default=1024)
-    ap.add_argument("--cpu-train-rows", type=int, default=20000)
+    ap.add_argument("--cpu-batches", type=int, default=2, help="logging batches in the oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time bound of the logging sample")
+    ap.add_argument("--cpu-queries", type=int, default=256, help="test gradients in the oracle sample")
+    ap.add_argument("--cpu-train-rows", type=int, default=20000, help="stored gradients in the oracle sample")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md on sharding)",
