@@ -7,11 +7,13 @@
 // and the padding (layers differ up to 4x in bytes per token; half of the
 // tiles of a ragged batch are empty):
 //
-//  0. k_tile_list (masked inputs only): the ordered list of 64-token tiles
-//     holding at least one valid token.
+//  0. k_project_prep: clears the work counter and, for masked inputs, builds
+//     the ordered list of 64-token tiles holding at least one valid token.
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
 //     = one contraction chunk (<= 4096 columns) of one side (x or dy) of one
-//     listed tile.  The four waves deal the chunk's 32-wide steps
+//     listed tile.  Workgroups take items from an atomic counter as they
+//     finish (items differ up to 4x in columns and workgroups in speed, so a
+//     static assignment leaves a long tail).  The four waves deal the chunk's 32-wide steps
 //     round-robin; each lane feeds a 128-bit buffer load straight into its
 //     MFMA operand (row = token for x/dy, row = projection dimension for P;
 //     16x16x32 bf16 or 16x16x4 fp32, fp32 accumulation).  Masked tokens, rows
@@ -21,7 +23,7 @@
 //     order and written, in the MFMA result layout, to the workspace.
 //  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
 //     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
-//     formed in fp32 from LDS (4x4 outputs per thread).  Empty tiles give 0.
+//     formed in fp32 from LDS (KT x KT outputs per thread).  Empty tiles give 0.
 //  C. k_project_reduce: per example, the tile sums are added in tile order
 //     and G_b is written (fp32 or bf16, round to nearest even) to the
 //     caller's store row.
@@ -44,9 +46,13 @@ namespace {
 #ifndef LOGRA_PROJ_NT
 #define LOGRA_PROJ_NT 0
 #endif
+#ifndef LOGRA_PROJ_MINWAVES
+#define LOGRA_PROJ_MINWAVES 1   // waves per SIMD the chunk kernel's registers must allow
+#endif
 constexpr int MB = LOGRA_PROJ_ROWBLOCKS;  // 16-token row blocks per tile
 constexpr int TT = 16 * MB;               // tokens per tile
 constexpr int NW = 4;                     // waves per workgroup
+constexpr int kMaxSlots = 1024;           // chunk slots a group can order by width
 constexpr int NT = NW * kWave;            // threads per workgroup
 
 // Contraction columns per work item, and register pipeline depth, by
@@ -69,9 +75,12 @@ struct ProjArgs {
     ChunkLayer layer[kMaxGroup];
     int n_layers;
     int slots;      // chunk slots of all layers
+    int ordered;    // slot_order holds the processing order of the slots
+    uint16_t slot_order[kMaxSlots];
     const uint8_t *mask;
     const int *tiles;     // non-empty tiles (b * tpe + tile) in index order; NULL = all
     const int *n_tiles;   // their count (device), read when tiles != NULL
+    int *work;            // items handed out beyond the first gridDim.x (device counter)
     float *part;    // chunk partials, MFMA result layout, TT x 16KT floats each
     float *gpart;   // per-tile sums  [layer][b][tile][k_out * k_in]
     int B, T, tpe;  // tpe = tiles per example
@@ -198,8 +207,9 @@ __device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, in
 template <int KT, typename TIn>
 __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int count, f32x4 *slot, int lane,
                                            int wave) {
-    const int gslot = item / count;             // chunk slot over all layers
-    const int j = item - gslot * count;         // listed tile
+    const int rank = item / count;              // position of the chunk slot in processing order
+    const int j = item - rank * count;          // listed tile
+    const int gslot = a.ordered ? a.slot_order[rank] : rank;   // chunk slot over all layers
     int l = 0;
     while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
     const ChunkLayer &L = a.layer[l];
@@ -254,27 +264,44 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     }
 }
 
-// Persistent: the grid is sized to the resident capacity of the GPU and each
-// workgroup strides over the items (chunk slot x non-empty tile), which all
-// carry the same work.  The loop bound is uniform and finite.
+// Persistent: the grid is sized to the resident capacity of the GPU.  Each
+// workgroup starts on item blockIdx.x and, when done, takes the next
+// unclaimed item from the work counter.  Claiming only when free keeps the
+// tail to at most one item per workgroup.  The loop ends once the counter
+// passes the item count, which every workgroup reaches.
 template <int KT, typename TIn>
-__global__ __launch_bounds__(NT) void k_project_chunks(ProjArgs a) {
+__global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(ProjArgs a) {
     __shared__ f32x4 slot[MB * KT * kWave];   // cross-wave fold
+    __shared__ int next;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int count = a.tiles ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : a.B * a.tpe;
     const int items = count * a.slots;
-    for (int item = blockIdx.x; item < items; item += gridDim.x) chunk_item<KT, TIn>(a, item, count, slot, lane, wave);
+    int item = blockIdx.x;
+    while (item < items) {
+        chunk_item<KT, TIn>(a, item, count, slot, lane, wave);
+        if (tid == 0) next = static_cast<int>(gridDim.x) + atomicAdd(a.work, 1);
+        __syncthreads();
+        item = next;
+        __syncthreads();   // every thread has read `next` before it is rewritten
+    }
 }
 
-// Ordered list of the tiles with at least one valid token (one workgroup;
-// block-wide prefix counts keep the list in tile order).
-__global__ __launch_bounds__(1024) void k_tile_list(const uint8_t *mask, int B, int T, int tpe, int *tiles,
-                                                     int *n_tiles) {
+// Clears the work counter and, with a mask, lists the tiles that hold at
+// least one valid token, in tile order (one workgroup; block-wide prefix
+// counts keep the order).  A full tile's 64 mask bytes are read as four
+// 128-bit loads when the mask rows are 16-byte aligned.
+__global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int B, int T, int tpe, int *tiles,
+                                                        int *n_tiles, int *work) {
     __shared__ int wsum[16];
     __shared__ int base;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    if (tid == 0) base = 0;
+    if (tid == 0) {
+        *work = 0;
+        base = 0;
+    }
+    if (mask == nullptr) return;
+    const bool vec = (reinterpret_cast<uintptr_t>(mask) & 15) == 0 && (T & 15) == 0;
     __syncthreads();
     const int total = B * tpe;
     for (int t0 = 0; t0 < total; t0 += 1024) {
@@ -284,7 +311,14 @@ __global__ __launch_bounds__(1024) void k_tile_list(const uint8_t *mask, int B, 
             const int b = bt / tpe, tile = bt - b * tpe;
             const uint8_t *m = mask + static_cast<size_t>(b) * T + static_cast<size_t>(tile) * TT;
             const int n = min(TT, T - tile * TT);
-            for (int i = 0; i < n && !any; ++i) any = m[i] != 0;
+            if (vec && n == TT) {
+                u32x4 v = ld128(m);
+#pragma unroll
+                for (int q = 1; q < TT / 16; ++q) v |= ld128(m + 16 * q);
+                any = (v[0] | v[1] | v[2] | v[3]) != 0;
+            } else {
+                for (int i = 0; i < n && !any; ++i) any = m[i] != 0;
+            }
         }
         int x = any;
 #pragma unroll
@@ -345,32 +379,34 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a) {
     }
     __syncthreads();
 
-    // Sum over the tile's tokens of dy'_t x'_t^T; 4x4 outputs per thread.
-    constexpr int NB = 4 * KT;
-    for (int blk = tid; blk < NB * NB; blk += 256) {
-        const int ob = blk / NB, ib = blk - (blk / NB) * NB;
-        float c[4][4];
+    // Sum over the tile's tokens of dy'_t x'_t^T: thread (ob, ib) of a 16 x 16
+    // grid owns outputs o = KT ob + u, i = KT ib + v for u, v < KT.
+    const int ob = tid >> 4, ib = tid & 15;
+    float c[KT][KT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < KT; ++u)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) c[u][v] = 0.f;
-        for (int t = 0; t < TT; ++t) {
-            const f32x4 dv = *reinterpret_cast<const f32x4 *>(&ds[t * KP + 4 * ob]);
-            const f32x4 xv = *reinterpret_cast<const f32x4 *>(&xs[t * KP + 4 * ib]);
+        for (int v = 0; v < KT; ++v) c[u][v] = 0.f;
+    for (int t = 0; t < TT; ++t) {
+        float dv[KT], xv[KT];
 #pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) c[u][v] = __builtin_fmaf(dv[u], xv[v], c[u][v]);
+        for (int u = 0; u < KT; ++u) {
+            dv[u] = ds[t * KP + KT * ob + u];
+            xv[u] = xs[t * KP + KT * ib + u];
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int o = 4 * ob + u;
-            if (o >= a.k_out) break;
+        for (int u = 0; u < KT; ++u)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int i = 4 * ib + v;
-                if (i < a.k_in) gdst[o * a.k_in + i] = c[u][v];
-            }
+            for (int v = 0; v < KT; ++v) c[u][v] = __builtin_fmaf(dv[u], xv[v], c[u][v]);
+    }
+#pragma unroll
+    for (int u = 0; u < KT; ++u) {
+        const int o = KT * ob + u;
+        if (o >= a.k_out) break;
+#pragma unroll
+        for (int v = 0; v < KT; ++v) {
+            const int i = KT * ib + v;
+            if (i < a.k_in) gdst[o * a.k_in + i] = c[u][v];
         }
     }
 }
@@ -384,7 +420,15 @@ __global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const flo
     TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
     for (int i = threadIdx.x; i < D; i += blockDim.x) {
         float s = 0.f;
-        for (int t = 0; t < tpe; ++t) s += p[static_cast<size_t>(t) * D + i];
+        int t = 0;
+        for (; t + 8 <= tpe; t += 8) {   // eight loads in flight, summed in tile order
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * D + i];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * D + i];
         store_out<TOut>(out + i, s);
     }
 }
@@ -459,7 +503,7 @@ size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, 
     const Plan p = plan_group(n_in, n_out, n_layers, B, T, k_in, k_out, nullptr);
     const size_t tiles = static_cast<size_t>(B) * ((T + TT - 1) / TT);
     return align256(p.part_floats * sizeof(float)) + align256(p.gpart_floats * sizeof(float)) +
-           align256((tiles + 1) * sizeof(int));
+           align256((tiles + 2) * sizeof(int));
 }
 
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
@@ -479,6 +523,29 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     const int KT = kt_for(k_in, k_out);
     a.n_layers = grp.n_layers;
     a.slots = p.slots;
+    // Slots widest first (stable), so that the last items handed out are the
+    // narrow ones and the tail after the last claim is short.
+    a.ordered = p.slots <= kMaxSlots;
+    if (a.ordered) {
+        int width[kMaxSlots];
+        for (int l = 0; l < grp.n_layers; ++l) {
+            const ChunkLayer &L = a.layer[l];
+            for (int c = 0; c < L.c_in + L.c_out; ++c) {
+                const int n = c < L.c_in ? L.n_in : L.n_out;
+                const int col0 = (c < L.c_in ? c : c - L.c_in) * chunk_cols(KT);
+                width[L.slot_begin + c] = min(chunk_cols(KT), n - col0);
+            }
+        }
+        int n = 0;
+        for (int w = chunk_cols(KT); w > 0; ) {   // descending distinct widths
+            int next = 0;
+            for (int sl = 0; sl < p.slots; ++sl) {
+                if (width[sl] == w) a.slot_order[n++] = static_cast<uint16_t>(sl);
+                else if (width[sl] < w && width[sl] > next) next = width[sl];
+            }
+            w = next;
+        }
+    }
     a.mask = mask;
     char *w = static_cast<char *>(ws);
     a.part = reinterpret_cast<float *>(w);
@@ -491,15 +558,12 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     a.k_in = k_in;
     a.k_out = k_out;
     a.ck = chunk_cols(KT);
-    a.tiles = nullptr;
-    a.n_tiles = nullptr;
-    if (mask) {
-        int *list = reinterpret_cast<int *>(w);
-        int *count = list + static_cast<size_t>(B) * a.tpe;
-        hipLaunchKernelGGL(k_tile_list, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count);
-        a.tiles = list;
-        a.n_tiles = count;
-    }
+    int *list = reinterpret_cast<int *>(w);
+    int *count = list + static_cast<size_t>(B) * a.tpe;
+    a.work = count + 1;
+    a.tiles = mask ? list : nullptr;
+    a.n_tiles = mask ? count : nullptr;
+    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count, a.work);
     const int max_items = p.slots * B * a.tpe;
     switch (KT) {
         case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, s) : launch_chunks<1, float>(a, max_items, s); break;

@@ -144,3 +144,35 @@ def test_project_grouped_equals_single():
     P.logra_project_layers(layers, mask=mask)
     torch.cuda.synchronize()
     assert np.array_equal(host(store_g), host(store_s))
+
+
+def test_project_grouped_multichunk_vs_oracle():
+    """A group whose layers span several 4096-column chunks per side, with
+    partial last chunks of different widths (the launch processes the chunk
+    slots widest first), against the oracle layer by layer."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[project] grouped multi-chunk layers vs oracle")
+    shapes = [(6144, 1024), (1024, 9000), (4096, 4096)]
+    B, T, k = 2, 70, 16
+    lens = np.array([70, 41])
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = dev(mask_np)
+    D = k * k
+    store = torch.zeros((B, len(shapes) * D), dtype=torch.float32, device="cuda")
+    layers, data = [], []
+    for i, (ni, no) in enumerate(shapes):
+        d = W.layer_inputs(11, i, B, T, ni, no, k, k, 1.0, 1e-2, "bf16")
+        data.append(d)
+        t = {key: dev(d[key]) for key in ("x", "dy", "p_in", "p_out")}
+        layers.append(dict(t, g_out=store[:, i * D:(i + 1) * D]))
+    P.logra_project_layers(layers, mask=mask)
+    torch.cuda.synchronize()
+    got = host(store).astype(np.float64)
+    for i, d in enumerate(data):
+        want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], mask_np)
+        g = got[:, i * D:(i + 1) * D]
+        err = np.linalg.norm(g - want) / np.linalg.norm(want)
+        say(f"  layer {i} {shapes[i]}: normwise err {err:.2e}")
+        assert err <= 1e-3
