@@ -309,6 +309,28 @@ def influence_leg(args, torch, P):
                      "frac": achieved / BF16_PEAK_TFLOPS, "traffic": traffic, "traffic_over_algorithmic": ratio,
                      "kernel": "score GEMM (bf16 MFMA, fp32 accumulation)", "flops_per_launch": flops},
     }
+    if args.vendor_gemm:
+        # the same operands through torch's library GEMM (hipBLASLt) and through this
+        # library's scores-only path, on a 125,000-row slice (context for the roofline)
+        nv = min(N, 125_000)
+        sv = torch.empty((Q, nv), dtype=torch.float32, device=dev)
+        sb = torch.empty((Q, nv), dtype=torch.bfloat16, device=dev)   # torch keeps the input dtype
+        tv_, to_ = EventTimer(torch), EventTimer(torch)
+        for timed in (False, True, True, True):
+            e0 = tv_.start() if timed else None
+            torch.matmul(pre, train[:nv].T, out=sb)
+            if timed:
+                tv_.stop(e0)
+            e0 = to_.start() if timed else None
+            P.logra_influence_scores(pre, train[:nv], scores=sv, topk=0)
+            if timed:
+                to_.stop(e0)
+        torch.cuda.synchronize()
+        fl = 2.0 * Q * nv * D_tot
+        res["vendor_gemm"] = {"rows": nv, "torch_output": "bf16", "torch_matmul_ms": tv_.mean_ms(),
+                              "torch_matmul_tflops": fl / tv_.mean_ms() / 1e9,
+                              "logra_ms": to_.mean_ms(), "logra_tflops": fl / to_.mean_ms() / 1e9}
+        del sv, sb
     sample = None
     if args.cpu_baseline:
         ns = args.cpu_train_rows
@@ -347,6 +369,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--leg", choices=["all", "log", "influence"], default="all")
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--vendor-gemm", action="store_true",
+                    help="also time torch.matmul (hipBLASLt) on the score GEMM's operands")
     ap.add_argument("--cpu-batches", type=int, default=2, help="logging batches in the oracle sample")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time bound of the logging sample")
     ap.add_argument("--cpu-queries", type=int, default=256, help="test gradients in the oracle sample")

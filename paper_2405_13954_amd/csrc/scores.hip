@@ -5,18 +5,17 @@
 //
 // Score GEMM (bf16): one workgroup per 256 x 256 output tile; 4 waves, each
 // owning a 128 x 128 quadrant as 4 x 4 blocks of 32x32x16 bf16 MFMAs (256
-// fp32 accumulators per lane).  The contraction advances 64 columns (one
-// slab) per step.  Slabs are fetched two steps ahead with range-checked
-// 128-bit buffer loads into two register sets (rows past the operands and
-// columns past D read as zeros), stored into one of two LDS buffers one step
-// ahead, and multiplied out of LDS with each 16-wide step's fragments read
-// while the previous step multiplies; one barrier per slab.  Scheduling
-// groups spread the global loads, fragment reads and LDS stores over the
-// MFMA stream.  LDS rows are padded to 144 bytes, which makes the lanes'
-// 128-bit operand reads conflict-free.  Tiles are ordered so that the
-// workgroups sharing one 256-row train slab are dispatched together onto the
-// same XCD (dispatch round-robins workgroups over the 8 XCDs), so the slab
-// is fetched from HBM once into that XCD's L2.
+// fp32 accumulators per lane), 64 contraction columns (one slab) per step.
+// Tiles are ordered so that the workgroups sharing one 256-row train slab are
+// dispatched together onto the same XCD (dispatch round-robins workgroups
+// over the 8 XCDs), so the slab is fetched from HBM once into that XCD's L2.
+// Two main loops:
+//  - k_scores_dma (default): operands copied straight from memory into an
+//    LDS ring with gfx950's buffer_load ... lds, no register staging; the
+//    issue order of MFMAs, copies and fragment reads is fixed by hand.
+//  - k_scores_bf16: slabs staged through registers two steps ahead and
+//    stored into two LDS buffers.
+// Both compute the same sums in the same order.
 //
 // Top-k: one workgroup per query row.  An exact radix select (four 8-bit
 // passes over order-preserving keys) finds the k-th largest score; when more
@@ -41,6 +40,9 @@ namespace {
 #ifndef LOGRA_SC_NT
 #define LOGRA_SC_NT 0      // non-temporal hint on the train-operand loads
 #endif
+#ifndef LOGRA_SC_DMA
+#define LOGRA_SC_DMA 1     // 1: operands copied straight into LDS (k_scores_dma)
+#endif
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int LDR = BK + 8;       // padded LDS row (bf16 elements): 144 bytes
@@ -57,6 +59,47 @@ struct Slab {
 // scheduling-group masks of __builtin_amdgcn_sched_group_barrier
 constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100,
               kSchedDsWrite = 0x200;
+
+// Epilogue of a 256 x 256 tile: the fp32 scores go to s (rows past Q and
+// columns past N are skipped).  With a filter, scores at or above the row's
+// threshold are also appended to the row's top-k candidate list (order
+// arbitrary; the count keeps growing past the capacity so that an overflow is
+// visible).  `ths` is 1 KB of free LDS for the tile's thresholds.
+__device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *ths, float *__restrict__ s,
+                                             int64_t ld_s, int m0, int64_t n0, int rows_a, int rows_b,
+                                             int wm, int wn, int tid, int lane, const ScoreFilter &filt) {
+    const bool filter = filt.thr != nullptr;
+    if (filter) {
+        ths[tid] = tid < rows_a ? filt.thr[m0 + tid] : __builtin_inff();
+        __syncthreads();
+    }
+    // result register r of block (i, j): row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row >= rows_a) continue;
+            const int64_t q = m0 + row;
+            float *srow_p = s + q * ld_s + n0;
+            const float t = filter ? ths[row] : 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int col = wn * 128 + j * 32 + (lane & 31);
+                const float v = acc[i][j][r];
+                if (col < rows_b) {
+                    srow_p[col] = v;
+                    if (filter && v >= t) {
+                        const int pos = atomicAdd(filt.cnt + q, 1);
+                        if (pos < filt.cap) {
+                            filt.val[q * filt.cap + pos] = v;
+                            filt.idx[q * filt.cap + pos] = static_cast<int>(n0) + col;
+                        }
+                    }
+                }
+            }
+        }
+}
 
 __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restrict__ te, int64_t ld_te,
                                                        int Q, const bf16_bits *__restrict__ tr,
@@ -196,41 +239,184 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
         half(1, s1, (kt + 3) * BK, s0);
     }
 
-    // Epilogue.  With a filter, scores at or above the row's threshold are
-    // also appended to the row's top-k candidate list (order arbitrary; the
-    // count keeps growing past the capacity so that an overflow is visible).
-    const bool filter = filt.thr != nullptr;
-    float *ths = reinterpret_cast<float *>(&As[0][0]);   // LDS is free after the last barrier
-    if (filter) {
-        ths[tid] = tid < rows_a ? filt.thr[m0 + tid] : __builtin_inff();
-        __syncthreads();
+    store_scores(acc, reinterpret_cast<float *>(&As[0][0]), s, ld_s, m0, n0, rows_a, rows_b, wm, wn,
+                 tid, lane, filt);   // LDS is free after the last barrier
+}
+
+// ------------------------------------------------------------------------
+// Score GEMM with asynchronous global->LDS copies (gfx950 buffer_load ... lds).
+// Same tile, waves, MFMA shape and 64-column slabs as above, but the operands
+// travel from memory straight into LDS (no register staging, no LDS store
+// instructions).  The LDS ring holds three slabs of the train operand, which
+// streams from HBM and is copied two slabs ahead, and two slabs of the test
+// operand, which the L2 mostly serves and is copied one slab ahead
+// (3 x 32 KB + 2 x 32 KB = 160 KB).  One barrier per slab: each wave waits
+// for its own copies of the slab, the barrier makes every wave's copies
+// visible and frees the stages of the previous slab, and the next copies are
+// issued before the slab is multiplied.
+//
+// LDS layout of an operand slab: 256 rows of 128 bytes (8 chunks of 16 B);
+// chunk c of row r is stored at position c ^ ((r >> 1) & 7), which makes the
+// 16 lanes of each quarter-wave fragment read (16 consecutive rows, one chunk)
+// hit 16 different 16-byte bank groups.  A copy instruction writes a
+// contiguous 1 KB (8 whole rows, so every request is a full 128-byte line):
+// lane l stores row (l >> 3), position (l & 7).
+constexpr int kSlabOp = BM * BK * 2;         // bytes of one operand slab (32 KB)
+constexpr int kStagesA = 2, kStagesB = 3;
+constexpr int kLdsB = kStagesA * kSlabOp;    // B stages follow the A stages
+constexpr int kLdsBytes = (kStagesA + kStagesB) * kSlabOp;
+constexpr int kCopies = kSlabOp / 1024 / 4;  // 1 KB copies per wave and operand per slab (8)
+
+// 16 bytes per lane from buffer offset `voff` to LDS address m0 + 16 * lane;
+// offsets at or past the buffer's range store zeros.  The load reads M0 one
+// wait state after the scalar write (s_nop 0), as the hardware requires.  It
+// is tracked by vmcnt, which the callers wait on explicitly: the compiler
+// does not see this load.
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r) : "memory");
+}
+
+__global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restrict__ te, int64_t ld_te,
+                                                      int Q, const bf16_bits *__restrict__ tr,
+                                                      int64_t ld_tr, int64_t N, int D,
+                                                      float *__restrict__ s, int64_t ld_s,
+                                                      int m_tiles, int n_tiles, ScoreFilter filt) {
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[kLdsBytes];
+
+    const int bid = blockIdx.x;
+    const int xcd = bid % kXcd, local = bid / kXcd;
+    const int mt = local % m_tiles;
+    const int nt = (local / m_tiles) * kXcd + xcd;
+    if (nt >= n_tiles) return;
+    const int m0 = mt * BM;
+    const int64_t n0 = static_cast<int64_t>(nt) * BN;
+    const int rows_a = Q - m0 < BM ? Q - m0 : BM;
+    const int rows_b = N - n0 < BN ? static_cast<int>(N - n0) : BN;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    // LDS byte address of the ring (the address-space cast yields the 32-bit LDS offset)
+    const uint32_t lds0 = static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t *)smem));
+
+    const auto rsa = buf_rsrc_uniform(te + static_cast<int64_t>(m0) * ld_te,
+                                      static_cast<uint32_t>(rows_a * ld_te * 2));
+    const auto rsb = buf_rsrc_uniform(tr + n0 * ld_tr, static_cast<uint32_t>(rows_b * ld_tr * 2));
+    // copy i of this wave covers rows (8 wave + i) * 8 .. +8 of an operand slab;
+    // lane l loads chunk (l & 7) ^ (((8 wave + i) * 4 + (l >> 4)) & 7) of its row
+    uint32_t oa[kCopies], ob[kCopies];
+    int ccol[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) ccol[h] = 8 * ((lane & 7) ^ ((4 * h + (lane >> 4)) & 7));
+#pragma unroll
+    for (int i = 0; i < kCopies; ++i) {
+        const int r = (wave * kCopies + i) * 8 + (lane >> 3);
+        oa[i] = r < rows_a ? static_cast<uint32_t>((r * ld_te + ccol[i & 1]) * 2) : kBufOOB;
+        ob[i] = r < rows_b ? static_cast<uint32_t>((r * ld_tr + ccol[i & 1]) * 2) : kBufOOB;
     }
-    // result register r of block (i, j): row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
+    auto issue = [&](const __amdgpu_buffer_rsrc_t &rs, const uint32_t(&o)[kCopies], int slab, uint32_t lds) {
+        const int k0 = slab * BK;
+        const uint32_t dk = static_cast<uint32_t>(k0) * 2u;
+        const bool kin0 = k0 + ccol[0] < D, kin1 = k0 + ccol[1] < D;
+        const uint32_t la = lds + wave * kCopies * 1024;
+#pragma unroll
+        for (int i = 0; i < kCopies; ++i)
+            copy_to_lds(rs, ((i & 1) ? kin1 : kin0) ? o[i] + dk : kBufOOB, la + i * 1024);
+    };
+
+    // fragment byte offsets inside an operand slab: lane l reads row (l % 32) of
+    // each 32-row block, logical chunk 2 ks + (l / 32) at position chunk ^ sw
+    const int sw = (lane >> 1) & 7;
+    const uint32_t fa0 = (wm * 128 + (lane & 31)) * 128, fb0 = (wn * 128 + (lane & 31)) * 128;
+    uint32_t fo[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) fo[ks] = static_cast<uint32_t>(((2 * ks + (lane >> 5)) ^ sw) * 16);
+
+    f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            if (row >= rows_a) continue;
-            const int64_t q = m0 + row;
-            float *srow_p = s + q * ld_s + n0;
-            const float t = filter ? ths[row] : 0.f;
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int col = wn * 128 + j * 32 + (lane & 31);
-                const float v = acc[i][j][r];
-                if (col < rows_b) {
-                    srow_p[col] = v;
-                    if (filter && v >= t) {
-                        const int pos = atomicAdd(filt.cnt + q, 1);
-                        if (pos < filt.cap) {
-                            filt.val[q * filt.cap + pos] = v;
-                            filt.idx[q * filt.cap + pos] = static_cast<int>(n0) + col;
-                        }
-                    }
-                }
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    bf16x8 fa[2][4], fb[2][4];
+    // fragment read g (0..7) of a 16-wide step: A block g/2 for even g, B block g/2 for odd g
+    auto ldfrag1 = [&](int f, const uint8_t *abase, const uint8_t *bbase, int ks, int g) {
+        const int i = g >> 1;
+        if (g & 1)
+            fb[f][i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(bbase + fb0 + fo[ks] + i * 4096));
+        else
+            fa[f][i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(abase + fa0 + fo[ks] + i * 4096));
+    };
+    auto mfma1 = [&](int f, int idx) {
+        const int i = idx >> 2, j = idx & 3;
+        acc[i][j] = mfma32_bf16(fa[f][i], fb[f][j], acc[i][j]);
+    };
+
+    // Slab kt lives in A stage kt % 2 and B stage kt % 3.  Before slab kt
+    // is read, the copies in flight are (A kt, B kt+1), issued during slab
+    // kt-1, and B kt from before; waiting until at most kCopies remain leaves
+    // only B kt+1 (issued last).  The wait and the barrier sit in the middle
+    // of the previous slab's last 16-wide step: its first 8 MFMAs cover the
+    // barrier, its last 8 cover the reads of the new slab's first fragments.
+    // (lgkmcnt(0) first: this wave's reads of the stages that the next copies
+    // overwrite are complete before any wave passes the barrier.)  The step
+    // is issued in a fixed order (scheduling barriers): groups of two MFMAs
+    // with one copy of the next slabs and one fragment read of the next
+    // 16-wide step.
+    const int nk = (D + BK - 1) / BK;
+    issue(rsa, oa, 0, lds0);
+    issue(rsb, ob, 0, lds0 + kLdsB);
+    issue(rsb, ob, 1, lds0 + kLdsB + kSlabOp);
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" :: "n"(kCopies) : "memory");
+#pragma unroll
+    for (int g = 0; g < 8; ++g) ldfrag1(0, smem, smem + kLdsB, 0, g);
+    int sa = 0, sb = 0;   // stages of slab kt
+    for (int kt = 0; kt < nk; ++kt) {
+        const int na = sa ^ 1, nb2 = sb == 0 ? 2 : sb - 1;   // stages of A kt+1 and B kt+2
+        const int nb1 = sb == 2 ? 0 : sb + 1;                // stage of B kt+1
+        const uint8_t *abase = smem + sa * kSlabOp, *bbase = smem + kLdsB + sb * kSlabOp;
+        const uint32_t dka = static_cast<uint32_t>((kt + 1) * BK) * 2u, dkb = dka + BK * 2u;
+        const bool ka0 = (kt + 1) * BK + ccol[0] < D, ka1 = (kt + 1) * BK + ccol[1] < D;
+        const bool kb0 = (kt + 2) * BK + ccol[0] < D, kb1 = (kt + 2) * BK + ccol[1] < D;
+        const uint32_t la = lds0 + na * kSlabOp + wave * kCopies * 1024;
+        const uint32_t lb = lds0 + kLdsB + nb2 * kSlabOp + wave * kCopies * 1024;
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int ks = 0; ks < 3; ++ks) {
+            const int f = ks & 1;
+#pragma unroll
+            for (int g = 0; g < 8; ++g) {
+                mfma1(f, 2 * g);
+                mfma1(f, 2 * g + 1);
+                if (ks == 0)
+                    copy_to_lds(rsa, ((g & 1) ? ka1 : ka0) ? oa[g] + dka : kBufOOB, la + g * 1024);
+                else if (ks == 1)
+                    copy_to_lds(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
+                ldfrag1(f ^ 1, abase, bbase, ks + 1, g);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+#pragma unroll
+        for (int m = 0; m < 8; ++m) mfma1(1, m);
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(kCopies) : "memory");
+        const uint8_t *nabase = smem + na * kSlabOp, *nbbase = smem + kLdsB + nb1 * kSlabOp;
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+            ldfrag1(0, nabase, nbbase, 0, g);
+            mfma1(1, 8 + g);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        sa = na;
+        sb = nb1;
+    }
+    // the copies of the slabs past the end are still in flight
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    store_scores(acc, reinterpret_cast<float *>(smem), s, ld_s, m0, n0, rows_a, rows_b, wm, wn, tid,
+                 lane, filt);
 }
 
 // fp32 scores (small problems): one thread per score, sequential contraction.
@@ -512,7 +698,7 @@ hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, i
         const int n_groups = (n_tiles + kXcd - 1) / kXcd;
         const unsigned grid = static_cast<unsigned>(kXcd) * n_groups * m_tiles;
         const ScoreFilter none{nullptr, nullptr, nullptr, nullptr, 0};
-        hipLaunchKernelGGL(k_scores_bf16, dim3(grid), dim3(GT), 0, st,
+        hipLaunchKernelGGL(LOGRA_SC_DMA ? k_scores_dma : k_scores_bf16, dim3(grid), dim3(GT), 0, st,
                            static_cast<const bf16_bits *>(te), ld_te, Q,
                            static_cast<const bf16_bits *>(tr), ld_tr, N, D, s, ld_s, m_tiles, n_tiles,
                            filt ? *filt : none);
