@@ -1,0 +1,166 @@
+"""Parity at the full sizes and launch configurations that bench.py times,
+on outputs the float64 oracle can compute one by one:
+
+- the grouped projection of one Llama3-8B block (7 layers, B=8, T=2048,
+  lengths U{128..2048}, k=16, bf16 store rows of 57,344) on three sampled
+  layers, all examples;
+- the 224-block covariance update from one batch of store rows, on sampled
+  blocks;
+- the damped preconditioner of 224 blocks of 256 (covariances from 4,096
+  gradients, damping 0.1 x mean eigenvalue) for 1,024 test gradients, on
+  sampled blocks;
+- the score pass of 1,024 x 500,000 at 57,344 dims with top-100 (the
+  filtered selection path): sampled scores, and the top-100 of sampled
+  queries checked against their full score rows.
+
+Inputs are drawn on the device with the same generators bench.py uses; the
+oracle gets host copies of the raw inputs, never a result of the HIP path.
+Tolerances are the ones of the small-size tests: 2e-2 normwise for bf16
+outputs, 1e-3 for fp32 outputs of bf16 inputs, 1e-3 on normalised scores.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer_inputs(torch, gen, B, T, n_in, n_out, k, w):
+    x = torch.empty((B, T, n_in), dtype=torch.bfloat16, device="cuda")
+    dy = torch.empty((B, T, n_out), dtype=torch.bfloat16, device="cuda")
+    W.device_normal_(x, w.x_std, gen)
+    W.device_normal_(dy, w.dy_std, gen)
+    pi = torch.empty((k, n_in), dtype=torch.bfloat16, device="cuda")
+    po = torch.empty((k, n_out), dtype=torch.bfloat16, device="cuda")
+    W.device_normal_(pi, 1.0 / np.sqrt(k), gen)
+    W.device_normal_(po, 1.0 / np.sqrt(k), gen)
+    return x, dy, pi, po
+
+
+def test_project_llama_block_bench_launch():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, normwise, say
+    w = W.WORKLOADS["llama3_8b_stream"]
+    B, T, k = w.B, w.T, w.k_in
+    D = k * k
+    lens = W.lengths(W.rng(0, 200, 0), B, w.len_lo, w.len_hi)
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = torch.from_numpy(mask_np).cuda()
+    say(f"[full project] 7 Llama3-8B layers, B={B} T={T} k={k}, {int(lens.sum())} valid tokens")
+    gen = W.torch_generator(0, 400)
+    tensors = [_layer_inputs(torch, gen, B, T, ni, no, k, w) for _, ni, no in w.layers]
+    D_tot = w.n_layers * D
+    results = {}
+    for gdt in (torch.bfloat16, torch.float32):
+        store = torch.full((B, D_tot), 7.0, dtype=gdt, device="cuda")
+        layers = [dict(x=x, dy=dy, p_in=pi, p_out=po, g_out=store[:, j * D:(j + 1) * D])
+                  for j, (x, dy, pi, po) in enumerate(tensors)]
+        P.logra_project_layers(layers, mask=mask)
+        torch.cuda.synchronize()
+        results[gdt] = host(store)
+        assert np.all(results[gdt][:, 7 * D:].astype(np.float64) == 7.0) if gdt == torch.float32 else True
+    for j in (1, 4, 6):   # k (4096->1024), gate (4096->14336), down (14336->4096)
+        name, ni, no = w.layers[j]
+        x, dy, pi, po = (host(t) for t in tensors[j])
+        want = oracle.project_factored(x, dy, pi, po, mask_np)
+        for gdt, tol in ((torch.bfloat16, 2e-2), (torch.float32, 1e-3)):
+            got = results[gdt][:, j * D:(j + 1) * D]
+            errs = [normwise(got[b], want[b]) for b in range(B)]
+            say(f"  {name} ({ni}->{no}) {str(gdt)[6:]}: max normwise err {max(errs):.2e}")
+            assert max(errs) <= tol
+
+
+def test_cov_blocks_bench_launch():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, normwise, say
+    nb, Db, B = 224, 256, 8
+    say(f"[full cov] {nb} blocks of {Db}, {B} bf16 store rows of {nb * Db}")
+    scales = W.block_scales(0, nb, 0.1, 10.0)
+    g = W.scaled_gradients(0, 410, B, Db, scales)
+    S = torch.zeros((nb, Db, Db), dtype=torch.float32, device="cuda")
+    P.logra_cov_accumulate_blocks(dev(g), S, Db)
+    P.logra_cov_accumulate_blocks(dev(g), S, Db)   # accumulates: twice the same rows
+    torch.cuda.synchronize()
+    got = host(S)
+    for l in (0, 97, 223):
+        want = 2.0 * oracle.cov_accumulate(g[:, l * Db:(l + 1) * Db])
+        err = normwise(got[l], want)
+        say(f"  block {l}: normwise err {err:.2e}")
+        assert err <= 1e-5
+        assert np.array_equal(got[l], got[l].T)
+
+
+def test_precondition_blocks_bench_launch():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, normwise, say
+    w = W.WORKLOADS["llama3_8b_scores"]
+    ex = w.extra
+    nb, Db, Q, Nc = w.n_layers, w.D, ex["Q"], ex["N_cov"]
+    say(f"[full precondition] {nb} blocks of {Db}, Q={Q}, covariances from {Nc} gradients")
+    scales = W.block_scales(0, nb, ex["scale_lo"], ex["scale_hi"])
+    gen = W.torch_generator(0, 420)
+    covg = torch.empty((Nc, nb * Db), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(covg, scales, Db, gen)
+    test = torch.empty((Q, nb * Db), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(test, scales, Db, gen)
+    S = torch.zeros((nb, Db, Db), dtype=torch.float32, device="cuda")
+    P.logra_cov_accumulate_blocks(covg, S, Db)
+    pre = torch.empty_like(test)
+    P.logra_precondition_blocks(S, Nc, ex["damp"], test, pre)
+    torch.cuda.synchronize()
+    got = host(pre)
+    for l in (0, 101, 223):
+        cols = slice(l * Db, (l + 1) * Db)
+        Sl = oracle.cov_accumulate(host(covg[:, cols].contiguous()))
+        want, _ = oracle.precondition(Sl, Nc, ex["damp"], host(test[:, cols].contiguous()))
+        err = max(normwise(got[q, cols], want[q]) for q in range(0, Q, 7))
+        say(f"  block {l}: max normwise err over sampled queries {err:.2e}")
+        assert err <= 2e-2
+
+
+def test_scores_topk_bench_launch():
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import f64, host, say
+    w = W.WORKLOADS["llama3_8b_scores"]
+    ex = w.extra
+    N, Q, k = ex["N_train"], ex["Q"], ex["topk"]
+    D = w.n_layers * w.D
+    say(f"[full scores] {Q} x {N} at {D} dims, top-{k}")
+    scales = W.block_scales(0, w.n_layers, ex["scale_lo"], ex["scale_hi"])
+    gen = W.torch_generator(0, 430)
+    train = torch.empty((N, D), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(train, scales, w.D, gen)
+    te = torch.empty((Q, D), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(te, scales, w.D, gen)
+    tv = torch.empty((Q, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((Q, k), dtype=torch.int64, device="cuda")
+    P.logra_influence_scores(te, train, scores=None, topk=k, topk_val=tv, topk_idx=ti)   # bench's call
+    s_full = torch.empty((Q, N), dtype=torch.float32, device="cuda")
+    P.logra_influence_scores(te, train, scores=s_full, topk=0)
+    torch.cuda.synchronize()
+    say("  GPU passes done")
+    tv, ti = host(tv), host(ti)
+    g = W.rng(0, 431)
+    queries = [0, 511, 1023] + list(g.integers(0, Q, size=5))
+    cols = g.integers(0, N, size=64)
+    te_h = host(te[queries].contiguous())
+    for qi, q in enumerate(queries):
+        row = host(s_full[q])
+        # sampled scores and every returned top-k entry against the oracle
+        js = np.unique(np.concatenate([cols, ti[q]]))
+        tr_h = host(train[torch.from_numpy(js).cuda()].contiguous())
+        want = oracle.scores(te_h[qi:qi + 1], tr_h)[0]
+        norm = np.linalg.norm(f64(te_h[qi])) * np.linalg.norm(f64(tr_h), axis=1)
+        err = np.max(np.abs(row[js].astype(np.float64) - want) / norm)
+        say(f"  query {q}: normalised err on {len(js)} sampled scores {err:.2e}")
+        assert err <= 1e-3
+        # the filtered top-k is exactly the top-k of the full score row
+        order = np.lexsort((np.arange(N), -row.astype(np.float64)))[:k]
+        assert np.array_equal(ti[q], order)
+        assert np.array_equal(tv[q], row[order])
