@@ -59,9 +59,12 @@ def lib():
         L.oracle_precondition.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp, i64, vp]
         L.oracle_scores.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, vp, i64]
         L.oracle_topk.argtypes = [vp, i64, i32, i64, i64, i32, vp, vp]
+        L.oracle_self_influence.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp]
+        L.oracle_normalise_scores.argtypes = [vp, i64, i32, i64, vp, vp]
         L.oracle_num_threads.argtypes = []
         for name in ("oracle_project_factored", "oracle_project_dense", "oracle_cov_accumulate",
-                     "oracle_precondition", "oracle_scores", "oracle_topk", "oracle_num_threads"):
+                     "oracle_precondition", "oracle_scores", "oracle_topk", "oracle_self_influence",
+                     "oracle_normalise_scores", "oracle_num_threads"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -181,6 +184,38 @@ def topk(s, k: int, base: int = 0):
     rc = lib().oracle_topk(_ptr(s), max(N, 1), Q, N, int(base), int(k), _ptr(val), _ptr(idx))
     _check(rc, "oracle_topk")
     return val, idx
+
+
+def self_influence(S, N: int, damp_ratio: float, g) -> np.ndarray:
+    """self_j = g_j^T (S/N + lambda I)^{-1} g_j for one block (l-RelatIF's normaliser).
+    damp_ratio < 0: identity (self = |g_j|^2).  Returns [rows] float64."""
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    g = _c(g)
+    rows, D = g.shape
+    assert S.shape == (D, D)
+    out = np.zeros(max(rows, 1), dtype=np.float64)
+    rc = lib().oracle_self_influence(_ptr(S), D, int(N), float(damp_ratio), _ptr(g), _code(g), D, rows, _ptr(out))
+    _check(rc, "oracle_self_influence")
+    return out[:rows]
+
+
+def self_influence_blocks(S_blocks, N: int, damp_ratio: float, g) -> np.ndarray:
+    """Whole-model self-influence of a block-diagonal Hessian: the sum over column blocks."""
+    nb, D, _ = np.shape(S_blocks)
+    g = np.asarray(g)
+    return sum(self_influence(S_blocks[l], N, damp_ratio, np.ascontiguousarray(g[:, l * D:(l + 1) * D]))
+               for l in range(nb))
+
+
+def normalise_scores(s, self_tr, self_te=None) -> np.ndarray:
+    """l-RelatIF: s[q, j] / sqrt(self_tr[j]); cosine when self_te is given (also / sqrt(self_te[q]))."""
+    s = np.array(s, dtype=np.float64, order="C")
+    Q, N = s.shape
+    tr = np.ascontiguousarray(self_tr, dtype=np.float64)
+    te = None if self_te is None else np.ascontiguousarray(self_te, dtype=np.float64)
+    rc = lib().oracle_normalise_scores(_ptr(s), max(N, 1), Q, N, None if te is None else _ptr(te), _ptr(tr))
+    _check(rc, "oracle_normalise_scores")
+    return s
 
 
 def num_threads() -> int:

@@ -269,6 +269,52 @@ int oracle_scores(const void *te, int te_dtype, int64_t ld_te, int Q, const void
     return OR_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Self-influence of a gradient (the normaliser of l-RelatIF, Sec. 4.2,     */
+/* which divides each influence score by the training example's own         */
+/* influence to penalise large-gradient outliers):                          */
+/*   self_j = g_j^T (C + lambda I)^{-1} g_j                                 */
+/* for one layer block, with C, lambda as in oracle_precondition (the       */
+/* whole-model value of a block-diagonal Hessian is the sum over blocks).   */
+/* Written as its definition: the damped inverse applied to g_j, then the   */
+/* dot product with g_j.                                                    */
+/* ------------------------------------------------------------------------ */
+int oracle_self_influence(const double *S, int D, int64_t N, double r, const void *g, int g_dtype,
+                          int64_t ld_g, int rows, double *self_out) {
+    if (D <= 0 || rows < 0 || ld_g < D || !dtype_ok(g_dtype)) return OR_ERR_INVALID_ARG;
+    double *y = (double *)malloc((size_t)(rows > 0 ? rows : 1) * (size_t)D * sizeof(double));
+    const int rc = oracle_precondition(S, D, N, r, g, g_dtype, ld_g, rows, y, D, NULL);
+    if (rc != OR_OK) {
+        free(y);
+        return rc;
+    }
+#pragma omp parallel for schedule(static)
+    for (int j = 0; j < rows; ++j) {
+        double acc = 0.0;
+        for (int d = 0; d < D; ++d) acc += widen(g, g_dtype, (int64_t)j * ld_g + d) * y[(int64_t)j * D + d];
+        self_out[j] = acc;
+    }
+    free(y);
+    return OR_OK;
+}
+
+/* Normalised scores: s[q][j] / sqrt(self_tr[j]) (l-RelatIF), and also       */
+/* / sqrt(self_te[q]) when self_te is given (the cosine form: the cosine of  */
+/* the angle between the two gradients in the (C + lambda I)^{-1} inner      */
+/* product).  A zero self-influence (a zero gradient, whose raw scores are   */
+/* zero) gives a zero normalised score.                                      */
+int oracle_normalise_scores(double *s, int64_t ld_s, int Q, int64_t N, const double *self_te,
+                            const double *self_tr) {
+    if (Q < 0 || N < 0 || ld_s < N || !self_tr) return OR_ERR_INVALID_ARG;
+    for (int q = 0; q < Q; ++q)
+        for (int64_t j = 0; j < N; ++j) {
+            double den = self_tr[j];
+            if (self_te) den *= self_te[q];
+            s[(int64_t)q * ld_s + j] = den > 0.0 ? s[(int64_t)q * ld_s + j] / sqrt(den) : 0.0;
+        }
+    return OR_OK;
+}
+
 /* (value, index) a ranks before (value, index) b: larger value first, the   */
 /* lower train index on equal values.  Padding (index -1) ranks last.        */
 static int ranks_before(double va, int64_t ia, double vb, int64_t ib) {

@@ -32,6 +32,10 @@ MUTATIONS = {
     "scores_sign": ("acc += widen(te", "acc -= widen(te"),
     "topk_ties_to_higher_index": ("return ia < ib;", "return ia > ib;"),
     "bf16_widen_wrong_shift": ("<< 16;", "<< 15;"),
+    "self_influence_drops_damping": ("const int rc = oracle_precondition(S, D, N, r, g, g_dtype, ld_g, rows, y, D, NULL);",
+                                     "const int rc = oracle_precondition(S, D, N, r > 0 ? 1e-12 : r, g, g_dtype, ld_g, rows, y, D, NULL);"),
+    "normalise_without_sqrt": ("? s[(int64_t)q * ld_s + j] / sqrt(den) : 0.0;",
+                               "? s[(int64_t)q * ld_s + j] / den : 0.0;"),
 }
 
 

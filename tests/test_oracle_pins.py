@@ -284,6 +284,61 @@ def test_precondition_identity_and_not_pd():
 
 
 # --------------------------------------------------------------------------
+# Self-influence and normalised scores (l-RelatIF, Sec. 4.2)
+# --------------------------------------------------------------------------
+def test_self_influence_eigen_form_and_identity():
+    g = W.rng(15)
+    N, D = 5, 12                    # rank-deficient covariance: damping matters
+    G = g.standard_normal((N, D))
+    S = oracle.cov_accumulate(G)
+    rows = g.standard_normal((6, D)).astype(np.float32)
+    r = 0.1
+    got = oracle.self_influence(S, N, r, rows)
+    # eigen-form of g^T (C + lambda I)^{-1} g with an independent eigensolver
+    C = S / N
+    lam = r * np.trace(C) / D
+    ev, Qm = np.linalg.eigh(C)
+    c = rows.astype(np.float64) @ Qm
+    want = (c * c / (ev + lam)).sum(axis=1)
+    assert _rel(got, want) < 1e-10
+    assert np.all(got > 0)
+    # identity preconditioner: the squared norm
+    ident = oracle.self_influence(np.zeros((D, D)), 1, -1.0, rows)
+    assert np.allclose(ident, (rows.astype(np.float64) ** 2).sum(axis=1), rtol=1e-14, atol=0)
+    # quadratic in g
+    assert _rel(oracle.self_influence(S, N, r, 3 * rows.astype(np.float64)), 9 * got) < 1e-12
+
+
+def test_normalised_scores_cosine_and_outlier_invariance():
+    g = W.rng(16)
+    N, D = 9, 10
+    G = g.standard_normal((N, D))
+    S = oracle.cov_accumulate(G)
+    r = 0.05
+    tr = g.standard_normal((7, D))
+    te = g.standard_normal((4, D))
+    pre, _ = oracle.precondition(S, N, r, te)
+    s_tr = oracle.self_influence(S, N, r, tr)
+    s_te = oracle.self_influence(S, N, r, te)
+    cos = oracle.normalise_scores(oracle.scores(pre, tr), s_tr, s_te)
+    assert np.abs(cos).max() <= 1.0 + 1e-12                     # Cauchy-Schwarz in the inverse metric
+    pre_tr, _ = oracle.precondition(S, N, r, tr)
+    self_cos = oracle.normalise_scores(oracle.scores(pre_tr, tr), s_tr, s_tr)
+    assert np.allclose(np.diag(self_cos), 1.0, rtol=0, atol=1e-12)   # a gradient with itself
+    # l-RelatIF: scaling a train gradient by a > 0 leaves its scores unchanged
+    rel = oracle.normalise_scores(oracle.scores(pre, tr), s_tr)
+    tr2 = tr.copy()
+    tr2[3] *= 40.0
+    rel2 = oracle.normalise_scores(oracle.scores(pre, tr2), oracle.self_influence(S, N, r, tr2))
+    assert _rel(rel2, rel) < 1e-12
+    # and it is the raw score over the square root of the self-influence
+    assert _rel(rel, oracle.scores(pre, tr) / np.sqrt(s_tr)[None, :]) < 1e-14
+    # a zero gradient normalises to zero scores
+    z = oracle.normalise_scores(np.zeros((2, 3)), np.array([0.0, 1.0, 4.0]))
+    assert np.all(z == 0)
+
+
+# --------------------------------------------------------------------------
 # P8: scores -- identity preconditioner is a plain dot product; limits
 # --------------------------------------------------------------------------
 def test_scores_dot_product_and_limits():
