@@ -210,6 +210,44 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
                            float *topk_val, int64_t *topk_idx, int merge, void *ws,
                            size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Normalised influence scores (l-RelatIF, Sec. 4.2: each score divided by the
+ * training example's self-influence, which penalises outliers with large
+ * gradient norms; the cosine form also divides by the test example's):
+ *
+ *     self_j   = sum_l g_jl^T (C_l + lambda_l I)^{-1} g_jl     (blocks l)
+ *     s'[q][j] = s[q][j] * row_scale[q] * col_scale[j]
+ *
+ * with row_scale = 1/sqrt(self_test) (cosine) or 1 (l-RelatIF) and
+ * col_scale = 1/sqrt(self_train).
+ *
+ * logra_self_influence_blocks: for `rows` gradients g (rows at stride ld,
+ * n_blocks column blocks of width D, g_dtype F32 or BF16) writes self_out[j]
+ * and/or rsqrt_out[j] = 1/sqrt(self_j) (0 where self_j <= 0), fp32 device
+ * arrays of `rows` (either may be NULL, not both; rows = 0 returns at once).  C_l, lambda_l are formed
+ * from S + l*D*D and N with damp_ratio as in logra_precondition_blocks
+ * (damp_ratio < 0: identity, self_j = |g_j|^2).  The inverse Cholesky factor
+ * of each block is formed in float64 and applied as two bf16 halves (about 16
+ * significant bits) on the matrix cores with fp32 accumulation.
+ *   ws  workspace of logra_self_influence_ws_size(D, n_blocks) bytes.
+ * SYNCHRONOUS (returns LOGRA_ERR_NOT_PD like the preconditioner).
+ * D <= LOGRA_MAX_PRECOND_D; bf16: D, ld multiples of 8, ld < 2^22.
+ *
+ * logra_influence_scores_scaled: logra_influence_scores with the scales
+ * applied to every score before it is stored and before the top-k (row_scale
+ * [Q], col_scale [N_chunk] indexed like the chunk's rows; NULL = 1), so the
+ * top-k is the top-k of the normalised scores.
+ * ---------------------------------------------------------------------- */
+size_t logra_self_influence_ws_size(int D, int n_blocks);
+int logra_self_influence_blocks(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                                const void *g, int g_dtype, int64_t ld, int64_t rows, float *self_out,
+                                float *rsqrt_out, void *ws, size_t ws_bytes, void *stream);
+int logra_influence_scores_scaled(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
+                                  const void *g_train, int tr_dtype, int64_t ld_tr, int64_t N_chunk, int D,
+                                  int64_t train_base, const float *row_scale, const float *col_scale,
+                                  float *scores, int64_t ld_s, int topk, float *topk_val, int64_t *topk_idx,
+                                  int merge, void *ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -34,7 +34,8 @@ EXPORTED = (
     "logra_project_layers_ws_size", "logra_project_layers",
     "logra_cov_accumulate", "logra_cov_accumulate_blocks",
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
-    "logra_influence_ws_size", "logra_influence_scores",
+    "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
+    "logra_self_influence_ws_size", "logra_self_influence_blocks",
 )
 
 
@@ -82,9 +83,15 @@ def lib():
         L.logra_influence_ws_size.restype = sz
         L.logra_influence_scores.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, vp, i64, i32,
                                              vp, vp, i32, vp, sz, vp]
+        L.logra_influence_scores_scaled.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, vp, vp,
+                                                    vp, i64, i32, vp, vp, i32, vp, sz, vp]
+        L.logra_self_influence_ws_size.argtypes = [i32, i32]
+        L.logra_self_influence_ws_size.restype = sz
+        L.logra_self_influence_blocks.argtypes = [vp, i32, i32, i64, f64, vp, i32, i64, i64, vp, vp, vp, sz,
+                                                  vp]
         for name in ("logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
-                     "logra_influence_scores"):
+                     "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -235,15 +242,43 @@ def logra_influence_ws_size(Q, N_chunk, topk, scores_given) -> int:
 
 
 def logra_influence_scores(g_test_pre, g_train, scores=None, topk: int = 0, topk_val=None,
-                           topk_idx=None, train_base: int = 0, merge: bool = False, ws=None, stream=None):
-    """s = g_test_pre @ g_train^T (fp32) and/or the running per-query top-k."""
+                           topk_idx=None, train_base: int = 0, merge: bool = False, ws=None, stream=None,
+                           row_scale=None, col_scale=None):
+    """s = g_test_pre @ g_train^T (fp32) and/or the running per-query top-k.  With row_scale
+    [Q] / col_scale [N] (fp32 device arrays), the scores and the top-k are those of
+    s * row_scale[q] * col_scale[j] (logra_influence_scores_scaled)."""
     Q, D = g_test_pre.shape
     N = g_train.shape[0]
     ld_te = _rows(g_test_pre, D) if Q > 0 else D
     ld_tr = _rows(g_train, D) if N > 0 else D
     ld_s = _rows(scores, N) if scores is not None and Q > 0 else max(N, 1)
     ws, wsb = _workspace(logra_influence_ws_size(Q, N, topk, scores is not None), g_test_pre.device, ws)
-    _check(lib().logra_influence_scores(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q, _ptr(g_train),
-                                        _dtype_code(g_train), ld_tr, N, D, int(train_base), _ptr(scores), ld_s,
-                                        int(topk), _ptr(topk_val), _ptr(topk_idx), int(bool(merge)),
-                                        _ptr(ws), wsb, _stream(stream)))
+    if row_scale is None and col_scale is None:
+        _check(lib().logra_influence_scores(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q, _ptr(g_train),
+                                            _dtype_code(g_train), ld_tr, N, D, int(train_base), _ptr(scores),
+                                            ld_s, int(topk), _ptr(topk_val), _ptr(topk_idx), int(bool(merge)),
+                                            _ptr(ws), wsb, _stream(stream)))
+    else:
+        _check(lib().logra_influence_scores_scaled(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q,
+                                                   _ptr(g_train), _dtype_code(g_train), ld_tr, N, D,
+                                                   int(train_base), _ptr(row_scale), _ptr(col_scale),
+                                                   _ptr(scores), ld_s, int(topk), _ptr(topk_val),
+                                                   _ptr(topk_idx), int(bool(merge)), _ptr(ws), wsb,
+                                                   _stream(stream)))
+
+
+def logra_self_influence_ws_size(D, n_blocks) -> int:
+    return int(lib().logra_self_influence_ws_size(D, n_blocks))
+
+
+def logra_self_influence_blocks(S, N: int, damp_ratio: float, g, self_out=None, rsqrt_out=None, ws=None,
+                                stream=None):
+    """self_j = sum_l g_jl^T (S_l/N + lambda_l I)^{-1} g_jl and/or 1/sqrt(self_j) for the rows of g
+    [rows, n_blocks*D] (S [n_blocks, D, D] fp32)."""
+    n_blocks, D, _ = S.shape
+    rows = g.shape[0]
+    ld = _rows(g, D * n_blocks) if rows > 0 else D * n_blocks
+    ws, wsb = _workspace(logra_self_influence_ws_size(D, n_blocks), S.device, ws)
+    _check(lib().logra_self_influence_blocks(_ptr(S), D, n_blocks, int(N), float(damp_ratio), _ptr(g),
+                                             _dtype_code(g), ld, rows, _ptr(self_out), _ptr(rsqrt_out),
+                                             _ptr(ws), wsb, _stream(stream)))

@@ -180,6 +180,21 @@ int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, f
     return logra_cov_accumulate_blocks(g, g_dtype, ld, B, D, 1, S, stream);
 }
 
+// Waits for `s`, then returns NOT_PD naming the first block whose
+// factorisation met a non-positive pivot (the status words in the workspace).
+static int report_not_pd(void *ws, int D, int n_blocks, hipStream_t s) {
+    std::vector<int> info(static_cast<size_t>(n_blocks), 0);
+    hipError_t e = hipMemcpyAsync(info.data(), logra::precond_info_ptr(ws, D, n_blocks), sizeof(int) * n_blocks,
+                                  hipMemcpyDeviceToHost, s);
+    if (e != hipSuccess) return hip_fail(e, "status copy");
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+    for (int b = 0; b < n_blocks; ++b)
+        if (info[b] != 0)
+            return fail(LOGRA_ERR_NOT_PD, "block %d: pivot %d of C + lambda I is not positive", b, info[b] - 1);
+    return ok();
+}
+
 size_t logra_precondition_ws_size(int D, int n_blocks, int Q) {
     if (D <= 0 || n_blocks <= 0 || Q < 0) return 0;
     return round256(logra::precond_ws_bytes(D, n_blocks, Q));
@@ -216,16 +231,7 @@ int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, do
     hipError_t e = logra::launch_precondition(S, D, n_blocks, N, damp_ratio, g_test, in_dtype == LOGRA_BF16,
                                               ld_in, Q, g_out, out_dtype == LOGRA_BF16, ld_out, ws, s);
     if (e != hipSuccess) return hip_fail(e, "precondition launch");
-    std::vector<int> info(static_cast<size_t>(n_blocks), 0);
-    e = hipMemcpyAsync(info.data(), logra::precond_info_ptr(ws, D, n_blocks), sizeof(int) * n_blocks,
-                       hipMemcpyDeviceToHost, s);
-    if (e != hipSuccess) return hip_fail(e, "status copy");
-    e = hipStreamSynchronize(s);
-    if (e != hipSuccess) return hip_fail(e, "stream synchronize");
-    for (int b = 0; b < n_blocks; ++b)
-        if (info[b] != 0)
-            return fail(LOGRA_ERR_NOT_PD, "block %d: pivot %d of C + lambda I is not positive", b, info[b] - 1);
-    return ok();
+    return report_not_pd(ws, D, n_blocks, s);
 }
 
 int logra_precondition(const float *S, int D, int64_t N, double damp_ratio, const void *g_test,
@@ -244,10 +250,11 @@ size_t logra_influence_ws_size(int Q, int64_t N_chunk, int topk, int scores_give
     return b;
 }
 
-int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
-                           const void *g_train, int tr_dtype, int64_t ld_tr, int64_t N_chunk, int D,
-                           int64_t train_base, float *scores, int64_t ld_s, int topk, float *topk_val,
-                           int64_t *topk_idx, int merge, void *ws, size_t ws_bytes, void *stream) {
+static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q, const void *g_train,
+                          int tr_dtype, int64_t ld_tr, int64_t N_chunk, int D, int64_t train_base,
+                          float *scores, int64_t ld_s, int topk, float *topk_val, int64_t *topk_idx, int merge,
+                          const float *row_scale, const float *col_scale, void *ws, size_t ws_bytes,
+                          void *stream) {
     if (!valid_dtype(te_dtype) || !valid_dtype(tr_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
     if (te_dtype != tr_dtype) return fail(LOGRA_ERR_UNSUPPORTED, "test and train dtypes must match");
     if (Q < 0 || N_chunk < 0 || D <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need Q >= 0, N_chunk >= 0, D > 0");
@@ -280,6 +287,9 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     }
     TRY(check_dev(g_test_pre, "g_test_pre", bf16 ? 16 : 4));
     TRY(check_dev(g_train, "g_train", bf16 ? 16 : 4));
+    if (row_scale) TRY(check_dev(row_scale, "row_scale", 4));
+    if (col_scale) TRY(check_dev(col_scale, "col_scale", 4));
+    const logra::ScoreScale scale{row_scale, col_scale};
     const size_t need = logra_influence_ws_size(Q, N_chunk, topk, scores != nullptr);
     if (need) TRY(check_ws(ws, ws_bytes, need));
     char *wp = static_cast<char *>(ws);
@@ -296,7 +306,7 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     const int64_t pre = (bf16 && topk > 0) ? logra::topk_prefix_rows(N_chunk, topk) : 0;
     if (pre == 0) {
         hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, N_chunk, D, bf16, s_buf,
-                                            ld, nullptr, s);
+                                            ld, nullptr, scale, s);
         if (e != hipSuccess) return hip_fail(e, "score launch");
         if (topk > 0) {
             e = logra::launch_topk(s_buf, ld, Q, N_chunk, train_base, topk, topk_val, topk_idx, merge != 0, s);
@@ -312,7 +322,8 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     int *cnt = reinterpret_cast<int *>(wp + q4);
     float *cval = reinterpret_cast<float *>(wp + 2 * q4);
     int *cidx = reinterpret_cast<int *>(wp + 2 * q4 + round256(4 * static_cast<size_t>(Q) * logra::kCandCap));
-    hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, pre, D, true, s_buf, ld, nullptr, s);
+    hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, pre, D, true, s_buf, ld, nullptr,
+                                        scale, s);
     if (e != hipSuccess) return hip_fail(e, "score launch");
     e = logra::launch_topk(s_buf, ld, Q, pre, train_base, topk, topk_val, topk_idx, merge != 0, s);
     if (e != hipSuccess) return hip_fail(e, "top-k launch");
@@ -320,13 +331,70 @@ int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     if (e != hipSuccess) return hip_fail(e, "top-k threshold launch");
     const logra::ScoreFilter filt{thr, cnt, cval, cidx, logra::kCandCap};
     const void *tr_rest = static_cast<const uint16_t *>(g_train) + pre * ld_tr;
+    const logra::ScoreScale scale_rest{row_scale, col_scale ? col_scale + pre : nullptr};
     e = logra::launch_scores(g_test_pre, ld_te, Q, tr_rest, ld_tr, N_chunk - pre, D, true, s_buf + pre, ld,
-                             &filt, s);
+                             &filt, scale_rest, s);
     if (e != hipSuccess) return hip_fail(e, "score launch");
     e = logra::launch_topk_filtered(s_buf + pre, ld, Q, N_chunk - pre, train_base + pre, topk, topk_val, topk_idx,
                                     cnt, cval, cidx, logra::kCandCap, s);
     if (e != hipSuccess) return hip_fail(e, "top-k merge launch");
     return ok();
+}
+
+
+int logra_influence_scores(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
+                           const void *g_train, int tr_dtype, int64_t ld_tr, int64_t N_chunk, int D,
+                           int64_t train_base, float *scores, int64_t ld_s, int topk, float *topk_val,
+                           int64_t *topk_idx, int merge, void *ws, size_t ws_bytes, void *stream) {
+    return influence_impl(g_test_pre, te_dtype, ld_te, Q, g_train, tr_dtype, ld_tr, N_chunk, D, train_base,
+                          scores, ld_s, topk, topk_val, topk_idx, merge, nullptr, nullptr, ws, ws_bytes, stream);
+}
+
+int logra_influence_scores_scaled(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q,
+                                  const void *g_train, int tr_dtype, int64_t ld_tr, int64_t N_chunk, int D,
+                                  int64_t train_base, const float *row_scale, const float *col_scale,
+                                  float *scores, int64_t ld_s, int topk, float *topk_val, int64_t *topk_idx,
+                                  int merge, void *ws, size_t ws_bytes, void *stream) {
+    return influence_impl(g_test_pre, te_dtype, ld_te, Q, g_train, tr_dtype, ld_tr, N_chunk, D, train_base,
+                          scores, ld_s, topk, topk_val, topk_idx, merge, row_scale, col_scale, ws, ws_bytes,
+                          stream);
+}
+
+size_t logra_self_influence_ws_size(int D, int n_blocks) {
+    if (D <= 0 || n_blocks <= 0) return 0;
+    return round256(logra::self_influence_ws_bytes(D, n_blocks));
+}
+
+int logra_self_influence_blocks(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                                const void *g, int g_dtype, int64_t ld, int64_t rows, float *self_out,
+                                float *rsqrt_out, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(g_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (D <= 0 || n_blocks <= 0 || rows < 0) return fail(LOGRA_ERR_INVALID_ARG, "need D > 0, n_blocks > 0, rows >= 0");
+    if (D > LOGRA_MAX_PRECOND_D) return fail(LOGRA_ERR_UNSUPPORTED, "D must be <= %d", LOGRA_MAX_PRECOND_D);
+    if (n_blocks > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "n_blocks must be <= 65535");
+    if (ld < static_cast<int64_t>(D) * n_blocks) return fail(LOGRA_ERR_INVALID_ARG, "ld must be >= D * n_blocks");
+    if (damp_ratio != damp_ratio) return fail(LOGRA_ERR_INVALID_ARG, "damp_ratio is NaN");
+    if (damp_ratio >= 0.0 && N <= 0) return fail(LOGRA_ERR_INVALID_ARG, "N must be > 0");
+    if (rows == 0) return ok();   // nothing to factor for
+    if (self_out == nullptr && rsqrt_out == nullptr)
+        return fail(LOGRA_ERR_INVALID_ARG, "nothing to compute: self_out and rsqrt_out are NULL");
+    const bool bf16 = g_dtype == LOGRA_BF16;
+    if (bf16 && (D % 8 || ld % 8)) return fail(LOGRA_ERR_INVALID_ARG, "bf16 gradients need D and ld multiples of 8");
+    if (bf16 && ld >= (int64_t{1} << 22)) return fail(LOGRA_ERR_UNSUPPORTED, "bf16 gradients support ld < 4194304");
+    if ((!bf16 || D % 32) && rows > INT32_MAX)
+        return fail(LOGRA_ERR_UNSUPPORTED, "fp32 gradients, or D not a multiple of 32, support rows < 2^31");
+    if (damp_ratio >= 0.0) TRY(check_dev(S, "S", 4));
+    if (self_out) TRY(check_dev(self_out, "self_out", 4));
+    if (rsqrt_out) TRY(check_dev(rsqrt_out, "rsqrt_out", 4));
+    TRY(check_ws(ws, ws_bytes, logra_self_influence_ws_size(D, n_blocks)));
+    TRY(check_dev(g, "g", bf16 ? 16 : 4));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = logra::launch_inverse_factor(S, D, n_blocks, N, damp_ratio, ws, s);
+    if (e != hipSuccess) return hip_fail(e, "factor launch");
+    e = logra::launch_self_influence(g, bf16, ld, rows, D, n_blocks, ws, self_out, rsqrt_out, s);
+    if (e != hipSuccess) return hip_fail(e, "self-influence launch");
+    // synchronous, like the preconditioner, so that a non-positive pivot is reported
+    return report_not_pd(ws, D, n_blocks, s);
 }
 
 }  // extern "C"

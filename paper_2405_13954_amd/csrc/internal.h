@@ -6,6 +6,7 @@
 
 namespace logra {
 
+typedef uint16_t bf16_bits_t;   // a bf16 value as its bit pattern
 constexpr int kMaxGroup = 16;   // layers per grouped projection launch
 constexpr int kMaxK = 128;
 constexpr int kMaxTopk = 1024;
@@ -47,6 +48,17 @@ hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, d
 hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int rows, int cols,
                             void *dst, bool bf16_out, int64_t ld_out, hipStream_t s);
 
+// Self-influence (l-RelatIF's normaliser): per block, W = L^{-1} of the
+// damped covariance's Cholesky factor (identity when damp_ratio < 0), kept as
+// bf16 hi + lo halves in the workspace after the preconditioner's layout;
+// then self_j = sum over blocks of |W_l g_jl|^2.
+size_t self_influence_ws_bytes(int D, int n_blocks);
+bf16_bits_t *self_influence_w(void *ws, int D, int n_blocks, bool lo);
+hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                                 void *ws, hipStream_t s);
+hipError_t launch_self_influence(const void *g, bool bf16, int64_t ld, int64_t rows, int D, int n_blocks,
+                                 const void *ws, float *self_out, float *rsqrt_out, hipStream_t s);
+
 // Score GEMM s = te * tr^T (fp32 result) and per-query top-k.  With a
 // filter (bf16 only), scores at or above thr[q] are also appended to row q's
 // candidate list: cnt[q] counts them (past `cap` too), val/idx hold the
@@ -59,9 +71,15 @@ struct ScoreFilter {
     int *idx;
     int cap;
 };
+// Optional scales of normalised scores: s[q][j] * row[q] * col[j] (NULL = 1;
+// col is indexed by the column of this launch).
+struct ScoreScale {
+    const float *row;
+    const float *col;
+};
 hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
                          int64_t N, int D, bool bf16, float *s, int64_t ld_s, const ScoreFilter *filt,
-                         hipStream_t st);
+                         const ScoreScale &scale, hipStream_t st);
 // Rows of a chunk scored and selected exactly before candidate filtering
 // starts (their running top-k sets the thresholds); 0 = no filtering.
 int64_t topk_prefix_rows(int64_t N, int k);

@@ -225,7 +225,9 @@ __global__ __launch_bounds__(64) void k_diag_inv(const double *A_all, int D, dou
 // q0 .. q0+63) of one layer block.  Wave w owns rows 16w..16w+15 of the
 // 64 x 64 (rows x queries) tile; acc[c] holds columns 16c..16c+15 in the
 // fp64 16x16 result layout (register r of lane l: row l/16 + 4r).
-template <typename TIn, typename TOut>
+// IDENT: the right-hand sides are the identity columns (g is not read) and
+// only the forward solve runs, leaving L^{-1} in Y.
+template <typename TIn, typename TOut, bool IDENT = false>
 __global__ __launch_bounds__(256) void k_trsm_f64(const double *A_all, const double *Linv_all, int D,
                                                   const TIn *g, int64_t ld_in, int Q, int Qp, double *Y_all,
                                                   double *Z_all, TOut *out, int64_t ld_out) {
@@ -302,9 +304,12 @@ __global__ __launch_bounds__(256) void k_trsm_f64(const double *A_all, const dou
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int q = q0 + 16 * c + row, d = i * NB + 16 * w + kg + 4 * r;
-                acc[c][r] = (q < Q && d < D) ? load_in_d<TIn>(g + static_cast<int64_t>(q) * ld_in +
-                                                               static_cast<int64_t>(blk) * D + d)
-                                             : 0.0;
+                if (IDENT)
+                    acc[c][r] = (q < Q && d == q) ? 1.0 : 0.0;
+                else
+                    acc[c][r] = (q < Q && d < D) ? load_in_d<TIn>(g + static_cast<int64_t>(q) * ld_in +
+                                                                   static_cast<int64_t>(blk) * D + d)
+                                                 : 0.0;
             }
         for (int j = 0; j < i; ++j) {
             stage_L(i * NB, j * NB, false);
@@ -321,6 +326,7 @@ __global__ __launch_bounds__(256) void k_trsm_f64(const double *A_all, const dou
         store_ws(Y, i);
         __syncthreads();
     }
+    if (IDENT) return;
     // ---------------- backward: L^T Z = Y ----------------
     for (int i = nbt - 1; i >= 0; --i) {
 #pragma unroll
@@ -356,6 +362,33 @@ __global__ __launch_bounds__(256) void k_trsm_f64(const double *A_all, const dou
     }
 }
 
+__global__ __launch_bounds__(256) void k_clear_info(int *info, int n) {
+    for (int i = threadIdx.x; i < n; i += 256) info[i] = 0;
+}
+
+// W = L^{-1} (fp64, rows d, columns q of the forward solution) as two bf16
+// arrays whose sum carries about 16 significant bits: hi = RNE(W), lo =
+// RNE(W - hi).  Row-major [blk][Dp][D] with Dp = D rounded up to 256; rows
+// past D are zero.  With `ident`, W = I.
+__global__ __launch_bounds__(256) void k_split_w(const double *Y_all, int D, int Qp, bool ident,
+                                                  bf16_bits *w_hi, bf16_bits *w_lo) {
+    const int blk = blockIdx.y, d = blockIdx.x;
+    const int Dp = gridDim.x;
+    bf16_bits *h = w_hi + (static_cast<size_t>(blk) * Dp + d) * D;
+    bf16_bits *l = w_lo + (static_cast<size_t>(blk) * Dp + d) * D;
+    if (d >= D) {
+        for (int q = threadIdx.x; q < D; q += 256) h[q] = l[q] = 0;
+        return;
+    }
+    const double *Y = Y_all + static_cast<size_t>(blk) * D * Qp + static_cast<size_t>(d) * Qp;
+    for (int q = threadIdx.x; q < D; q += 256) {
+        const float v = ident ? (q == d ? 1.f : 0.f) : static_cast<float>(Y[q]);
+        const bf16_bits hb = f32_to_bf16_rne(v);
+        h[q] = hb;
+        l[q] = ident ? bf16_bits{0} : f32_to_bf16_rne(static_cast<float>(Y[q] - static_cast<double>(bf16_to_f32(hb))));
+    }
+}
+
 template <typename TIn, typename TOut>
 __global__ __launch_bounds__(256) void k_copy_rows(const TIn *src, int64_t ld_in, int cols,
                                                    TOut *dst, int64_t ld_out) {
@@ -375,6 +408,21 @@ hipError_t launch_solve(const WsLayout &w, int D, int n_blocks, const void *g, i
 }
 
 }  // namespace
+
+inline size_t w_half_bytes(int D, int n_blocks) {
+    const size_t Dp = static_cast<size_t>(D + 255) / 256 * 256;
+    return align256(sizeof(bf16_bits) * static_cast<size_t>(n_blocks) * Dp * D);
+}
+
+size_t self_influence_ws_bytes(int D, int n_blocks) {
+    return precond_ws_bytes(D, n_blocks, D) + 2 * w_half_bytes(D, n_blocks);
+}
+
+bf16_bits *self_influence_w(void *ws, int D, int n_blocks, bool lo) {
+    char *p = static_cast<char *>(ws) + precond_ws_bytes(D, n_blocks, D);
+    if (lo) p += w_half_bytes(D, n_blocks);
+    return reinterpret_cast<bf16_bits *>(p);
+}
 
 size_t precond_ws_bytes(int D, int n_blocks, int Q) {
     const size_t nb = static_cast<size_t>(n_blocks);
@@ -424,6 +472,29 @@ hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, d
     if (bf16_in) return launch_solve<bf16_bits, float>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
     if (bf16_out) return launch_solve<float, bf16_bits>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
     return launch_solve<float, float>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+}
+
+hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                                 void *ws, hipStream_t s) {
+    const WsLayout w = ws_layout(ws, D, n_blocks, D);
+    bf16_bits *hi = self_influence_w(ws, D, n_blocks, false), *lo = self_influence_w(ws, D, n_blocks, true);
+    const bool ident = damp_ratio < 0;
+    if (!ident) {
+        // factor (status words as for the preconditioner), then L^{-1} = forward solve of I
+        const hipError_t e = launch_precondition(S, D, n_blocks, N, damp_ratio, nullptr, false, D, 0, nullptr,
+                                                 false, D, ws, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_diag_inv, dim3(tiles_of(D), n_blocks), dim3(64), 0, s, w.A, D, w.Linv);
+        const dim3 grid(static_cast<unsigned>(padded_q(D) / NB), static_cast<unsigned>(n_blocks));
+        hipLaunchKernelGGL((k_trsm_f64<float, float, true>), grid, dim3(256), 0, s, w.A, w.Linv, D,
+                           static_cast<const float *>(nullptr), int64_t{0}, D, padded_q(D), w.Y, w.Z,
+                           static_cast<float *>(nullptr), int64_t{0});
+    } else {
+        hipLaunchKernelGGL(k_clear_info, dim3(1), dim3(256), 0, s, w.info, n_blocks);
+    }
+    hipLaunchKernelGGL(k_split_w, dim3((D + 255) / 256 * 256, n_blocks), dim3(256), 0, s, w.Y, D, padded_q(D),
+                       ident, hi, lo);
+    return hipGetLastError();
 }
 
 }  // namespace logra

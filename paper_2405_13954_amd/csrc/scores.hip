@@ -60,14 +60,16 @@ struct Slab {
 constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100,
               kSchedDsWrite = 0x200;
 
-// Epilogue of a 256 x 256 tile: the fp32 scores go to s (rows past Q and
-// columns past N are skipped).  With a filter, scores at or above the row's
+// Epilogue of a 256 x 256 tile: the fp32 scores, times the optional row and
+// column scales (s * row_scale[q] * col_scale[j], for normalised scores), go
+// to s (rows past Q and columns past N are skipped).  With a filter, scores at or above the row's
 // threshold are also appended to the row's top-k candidate list (order
 // arbitrary; the count keeps growing past the capacity so that an overflow is
 // visible).  `ths` is 1 KB of free LDS for the tile's thresholds.
 __device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *ths, float *__restrict__ s,
                                              int64_t ld_s, int m0, int64_t n0, int rows_a, int rows_b,
-                                             int wm, int wn, int tid, int lane, const ScoreFilter &filt) {
+                                             int wm, int wn, int tid, int lane, const ScoreFilter &filt,
+                                             const ScoreScale &scale) {
     const bool filter = filt.thr != nullptr;
     if (filter) {
         ths[tid] = tid < rows_a ? filt.thr[m0 + tid] : __builtin_inff();
@@ -83,10 +85,13 @@ __device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *t
             const int64_t q = m0 + row;
             float *srow_p = s + q * ld_s + n0;
             const float t = filter ? ths[row] : 0.f;
+            const float rs = scale.row ? scale.row[q] : 1.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int col = wn * 128 + j * 32 + (lane & 31);
-                const float v = acc[i][j][r];
+                float v = acc[i][j][r];
+                if (scale.row) v *= rs;
+                if (scale.col && col < rows_b) v *= scale.col[n0 + col];
                 if (col < rows_b) {
                     srow_p[col] = v;
                     if (filter && v >= t) {
@@ -105,7 +110,8 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
                                                        int Q, const bf16_bits *__restrict__ tr,
                                                        int64_t ld_tr, int64_t N, int D,
                                                        float *__restrict__ s, int64_t ld_s,
-                                                       int m_tiles, int n_tiles, ScoreFilter filt) {
+                                                       int m_tiles, int n_tiles, ScoreFilter filt,
+                                                       ScoreScale scale) {
     __shared__ __attribute__((aligned(16))) bf16_bits As[2][BM * LDR];
     __shared__ __attribute__((aligned(16))) bf16_bits Bs[2][BN * LDR];
 
@@ -240,7 +246,7 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
     }
 
     store_scores(acc, reinterpret_cast<float *>(&As[0][0]), s, ld_s, m0, n0, rows_a, rows_b, wm, wn,
-                 tid, lane, filt);   // LDS is free after the last barrier
+                 tid, lane, filt, scale);   // LDS is free after the last barrier
 }
 
 // ------------------------------------------------------------------------
@@ -281,7 +287,8 @@ __global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restric
                                                       int Q, const bf16_bits *__restrict__ tr,
                                                       int64_t ld_tr, int64_t N, int D,
                                                       float *__restrict__ s, int64_t ld_s,
-                                                      int m_tiles, int n_tiles, ScoreFilter filt) {
+                                                      int m_tiles, int n_tiles, ScoreFilter filt,
+                                                       ScoreScale scale) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kLdsBytes];
 
     const int bid = blockIdx.x;
@@ -416,13 +423,13 @@ __global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restric
     // the copies of the slabs past the end are still in flight
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     store_scores(acc, reinterpret_cast<float *>(smem), s, ld_s, m0, n0, rows_a, rows_b, wm, wn, tid,
-                 lane, filt);
+                 lane, filt, scale);
 }
 
 // fp32 scores (small problems): one thread per score, sequential contraction.
 __global__ __launch_bounds__(256) void k_scores_f32(const float *te, int64_t ld_te, int Q,
                                                     const float *tr, int64_t ld_tr, int64_t N, int D,
-                                                    float *s, int64_t ld_s) {
+                                                    float *s, int64_t ld_s, ScoreScale scale) {
     const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     const int q = blockIdx.y;
     if (j >= N) return;
@@ -430,6 +437,8 @@ __global__ __launch_bounds__(256) void k_scores_f32(const float *te, int64_t ld_
     const float *b = tr + j * ld_tr;
     float acc = 0.f;
     for (int d = 0; d < D; ++d) acc = __builtin_fmaf(a[d], b[d], acc);
+    if (scale.row) acc *= scale.row[q];
+    if (scale.col) acc *= scale.col[j];
     s[static_cast<int64_t>(q) * ld_s + j] = acc;
 }
 
@@ -690,7 +699,7 @@ __global__ __launch_bounds__(KT_THREADS) void k_topk_filtered(
 
 hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
                          int64_t N, int D, bool bf16, float *s, int64_t ld_s, const ScoreFilter *filt,
-                         hipStream_t st) {
+                         const ScoreScale &scale, hipStream_t st) {
     if (Q == 0 || N == 0) return hipSuccess;
     if (bf16) {
         const int m_tiles = (Q + BM - 1) / BM;
@@ -701,12 +710,12 @@ hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, i
         hipLaunchKernelGGL(LOGRA_SC_DMA ? k_scores_dma : k_scores_bf16, dim3(grid), dim3(GT), 0, st,
                            static_cast<const bf16_bits *>(te), ld_te, Q,
                            static_cast<const bf16_bits *>(tr), ld_tr, N, D, s, ld_s, m_tiles, n_tiles,
-                           filt ? *filt : none);
+                           filt ? *filt : none, scale);
     } else {
         if (filt) return hipErrorInvalidValue;   // candidate filtering is a bf16-path feature
         const dim3 grid(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(Q));
         hipLaunchKernelGGL(k_scores_f32, grid, dim3(256), 0, st, static_cast<const float *>(te), ld_te,
-                           Q, static_cast<const float *>(tr), ld_tr, N, D, s, ld_s);
+                           Q, static_cast<const float *>(tr), ld_tr, N, D, s, ld_s, scale);
     }
     return hipGetLastError();
 }

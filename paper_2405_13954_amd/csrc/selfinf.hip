@@ -1,0 +1,265 @@
+// Self-influence of gradients, the normaliser of l-RelatIF (Sec. 4.2: each
+// influence score is divided by the training example's own influence, which
+// penalises outliers with large gradient norms):
+//
+//   self_j = sum_l g_jl^T (C_l + lambda_l I)^{-1} g_jl = sum_l |W_l g_jl|^2,
+//   W_l = L_l^{-1},  C_l + lambda_l I = L_l L_l^T
+//
+// for a block-diagonal (per-layer) Hessian.  W_l comes from the damped
+// Cholesky factor in float64 and is held as two bf16 arrays hi + lo (about
+// 16 significant bits together), so the products run on the bf16 matrix
+// cores with fp32 accumulation: y = g W_hi^T + g W_lo^T.
+//
+// bf16 gradients with D a multiple of 32: one workgroup per 256 gradients;
+// for each block and each
+// 256-wide pass over the output dimension, the contraction advances 32
+// columns (one slab) per step: the slab of the gradients and of both W halves
+// is fetched one step ahead into registers (range-checked buffer loads; rows
+// and columns past the data read as zeros) and stored into one of two LDS
+// buffers (80-byte rows, conflict-free fragment reads); 4 waves, each owning
+// 128 gradients x 128 outputs as 4 x 4 blocks of 32x32x16 MFMAs.  After the
+// last slab of a pass the squares of the outputs are summed over the wave's
+// columns (registers, then lane shuffles) into the gradients' running sums;
+// at the end the two wave halves are added through LDS, in a fixed order.
+#include "common.h"
+#include "internal.h"
+
+namespace logra {
+namespace {
+
+constexpr int SR = 256;                    // gradients per workgroup
+constexpr int SO = 256;                    // output dimensions per pass
+constexpr int SK = 32;                     // contraction columns per slab
+constexpr int SLD = SK + 8;                // padded LDS row (bf16): 80 bytes
+constexpr int STH = 256;                   // threads
+constexpr int SL = SR * SK / 8 / STH;      // 128-bit loads per operand and thread per slab (4)
+
+struct Slab3 {
+    u32x4 a[SL], h[SL], l[SL];
+};
+
+__global__ __launch_bounds__(STH, 1) void k_self_influence(const bf16_bits *__restrict__ g, int64_t ld,
+                                                           int64_t rows, int D, int n_blocks,
+                                                           const bf16_bits *__restrict__ w_hi,
+                                                           const bf16_bits *__restrict__ w_lo,
+                                                           float *__restrict__ self_out,
+                                                           float *__restrict__ rsqrt_out) {
+    __shared__ __attribute__((aligned(16))) bf16_bits As[2][SR * SLD];
+    __shared__ __attribute__((aligned(16))) bf16_bits Hs[2][SO * SLD];
+    __shared__ __attribute__((aligned(16))) bf16_bits Ls[2][SO * SLD];
+    __shared__ float rowsum[2][SR];
+
+    const int64_t r0 = static_cast<int64_t>(blockIdx.x) * SR;
+    const int nrows = rows - r0 < SR ? static_cast<int>(rows - r0) : SR;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int n_ot = (D + SO - 1) / SO;
+    const int Dp = n_ot * SO;        // rows of each W half, zero past D
+    const int ns = (D + SK - 1) / SK;
+    const int ns2 = ns + (ns & 1);   // slabs per output pass, rounded up to even (extra slabs load zeros)
+
+    // staging: load i of a thread covers row (or output) srow + 64 i, columns scol..scol+7
+    const int srow = tid >> 2, scol = 8 * (tid & 3);
+    const auto rsa = buf_rsrc_uniform(g + r0 * ld, static_cast<uint32_t>(nrows * ld * 2));
+    uint32_t oa[SL];
+#pragma unroll
+    for (int i = 0; i < SL; ++i) {
+        const int r = srow + 64 * i;
+        oa[i] = r < nrows ? static_cast<uint32_t>((r * ld + scol) * 2) : kBufOOB;
+    }
+    // load cursor: slab (ls, lot, ll) = (contraction slab, output pass, block),
+    // advanced by one slab per gload in the order the slabs are consumed
+    int ls = 0, lot = 0, ll = 0;
+    auto gload = [&](Slab3 &st) {
+        const bool live = ll < n_blocks && ls < ns;   // uniform (D is a multiple of SK)
+        const int col = ls * SK + scol;
+        const bool cin = live;
+        const uint32_t da = static_cast<uint32_t>((static_cast<int64_t>(ll) * D + ls * SK) * 2);
+        const size_t wblk = static_cast<size_t>(live ? ll : 0) * Dp * D;
+        const auto rh = buf_rsrc_uniform(w_hi + wblk, static_cast<uint32_t>(Dp * D * 2));
+        const auto rl = buf_rsrc_uniform(w_lo + wblk, static_cast<uint32_t>(Dp * D * 2));
+#pragma unroll
+        for (int i = 0; i < SL; ++i) {
+            const int o = lot * SO + srow + 64 * i;   // output dimension = row of W (zero rows past D)
+            const uint32_t ow = cin ? static_cast<uint32_t>((o * D + col) * 2) : kBufOOB;
+            st.a[i] = buf_ld128(rsa, cin ? oa[i] + da : kBufOOB);
+            st.h[i] = buf_ld128(rh, ow);
+            st.l[i] = buf_ld128(rl, ow);
+        }
+        if (++ls == ns2) {
+            ls = 0;
+            if (++lot == n_ot) {
+                lot = 0;
+                ++ll;
+            }
+        }
+    };
+    auto lstore = [&](const Slab3 &st, int buf) {
+#pragma unroll
+        for (int i = 0; i < SL; ++i) {
+            const int off = (srow + 64 * i) * SLD + scol;
+            *reinterpret_cast<u32x4 *>(&As[buf][off]) = st.a[i];
+            *reinterpret_cast<u32x4 *>(&Hs[buf][off]) = st.h[i];
+            *reinterpret_cast<u32x4 *>(&Ls[buf][off]) = st.l[i];
+        }
+    };
+
+    f32x16 acc[4][4];
+    // Row sums are kept reduced: entry e = 16 i + r of the 64 (i, r) result
+    // rows of a half-wave belongs to lane e % 32 of that half, slot e / 32.
+    float psum[2] = {0.f, 0.f};
+    auto zero_acc = [&]() {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    };
+    zero_acc();
+
+    // fragments: lane l reads row (l % 32) of each 32-row block, columns
+    // 8 (l / 32) .. +8 of each 16-wide step
+    const int frow = lane & 31, fk = 8 * (lane >> 5);
+    auto compute = [&](int buf) {
+#pragma unroll
+        for (int ks = 0; ks < SK / 16; ++ks) {
+            bf16x8 fa[4], fh[4], fl[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                fa[i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(
+                    &As[buf][(wm * 128 + i * 32 + frow) * SLD + fk + 16 * ks]));
+                fh[i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(
+                    &Hs[buf][(wn * 128 + i * 32 + frow) * SLD + fk + 16 * ks]));
+                fl[i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(
+                    &Ls[buf][(wn * 128 + i * 32 + frow) * SLD + fk + 16 * ks]));
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    acc[i][j] = mfma32_bf16(fa[i], fh[j], acc[i][j]);
+                    acc[i][j] = mfma32_bf16(fa[i], fl[j], acc[i][j]);
+                }
+            __builtin_amdgcn_sched_barrier(0);   // one step's fragments live at a time
+        }
+    };
+    // after the last slab of an output pass: add the squared outputs, summed
+    // over the lane's columns, then over the 32 lanes of the half-wave (all
+    // columns of the pass), into the owning lane's slot
+    auto fold = [&]() {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float v = 0.f;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) v = __builtin_fmaf(acc[i][j][r], acc[i][j][r], v);
+#pragma unroll
+                for (int o = 16; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+                const int e = 16 * i + r;
+                if ((lane & 31) == (e & 31)) psum[e >> 5] += v;
+                __builtin_amdgcn_sched_barrier(0);   // one row at a time: short live ranges
+            }
+        zero_acc();
+    };
+
+    // One slab in flight in registers while the previous one is multiplied out
+    // of LDS (the prefetch runs across pass and block boundaries, in the order
+    // of the cursor).
+    Slab3 st;
+    gload(st);
+    lstore(st, 0);
+    __syncthreads();
+    for (int l = 0; l < n_blocks; ++l)
+        for (int ot = 0; ot < n_ot; ++ot) {
+            for (int k = 0; k < ns2; k += 2) {
+                gload(st);
+                compute(0);
+                lstore(st, 1);
+                __syncthreads();
+                gload(st);
+                compute(1);
+                lstore(st, 0);
+                __syncthreads();
+            }
+            fold();
+        }
+
+    // combine the two wave halves wn = 0, 1 (in that order) through LDS
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int e = 32 * h + (lane & 31), i = e >> 4, r = e & 15;
+        rowsum[wn][wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)] = psum[h];
+    }
+    __syncthreads();
+    if (tid < nrows) {
+        const float sv = rowsum[0][tid] + rowsum[1][tid];
+        if (self_out) self_out[r0 + tid] = sv;
+        if (rsqrt_out) rsqrt_out[r0 + tid] = sv > 0.f ? 1.0f / sqrtf(sv) : 0.f;
+    }
+}
+
+// Any D (and fp32 gradients): one workgroup per gradient; thread d forms
+// output d of W_l g_l with the hi + lo halves (all D columns), a fixed-order
+// block sum adds the squares, blocks in order.  For small problems.
+template <typename TIn>
+__global__ __launch_bounds__(256) void k_self_influence_rows(const TIn *__restrict__ g, int64_t ld, int D,
+                                                             int n_blocks, const bf16_bits *__restrict__ w_hi,
+                                                             const bf16_bits *__restrict__ w_lo,
+                                                             float *__restrict__ self_out,
+                                                             float *__restrict__ rsqrt_out) {
+    __shared__ float red[256];
+    const int64_t j = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int Dp = (D + 255) / 256 * 256;
+    float total = 0.f;
+    for (int l = 0; l < n_blocks; ++l) {
+        const TIn *gl = g + j * ld + static_cast<int64_t>(l) * D;
+        float part = 0.f;
+        for (int d = tid; d < D; d += 256) {
+            const bf16_bits *h = w_hi + (static_cast<size_t>(l) * Dp + d) * D;
+            const bf16_bits *lo = w_lo + (static_cast<size_t>(l) * Dp + d) * D;
+            float y = 0.f;
+            for (int k = 0; k < D; ++k)
+                y = __builtin_fmaf(bf16_to_f32(h[k]) + bf16_to_f32(lo[k]), static_cast<float>(load_in_d<TIn>(gl + k)), y);
+            part = __builtin_fmaf(y, y, part);
+        }
+        red[tid] = part;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (tid < w) red[tid] += red[tid + w];
+            __syncthreads();
+        }
+        if (tid == 0) total += red[0];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        if (self_out) self_out[j] = total;
+        if (rsqrt_out) rsqrt_out[j] = total > 0.f ? 1.0f / sqrtf(total) : 0.f;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_self_influence(const void *g, bool bf16, int64_t ld, int64_t rows, int D, int n_blocks,
+                                 const void *ws, float *self_out, float *rsqrt_out, hipStream_t s) {
+    if (rows == 0) return hipSuccess;
+    void *w = const_cast<void *>(ws);
+    const bf16_bits *hi = self_influence_w(w, D, n_blocks, false), *lo = self_influence_w(w, D, n_blocks, true);
+    if (bf16 && D % SK == 0) {
+        const unsigned grid = static_cast<unsigned>((rows + SR - 1) / SR);
+        hipLaunchKernelGGL(k_self_influence, dim3(grid), dim3(STH), 0, s, static_cast<const bf16_bits *>(g), ld,
+                           rows, D, n_blocks, hi, lo, self_out, rsqrt_out);
+    } else if (bf16) {
+        hipLaunchKernelGGL(k_self_influence_rows<bf16_bits>, dim3(static_cast<unsigned>(rows)), dim3(256), 0, s,
+                           static_cast<const bf16_bits *>(g), ld, D, n_blocks, hi, lo, self_out, rsqrt_out);
+    } else {
+        hipLaunchKernelGGL(k_self_influence_rows<float>, dim3(static_cast<unsigned>(rows)), dim3(256), 0, s,
+                           static_cast<const float *>(g), ld, D, n_blocks, hi, lo, self_out, rsqrt_out);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace logra

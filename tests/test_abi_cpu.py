@@ -116,3 +116,41 @@ def test_influence_validation(L):
     assert f(*args(merge=2)) == P.ERR_INVALID_ARG
     assert f(*args(base=-1)) == P.ERR_INVALID_ARG
     assert f(*args(Q=0)) == P.OK
+
+
+def test_self_influence_ws_and_validation(L):
+    # the preconditioner's workspace for Q = D (the identity solve) plus the
+    # inverse factor's two bf16 halves, each [n_blocks][D rounded up to 256][D]
+    assert P.logra_self_influence_ws_size(256, 224) == (P.logra_precondition_ws_size(256, 224, 256)
+                                                        + 2 * 224 * 256 * 256 * 2)
+    assert P.logra_self_influence_ws_size(40, 3) == (P.logra_precondition_ws_size(40, 3, 40)
+                                                     + 2 * ((3 * 256 * 40 * 2 + 255) // 256 * 256))
+    assert P.logra_self_influence_ws_size(0, 3) == 0
+    f = L.logra_self_influence_blocks
+    fake = ctypes.c_void_p(0x1000)    # never dereferenced: every case fails host validation first
+    args = lambda **kw: [kw.get(k, v) for k, v in dict(
+        S=None, D=64, nb=2, N=4, damp=0.1, g=None, gdt=1, ld=128, rows=4, so=fake, ro=None, ws=None, wsb=0,
+        st=None).items()]
+    assert f(*args(gdt=5)) == P.ERR_INVALID_ARG
+    assert f(*args(D=0)) == P.ERR_INVALID_ARG
+    assert f(*args(rows=-1)) == P.ERR_INVALID_ARG
+    assert f(*args(D=8193, ld=8193 * 2)) == P.ERR_UNSUPPORTED
+    assert f(*args(ld=127)) == P.ERR_INVALID_ARG
+    assert f(*args(damp=float("nan"))) == P.ERR_INVALID_ARG
+    assert f(*args(N=0)) == P.ERR_INVALID_ARG
+    assert f(*args(so=None)) == P.ERR_INVALID_ARG          # nothing requested
+    assert "nothing to compute" in P.logra_last_error()
+    assert f(*args(D=60, ld=120)) == P.ERR_INVALID_ARG       # bf16 rows need multiples of 8
+    assert f(*args(ld=1 << 22)) == P.ERR_UNSUPPORTED
+    assert f(*args(rows=0, so=None)) == P.OK                # no rows: a no-op, no device access
+
+
+def test_scaled_influence_validation(L):
+    f = L.logra_influence_scores_scaled
+    args = lambda **kw: [kw.get(k, v) for k, v in dict(
+        te=None, tdt=1, ld_te=64, Q=2, tr=None, rdt=1, ld_tr=64, N=10, D=64, base=0, rs=None, cs=None, s=None,
+        ld_s=10, topk=3, tv=None, ti=None, merge=0, ws=None, wsb=0, st=None).items()]
+    assert f(*args(rdt=0)) == P.ERR_UNSUPPORTED
+    assert f(*args(topk=1025)) == P.ERR_UNSUPPORTED
+    assert f(*args(topk=0)) == P.ERR_INVALID_ARG
+    assert f(*args(Q=0)) == P.OK
