@@ -11,7 +11,9 @@ Influence leg (reported under "influence", scores/s): 1,024 test gradients
 against 500,000 stored training gradients of 57,344 dims -- damped-Cholesky
 preconditioning of the test gradients over 224 blocks of 256 (covariances of
 4,096 gradients, damping 0.1 x mean eigenvalue), the score GEMM and the
-per-query top-100.
+per-query top-100.  Its "relatif" entry times l-RelatIF on the same store: the
+self-influence of every training row (once per store) and the score pass with
+the 1/sqrt(self) scales applied before the top-100.
 
 All inputs are synthetic, drawn on the device before timing.  Each leg
 reports the roofline of its dominant kernel from HIP events recorded on the
@@ -309,6 +311,8 @@ def influence_leg(args, torch, P):
                      "frac": achieved / BF16_PEAK_TFLOPS, "traffic": traffic, "traffic_over_algorithmic": ratio,
                      "kernel": "score GEMM (bf16 MFMA, fp32 accumulation)", "flops_per_launch": flops},
     }
+    if args.relatif:
+        res["relatif"] = relatif_sub_leg(args, torch, P, S, Nc, ex["damp"], pre, train, topk, sws, tv, ti)
     if args.vendor_gemm:
         # the same operands through torch's library GEMM (hipBLASLt) and through this
         # library's scores-only path, on a 125,000-row slice (context for the roofline)
@@ -342,6 +346,37 @@ def influence_leg(args, torch, P):
     return res, sample
 
 
+def relatif_sub_leg(args, torch, P, S, Nc, damp, pre, train, topk, sws, tv, ti):
+    """l-RelatIF on the same store: the self-influence of every train row
+    (once per store: sum over blocks of g^T (C + lambda I)^{-1} g, two bf16
+    MFMA products with the split inverse factor), then the score pass with the
+    1/sqrt(self) column scales applied before the top-k."""
+    N = train.shape[0]
+    nb, D, _ = S.shape
+    rsq = torch.empty(N, dtype=torch.float32, device=train.device)
+    iws = torch.empty(P.logra_self_influence_ws_size(D, nb), dtype=torch.uint8, device=train.device)
+    self_t, scaled_t = EventTimer(torch), EventTimer(torch)
+    log("[inf] l-RelatIF: self-influence of the store, scaled score passes")
+    for timed in [False] + [True] * args.inf_passes:
+        e0 = self_t.start() if timed else None
+        P.logra_self_influence_blocks(S, Nc, damp, train, rsqrt_out=rsq, ws=iws)   # synchronous
+        if timed:
+            self_t.stop(e0)
+        e0 = scaled_t.start() if timed else None
+        P.logra_influence_scores(pre, train, scores=None, topk=topk, topk_val=tv, topk_idx=ti, ws=sws,
+                                 col_scale=rsq)
+        if timed:
+            scaled_t.stop(e0)
+    torch.cuda.synchronize()
+    flops = 4.0 * N * nb * D * D
+    tf = flops / (self_t.mean_ms() * 1e-3) / 1e12
+    return {"self_influence_ms": self_t.mean_ms(), "self_influence_tflops": tf,
+            "self_influence_frac": tf / BF16_PEAK_TFLOPS, "self_influence_flops": flops,
+            "scaled_scores_topk_ms": scaled_t.mean_ms(),
+            "note": "self-influence runs once per store; each query batch pays the preconditioner and "
+                    "the scaled score pass"}
+
+
 def cpu_influence_baseline(sample):
     import oracle
     D = sample["D"]
@@ -369,6 +404,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--leg", choices=["all", "log", "influence"], default="all")
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--no-relatif", dest="relatif", action="store_false",
+                    help="skip the l-RelatIF sub-leg (self-influence + scaled scores)")
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="also time torch.matmul (hipBLASLt) on the score GEMM's operands")
     ap.add_argument("--cpu-batches", type=int, default=2, help="logging batches in the oracle sample")

@@ -11,7 +11,9 @@ on outputs the float64 oracle can compute one by one:
   sampled blocks;
 - the score pass of 1,024 x 500,000 at 57,344 dims with top-100 (the
   filtered selection path): sampled scores, and the top-100 of sampled
-  queries checked against their full score rows.
+  queries checked against their full score rows;
+- l-RelatIF on the same store: the self-influence of all 500,000 rows
+  (sampled rows), and the scaled score pass with top-100.
 
 Inputs are drawn on the device with the same generators bench.py uses; the
 oracle gets host copies of the raw inputs, never a result of the HIP path.
@@ -123,7 +125,29 @@ def test_precondition_blocks_bench_launch():
         assert err <= 2e-2
 
 
-def test_scores_topk_bench_launch():
+@pytest.fixture(scope="module")
+def score_store():
+    """The 500,000-row train store and 1,024 test gradients of the scoring
+    workload (drawn once for the tests below)."""
+    import torch
+    from gpu_util import say
+    w = W.WORKLOADS["llama3_8b_scores"]
+    ex = w.extra
+    N, Q = ex["N_train"], ex["Q"]
+    D = w.n_layers * w.D
+    say(f"[full store] drawing {N} x {D} train and {Q} test gradients")
+    scales = W.block_scales(0, w.n_layers, ex["scale_lo"], ex["scale_hi"])
+    gen = W.torch_generator(0, 430)
+    train = torch.empty((N, D), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(train, scales, w.D, gen)
+    te = torch.empty((Q, D), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(te, scales, w.D, gen)
+    yield train, te, scales
+    del train, te
+    torch.cuda.empty_cache()
+
+
+def test_scores_topk_bench_launch(score_store):
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import f64, host, say
@@ -132,12 +156,7 @@ def test_scores_topk_bench_launch():
     N, Q, k = ex["N_train"], ex["Q"], ex["topk"]
     D = w.n_layers * w.D
     say(f"[full scores] {Q} x {N} at {D} dims, top-{k}")
-    scales = W.block_scales(0, w.n_layers, ex["scale_lo"], ex["scale_hi"])
-    gen = W.torch_generator(0, 430)
-    train = torch.empty((N, D), dtype=torch.bfloat16, device="cuda")
-    W.device_scaled_rows_(train, scales, w.D, gen)
-    te = torch.empty((Q, D), dtype=torch.bfloat16, device="cuda")
-    W.device_scaled_rows_(te, scales, w.D, gen)
+    train, te, _ = score_store
     tv = torch.empty((Q, k), dtype=torch.float32, device="cuda")
     ti = torch.empty((Q, k), dtype=torch.int64, device="cuda")
     P.logra_influence_scores(te, train, scores=None, topk=k, topk_val=tv, topk_idx=ti)   # bench's call
@@ -164,3 +183,59 @@ def test_scores_topk_bench_launch():
         order = np.lexsort((np.arange(N), -row.astype(np.float64)))[:k]
         assert np.array_equal(ti[q], order)
         assert np.array_equal(tv[q], row[order])
+
+
+def test_relatif_bench_launch(score_store):
+    """l-RelatIF at the benchmarked size: self-influence of all 500,000 store
+    rows over 224 blocks (sampled rows against the oracle), then the scaled
+    score pass with top-100 through the candidate filter: the top-100 of
+    sampled queries equals the top-100 of their full scaled score rows, and
+    sampled scaled scores match the oracle's normalised scores."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import f64, host, say
+    w = W.WORKLOADS["llama3_8b_scores"]
+    ex = w.extra
+    nb, Db, N, Q, k, Nc = w.n_layers, w.D, ex["N_train"], ex["Q"], ex["topk"], ex["N_cov"]
+    train, te, scales = score_store
+    say(f"[full l-RelatIF] self-influence of {N} rows over {nb} blocks of {Db}, scaled top-{k}")
+    gen = W.torch_generator(0, 440)
+    covg = torch.empty((Nc, nb * Db), dtype=torch.bfloat16, device="cuda")
+    W.device_scaled_rows_(covg, scales, Db, gen)
+    S = torch.zeros((nb, Db, Db), dtype=torch.float32, device="cuda")
+    P.logra_cov_accumulate_blocks(covg, S, Db)
+    self_tr = torch.empty(N, dtype=torch.float32, device="cuda")
+    rsq = torch.empty(N, dtype=torch.float32, device="cuda")
+    P.logra_self_influence_blocks(S, Nc, ex["damp"], train, self_out=self_tr, rsqrt_out=rsq)
+    tv = torch.empty((Q, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((Q, k), dtype=torch.int64, device="cuda")
+    P.logra_influence_scores(te, train, topk=k, topk_val=tv, topk_idx=ti, col_scale=rsq)   # bench's call
+    s_full = torch.empty((Q, N), dtype=torch.float32, device="cuda")
+    P.logra_influence_scores(te, train, scores=s_full, topk=0, col_scale=rsq)
+    torch.cuda.synchronize()
+    say("  GPU passes done")
+    S_h = host(S).astype(np.float64)
+    g = W.rng(0, 441)
+    rows = np.unique(np.concatenate([[0, N - 1], g.integers(0, N, size=6)]))
+    tr_rows = host(train[torch.from_numpy(rows).cuda()].contiguous())
+    want_self = oracle.self_influence_blocks(S_h, Nc, ex["damp"], tr_rows)
+    got_self = host(self_tr)[rows]
+    err = float(np.max(np.abs(f64(got_self) - want_self) / want_self))
+    say(f"  self-influence of {len(rows)} sampled rows: max relative err {err:.2e}")
+    assert err <= 1e-4
+    tv, ti = host(tv), host(ti)
+    queries = [0, 1023] + list(g.integers(0, Q, size=3))
+    js = np.unique(np.concatenate([g.integers(0, N, size=8)] + [ti[q, :4] for q in queries]))
+    tr_h = host(train[torch.from_numpy(js).cuda()].contiguous())
+    self_js = oracle.self_influence_blocks(S_h, Nc, ex["damp"], tr_h)
+    te_h = host(te[queries].contiguous())
+    want = oracle.normalise_scores(oracle.scores(te_h, tr_h), self_js)
+    for qi, q in enumerate(queries):
+        row = host(s_full[q])
+        order = np.lexsort((np.arange(N), -row.astype(np.float64)))[:k]
+        assert np.array_equal(ti[q], order)
+        assert np.array_equal(tv[q], row[order])
+        bound = np.linalg.norm(f64(te_h[qi])) * np.linalg.norm(f64(tr_h), axis=1) / np.sqrt(self_js)
+        err = float(np.max(np.abs(row[js].astype(np.float64) - want[qi]) / bound))
+        say(f"  query {q}: normalised err on {len(js)} sampled scaled scores {err:.2e}")
+        assert err <= 1e-3
