@@ -19,8 +19,9 @@
 // buffers (80-byte rows, conflict-free fragment reads); 4 waves, each owning
 // 128 gradients x 128 outputs as 4 x 4 blocks of 32x32x16 MFMAs.  After the
 // last slab of a pass the squares of the outputs are summed over the wave's
-// columns (registers, then lane shuffles) into the gradients' running sums;
-// at the end the two wave halves are added through LDS, in a fixed order.
+// columns (registers, then DPP lane permutations inside rows of 16 lanes)
+// into the gradients' running sums; at the end the partial sums are added
+// through LDS, in a fixed order.
 #include "common.h"
 #include "internal.h"
 
@@ -33,6 +34,17 @@ constexpr int SK = 32;                     // contraction columns per slab
 constexpr int SLD = SK + 8;                // padded LDS row (bf16): 80 bytes
 constexpr int STH = 256;                   // threads
 constexpr int SL = SR * SK / 8 / STH;      // 128-bit loads per operand and thread per slab (4)
+
+// DPP lane permutations within rows of 16 lanes (dpp_ctrl encodings)
+constexpr int kDppXor1 = 0xB1;             // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;             // quad_perm [2, 3, 0, 1]
+constexpr int kDppRowHalfMirror = 0x141;   // lane i <-> 7 - i within 8
+constexpr int kDppRowMirror = 0x140;       // lane i <-> 15 - i within 16
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
+}
 
 struct Slab3 {
     u32x4 a[SL], h[SL], l[SL];
@@ -47,7 +59,7 @@ __global__ __launch_bounds__(STH, 1) void k_self_influence(const bf16_bits *__re
     __shared__ __attribute__((aligned(16))) bf16_bits As[2][SR * SLD];
     __shared__ __attribute__((aligned(16))) bf16_bits Hs[2][SO * SLD];
     __shared__ __attribute__((aligned(16))) bf16_bits Ls[2][SO * SLD];
-    __shared__ float rowsum[2][SR];
+    __shared__ float rowsum[2][2][SR];
 
     const int64_t r0 = static_cast<int64_t>(blockIdx.x) * SR;
     const int nrows = rows - r0 < SR ? static_cast<int>(rows - r0) : SR;
@@ -106,9 +118,11 @@ __global__ __launch_bounds__(STH, 1) void k_self_influence(const bf16_bits *__re
     };
 
     f32x16 acc[4][4];
-    // Row sums are kept reduced: entry e = 16 i + r of the 64 (i, r) result
-    // rows of a half-wave belongs to lane e % 32 of that half, slot e / 32.
-    float psum[2] = {0.f, 0.f};
+    // Row sums are kept reduced over the 16 lanes of each DPP row: after a
+    // fold, lane l holds in psum[s] the partial sum of result row entry
+    // e = 4 (l % 16) + s of its half-wave (e = 16 i + r for block i, register
+    // r); lanes l and l ^ 16 hold the two halves of the same rows' sums.
+    float psum[4] = {0.f, 0.f, 0.f, 0.f};
     auto zero_acc = [&]() {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -145,23 +159,34 @@ __global__ __launch_bounds__(STH, 1) void k_self_influence(const bf16_bits *__re
             __builtin_amdgcn_sched_barrier(0);   // one step's fragments live at a time
         }
     };
-    // after the last slab of an output pass: add the squared outputs, summed
-    // over the lane's columns, then over the 32 lanes of the half-wave (all
-    // columns of the pass), into the owning lane's slot
+    // After the last slab of an output pass: the squared outputs, summed over
+    // the lane's four column blocks, then reduce-scattered over the 16 lanes
+    // of each DPP row in four halvings (partners l ^ 15, l ^ 7, l ^ 2, l ^ 1,
+    // all within the row; each lane keeps the half selected by the bit in
+    // which it differs from its partner), so each lane ends with 4 of the 64
+    // row entries summed over the row's 16 columns.
+    const bool b3 = lane & 8, b2 = lane & 4, b1 = lane & 2, b0 = lane & 1;
+    auto sq = [&](int e) {
+        const int i = e >> 4, r = e & 15;
+        float v = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v = __builtin_fmaf(acc[i][j][r], acc[i][j][r], v);
+        return v;
+    };
     auto fold = [&]() {
+        float u[32], w[16], x[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int k = 0; k < 32; ++k) {
+            const float lo = sq(k), hi = sq(32 + k);
+            u[k] = (b3 ? hi : lo) + dpp_f<kDppRowMirror>(b3 ? lo : hi);
+        }
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float v = 0.f;
+        for (int k = 0; k < 16; ++k)
+            w[k] = (b2 ? u[16 + k] : u[k]) + dpp_f<kDppRowHalfMirror>(b2 ? u[k] : u[16 + k]);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) v = __builtin_fmaf(acc[i][j][r], acc[i][j][r], v);
+        for (int k = 0; k < 8; ++k) x[k] = (b1 ? w[8 + k] : w[k]) + dpp_f<kDppXor2>(b1 ? w[k] : w[8 + k]);
 #pragma unroll
-                for (int o = 16; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-                const int e = 16 * i + r;
-                if ((lane & 31) == (e & 31)) psum[e >> 5] += v;
-                __builtin_amdgcn_sched_barrier(0);   // one row at a time: short live ranges
-            }
+        for (int k = 0; k < 4; ++k) psum[k] += (b0 ? x[4 + k] : x[k]) + dpp_f<kDppXor1>(b0 ? x[k] : x[4 + k]);
         zero_acc();
     };
 
@@ -187,15 +212,17 @@ __global__ __launch_bounds__(STH, 1) void k_self_influence(const bf16_bits *__re
             fold();
         }
 
-    // combine the two wave halves wn = 0, 1 (in that order) through LDS
+    // combine the partial row sums -- two column halves (waves wn = 0, 1) x
+    // the two 16-lane rows of each half-wave -- through LDS, in a fixed order
+    const int h16 = (lane >> 4) & 1;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int e = 32 * h + (lane & 31), i = e >> 4, r = e & 15;
-        rowsum[wn][wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)] = psum[h];
+    for (int k = 0; k < 4; ++k) {
+        const int e = 4 * (lane & 15) + k, i = e >> 4, r = e & 15;
+        rowsum[wn][h16][wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)] = psum[k];
     }
     __syncthreads();
     if (tid < nrows) {
-        const float sv = rowsum[0][tid] + rowsum[1][tid];
+        const float sv = (rowsum[0][0][tid] + rowsum[0][1][tid]) + (rowsum[1][0][tid] + rowsum[1][1][tid]);
         if (self_out) self_out[r0 + tid] = sv;
         if (rsqrt_out) rsqrt_out[r0 + tid] = sv > 0.f ? 1.0f / sqrtf(sv) : 0.f;
     }
