@@ -389,7 +389,8 @@ int logra_self_influence_blocks(const float *S, int D, int n_blocks, int64_t N, 
     TRY(check_ws(ws, ws_bytes, logra_self_influence_ws_size(D, n_blocks)));
     TRY(check_dev(g, "g", bf16 ? 16 : 4));
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = logra::launch_inverse_factor(S, D, n_blocks, N, damp_ratio, ws, s);
+    hipError_t e = logra::launch_inverse_factor(S, D, n_blocks, N, damp_ratio,
+                                                 logra::self_influence_interleaved(bf16, D), ws, s);
     if (e != hipSuccess) return hip_fail(e, "factor launch");
     e = logra::launch_self_influence(g, bf16, ld, rows, D, n_blocks, ws, self_out, rsqrt_out, s);
     if (e != hipSuccess) return hip_fail(e, "self-influence launch");

@@ -52,6 +52,24 @@ __device__ __forceinline__ u32x4 buf_ld128_nt(__amdgpu_buffer_rsrc_t r, uint32_t
     return __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 2);
 }
 
+// gfx950 asynchronous copy: 16 bytes per lane from buffer offset `voff`
+// straight into LDS at byte address lds + 16 * lane (lds is wave-uniform);
+// offsets at or past the buffer's range store zeros.  The load reads M0 one
+// wait state after the scalar write (s_nop 0), as the hardware requires.  It
+// is tracked by vmcnt, which the callers wait on explicitly (s_waitcnt in
+// inline asm): the compiler does not see this load.
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r) : "memory");
+}
+
+// 32-bit LDS byte address of a __shared__ object (the address-space cast
+// yields the offset within the workgroup's LDS allocation).
+template <typename T>
+__device__ __forceinline__ uint32_t lds_addr(T *p) {
+    return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) T *)p));
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
     return __builtin_bit_cast(bf16x8, v);
 }

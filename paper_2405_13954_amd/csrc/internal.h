@@ -51,11 +51,17 @@ hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int ro
 // Self-influence (l-RelatIF's normaliser): per block, W = L^{-1} of the
 // damped covariance's Cholesky factor (identity when damp_ratio < 0), kept as
 // bf16 hi + lo halves in the workspace after the preconditioner's layout;
-// then self_j = sum over blocks of |W_l g_jl|^2.
+// then self_j = sum over blocks of |W_l g_jl|^2.  Rows of W are padded with
+// zeros to Dp = D rounded up to 256.  Two layouts of the halves:
+//  - split: hi [n_blocks][Dp][D], then lo likewise (self_influence_w);
+//  - interleaved (bf16 gradients with D a multiple of 64): one array
+//    [n_blocks][Dp][2D] at self_influence_w(.., false) whose row o holds,
+//    for each 64-column chunk c, hi of the chunk then lo of the chunk.
+inline bool self_influence_interleaved(bool bf16, int D) { return bf16 && D % 64 == 0; }
 size_t self_influence_ws_bytes(int D, int n_blocks);
 bf16_bits_t *self_influence_w(void *ws, int D, int n_blocks, bool lo);
 hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
-                                 void *ws, hipStream_t s);
+                                 bool interleaved, void *ws, hipStream_t s);
 hipError_t launch_self_influence(const void *g, bool bf16, int64_t ld, int64_t rows, int D, int n_blocks,
                                  const void *ws, float *self_out, float *rsqrt_out, hipStream_t s);
 

@@ -368,24 +368,26 @@ __global__ __launch_bounds__(256) void k_clear_info(int *info, int n) {
 
 // W = L^{-1} (fp64, rows d, columns q of the forward solution) as two bf16
 // arrays whose sum carries about 16 significant bits: hi = RNE(W), lo =
-// RNE(W - hi).  Row-major [blk][Dp][D] with Dp = D rounded up to 256; rows
-// past D are zero.  With `ident`, W = I.
+// RNE(W - hi); rows d past D (up to Dp = gridDim.x) are zero.  Split layout:
+// hi [blk][Dp][D] then lo; interleaved: [blk][Dp][2D], the 64 columns of
+// chunk c at 128 c (hi) and 128 c + 64 (lo).  With `ident`, W = I.
 __global__ __launch_bounds__(256) void k_split_w(const double *Y_all, int D, int Qp, bool ident,
-                                                  bf16_bits *w_hi, bf16_bits *w_lo) {
+                                                  bool interleaved, bf16_bits *w_hi, bf16_bits *w_lo) {
     const int blk = blockIdx.y, d = blockIdx.x;
-    const int Dp = gridDim.x;
-    bf16_bits *h = w_hi + (static_cast<size_t>(blk) * Dp + d) * D;
-    bf16_bits *l = w_lo + (static_cast<size_t>(blk) * Dp + d) * D;
-    if (d >= D) {
-        for (int q = threadIdx.x; q < D; q += 256) h[q] = l[q] = 0;
-        return;
-    }
-    const double *Y = Y_all + static_cast<size_t>(blk) * D * Qp + static_cast<size_t>(d) * Qp;
+    const size_t row = static_cast<size_t>(blk) * gridDim.x + d;
+    bf16_bits *h = interleaved ? w_hi + row * 2 * D : w_hi + row * D;
+    bf16_bits *l = interleaved ? h + 64 : w_lo + row * D;
     for (int q = threadIdx.x; q < D; q += 256) {
-        const float v = ident ? (q == d ? 1.f : 0.f) : static_cast<float>(Y[q]);
-        const bf16_bits hb = f32_to_bf16_rne(v);
-        h[q] = hb;
-        l[q] = ident ? bf16_bits{0} : f32_to_bf16_rne(static_cast<float>(Y[q] - static_cast<double>(bf16_to_f32(hb))));
+        const int at = interleaved ? q + (q & ~63) : q;   // 128 (q / 64) + q % 64
+        if (d >= D) {
+            h[at] = l[at] = 0;
+            continue;
+        }
+        const double y = ident ? (q == d ? 1.0 : 0.0)
+                               : Y_all[static_cast<size_t>(blk) * D * Qp + static_cast<size_t>(d) * Qp + q];
+        const bf16_bits hb = f32_to_bf16_rne(static_cast<float>(y));
+        h[at] = hb;
+        l[at] = f32_to_bf16_rne(static_cast<float>(y - static_cast<double>(bf16_to_f32(hb))));
     }
 }
 
@@ -475,7 +477,7 @@ hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, d
 }
 
 hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
-                                 void *ws, hipStream_t s) {
+                                 bool interleaved, void *ws, hipStream_t s) {
     const WsLayout w = ws_layout(ws, D, n_blocks, D);
     bf16_bits *hi = self_influence_w(ws, D, n_blocks, false), *lo = self_influence_w(ws, D, n_blocks, true);
     const bool ident = damp_ratio < 0;
@@ -493,7 +495,7 @@ hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N,
         hipLaunchKernelGGL(k_clear_info, dim3(1), dim3(256), 0, s, w.info, n_blocks);
     }
     hipLaunchKernelGGL(k_split_w, dim3((D + 255) / 256 * 256, n_blocks), dim3(256), 0, s, w.Y, D, padded_q(D),
-                       ident, hi, lo);
+                       ident, interleaved, hi, lo);
     return hipGetLastError();
 }
 

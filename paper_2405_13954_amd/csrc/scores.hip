@@ -273,16 +273,6 @@ constexpr int kLdsB = kStagesA * kSlabOp;    // B stages follow the A stages
 constexpr int kLdsBytes = (kStagesA + kStagesB) * kSlabOp;
 constexpr int kCopies = kSlabOp / 1024 / 4;  // 1 KB copies per wave and operand per slab (8)
 
-// 16 bytes per lane from buffer offset `voff` to LDS address m0 + 16 * lane;
-// offsets at or past the buffer's range store zeros.  The load reads M0 one
-// wait state after the scalar write (s_nop 0), as the hardware requires.  It
-// is tracked by vmcnt, which the callers wait on explicitly: the compiler
-// does not see this load.
-__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :: "s"(lds), "v"(voff), "s"(r) : "memory");
-}
-
 __global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restrict__ te, int64_t ld_te,
                                                       int Q, const bf16_bits *__restrict__ tr,
                                                       int64_t ld_tr, int64_t N, int D,
