@@ -45,22 +45,94 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
+PROJ_SOURCES = ["paper_2405_13954_amd/csrc/project.hip", "paper_2405_13954_amd/csrc/common.h"]
+SCORE_SOURCES = ["paper_2405_13954_amd/csrc/scores.hip", "paper_2405_13954_amd/csrc/common.h"]
+SELF_SOURCES = ["paper_2405_13954_amd/csrc/selfinf.hip", "paper_2405_13954_amd/csrc/common.h"]
+
+
+def source_sha(sources):
+    import hashlib
+    h = hashlib.sha256()
+    for f in sources:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
 def measured_traffic(key, sources):
     """HBM bytes per launch of a kernel from the committed counter summary
     (profiles/traffic.json), or None when the kernel's sources changed since
     the counters were taken."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
-        rec = json.load(open(path))[key]
+        rec = json.load(open(TRAFFIC_PATH))[key]
     except (OSError, KeyError, ValueError):
         return None, None
-    h = hashlib.sha256()
-    for f in sources:
-        h.update(open(os.path.join(ROOT, f), "rb").read())
-    if h.hexdigest()[:16] != rec.get("source_sha"):
+    if source_sha(sources) != rec.get("source_sha"):
         return None, None
     return rec["traffic_bytes"], rec["traffic_over_algorithmic"]
+
+
+def write_traffic(fetch_csv, write_csv):
+    """profiles/traffic.json from the counter files of two runs
+    `rocprofv3 --pmc FETCH_SIZE` and `rocprofv3 --pmc WRITE_SIZE` (csv) of
+    `bench.py --no-cpu-baseline --steps 3 --warmup 1 --inf-passes 1`.  Per
+    kernel, the launches with the largest grid are averaged (the full-size
+    launches: the scores-only GEMM over all 500,000 rows, the self-influence
+    of the store).  Reads = 2 x FETCH_SIZE and writes = 1 x WRITE_SIZE (KiB):
+    the factors a plain copy of 1 GiB shows (524,288 KiB fetched, 1,048,576
+    KiB written)."""
+    import collections
+    import csv
+    import re
+
+    def load(path, ctr):
+        d = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] == ctr and "logra" in r["Kernel_Name"]:
+                n = re.sub(r"\(.*", "", r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("void ", ""))
+                d[n].append((int(r["Grid_Size"]), float(r["Counter_Value"])))
+        out = {}
+        for n, v in d.items():
+            gmax = max(g for g, _ in v)
+            vals = [x for g, x in v if g == gmax]
+            out[n] = sum(vals) / len(vals)
+        return out
+
+    f, w = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+    stream = W.WORKLOADS["llama3_8b_stream"]
+    lens = [W.lengths(W.rng(0, 200, s), stream.B, stream.len_lo, stream.len_hi) for s in range(4)]
+    per_tok = sum(2 * (a + b) for _, a, b in stream.layers)
+    p_bytes = sum(2 * stream.k_in * (a + b) for _, a, b in stream.layers)
+    sc = W.WORKLOADS["llama3_8b_scores"]
+    N, Q, D_tot = sc.extra["N_train"], sc.extra["Q"], sc.n_layers * sc.D
+    rows = {
+        "projection": ("logra::k_project_chunks<1, unsigned short>", "k_project_chunks<1, bf16>",
+                       "7 Llama3-8B layers, B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
+                       sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes),
+        "scores": ("logra::k_scores_dma", "k_scores_dma", "1,024 x 500,000 x 57,344 bf16", SCORE_SOURCES,
+                   (N + Q) * D_tot * 2 + Q * N * 4),
+        "self_influence": ("logra::k_self_influence_dma", "k_self_influence_dma",
+                           "500,000 x 57,344 bf16, 224 blocks of 256", SELF_SOURCES,
+                           N * D_tot * 2 + sc.n_layers * sc.D * 2 * sc.D * 2 + N * 4),
+    }
+    out = {"_about": "HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs of "
+                     "bench.py (--no-cpu-baseline --steps 3 --warmup 1 --inf-passes 1), written by "
+                     "`python bench.py --write-traffic <FETCH_SIZE csv> <WRITE_SIZE csv>`. Read bytes = "
+                     "2 x FETCH_SIZE (KiB x 1024): a plain copy of 1 GiB reads 524,288 KiB of FETCH_SIZE and "
+                     "writes 1,048,576 KiB of WRITE_SIZE, so reads are scaled by 2 and writes by 1. source_sha "
+                     "covers the kernel's source files; bench.py reports traffic only while it matches."}
+    for key, (name, kernel, workload, sources, alg) in rows.items():
+        if name not in f or name not in w:
+            continue
+        rec = {"kernel": kernel, "workload": workload, "source_sha": source_sha(sources),
+               "read_bytes": 2 * f[name] * 1024, "write_bytes": w[name] * 1024, "algorithmic_bytes": alg}
+        rec["traffic_bytes"] = rec["read_bytes"] + rec["write_bytes"]
+        rec["traffic_over_algorithmic"] = rec["traffic_bytes"] / alg
+        out[key] = rec
+    with open(TRAFFIC_PATH, "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(out, indent=1))
 
 
 class EventTimer:
@@ -183,8 +255,7 @@ def logging_leg(args, torch, P):
     bytes_per_launch = tokens / args.steps * per_tok + proj_bytes
     proj_ms = proj_timer.mean_ms()
     achieved = bytes_per_launch / (proj_ms * 1e-3) / 1e9
-    traffic, ratio = measured_traffic("projection", ["paper_2405_13954_amd/csrc/project.hip",
-                                                     "paper_2405_13954_amd/csrc/common.h"])
+    traffic, ratio = measured_traffic("projection", PROJ_SOURCES)
     res = {
         "tokens": tokens, "seconds": dt,
         "tokens_per_s": tokens / dt, "examples_per_s": examples / dt,
@@ -298,8 +369,7 @@ def influence_leg(args, torch, P):
     torch.cuda.synchronize()
     gemm_ms = only.mean_ms()
     achieved = flops / (gemm_ms * 1e-3) / 1e12
-    traffic, ratio = measured_traffic("scores", ["paper_2405_13954_amd/csrc/scores.hip",
-                                                 "paper_2405_13954_amd/csrc/common.h"])
+    traffic, ratio = measured_traffic("scores", SCORE_SOURCES)
     res = {
         "metric": "influence scores/sec (1,024 x 500,000 at 57,344 dims, top-100)",
         "value": Q * N / dt, "unit": "scores/s", "ms_per_pass": dt * 1e3,
@@ -370,11 +440,14 @@ def relatif_sub_leg(args, torch, P, S, Nc, damp, pre, train, topk, sws, tv, ti):
     torch.cuda.synchronize()
     flops = 4.0 * N * nb * D * D
     tf = flops / (self_t.mean_ms() * 1e-3) / 1e12
-    return {"self_influence_ms": self_t.mean_ms(), "self_influence_tflops": tf,
-            "self_influence_frac": tf / BF16_PEAK_TFLOPS, "self_influence_flops": flops,
-            "scaled_scores_topk_ms": scaled_t.mean_ms(),
-            "note": "self-influence runs once per store; each query batch pays the preconditioner and "
-                    "the scaled score pass"}
+    traffic, ratio = measured_traffic("self_influence", SELF_SOURCES)
+    return {"self_influence_ms": self_t.mean_ms(), "scaled_scores_topk_ms": scaled_t.mean_ms(),
+            "roofline": {"bound": "mfma", "achieved": tf, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": tf / BF16_PEAK_TFLOPS, "traffic": traffic, "traffic_over_algorithmic": ratio,
+                         "kernel": "self-influence call (inverse factor + bf16 MFMA products)",
+                         "flops_per_launch": flops},
+            "note": "self-influence runs once per store (timed over the whole call, factorisation "
+                    "included); each query batch pays the preconditioner and the scaled score pass"}
 
 
 def cpu_influence_baseline(sample):
@@ -412,7 +485,13 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time bound of the logging sample")
     ap.add_argument("--cpu-queries", type=int, default=256, help="test gradients in the oracle sample")
     ap.add_argument("--cpu-train-rows", type=int, default=20000, help="stored gradients in the oracle sample")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic.json from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter "
+                         "files of this benchmark, and exit (no GPU needed)")
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(*args.write_traffic)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md on sharding)",
               file=sys.stderr)
