@@ -266,6 +266,7 @@ def logging_leg(args, torch, P):
                      "kernel": "logra_project_layers (7 Llama3-8B layers, B=8 ragged, k=16)",
                      "bytes_per_launch": bytes_per_launch},
     }
+    res["roofline"]["copy_gbs"] = copy_bandwidth(torch)
     sample = None
     if args.cpu_baseline:
         n_b = min(args.cpu_batches, n_buf)
@@ -278,6 +279,25 @@ def logging_leg(args, torch, P):
     del bufs, store, S, ws
     torch.cuda.empty_cache()
     return res, sample
+
+
+def copy_bandwidth(torch, nbytes=2 << 30, reps=5):
+    """HBM bytes moved per second (read + write) by torch's device-to-device
+    copy of `nbytes` (2 GiB, far above the 256 MB MALL): a measured reference
+    for what a plain streaming kernel reaches on this GPU, next to the
+    published peak."""
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").normal_()
+    dst = torch.empty_like(src)
+    t = EventTimer(torch)
+    dst.copy_(src)
+    for _ in range(reps):
+        e0 = t.start()
+        dst.copy_(src)
+        t.stop(e0)
+    torch.cuda.synchronize()
+    gbs = 2 * nbytes / (t.mean_ms() * 1e-3) / 1e9
+    del src, dst
+    return gbs
 
 
 def host_bf16(t):

@@ -1,9 +1,13 @@
 """Parity at the full sizes and launch configurations that bench.py times,
-on outputs the float64 oracle can compute one by one:
+and at the full sizes of the two other logging workloads, on outputs the
+float64 oracle can compute one by one:
 
 - the grouped projection of one Llama3-8B block (7 layers, B=8, T=2048,
   lengths U{128..2048}, k=16, bf16 store rows of 57,344) on three sampled
   layers, all examples;
+- GPT-2-small logging (48 layers, B=32, T=512, ragged) and one Llama3-8B
+  block at k = 64 (B=16, T=1024, 4096 x 4096 covariances): sampled layers
+  and covariance blocks;
 - the 224-block covariance update from one batch of store rows, on sampled
   blocks;
 - the damped preconditioner of 224 blocks of 256 (covariances from 4,096
@@ -73,6 +77,84 @@ def test_project_llama_block_bench_launch():
             errs = [normwise(got[b], want[b]) for b in range(B)]
             say(f"  {name} ({ni}->{no}) {str(gdt)[6:]}: max normwise err {max(errs):.2e}")
             assert max(errs) <= tol
+
+
+def test_gpt2_small_logging_full():
+    """GPT-2-small logging at its full size: 12 blocks x {qkv, out, fc, proj},
+    B=32, T=512, lengths U{64..512}, k=16, one grouped launch per block into
+    a bf16 store of 48 x 256 columns, then the 48 covariance blocks from the
+    store rows.  Sampled layers (all 32 examples) and covariance blocks
+    against the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, normwise, say
+    w = W.WORKLOADS["gpt2_small_log"]
+    B, T, k = w.B, w.T, w.k_in
+    D, nl = k * k, len(w.layers)
+    lens = W.lengths(W.rng(0, 500, 0), B, w.len_lo, w.len_hi)
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = torch.from_numpy(mask_np).cuda()
+    say(f"[full gpt2-small] {w.blocks} blocks x {nl} layers, B={B} T={T} k={k}, {int(lens.sum())} valid tokens")
+    store = torch.empty((B, w.blocks * nl * D), dtype=torch.bfloat16, device="cuda")
+    sampled = {(0, 0), (0, 3), (5, 2), (11, 1)}           # (block, layer)
+    kept = {}
+    for blk in range(w.blocks):
+        gen = W.torch_generator(0, 510, blk)
+        tensors = [_layer_inputs(torch, gen, B, T, ni, no, k, w) for _, ni, no in w.layers]
+        layers = [dict(x=x, dy=dy, p_in=pi, p_out=po, g_out=store[:, (blk * nl + j) * D:(blk * nl + j + 1) * D])
+                  for j, (x, dy, pi, po) in enumerate(tensors)]
+        P.logra_project_layers(layers, mask=mask)
+        for j in range(nl):
+            if (blk, j) in sampled:
+                kept[(blk, j)] = [host(t) for t in tensors[j]]
+        del tensors, layers
+    S = torch.zeros((w.blocks * nl, D, D), dtype=torch.float32, device="cuda")
+    P.logra_cov_accumulate_blocks(store, S, D)
+    torch.cuda.synchronize()
+    got, S_h = host(store), host(S)
+    for (blk, j), (x, dy, pi, po) in sorted(kept.items()):
+        want = oracle.project_factored(x, dy, pi, po, mask_np)
+        c = (blk * nl + j) * D
+        err = max(normwise(got[b, c:c + D], want[b]) for b in range(B))
+        say(f"  block {blk} {w.layers[j][0]}: max normwise err {err:.2e}")
+        assert err <= 2e-2
+    for l in (0, 21, 47):
+        err = normwise(S_h[l], oracle.cov_accumulate(got[:, l * D:(l + 1) * D]))
+        say(f"  covariance block {l}: normwise err {err:.2e}")
+        assert err <= 1e-5
+
+
+def test_llama_block_k64_full():
+    """One Llama3-8B block at k = 64 at its full size: 7 layers, B=16,
+    T=1024 all valid, fp32 G of 4,096 per layer, and the seven 4096 x 4096
+    covariances.  Three layers (all examples) and their covariances against
+    the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, normwise, say
+    w = W.WORKLOADS["llama3_8b_block"]
+    B, T, k = w.B, w.T, w.k_in
+    D, nl = k * k, len(w.layers)
+    say(f"[full llama block k=64] {nl} layers, B={B} T={T}, D={D} per layer")
+    gen = W.torch_generator(0, 520)
+    tensors = [_layer_inputs(torch, gen, B, T, ni, no, k, w) for _, ni, no in w.layers]
+    store = torch.empty((B, nl * D), dtype=torch.float32, device="cuda")
+    layers = [dict(x=x, dy=dy, p_in=pi, p_out=po, g_out=store[:, j * D:(j + 1) * D])
+              for j, (x, dy, pi, po) in enumerate(tensors)]
+    P.logra_project_layers(layers)                     # no mask: every token valid
+    S = torch.zeros((nl, D, D), dtype=torch.float32, device="cuda")
+    P.logra_cov_accumulate_blocks(store, S, D)
+    torch.cuda.synchronize()
+    got = host(store)
+    for j in (2, 5, 6):   # v (4096->1024), up (4096->14336), down (14336->4096)
+        x, dy, pi, po = (host(t) for t in tensors[j])
+        want = oracle.project_factored(x, dy, pi, po)
+        err = max(normwise(got[b, j * D:(j + 1) * D], want[b]) for b in range(B))
+        say(f"  {w.layers[j][0]}: max normwise err {err:.2e}")
+        assert err <= 1e-3
+        err = normwise(host(S[j]), oracle.cov_accumulate(got[:, j * D:(j + 1) * D]))
+        say(f"  {w.layers[j][0]} covariance 4096 x 4096: normwise err {err:.2e}")
+        assert err <= 1e-5
 
 
 def test_cov_blocks_bench_launch():
