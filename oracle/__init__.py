@@ -2,7 +2,9 @@
 
 Thin numpy wrappers over ``logra_oracle.c``: a plain, slow float64
 implementation of what the LoGra hot path computes (arXiv 2405.13954,
-Sec. 2 Eq. (2)-(3), Sec. 3.1 Eq. (4)-(5), App. C and App. D).  Only the test
+Sec. 2 Eq. (2)-(3), Sec. 3.1 Eq. (4)-(5), Sec. 3.2 (the KFAC-eigenvector
+initialisation of the projections), Sec. 4.2 (l-RelatIF), App. C and App. D).
+The PCA step takes numpy's float64 eigh as its eigendecomposition.  Only the test
 suite, the smoke check and the benchmark's CPU-baseline leg may import this
 package; the product path never does, and this package imports nothing from
 it.
@@ -61,10 +63,11 @@ def lib():
         L.oracle_topk.argtypes = [vp, i64, i32, i64, i64, i32, vp, vp]
         L.oracle_self_influence.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp]
         L.oracle_normalise_scores.argtypes = [vp, i64, i32, i64, vp, vp]
+        L.oracle_act_cov.argtypes = [vp, i32, i32, i32, i32, vp, vp]
         L.oracle_num_threads.argtypes = []
         for name in ("oracle_project_factored", "oracle_project_dense", "oracle_cov_accumulate",
                      "oracle_precondition", "oracle_scores", "oracle_topk", "oracle_self_influence",
-                     "oracle_normalise_scores", "oracle_num_threads"):
+                     "oracle_normalise_scores", "oracle_act_cov", "oracle_num_threads"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -216,6 +219,40 @@ def normalise_scores(s, self_tr, self_te=None) -> np.ndarray:
     rc = lib().oracle_normalise_scores(_ptr(s), max(N, 1), Q, N, None if te is None else _ptr(te), _ptr(tr))
     _check(rc, "oracle_normalise_scores")
     return s
+
+
+def act_cov(a, mask=None, C=None) -> np.ndarray:
+    """KFAC factor of one layer (Sec. 3.2): C += sum over unmasked tokens of a_t a_t^T.
+    a: [B, T, n] (activations x for C_F, output gradients dy for C_B); returns [n, n] float64."""
+    a = _c(a)
+    B, T, n = a.shape
+    if mask is not None:
+        mask = np.ascontiguousarray(mask.astype(np.uint8, copy=False))
+        assert mask.shape == (B, T)
+    if C is None:
+        C = np.zeros((n, n), dtype=np.float64)
+    assert C.dtype == np.float64 and C.shape == (n, n) and C.flags.c_contiguous
+    rc = lib().oracle_act_cov(_ptr(a), _code(a), B, T, n, _ptr(mask), _ptr(C))
+    _check(rc, "oracle_act_cov")
+    return C
+
+
+def pca_topk(C, k: int):
+    """PCA initialisation of a projection (Sec. 3.2): the top-k eigenvectors of the symmetric
+    covariance C as the rows of P [k, n], by decreasing eigenvalue, each signed so that its entry
+    of largest magnitude (the lowest index among equal magnitudes) is positive.  The
+    eigendecomposition is numpy's float64 eigh.  Returns (P, eigenvalues [k])."""
+    C = np.asarray(C, dtype=np.float64)
+    n = C.shape[0]
+    assert C.shape == (n, n) and 1 <= k <= n
+    w, V = np.linalg.eigh(C)                 # ascending
+    order = np.argsort(-w, kind="stable")[:k]
+    P = V[:, order].T.copy()
+    for r in range(k):
+        i = int(np.argmax(np.abs(P[r])))     # first index of the largest magnitude
+        if P[r, i] < 0:
+            P[r] = -P[r]
+    return P, w[order]
 
 
 def num_threads() -> int:

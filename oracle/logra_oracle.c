@@ -315,6 +315,29 @@ int oracle_normalise_scores(double *s, int64_t ld_s, int Q, int64_t N, const dou
     return OR_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Uncentered activation covariance of one layer, the KFAC factor behind     */
+/* the PCA initialisation of the projections (Sec. 3.2: C_F from the forward */
+/* activations x, C_B from the backward output gradients Dx_o, H_KFAC =      */
+/* C_F (x) C_B; P_i and P_o are their top-k eigenvectors):                   */
+/*   C[i][j] += sum over unmasked (b, t) of a_bt[i] a_bt[j]                  */
+/* a: [B][T][n] of dtype a_dtype; mask: [B][T] or NULL (NULL = all tokens);  */
+/* a masked token is never read.  C: [n][n] doubles, accumulated in place.   */
+/* ------------------------------------------------------------------------ */
+int oracle_act_cov(const void *a, int a_dtype, int B, int T, int n, const uint8_t *mask, double *C) {
+    if (B < 0 || T < 0 || n <= 0 || !dtype_ok(a_dtype)) return OR_ERR_INVALID_ARG;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < n; ++i)
+        for (int b = 0; b < B; ++b)
+            for (int t = 0; t < T; ++t) {
+                int64_t bt = (int64_t)b * T + t;
+                if (mask && mask[bt] == 0) continue;
+                double ai = widen(a, a_dtype, bt * n + i);
+                for (int j = 0; j < n; ++j) C[(int64_t)i * n + j] += ai * widen(a, a_dtype, bt * n + j);
+            }
+    return OR_OK;
+}
+
 /* (value, index) a ranks before (value, index) b: larger value first, the   */
 /* lower train index on equal values.  Padding (index -1) ranks last.        */
 static int ranks_before(double va, int64_t ia, double vb, int64_t ib) {

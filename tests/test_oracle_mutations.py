@@ -36,6 +36,19 @@ MUTATIONS = {
                                      "const int rc = oracle_precondition(S, D, N, r > 0 ? 1e-12 : r, g, g_dtype, ld_g, rows, y, D, NULL);"),
     "normalise_without_sqrt": ("? s[(int64_t)q * ld_s + j] / sqrt(den) : 0.0;",
                                "? s[(int64_t)q * ld_s + j] / den : 0.0;"),
+    "act_cov_mask_ignored": ("if (mask && mask[bt] == 0) continue;\n                double ai",
+                             "double ai"),
+    "act_cov_skips_first_token": ("for (int t = 0; t < T; ++t) {\n                int64_t bt = (int64_t)b * T + t;\n                if (mask && mask[bt] == 0) continue;\n                double ai",
+                                  "for (int t = 1; t < T; ++t) {\n                int64_t bt = (int64_t)b * T + t;\n                if (mask && mask[bt] == 0) continue;\n                double ai"),
+}
+
+# Slips in the numpy part of the oracle (the PCA initialisation), planted in a
+# copy of the oracle package that the pin suite imports in place of the real one.
+PY_SRC = os.path.join(ROOT, "oracle", "__init__.py")
+PY_MUTATIONS = {
+    "pca_bottom_k": ('order = np.argsort(-w, kind="stable")[:k]', 'order = np.argsort(w, kind="stable")[:k]'),
+    "pca_columns_as_rows": ("P = V[:, order].T.copy()", "P = V[order, :].copy()"),
+    "pca_no_sign_rule": ("if P[r, i] < 0:", "if False:"),
 }
 
 
@@ -59,4 +72,27 @@ def test_pins_catch_mutation(name):
         r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
                             os.path.join(ROOT, "tests", "test_oracle_pins.py")],
                            env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
+        assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"
+
+
+@pytest.mark.parametrize("name", sorted(PY_MUTATIONS))
+def test_pins_catch_python_mutation(name):
+    old, new = PY_MUTATIONS[name]
+    src = open(PY_SRC).read()
+    assert old in src, f"mutation anchor not found: {name}"
+    with tempfile.TemporaryDirectory() as td:
+        pkg = os.path.join(td, "oracle")
+        os.makedirs(pkg)
+        open(os.path.join(pkg, "__init__.py"), "w").write(src.replace(old, new, 1))
+        driver = (
+            "import importlib.util, sys\n"
+            f"spec = importlib.util.spec_from_file_location('oracle', {os.path.join(pkg, '__init__.py')!r}, "
+            f"submodule_search_locations=[{pkg!r}])\n"
+            "m = importlib.util.module_from_spec(spec); sys.modules['oracle'] = m; spec.loader.exec_module(m)\n"
+            "import pytest\n"
+            f"sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', {os.path.join(ROOT, 'tests', 'test_oracle_pins.py')!r}]))\n")
+        import oracle
+        env = dict(os.environ, LOGRA_ORACLE_LIB=oracle.build(force=False))
+        r = subprocess.run([sys.executable, "-c", driver], env=env, cwd=ROOT, capture_output=True, text=True,
+                           timeout=300)
         assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"

@@ -396,3 +396,83 @@ def test_topk_padding_and_chunk_merge():
         ok = ci[q] >= 0
         order = np.lexsort((ci[q][ok], -cv[q][ok]))[:10]
         assert np.array_equal(ci[q][ok][order], full_i[q])
+
+
+# --------------------------------------------------------------------------
+# KFAC factors and the PCA initialisation of the projections (Sec. 3.2)
+# --------------------------------------------------------------------------
+def test_golden_kfac_pca_2x2():
+    e = json.load(open(GOLD))["kfac_pca_2x2"]
+    a = np.array([[float(v) for v in row] for row in e["a"]])[None]
+    C = oracle.act_cov(a, np.array([e["mask"]], np.uint8))
+    assert np.array_equal(C, np.array(e["C_F"], np.float64))
+    P, w = oracle.pca_topk(C, 2)
+    assert np.allclose(w, e["eigvals"], rtol=0, atol=1e-13)
+    assert np.allclose(P, e["P_top2"], rtol=0, atol=1e-15)
+    H = np.kron(C, np.array(e["C_B"], np.float64))
+    Pk, wk = oracle.pca_topk(H, 1)
+    assert abs(wk[0] - e["kfac_top_eigval"]) < 1e-12
+    assert np.allclose(Pk[0], e["kfac_top_eigvec"], rtol=0, atol=1e-15)
+
+
+def test_act_cov_mask_is_deletion_and_invariants():
+    g = W.rng(17)
+    B, T, n = 3, 9, 12
+    a = g.standard_normal((B, T, n))
+    mask = (g.random((B, T)) < 0.6).astype(np.uint8)
+    mask[0] = 0                                   # a fully masked example
+    a_nan = a.copy()
+    a_nan[mask == 0] = np.nan                     # masked slots are never read
+    C = oracle.act_cov(a_nan, mask)
+    kept = a[mask > 0]                            # the valid tokens, in order
+    assert np.array_equal(C, oracle.act_cov(kept[None]))
+    assert np.array_equal(C, C.T)
+    assert abs(np.trace(C) - np.sum(kept ** 2)) <= 1e-12 * np.trace(C)
+    ev = np.linalg.eigvalsh(C)
+    assert ev.min() >= -1e-12 * ev.max()
+    assert np.linalg.matrix_rank(oracle.act_cov(kept[:5][None])) == 5    # rank = tokens < n
+    # one token gives its outer product exactly; accumulating two halves gives the whole
+    assert np.array_equal(oracle.act_cov(kept[:1][None]), np.outer(kept[0], kept[0]))
+    half = oracle.act_cov(a_nan[:2], mask[:2])
+    both = oracle.act_cov(a_nan[2:], mask[2:], C=half.copy())
+    assert _rel(both, C) < 1e-14
+    # bf16 inputs are widened exactly
+    ab = W.f32_to_bf16_bits(a.astype(np.float32))
+    assert np.array_equal(oracle.act_cov(ab, mask), oracle.act_cov(_f64(ab), mask))
+
+
+def test_pca_topk_eigen_properties():
+    n, k = 40, 7
+    C = W.spd_matrix(18, n, n).astype(np.float64)
+    P, w = oracle.pca_topk(C, k)
+    assert np.all(np.diff(w) <= 0)                                  # descending
+    assert _rel(C @ P.T, P.T * w) < 1e-12                          # eigenpairs
+    assert _rel(P @ P.T, np.eye(k)) < 1e-12                        # orthonormal rows
+    full = np.linalg.eigvalsh(C)[::-1]
+    assert _rel(w, full[:k]) < 1e-12                               # the k largest
+    for r in range(k):                                             # the sign rule
+        i = int(np.argmax(np.abs(P[r])))
+        assert P[r, i] > 0
+    # a diagonal covariance: coordinate vectors of its k largest entries, in order
+    d = W.rng(19).permutation(np.arange(1.0, n + 1.0))
+    Pd, wd = oracle.pca_topk(np.diag(d), k)
+    top = np.argsort(-d)[:k]
+    assert np.array_equal(wd, d[top])
+    assert np.array_equal(Pd, np.eye(n)[top])
+
+
+def test_pca_topk_kfac_kronecker_structure():
+    """Sec. 3.2: eigenvectors of C_F (x) C_B are Kronecker products of the
+    factors' eigenvectors, so the top eigenvectors of H_KFAC are products of
+    top eigenvectors, and projecting H_KFAC with P_i (x) P_o (the PCA
+    initialisation) leaves the diagonal matrix of the kept eigenvalue products."""
+    nf, nb, kf, kb = 9, 6, 3, 2
+    CF, CB = W.spd_matrix(20, nf, nf).astype(np.float64), W.spd_matrix(21, nb, nb).astype(np.float64)
+    PF, wF = oracle.pca_topk(CF, kf)
+    PB, wB = oracle.pca_topk(CB, kb)
+    H = np.kron(CF, CB)
+    PH, wH = oracle.pca_topk(H, 1)
+    assert _rel(wH, [wF[0] * wB[0]]) < 1e-12
+    assert _rel(PH[0], np.kron(PF[0], PB[0])) < 1e-10
+    Pk = np.kron(PF, PB)
+    assert _rel(Pk @ H @ Pk.T, np.diag(np.kron(wF, wB))) < 1e-12
