@@ -248,6 +248,28 @@ int logra_influence_scores_scaled(const void *g_test_pre, int te_dtype, int64_t 
                                   float *scores, int64_t ld_s, int topk, float *topk_val, int64_t *topk_idx,
                                   int merge, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------------------------
+ * PCA initialisation of the projections (Sec. 3.2).  KFAC approximates a
+ * layer's Hessian block by C_F (x) C_B, the Kronecker product of the
+ * uncentered covariances of the layer's forward activations x and backward
+ * output gradients dy; P_in and P_out are initialised with the top-k_in
+ * eigenvectors of C_F and the top-k_out eigenvectors of C_B.
+ *
+ * logra_act_cov_accumulate: C[i][j] += sum over unmasked tokens (b, t) of
+ *   a[b][t][i] * a[b][t][j]   (call it with x for C_F, with dy for C_B).
+ *   a      device [B][T][n] of a_dtype (rows of n elements, contiguous);
+ *          bf16: n a multiple of 8 (bf16 MFMA, fp32 accumulation); fp32: any n.
+ *   mask   device u8 [B][T] or NULL (all tokens).  A masked token is never
+ *          read, so NaN/Inf there cannot leak.
+ *   C      device fp32 [n][n], accumulated in place and kept exactly
+ *          symmetric (give it symmetric, e.g. zeroed).
+ *   ws     workspace of logra_act_cov_ws_size(B, T) bytes (the list of
+ *          non-empty 32-token slabs).  B = 0 or T = 0 is a no-op.
+ * ---------------------------------------------------------------------- */
+size_t logra_act_cov_ws_size(int B, int T);
+int logra_act_cov_accumulate(const void *a, int a_dtype, int B, int T, int n, const uint8_t *mask, float *C,
+                             void *ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -36,6 +36,7 @@ EXPORTED = (
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
+    "logra_act_cov_ws_size", "logra_act_cov_accumulate",
 )
 
 
@@ -89,7 +90,10 @@ def lib():
         L.logra_self_influence_ws_size.restype = sz
         L.logra_self_influence_blocks.argtypes = [vp, i32, i32, i64, f64, vp, i32, i64, i64, vp, vp, vp, sz,
                                                   vp]
-        for name in ("logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
+        L.logra_act_cov_ws_size.argtypes = [i32, i32]
+        L.logra_act_cov_ws_size.restype = sz
+        L.logra_act_cov_accumulate.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        for name in ("logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
@@ -282,3 +286,18 @@ def logra_self_influence_blocks(S, N: int, damp_ratio: float, g, self_out=None, 
     _check(lib().logra_self_influence_blocks(_ptr(S), D, n_blocks, int(N), float(damp_ratio), _ptr(g),
                                              _dtype_code(g), ld, rows, _ptr(self_out), _ptr(rsqrt_out),
                                              _ptr(ws), wsb, _stream(stream)))
+
+
+def logra_act_cov_ws_size(B, T) -> int:
+    return int(lib().logra_act_cov_ws_size(B, T))
+
+
+def logra_act_cov_accumulate(a, C, mask=None, ws=None, stream=None):
+    """KFAC factor of one layer (Sec. 3.2): C [n, n] fp32 += sum over unmasked tokens of a_t a_t^T
+    for a [B, T, n] (x for C_F, dy for C_B); mask [B, T] uint8 or None."""
+    B, T, n = a.shape
+    if B > 0 and T > 0:
+        assert a.is_contiguous(), "a must be contiguous [B, T, n]"
+    ws, wsb = _workspace(logra_act_cov_ws_size(B, T), C.device, ws)
+    _check(lib().logra_act_cov_accumulate(_ptr(a), _dtype_code(a), B, T, n, _ptr(mask), _ptr(C), _ptr(ws), wsb,
+                                          _stream(stream)))

@@ -398,4 +398,27 @@ int logra_self_influence_blocks(const float *S, int D, int n_blocks, int64_t N, 
     return report_not_pd(ws, D, n_blocks, s);
 }
 
+size_t logra_act_cov_ws_size(int B, int T) {
+    if (B <= 0 || T <= 0) return 0;
+    return round256(logra::act_cov_ws_bytes(B, T));
+}
+
+int logra_act_cov_accumulate(const void *a, int a_dtype, int B, int T, int n, const uint8_t *mask, float *C,
+                             void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(a_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (B < 0 || T < 0 || n <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need B >= 0, T >= 0, n > 0");
+    const bool bf16 = a_dtype == LOGRA_BF16;
+    if (bf16 && n % 8) return fail(LOGRA_ERR_INVALID_ARG, "bf16 activations need n a multiple of 8");
+    if (n > (1 << 20)) return fail(LOGRA_ERR_UNSUPPORTED, "n must be <= 1048576");
+    if (static_cast<int64_t>(B) * T > INT32_MAX) return fail(LOGRA_ERR_UNSUPPORTED, "B * T must be < 2^31");
+    if (B == 0 || T == 0) return ok();
+    TRY(check_dev(a, "a", bf16 ? 16 : 4));
+    TRY(check_dev(C, "C", 4));
+    if (mask) TRY(check_dev(mask, "mask", 1));
+    TRY(check_ws(ws, ws_bytes, logra_act_cov_ws_size(B, T)));
+    hipError_t e = logra::launch_act_cov(a, bf16, B, T, n, mask, C, ws, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "activation covariance launch");
+    return ok();
+}
+
 }  // extern "C"

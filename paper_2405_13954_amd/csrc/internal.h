@@ -12,6 +12,9 @@ constexpr int kMaxK = 128;
 constexpr int kMaxTopk = 1024;
 constexpr int kMaxPrecondD = 8192;
 
+// Workspace regions are carved at 256-byte boundaries.
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
 struct ProjLayer {
     const void *x;
     const void *dy;
@@ -64,6 +67,13 @@ hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N,
                                  bool interleaved, void *ws, hipStream_t s);
 hipError_t launch_self_influence(const void *g, bool bf16, int64_t ld, int64_t rows, int D, int n_blocks,
                                  const void *ws, float *self_out, float *rsqrt_out, hipStream_t s);
+
+// KFAC activation covariance (the PCA initialisation of P): C [n][n] fp32 +=
+// sum over unmasked tokens of a_t a_t^T for a [B][T][n]; workspace holds the
+// list of non-empty 32-token slabs.
+size_t act_cov_ws_bytes(int B, int T);
+hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const uint8_t *mask, float *C, void *ws,
+                          hipStream_t s);
 
 // Score GEMM s = te * tr^T (fp32 result) and per-query top-k.  With a
 // filter (bf16 only), scores at or above thr[q] are also appended to row q's

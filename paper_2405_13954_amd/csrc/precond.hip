@@ -36,7 +36,6 @@ struct WsLayout {
     double *Z;      // [n_blocks][D][Qp] backward solutions
 };
 
-__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 inline int tiles_of(int D) { return (D + NB - 1) / NB; }
 inline int padded_q(int Q) { return (Q + NB - 1) / NB * NB; }
 

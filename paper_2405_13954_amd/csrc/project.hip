@@ -438,7 +438,6 @@ inline int kt_for(int k_in, int k_out) {
     return kmax <= 16 ? 1 : kmax <= 32 ? 2 : kmax <= 64 ? 4 : 8;
 }
 
-inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct Plan {
     size_t part_floats = 0, gpart_floats = 0;
