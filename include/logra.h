@@ -270,6 +270,28 @@ size_t logra_act_cov_ws_size(int B, int T);
 int logra_act_cov_accumulate(const void *a, int a_dtype, int B, int T, int n, const uint8_t *mask, float *C,
                              void *ws, size_t ws_bytes, void *stream);
 
+/* logra_pca_topk: the top-k eigenvectors of a symmetric PSD C (an
+ * accumulated C_F or C_B) as the rows of a projection, P[e][i] = v_e[i] for
+ * the eigenvalues in decreasing order, each v_e of unit norm and signed so
+ * that its entry of largest magnitude (the lowest index among equal
+ * magnitudes) is positive.
+ *   C        device fp32 [n][n] (read only; only its symmetric part matters).
+ *   k        1 <= k <= min(n, LOGRA_MAX_PCA_K).
+ *   iters    >= 1 subspace iterations on p = min(n, max(2k, 16)) vectors,
+ *            each one pass over C (fp32 MFMA products; fp64 orthonormalisation
+ *            by shifted Cholesky-QR); then Rayleigh-Ritz with an fp64 Jacobi
+ *            eigensolver.  The error of v_e falls like (theta_{p+1} /
+ *            theta_e)^iters; 30 suits spectra whose top eigenvalues decay.
+ *   P        device [k][ld_p] of P_dtype (F32 or BF16, rounded to nearest
+ *            even), ld_p >= n.
+ *   eigvals  device fp32 [k] (Ritz values) or NULL.
+ *   ws       workspace of logra_pca_ws_size(n, k) bytes.
+ * Asynchronous. */
+#define LOGRA_MAX_PCA_K 64
+size_t logra_pca_ws_size(int n, int k);
+int logra_pca_topk(const float *C, int n, int k, int iters, void *P, int P_dtype, int64_t ld_p, float *eigvals,
+                   void *ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -36,7 +36,7 @@ EXPORTED = (
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
-    "logra_act_cov_ws_size", "logra_act_cov_accumulate",
+    "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_pca_ws_size", "logra_pca_topk",
 )
 
 
@@ -93,7 +93,10 @@ def lib():
         L.logra_act_cov_ws_size.argtypes = [i32, i32]
         L.logra_act_cov_ws_size.restype = sz
         L.logra_act_cov_accumulate.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, sz, vp]
-        for name in ("logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
+        L.logra_pca_ws_size.argtypes = [i32, i32]
+        L.logra_pca_ws_size.restype = sz
+        L.logra_pca_topk.argtypes = [vp, i32, i32, i32, vp, i32, i64, vp, vp, sz, vp]
+        for name in ("logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
@@ -301,3 +304,18 @@ def logra_act_cov_accumulate(a, C, mask=None, ws=None, stream=None):
     ws, wsb = _workspace(logra_act_cov_ws_size(B, T), C.device, ws)
     _check(lib().logra_act_cov_accumulate(_ptr(a), _dtype_code(a), B, T, n, _ptr(mask), _ptr(C), _ptr(ws), wsb,
                                           _stream(stream)))
+
+
+def logra_pca_ws_size(n, k) -> int:
+    return int(lib().logra_pca_ws_size(n, k))
+
+
+def logra_pca_topk(C, k: int, P, eigvals=None, iters: int = 30, ws=None, stream=None):
+    """PCA initialisation (Sec. 3.2): rows of P [k, >= n] (fp32 or bf16) = the top-k eigenvectors
+    of the symmetric fp32 C [n, n], by decreasing eigenvalue, sign rule as documented; eigvals
+    [k] fp32 or None."""
+    n = C.shape[0]
+    ld_p = _rows(P, n)
+    ws, wsb = _workspace(logra_pca_ws_size(n, k), C.device, ws)
+    _check(lib().logra_pca_topk(_ptr(C), n, int(k), int(iters), _ptr(P), _dtype_code(P), ld_p, _ptr(eigvals),
+                                _ptr(ws), wsb, _stream(stream)))

@@ -421,4 +421,27 @@ int logra_act_cov_accumulate(const void *a, int a_dtype, int B, int T, int n, co
     return ok();
 }
 
+size_t logra_pca_ws_size(int n, int k) {
+    if (n <= 0 || k <= 0 || k > n || k > LOGRA_MAX_PCA_K) return 0;
+    return round256(logra::pca_ws_bytes(n, k));
+}
+
+int logra_pca_topk(const float *C, int n, int k, int iters, void *P, int P_dtype, int64_t ld_p, float *eigvals,
+                   void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(P_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (n <= 0 || k <= 0 || k > n) return fail(LOGRA_ERR_INVALID_ARG, "need 1 <= k <= n");
+    if (k > LOGRA_MAX_PCA_K) return fail(LOGRA_ERR_UNSUPPORTED, "k must be <= %d", LOGRA_MAX_PCA_K);
+    if (n > 65536) return fail(LOGRA_ERR_UNSUPPORTED, "n must be <= 65536");
+    if (iters < 1 || iters > 100000) return fail(LOGRA_ERR_INVALID_ARG, "need 1 <= iters <= 100000");
+    if (ld_p < n) return fail(LOGRA_ERR_INVALID_ARG, "ld_p must be >= n");
+    TRY(check_dev(C, "C", 4));
+    TRY(check_dev(P, "P", P_dtype == LOGRA_BF16 ? 2 : 4));
+    if (eigvals) TRY(check_dev(eigvals, "eigvals", 4));
+    TRY(check_ws(ws, ws_bytes, logra_pca_ws_size(n, k)));
+    hipError_t e = logra::launch_pca_topk(C, n, k, iters, P, P_dtype == LOGRA_BF16, ld_p, eigvals, ws,
+                                          static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "pca launch");
+    return ok();
+}
+
 }  // extern "C"

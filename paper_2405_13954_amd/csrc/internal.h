@@ -75,6 +75,12 @@ size_t act_cov_ws_bytes(int B, int T);
 hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const uint8_t *mask, float *C, void *ws,
                           hipStream_t s);
 
+// Top-k eigenvectors of a symmetric PSD fp32 C [n][n] (k <= 64) as the rows
+// of P [k][ld_p], by subspace iteration with Rayleigh-Ritz extraction.
+size_t pca_ws_bytes(int n, int k);
+hipError_t launch_pca_topk(const float *C, int n, int k, int iters, void *P, bool bf16_out, int64_t ld_p,
+                           float *eigvals, void *ws, hipStream_t s);
+
 // Score GEMM s = te * tr^T (fp32 result) and per-query top-k.  With a
 // filter (bf16 only), scores at or above thr[q] are also appended to row q's
 // candidate list: cnt[q] counts them (past `cap` too), val/idx hold the

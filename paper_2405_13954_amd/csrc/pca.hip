@@ -23,6 +23,28 @@
 //     the lower part, so C stays exactly symmetric.
 //  1'. k_act_cov_f32: fp32 activations (small problems), one thread per entry.
 //
+// Top-k eigenvectors of C (n x n, symmetric PSD, fp32), by subspace
+// iteration on p = min(n, max(2k, 16)) vectors with Rayleigh-Ritz extraction:
+//
+//   Q_0 = a fixed pseudo-random n x p block;  repeat `iters` times:
+//       Z = C Q  (fp32 MFMA, one pass over C);  Q = Z R^{-1}, R^T R = Z^T Z + eps
+//   then once more with a second orthonormalisation (CholQR2), T = Q^T C Q,
+//   T = W diag(theta) W^T (cyclic Jacobi, fp64), and the Ritz vectors
+//   v_e = Q w_e of the k largest theta, each signed so that its entry of
+//   largest magnitude (lowest index among equal magnitudes) is positive.
+//
+//  2. k_cq: Z = C Q; a wave owns 16 rows of C and streams them (128-bit
+//     loads) into 16x16x4 fp32 MFMAs against Q (read through L2).
+//  3. k_gram_part: fp64 partial sums of X^T Y over 256-row chunks (X^T X for
+//     the orthonormalisation, Q^T Z for Rayleigh-Ritz), fixed order.
+//  4. k_chol_inv (one workgroup): the chunk sums, a shifted Cholesky
+//     Z^T Z + eps tr/p I = R^T R and R^{-1}, in fp64 in LDS.
+//  5. k_apply_rinv: Q = Z R^{-1} (fp64 arithmetic, fp32 result).
+//  6. k_jacobi (one workgroup): T in LDS, round-robin parallel cyclic Jacobi
+//     (p/2 disjoint rotations per round), eigenvectors accumulated in W^T.
+//  7. k_ritz, k_pca_out: Ritz vectors in the order of decreasing theta, the
+//     sign rule, and the rows of P in the output dtype.
+//
 // Every sum has a fixed order, so results are bitwise reproducible.
 #include "common.h"
 #include "internal.h"
@@ -272,6 +294,361 @@ __global__ __launch_bounds__(256) void k_act_cov_f32(const float *__restrict__ a
     if (i != j) C[static_cast<size_t>(j) * n + i] = v;
 }
 
+// ------------------------------------------------------------------------
+// Subspace iteration for the top-k eigenvectors.
+constexpr int kGramRows = 256;   // rows per partial sum of a Gram matrix
+constexpr int kMaxP = 128;       // subspace width (at most 2 k for k <= 64)
+
+__device__ __forceinline__ float hash_uniform(uint32_t i, uint32_t j) {
+    // integer hash of (i, j) (a multiply-xorshift mixer) -> uniform in [-1, 1)
+    uint32_t h = i * 0x9E3779B1u ^ (j + 0x7F4A7C15u) * 0x85EBCA77u;
+    h ^= h >> 16;
+    h *= 0x7FEB352Du;
+    h ^= h >> 15;
+    h *= 0x846CA68Bu;
+    h ^= h >> 16;
+    return static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f;
+}
+
+// Q_0: pseudo-random columns j < p, zero padding columns up to pp.
+__global__ __launch_bounds__(256) void k_pca_init(float *Q, int n, int p, int pp) {
+    const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (e >= static_cast<int64_t>(n) * pp) return;
+    const int i = static_cast<int>(e / pp), j = static_cast<int>(e - static_cast<int64_t>(i) * pp);
+    Q[e] = j < p ? hash_uniform(static_cast<uint32_t>(i), static_cast<uint32_t>(j)) : 0.f;
+}
+
+// Z = C Q for Z, Q [n][pp] (pp a multiple of 16, at most 128).  A wave owns
+// 16 rows: lane l streams row (l % 16) of C, four columns k + 4 (l / 16) + e
+// (e < 4) per 128-bit load, and feeds MFMA e with column k + 4 (l / 16) + e of
+// its row and the matching row of Q.  Rows and columns past n read zeros.
+template <int NB>
+__global__ __launch_bounds__(256) void k_cq(const float *__restrict__ C, int n, const float *__restrict__ Q,
+                                            float *__restrict__ Z) {
+    constexpr int pp = 16 * NB;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m0 = (blockIdx.x * 4 + wave) * 16;
+    if (m0 >= n) return;
+    const int row = lane & 15, kq = lane >> 4;
+    const int rows = min(16, n - m0);
+    const auto rc = buf_rsrc_uniform(C + static_cast<size_t>(m0) * n, static_cast<uint32_t>(rows * n * 4));
+    const auto rq = buf_rsrc_uniform(Q, static_cast<uint32_t>(n * pp * 4));
+    f32x4 acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint32_t crow = static_cast<uint32_t>(row) * static_cast<uint32_t>(n) * 4u;
+    for (int k = 0; k < n; k += 16) {
+        const int kk = k + 4 * kq;
+        // C[row][kk .. kk+3]: past the row's end only at the last row block
+        // of the matrix, where the range check returns zeros; columns past n
+        // meet rows of Q past n, which read zeros too
+        const u32x4 cv = buf_ld128(rc, kk < n ? crow + static_cast<uint32_t>(kk) * 4u : kBufOOB);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t qoff = static_cast<uint32_t>((kk + e) * pp + row) * 4u;
+            const float a = __uint_as_float(cv[e]);
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const float q = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    rq, kk + e < n ? static_cast<int>(qoff + 64u * b) : static_cast<int>(kBufOOB), 0, 0));
+                acc[b] = mfma16_f32(a, q, acc[b]);
+            }
+        }
+    }
+    // result register r of lane l: row 4 (l / 16) + r, column l % 16 of block b
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int i = m0 + 4 * kq + r;
+            if (i < n) Z[static_cast<size_t>(i) * pp + 16 * b + row] = acc[b][r];
+        }
+}
+
+// Partial Gram sums G_c[a][b] = sum over rows r of chunk c of X[r][a] Y[r][b]
+// (fp64), a, b < p, for X, Y [n][pp] fp32; rows staged through LDS.
+__global__ __launch_bounds__(256) void k_gram_part(const float *__restrict__ X, const float *__restrict__ Y, int n,
+                                                   int p, int pp, double *__restrict__ part) {
+    __shared__ float xs[64][129], ys[64][129];
+    const int tid = threadIdx.x;
+    const int r0 = blockIdx.x * kGramRows;
+    const int rend = min(n, r0 + kGramRows);
+    const int np = p * p;
+    double acc[64];
+#pragma unroll
+    for (int u = 0; u < 64; ++u) acc[u] = 0.0;
+    for (int c0 = r0; c0 < rend; c0 += 64) {
+        const int nr = min(64, rend - c0);
+        for (int e = tid; e < 64 * pp; e += 256) {
+            const int r = e / pp, j = e - r * pp;
+            xs[r][j] = r < nr ? X[static_cast<size_t>(c0 + r) * pp + j] : 0.f;
+            ys[r][j] = r < nr ? Y[static_cast<size_t>(c0 + r) * pp + j] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 64; ++u) {
+            const int e = tid + 256 * u;
+            if (e < np) {
+                const int a = e / p, b = e - (e / p) * p;
+                double s = acc[u];
+                for (int r = 0; r < nr; ++r) s = fma(static_cast<double>(xs[r][a]), static_cast<double>(ys[r][b]), s);
+                acc[u] = s;
+            }
+        }
+        __syncthreads();
+    }
+    double *dst = part + static_cast<size_t>(blockIdx.x) * np;
+#pragma unroll
+    for (int u = 0; u < 64; ++u) {
+        const int e = tid + 256 * u;
+        if (e < np) dst[e] = acc[u];
+    }
+}
+
+// One workgroup: G = sum of the chunk partials (in chunk order), then the
+// shifted Cholesky G + eps (tr G / p) I = R^T R (R upper) and R^{-1}, all in
+// fp64.  Writes R^{-1} [p][p] (zero below the diagonal).
+__global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ part, int chunks, int p,
+                                                  double *__restrict__ Rinv) {
+    __shared__ double A[kMaxP * kMaxP];   // G, then R in its upper triangle
+    __shared__ double red[256];
+    const int tid = threadIdx.x, np = p * p;
+    for (int e = tid; e < np; e += 256) {
+        double s = 0.0;
+        for (int c = 0; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
+        A[e] = s;
+    }
+    __syncthreads();
+    double tr = 0.0;
+    for (int a = tid; a < p; a += 256) tr += A[a * p + a];
+    red[tid] = tr;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (tid < w) red[tid] += red[tid + w];
+        __syncthreads();
+    }
+    const double shift = 1e-12 * (red[0] > 0.0 ? red[0] / p : 1.0);
+    for (int a = tid; a < p; a += 256) A[a * p + a] += shift;
+    __syncthreads();
+    // right-looking Cholesky on the upper triangle: row j of R
+    for (int j = 0; j < p; ++j) {
+        if (tid == 0) {
+            const double d = A[j * p + j];
+            A[j * p + j] = d > 0.0 ? sqrt(d) : 1.0;   // a non-positive pivot (cannot follow the shift) keeps R invertible
+        }
+        __syncthreads();
+        const double rjj = A[j * p + j];
+        for (int c = j + 1 + tid; c < p; c += 256) A[j * p + c] /= rjj;
+        __syncthreads();
+        for (int e = tid; e < (p - j - 1) * (p - j - 1); e += 256) {
+            const int r = j + 1 + e / (p - j - 1), c = j + 1 + e % (p - j - 1);
+            if (c >= r) A[r * p + c] -= A[j * p + r] * A[j * p + c];
+        }
+        __syncthreads();
+    }
+    // R^{-1}: column c solves R x = e_c (back substitution), one thread per column
+    for (int c = tid; c < p; c += 256) {
+        for (int r = p - 1; r >= 0; --r) {
+            double s = r == c ? 1.0 : 0.0;
+            for (int m = r + 1; m <= c; ++m) s -= A[r * p + m] * Rinv[static_cast<size_t>(m) * p + c];
+            Rinv[static_cast<size_t>(r) * p + c] = r <= c ? s / A[r * p + r] : 0.0;
+        }
+    }
+}
+
+// Q = Z R^{-1}: row i of Q is row i of Z times the upper-triangular R^{-1};
+// fp64 sums, fp32 result, padding columns zero.
+__global__ __launch_bounds__(256) void k_apply_rinv(const float *__restrict__ Z, int n, int p, int pp,
+                                                    const double *__restrict__ Rinv, float *__restrict__ Q) {
+    const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (e >= static_cast<int64_t>(n) * pp) return;
+    const int i = static_cast<int>(e / pp), j = static_cast<int>(e - static_cast<int64_t>(i) * pp);
+    double s = 0.0;
+    if (j < p)
+        for (int m = 0; m <= j; ++m) s = fma(static_cast<double>(Z[static_cast<size_t>(i) * pp + m]), Rinv[static_cast<size_t>(m) * p + j], s);
+    Q[e] = static_cast<float>(s);
+}
+
+// One workgroup: T = (sum of the chunk partials of Q^T Z), symmetrised, is
+// diagonalised by round-robin parallel cyclic Jacobi in fp64: each round
+// applies p'/2 disjoint plane rotations (p' = p rounded up to even; a pair
+// with the padding index p is skipped), each zeroing T[a][b] (the symmetric
+// 2 x 2 Schur decomposition).  Sweeps stop when the off-diagonal mass is
+// below 1e-30 of the total, or after 40.  Writes theta [p] and the
+// eigenvectors as the rows of Wt [p][p].
+__global__ __launch_bounds__(256) void k_jacobi(const double *__restrict__ part, int chunks, int p,
+                                                double *__restrict__ Wt, double *__restrict__ theta) {
+    __shared__ double T[kMaxP * kMaxP];
+    __shared__ double cs[64], sn[64];
+    __shared__ int pa[64], pb[64];
+    __shared__ double red[256];
+    const int tid = threadIdx.x, np = p * p;
+    for (int e = tid; e < np; e += 256) {
+        double s = 0.0;
+        for (int c = 0; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
+        T[e] = s;
+    }
+    __syncthreads();
+    for (int e = tid; e < np; e += 256) {
+        const int a = e / p, b = e - (e / p) * p;
+        if (a < b) {
+            const double v = 0.5 * (T[a * p + b] + T[b * p + a]);
+            T[a * p + b] = v;
+            T[b * p + a] = v;
+        }
+        Wt[e] = a == b ? 1.0 : 0.0;
+    }
+    __syncthreads();
+    const int m = p + (p & 1);   // players of the round-robin schedule
+    const int half = m / 2;
+    for (int sweep = 0; sweep < 40; ++sweep) {
+        double off = 0.0, all = 0.0;
+        for (int e = tid; e < np; e += 256) {
+            const int a = e / p, b = e - (e / p) * p;
+            const double v = T[e] * T[e];
+            all += v;
+            if (a != b) off += v;
+        }
+        red[tid] = off;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (tid < w) red[tid] += red[tid + w];
+            __syncthreads();
+        }
+        const double off_sum = red[0];
+        __syncthreads();
+        red[tid] = all;
+        __syncthreads();
+        for (int w = 128; w > 0; w >>= 1) {
+            if (tid < w) red[tid] += red[tid + w];
+            __syncthreads();
+        }
+        const double all_sum = red[0];
+        __syncthreads();
+        if (!(off_sum > 1e-30 * all_sum)) break;   // uniform: every thread read the same sums
+        for (int rnd = 0; rnd < m - 1; ++rnd) {
+            if (tid < half) {
+                // circle method: position 0 fixed, positions 1..m-1 rotate by rnd
+                auto player = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + rnd) % (m - 1); };
+                int a = player(tid), b = player(m - 1 - tid);
+                if (a > b) {
+                    const int t = a;
+                    a = b;
+                    b = t;
+                }
+                double c = 1.0, s = 0.0;
+                if (b < p) {
+                    const double apq = T[a * p + b];
+                    if (apq != 0.0) {
+                        const double tau = (T[b * p + b] - T[a * p + a]) / (2.0 * apq);
+                        const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+                        c = 1.0 / sqrt(1.0 + t * t);
+                        s = t * c;
+                    }
+                }
+                pa[tid] = a;
+                pb[tid] = b;
+                cs[tid] = c;
+                sn[tid] = s;
+            }
+            __syncthreads();
+            // rows a, b of T (all columns), then columns a, b (all rows), and rows a, b of W^T
+            for (int e = tid; e < half * p; e += 256) {
+                const int q = e / p, j = e - (e / p) * p;
+                const int a = pa[q], b = pb[q];
+                if (b < p) {
+                    const double c = cs[q], s = sn[q];
+                    const double ta = T[a * p + j], tb = T[b * p + j];
+                    T[a * p + j] = c * ta - s * tb;
+                    T[b * p + j] = s * ta + c * tb;
+                }
+            }
+            __syncthreads();
+            for (int e = tid; e < half * p; e += 256) {
+                const int q = e / p, i = e - (e / p) * p;
+                const int a = pa[q], b = pb[q];
+                if (b < p) {
+                    const double c = cs[q], s = sn[q];
+                    const double ta = T[i * p + a], tb = T[i * p + b];
+                    T[i * p + a] = c * ta - s * tb;
+                    T[i * p + b] = s * ta + c * tb;
+                    const double wa = Wt[static_cast<size_t>(a) * p + i], wb = Wt[static_cast<size_t>(b) * p + i];
+                    Wt[static_cast<size_t>(a) * p + i] = c * wa - s * wb;
+                    Wt[static_cast<size_t>(b) * p + i] = s * wa + c * wb;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int a = tid; a < p; a += 256) theta[a] = T[a * p + a];
+}
+
+// Ritz vectors of the k largest theta (decreasing; equal values in index
+// order): V[e][i] = sum_j Q[i][j] Wt[order_e][j] (fp64 sums), eigvals[e].
+// The order is found by every thread from theta (p <= 128).
+__global__ __launch_bounds__(256) void k_ritz(const float *__restrict__ Q, int n, int p, int pp, int k,
+                                              const double *__restrict__ Wt, const double *__restrict__ theta,
+                                              float *__restrict__ V, float *__restrict__ eigvals) {
+    __shared__ int order[64];
+    __shared__ double w[128];
+    const int e = blockIdx.y;
+    if (threadIdx.x == 0) {
+        // rank of each theta among all (larger first, lower index first): the e-th is order[e]
+        for (int a = 0; a < p; ++a) {
+            int rank = 0;
+            for (int b = 0; b < p; ++b) rank += theta[b] > theta[a] || (theta[b] == theta[a] && b < a);
+            if (rank < k) order[rank] = a;
+        }
+    }
+    __syncthreads();
+    const int col = order[e];
+    for (int j = threadIdx.x; j < p; j += 256) w[j] = Wt[static_cast<size_t>(col) * p + j];
+    __syncthreads();
+    if (blockIdx.x == 0 && threadIdx.x == 0 && eigvals) eigvals[e] = static_cast<float>(theta[col]);
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    double s = 0.0;
+    for (int j = 0; j < p; ++j) s = fma(static_cast<double>(Q[static_cast<size_t>(i) * pp + j]), w[j], s);
+    V[static_cast<size_t>(e) * n + i] = static_cast<float>(s);
+}
+
+// One workgroup per Ritz vector: the index of its largest magnitude (lowest
+// index among equal magnitudes) sets the sign; the row of P is written in the
+// output dtype.
+template <typename TOut>
+__global__ __launch_bounds__(256) void k_pca_out(const float *__restrict__ V, int n, TOut *__restrict__ P,
+                                                 int64_t ld_p) {
+    __shared__ float bv[256];
+    __shared__ int bi[256];
+    const int e = blockIdx.x, tid = threadIdx.x;
+    const float *v = V + static_cast<size_t>(e) * n;
+    float best = -1.f;
+    int idx = 0x7fffffff;
+    for (int i = tid; i < n; i += 256) {
+        const float a = fabsf(v[i]);
+        if (a > best) {   // increasing i: the first of equal magnitudes is kept
+            best = a;
+            idx = i;
+        }
+    }
+    bv[tid] = best;
+    bi[tid] = idx;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+        if (tid < w) {
+            const float ob = bv[tid + w];
+            const int oi = bi[tid + w];
+            if (ob > bv[tid] || (ob == bv[tid] && oi < bi[tid])) {
+                bv[tid] = ob;
+                bi[tid] = oi;
+            }
+        }
+        __syncthreads();
+    }
+    const float sgn = v[bi[0]] < 0.f ? -1.f : 1.f;
+    for (int i = tid; i < n; i += 256) store_out<TOut>(P + static_cast<int64_t>(e) * ld_p + i, sgn * v[i]);
+}
+
 }  // namespace
 
 size_t act_cov_ws_bytes(int B, int T) {
@@ -298,6 +675,106 @@ hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const u
         hipLaunchKernelGGL(k_act_cov_f32, dim3(nb, nb), dim3(256), 0, s, static_cast<const float *>(a), T, n, spe,
                            list, bits, count, C);
     }
+    return hipGetLastError();
+}
+
+}  // namespace logra
+
+namespace logra {
+namespace {
+
+struct PcaLayout {
+    float *Q, *Z;
+    double *part, *Rinv, *Wt, *theta;
+};
+
+inline int pca_p(int n, int k) {
+    const int w = 2 * k > 16 ? 2 * k : 16;   // at least one MFMA column block of vectors
+    return w < n ? w : n;
+}
+inline int pca_pp(int n, int k) { return (pca_p(n, k) + 15) / 16 * 16; }
+inline int gram_chunks(int n) { return (n + kGramRows - 1) / kGramRows; }
+
+PcaLayout pca_layout(void *ws, int n, int k) {
+    const int p = pca_p(n, k), pp = pca_pp(n, k);
+    char *w = static_cast<char *>(ws);
+    PcaLayout L;
+    L.Q = reinterpret_cast<float *>(w);
+    w += align256(sizeof(float) * static_cast<size_t>(n) * pp);
+    L.Z = reinterpret_cast<float *>(w);
+    w += align256(sizeof(float) * static_cast<size_t>(n) * pp);
+    L.part = reinterpret_cast<double *>(w);
+    w += align256(sizeof(double) * static_cast<size_t>(gram_chunks(n)) * p * p);
+    L.Rinv = reinterpret_cast<double *>(w);
+    w += align256(sizeof(double) * static_cast<size_t>(p) * p);
+    L.Wt = reinterpret_cast<double *>(w);
+    w += align256(sizeof(double) * static_cast<size_t>(p) * p);
+    L.theta = reinterpret_cast<double *>(w);
+    return L;
+}
+
+hipError_t launch_cq(const float *C, int n, int pp, const float *Q, float *Z, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>((n + 63) / 64));
+    switch (pp / 16) {
+        case 1: hipLaunchKernelGGL(k_cq<1>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 2: hipLaunchKernelGGL(k_cq<2>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 3: hipLaunchKernelGGL(k_cq<3>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 4: hipLaunchKernelGGL(k_cq<4>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 5: hipLaunchKernelGGL(k_cq<5>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 6: hipLaunchKernelGGL(k_cq<6>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 7: hipLaunchKernelGGL(k_cq<7>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        default: hipLaunchKernelGGL(k_cq<8>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+    }
+    return hipGetLastError();
+}
+
+// Q = orthonormalised Z (shifted CholQR)
+void cholqr(const PcaLayout &L, int n, int p, int pp, const float *Z, float *Q, hipStream_t s) {
+    const int chunks = gram_chunks(n);
+    hipLaunchKernelGGL(k_gram_part, dim3(static_cast<unsigned>(chunks)), dim3(256), 0, s, Z, Z, n, p, pp, L.part);
+    hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Rinv);
+    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(n) * pp + 255) / 256);
+    hipLaunchKernelGGL(k_apply_rinv, dim3(g), dim3(256), 0, s, Z, n, p, pp, L.Rinv, Q);
+}
+
+}  // namespace
+
+size_t pca_ws_bytes(int n, int k) {
+    const int p = pca_p(n, k), pp = pca_pp(n, k);
+    return 2 * align256(sizeof(float) * static_cast<size_t>(n) * pp) +
+           align256(sizeof(double) * static_cast<size_t>(gram_chunks(n)) * p * p) +
+           2 * align256(sizeof(double) * static_cast<size_t>(p) * p) + align256(sizeof(double) * p);
+}
+
+hipError_t launch_pca_topk(const float *C, int n, int k, int iters, void *P, bool bf16_out, int64_t ld_p,
+                           float *eigvals, void *ws, hipStream_t s) {
+    const int p = pca_p(n, k), pp = pca_pp(n, k);
+    const PcaLayout L = pca_layout(ws, n, k);
+    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(n) * pp + 255) / 256);
+    hipLaunchKernelGGL(k_pca_init, dim3(g), dim3(256), 0, s, L.Q, n, p, pp);
+    for (int it = 0; it < iters; ++it) {
+        hipError_t e = launch_cq(C, n, pp, L.Q, L.Z, s);
+        if (e != hipSuccess) return e;
+        cholqr(L, n, p, pp, L.Z, L.Q, s);
+    }
+    // second orthonormalisation (CholQR2) into Z, then Rayleigh-Ritz on the
+    // basis Z: Q = C Z, T = Z^T Q
+    cholqr(L, n, p, pp, L.Q, L.Z, s);
+    hipError_t e = launch_cq(C, n, pp, L.Z, L.Q, s);
+    if (e != hipSuccess) return e;
+    const int chunks = gram_chunks(n);
+    hipLaunchKernelGGL(k_gram_part, dim3(static_cast<unsigned>(chunks)), dim3(256), 0, s, L.Z, L.Q, n, p, pp,
+                       L.part);
+    hipLaunchKernelGGL(k_jacobi, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
+    // the Ritz vectors [k][n] overwrite Q (k <= pp)
+    hipLaunchKernelGGL(k_ritz, dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(k)), dim3(256), 0,
+                       s, L.Z, n, p, pp, k, L.Wt, L.theta, L.Q, eigvals);
+    if (bf16_out)
+        hipLaunchKernelGGL(k_pca_out<bf16_bits>, dim3(static_cast<unsigned>(k)), dim3(256), 0, s, L.Q, n,
+                           static_cast<bf16_bits *>(P), ld_p);
+    else
+        hipLaunchKernelGGL(k_pca_out<float>, dim3(static_cast<unsigned>(k)), dim3(256), 0, s, L.Q, n,
+                           static_cast<float *>(P), ld_p);
     return hipGetLastError();
 }
 

@@ -154,3 +154,25 @@ def test_scaled_influence_validation(L):
     assert f(*args(topk=1025)) == P.ERR_UNSUPPORTED
     assert f(*args(topk=0)) == P.ERR_INVALID_ARG
     assert f(*args(Q=0)) == P.OK
+
+
+def test_pca_entry_points_validation(L):
+    # activation covariance: the slab list (one int and one 32-bit token map per
+    # 32-token slab) and its count
+    assert P.logra_act_cov_ws_size(8, 2048) == 2 * (8 * 64 * 4) + 256
+    assert P.logra_act_cov_ws_size(0, 16) == 0
+    f = L.logra_act_cov_accumulate
+    fake = ctypes.c_void_p(0x1000)
+    assert f(None, 5, 2, 4, 64, None, fake, None, 0, None) == P.ERR_INVALID_ARG     # dtype
+    assert f(None, 1, 2, 4, 60, None, fake, None, 0, None) == P.ERR_INVALID_ARG     # bf16 n % 8
+    assert f(None, 1, -1, 4, 64, None, fake, None, 0, None) == P.ERR_INVALID_ARG
+    assert f(None, 1, 0, 4, 64, None, fake, None, 0, None) == P.OK                  # no tokens: a no-op
+    # PCA: k limits, iterations, output stride
+    assert P.logra_pca_ws_size(100, 65) == 0 and P.logra_pca_ws_size(10, 11) == 0
+    assert P.logra_pca_ws_size(4096, 16) > 2 * 4096 * 32 * 4
+    g = L.logra_pca_topk
+    assert g(fake, 100, 0, 30, fake, 0, 100, None, None, 0, None) == P.ERR_INVALID_ARG
+    assert g(fake, 100, 65, 30, fake, 0, 100, None, None, 0, None) == P.ERR_UNSUPPORTED
+    assert g(fake, 10, 11, 30, fake, 0, 10, None, None, 0, None) == P.ERR_INVALID_ARG
+    assert g(fake, 100, 8, 0, fake, 0, 100, None, None, 0, None) == P.ERR_INVALID_ARG
+    assert g(fake, 100, 8, 30, fake, 0, 99, None, None, 0, None) == P.ERR_INVALID_ARG

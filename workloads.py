@@ -210,6 +210,32 @@ def spd_matrix(seed: int, D: int, rank: int, scale: float = 1.0) -> np.ndarray:
     return s + np.triu(s, 1).T
 
 
+def orthogonal(g: np.random.Generator, n: int) -> np.ndarray:
+    """A uniformly random n x n orthogonal matrix (QR of a Gaussian, signs fixed), float64."""
+    q, r = np.linalg.qr(g.standard_normal((n, n)))
+    return q * np.sign(np.diag(r))
+
+
+def spectral_matrix(seed: int, n: int, decay: float, scale: float = 1.0) -> np.ndarray:
+    """Symmetric fp32 U diag(scale * decay^i) U^T with a random orthogonal U: a covariance
+    whose top eigenvectors are well separated (ratio `decay` between neighbours); exactly
+    symmetric after rounding."""
+    u = orthogonal(rng(seed, 6, n), n)
+    s = (u * (scale * decay ** np.arange(n))) @ u.T
+    s = np.triu(s.astype(np.float32))
+    return s + np.triu(s, 1).T
+
+
+def structured_activations(g: np.random.Generator, B: int, T: int, n: int, decay: float, dtype: str):
+    """Activations a_t = U (s * z_t), z ~ N(0, I), s_i = decay^(i / 2), U random orthogonal: the
+    token covariance U diag(decay^i) U^T has a decaying spectrum, like the activations of a
+    trained network (i.i.d. entries would give a flat one with no distinguished top-k)."""
+    u = orthogonal(g, n)
+    z = g.standard_normal((B, T, n)) * np.sqrt(decay ** np.arange(n))
+    a = (z @ u.T).astype(np.float32)
+    return f32_to_bf16_bits(a) if dtype == "bf16" else a
+
+
 def integer_array(g: np.random.Generator, shape, lo: int, hi: int, dtype: str, density: float = 1.0):
     """Small integers in [lo, hi] (exact in bf16/fp32), zeroed with probability 1 - density."""
     a = g.integers(lo, hi + 1, size=shape).astype(np.float32)
