@@ -10,16 +10,16 @@
 //     example) that hold at least one unmasked token, each with the 32-bit
 //     map of its unmasked tokens.
 //  1. k_act_cov_dma (bf16): one workgroup per upper-triangle 256 x 256 tile
-//     (I <= J) of C; 4 waves, each owning a 128 x 128 quadrant as 4 x 4
+//     (I <= J) of C, tiles grouped per XCD for L2 reuse; 4 waves, each owning a 128 x 128 quadrant as 4 x 4
 //     blocks of 32x32x16 bf16 MFMAs (fp32 accumulation).  The contraction
 //     runs over the listed slabs.  A slab of the two operands (the tile's
 //     256 features I.. and J.. of 32 tokens, 16 KB each in token-major
 //     order) is copied straight from memory into an LDS ring (gfx950
-//     buffer_load ... lds), three slabs ahead; a masked token's row is read
+//     buffer_load ... lds), four slabs ahead; a masked token's row is read
 //     as zeros without a memory access.  The MFMA operands need 8
-//     consecutive tokens of one feature, so each fragment is gathered from
-//     the token-major slab with 16-bit LDS reads.  A diagonal tile has one
-//     operand.  The tile is added to C (upper part) and written mirrored to
+//     consecutive tokens of one feature: each fragment is two transposed
+//     LDS reads (gfx950 ds_read_b64_tr_b16) of the token-major slab.  A
+//     diagonal tile has one operand.  The tile is added to C (upper part) and written mirrored to
 //     the lower part, so C stays exactly symmetric.
 //  1'. k_act_cov_f32: fp32 activations (small problems), one thread per entry.
 //
@@ -55,22 +55,43 @@ namespace {
 constexpr int ST = 32;                          // tokens per slab
 constexpr int CT = 256;                         // tile edge (features)
 constexpr int kCSlab = ST * CT * 2;             // bytes of one operand slab (16 KB)
-constexpr int kCStages = 4;                     // ring stages (slabs); each holds both operands
+constexpr int kCStages = 5;                     // ring stages (slabs); each holds both operands
 constexpr int kCStage = 2 * kCSlab;
 constexpr int kCRow = CT + 1;                   // padded row of the epilogue's staging (floats)
-constexpr int kCLds = 128 * kCRow * 4;          // >= ring (128 KB): the epilogue stages 128 rows
-static_assert(kCStages * kCStage <= kCLds, "ring must fit the LDS allocation");
+constexpr int kCLds = kCStages * kCStage;       // 160 KB
+static_assert(128 * kCRow * 4 <= kCLds, "the epilogue stages 128 rows of a tile in the ring");
+constexpr int kGR = 4, kGC = 8;                 // tiles per XCD group: 4 tile rows x 8 tile columns
 constexpr int kCCopies = kCSlab / 1024 / 4;     // 1 KB copies per wave and operand slab (4)
 
-__device__ __forceinline__ void tile_coords(int t, int nt, int &ti, int &tj) {
-    // t enumerates the upper triangle row by row: (0,0),(0,1)..(0,nt-1),(1,1),...
-    int i = 0;
-    while (t >= nt - i) {
-        t -= nt - i;
-        ++i;
+// Tile of workgroup `bid`, grouped for the L2 caches.  Dispatch deals
+// workgroups round-robin over the 8 XCDs (bid % 8) and one workgroup fills a
+// CU, so each XCD runs 32 at a time.  They get a group of 4 tile rows x 8 tile
+// columns, which reads 12 distinct 256-feature blocks of the activations
+// instead of 64, in step (same slabs at about the same time).  Groups holding
+// an upper-triangle tile are numbered row by row (group row gr starts at
+// group column gr / 2) and dealt to XCDs in turn.  Returns false for a slot
+// with no upper tile.
+__device__ __forceinline__ bool tile_of(int bid, int nt, int &ti, int &tj) {
+    const int x = bid & 7, u = bid >> 3;
+    int g = (u / (kGR * kGC)) * 8 + x;
+    const int slot = u % (kGR * kGC);
+    const int ngr = (nt + kGR - 1) / kGR, ngc = (nt + kGC - 1) / kGC;
+    int gr = 0;
+    while (gr < ngr && g >= ngc - gr / 2) {
+        g -= ngc - gr / 2;
+        ++gr;
     }
-    ti = i;
-    tj = i + t;
+    if (gr >= ngr) return false;
+    ti = gr * kGR + slot / kGC;
+    tj = (gr / 2 + g) * kGC + slot % kGC;
+    return ti < nt && tj < nt && ti <= tj;
+}
+
+inline int tile_slots(int nt) {
+    const int ngr = (nt + kGR - 1) / kGR, ngc = (nt + kGC - 1) / kGC;
+    int groups = 0;
+    for (int gr = 0; gr < ngr; ++gr) groups += ngc - gr / 2;
+    return (groups + 7) / 8 * 8 * kGR * kGC;
 }
 
 // Slabs of B examples of T tokens (spe = ceil(T / 32) per example): the
@@ -129,56 +150,71 @@ __device__ __forceinline__ void act_cov_tile(const bf16_bits *__restrict__ a, in
     constexpr int NOP = DIAG ? 1 : 2;               // operand slabs copied per slab
     constexpr int NCP = NOP * kCCopies;             // copies per wave per slab
 
-    // copy q of this wave: token rows 2 (4 wave + q) + (lane >> 5) of the slab,
-    // LDS chunk position lane & 31 of the row, holding feature chunk
-    // (lane & 31) ^ (4 ((row >> 3) & 1)) (tokens r and r + 8 land 64 bytes
-    // apart in the banks, so the fragment reads of the two half-waves do not
-    // collide)
+    // LDS slab layout: 32 token rows of 512 bytes (the tile's 256 features);
+    // the 16-byte chunk c of token row t sits at position c ^ (4 (t & 3)), so
+    // that the four token rows read together by a transposed read (below)
+    // fall in different banks.  Copy q of this wave fills token rows
+    // 2 (4 wave + q) + (lane >> 5): lane l stores position l & 31 of its row.
     int crow[kCCopies];
     uint32_t cofs[kCCopies];   // byte offset of the lane's 16 bytes within a token row, from feature 0
 #pragma unroll
     for (int q = 0; q < kCCopies; ++q) {
         crow[q] = 2 * (4 * wave + q) + (lane >> 5);
-        cofs[q] = static_cast<uint32_t>(((lane & 31) ^ (4 * ((crow[q] >> 3) & 1))) * 16);
+        cofs[q] = static_cast<uint32_t>(((lane & 31) ^ (4 * (crow[q] & 3))) * 16);
     }
-    auto issue = [&](int s, int stage) {
-        const bool live = s < ns;
-        const int sid = live ? slabs[s] : 0;
-        const uint32_t m = live ? bits[s] : 0u;
+    // copy c (< NCP) of a slab: operand c / 4 (I, then J), copy c % 4 of the wave
+    struct Slab {
+        __amdgpu_buffer_rsrc_t rs;
+        uint32_t m;
+    };
+    auto slab_of = [&](int sid, uint32_t m) {
         const int b = sid / spe, t0 = (sid - b * spe) * ST;
         const int rows = min(ST, T - t0);
         const bf16_bits *base = a + (static_cast<size_t>(b) * T + t0) * n;
-        const auto rs = buf_rsrc_uniform(base, live ? static_cast<uint32_t>(rows * n * 2) : 0u);
-        const uint32_t st = lds0 + stage * kCStage + wave * kCCopies * 1024;
-#pragma unroll
-        for (int o = 0; o < NOP; ++o) {
-            const uint32_t f0 = static_cast<uint32_t>((o == 0 ? I : J) * 2);
-#pragma unroll
-            for (int q = 0; q < kCCopies; ++q) {
-                const bool ok = (m >> crow[q]) & 1u;
-                const uint32_t off = static_cast<uint32_t>(crow[q]) * static_cast<uint32_t>(n * 2) + f0 + cofs[q];
-                copy_to_lds(rs, ok ? off : kBufOOB, st + o * kCSlab + q * 1024);
-            }
-        }
+        return Slab{buf_rsrc_uniform(base, m ? static_cast<uint32_t>(rows * n * 2) : 0u), m};
+    };
+    auto copy1 = [&](const Slab &sl, int stage, int c) {
+        const int o = c / kCCopies, q = c % kCCopies;
+        const uint32_t f0 = static_cast<uint32_t>((o == 0 ? I : J) * 2);
+        const bool ok = (sl.m >> crow[q]) & 1u;
+        const uint32_t off = static_cast<uint32_t>(crow[q]) * static_cast<uint32_t>(n * 2) + f0 + cofs[q];
+        copy_to_lds(sl.rs, ok ? off : kBufOOB,
+                    lds0 + stage * kCStage + o * kCSlab + wave * kCCopies * 1024 + q * 1024);
     };
 
-    // fragment of block i (32 features) for the 16-token step ks: lane l holds
-    // feature (l % 32) of the block, tokens 16 ks + 8 (l / 32) + e, e < 8
-    const int sx = lane >> 5;   // (token >> 3) & 1 of every token the lane reads
+    // MFMA fragment of block i (32 features) for the 16-token step ks: lane l
+    // must hold feature l % 32 of the block and tokens 16 ks + 8 (l / 32) + 0..7.
+    // A transposed LDS read (ds_read_b64_tr_b16) works on groups of 16 lanes:
+    // slot e of lane i receives element i % 4 of the 8 bytes addressed by lane
+    // 4 e + i / 4.  So lane j of group g (= l / 16) addresses token
+    // 16 ks + 8 (g / 2) + 4 r + j / 4, features (g % 2) 16 + 4 (j % 4) .. + 3 of
+    // the block, and read r (0, 1) hands every lane tokens 4 r .. 4 r + 3 of
+    // its feature.
+    const int gq = lane >> 4, jq = lane & 15;
     uint32_t fa[4], fb[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int fA = wm * 128 + i * 32 + (lane & 31), fB = wn * 128 + i * 32 + (lane & 31);
-        fa[i] = static_cast<uint32_t>(8 * sx * 512 + (((fA >> 3) ^ (4 * sx)) * 16) + (fA & 7) * 2);
-        fb[i] = static_cast<uint32_t>(8 * sx * 512 + (((fB >> 3) ^ (4 * sx)) * 16) + (fB & 7) * 2) +
+        const int t = 8 * (gq >> 1) + (jq >> 2);                    // token within the step, r = 0
+        const int fA = wm * 128 + i * 32 + (gq & 1) * 16 + 4 * (jq & 3);
+        const int fB = wn * 128 + i * 32 + (gq & 1) * 16 + 4 * (jq & 3);
+        fa[i] = static_cast<uint32_t>(t * 512 + (((fA >> 3) ^ (4 * (t & 3))) * 16) + (fA & 7) * 2);
+        fb[i] = static_cast<uint32_t>(t * 512 + (((fB >> 3) ^ (4 * (t & 3))) * 16) + (fB & 7) * 2) +
                 (DIAG ? 0u : static_cast<uint32_t>(kCSlab));
     }
-    typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-    auto frag = [&](const uint8_t *stage, uint32_t off, int ks) {
-        u16x8 v;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = *reinterpret_cast<const uint16_t *>(stage + off + (16 * ks + e) * 512);
-        return __builtin_bit_cast(bf16x8, v);
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    bf16x8 xa[2][4], xb[2][4];   // fragments: buffer 0 for the step ks = 0, buffer 1 for ks = 1
+    // fragment q of a step: A block q for q < 4, B block q - 4 otherwise
+    auto ldfrag = [&](int buf, uint32_t stage_off, int ks, int q) {
+        const uint32_t p0 = lds0 + stage_off + (q < 4 ? fa[q] : fb[q - 4]) + static_cast<uint32_t>(16 * ks * 512);
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(uintptr_t)p0);
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(uintptr_t)(p0 + 4 * 512));
+        const s16x4 v8[2] = {lo, hi};
+        const bf16x8 v = __builtin_bit_cast(bf16x8, v8);
+        if (q < 4)
+            xa[buf][q] = v;
+        else
+            xb[buf][q - 4] = v;
     };
 
     f32x16 acc[4][4];
@@ -188,34 +224,73 @@ __device__ __forceinline__ void act_cov_tile(const bf16_bits *__restrict__ a, in
         for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    auto mfma1 = [&](int buf, int idx) {
+        const int i = idx >> 2, j = idx & 3;
+        acc[i][j] = mfma32_bf16(xa[buf][i], xb[buf][j], acc[i][j]);
+    };
 
-    // Slab s lives in stage s % 4.  Before slab s is read, the copies in
-    // flight are those of slabs s + 1 and s + 2 (issued in the two previous
-    // steps): waiting until at most 2 NCP remain completes slab s.  The
-    // barrier also ends every wave's reads of stage (s - 1) % 4, which the
-    // copies of slab s + 3, issued next, overwrite.
-    issue(0, 0);
-    issue(1, 1);
-    issue(2, 2);
-    for (int s = 0; s < ns; ++s) {
-        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(2 * NCP) : "memory");
-        issue(s + 3, (s + 3) & 3);
-        const uint8_t *stage = smem + (s & 3) * kCStage;
-        // (the below-diagonal quadrant of a diagonal tile is computed too and
-        // discarded: a branch around the products would copy the accumulators)
+    // Slab s lives in stage s % 5; the copies of slab s + 4 go to stage
+    // (s - 1) % 5 while slab s is multiplied (that stage's last reads, the
+    // fragments of slab s - 1, completed before the previous barrier).  The
+    // step ks = 0 of a slab reads the fragments of its step ks = 1 and
+    // issues the copies; the barrier sits in the middle of step ks = 1, after
+    // each wave has waited for its copies of slab s + 1 (at most the three
+    // later slabs' copies in flight) and its fragment reads; the second half
+    // of step ks = 1 reads the fragments of slab s + 1's step ks = 0.  The
+    // order is fixed (scheduling barriers): groups of MFMAs with one
+    // fragment and one copy.  The list entry of a slab is loaded one step
+    // before its copies are issued.  (The below-diagonal quadrant of a
+    // diagonal tile is computed and discarded: a branch around the products
+    // would copy the accumulators.)
+    auto entry = [&](int s, int &sid, uint32_t &m) {
+        sid = s < ns ? slabs[s] : 0;
+        m = s < ns ? bits[s] : 0u;
+    };
+    {
+        int sid;
+        uint32_t m;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            bf16x8 xa[4], xb[4];
+        for (int s = 0; s < kCStages - 1; ++s) {
+            entry(s, sid, m);
+            const Slab sl = slab_of(sid, m);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                xa[i] = frag(stage, fa[i], ks);
-                xb[i] = frag(stage, fb[i], ks);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma32_bf16(xa[i], xb[j], acc[i][j]);
+            for (int c = 0; c < NCP; ++c) copy1(sl, s, c);
         }
+    }
+    int nsid;
+    uint32_t nm;
+    entry(kCStages - 1, nsid, nm);
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" :: "n"((kCStages - 2) * NCP) : "memory");
+#pragma unroll
+    for (int q = 0; q < 8; ++q) ldfrag(0, 0u, 0, q);
+    int cur = 0, nxt = kCStages - 1;   // stages of slab s and of slab s + 4
+    for (int s = 0; s < ns; ++s) {
+        const Slab sl = slab_of(nsid, nm);
+        entry(s + kCStages, nsid, nm);
+        const uint32_t cur_off = static_cast<uint32_t>(cur * kCStage);
+        const int nc = cur == kCStages - 1 ? 0 : cur + 1;   // stage of slab s + 1
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            mfma1(0, 2 * q);
+            mfma1(0, 2 * q + 1);
+            ldfrag(1, cur_off, 1, q);
+            if (q < NCP) copy1(sl, nxt, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) mfma1(1, q);
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"((kCStages - 2) * NCP) : "memory");
+        const uint32_t next_off = static_cast<uint32_t>(nc * kCStage);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            ldfrag(0, next_off, 0, q);
+            mfma1(1, 8 + q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        cur = nc;
+        nxt = nxt == kCStages - 1 ? 0 : nxt + 1;
     }
     // the copies past the last slab are still in flight
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
@@ -263,7 +338,7 @@ __global__ __launch_bounds__(256, 1) void k_act_cov_dma(const bf16_bits *__restr
                                                         float *__restrict__ C) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kCLds];
     int ti, tj;
-    tile_coords(blockIdx.x, nt, ti, tj);
+    if (!tile_of(blockIdx.x, nt, ti, tj)) return;
     const int ns = __builtin_amdgcn_readfirstlane(*n_slabs);
     if (ti == tj)
         act_cov_tile<true>(a, T, n, spe, slabs, bits, ns, ti * CT, tj * CT, C, smem);
@@ -668,7 +743,7 @@ hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const u
     hipLaunchKernelGGL(k_slab_prep, dim3(1), dim3(1024), 0, s, mask, B, T, spe, list, bits, count);
     if (bf16) {
         const int nt = (n + CT - 1) / CT;
-        hipLaunchKernelGGL(k_act_cov_dma, dim3(static_cast<unsigned>(nt * (nt + 1) / 2)), dim3(256), 0, s,
+        hipLaunchKernelGGL(k_act_cov_dma, dim3(static_cast<unsigned>(tile_slots(nt))), dim3(256), 0, s,
                            static_cast<const bf16_bits *>(a), T, n, spe, list, bits, count, nt, C);
     } else {
         const unsigned nb = static_cast<unsigned>((n + 15) / 16);
