@@ -19,8 +19,9 @@
 //     as zeros without a memory access.  The MFMA operands need 8
 //     consecutive tokens of one feature: each fragment is two transposed
 //     LDS reads (gfx950 ds_read_b64_tr_b16) of the token-major slab.  A
-//     diagonal tile has one operand.  The tile is added to C (upper part) and written mirrored to
-//     the lower part, so C stays exactly symmetric.
+//     diagonal tile has one operand.  The tile is staged in LDS, added to
+//     C's upper part with coalesced read-modify-writes and written mirrored
+//     to the lower part, so C stays exactly symmetric.
 //  1'. k_act_cov_f32: fp32 activations (small problems), one thread per entry.
 //
 // Top-k eigenvectors of C (n x n, symmetric PSD, fp32), by subspace
@@ -296,9 +297,10 @@ __device__ __forceinline__ void act_cov_tile(const bf16_bits *__restrict__ a, in
     asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
 
     // Epilogue, one half of the tile's rows (wm = h) at a time: the owning
-    // waves add their quadrants to C's upper part and stage the new values in
-    // LDS; then all threads write them mirrored (rows of the mirror are
-    // contiguous along the tile's rows).
+    // waves stage their quadrants in LDS; all threads then add the staged
+    // rows to C's upper part (coalesced 16-byte read-modify-writes, the new
+    // values written back to the staging) and write them mirrored (rows of
+    // the mirror run along the tile's rows).
     float *ct = reinterpret_cast<float *>(smem);
 #pragma unroll 1
     for (int h = 0; h < 2; ++h) {
@@ -311,14 +313,30 @@ __device__ __forceinline__ void act_cov_tile(const bf16_bits *__restrict__ a, in
                     for (int r = 0; r < 16; ++r) {
                         const int row = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                         const int col = wn * 128 + j * 32 + (lane & 31);
-                        const int gi = I + h * 128 + row, gj = J + col;
-                        if (gi < n && gj < n && (!DIAG || gi <= gj)) {
-                            float *p = C + static_cast<size_t>(gi) * n + gj;
-                            const float v = *p + acc[i][j][r];
-                            *p = v;
-                            ct[row * kCRow + col] = v;
-                        }
+                        ct[row * kCRow + col] = acc[i][j][r];
                     }
+        }
+        __syncthreads();
+        for (int e = tid; e < 128 * (CT / 4); e += 256) {
+            const int row = e / (CT / 4), c4 = 4 * (e % (CT / 4));
+            const int gi = I + h * 128 + row, gj = J + c4;
+            if (gi >= n) continue;
+            float *p = C + static_cast<size_t>(gi) * n + gj;
+            float *st = ct + row * kCRow + c4;
+            if (gj + 3 < n && (!DIAG || gi <= gj)) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(p) + f32x4{st[0], st[1], st[2], st[3]};
+                *reinterpret_cast<f32x4 *>(p) = v;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) st[u] = v[u];
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (gj + u < n && (!DIAG || gi <= gj + u)) {
+                        const float v = p[u] + st[u];
+                        p[u] = v;
+                        st[u] = v;
+                    }
+            }
         }
         __syncthreads();
         for (int e = tid; e < 128 * CT; e += 256) {
