@@ -7,11 +7,18 @@ lengths uniform on 128..2048, through all 224 linear layers (k_in = k_out = 16,
 store (32 grouped launches of 7 layers) and the 224 per-layer covariance
 updates.
 
+The logging leg's "pca" entry times the PCA initialisation of the
+projections on one of its batches: the KFAC factor SYRKs of the gate layer
+(n = 4096 and 14,336) and their top-16 eigenvectors.
+
 Influence leg (reported under "influence", scores/s): 1,024 test gradients
 against 500,000 stored training gradients of 57,344 dims -- damped-Cholesky
 preconditioning of the test gradients over 224 blocks of 256 (covariances of
 4,096 gradients, damping 0.1 x mean eigenvalue), the score GEMM and the
-per-query top-100.  Its "relatif" entry times l-RelatIF on the same store: the
+per-query top-100.  Its "out_of_core" entry streams 131,072 of the stored
+rows from pinned host memory through two device buffers (the store of the
+paper outgrows GPU memory) and compares the rate with a plain copy over the
+same link.  Its "relatif" entry times l-RelatIF on the same store: the
 self-influence of every training row (once per store) and the score pass with
 the 1/sqrt(self) scales applied before the top-100.
 
@@ -38,6 +45,7 @@ import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
+PCIE_PEAK_GBS = 64.0   # PCIe 5.0 x16, one direction
 METRIC = "projected per-example grads/sec (tokens/s) at Llama3-8B shapes; influence scores/sec"
 
 
@@ -267,6 +275,8 @@ def logging_leg(args, torch, P):
                      "bytes_per_launch": bytes_per_launch},
     }
     res["roofline"]["copy_gbs"] = copy_bandwidth(torch)
+    if args.pca:
+        res["pca"] = pca_sub_leg(args, torch, P, bufs[0], lens[0], masks[0], k)
     sample = None
     if args.cpu_baseline:
         n_b = min(args.cpu_batches, n_buf)
@@ -279,6 +289,45 @@ def logging_leg(args, torch, P):
     del bufs, store, S, ws
     torch.cuda.empty_cache()
     return res, sample
+
+
+def pca_sub_leg(args, torch, P, blk, lens, mask, k):
+    """PCA initialisation on the logging workload (Sec. 3.2): the KFAC factor
+    SYRK over one batch of B=8 ragged sequences for the gate layer's input x
+    (n = 4096) and output gradient dy (n = 14,336), each timed per call with
+    HIP events; then the top-k eigenvectors of each factor (30 subspace
+    iterations).  Algorithmic flops of a SYRK call: valid tokens x n (n + 1)
+    (the upper triangle of the symmetric product)."""
+    x, dy = blk[4]                      # gate: 4096 -> 14336
+    tokens = int(lens.sum())
+    out = {"layer": "gate (x: 4096, dy: 14336)", "valid_tokens": tokens, "k": k, "iters": 30}
+    for name, a in (("C_F", x), ("C_B", dy)):
+        n = a.shape[2]
+        C = torch.zeros((n, n), dtype=torch.float32, device="cuda")
+        ws = torch.empty(P.logra_act_cov_ws_size(a.shape[0], a.shape[1]), dtype=torch.uint8, device="cuda")
+        t = EventTimer(torch)
+        for timed in [False] + [True] * args.pca_reps:
+            e0 = t.start() if timed else None
+            P.logra_act_cov_accumulate(a, C, mask=mask, ws=ws)
+            if timed:
+                t.stop(e0)
+        Pk = torch.empty((k, n), dtype=torch.bfloat16, device="cuda")
+        pws = torch.empty(P.logra_pca_ws_size(n, k), dtype=torch.uint8, device="cuda")
+        te = EventTimer(torch)
+        for timed in (False, True):
+            e0 = te.start() if timed else None
+            P.logra_pca_topk(C, k, Pk, iters=30, ws=pws)
+            if timed:
+                te.stop(e0)
+        torch.cuda.synchronize()
+        flops = float(tokens) * n * (n + 1)
+        tf = flops / (t.mean_ms() * 1e-3) / 1e12
+        out[name] = {"n": n, "syrk_ms": t.mean_ms(), "pca_topk_ms": te.mean_ms(),
+                     "roofline": {"bound": "mfma", "achieved": tf, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                  "frac": tf / BF16_PEAK_TFLOPS, "flops_per_launch": flops,
+                                  "kernel": "k_act_cov_dma (masked bf16 SYRK)"}}
+        del C, ws, Pk, pws
+    return out
 
 
 def copy_bandwidth(torch, nbytes=2 << 30, reps=5):
@@ -403,6 +452,8 @@ def influence_leg(args, torch, P):
     }
     if args.relatif:
         res["relatif"] = relatif_sub_leg(args, torch, P, S, Nc, ex["damp"], pre, train, topk, sws, tv, ti)
+    if args.ooc_rows > 0:
+        res["out_of_core"] = out_of_core_sub_leg(args, torch, P, pre, train, topk)
     if args.vendor_gemm:
         # the same operands through torch's library GEMM (hipBLASLt) and through this
         # library's scores-only path, on a 125,000-row slice (context for the roofline)
@@ -470,6 +521,47 @@ def relatif_sub_leg(args, torch, P, S, Nc, damp, pre, train, topk, sws, tv, ti):
                     "included); each query batch pays the preconditioner and the scaled score pass"}
 
 
+def out_of_core_sub_leg(args, torch, P, pre, train, topk):
+    """The same scoring with the store in pinned host memory, streamed over
+    PCIe in chunks through two device staging buffers while the previous
+    chunk is scored.  Bound: the host-to-device link; the reference is a
+    plain host-to-device copy of the same bytes."""
+    n = min(args.ooc_rows, train.shape[0])
+    chunk = min(args.ooc_chunk, n)
+    Q, D = pre.shape
+    log(f"[inf] out-of-core: {n} rows in pinned host memory, chunks of {chunk}")
+    host = torch.empty((n, D), dtype=train.dtype, pin_memory=True)
+    host.copy_(train[:n])
+    tv = torch.empty((Q, topk), dtype=torch.float32, device=train.device)
+    ti = torch.empty((Q, topk), dtype=torch.int64, device=train.device)
+    ws = torch.empty(P.logra_influence_stream_ws_size(Q, chunk, D, P.BF16, topk), dtype=torch.uint8,
+                     device=train.device)
+    ts = []
+    for timed in (False, True):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        P.logra_influence_stream(pre, host, topk, tv, ti, chunk, ws=ws)   # synchronous
+        if timed:
+            ts.append(time.perf_counter() - t0)
+    dev_buf = train[:n]          # a plain copy of the same bytes over the same link
+    ct = EventTimer(torch)
+    for timed in (False, True):
+        e0 = ct.start() if timed else None
+        dev_buf.copy_(host, non_blocking=True)
+        if timed:
+            ct.stop(e0)
+    torch.cuda.synchronize()
+    nbytes = float(n) * D * 2
+    sec = float(np.mean(ts))
+    gbs = nbytes / sec / 1e9
+    copy_gbs = nbytes / (ct.mean_ms() * 1e-3) / 1e9
+    del host, ws
+    return {"rows": n, "chunk_rows": chunk, "ms_per_pass": sec * 1e3, "scores_per_s": Q * n / sec,
+            "roofline": {"bound": "pcie", "achieved": gbs, "peak": PCIE_PEAK_GBS, "unit": "GB/s",
+                         "frac": gbs / PCIE_PEAK_GBS, "plain_copy_gbs": copy_gbs,
+                         "kernel": "host-to-device stream of the store (copies overlapped with scoring)"}}
+
+
 def cpu_influence_baseline(sample):
     import oracle
     D = sample["D"]
@@ -499,6 +591,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
     ap.add_argument("--no-relatif", dest="relatif", action="store_false",
                     help="skip the l-RelatIF sub-leg (self-influence + scaled scores)")
+    ap.add_argument("--no-pca", dest="pca", action="store_false",
+                    help="skip the PCA sub-leg (KFAC factor SYRK and top-k eigenvectors)")
+    ap.add_argument("--pca-reps", type=int, default=3, help="timed SYRK calls per factor")
+    ap.add_argument("--ooc-rows", type=int, default=131072,
+                    help="rows of the out-of-core sub-leg's pinned host store (0 = skip)")
+    ap.add_argument("--ooc-chunk", type=int, default=32768, help="rows per streamed chunk")
     ap.add_argument("--vendor-gemm", action="store_true",
                     help="also time torch.matmul (hipBLASLt) on the score GEMM's operands")
     ap.add_argument("--cpu-batches", type=int, default=2, help="logging batches in the oracle sample")
@@ -532,6 +630,8 @@ def main():
         r, log_sample = logging_leg(args, torch, P)
         out.update(value=r["tokens_per_s"], ms_per_step=r["ms_per_step"], examples_per_s=r["examples_per_s"],
                    roofline=r["roofline"], proj_launch_ms=r["proj_launch_ms"], cov_launch_ms=r["cov_launch_ms"])
+        if "pca" in r:
+            out["pca"] = r["pca"]
     if args.leg in ("all", "influence"):
         r, inf_sample = influence_leg(args, torch, P)
         out["influence"] = r

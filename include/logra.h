@@ -249,6 +249,31 @@ int logra_influence_scores_scaled(const void *g_test_pre, int te_dtype, int64_t 
                                   int merge, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
+ * Out-of-core scoring.  The store of projected training gradients outgrows
+ * GPU memory at scale (Table 1: 3.5 TB for Llama3-8B on 1B tokens), and the
+ * paper hides the data IO by overlapping the reading of training gradients
+ * with the influence computation (Sec. 4.2, Efficiency).
+ *
+ * logra_influence_stream: the running top-k of logra_influence_scores over a
+ * store in PINNED HOST memory (hipHostMalloc; pageable memory is rejected),
+ * g_train_host [N][ld_tr] of tr_dtype, streamed over PCIe in chunks of
+ * chunk_rows rows: chunk c is copied into device staging buffer c % 2 on a
+ * copy stream while chunk c - 1 is scored on `stream` (events order the
+ * reuse of the two buffers).  topk_val / topk_idx [Q][topk] (device) get the
+ * top-k over all N rows with global indices 0..N-1, exactly as one
+ * logra_influence_scores call over the whole store would give them (N = 0:
+ * padding).  copy_stream: a hipStream_t of the caller, or NULL for one
+ * created for the call.  ws: logra_influence_stream_ws_size(Q, chunk_rows,
+ * D, tr_dtype, topk) bytes (two staging buffers and one chunk's scoring
+ * workspace).  SYNCHRONOUS: returns when the top-k is complete.
+ * ---------------------------------------------------------------------- */
+size_t logra_influence_stream_ws_size(int Q, int64_t chunk_rows, int D, int tr_dtype, int topk);
+int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q, const void *g_train_host,
+                           int tr_dtype, int64_t ld_tr, int64_t N, int D, int64_t chunk_rows, int topk,
+                           float *topk_val, int64_t *topk_idx, void *ws, size_t ws_bytes, void *stream,
+                           void *copy_stream);
+
+/* ------------------------------------------------------------------------
  * PCA initialisation of the projections (Sec. 3.2).  KFAC approximates a
  * layer's Hessian block by C_F (x) C_B, the Kronecker product of the
  * uncentered covariances of the layer's forward activations x and backward

@@ -37,6 +37,7 @@ EXPORTED = (
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
     "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_pca_ws_size", "logra_pca_topk",
+    "logra_influence_stream_ws_size", "logra_influence_stream",
 )
 
 
@@ -96,7 +97,11 @@ def lib():
         L.logra_pca_ws_size.argtypes = [i32, i32]
         L.logra_pca_ws_size.restype = sz
         L.logra_pca_topk.argtypes = [vp, i32, i32, i32, vp, i32, i64, vp, vp, sz, vp]
-        for name in ("logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
+        L.logra_influence_stream_ws_size.argtypes = [i32, i64, i32, i32, i32]
+        L.logra_influence_stream_ws_size.restype = sz
+        L.logra_influence_stream.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, i32, vp, vp, vp, sz,
+                                             vp, vp]
+        for name in ("logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
@@ -319,3 +324,24 @@ def logra_pca_topk(C, k: int, P, eigvals=None, iters: int = 30, ws=None, stream=
     ws, wsb = _workspace(logra_pca_ws_size(n, k), C.device, ws)
     _check(lib().logra_pca_topk(_ptr(C), n, int(k), int(iters), _ptr(P), _dtype_code(P), ld_p, _ptr(eigvals),
                                 _ptr(ws), wsb, _stream(stream)))
+
+
+def logra_influence_stream_ws_size(Q, chunk_rows, D, tr_dtype, topk) -> int:
+    return int(lib().logra_influence_stream_ws_size(Q, chunk_rows, D, tr_dtype, topk))
+
+
+def logra_influence_stream(g_test_pre, g_train_host, topk: int, topk_val, topk_idx, chunk_rows: int, ws=None,
+                           stream=None, copy_stream=None):
+    """Running top-k of the scores of g_test_pre [Q, D] (device) against a store g_train_host
+    [N, D] in pinned host memory (torch pin_memory=True), streamed in chunks of chunk_rows rows
+    through two device staging buffers.  Synchronous."""
+    Q, D = g_test_pre.shape
+    N = g_train_host.shape[0]
+    ld_te = _rows(g_test_pre, D) if Q > 0 else D
+    ld_tr = _rows(g_train_host, D) if N > 0 else D
+    code = _dtype_code(g_train_host)
+    ws, wsb = _workspace(logra_influence_stream_ws_size(Q, chunk_rows, D, code, topk), g_test_pre.device, ws)
+    cs = None if copy_stream is None else ctypes.c_void_p(copy_stream.cuda_stream)
+    _check(lib().logra_influence_stream(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q, _ptr(g_train_host),
+                                        code, ld_tr, N, D, int(chunk_rows), int(topk), _ptr(topk_val),
+                                        _ptr(topk_idx), _ptr(ws), wsb, _stream(stream), cs))

@@ -49,6 +49,21 @@ int check_dev(const void *p, const char *name, size_t align) {
     return LOGRA_OK;
 }
 
+// Pinned (page-locked) host memory, which asynchronous copies need.
+int check_pinned(const void *p, const char *name, size_t align) {
+    if (p == nullptr) return fail(LOGRA_ERR_INVALID_ARG, "%s is NULL", name);
+    if ((reinterpret_cast<uintptr_t>(p) & (align - 1)) != 0)
+        return fail(LOGRA_ERR_INVALID_ARG, "%s is not %zu-byte aligned", name, align);
+    hipPointerAttribute_t attr;
+    std::memset(&attr, 0, sizeof attr);
+    const hipError_t e = hipPointerGetAttributes(&attr, p);
+    if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(LOGRA_ERR_INVALID_ARG, "%s is not pinned host memory (allocate it with hipHostMalloc)", name);
+    }
+    return LOGRA_OK;
+}
+
 int hip_fail(hipError_t e, const char *what) {
     return fail(LOGRA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
@@ -396,6 +411,94 @@ int logra_self_influence_blocks(const float *S, int D, int n_blocks, int64_t N, 
     if (e != hipSuccess) return hip_fail(e, "self-influence launch");
     // synchronous, like the preconditioner, so that a non-positive pivot is reported
     return report_not_pd(ws, D, n_blocks, s);
+}
+
+// ---------------------------------------------------------------------------
+// Out-of-core scoring: the store in pinned host memory, streamed in chunks.
+size_t logra_influence_stream_ws_size(int Q, int64_t chunk_rows, int D, int tr_dtype, int topk) {
+    if (Q < 0 || chunk_rows <= 0 || D <= 0 || !valid_dtype(tr_dtype) || topk <= 0) return 0;
+    const size_t stage = round256(static_cast<size_t>(chunk_rows) * D * esize(tr_dtype));
+    return 2 * stage + logra_influence_ws_size(Q, chunk_rows, topk, 0);
+}
+
+int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q, const void *g_train_host,
+                           int tr_dtype, int64_t ld_tr, int64_t N, int D, int64_t chunk_rows, int topk,
+                           float *topk_val, int64_t *topk_idx, void *ws, size_t ws_bytes, void *stream,
+                           void *copy_stream) {
+    if (!valid_dtype(te_dtype) || !valid_dtype(tr_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (te_dtype != tr_dtype) return fail(LOGRA_ERR_UNSUPPORTED, "test and train dtypes must match");
+    if (Q < 0 || N < 0 || D <= 0 || chunk_rows <= 0)
+        return fail(LOGRA_ERR_INVALID_ARG, "need Q >= 0, N >= 0, D > 0, chunk_rows > 0");
+    if (topk <= 0) return fail(LOGRA_ERR_INVALID_ARG, "topk must be > 0");
+    if (topk > LOGRA_MAX_TOPK) return fail(LOGRA_ERR_UNSUPPORTED, "topk must be <= %d", LOGRA_MAX_TOPK);
+    if (ld_tr < D) return fail(LOGRA_ERR_INVALID_ARG, "ld_tr must be >= D");
+    if (chunk_rows > INT32_MAX) return fail(LOGRA_ERR_UNSUPPORTED, "chunk_rows must be < 2^31");
+    if (tr_dtype == LOGRA_BF16 && (D % 8 || ld_te % 8))
+        return fail(LOGRA_ERR_INVALID_ARG, "bf16 scores need D and ld_te multiples of 8");
+    if (Q == 0) return ok();
+    const size_t es = esize(tr_dtype);
+    if (N > 0) TRY(check_pinned(g_train_host, "g_train_host", es == 2 ? 16 : 4));
+    TRY(check_dev(topk_val, "topk_val", 4));
+    TRY(check_dev(topk_idx, "topk_idx", 8));
+    const size_t need = logra_influence_stream_ws_size(Q, chunk_rows, D, tr_dtype, topk);
+    TRY(check_ws(ws, ws_bytes, need));
+    const hipStream_t cs = static_cast<hipStream_t>(stream);
+    const size_t stage = round256(static_cast<size_t>(chunk_rows) * D * es);
+    char *buf[2] = {static_cast<char *>(ws), static_cast<char *>(ws) + stage};
+    void *iws = static_cast<char *>(ws) + 2 * stage;
+    const size_t iws_bytes = ws_bytes - 2 * stage;
+    if (N == 0)   // an empty store: the top-k padding only
+        return logra_influence_scores(g_test_pre, te_dtype, ld_te, Q, buf[0], tr_dtype, D, 0, D, 0, nullptr, 1,
+                                      topk, topk_val, topk_idx, 0, iws, iws_bytes, stream);
+
+    // Copy stream (created for the call unless given) and the events that
+    // order the double buffer: chunk c fills buffer c % 2 once the scoring of
+    // chunk c - 2 has released it; scoring waits for the fill.
+    hipStream_t xs = static_cast<hipStream_t>(copy_stream);
+    const bool own = xs == nullptr;
+    hipError_t e = hipSuccess;
+    if (own && (e = hipStreamCreateWithFlags(&xs, hipStreamNonBlocking)) != hipSuccess)
+        return hip_fail(e, "copy stream");
+    hipEvent_t filled[2] = {nullptr, nullptr}, freed[2] = {nullptr, nullptr};
+    int rc = LOGRA_OK;
+    for (int b = 0; b < 2 && e == hipSuccess; ++b) {
+        e = hipEventCreateWithFlags(&filled[b], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&freed[b], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) rc = hip_fail(e, "event");
+    const int64_t chunks = (N + chunk_rows - 1) / chunk_rows;
+    for (int64_t c = 0; c < chunks && rc == LOGRA_OK; ++c) {
+        const int b = static_cast<int>(c & 1);
+        const int64_t r0 = c * chunk_rows, rows = N - r0 < chunk_rows ? N - r0 : chunk_rows;
+        const char *src = static_cast<const char *>(g_train_host) + static_cast<size_t>(r0) * ld_tr * es;
+        if (c >= 2 && (e = hipStreamWaitEvent(xs, freed[b], 0)) != hipSuccess) {
+            rc = hip_fail(e, "wait for a free buffer");
+            break;
+        }
+        e = ld_tr == D ? hipMemcpyAsync(buf[b], src, static_cast<size_t>(rows) * D * es, hipMemcpyHostToDevice, xs)
+                       : hipMemcpy2DAsync(buf[b], D * es, src, ld_tr * es, D * es, static_cast<size_t>(rows),
+                                          hipMemcpyHostToDevice, xs);
+        if (e == hipSuccess) e = hipEventRecord(filled[b], xs);
+        if (e == hipSuccess) e = hipStreamWaitEvent(cs, filled[b], 0);
+        if (e != hipSuccess) {
+            rc = hip_fail(e, "chunk copy");
+            break;
+        }
+        rc = logra_influence_scores(g_test_pre, te_dtype, ld_te, Q, buf[b], tr_dtype, D, rows, D, r0, nullptr, 1,
+                                    topk, topk_val, topk_idx, c > 0, iws, iws_bytes, stream);
+        if (rc == LOGRA_OK && (e = hipEventRecord(freed[b], cs)) != hipSuccess) rc = hip_fail(e, "event record");
+    }
+    // synchronous: the buffers, events and (own) stream live until the last chunk is scored
+    e = hipStreamSynchronize(cs);
+    if (rc == LOGRA_OK && e != hipSuccess) rc = hip_fail(e, "stream synchronize");
+    e = hipStreamSynchronize(xs);
+    if (rc == LOGRA_OK && e != hipSuccess) rc = hip_fail(e, "copy stream synchronize");
+    for (int b = 0; b < 2; ++b) {
+        if (filled[b]) (void)hipEventDestroy(filled[b]);
+        if (freed[b]) (void)hipEventDestroy(freed[b]);
+    }
+    if (own) (void)hipStreamDestroy(xs);
+    return rc == LOGRA_OK ? ok() : rc;
 }
 
 size_t logra_act_cov_ws_size(int B, int T) {

@@ -176,3 +176,21 @@ def test_pca_entry_points_validation(L):
     assert g(fake, 10, 11, 30, fake, 0, 10, None, None, 0, None) == P.ERR_INVALID_ARG
     assert g(fake, 100, 8, 0, fake, 0, 100, None, None, 0, None) == P.ERR_INVALID_ARG
     assert g(fake, 100, 8, 30, fake, 0, 99, None, None, 0, None) == P.ERR_INVALID_ARG
+
+
+def test_influence_stream_ws_and_validation(L):
+    # two staging buffers of chunk_rows x D plus one chunk's scoring workspace
+    assert P.logra_influence_stream_ws_size(16, 1000, 64, P.BF16, 10) == (
+        2 * ((1000 * 64 * 2 + 255) // 256 * 256) + P.logra_influence_ws_size(16, 1000, 10, 0))
+    assert P.logra_influence_stream_ws_size(16, 0, 64, P.BF16, 10) == 0
+    f = L.logra_influence_stream
+    args = lambda **kw: [kw.get(k, v) for k, v in dict(
+        te=None, tdt=1, ld_te=64, Q=2, tr=None, rdt=1, ld_tr=64, N=10, D=64, chunk=4, topk=3, tv=None,
+        ti=None, ws=None, wsb=0, st=None, cst=None).items()]
+    assert f(*args(rdt=0)) == P.ERR_UNSUPPORTED
+    assert f(*args(topk=0)) == P.ERR_INVALID_ARG
+    assert f(*args(topk=1025)) == P.ERR_UNSUPPORTED
+    assert f(*args(chunk=0)) == P.ERR_INVALID_ARG
+    assert f(*args(ld_tr=32)) == P.ERR_INVALID_ARG
+    assert f(*args(D=60, ld_te=60, ld_tr=60)) == P.ERR_INVALID_ARG
+    assert f(*args(Q=0)) == P.OK

@@ -321,3 +321,60 @@ def test_relatif_bench_launch(score_store):
         err = float(np.max(np.abs(row[js].astype(np.float64) - want[qi]) / bound))
         say(f"  query {q}: normalised err on {len(js)} sampled scaled scores {err:.2e}")
         assert err <= 1e-3
+
+
+def test_act_cov_gate_bench_launch():
+    """The KFAC factor SYRKs that bench.py times: the gate layer's x
+    (n = 4096) and dy (n = 14,336) over one logging batch (B=8, T=2048,
+    lengths U{128..2048}); entries on a random 48-feature subset against the
+    oracle on those features' host copies."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, normwise, say
+    w = W.WORKLOADS["llama3_8b_stream"]
+    B, T = w.B, w.T
+    lens = W.lengths(W.rng(0, 200, 0), B, w.len_lo, w.len_hi)
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = torch.from_numpy(mask_np).cuda()
+    gen = W.torch_generator(0, 450)
+    for name, n, std in (("x", 4096, w.x_std), ("dy", 14336, w.dy_std)):
+        say(f"[full act cov] gate {name}: B={B} T={T} n={n}, {int(lens.sum())} valid tokens")
+        a = torch.empty((B, T, n), dtype=torch.bfloat16, device="cuda")
+        W.device_normal_(a, std, gen)
+        C = torch.zeros((n, n), dtype=torch.float32, device="cuda")
+        P.logra_act_cov_accumulate(a, C, mask=mask)
+        torch.cuda.synchronize()
+        F = np.sort(W.rng(0, 451, n).choice(n, size=48, replace=False))
+        Fd = torch.from_numpy(F).cuda()
+        got = host(C[Fd][:, Fd])
+        want = oracle.act_cov(host(a[:, :, Fd].contiguous()), mask_np)
+        err = normwise(got, want)
+        say(f"  48 x 48 sampled entries: normwise err {err:.2e}")
+        assert err <= 1e-5
+        assert np.array_equal(host(C[Fd][:, Fd]), host(C[:, Fd][Fd]).T)
+        del a, C
+
+
+def test_pca_topk_n4096():
+    """The top-16 eigenvectors of a 4096 x 4096 covariance (the gate layer's
+    C_F size) with a geometric spectrum (neighbour ratio 0.95), 30
+    iterations, against numpy's float64 eigh on the same fp32 matrix."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    n, k = 4096, 16
+    say(f"[full pca] n={n} k={k}")
+    C = W.spectral_matrix(65, n, 0.95, scale=1e3)
+    Pt = torch.empty((k, n), dtype=torch.float32, device="cuda")
+    ev = torch.empty(k, dtype=torch.float32, device="cuda")
+    P.logra_pca_topk(dev(C), k, Pt, eigvals=ev, iters=30)
+    torch.cuda.synchronize()
+    got, ev = host(Pt), host(ev)
+    want, wev = oracle.pca_topk(C.astype(np.float64), k)
+    err = 0.0
+    for r in range(k):
+        s = 1.0 if np.dot(got[r].astype(np.float64), want[r]) >= 0 else -1.0
+        err = max(err, float(np.max(np.abs(s * got[r] - want[r]))))
+    eerr = float(np.max(np.abs(ev - wev) / wev))
+    say(f"  max entry err {err:.2e}, eigenvalue err {eerr:.2e}")
+    assert err <= 1e-4 and eerr <= 1e-5
