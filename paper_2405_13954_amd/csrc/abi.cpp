@@ -147,6 +147,17 @@ int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dt
         TRY(check_dev(d.p_in, "p_in", 16));
         TRY(check_dev(d.p_out, "p_out", 16));
         TRY(check_dev(d.g_out, "g_out", esize(g_dtype)));
+        // the last element written must lie in device memory too (a wrong row
+        // stride is reported instead of faulting the kernel)
+        const double span = (static_cast<double>(B - 1) * static_cast<double>(g_ld) + k_in * k_out) *
+                            static_cast<double>(esize(g_dtype));
+        if (span > 281474976710656.0)   // 2^48 bytes: beyond any device allocation
+            return fail(LOGRA_ERR_INVALID_ARG, "g_out rows at stride g_ld = %lld exceed device memory",
+                        static_cast<long long>(g_ld));
+        const char *g_end = static_cast<const char *>(d.g_out) +
+                            (static_cast<int64_t>(B - 1) * g_ld + static_cast<int64_t>(k_in) * k_out - 1) *
+                                static_cast<int64_t>(esize(g_dtype));
+        TRY(check_dev(g_end, "the last row of g_out", 1));
         grp.layer[l] = {d.x, d.dy, d.p_in, d.p_out, d.g_out, d.n_in, d.n_out};
     }
     if (mask) TRY(check_dev(mask, "mask", 1));

@@ -11,7 +11,10 @@
 //     the ordered list of 64-token tiles holding at least one valid token.
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
 //     = one contraction chunk (<= 4096 columns) of one side (x or dy) of one
-//     listed tile.  Workgroups take items from an atomic counter as they
+//     listed tile.  Layers given the same x tensor (q/k/v, gate/up of a
+//     transformer block) share their x items: one pass over the chunk feeds
+//     up to three projections P_in (k <= 32), each with the same per-element
+//     sums as a pass of its own.  Workgroups take items from an atomic counter as they
 //     finish (items differ up to 4x in columns and workgroups in speed, so a
 //     static assignment leaves a long tail).  The four waves deal the chunk's 32-wide steps
 //     round-robin; each lane feeds a 128-bit buffer load straight into its
@@ -60,6 +63,8 @@ constexpr int NT = NW * kWave;            // threads per workgroup
 __host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? 4096 : LOGRA_PROJ_CHUNK; }
 __host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGRA_PROJ_STAGES; }
 
+constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
+
 struct ChunkLayer {
     const void *x;
     const void *dy;
@@ -67,8 +72,11 @@ struct ChunkLayer {
     const void *p_out;
     int64_t part_begin;  // first float of this layer's chunk partials
     int n_in, n_out;
-    int c_in, c_out;     // chunks of the x side and of the dy side
-    int slot_begin;      // chunk slots of the layers before this one
+    int c_in, c_out;     // chunks of the x side and of the dy side (partial slots per tile)
+    int x_items;         // x-side work slots: c_in for the first layer of a shared x, else 0
+    int slot_begin;      // work slots of the layers before this one
+    uint8_t share_n;     // layers whose x' this layer's x items produce (itself first)
+    uint8_t share[kMaxShare];
 };
 
 struct ProjArgs {
@@ -121,31 +129,37 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[MB][KT], const u32x4 (&xa)
                 acc[m][j] = mfma16_f32(__uint_as_float(xa[m][e]), __uint_as_float(pb[j][e]), acc[m][j]);
 }
 
-// One wave's share of  A'[TT x 16KT] = A[TT x nk] * P[k x nk]^T, A and P with
-// row strides lda and ldp.  Contraction steps s = wave, wave + NW, ... .
-// Every load is unconditional (out-of-range offsets read zeros), and the
-// ST-stage register pipeline keeps ST-1 steps in flight while a step
-// multiplies.  Each wave's step count is rounded up to a multiple of ST with
-// empty steps (no memory access, zero operands), so the loop body has no exits.
-template <int KT, typename TIn, int ST>
-__device__ __forceinline__ void project_part(f32x4 (&acc)[MB][KT], const TIn *A, int lda, const TIn *P,
-                                             int ldp, int nk, int k, const bool (&tok_ok)[MB], int wave,
-                                             int lane) {
+// One wave's share of  A'_s[TT x 16KT] = A[TT x nk] * P_s[k x nk]^T for the
+// S projections P_s (s < S) of one operand A (a shared input: one pass over
+// A; a missing P_s reads zeros), A and P_s with row strides lda and ldp.
+// Contraction steps s = wave, wave + NW, ... .  Every load is unconditional
+// (out-of-range offsets read zeros), and the ST-stage register pipeline
+// keeps ST-1 steps in flight while a step multiplies.  Each wave's step
+// count is rounded up to a multiple of ST with empty steps (no memory access,
+// zero operands), so the loop body has no exits.  Result column block
+// s * KT + j of acc holds block j of A'_s.
+template <int KT, int S, typename TIn, int ST>
+__device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn *A, int lda,
+                                             const TIn *const (&P)[S], int ldp, int nk, int k,
+                                             const bool (&tok_ok)[MB], int wave, int lane) {
     constexpr int E = InTraits<TIn>::kElems;
-    constexpr int S = InTraits<TIn>::kStep;
+    constexpr int SS = InTraits<TIn>::kStep;
     constexpr uint32_t ES = sizeof(TIn);
     const int row = lane & 15;
     const int kg = lane >> 4;
 #pragma unroll
     for (int m = 0; m < MB; ++m)
 #pragma unroll
-        for (int j = 0; j < KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int nsteps = (nk + S - 1) / S;
+        for (int j = 0; j < S * KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nsteps = (nk + SS - 1) / SS;
     int s = wave;
     if (s >= nsteps) return;
 
     const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * ES);
-    const auto rp = buf_rsrc(P, (static_cast<uint32_t>(k - 1) * ldp + nk) * ES);
+    __amdgpu_buffer_rsrc_t rp[S];
+#pragma unroll
+    for (int q = 0; q < S; ++q)
+        rp[q] = buf_rsrc(P[q] ? P[q] : A, P[q] ? (static_cast<uint32_t>(k - 1) * ldp + nk) * ES : 0u);
     uint32_t aoff[MB], poff[KT];
 #pragma unroll
     for (int m = 0; m < MB; ++m)
@@ -154,26 +168,28 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][KT], const TIn *A,
     for (int j = 0; j < KT; ++j)
         poff[j] = (16 * j + row < k) ? (static_cast<uint32_t>(16 * j + row) * ldp + kg * E) * ES : kBufOOB;
 
-    auto load = [&](int st, u32x4(&xa)[MB], u32x4(&pb)[KT]) {
-        const bool in_k = st * S + kg * E < nk;   // false past the last step: all lanes zero
-        const uint32_t koff = static_cast<uint32_t>(st * S) * ES;
+    auto load = [&](int st, u32x4(&xa)[MB], u32x4(&pb)[S * KT]) {
+        const bool in_k = st * SS + kg * E < nk;   // false past the last step: all lanes zero
+        const uint32_t koff = static_cast<uint32_t>(st * SS) * ES;
 #pragma unroll
         for (int m = 0; m < MB; ++m)
             xa[m] = LOGRA_PROJ_NT ? buf_ld128_nt(ra, in_k ? aoff[m] + koff : kBufOOB)
                                   : buf_ld128(ra, in_k ? aoff[m] + koff : kBufOOB);
 #pragma unroll
-        for (int j = 0; j < KT; ++j) pb[j] = buf_ld128(rp, in_k ? poff[j] + koff : kBufOOB);
+        for (int q = 0; q < S; ++q)
+#pragma unroll
+            for (int j = 0; j < KT; ++j) pb[q * KT + j] = buf_ld128(rp[q], in_k ? poff[j] + koff : kBufOOB);
     };
 
     const int iters = ((nsteps - wave + NW - 1) / NW + ST - 1) / ST;
-    u32x4 xa[ST][MB], pb[ST][KT];
+    u32x4 xa[ST][MB], pb[ST][S * KT];
 #pragma unroll
     for (int i = 0; i < ST - 1; ++i) load(s + i * NW, xa[i], pb[i]);
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int i = 0; i < ST; ++i) {
             load(s + (i + ST - 1) * NW, xa[(i + ST - 1) % ST], pb[(i + ST - 1) % ST]);
-            mma_step<KT>(acc, xa[i], pb[i], TIn{});
+            mma_step<S * KT>(acc, xa[i], pb[i], TIn{});
         }
         s += ST * NW;
     }
@@ -204,16 +220,18 @@ __device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, in
 
 // One chunk item (see the file comment).  Returns without a barrier when the
 // tile is fully masked; every thread of the workgroup takes the same path.
-template <int KT, typename TIn>
+// An x-side item of a layer whose x is shared produces the x' partials of
+// every layer sharing it (S >= share_n).
+template <int KT, int S, typename TIn>
 __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int count, f32x4 *slot, int lane,
                                            int wave) {
-    const int rank = item / count;              // position of the chunk slot in processing order
+    const int rank = item / count;              // position of the work slot in processing order
     const int j = item - rank * count;          // listed tile
-    const int gslot = a.ordered ? a.slot_order[rank] : rank;   // chunk slot over all layers
+    const int gslot = a.ordered ? a.slot_order[rank] : rank;   // work slot over all layers
     int l = 0;
     while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
     const ChunkLayer &L = a.layer[l];
-    const int cs = gslot - L.slot_begin;        // chunk slot of the layer: x chunks, then dy chunks
+    const int cs = gslot - L.slot_begin;        // work slot of the layer: x items, then dy chunks
     const int bt = a.tiles ? a.tiles[j] : j;
     const int b = bt / a.tpe, tile = bt - b * a.tpe;
 
@@ -221,27 +239,34 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     lane_tokens(a, b, tile * TT, lane, tok_ok);  // listed tiles have at least one valid token
     __syncthreads();   // the previous item's reads of `slot` are done
 
-    const bool xside = cs < L.c_in;
-    const int c = xside ? cs : cs - L.c_in;
+    const bool xside = cs < L.x_items;
+    const int c = xside ? cs : cs - L.x_items;
     const int n = xside ? L.n_in : L.n_out;
     const int k = xside ? a.k_in : a.k_out;
+    const int nmem = xside ? L.share_n : 1;
     const int col0 = c * a.ck;
     const int nk = min(a.ck, n - col0);
     const size_t tok0 = static_cast<size_t>(b) * a.T + static_cast<size_t>(tile) * TT;
     const TIn *A = static_cast<const TIn *>(xside ? L.x : L.dy) + tok0 * n + col0;
-    const TIn *P = static_cast<const TIn *>(xside ? L.p_in : L.p_out) + col0;
+    const TIn *P[S];
+#pragma unroll
+    for (int q = 0; q < S; ++q) {
+        const void *pm = q >= nmem ? nullptr : xside ? a.layer[L.share[q]].p_in : L.p_out;
+        P[q] = pm ? static_cast<const TIn *>(pm) + col0 : nullptr;
+    }
 
-    f32x4 acc[MB][KT];
-    project_part<KT, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
+    f32x4 acc[MB][S * KT];
+    project_part<KT, S, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
 
-    // fold the waves in the order ((w3 + w2) + w1) + w0, then write the
+    // fold the waves in the order ((w3 + w2) + w1) + w0, then write each
     // result in the MFMA layout: element (m, j) of lane l at [(m*KT + j)*64 + l]
+    // of the partial slot of its layer
     f32x4 *my = slot + lane;
     if (wave == NW - 1) {
 #pragma unroll
         for (int m = 0; m < MB; ++m)
 #pragma unroll
-            for (int j = 0; j < KT; ++j) my[(m * KT + j) * kWave] = acc[m][j];
+            for (int j = 0; j < S * KT; ++j) my[(m * S * KT + j) * kWave] = acc[m][j];
     }
     __syncthreads();
 #pragma unroll
@@ -250,17 +275,26 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 #pragma unroll
             for (int m = 0; m < MB; ++m)
 #pragma unroll
-                for (int j = 0; j < KT; ++j) my[(m * KT + j) * kWave] = my[(m * KT + j) * kWave] + acc[m][j];
+                for (int j = 0; j < S * KT; ++j)
+                    my[(m * S * KT + j) * kWave] = my[(m * S * KT + j) * kWave] + acc[m][j];
         }
         __syncthreads();
     }
     if (wave == 0) {
-        f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + L.part_begin +
-                                               (static_cast<size_t>(bt) * (L.c_in + L.c_out) + cs) * (TT * 16 * KT));
 #pragma unroll
-        for (int m = 0; m < MB; ++m)
+        for (int q = 0; q < S; ++q) {
+            if (q >= nmem) break;
+            const ChunkLayer &M = xside ? a.layer[L.share[q]] : L;
+            const int pslot = xside ? c : M.c_in + c;
+            f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + M.part_begin +
+                                                   (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) *
+                                                       (TT * 16 * KT));
 #pragma unroll
-            for (int j = 0; j < KT; ++j) dst[(m * KT + j) * kWave + lane] = my[(m * KT + j) * kWave] + acc[m][j];
+            for (int m = 0; m < MB; ++m)
+#pragma unroll
+                for (int jj = 0; jj < KT; ++jj)
+                    dst[(m * KT + jj) * kWave + lane] = my[(m * S * KT + q * KT + jj) * kWave] + acc[m][q * KT + jj];
+        }
     }
 }
 
@@ -269,9 +303,9 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 // unclaimed item from the work counter.  Claiming only when free keeps the
 // tail to at most one item per workgroup.  The loop ends once the counter
 // passes the item count, which every workgroup reaches.
-template <int KT, typename TIn>
+template <int KT, int S, typename TIn>
 __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(ProjArgs a) {
-    __shared__ f32x4 slot[MB * KT * kWave];   // cross-wave fold
+    __shared__ f32x4 slot[MB * S * KT * kWave];   // cross-wave fold
     __shared__ int next;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -279,7 +313,7 @@ __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(Proj
     const int items = count * a.slots;
     int item = blockIdx.x;
     while (item < items) {
-        chunk_item<KT, TIn>(a, item, count, slot, lane, wave);
+        chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave);
         if (tid == 0) next = static_cast<int>(gridDim.x) + atomicAdd(a.work, 1);
         __syncthreads();
         item = next;
@@ -468,9 +502,44 @@ Plan plan_group(const int *n_in, const int *n_out, int n_layers, int B, int T, i
     return p;
 }
 
+// Shared inputs: a layer whose x is the same tensor (same pointer and
+// width) as an earlier layer's joins that layer's share set (up to
+// kMaxShare; k <= 32 only), whose x items then project x once for every
+// member.  Sets x_items, share_n, share and the work slots; returns the
+// number of work slots and the largest share set.
+int plan_shares(ProjArgs &a, int n_layers, int KT, int &smax) {
+    smax = 1;
+    for (int l = 0; l < n_layers; ++l) {
+        ChunkLayer &L = a.layer[l];
+        L.share_n = 0;
+        int owner = -1;
+        if (KT <= 2)
+            for (int o = 0; o < l && owner < 0; ++o)
+                if (a.layer[o].share_n > 0 && a.layer[o].share_n < kMaxShare && a.layer[o].x == L.x &&
+                    a.layer[o].n_in == L.n_in)
+                    owner = o;
+        if (owner >= 0) {
+            ChunkLayer &O = a.layer[owner];
+            O.share[O.share_n++] = static_cast<uint8_t>(l);
+            smax = O.share_n > smax ? O.share_n : smax;
+            L.x_items = 0;
+        } else {
+            L.share_n = 1;
+            L.share[0] = static_cast<uint8_t>(l);
+            L.x_items = L.c_in;
+        }
+    }
+    int slots = 0;
+    for (int l = 0; l < n_layers; ++l) {
+        a.layer[l].slot_begin = slots;
+        slots += a.layer[l].x_items + a.layer[l].c_out;
+    }
+    return slots;
+}
+
 // Resident workgroups of a kernel on the current device (computed once per
 // device and kernel).
-template <int KT, typename TIn>
+template <int KT, int S, typename TIn>
 int resident_groups() {
     static int cache[64] = {0};
     int dev = 0;
@@ -480,7 +549,7 @@ int resident_groups() {
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void *>(k_project_chunks<KT, TIn>), NT, 0) != hipSuccess ||
+                &per_cu, reinterpret_cast<const void *>(k_project_chunks<KT, S, TIn>), NT, 0) != hipSuccess ||
             per_cu <= 0)
             per_cu = 1;
         cache[dev] = cus * per_cu;
@@ -488,11 +557,22 @@ int resident_groups() {
     return cache[dev];
 }
 
-template <int KT, typename TIn>
-void launch_chunks(const ProjArgs &a, int max_items, hipStream_t s) {
-    const int grid = max_items < resident_groups<KT, TIn>() ? max_items : resident_groups<KT, TIn>();
-    hipLaunchKernelGGL((k_project_chunks<KT, TIn>), dim3(grid), dim3(NT), 0, s, a);
+template <int KT, int S, typename TIn>
+void launch_chunks_s(const ProjArgs &a, int max_items, hipStream_t s) {
+    const int cap = resident_groups<KT, S, TIn>();
+    hipLaunchKernelGGL((k_project_chunks<KT, S, TIn>), dim3(max_items < cap ? max_items : cap), dim3(NT), 0, s, a);
 }
+
+template <int KT, typename TIn>
+void launch_chunks(const ProjArgs &a, int max_items, int smax, hipStream_t s) {
+    if constexpr (KT <= 2) {
+        if (smax == 3) return launch_chunks_s<KT, 3, TIn>(a, max_items, s);
+        if (smax == 2) return launch_chunks_s<KT, 2, TIn>(a, max_items, s);
+    }
+    launch_chunks_s<KT, 1, TIn>(a, max_items, s);
+}
+
+static_assert(sizeof(ProjArgs) <= 3840, "kernel arguments must stay well under the 4 KB limit");
 
 }  // namespace
 
@@ -521,24 +601,25 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     const Plan p = plan_group(n_in, n_out, grp.n_layers, B, T, k_in, k_out, &a);
     const int KT = kt_for(k_in, k_out);
     a.n_layers = grp.n_layers;
-    a.slots = p.slots;
+    int smax = 1;
+    a.slots = plan_shares(a, grp.n_layers, KT, smax);
     // Slots widest first (stable), so that the last items handed out are the
     // narrow ones and the tail after the last claim is short.
-    a.ordered = p.slots <= kMaxSlots;
+    a.ordered = a.slots <= kMaxSlots;
     if (a.ordered) {
         int width[kMaxSlots];
         for (int l = 0; l < grp.n_layers; ++l) {
             const ChunkLayer &L = a.layer[l];
-            for (int c = 0; c < L.c_in + L.c_out; ++c) {
-                const int n = c < L.c_in ? L.n_in : L.n_out;
-                const int col0 = (c < L.c_in ? c : c - L.c_in) * chunk_cols(KT);
+            for (int c = 0; c < L.x_items + L.c_out; ++c) {
+                const int n = c < L.x_items ? L.n_in : L.n_out;
+                const int col0 = (c < L.x_items ? c : c - L.x_items) * chunk_cols(KT);
                 width[L.slot_begin + c] = min(chunk_cols(KT), n - col0);
             }
         }
         int n = 0;
         for (int w = chunk_cols(KT); w > 0; ) {   // descending distinct widths
             int next = 0;
-            for (int sl = 0; sl < p.slots; ++sl) {
+            for (int sl = 0; sl < a.slots; ++sl) {
                 if (width[sl] == w) a.slot_order[n++] = static_cast<uint16_t>(sl);
                 else if (width[sl] < w && width[sl] > next) next = width[sl];
             }
@@ -563,12 +644,12 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     a.tiles = mask ? list : nullptr;
     a.n_tiles = mask ? count : nullptr;
     hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count, a.work);
-    const int max_items = p.slots * B * a.tpe;
+    const int max_items = a.slots * B * a.tpe;
     switch (KT) {
-        case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, s) : launch_chunks<1, float>(a, max_items, s); break;
-        case 2: bf16_in ? launch_chunks<2, bf16_bits>(a, max_items, s) : launch_chunks<2, float>(a, max_items, s); break;
-        case 4: bf16_in ? launch_chunks<4, bf16_bits>(a, max_items, s) : launch_chunks<4, float>(a, max_items, s); break;
-        default: bf16_in ? launch_chunks<8, bf16_bits>(a, max_items, s) : launch_chunks<8, float>(a, max_items, s); break;
+        case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, smax, s) : launch_chunks<1, float>(a, max_items, smax, s); break;
+        case 2: bf16_in ? launch_chunks<2, bf16_bits>(a, max_items, smax, s) : launch_chunks<2, float>(a, max_items, smax, s); break;
+        case 4: bf16_in ? launch_chunks<4, bf16_bits>(a, max_items, smax, s) : launch_chunks<4, float>(a, max_items, smax, s); break;
+        default: bf16_in ? launch_chunks<8, bf16_bits>(a, max_items, smax, s) : launch_chunks<8, float>(a, max_items, smax, s); break;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

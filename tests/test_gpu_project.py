@@ -176,3 +176,70 @@ def test_project_grouped_multichunk_vs_oracle():
         err = np.linalg.norm(g - want) / np.linalg.norm(want)
         say(f"  layer {i} {shapes[i]}: normwise err {err:.2e}")
         assert err <= 1e-3
+
+
+def test_project_shared_inputs_bitwise_equal():
+    """Layers given the same x tensor (q/k/v and gate/up of a transformer
+    block) are projected from one pass over x; every output must equal, bit
+    for bit, the output of the same layers given separate copies of x (each
+    projection sees the same operands in the same order), and the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, normwise, say
+    say("[project] shared inputs: one pass over x for q/k/v and for gate/up")
+    g = W.rng(80)
+    B, T, k = 3, 150, 16
+    shapes = [("q", 512, 512), ("k", 512, 128), ("v", 512, 128), ("o", 512, 512), ("gate", 512, 1024),
+              ("up", 512, 1024), ("down", 1024, 512)]
+    lens = W.lengths(g, B, 1, T)
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = dev(mask_np)
+    x_attn = W.normal(g, (B, T, 512), 1.0, "bf16")
+    x_mlp = W.normal(g, (B, T, 512), 1.0, "bf16")
+    x_o = W.normal(g, (B, T, 512), 1.0, "bf16")
+    x_down = W.normal(g, (B, T, 1024), 1.0, "bf16")
+    xs = [x_attn, x_attn, x_attn, x_o, x_mlp, x_mlp, x_down]
+    dys = [W.normal(g, (B, T, no), 1e-2, "bf16") for _, _, no in shapes]
+    pis = [W.projection(g, k, ni, "bf16") for _, ni, _ in shapes]
+    pos = [W.projection(g, k, no, "bf16") for _, _, no in shapes]
+    xa, xm = dev(x_attn), dev(x_mlp)
+    shared_x = [xa, xa, xa, dev(x_o), xm, xm, dev(x_down)]          # the same tensors: shared
+    copies_x = [dev(x) for x in xs]                                  # separate copies: not shared
+    outs = []
+    for xlist in (shared_x, copies_x):
+        store = torch.full((B, 7 * k * k), np.nan, dtype=torch.float32, device="cuda")
+        layers = [dict(x=xlist[j], dy=dev(dys[j]), p_in=dev(pis[j]), p_out=dev(pos[j]),
+                       g_out=store[:, j * k * k:(j + 1) * k * k]) for j in range(7)]
+        P.logra_project_layers(layers, mask=mask)
+        torch.cuda.synchronize()
+        outs.append(host(store))
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    for j in (0, 2, 5):
+        want = oracle.project_factored(xs[j], dys[j], pis[j], pos[j], mask_np)
+        err = max(normwise(outs[0][b, j * k * k:(j + 1) * k * k], want[b]) for b in range(B))
+        say(f"  {shapes[j][0]}: max normwise err {err:.2e}")
+        assert err <= 1e-3
+
+
+def test_project_rejects_out_of_range_row_stride():
+    """A row stride that puts the last output row beyond device memory is
+    refused on the host (no kernel is launched)."""
+    import ctypes
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import say
+    say("[project] out-of-range g_ld is rejected")
+    B, T, n, k = 2, 64, 64, 4
+    x = torch.zeros((B, T, n), dtype=torch.bfloat16, device="cuda")
+    pi = torch.zeros((k, n), dtype=torch.bfloat16, device="cuda")
+    g = torch.zeros((B, k * k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.logra_project_ws_size(B, T, n, n, k, k), dtype=torch.uint8, device="cuda")
+    L = P.lib()
+
+    def call(g_ld):
+        return L.logra_project_layer(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(x.data_ptr()), P.BF16, B, T, n,
+                                     n, None, ctypes.c_void_p(pi.data_ptr()), ctypes.c_void_p(pi.data_ptr()), k, k,
+                                     ctypes.c_void_p(g.data_ptr()), P.F32, g_ld, ctypes.c_void_p(ws.data_ptr()),
+                                     ws.numel(), None)
+    assert call(1 << 47) == P.ERR_INVALID_ARG and "exceed device memory" in P.logra_last_error()
+    assert call(1 << 40) == P.ERR_INVALID_ARG and "last row of g_out" in P.logra_last_error()
