@@ -59,6 +59,7 @@ TRAFFIC_PATH = os.path.join(ROOT, "profiles", "traffic.json")
 PROJ_SOURCES = ["paper_2405_13954_amd/csrc/project.hip", "paper_2405_13954_amd/csrc/common.h"]
 SCORE_SOURCES = ["paper_2405_13954_amd/csrc/scores.hip", "paper_2405_13954_amd/csrc/common.h"]
 SELF_SOURCES = ["paper_2405_13954_amd/csrc/selfinf.hip", "paper_2405_13954_amd/csrc/common.h"]
+PCA_SOURCES = ["paper_2405_13954_amd/csrc/pca.hip", "paper_2405_13954_amd/csrc/common.h"]
 
 
 def source_sha(sources):
@@ -116,7 +117,7 @@ def write_traffic(fetch_csv, write_csv):
     sc = W.WORKLOADS["llama3_8b_scores"]
     N, Q, D_tot = sc.extra["N_train"], sc.extra["Q"], sc.n_layers * sc.D
     rows = {
-        "projection": ("logra::k_project_chunks<1, unsigned short>", "k_project_chunks<1, bf16>",
+        "projection": ("logra::k_project_chunks<1, 1, unsigned short>", "k_project_chunks<1, 1, bf16>",
                        "7 Llama3-8B layers, B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
                        sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes),
         "scores": ("logra::k_scores_dma", "k_scores_dma", "1,024 x 500,000 x 57,344 bf16", SCORE_SOURCES,
@@ -124,6 +125,11 @@ def write_traffic(fetch_csv, write_csv):
         "self_influence": ("logra::k_self_influence_dma", "k_self_influence_dma",
                            "500,000 x 57,344 bf16, 224 blocks of 256", SELF_SOURCES,
                            N * D_tot * 2 + sc.n_layers * sc.D * 2 * sc.D * 2 + N * 4),
+        # the largest launch of the PCA sub-leg: the gate layer's dy (n = 14,336) over one
+        # batch; algorithmic = the valid tokens' rows read once + C read once and written once
+        "act_cov": ("logra::k_act_cov_dma", "k_act_cov_dma",
+                    "gate dy, n = 14,336, one batch (B=8, lengths of step 0)", PCA_SOURCES,
+                    int(lens[0].sum()) * 14336 * 2 + 2 * 14336 * 14336 * 4),
     }
     out = {"_about": "HBM traffic per launch from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs of "
                      "bench.py (--no-cpu-baseline --steps 3 --warmup 1 --inf-passes 1), written by "
@@ -352,9 +358,11 @@ def pca_sub_leg(args, torch, P, blk, lens, mask, k):
         torch.cuda.synchronize()
         flops = float(tokens) * n * (n + 1)
         tf = flops / (t.mean_ms() * 1e-3) / 1e12
+        traffic, ratio = measured_traffic("act_cov", PCA_SOURCES) if n == 14336 else (None, None)
         out[name] = {"n": n, "syrk_ms": t.mean_ms(), "pca_topk_ms": te.mean_ms(),
                      "roofline": {"bound": "mfma", "achieved": tf, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                  "frac": tf / BF16_PEAK_TFLOPS, "flops_per_launch": flops,
+                                  "frac": tf / BF16_PEAK_TFLOPS, "flops_per_launch": flops, "traffic": traffic,
+                                  "traffic_over_algorithmic": ratio,
                                   "kernel": "k_act_cov_dma (masked bf16 SYRK)"}}
         del C, ws, Pk, pws
     return out
