@@ -152,7 +152,10 @@ def write_traffic(fetch_csv, write_csv):
 
 
 class EventTimer:
-    """Pairs of HIP events on the launch stream; mean duration per launch in ms."""
+    """Pairs of HIP events on the launch stream; mean duration per launch in ms.
+    A pair may bracket n back-to-back launches (stop(s, n)): each event record
+    puts a marker in the queue that holds the next launch for about 10 us, so
+    bracketing every launch would add that gap to the work being timed."""
 
     def __init__(self, torch):
         self.torch = torch
@@ -163,13 +166,13 @@ class EventTimer:
         e.record()
         return e
 
-    def stop(self, s):
+    def stop(self, s, n=1):
         e = self.torch.cuda.Event(enable_timing=True)
         e.record()
-        self.pairs.append((s, e))
+        self.pairs.append((s, e, n))
 
     def mean_ms(self):
-        return float(np.mean([a.elapsed_time(b) for a, b in self.pairs])) if self.pairs else float("nan")
+        return float(np.mean([a.elapsed_time(b) / n for a, b, n in self.pairs])) if self.pairs else float("nan")
 
 
 # ------------------------------------------------------------------ logging --
@@ -235,14 +238,14 @@ def logging_leg(args, torch, P):
 
     def step(s, timed, descs_of=all_descs, ptimer=proj_timer):
         m = masks[s]
+        e0 = ptimer.start() if timed else None   # one pair over the step's back-to-back launches
         for b in range(w.blocks):
-            e0 = ptimer.start() if timed else None
             rc = L.logra_project_layers(descs_of[s][b], nl_block, P.BF16, B, T, ctypes.c_void_p(m.data_ptr()),
                                         k, k, P.BF16, g_ld, ctypes.c_void_p(ws.data_ptr()), ws_bytes, stream)
             if rc != 0:
                 raise P.LograError(rc, P.logra_last_error())
-            if timed:
-                ptimer.stop(e0)
+        if timed:
+            ptimer.stop(e0, w.blocks)
         rows = store[s * B:(s + 1) * B]
         e0 = cov_timer.start() if timed else None
         rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(rows.data_ptr()), P.BF16, g_ld, B, D, n_layers,
@@ -330,8 +333,8 @@ def logging_leg(args, torch, P):
 def pca_sub_leg(args, torch, P, blk, lens, mask, k):
     """PCA initialisation on the logging workload (Sec. 3.2): the KFAC factor
     SYRK over one batch of B=8 ragged sequences for the gate layer's input x
-    (n = 4096) and output gradient dy (n = 14,336), each timed per call with
-    HIP events; then the top-k eigenvectors of each factor (30 subspace
+    (n = 4096) and output gradient dy (n = 14,336), timed over back-to-back
+    calls with HIP events; then the top-k eigenvectors of each factor (30 subspace
     iterations).  Algorithmic flops of a SYRK call: valid tokens x n (n + 1)
     (the upper triangle of the symmetric product)."""
     x, dy = blk[4]                      # gate: 4096 -> 14336
@@ -342,11 +345,11 @@ def pca_sub_leg(args, torch, P, blk, lens, mask, k):
         C = torch.zeros((n, n), dtype=torch.float32, device="cuda")
         ws = torch.empty(P.logra_act_cov_ws_size(a.shape[0], a.shape[1]), dtype=torch.uint8, device="cuda")
         t = EventTimer(torch)
-        for timed in [False] + [True] * args.pca_reps:
-            e0 = t.start() if timed else None
+        P.logra_act_cov_accumulate(a, C, mask=mask, ws=ws)
+        e0 = t.start()                  # one pair over back-to-back calls
+        for _ in range(args.pca_reps):
             P.logra_act_cov_accumulate(a, C, mask=mask, ws=ws)
-            if timed:
-                t.stop(e0)
+        t.stop(e0, args.pca_reps)
         Pk = torch.empty((k, n), dtype=torch.bfloat16, device="cuda")
         pws = torch.empty(P.logra_pca_ws_size(n, k), dtype=torch.uint8, device="cuda")
         te = EventTimer(torch)

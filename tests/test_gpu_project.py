@@ -221,6 +221,78 @@ def test_project_shared_inputs_bitwise_equal():
         assert err <= 1e-3
 
 
+def test_project_all_masked_batch_writes_zeros():
+    """No valid token anywhere: no tile is listed and no chunk item runs; every
+    output row (pre-filled with 7.0) must still be written as zeros."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[project] fully masked batch")
+    B, T, k = 3, 130, 16
+    d = W.layer_inputs(12, 0, B, T, 256, 320, k, k, 1.0, 1.0, "bf16", np.zeros(B, dtype=np.int64))
+    for out in (torch.float32, torch.bfloat16):
+        store = torch.full((B, k * k + 5), 7.0, dtype=out, device="cuda")
+        P.logra_project_layer(dev(d["x"]), dev(d["dy"]), dev(d["p_in"]), dev(d["p_out"]), store[:, :k * k],
+                              mask=dev(d["mask"]))
+        torch.cuda.synchronize()
+        got = host(store).astype(np.float64) if out == torch.float32 else W.bf16_bits_to_f32(host(store))
+        assert np.all(got[:, :k * k] == 0.0) and np.all(got[:, k * k:] == 7.0)
+
+
+def test_project_many_examples_vs_oracle():
+    """B = 1100 short examples (1100 tiles: the tile listing and the per-example
+    bookkeeping take more than one pass of the 1024-thread prep workgroup),
+    a fifth of them fully masked, k = 24 (two 16-wide projection blocks)."""
+    from gpu_util import rowwise_normwise, say
+    say("[project] B = 1100 examples, ragged, some fully masked")
+    B, T = 1100, 40
+    g = W.rng(13)
+    lens = W.lengths(g, B, 0, T)
+    lens[g.random(B) < 0.2] = 0
+    d = W.layer_inputs(13, 1, B, T, 96, 160, 24, 20, 1.0, 1.0, "bf16", lens)
+    got = _run(d, "f32")
+    want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], d["mask"])
+    err = rowwise_normwise(got, want)
+    say(f"  normwise err {err:.2e}")
+    assert err <= 1e-3
+    assert np.all(got[lens == 0] == 0.0)
+
+
+def test_project_reused_workspace_across_masks():
+    """One workspace, filled with garbage first, serves consecutive grouped
+    launches with different masks: the launch clears its own counters, and
+    each result equals the oracle's and a fresh-workspace launch bit for bit."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[project] workspace reused across launches with different masks")
+    B, T, k = 4, 200, 16
+    shapes = [(512, 256), (256, 4608)]
+    g = W.rng(14)
+    data = [W.layer_inputs(14, i, B, T, ni, no, k, k, 1.0, 1e-2, "bf16") for i, (ni, no) in enumerate(shapes)]
+    tens = [{key: dev(d[key]) for key in ("x", "dy", "p_in", "p_out")} for d in data]
+    D = k * k
+    descs = (P.LayerDesc * 2)(*[P.LayerDesc(0, 0, 0, 0, 0, ni, no) for ni, no in shapes])
+    ws = torch.full((P.logra_project_layers_ws_size(descs, 2, B, T, k, k),), 0x7F, dtype=torch.uint8, device="cuda")
+    for trial in range(3):
+        lens = W.lengths(g, B, 0, T)
+        lens[trial % B] = 0
+        mask_np = W.mask_from_lengths(lens, T)
+        outs = []
+        for w in (ws, None):
+            store = torch.full((B, 2 * D), np.nan, dtype=torch.float32, device="cuda")
+            layers = [dict(t, g_out=store[:, i * D:(i + 1) * D]) for i, t in enumerate(tens)]
+            P.logra_project_layers(layers, mask=dev(mask_np), ws=w)
+            torch.cuda.synchronize()
+            outs.append(host(store))
+        assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32)), trial
+        for i, d in enumerate(data):
+            want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], mask_np)
+            gi = outs[0][:, i * D:(i + 1) * D].astype(np.float64)
+            assert np.linalg.norm(gi - want) <= 1e-3 * np.linalg.norm(want), (trial, i)
+            assert np.all(gi[lens == 0] == 0.0)
+
+
 def test_project_rejects_out_of_range_row_stride():
     """A row stride that puts the last output row beyond device memory is
     refused on the host (no kernel is launched)."""
