@@ -34,12 +34,17 @@
 //   v_e = Q w_e of the k largest theta, each signed so that its entry of
 //   largest magnitude (lowest index among equal magnitudes) is positive.
 //
-//  2. k_cq: Z = C Q; a wave owns 16 rows of C and streams them (128-bit
-//     loads) into 16x16x4 fp32 MFMAs against Q (read through L2).
+//  Q and Z are kept in row quads (four rows of a column adjacent).
+//  2. k_cq_part (+ k_cq_sum): Z = C Q; a workgroup owns 64 rows of C (32
+//     for p > 64) and a range of its columns, its waves splitting the range;
+//     128-bit loads of C and Q feed 16x16x4 fp32 MFMAs.  Column ranges
+//     (splits) give about 2048 workgroups; their partials are summed in
+//     split order.
 //  3. k_gram_part: fp64 partial sums of X^T Y over 256-row chunks (X^T X for
-//     the orthonormalisation, Q^T Z for Rayleigh-Ritz), fixed order.
-//  4. k_chol_inv (one workgroup): the chunk sums, a shifted Cholesky
-//     Z^T Z + eps tr/p I = R^T R and R^{-1}, in fp64 in LDS.
+//     the orthonormalisation, Z^T Q for Rayleigh-Ritz), fixed order.
+//  4. k_chol_inv_reg / k_chol_inv (one workgroup): the chunk sums, a
+//     shifted Cholesky Z^T Z + eps tr/p I = R^T R and R^{-1} in fp64 (p <= 64:
+//     one wave, a column per lane in registers; wider: LDS).
 //  5. k_apply_rinv: Q = Z R^{-1} (fp64 arithmetic, fp32 result).
 //  6. k_jacobi (one workgroup): T in LDS, round-robin parallel cyclic Jacobi
 //     (p/2 disjoint rotations per round), eigenvectors accumulated in W^T.
@@ -389,8 +394,21 @@ __global__ __launch_bounds__(256) void k_act_cov_f32(const float *__restrict__ a
 
 // ------------------------------------------------------------------------
 // Subspace iteration for the top-k eigenvectors.
+//
+// Q and Z (n x pp fp32; pp = p rounded up to 16) are stored in row quads:
+// element (i, j) at ((i / 4) pp + j) 4 + i % 4, with the rows padded to
+// n4 = n rounded up to 4 and every element past n or p zero.  Four
+// consecutive rows of one column (the B operand of a 16x16x4 MFMA) are then
+// one 128-bit load, and a run of rows is one contiguous range.
 constexpr int kGramRows = 256;   // rows per partial sum of a Gram matrix
+constexpr int kGramChunk = 64;   // rows staged in LDS at a time
 constexpr int kMaxP = 128;       // subspace width (at most 2 k for k <= 64)
+constexpr int kCqStages = 3;     // register pipeline depth of k_cq_part
+
+__host__ __device__ constexpr int round4(int n) { return (n + 3) & ~3; }
+__device__ __forceinline__ size_t qidx(int i, int j, int pp) {
+    return ((static_cast<size_t>(i >> 2) * pp + j) << 2) + (i & 3);
+}
 
 __device__ __forceinline__ float hash_uniform(uint32_t i, uint32_t j) {
     // integer hash of (i, j) (a multiply-xorshift mixer) -> uniform in [-1, 1)
@@ -403,88 +421,193 @@ __device__ __forceinline__ float hash_uniform(uint32_t i, uint32_t j) {
     return static_cast<float>(h >> 8) * (2.0f / 16777216.0f) - 1.0f;
 }
 
-// Q_0: pseudo-random columns j < p, zero padding columns up to pp.
+// Q_0: pseudo-random columns j < p, zeros elsewhere (row quads, n4 rows).
 __global__ __launch_bounds__(256) void k_pca_init(float *Q, int n, int p, int pp) {
     const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (e >= static_cast<int64_t>(n) * pp) return;
-    const int i = static_cast<int>(e / pp), j = static_cast<int>(e - static_cast<int64_t>(i) * pp);
-    Q[e] = j < p ? hash_uniform(static_cast<uint32_t>(i), static_cast<uint32_t>(j)) : 0.f;
+    if (e >= static_cast<int64_t>(round4(n)) * pp) return;
+    const int64_t qj = e >> 2;
+    const int i = static_cast<int>(qj / pp) * 4 + static_cast<int>(e & 3);
+    const int j = static_cast<int>(qj % pp);
+    Q[e] = i < n && j < p ? hash_uniform(static_cast<uint32_t>(i), static_cast<uint32_t>(j)) : 0.f;
 }
 
-// Z = C Q for Z, Q [n][pp] (pp a multiple of 16, at most 128).  A wave owns
-// 16 rows: lane l streams row (l % 16) of C, four columns k + 4 (l / 16) + e
-// (e < 4) per 128-bit load, and feeds MFMA e with column k + 4 (l / 16) + e of
-// its row and the matching row of Q.  Rows and columns past n read zeros.
-template <int NB>
-__global__ __launch_bounds__(256) void k_cq(const float *__restrict__ C, int n, const float *__restrict__ Q,
-                                            float *__restrict__ Z) {
+// Z_s = C[:, K_s] Q[K_s, :] over the column range K_s = [s kr, (s + 1) kr) of
+// split s = blockIdx.y (kr a multiple of 64).  A workgroup owns 16 MR rows
+// of C; its four waves take the range's 16-column steps round-robin.  Lane
+// (row, q) of a wave streams columns k + 4q .. k + 4q + 3 of its row in each
+// row block (one 128-bit load per block) and rows k + 4q .. k + 4q + 3 of
+// one column of each 16-column block of Q (one 128-bit load), and feeds
+// them to 16x16x4 fp32 MFMAs, element e of both to MFMA e.  A register
+// pipeline keeps kCqStages - 1 steps in flight; every load is unconditional
+// (out-of-range offsets read zeros).  The waves' sums are folded in a fixed
+// order through LDS and written, in row quads, to Z (one split) or to the
+// split's partial.  Rows past n read zeros; columns past n meet the zero
+// rows of Q past n (a load straddling the end of a row reads the next row's
+// first columns, or zeros past the end of C, against those zeros).
+template <int NB, int MR>
+__global__ __launch_bounds__(256) void k_cq_part(const float *__restrict__ C, int n, const float *__restrict__ Q,
+                                                 int kr, float *__restrict__ Zs) {
     constexpr int pp = 16 * NB;
+    constexpr int ST = kCqStages;
+    __shared__ f32x4 fold[MR * NB * kWave];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int m0 = (blockIdx.x * 4 + wave) * 16;
-    if (m0 >= n) return;
-    const int row = lane & 15, kq = lane >> 4;
-    const int rows = min(16, n - m0);
-    const auto rc = buf_rsrc_uniform(C + static_cast<size_t>(m0) * n, static_cast<uint32_t>(rows * n * 4));
-    const auto rq = buf_rsrc_uniform(Q, static_cast<uint32_t>(n * pp * 4));
-    f32x4 acc[NB];
+    const int row = lane & 15, q = lane >> 4;
+    const int m0 = blockIdx.x * 16 * MR;
+    const int k0 = blockIdx.y * kr;
+    const int k1 = min(n, k0 + kr);
+    const int n4 = round4(n);
+    const int rows = min(16 * MR, n - m0);
+    const auto rc = buf_rsrc_uniform(C + static_cast<size_t>(m0) * n, static_cast<uint32_t>(rows) * n * 4u);
+    const auto rq = buf_rsrc_uniform(Q, static_cast<uint32_t>(n4) * pp * 4u);
+    uint32_t coff[MR];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint32_t crow = static_cast<uint32_t>(row) * static_cast<uint32_t>(n) * 4u;
-    for (int k = 0; k < n; k += 16) {
-        const int kk = k + 4 * kq;
-        // C[row][kk .. kk+3]: past the row's end only at the last row block
-        // of the matrix, where the range check returns zeros; columns past n
-        // meet rows of Q past n, which read zeros too
-        const u32x4 cv = buf_ld128(rc, kk < n ? crow + static_cast<uint32_t>(kk) * 4u : kBufOOB);
+    for (int m = 0; m < MR; ++m)
+        coff[m] = 16 * m + row < rows ? (static_cast<uint32_t>(16 * m + row) * n + 4 * q) * 4u : kBufOOB;
+    const uint32_t qoff = static_cast<uint32_t>(q * pp + row) * 16u;   // bytes of Q's element (4 q, row)
+
+    f32x4 acc[MR][NB];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t qoff = static_cast<uint32_t>((kk + e) * pp + row) * 4u;
-            const float a = __uint_as_float(cv[e]);
+    for (int m = 0; m < MR; ++m)
 #pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const float q = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                    rq, kk + e < n ? static_cast<int>(qoff + 64u * b) : static_cast<int>(kBufOOB), 0, 0));
-                acc[b] = mfma16_f32(a, q, acc[b]);
+        for (int b = 0; b < NB; ++b) acc[m][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nsteps = (k1 - k0 + 15) / 16;
+    if (wave < nsteps) {
+        auto load = [&](int st, u32x4(&cv)[MR], u32x4(&qv)[NB]) {
+            const int k = k0 + 16 * st;
+            const bool in = k + 4 * q < k1;   // false past the split's end: zeros on both sides
+#pragma unroll
+            for (int m = 0; m < MR; ++m) cv[m] = buf_ld128(rc, in ? coff[m] + static_cast<uint32_t>(k) * 4u : kBufOOB);
+            const uint32_t kq = static_cast<uint32_t>(k) * pp * 4u;   // bytes of row quad k / 4
+#pragma unroll
+            for (int b = 0; b < NB; ++b) qv[b] = buf_ld128(rq, in ? kq + qoff + 256u * b : kBufOOB);
+        };
+        const int iters = ((nsteps - wave + 3) / 4 + ST - 1) / ST;
+        u32x4 cv[ST][MR], qv[ST][NB];
+        int s = wave;
+#pragma unroll
+        for (int i = 0; i < ST - 1; ++i) load(s + 4 * i, cv[i], qv[i]);
+        for (int it = 0; it < iters; ++it) {
+#pragma unroll
+            for (int i = 0; i < ST; ++i) {
+                load(s + 4 * (i + ST - 1), cv[(i + ST - 1) % ST], qv[(i + ST - 1) % ST]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int m = 0; m < MR; ++m)
+#pragma unroll
+                        for (int b = 0; b < NB; ++b)
+                            acc[m][b] = mfma16_f32(__uint_as_float(cv[i][m][e]), __uint_as_float(qv[i][b][e]),
+                                                   acc[m][b]);
             }
+            s += 4 * ST;
         }
     }
-    // result register r of lane l: row 4 (l / 16) + r, column l % 16 of block b
+    // fold ((w3 + w2) + w1) + w0; result register r of lane (row, q) is row
+    // 4 q + r, column row of its 16 x 16 block: four consecutive rows of one
+    // column, one 128-bit store in row quads
+    f32x4 *my = fold + lane;
+    if (wave == 3) {
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+        for (int m = 0; m < MR; ++m)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int i = m0 + 4 * kq + r;
-            if (i < n) Z[static_cast<size_t>(i) * pp + 16 * b + row] = acc[b][r];
+            for (int b = 0; b < NB; ++b) my[(m * NB + b) * kWave] = acc[m][b];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 2; w >= 1; --w) {
+        if (wave == w) {
+#pragma unroll
+            for (int m = 0; m < MR; ++m)
+#pragma unroll
+                for (int b = 0; b < NB; ++b) my[(m * NB + b) * kWave] = my[(m * NB + b) * kWave] + acc[m][b];
         }
+        __syncthreads();
+    }
+    if (wave == 0) {
+        float *dst = Zs + static_cast<size_t>(blockIdx.y) * n4 * pp;
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+            const int i0 = m0 + 16 * m + 4 * q;
+            if (i0 >= n4) continue;
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                *reinterpret_cast<f32x4 *>(dst + qidx(i0, 16 * b + row, pp)) =
+                    my[(m * NB + b) * kWave] + acc[m][b];
+        }
+    }
+}
+
+// Z = sum of the splits' partials, in split order (128-bit elements).
+__global__ __launch_bounds__(256) void k_cq_sum(const f32x4 *__restrict__ Zs, int64_t n_vec, int splits,
+                                                f32x4 *__restrict__ Z) {
+    const int64_t v = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (v >= n_vec) return;
+    f32x4 s = Zs[v];
+    for (int t = 1; t < splits; ++t) s += Zs[static_cast<size_t>(t) * n_vec + v];
+    Z[v] = s;
 }
 
 // Partial Gram sums G_c[a][b] = sum over rows r of chunk c of X[r][a] Y[r][b]
-// (fp64), a, b < p, for X, Y [n][pp] fp32; rows staged through LDS.
+// (fp64), a, b < p, for X, Y in row quads (n4 rows, zero past n).  Rows are
+// staged through LDS 64 at a time, the next 64 loaded into registers while
+// the current ones are summed; an LDS read of 128 bits gives one column's
+// values in four consecutive rows.  PMAX (32, 64 or 128) bounds p; a
+// workgroup forms at most 4096 of the p x p sums (16 per thread), the
+// blockIdx.y-th group of them.
+template <int PMAX>
 __global__ __launch_bounds__(256) void k_gram_part(const float *__restrict__ X, const float *__restrict__ Y, int n,
                                                    int p, int pp, double *__restrict__ part) {
-    __shared__ float xs[64][129], ys[64][129];
+    constexpr int kV = PMAX / 16;               // 128-bit loads per thread and operand, at most
+    constexpr int kU = PMAX * PMAX / 256 < 16 ? PMAX * PMAX / 256 : 16;   // outputs per thread, at most
+    __shared__ f32x4 xs[kGramChunk / 4 * PMAX], ys[kGramChunk / 4 * PMAX];
     const int tid = threadIdx.x;
+    const int n4 = round4(n);
     const int r0 = blockIdx.x * kGramRows;
-    const int rend = min(n, r0 + kGramRows);
+    const int rend = min(n4, r0 + kGramRows);
     const int np = p * p;
-    double acc[64];
+    const int nv = pp / 16;                     // 128-bit loads per thread of a full chunk
+    const f32x4 *X4 = reinterpret_cast<const f32x4 *>(X);
+    const f32x4 *Y4 = reinterpret_cast<const f32x4 *>(Y);
+    f32x4 xr[kV], yr[kV];
+    auto fetch = [&](int c0) {
+        const int lim = (min(kGramChunk, rend - c0) / 4) * pp;   // 128-bit elements of this chunk
+        const size_t base = static_cast<size_t>(c0 / 4) * pp;
 #pragma unroll
-    for (int u = 0; u < 64; ++u) acc[u] = 0.0;
-    for (int c0 = r0; c0 < rend; c0 += 64) {
-        const int nr = min(64, rend - c0);
-        for (int e = tid; e < 64 * pp; e += 256) {
-            const int r = e / pp, j = e - r * pp;
-            xs[r][j] = r < nr ? X[static_cast<size_t>(c0 + r) * pp + j] : 0.f;
-            ys[r][j] = r < nr ? Y[static_cast<size_t>(c0 + r) * pp + j] : 0.f;
+        for (int v = 0; v < kV; ++v) {
+            const int f = tid + 256 * v;
+            const bool ok = v < nv && f < lim;
+            xr[v] = ok ? X4[base + f] : f32x4{0.f, 0.f, 0.f, 0.f};
+            yr[v] = ok ? Y4[base + f] : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    double acc[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) acc[u] = 0.0;
+    const int e0 = blockIdx.y * 256 * kU;       // first output of this workgroup
+    if (r0 < rend) fetch(r0);
+    for (int c0 = r0; c0 < rend; c0 += kGramChunk) {
+        const int nq = min(kGramChunk, rend - c0) / 4;
+#pragma unroll
+        for (int v = 0; v < kV; ++v) {
+            const int f = tid + 256 * v;
+            if (v < nv && f < nq * pp) {
+                xs[f] = xr[v];
+                ys[f] = yr[v];
+            }
         }
         __syncthreads();
+        if (c0 + kGramChunk < rend) fetch(c0 + kGramChunk);
 #pragma unroll
-        for (int u = 0; u < 64; ++u) {
-            const int e = tid + 256 * u;
+        for (int u = 0; u < kU; ++u) {
+            const int e = e0 + tid + 256 * u;
             if (e < np) {
                 const int a = e / p, b = e - (e / p) * p;
                 double s = acc[u];
-                for (int r = 0; r < nr; ++r) s = fma(static_cast<double>(xs[r][a]), static_cast<double>(ys[r][b]), s);
+                for (int qq = 0; qq < nq; ++qq) {
+                    const f32x4 xv = xs[qq * pp + a], yv = ys[qq * pp + b];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) s = fma(static_cast<double>(xv[r]), static_cast<double>(yv[r]), s);
+                }
                 acc[u] = s;
             }
         }
@@ -492,25 +615,115 @@ __global__ __launch_bounds__(256) void k_gram_part(const float *__restrict__ X, 
     }
     double *dst = part + static_cast<size_t>(blockIdx.x) * np;
 #pragma unroll
-    for (int u = 0; u < 64; ++u) {
-        const int e = tid + 256 * u;
+    for (int u = 0; u < kU; ++u) {
+        const int e = e0 + tid + 256 * u;
         if (e < np) dst[e] = acc[u];
     }
 }
 
-// One workgroup: G = sum of the chunk partials (in chunk order), then the
-// shifted Cholesky G + eps (tr G / p) I = R^T R (R upper) and R^{-1}, all in
-// fp64.  Writes R^{-1} [p][p] (zero below the diagonal).
-__global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ part, int chunks, int p,
-                                                  double *__restrict__ Rinv) {
-    __shared__ double A[kMaxP * kMaxP];   // G, then R in its upper triangle
-    __shared__ double red[256];
-    const int tid = threadIdx.x, np = p * p;
+void launch_gram(const float *X, const float *Y, int n, int p, int pp, double *part, hipStream_t s) {
+    const dim3 grid(static_cast<unsigned>((round4(n) + kGramRows - 1) / kGramRows),
+                    static_cast<unsigned>((p * p + 4095) / 4096));
+    if (pp <= 32) hipLaunchKernelGGL(k_gram_part<32>, grid, dim3(256), 0, s, X, Y, n, p, pp, part);
+    else if (pp <= 64) hipLaunchKernelGGL(k_gram_part<64>, grid, dim3(256), 0, s, X, Y, n, p, pp, part);
+    else hipLaunchKernelGGL(k_gram_part<128>, grid, dim3(256), 0, s, X, Y, n, p, pp, part);
+}
+
+// G = sum of the chunk partials, in chunk order, into A (all threads; eight
+// loads in flight).
+__device__ __forceinline__ void sum_partials(const double *__restrict__ part, int chunks, int np, double *A,
+                                             int tid) {
     for (int e = tid; e < np; e += 256) {
         double s = 0.0;
-        for (int c = 0; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
+        int c = 0;
+        for (; c + 8 <= chunks; c += 8) {
+            double v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = part[static_cast<size_t>(c + u) * np + e];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
         A[e] = s;
     }
+}
+
+// A double from lane `src` (a compile-time lane), as two 32-bit readlanes.
+__device__ __forceinline__ double readlane_d(double v, int src) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), src));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u >> 32), src));
+    return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// p <= PM (32 or 64).  One workgroup sums the partials into G; wave 0 then,
+// in registers, forms the shifted Cholesky G + eps (tr G / p) I = R^T R
+// (R upper) and R^{-1}, lane r holding row r of the matrix padded to PM
+// with the identity (whose factor and inverse are the identity).  Step j of
+// the right-looking factorisation takes row j from lane j (readlanes) and,
+// the trailing matrix being kept whole and symmetric, each lane's own entry
+// of column j from its own row.  Then lane r solves x R = e_r for row r of
+// X = R^{-1} column by column, x_c = (delta_rc - sum over m < c of
+// x_m R_mc) / R_cc, with column c of R read from lanes m <= c; x_c replaces
+// the row's entry c, whose last reader was that column.  All in fp64.
+// Writes R^{-1} [p][p] (zero below the diagonal).
+template <int PM>
+__global__ __launch_bounds__(256) void k_chol_inv_reg(const double *__restrict__ part, int chunks, int p,
+                                                      double *__restrict__ Rinv) {
+    __shared__ double A[PM * PM];
+    const int tid = threadIdx.x, np = p * p;
+    sum_partials(part, chunks, np, A, tid);
+    __syncthreads();
+    if (tid >= kWave) return;
+    const int r = tid;                // the lane's row (lanes >= PM carry an unused identity row)
+    double a[PM];
+#pragma unroll
+    for (int c = 0; c < PM; ++c) a[c] = r < p && c < p ? A[r * p + c] : r == c ? 1.0 : 0.0;
+    double tr = r < p ? A[r * p + r] : 0.0;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) tr += __shfl_xor(tr, o, kWave);   // the same butterfly in every lane
+    const double shift = 1e-12 * (tr > 0.0 ? tr / p : 1.0);
+#pragma unroll
+    for (int c = 0; c < PM; ++c)
+        if (c == r && r < p) a[c] += shift;
+#pragma unroll
+    for (int j = 0; j < PM; ++j) {
+        const double d = readlane_d(a[j], j);
+        const double rjj = d > 0.0 ? sqrt(d) : 1.0;   // a non-positive pivot (cannot follow the shift) keeps R invertible
+        const double inv = 1.0 / rjj;
+        const double rjr = a[j] * inv;                // R_jr (lanes r > j)
+#pragma unroll
+        for (int c = j + 1; c < PM; ++c) {
+            const double rjc = readlane_d(a[c], j) * inv;   // R_jc
+            if (r > j) a[c] = fma(-rjr, rjc, a[c]);
+            else if (r == j) a[c] = rjc;
+        }
+        if (r == j) a[j] = rjj;
+    }
+#pragma unroll
+    for (int c = 0; c < PM; ++c) {
+        double s = c == r ? 1.0 : 0.0;
+#pragma unroll
+        for (int m = 0; m < c; ++m) s = fma(-a[m], readlane_d(a[c], m), s);
+        a[c] = s / readlane_d(a[c], c);
+    }
+    if (r < p) {
+#pragma unroll
+        for (int c = 0; c < PM; ++c)
+            if (c < p) Rinv[r * p + c] = a[c];
+    }
+}
+
+// p > 64: one workgroup, G = sum of the chunk partials, then the shifted
+// Cholesky (right-looking, a barrier per phase of each step) and R^{-1}
+// (thread c solves R x = e_c upwards, x kept below the diagonal), in fp64 in
+// LDS.  Writes R^{-1} [p][p] (zero below the diagonal).
+__global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ part, int chunks, int p,
+                                                  double *__restrict__ Rinv) {
+    __shared__ double A[kMaxP * kMaxP];   // G; then R on and above the diagonal, R^{-1} (transposed) below it
+    __shared__ double red[256];
+    const int tid = threadIdx.x, np = p * p;
+    sum_partials(part, chunks, np, A, tid);
     __syncthreads();
     double tr = 0.0;
     for (int a = tid; a < p; a += 256) tr += A[a * p + a];
@@ -523,11 +736,10 @@ __global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ par
     const double shift = 1e-12 * (red[0] > 0.0 ? red[0] / p : 1.0);
     for (int a = tid; a < p; a += 256) A[a * p + a] += shift;
     __syncthreads();
-    // right-looking Cholesky on the upper triangle: row j of R
     for (int j = 0; j < p; ++j) {
         if (tid == 0) {
             const double d = A[j * p + j];
-            A[j * p + j] = d > 0.0 ? sqrt(d) : 1.0;   // a non-positive pivot (cannot follow the shift) keeps R invertible
+            A[j * p + j] = d > 0.0 ? sqrt(d) : 1.0;
         }
         __syncthreads();
         const double rjj = A[j * p + j];
@@ -539,27 +751,49 @@ __global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ par
         }
         __syncthreads();
     }
-    // R^{-1}: column c solves R x = e_c (back substitution), one thread per column
     for (int c = tid; c < p; c += 256) {
-        for (int r = p - 1; r >= 0; --r) {
-            double s = r == c ? 1.0 : 0.0;
-            for (int m = r + 1; m <= c; ++m) s -= A[r * p + m] * Rinv[static_cast<size_t>(m) * p + c];
-            Rinv[static_cast<size_t>(r) * p + c] = r <= c ? s / A[r * p + r] : 0.0;
+        const double xc = 1.0 / A[c * p + c];
+        for (int r = c - 1; r >= 0; --r) {
+            double s = A[r * p + c] * xc;
+            for (int m = r + 1; m < c; ++m) s = fma(A[r * p + m], A[c * p + m], s);
+            A[c * p + r] = -s / A[r * p + r];
         }
+    }
+    __syncthreads();
+    for (int e = tid; e < np; e += 256) {
+        const int r = e / p, c = e - (e / p) * p;
+        Rinv[e] = r < c ? A[c * p + r] : r == c ? 1.0 / A[r * p + r] : 0.0;
     }
 }
 
-// Q = Z R^{-1}: row i of Q is row i of Z times the upper-triangular R^{-1};
-// fp64 sums, fp32 result, padding columns zero.
+void launch_chol_inv(const double *part, int chunks, int p, double *Rinv, hipStream_t s) {
+    if (p <= 32) hipLaunchKernelGGL(k_chol_inv_reg<32>, dim3(1), dim3(256), 0, s, part, chunks, p, Rinv);
+    else if (p <= 64) hipLaunchKernelGGL(k_chol_inv_reg<64>, dim3(1), dim3(256), 0, s, part, chunks, p, Rinv);
+    else hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, part, chunks, p, Rinv);
+}
+
+// Q = Z R^{-1} in row quads: a thread forms one column j of four rows, each
+// entry sum over m <= j of Z[i][m] R^{-1}[m][j] in fp64 (fp32 result); the
+// padding columns j >= p are zero.
 __global__ __launch_bounds__(256) void k_apply_rinv(const float *__restrict__ Z, int n, int p, int pp,
                                                     const double *__restrict__ Rinv, float *__restrict__ Q) {
-    const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (e >= static_cast<int64_t>(n) * pp) return;
-    const int i = static_cast<int>(e / pp), j = static_cast<int>(e - static_cast<int64_t>(i) * pp);
-    double s = 0.0;
+    const int64_t v = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;   // 128-bit element of Q
+    if (v >= static_cast<int64_t>(round4(n) / 4) * pp) return;
+    const int64_t quad = v / pp;
+    const int j = static_cast<int>(v - quad * pp);
+    const f32x4 *Z4 = reinterpret_cast<const f32x4 *>(Z) + quad * pp;
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
     if (j < p)
-        for (int m = 0; m <= j; ++m) s = fma(static_cast<double>(Z[static_cast<size_t>(i) * pp + m]), Rinv[static_cast<size_t>(m) * p + j], s);
-    Q[e] = static_cast<float>(s);
+        for (int m = 0; m <= j; ++m) {
+            const f32x4 z = Z4[m];
+            const double r = Rinv[static_cast<size_t>(m) * p + j];
+            s0 = fma(static_cast<double>(z[0]), r, s0);
+            s1 = fma(static_cast<double>(z[1]), r, s1);
+            s2 = fma(static_cast<double>(z[2]), r, s2);
+            s3 = fma(static_cast<double>(z[3]), r, s3);
+        }
+    reinterpret_cast<f32x4 *>(Q)[v] =
+        f32x4{static_cast<float>(s0), static_cast<float>(s1), static_cast<float>(s2), static_cast<float>(s3)};
 }
 
 // One workgroup: T = (sum of the chunk partials of Q^T Z), symmetrised, is
@@ -677,7 +911,8 @@ __global__ __launch_bounds__(256) void k_jacobi(const double *__restrict__ part,
 }
 
 // Ritz vectors of the k largest theta (decreasing; equal values in index
-// order): V[e][i] = sum_j Q[i][j] Wt[order_e][j] (fp64 sums), eigvals[e].
+// order): V[e][i] = sum_j Q[i][j] Wt[order_e][j] (fp64 sums; Q in row
+// quads), eigvals[e].
 // The order is found by every thread from theta (p <= 128).
 __global__ __launch_bounds__(256) void k_ritz(const float *__restrict__ Q, int n, int p, int pp, int k,
                                               const double *__restrict__ Wt, const double *__restrict__ theta,
@@ -701,7 +936,7 @@ __global__ __launch_bounds__(256) void k_ritz(const float *__restrict__ Q, int n
     const int i = blockIdx.x * 256 + threadIdx.x;
     if (i >= n) return;
     double s = 0.0;
-    for (int j = 0; j < p; ++j) s = fma(static_cast<double>(Q[static_cast<size_t>(i) * pp + j]), w[j], s);
+    for (int j = 0; j < p; ++j) s = fma(static_cast<double>(Q[qidx(i, j, pp)]), w[j], s);
     V[static_cast<size_t>(e) * n + i] = static_cast<float>(s);
 }
 
@@ -777,7 +1012,7 @@ namespace logra {
 namespace {
 
 struct PcaLayout {
-    float *Q, *Z;
+    float *Q, *Z, *Zs;
     double *part, *Rinv, *Wt, *theta;
 };
 
@@ -786,16 +1021,33 @@ inline int pca_p(int n, int k) {
     return w < n ? w : n;
 }
 inline int pca_pp(int n, int k) { return (pca_p(n, k) + 15) / 16 * 16; }
-inline int gram_chunks(int n) { return (n + kGramRows - 1) / kGramRows; }
+inline int gram_chunks(int n) { return (round4(n) + kGramRows - 1) / kGramRows; }
+inline size_t block_floats(int n, int pp) { return static_cast<size_t>(round4(n)) * pp; }
+
+// Z = C Q: row blocks of 16 MR rows per workgroup, and the columns of C cut
+// into splits of kr (a multiple of 64, at least 512 unless n is smaller) so
+// that the grid has about 2048 workgroups.
+inline int cq_mr(int pp) { return pp / 16 <= 4 ? 4 : 2; }
+inline int cq_kr(int n, int pp) {
+    const int rb = (n + 16 * cq_mr(pp) - 1) / (16 * cq_mr(pp));
+    int sp = (2048 + rb - 1) / rb;
+    sp = sp < n / 512 ? sp : n / 512;
+    sp = sp > 1 ? sp : 1;
+    return ((n + sp - 1) / sp + 63) / 64 * 64;
+}
+inline int cq_splits(int n, int pp) { return (n + cq_kr(n, pp) - 1) / cq_kr(n, pp); }
 
 PcaLayout pca_layout(void *ws, int n, int k) {
     const int p = pca_p(n, k), pp = pca_pp(n, k);
     char *w = static_cast<char *>(ws);
     PcaLayout L;
     L.Q = reinterpret_cast<float *>(w);
-    w += align256(sizeof(float) * static_cast<size_t>(n) * pp);
+    w += align256(sizeof(float) * block_floats(n, pp));
     L.Z = reinterpret_cast<float *>(w);
-    w += align256(sizeof(float) * static_cast<size_t>(n) * pp);
+    w += align256(sizeof(float) * block_floats(n, pp));
+    const int sp = cq_splits(n, pp);
+    L.Zs = sp > 1 ? reinterpret_cast<float *>(w) : L.Z;
+    w += sp > 1 ? align256(sizeof(float) * block_floats(n, pp) * sp) : 0;
     L.part = reinterpret_cast<double *>(w);
     w += align256(sizeof(double) * static_cast<size_t>(gram_chunks(n)) * p * p);
     L.Rinv = reinterpret_cast<double *>(w);
@@ -806,17 +1058,31 @@ PcaLayout pca_layout(void *ws, int n, int k) {
     return L;
 }
 
-hipError_t launch_cq(const float *C, int n, int pp, const float *Q, float *Z, hipStream_t s) {
-    const dim3 grid(static_cast<unsigned>((n + 63) / 64));
+template <int NB>
+void launch_cq_nb(const float *C, int n, const float *Q, float *Zs, hipStream_t s) {
+    constexpr int MR = NB <= 4 ? 4 : 2;
+    const int kr = cq_kr(n, 16 * NB);
+    const dim3 grid(static_cast<unsigned>((n + 16 * MR - 1) / (16 * MR)), static_cast<unsigned>((n + kr - 1) / kr));
+    hipLaunchKernelGGL((k_cq_part<NB, MR>), grid, dim3(256), 0, s, C, n, Q, kr, Zs);
+}
+
+hipError_t launch_cq(const PcaLayout &L, const float *C, int n, int pp, const float *Q, float *Z, hipStream_t s) {
+    const int sp = cq_splits(n, pp);
+    float *dst = sp > 1 ? L.Zs : Z;
     switch (pp / 16) {
-        case 1: hipLaunchKernelGGL(k_cq<1>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        case 2: hipLaunchKernelGGL(k_cq<2>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        case 3: hipLaunchKernelGGL(k_cq<3>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        case 4: hipLaunchKernelGGL(k_cq<4>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        case 5: hipLaunchKernelGGL(k_cq<5>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        case 6: hipLaunchKernelGGL(k_cq<6>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        case 7: hipLaunchKernelGGL(k_cq<7>, grid, dim3(256), 0, s, C, n, Q, Z); break;
-        default: hipLaunchKernelGGL(k_cq<8>, grid, dim3(256), 0, s, C, n, Q, Z); break;
+        case 1: launch_cq_nb<1>(C, n, Q, dst, s); break;
+        case 2: launch_cq_nb<2>(C, n, Q, dst, s); break;
+        case 3: launch_cq_nb<3>(C, n, Q, dst, s); break;
+        case 4: launch_cq_nb<4>(C, n, Q, dst, s); break;
+        case 5: launch_cq_nb<5>(C, n, Q, dst, s); break;
+        case 6: launch_cq_nb<6>(C, n, Q, dst, s); break;
+        case 7: launch_cq_nb<7>(C, n, Q, dst, s); break;
+        default: launch_cq_nb<8>(C, n, Q, dst, s); break;
+    }
+    if (sp > 1) {
+        const int64_t nv = static_cast<int64_t>(block_floats(n, pp) / 4);
+        hipLaunchKernelGGL(k_cq_sum, dim3(static_cast<unsigned>((nv + 255) / 256)), dim3(256), 0, s,
+                           reinterpret_cast<const f32x4 *>(L.Zs), nv, sp, reinterpret_cast<f32x4 *>(Z));
     }
     return hipGetLastError();
 }
@@ -824,9 +1090,9 @@ hipError_t launch_cq(const float *C, int n, int pp, const float *Q, float *Z, hi
 // Q = orthonormalised Z (shifted CholQR)
 void cholqr(const PcaLayout &L, int n, int p, int pp, const float *Z, float *Q, hipStream_t s) {
     const int chunks = gram_chunks(n);
-    hipLaunchKernelGGL(k_gram_part, dim3(static_cast<unsigned>(chunks)), dim3(256), 0, s, Z, Z, n, p, pp, L.part);
-    hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Rinv);
-    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(n) * pp + 255) / 256);
+    launch_gram(Z, Z, n, p, pp, L.part, s);
+    launch_chol_inv(L.part, chunks, p, L.Rinv, s);
+    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(block_floats(n, pp) / 4) + 255) / 256);
     hipLaunchKernelGGL(k_apply_rinv, dim3(g), dim3(256), 0, s, Z, n, p, pp, L.Rinv, Q);
 }
 
@@ -834,7 +1100,9 @@ void cholqr(const PcaLayout &L, int n, int p, int pp, const float *Z, float *Q, 
 
 size_t pca_ws_bytes(int n, int k) {
     const int p = pca_p(n, k), pp = pca_pp(n, k);
-    return 2 * align256(sizeof(float) * static_cast<size_t>(n) * pp) +
+    const int sp = cq_splits(n, pp);
+    return 2 * align256(sizeof(float) * block_floats(n, pp)) +
+           (sp > 1 ? align256(sizeof(float) * block_floats(n, pp) * sp) : 0) +
            align256(sizeof(double) * static_cast<size_t>(gram_chunks(n)) * p * p) +
            2 * align256(sizeof(double) * static_cast<size_t>(p) * p) + align256(sizeof(double) * p);
 }
@@ -843,21 +1111,20 @@ hipError_t launch_pca_topk(const float *C, int n, int k, int iters, void *P, boo
                            float *eigvals, void *ws, hipStream_t s) {
     const int p = pca_p(n, k), pp = pca_pp(n, k);
     const PcaLayout L = pca_layout(ws, n, k);
-    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(n) * pp + 255) / 256);
+    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(block_floats(n, pp)) + 255) / 256);
     hipLaunchKernelGGL(k_pca_init, dim3(g), dim3(256), 0, s, L.Q, n, p, pp);
     for (int it = 0; it < iters; ++it) {
-        hipError_t e = launch_cq(C, n, pp, L.Q, L.Z, s);
+        hipError_t e = launch_cq(L, C, n, pp, L.Q, L.Z, s);
         if (e != hipSuccess) return e;
         cholqr(L, n, p, pp, L.Z, L.Q, s);
     }
     // second orthonormalisation (CholQR2) into Z, then Rayleigh-Ritz on the
     // basis Z: Q = C Z, T = Z^T Q
     cholqr(L, n, p, pp, L.Q, L.Z, s);
-    hipError_t e = launch_cq(C, n, pp, L.Z, L.Q, s);
+    hipError_t e = launch_cq(L, C, n, pp, L.Z, L.Q, s);
     if (e != hipSuccess) return e;
     const int chunks = gram_chunks(n);
-    hipLaunchKernelGGL(k_gram_part, dim3(static_cast<unsigned>(chunks)), dim3(256), 0, s, L.Z, L.Q, n, p, pp,
-                       L.part);
+    launch_gram(L.Z, L.Q, n, p, pp, L.part, s);
     hipLaunchKernelGGL(k_jacobi, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
     // the Ritz vectors [k][n] overwrite Q (k <= pp)
     hipLaunchKernelGGL(k_ritz, dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(k)), dim3(256), 0,
