@@ -666,10 +666,10 @@ __device__ __forceinline__ double readlane_d(double v, int src) {
 // X = R^{-1} column by column, x_c = (delta_rc - sum over m < c of
 // x_m R_mc) / R_cc, with column c of R read from lanes m <= c; x_c replaces
 // the row's entry c, whose last reader was that column.  All in fp64.
-// Writes R^{-1} [p][p] (zero below the diagonal).
+// Writes R^{-T} [p][p] (R^{-1} transposed: zero above the diagonal).
 template <int PM>
 __global__ __launch_bounds__(256) void k_chol_inv_reg(const double *__restrict__ part, int chunks, int p,
-                                                      double *__restrict__ Rinv) {
+                                                      double *__restrict__ RinvT) {
     __shared__ double A[PM * PM];
     const int tid = threadIdx.x, np = p * p;
     sum_partials(part, chunks, np, A, tid);
@@ -677,8 +677,12 @@ __global__ __launch_bounds__(256) void k_chol_inv_reg(const double *__restrict__
     if (tid >= kWave) return;
     const int r = tid;                // the lane's row (lanes >= PM carry an unused identity row)
     double a[PM];
+    const int rr = r < p ? r : p - 1;   // clamped: every lane loads, padding is selected afterwards
 #pragma unroll
-    for (int c = 0; c < PM; ++c) a[c] = r < p && c < p ? A[r * p + c] : r == c ? 1.0 : 0.0;
+    for (int c = 0; c < PM; ++c) {
+        const double g = A[rr * p + (c < p ? c : p - 1)];
+        a[c] = r < p && c < p ? g : r == c ? 1.0 : 0.0;
+    }
     double tr = r < p ? A[r * p + r] : 0.0;
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) tr += __shfl_xor(tr, o, kWave);   // the same butterfly in every lane
@@ -695,31 +699,36 @@ __global__ __launch_bounds__(256) void k_chol_inv_reg(const double *__restrict__
 #pragma unroll
         for (int c = j + 1; c < PM; ++c) {
             const double rjc = readlane_d(a[c], j) * inv;   // R_jc
-            if (r > j) a[c] = fma(-rjr, rjc, a[c]);
-            else if (r == j) a[c] = rjc;
+            const double upd = fma(-rjr, rjc, a[c]);
+            a[c] = r > j ? upd : r == j ? rjc : a[c];
+            if ((c - j) % 8 == 0) __builtin_amdgcn_sched_barrier(0);   // at most 8 readlane pairs live
         }
-        if (r == j) a[j] = rjj;
+        a[j] = r == j ? rjj : a[j];
+        __builtin_amdgcn_sched_barrier(0);   // a step's readlanes stay in the step (scalar registers)
     }
 #pragma unroll
     for (int c = 0; c < PM; ++c) {
         double s = c == r ? 1.0 : 0.0;
 #pragma unroll
-        for (int m = 0; m < c; ++m) s = fma(-a[m], readlane_d(a[c], m), s);
+        for (int m = 0; m < c; ++m) {
+            s = fma(-a[m], readlane_d(a[c], m), s);
+            if (m % 8 == 7) __builtin_amdgcn_sched_barrier(0);
+        }
         a[c] = s / readlane_d(a[c], c);
+        __builtin_amdgcn_sched_barrier(0);
     }
-    if (r < p) {
+    // R^{-T}: lane r's row of R^{-1} is column r, so each store is coalesced
 #pragma unroll
-        for (int c = 0; c < PM; ++c)
-            if (c < p) Rinv[r * p + c] = a[c];
-    }
+    for (int c = 0; c < PM; ++c)
+        if (r < p && c < p) RinvT[c * p + r] = a[c];
 }
 
 // p > 64: one workgroup, G = sum of the chunk partials, then the shifted
 // Cholesky (right-looking, a barrier per phase of each step) and R^{-1}
 // (thread c solves R x = e_c upwards, x kept below the diagonal), in fp64 in
-// LDS.  Writes R^{-1} [p][p] (zero below the diagonal).
+// LDS.  Writes R^{-T} [p][p] (R^{-1} transposed: zero above the diagonal).
 __global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ part, int chunks, int p,
-                                                  double *__restrict__ Rinv) {
+                                                  double *__restrict__ RinvT) {
     __shared__ double A[kMaxP * kMaxP];   // G; then R on and above the diagonal, R^{-1} (transposed) below it
     __shared__ double red[256];
     const int tid = threadIdx.x, np = p * p;
@@ -762,21 +771,23 @@ __global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ par
     __syncthreads();
     for (int e = tid; e < np; e += 256) {
         const int r = e / p, c = e - (e / p) * p;
-        Rinv[e] = r < c ? A[c * p + r] : r == c ? 1.0 / A[r * p + r] : 0.0;
+        // element e of R^{-T} is (R^{-1})[c][r]: nonzero for c <= r
+        RinvT[e] = c < r ? A[r * p + c] : r == c ? 1.0 / A[r * p + r] : 0.0;
     }
 }
 
-void launch_chol_inv(const double *part, int chunks, int p, double *Rinv, hipStream_t s) {
-    if (p <= 32) hipLaunchKernelGGL(k_chol_inv_reg<32>, dim3(1), dim3(256), 0, s, part, chunks, p, Rinv);
-    else if (p <= 64) hipLaunchKernelGGL(k_chol_inv_reg<64>, dim3(1), dim3(256), 0, s, part, chunks, p, Rinv);
-    else hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, part, chunks, p, Rinv);
+void launch_chol_inv(const double *part, int chunks, int p, double *RinvT, hipStream_t s) {
+    if (p <= 32) hipLaunchKernelGGL(k_chol_inv_reg<32>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
+    else if (p <= 64) hipLaunchKernelGGL(k_chol_inv_reg<64>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
+    else hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
 }
 
 // Q = Z R^{-1} in row quads: a thread forms one column j of four rows, each
-// entry sum over m <= j of Z[i][m] R^{-1}[m][j] in fp64 (fp32 result); the
-// padding columns j >= p are zero.
+// entry sum over m <= j of Z[i][m] R^{-1}[m][j] in fp64 (fp32 result), with
+// R^{-1} given transposed (column j is a contiguous row); the padding
+// columns j >= p are zero.
 __global__ __launch_bounds__(256) void k_apply_rinv(const float *__restrict__ Z, int n, int p, int pp,
-                                                    const double *__restrict__ Rinv, float *__restrict__ Q) {
+                                                    const double *__restrict__ RinvT, float *__restrict__ Q) {
     const int64_t v = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;   // 128-bit element of Q
     if (v >= static_cast<int64_t>(round4(n) / 4) * pp) return;
     const int64_t quad = v / pp;
@@ -786,7 +797,7 @@ __global__ __launch_bounds__(256) void k_apply_rinv(const float *__restrict__ Z,
     if (j < p)
         for (int m = 0; m <= j; ++m) {
             const f32x4 z = Z4[m];
-            const double r = Rinv[static_cast<size_t>(m) * p + j];
+            const double r = RinvT[static_cast<size_t>(j) * p + m];
             s0 = fma(static_cast<double>(z[0]), r, s0);
             s1 = fma(static_cast<double>(z[1]), r, s1);
             s2 = fma(static_cast<double>(z[2]), r, s2);
@@ -1013,7 +1024,7 @@ namespace {
 
 struct PcaLayout {
     float *Q, *Z, *Zs;
-    double *part, *Rinv, *Wt, *theta;
+    double *part, *RinvT, *Wt, *theta;
 };
 
 inline int pca_p(int n, int k) {
@@ -1050,7 +1061,7 @@ PcaLayout pca_layout(void *ws, int n, int k) {
     w += sp > 1 ? align256(sizeof(float) * block_floats(n, pp) * sp) : 0;
     L.part = reinterpret_cast<double *>(w);
     w += align256(sizeof(double) * static_cast<size_t>(gram_chunks(n)) * p * p);
-    L.Rinv = reinterpret_cast<double *>(w);
+    L.RinvT = reinterpret_cast<double *>(w);
     w += align256(sizeof(double) * static_cast<size_t>(p) * p);
     L.Wt = reinterpret_cast<double *>(w);
     w += align256(sizeof(double) * static_cast<size_t>(p) * p);
@@ -1091,9 +1102,9 @@ hipError_t launch_cq(const PcaLayout &L, const float *C, int n, int pp, const fl
 void cholqr(const PcaLayout &L, int n, int p, int pp, const float *Z, float *Q, hipStream_t s) {
     const int chunks = gram_chunks(n);
     launch_gram(Z, Z, n, p, pp, L.part, s);
-    launch_chol_inv(L.part, chunks, p, L.Rinv, s);
+    launch_chol_inv(L.part, chunks, p, L.RinvT, s);
     const unsigned g = static_cast<unsigned>((static_cast<int64_t>(block_floats(n, pp) / 4) + 255) / 256);
-    hipLaunchKernelGGL(k_apply_rinv, dim3(g), dim3(256), 0, s, Z, n, p, pp, L.Rinv, Q);
+    hipLaunchKernelGGL(k_apply_rinv, dim3(g), dim3(256), 0, s, Z, n, p, pp, L.RinvT, Q);
 }
 
 }  // namespace
