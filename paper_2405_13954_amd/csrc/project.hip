@@ -8,8 +8,7 @@
 // tiles of a ragged batch are empty):
 //
 //  0. k_project_prep: clears the work counter and, for masked inputs, builds
-//     the ordered list of 64-token tiles holding at least one valid token,
-//     with the list position of each example's first tile.
+//     the ordered list of 64-token tiles holding at least one valid token.
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
 //     = one contraction chunk (<= 4096 columns) of one side (x or dy) of one
 //     listed tile.  Layers given the same x tensor (q/k/v, gate/up of a
@@ -25,16 +24,12 @@
 //     they read zeros without a memory access or a branch, so NaN/Inf in
 //     padding cannot leak.  The waves' partial x'/dy' are folded in a fixed
 //     order and written, in the MFMA result layout, to the workspace.
-//  B. k_project_tile_finish: per listed tile, x' and dy' are the fixed-order
-//     sums of their chunk partials; the tile's sum over tokens of dy'_t x'_t^T
-//     is then formed in fp32 from LDS (KT x KT outputs per thread).
-//  C. k_project_reduce: per example, the sums of its listed tiles are added
-//     in tile order and G_b is written (fp32 or bf16, round to nearest even)
-//     to the caller's store row; an example without a valid token gets 0.
-// B and C stay separate kernels: handing partials between workgroups inside
-// A needs an agent-scope release and acquire per item, and on gfx950 those
-// write back and invalidate the L2 of the XCD (buffer_wbl2 / buffer_inv),
-// which the streaming loop cannot afford.
+//  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
+//     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
+//     formed in fp32 from LDS (KT x KT outputs per thread).  Empty tiles give 0.
+//  C. k_project_reduce: per example, the tile sums are added in tile order
+//     and G_b is written (fp32 or bf16, round to nearest even) to the
+//     caller's store row.
 // Every sum has a fixed order, so results are bitwise reproducible.
 #include "common.h"
 #include "internal.h"
@@ -68,7 +63,6 @@ constexpr int NT = NW * kWave;            // threads per workgroup
 __host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? 4096 : LOGRA_PROJ_CHUNK; }
 __host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGRA_PROJ_STAGES; }
 
-
 constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
 
 struct ChunkLayer {
@@ -76,7 +70,6 @@ struct ChunkLayer {
     const void *dy;
     const void *p_in;
     const void *p_out;
-    void *g_out;         // the caller's store row of example 0
     int64_t part_begin;  // first float of this layer's chunk partials
     int n_in, n_out;
     int c_in, c_out;     // chunks of the x side and of the dy side (partial slots per tile)
@@ -96,8 +89,6 @@ struct ProjArgs {
     const int *tiles;     // non-empty tiles (b * tpe + tile) in index order; NULL = all
     const int *n_tiles;   // their count (device), read when tiles != NULL
     int *work;            // items handed out beyond the first gridDim.x (device counter)
-    const int *ex_first;  // [B + 1]: list position of each example's first tile; [B] = count
-    int64_t g_ld;         // store row stride of g_out, elements
     float *part;    // chunk partials, MFMA result layout, TT x 16KT floats each
     float *gpart;   // per-tile sums  [layer][b][tile][k_out * k_in]
     int B, T, tpe;  // tpe = tiles per example
@@ -227,12 +218,13 @@ __device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, in
     return any;
 }
 
-// One chunk item (see the file comment); wave 0 stores the partials.  An
-// x-side item of a layer whose x is shared produces the x' partials of every
-// layer sharing it (S >= share_n).
+// One chunk item (see the file comment).  Returns without a barrier when the
+// tile is fully masked; every thread of the workgroup takes the same path.
+// An x-side item of a layer whose x is shared produces the x' partials of
+// every layer sharing it (S >= share_n).
 template <int KT, int S, typename TIn>
 __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int count, f32x4 *slot, int lane,
-                                               int wave) {
+                                           int wave) {
     const int rank = item / count;              // position of the work slot in processing order
     const int j = item - rank * count;          // listed tile
     const int gslot = a.ordered ? a.slot_order[rank] : rank;   // work slot over all layers
@@ -306,90 +298,6 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     }
 }
 
-// Sum over the tokens of tile bt of dy'_t x'_t^T for layer l (the whole
-// workgroup): x' and dy' are the fixed-order sums of the tile's chunk
-// partials, staged in LDS (xs, ds: TT x 16KT floats each); the k_out x k_in
-// result goes to gdst.  Thread (ob, ib) of a 16 x 16 grid owns outputs
-// o = KT ob + u, i = KT ib + v for u, v < KT.
-template <int KT>
-__device__ __forceinline__ void tile_sum(const ProjArgs &a, int l, int bt, float *xs, float *ds, float *gdst,
-                                         int tid) {
-    static_assert(NT == 256, "a 16 x 16 thread grid");
-    constexpr int KP = 16 * KT;
-    constexpr int NQ = MB * KT * kWave;     // f32x4 per chunk partial
-    const ChunkLayer &L = a.layer[l];
-    const int C = L.c_in + L.c_out;
-    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP));
-    for (int q = tid; q < NQ; q += NT) {
-        f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sd = {0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < L.c_in; ++c) sx += src[static_cast<size_t>(c) * NQ + q];
-        for (int c = L.c_in; c < C; ++c) sd += src[static_cast<size_t>(c) * NQ + q];
-        const int lane = q & (kWave - 1), mj = q / kWave;
-        const int m = mj / KT, j = mj - m * KT;
-        const int row = lane & 15, kg = lane >> 4;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            xs[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sx[r];
-            ds[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sd[r];
-        }
-    }
-    __syncthreads();
-    const int ob = tid >> 4, ib = tid & 15;
-    float c[KT][KT];
-#pragma unroll
-    for (int u = 0; u < KT; ++u)
-#pragma unroll
-        for (int v = 0; v < KT; ++v) c[u][v] = 0.f;
-#pragma unroll 4
-    for (int t = 0; t < TT; ++t) {
-        float dv[KT], xv[KT];
-#pragma unroll
-        for (int u = 0; u < KT; ++u) {
-            dv[u] = ds[t * KP + KT * ob + u];
-            xv[u] = xs[t * KP + KT * ib + u];
-        }
-#pragma unroll
-        for (int u = 0; u < KT; ++u)
-#pragma unroll
-            for (int v = 0; v < KT; ++v) c[u][v] = __builtin_fmaf(dv[u], xv[v], c[u][v]);
-    }
-#pragma unroll
-    for (int u = 0; u < KT; ++u) {
-        const int o = KT * ob + u;
-        if (o >= a.k_out) break;
-#pragma unroll
-        for (int v = 0; v < KT; ++v) {
-            const int i = KT * ib + v;
-            if (i < a.k_in) gdst[o * a.k_in + i] = c[u][v];
-        }
-    }
-}
-
-// G_b of layer l: the tile sums of example b added in tile order, over the
-// tiles at list positions ex_first[b] .. ex_first[b + 1] - 1 (fully masked
-// tiles are not listed: their sums are zero and adding +0 changes nothing),
-// written to the caller's store row (fp32 or bf16, round to nearest even).
-template <typename TOut>
-__device__ __forceinline__ void example_sum(const ProjArgs &a, int l, int b, int tid, int nthreads) {
-    const int D = a.k_in * a.k_out;
-    const int i0 = a.ex_first[b], i1 = a.ex_first[b + 1];
-    const float *p = a.gpart + static_cast<size_t>(l) * a.B * a.tpe * D;
-    TOut *out = static_cast<TOut *>(a.layer[l].g_out) + static_cast<int64_t>(b) * a.g_ld;
-    for (int i = tid; i < D; i += nthreads) {
-        float s = 0.f;
-        int t = i0;
-        for (; t + 8 <= i1; t += 8) {   // eight loads in flight, summed in tile order
-            float v[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(a.tiles ? a.tiles[t + u] : t + u) * D + i];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) s += v[u];
-        }
-        for (; t < i1; ++t) s += p[static_cast<size_t>(a.tiles ? a.tiles[t] : t) * D + i];
-        store_out<TOut>(out + i, s);
-    }
-}
-
 // Persistent: the grid is sized to the resident capacity of the GPU.  Each
 // workgroup starts on item blockIdx.x and, when done, takes the next
 // unclaimed item from the work counter.  Claiming only when free keeps the
@@ -415,11 +323,10 @@ __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(Proj
 
 // Clears the work counter and, with a mask, lists the tiles that hold at
 // least one valid token, in tile order (one workgroup; block-wide prefix
-// counts keep the order), with the list position of each example's first
-// tile.  A full tile's 64 mask bytes are read as four 128-bit loads when the
-// mask rows are 16-byte aligned.
+// counts keep the order).  A full tile's 64 mask bytes are read as four
+// 128-bit loads when the mask rows are 16-byte aligned.
 __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int B, int T, int tpe, int *tiles,
-                                                        int *n_tiles, int *work, int *ex_first) {
+                                                        int *n_tiles, int *work) {
     __shared__ int wsum[16];
     __shared__ int base;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -427,18 +334,15 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
         *work = 0;
         base = 0;
     }
-    if (mask == nullptr) {
-        for (int b = tid; b <= B; b += 1024) ex_first[b] = b * tpe;
-        return;
-    }
+    if (mask == nullptr) return;
     const bool vec = (reinterpret_cast<uintptr_t>(mask) & 15) == 0 && (T & 15) == 0;
     __syncthreads();
     const int total = B * tpe;
     for (int t0 = 0; t0 < total; t0 += 1024) {
         const int bt = t0 + tid;
-        const int b = bt / tpe, tile = bt - b * tpe;
         int any = 0;
         if (bt < total) {
+            const int b = bt / tpe, tile = bt - b * tpe;
             const uint8_t *m = mask + static_cast<size_t>(b) * T + static_cast<size_t>(tile) * TT;
             const int n = min(TT, T - tile * TT);
             if (vec && n == TT) {
@@ -464,37 +368,103 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
             all += wsum[w];
         }
         if (any) tiles[base + before + x - 1] = bt;
-        if (bt < total && tile == 0) ex_first[b] = base + before + x - any;
         __syncthreads();
         if (tid == 0) base += all;
         __syncthreads();
     }
-    if (tid == 0) {
-        *n_tiles = base;
-        ex_first[B] = base;
+    if (tid == 0) *n_tiles = base;
+}
+
+template <int KT>
+__global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a) {
+    constexpr int KP = 16 * KT;
+    constexpr int NQ = MB * KT * kWave;     // f32x4 per chunk partial
+    __shared__ float xs[TT * KP];            // x'  [token][i]
+    __shared__ float ds[TT * KP];            // dy' [token][o]
+    const int per_layer = a.B * a.tpe;
+    const int l = blockIdx.x / per_layer;
+    const int bt = blockIdx.x - l * per_layer;
+    const int b = bt / a.tpe, tile = bt - b * a.tpe;
+    const int tid = threadIdx.x;
+    const int D = a.k_in * a.k_out;
+    float *gdst = a.gpart + static_cast<size_t>(blockIdx.x) * D;
+
+    bool tok_ok[MB];
+    const bool any = lane_tokens(a, b, tile * TT, tid & (kWave - 1), tok_ok);
+    if (!__syncthreads_or(any)) {
+        for (int i = tid; i < D; i += 256) gdst[i] = 0.f;
+        return;
+    }
+    const ChunkLayer &L = a.layer[l];
+    const int C = L.c_in + L.c_out;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP));
+    for (int q = tid; q < NQ; q += 256) {
+        f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sd = {0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < L.c_in; ++c) sx += src[static_cast<size_t>(c) * NQ + q];
+        for (int c = L.c_in; c < C; ++c) sd += src[static_cast<size_t>(c) * NQ + q];
+        const int lane = q & (kWave - 1), mj = q / kWave;
+        const int m = mj / KT, j = mj - m * KT;
+        const int row = lane & 15, kg = lane >> 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            xs[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sx[r];
+            ds[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sd[r];
+        }
+    }
+    __syncthreads();
+
+    // Sum over the tile's tokens of dy'_t x'_t^T: thread (ob, ib) of a 16 x 16
+    // grid owns outputs o = KT ob + u, i = KT ib + v for u, v < KT.
+    const int ob = tid >> 4, ib = tid & 15;
+    float c[KT][KT];
+#pragma unroll
+    for (int u = 0; u < KT; ++u)
+#pragma unroll
+        for (int v = 0; v < KT; ++v) c[u][v] = 0.f;
+    for (int t = 0; t < TT; ++t) {
+        float dv[KT], xv[KT];
+#pragma unroll
+        for (int u = 0; u < KT; ++u) {
+            dv[u] = ds[t * KP + KT * ob + u];
+            xv[u] = xs[t * KP + KT * ib + u];
+        }
+#pragma unroll
+        for (int u = 0; u < KT; ++u)
+#pragma unroll
+            for (int v = 0; v < KT; ++v) c[u][v] = __builtin_fmaf(dv[u], xv[v], c[u][v]);
+    }
+#pragma unroll
+    for (int u = 0; u < KT; ++u) {
+        const int o = KT * ob + u;
+        if (o >= a.k_out) break;
+#pragma unroll
+        for (int v = 0; v < KT; ++v) {
+            const int i = KT * ib + v;
+            if (i < a.k_in) gdst[o * a.k_in + i] = c[u][v];
+        }
     }
 }
 
-// B and C of the file comment: the sum of every listed (layer, tile), then
-// every (layer, example) sum.  The grid covers all tiles of each layer;
-// workgroups past the listed count have nothing to do.
-template <int KT>
-__global__ __launch_bounds__(NT) void k_project_tile_finish(ProjArgs a) {
-    __shared__ float xs[TT * 16 * KT];   // x'  [token][i]
-    __shared__ float ds[TT * 16 * KT];   // dy' [token][o]
-    const int per_layer = a.B * a.tpe;
-    const int l = blockIdx.x / per_layer;
-    const int j = blockIdx.x - l * per_layer;
-    if (a.tiles && j >= *a.n_tiles) return;
-    const int bt = a.tiles ? a.tiles[j] : j;
-    tile_sum<KT>(a, l, bt, xs, ds, a.gpart + (static_cast<size_t>(l) * per_layer + bt) * (a.k_in * a.k_out),
-                 threadIdx.x);
-}
-
 template <typename TOut>
-__global__ __launch_bounds__(256) void k_project_reduce(ProjArgs a) {
-    const int l = blockIdx.x / a.B;
-    example_sum<TOut>(a, l, blockIdx.x - l * a.B, threadIdx.x, blockDim.x);
+__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, int B,
+                                                        int tpe, int D, int64_t g_ld) {
+    const int l = blockIdx.x / B;
+    const int b = blockIdx.x - l * B;
+    const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * D;
+    TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
+    for (int i = threadIdx.x; i < D; i += blockDim.x) {
+        float s = 0.f;
+        int t = 0;
+        for (; t + 8 <= tpe; t += 8) {   // eight loads in flight, summed in tile order
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * D + i];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * D + i];
+        store_out<TOut>(out + i, s);
+    }
 }
 
 inline int kt_for(int k_in, int k_out) {
@@ -604,20 +574,15 @@ void launch_chunks(const ProjArgs &a, int max_items, int smax, hipStream_t s) {
 
 static_assert(sizeof(ProjArgs) <= 3840, "kernel arguments must stay well under the 4 KB limit");
 
-// Integer workspace: tile list [B * tpe], its count, the work counter and
-// ex_first [B + 1].
-size_t index_ints(int B, int T) {
-    return static_cast<size_t>(B) * ((T + TT - 1) / TT) + 2 + (B + 1);
-}
-
 }  // namespace
 
 size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, int T, int k_in,
                         int k_out) {
     if (n_layers <= 0 || B <= 0 || T <= 0) return 0;
     const Plan p = plan_group(n_in, n_out, n_layers, B, T, k_in, k_out, nullptr);
+    const size_t tiles = static_cast<size_t>(B) * ((T + TT - 1) / TT);
     return align256(p.part_floats * sizeof(float)) + align256(p.gpart_floats * sizeof(float)) +
-           align256(index_ints(B, T) * sizeof(int));
+           align256((tiles + 2) * sizeof(int));
 }
 
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
@@ -632,7 +597,6 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
         a.layer[l].dy = grp.layer[l].dy;
         a.layer[l].p_in = grp.layer[l].p_in;
         a.layer[l].p_out = grp.layer[l].p_out;
-        a.layer[l].g_out = grp.layer[l].g_out;
     }
     const Plan p = plan_group(n_in, n_out, grp.n_layers, B, T, k_in, k_out, &a);
     const int KT = kt_for(k_in, k_out);
@@ -674,15 +638,12 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     a.k_in = k_in;
     a.k_out = k_out;
     a.ck = chunk_cols(KT);
-    a.g_ld = g_ld;
     int *list = reinterpret_cast<int *>(w);
     int *count = list + static_cast<size_t>(B) * a.tpe;
     a.work = count + 1;
     a.tiles = mask ? list : nullptr;
     a.n_tiles = mask ? count : nullptr;
-    int *ex_first = count + 2;
-    a.ex_first = ex_first;
-    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count, a.work, ex_first);
+    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count, a.work);
     const int max_items = a.slots * B * a.tpe;
     switch (KT) {
         case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, smax, s) : launch_chunks<1, float>(a, max_items, smax, s); break;
@@ -703,9 +664,11 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     if (e != hipSuccess) return e;
     const unsigned grid = static_cast<unsigned>(grp.n_layers) * B;
     if (bf16_out)
-        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+                           k_in * k_out, g_ld);
     else
-        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+                           k_in * k_out, g_ld);
     return hipGetLastError();
 }
 
