@@ -9,7 +9,10 @@ updates.
 
 The logging leg's "shared_inputs" entry runs the same stream with the
 inputs a transformer block shares (q/k/v one x, gate/up one x), which the
-projection reads once.  Its "pca" entry times the PCA initialisation of the
+projection reads once.  Its "offload" entry runs the stream again with each
+step's store rows copied to a pinned host store (out-of-core logging), the
+copy enqueued behind the step on the compute stream, so the host is free
+while it runs.  Its "pca" entry times the PCA initialisation of the
 projections on one of its batches: the KFAC factor SYRKs of the gate layer
 (n = 4096 and 14,336) and their top-16 eigenvectors.
 
@@ -26,7 +29,8 @@ the 1/sqrt(self) scales applied before the top-100.
 
 All inputs are synthetic, drawn on the device before timing.  Each leg
 reports the roofline of its dominant kernel from HIP events recorded on the
-launch stream around every launch, and the float64 oracle timed on a bounded
+launch stream around the timed launches (the logging leg: one pair over each
+step's back-to-back launches), and the float64 oracle timed on a bounded
 sample on the host (rank 0 only).
 """
 from __future__ import annotations
@@ -314,6 +318,35 @@ def logging_leg(args, torch, P):
             "achieved_gbs": bytes_sh / (sh_timer.mean_ms() * 1e-3) / 1e9,
             "note": "q/k/v and gate/up given one x each, as in a transformer block; the headline value "
                     "uses separate inputs"}
+    if args.offload:
+        # out-of-core logging: after each step, its B store rows go to a
+        # pinned host store.  The copy is enqueued on the compute stream: the
+        # blit kernel that moves the rows costs ~20 us in line there, while on
+        # a copy stream it shares the CUs with the streaming projection and
+        # costs about ten times that.
+        host_store = torch.empty((n_rows, D_tot), dtype=torch.bfloat16).pin_memory()
+        off_timer = EventTimer(torch)
+
+        def step_off(st, timed):
+            step(st, timed, all_descs, off_timer)
+            P.logra_offload_rows(store[st * B:(st + 1) * B], host_store[st * B:(st + 1) * B])
+
+        for st in range(args.warmup):
+            step_off(st, False)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        for st in range(args.warmup, n_steps):
+            step_off(st, True)
+        torch.cuda.synchronize()
+        dt_off = time.perf_counter() - t2
+        same = bool(torch.equal(host_store.view(torch.int16), store.view(torch.int16).cpu()))
+        res["offload"] = {
+            "tokens_per_s": tokens / dt_off, "ms_per_step": dt_off * 1e3 / args.steps,
+            "proj_launch_ms": off_timer.mean_ms(), "bytes_per_step": B * D_tot * 2,
+            "host_store_equal": same,
+            "note": "each step's store rows copied to pinned host memory behind the step on the compute "
+                    "stream (asynchronous for the host)"}
+        del host_store
     if args.pca:
         res["pca"] = pca_sub_leg(args, torch, P, bufs[0], lens[0], masks[0], k)
     sample = None
@@ -634,6 +667,8 @@ def main():
                     help="skip the l-RelatIF sub-leg (self-influence + scaled scores)")
     ap.add_argument("--no-shared-inputs", dest="shared_inputs", action="store_false",
                     help="skip the logging pass with the inputs a transformer block shares")
+    ap.add_argument("--no-offload", dest="offload", action="store_false",
+                    help="skip the logging pass that copies each step's store rows to pinned host memory")
     ap.add_argument("--no-pca", dest="pca", action="store_false",
                     help="skip the PCA sub-leg (KFAC factor SYRK and top-k eigenvectors)")
     ap.add_argument("--pca-reps", type=int, default=3, help="timed SYRK calls per factor")
@@ -673,7 +708,7 @@ def main():
         r, log_sample = logging_leg(args, torch, P)
         out.update(value=r["tokens_per_s"], ms_per_step=r["ms_per_step"], examples_per_s=r["examples_per_s"],
                    roofline=r["roofline"], proj_launch_ms=r["proj_launch_ms"], cov_launch_ms=r["cov_launch_ms"])
-        for key in ("pca", "shared_inputs"):
+        for key in ("pca", "shared_inputs", "offload"):
             if key in r:
                 out[key] = r[key]
     if args.leg in ("all", "influence"):

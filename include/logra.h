@@ -274,6 +274,31 @@ int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, 
                            void *copy_stream);
 
 /* ------------------------------------------------------------------------
+ * Out-of-core logging.  The projected gradients of every training example
+ * are written to the store once, and the logging of the next batch overlaps
+ * the saving of the current one (App. E.2, efficient data IO).
+ *
+ * logra_offload_rows: copies `rows` rows of `row_bytes` bytes from device
+ * memory src (row stride ld_src bytes) to PINNED HOST memory dst
+ * (hipHostMalloc; row stride ld_dst bytes), after the work already enqueued
+ * on `stream` (an event recorded there is waited for on copy_stream), so the
+ * copy runs on copy_stream while the next batch is projected on `stream`.
+ * copy_stream NULL: the copy is enqueued on `stream` itself (in order, no
+ * overlap on the device, still asynchronous for the host).  The copy is a
+ * blit kernel: for a batch's rows on MI355X the in-order form is the cheaper
+ * one (~20 us per 1 MB), as a concurrent blit shares the CUs with the
+ * streaming projection.  done (optional, a hipEvent_t of the caller): recorded on the
+ * copying stream after the copy; dst holds the rows once it has completed.
+ * ASYNCHRONOUS.  src must not be overwritten until the copy has finished
+ * (make `stream` wait for `done` before reusing those rows).
+ * Errors: rows < 0, row_bytes <= 0 or a stride below row_bytes ->
+ * INVALID_ARG; src (first and last row) not device memory or dst (first and
+ * last row) not pinned host memory -> INVALID_ARG.  rows == 0: nothing.
+ * ---------------------------------------------------------------------- */
+int logra_offload_rows(const void *src, int64_t ld_src, void *dst, int64_t ld_dst, int64_t rows, int64_t row_bytes,
+                       void *stream, void *copy_stream, void *done);
+
+/* ------------------------------------------------------------------------
  * PCA initialisation of the projections (Sec. 3.2).  KFAC approximates a
  * layer's Hessian block by C_F (x) C_B, the Kronecker product of the
  * uncentered covariances of the layer's forward activations x and backward

@@ -37,7 +37,7 @@ EXPORTED = (
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
     "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_pca_ws_size", "logra_pca_topk",
-    "logra_influence_stream_ws_size", "logra_influence_stream",
+    "logra_influence_stream_ws_size", "logra_influence_stream", "logra_offload_rows",
 )
 
 
@@ -101,7 +101,8 @@ def lib():
         L.logra_influence_stream_ws_size.restype = sz
         L.logra_influence_stream.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, i32, vp, vp, vp, sz,
                                              vp, vp]
-        for name in ("logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
+        L.logra_offload_rows.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, vp]
+        for name in ("logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
@@ -345,3 +346,19 @@ def logra_influence_stream(g_test_pre, g_train_host, topk: int, topk_val, topk_i
     _check(lib().logra_influence_stream(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q, _ptr(g_train_host),
                                         code, ld_tr, N, D, int(chunk_rows), int(topk), _ptr(topk_val),
                                         _ptr(topk_idx), _ptr(ws), wsb, _stream(stream), cs))
+
+
+def logra_offload_rows(src, dst, stream=None, copy_stream=None, done=None):
+    """Copy the rows of src [rows, w] (device) into dst [rows, w] (pinned host, torch pin_memory=True,
+    same dtype) after the work enqueued on `stream`, on copy_stream (a torch.cuda.Stream) when given;
+    done: an optional torch.cuda.Event recorded after the copy.  Asynchronous (App. E.2)."""
+    rows = src.shape[0]
+    if dst.shape[0] != rows or dst.shape[1] != src.shape[1] or dst.dtype != src.dtype:
+        raise ValueError("src and dst must have the same rows, width and dtype")
+    es = src.element_size()
+    row_bytes = src.shape[1] * es
+    ld_src = (_rows(src, src.shape[1]) if rows > 0 else src.shape[1]) * es
+    ld_dst = (_rows(dst, dst.shape[1]) if rows > 0 else dst.shape[1]) * es
+    cs = None if copy_stream is None else ctypes.c_void_p(copy_stream.cuda_stream)
+    ev = None if done is None else ctypes.c_void_p(done.cuda_event)
+    _check(lib().logra_offload_rows(_ptr(src), ld_src, _ptr(dst), ld_dst, rows, row_bytes, _stream(stream), cs, ev))

@@ -512,6 +512,45 @@ int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, 
     return rc == LOGRA_OK ? ok() : rc;
 }
 
+int logra_offload_rows(const void *src, int64_t ld_src, void *dst, int64_t ld_dst, int64_t rows, int64_t row_bytes,
+                       void *stream, void *copy_stream, void *done) {
+    if (rows < 0 || row_bytes <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need rows >= 0 and row_bytes > 0");
+    if (ld_src < row_bytes || ld_dst < row_bytes)
+        return fail(LOGRA_ERR_INVALID_ARG, "row strides must be >= row_bytes");
+    if (rows == 0) return ok();
+    const int64_t last_src = (rows - 1) * ld_src + row_bytes - 1, last_dst = (rows - 1) * ld_dst + row_bytes - 1;
+    TRY(check_dev(src, "src", 1));
+    TRY(check_dev(static_cast<const char *>(src) + last_src, "the last row of src", 1));
+    TRY(check_pinned(dst, "dst", 1));
+    TRY(check_pinned(static_cast<char *>(dst) + last_dst, "the last row of dst", 1));
+    const hipStream_t cs = static_cast<hipStream_t>(stream);
+    hipStream_t xs = copy_stream ? static_cast<hipStream_t>(copy_stream) : cs;
+    hipError_t e = hipSuccess;
+    if (xs != cs) {
+        // the copy waits for the work enqueued on `stream` so far.  One event
+        // per thread and device serves every call: a wait takes the event's
+        // state when it is enqueued, so re-recording it later is harmless,
+        // and no call destroys an event that may still be pending.
+        int dev = 0;
+        if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "current device");
+        static thread_local hipEvent_t ready[64] = {};
+        if (dev < 0 || dev >= 64) return fail(LOGRA_ERR_UNSUPPORTED, "device index %d >= 64", dev);
+        if (!ready[dev] && (e = hipEventCreateWithFlags(&ready[dev], hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "event");
+        e = hipEventRecord(ready[dev], cs);
+        if (e == hipSuccess) e = hipStreamWaitEvent(xs, ready[dev], 0);
+        if (e != hipSuccess) return hip_fail(e, "order the copy after the stream");
+    }
+    e = ld_src == row_bytes && ld_dst == row_bytes
+            ? hipMemcpyAsync(dst, src, static_cast<size_t>(rows * row_bytes), hipMemcpyDeviceToHost, xs)
+            : hipMemcpy2DAsync(dst, static_cast<size_t>(ld_dst), src, static_cast<size_t>(ld_src),
+                               static_cast<size_t>(row_bytes), static_cast<size_t>(rows), hipMemcpyDeviceToHost, xs);
+    if (e != hipSuccess) return hip_fail(e, "device-to-host copy");
+    if (done && (e = hipEventRecord(static_cast<hipEvent_t>(done), xs)) != hipSuccess)
+        return hip_fail(e, "record done");
+    return ok();
+}
+
 size_t logra_act_cov_ws_size(int B, int T) {
     if (B <= 0 || T <= 0) return 0;
     return round256(logra::act_cov_ws_bytes(B, T));

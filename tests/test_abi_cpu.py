@@ -194,3 +194,15 @@ def test_influence_stream_ws_and_validation(L):
     assert f(*args(ld_tr=32)) == P.ERR_INVALID_ARG
     assert f(*args(D=60, ld_te=60, ld_tr=60)) == P.ERR_INVALID_ARG
     assert f(*args(Q=0)) == P.OK
+
+
+def test_offload_rows_validation(L):
+    f = L.logra_offload_rows
+    args = lambda **kw: [kw.get(k, v) for k, v in dict(
+        src=None, ld_src=64, dst=None, ld_dst=64, rows=4, row_bytes=64, st=None, cst=None, done=None).items()]
+    assert f(*args(rows=-1)) == P.ERR_INVALID_ARG
+    assert f(*args(row_bytes=0)) == P.ERR_INVALID_ARG
+    assert f(*args(ld_src=32)) == P.ERR_INVALID_ARG
+    assert f(*args(ld_dst=63)) == P.ERR_INVALID_ARG
+    assert f(*args(rows=0)) == P.OK                       # nothing to copy: no pointer is looked at
+    assert f(*args()) == P.ERR_INVALID_ARG                 # NULL src
