@@ -63,6 +63,13 @@ __device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t v
                  :: "s"(lds), "v"(voff), "s"(r) : "memory");
 }
 
+// The same copy with the non-temporal hint (nt): the lines it brings in are
+// the first to be evicted, for an operand that is streamed once.
+__device__ __forceinline__ void copy_to_lds_nt(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+                 :: "s"(lds), "v"(voff), "s"(r) : "memory");
+}
+
 // 32-bit LDS byte address of a __shared__ object (the address-space cast
 // yields the offset within the workgroup's LDS allocation).
 template <typename T>

@@ -40,6 +40,9 @@ namespace {
 #ifndef LOGRA_SC_NT
 #define LOGRA_SC_NT 0      // non-temporal hint on the train-operand loads
 #endif
+#ifndef LOGRA_SC_DMA_NT
+#define LOGRA_SC_DMA_NT 1  // non-temporal hint on k_scores_dma's train-operand copies
+#endif
 #ifndef LOGRA_SC_DMA
 #define LOGRA_SC_DMA 1     // 1: operands copied straight into LDS (k_scores_dma)
 #endif
@@ -256,7 +259,9 @@ __global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restri
 // instructions).  The LDS ring holds three slabs of the train operand, which
 // streams from HBM and is copied two slabs ahead, and two slabs of the test
 // operand, which the L2 mostly serves and is copied one slab ahead
-// (3 x 32 KB + 2 x 32 KB = 160 KB).  One barrier per slab: each wave waits
+// (3 x 32 KB + 2 x 32 KB = 160 KB).  The train copies carry the
+// non-temporal hint: the streamed rows are evicted first, so the test operand
+// (re-read by every train tile) stays in the caches longer.  One barrier per slab: each wave waits
 // for its own copies of the slab, the barrier makes every wave's copies
 // visible and frees the stages of the previous slab, and the next copies are
 // issued before the slab is multiplied.
@@ -390,8 +395,12 @@ __global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restric
                 mfma1(f, 2 * g + 1);
                 if (ks == 0)
                     copy_to_lds(rsa, ((g & 1) ? ka1 : ka0) ? oa[g] + dka : kBufOOB, la + g * 1024);
-                else if (ks == 1)
-                    copy_to_lds(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
+                else if (ks == 1) {
+                    if (LOGRA_SC_DMA_NT)
+                        copy_to_lds_nt(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
+                    else
+                        copy_to_lds(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
+                }
                 ldfrag1(f ^ 1, abase, bbase, ks + 1, g);
                 __builtin_amdgcn_sched_barrier(0);
             }
