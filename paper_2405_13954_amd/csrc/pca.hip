@@ -46,8 +46,10 @@
 //     shifted Cholesky Z^T Z + eps tr/p I = R^T R and R^{-1} in fp64 (p <= 64:
 //     one wave, a column per lane in registers; wider: LDS).
 //  5. k_apply_rinv: Q = Z R^{-1} (fp64 arithmetic, fp32 result).
-//  6. k_jacobi (one workgroup): T in LDS, round-robin parallel cyclic Jacobi
-//     (p/2 disjoint rotations per round), eigenvectors accumulated in W^T.
+//  6. k_jacobi_lds / k_jacobi (one workgroup): T in LDS, round-robin parallel
+//     cyclic Jacobi (p/2 disjoint rotations per round), eigenvectors
+//     accumulated in W^T (p <= 64: in LDS, each round one pass of 2 x 2
+//     blocks).
 //  7. k_ritz, k_pca_out: Ritz vectors in the order of decreasing theta, the
 //     sign rule, and the rows of P in the output dtype.
 //
@@ -921,6 +923,112 @@ __global__ __launch_bounds__(256) void k_jacobi(const double *__restrict__ part,
     for (int a = tid; a < p; a += 256) theta[a] = T[a * p + a];
 }
 
+// p <= 64: the same iteration with T and W^T both in LDS, and each round in
+// one pass.  A round's pairs partition the indices, so the block of T on the
+// rows of pair P and the columns of pair Q becomes G_P T_PQ G_Q^T with
+// G = [[c, -s], [s, c]] (the identity for a pair with the padding index):
+// the same products as rotating the rows and then the columns, formed by one
+// thread per block in place.  Rows a, b of W^T turn by G_P.  Two barriers
+// per round; the convergence sums reduce by wave butterflies.
+__global__ __launch_bounds__(256) void k_jacobi_lds(const double *__restrict__ part, int chunks, int p,
+                                                    double *__restrict__ Wt, double *__restrict__ theta) {
+    constexpr int PM = 64;
+    __shared__ double T[PM * PM], W[PM * PM];
+    __shared__ double cs[PM / 2], sn[PM / 2];
+    __shared__ int pa[PM / 2], pb[PM / 2];
+    __shared__ double red[8];
+    const int tid = threadIdx.x, np = p * p, lane = tid & 63, wave = tid >> 6;
+    sum_partials(part, chunks, np, T, tid);
+    __syncthreads();
+    for (int e = tid; e < np; e += 256) {
+        const int a = e / p, b = e - (e / p) * p;
+        if (a < b) {
+            const double v = 0.5 * (T[a * p + b] + T[b * p + a]);
+            T[a * p + b] = v;
+            T[b * p + a] = v;
+        }
+        W[e] = a == b ? 1.0 : 0.0;
+    }
+    __syncthreads();
+    const int m = p + (p & 1);   // players of the round-robin schedule
+    const int half = m / 2;
+    for (int sweep = 0; sweep < 40; ++sweep) {
+        double off = 0.0, all = 0.0;
+        for (int e = tid; e < np; e += 256) {
+            const int a = e / p, b = e - (e / p) * p;
+            const double v = T[e] * T[e];
+            all += v;
+            if (a != b) off += v;
+        }
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            off += __shfl_xor(off, o, kWave);
+            all += __shfl_xor(all, o, kWave);
+        }
+        if (lane == 0) {
+            red[2 * wave] = off;
+            red[2 * wave + 1] = all;
+        }
+        __syncthreads();
+        const double off_sum = ((red[0] + red[2]) + red[4]) + red[6];
+        const double all_sum = ((red[1] + red[3]) + red[5]) + red[7];
+        if (!(off_sum > 1e-30 * all_sum)) break;   // uniform: every thread read the same sums
+        for (int rnd = 0; rnd < m - 1; ++rnd) {   // red is rewritten only after this round's barriers
+            if (tid < half) {
+                auto player = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + rnd) % (m - 1); };
+                int a = player(tid), b = player(m - 1 - tid);
+                if (a > b) {
+                    const int t = a;
+                    a = b;
+                    b = t;
+                }
+                double c = 1.0, sv = 0.0;
+                if (b < p) {
+                    const double apq = T[a * p + b];
+                    if (apq != 0.0) {
+                        const double tau = (T[b * p + b] - T[a * p + a]) / (2.0 * apq);
+                        const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+                        c = 1.0 / sqrt(1.0 + t * t);
+                        sv = t * c;
+                    }
+                }
+                pa[tid] = a;
+                pb[tid] = b;
+                cs[tid] = c;
+                sn[tid] = sv;
+            }
+            __syncthreads();
+            for (int e = tid; e < half * half; e += 256) {
+                const int P = e / half, Q = e - (e / half) * half;
+                const int a = pa[P], b = pb[P], c2 = pa[Q], d = pb[Q];
+                const bool bp = b < p, bq = d < p;
+                const double cp = cs[P], sp = sn[P], cq = cs[Q], sq = sn[Q];
+                const double t00 = T[a * p + c2], t01 = bq ? T[a * p + d] : 0.0;
+                const double t10 = bp ? T[b * p + c2] : 0.0, t11 = bp && bq ? T[b * p + d] : 0.0;
+                const double u00 = cp * t00 - sp * t10, u01 = cp * t01 - sp * t11;
+                const double u10 = sp * t00 + cp * t10, u11 = sp * t01 + cp * t11;
+                T[a * p + c2] = cq * u00 - sq * u01;
+                if (bq) T[a * p + d] = sq * u00 + cq * u01;
+                if (bp) T[b * p + c2] = cq * u10 - sq * u11;
+                if (bp && bq) T[b * p + d] = sq * u10 + cq * u11;
+            }
+            for (int e = tid; e < half * p; e += 256) {
+                const int P = e / p, i = e - (e / p) * p;
+                const int a = pa[P], b = pb[P];
+                if (b < p) {
+                    const double c = cs[P], sv = sn[P];
+                    const double wa = W[a * p + i], wb = W[b * p + i];
+                    W[a * p + i] = c * wa - sv * wb;
+                    W[b * p + i] = sv * wa + c * wb;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int e = tid; e < np; e += 256) Wt[e] = W[e];
+    for (int a = tid; a < p; a += 256) theta[a] = T[a * p + a];
+}
+
 // Ritz vectors of the k largest theta (decreasing; equal values in index
 // order): V[e][i] = sum_j Q[i][j] Wt[order_e][j] (fp64 sums; Q in row
 // quads), eigvals[e].
@@ -1136,7 +1244,8 @@ hipError_t launch_pca_topk(const float *C, int n, int k, int iters, void *P, boo
     if (e != hipSuccess) return e;
     const int chunks = gram_chunks(n);
     launch_gram(L.Z, L.Q, n, p, pp, L.part, s);
-    hipLaunchKernelGGL(k_jacobi, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
+    if (p <= 64) hipLaunchKernelGGL(k_jacobi_lds, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
+    else hipLaunchKernelGGL(k_jacobi, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
     // the Ritz vectors [k][n] overwrite Q (k <= pp)
     hipLaunchKernelGGL(k_ritz, dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(k)), dim3(256), 0,
                        s, L.Z, n, p, pp, k, L.Wt, L.theta, L.Q, eigvals);
