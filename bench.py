@@ -25,7 +25,10 @@ rows from pinned host memory through two device buffers (the store of the
 paper outgrows GPU memory) and compares the rate with a plain copy over the
 same link.  Its "relatif" entry times l-RelatIF on the same store: the
 self-influence of every training row (once per store) and the score pass with
-the 1/sqrt(self) scales applied before the top-100.
+the 1/sqrt(self) scales applied before the top-100.  Its "vendor_gemm" entry
+times torch.matmul (hipBLASLt) and this library's scores-only path on the same
+125,000-row slice of the operands: a measured reference beside the published
+peak.
 
 All inputs are synthetic, drawn on the device before timing.  Each leg
 reports the roofline of its dominant kernel from HIP events recorded on the
@@ -675,8 +678,8 @@ def main():
     ap.add_argument("--ooc-rows", type=int, default=131072,
                     help="rows of the out-of-core sub-leg's pinned host store (0 = skip)")
     ap.add_argument("--ooc-chunk", type=int, default=32768, help="rows per streamed chunk")
-    ap.add_argument("--vendor-gemm", action="store_true",
-                    help="also time torch.matmul (hipBLASLt) on the score GEMM's operands")
+    ap.add_argument("--no-vendor-gemm", dest="vendor_gemm", action="store_false",
+                    help="skip timing torch.matmul (hipBLASLt) on a slice of the score GEMM's operands")
     ap.add_argument("--cpu-batches", type=int, default=2, help="logging batches in the oracle sample")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time bound of the logging sample")
     ap.add_argument("--cpu-queries", type=int, default=256, help="test gradients in the oracle sample")
