@@ -243,29 +243,53 @@ __global__ __launch_bounds__(256) void k_trsm_f64(const double *A_all, const dou
     double *Z = Z_all + static_cast<size_t>(blk) * D * Qp;
     f64x4 acc[4];
 
+    // Tile staging: each thread's 16 elements are loaded into registers first
+    // (all loads in flight), then stored to LDS.
+    constexpr int kPer = NB * NB / 256;
     // La[rr][cc] = L[r0+rr][c0+cc] (strictly lower tiles only), or its transpose.
     auto stage_L = [&](int r0, int c0, bool transpose) {
-        for (int e = tid; e < NB * NB; e += 256) {
-            const int u = e / NB, v = e - (e / NB) * NB;   // consecutive threads: consecutive v
-            if (!transpose) {
-                La[u * LT + v] = (r0 + u < D && c0 + v < D) ? L[static_cast<size_t>(r0 + u) * D + c0 + v] : 0.0;
-            } else {   // La[v][u] = L[c0+u][r0+v]
-                La[v * LT + u] = (c0 + u < D && r0 + v < D) ? L[static_cast<size_t>(c0 + u) * D + r0 + v] : 0.0;
-            }
+        double v[kPer];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int e = tid + 256 * q;
+            const int u = e / NB, w2 = e - (e / NB) * NB;   // consecutive threads: consecutive w2
+            const int rr = transpose ? c0 + u : r0 + u, cc = transpose ? r0 + w2 : c0 + w2;
+            v[q] = (rr < D && cc < D) ? L[static_cast<size_t>(rr) * D + cc] : 0.0;
+        }
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int e = tid + 256 * q;
+            const int u = e / NB, w2 = e - (e / NB) * NB;
+            if (!transpose) La[u * LT + w2] = v[q];
+            else La[w2 * LT + u] = v[q];   // La[w2][u] = L[c0+u][r0+w2]
         }
     };
     auto stage_Linv = [&](int i, bool transpose) {
         const double *T = Li + static_cast<size_t>(i) * NB * NB;
-        for (int e = tid; e < NB * NB; e += 256) {
-            const int u = e / NB, v = e - (e / NB) * NB;
-            if (!transpose) La[u * LT + v] = T[e];
-            else La[v * LT + u] = T[e];
+        double v[kPer];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) v[q] = T[tid + 256 * q];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int e = tid + 256 * q;
+            const int u = e / NB, w2 = e - (e / NB) * NB;
+            if (!transpose) La[u * LT + w2] = v[q];
+            else La[w2 * LT + u] = v[q];
         }
     };
     auto stage_B = [&](const double *src, int j) {   // Yb[kk][qq] = src[j*64 + kk][q0 + qq]
-        for (int e = tid; e < NB * NB; e += 256) {
+        double v[kPer];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int e = tid + 256 * q;
             const int kk = e / NB, qq = e - (e / NB) * NB;
-            Yb[kk * LT + qq] = (j * NB + kk < D) ? src[static_cast<size_t>(j * NB + kk) * Qp + q0 + qq] : 0.0;
+            v[q] = (j * NB + kk < D) ? src[static_cast<size_t>(j * NB + kk) * Qp + q0 + qq] : 0.0;
+        }
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int e = tid + 256 * q;
+            const int kk = e / NB, qq = e - (e / NB) * NB;
+            Yb[kk * LT + qq] = v[q];
         }
     };
     auto mma = [&](double sign) {
