@@ -87,6 +87,22 @@ __global__ __launch_bounds__(256) void k_form(const float *S, int D, int64_t N, 
     if (i == 0 && threadIdx.x == 0) info[blk] = 0;
 }
 
+// sum over m in [m0, m1) of x[m sx] y[m sy] from LDS, in four interleaved
+// partial sums ((s0 + s1) + (s2 + s3)): eight loads in flight instead of one
+// LDS round trip per term.
+__device__ __forceinline__ double lds_dot(const double *x, int sx, const double *y, int sy, int m0, int m1) {
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    int m = m0;
+    for (; m + 4 <= m1; m += 4) {
+        s0 = fma(x[m * sx], y[m * sy], s0);
+        s1 = fma(x[(m + 1) * sx], y[(m + 1) * sy], s1);
+        s2 = fma(x[(m + 2) * sx], y[(m + 2) * sy], s2);
+        s3 = fma(x[(m + 3) * sx], y[(m + 3) * sy], s3);
+    }
+    for (; m < m1; ++m) s0 = fma(x[m * sx], y[m * sy], s0);
+    return (s0 + s1) + (s2 + s3);
+}
+
 // Unblocked Cholesky of the nb x nb diagonal block at (k0, k0); one wave.
 __global__ __launch_bounds__(64) void k_potrf_diag(double *A_all, int D, int k0, int *info) {
     __shared__ double a[NB * LT];
@@ -108,9 +124,20 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double *A_all, int D, int k0,
         __syncthreads();
         if (t > j && t < nb) a[t * LT + j] /= a[j * LT + j];
         __syncthreads();
-        if (t > j && t < nb) {
+        if (t > j && t < nb) {   // row t: independent updates, four at a time (loads before stores)
             const double lij = a[t * LT + j];
-            for (int k = j + 1; k <= t; ++k) a[t * LT + k] -= lij * a[k * LT + j];
+            int k = j + 1;
+            for (; k + 4 <= t + 1; k += 4) {
+                double u[4], w[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    u[q] = a[t * LT + k + q];
+                    w[q] = a[(k + q) * LT + j];
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) a[t * LT + k + q] = u[q] - lij * w[q];
+            }
+            for (; k <= t; ++k) a[t * LT + k] -= lij * a[k * LT + j];
         }
         __syncthreads();
     }
@@ -132,11 +159,7 @@ __global__ __launch_bounds__(64) void k_trsm_panel(double *A_all, int D, int k0)
     __syncthreads();
     if (t < nr) {
         double *xr = x + t * LT;
-        for (int j = 0; j < nb; ++j) {
-            double s = xr[j];
-            for (int m = 0; m < j; ++m) s -= xr[m] * l11[j * LT + m];
-            xr[j] = s / l11[j * LT + j];
-        }
+        for (int j = 0; j < nb; ++j) xr[j] = (xr[j] - lds_dot(xr, 1, l11 + j * LT, 1, 0, j)) / l11[j * LT + j];
     }
     __syncthreads();
     for (int i = 0; i < nr; ++i)
@@ -210,9 +233,7 @@ __global__ __launch_bounds__(64) void k_diag_inv(const double *A_all, int D, dou
             if (r == c) {
                 v = 1.0 / a[r * LT + r];
             } else {
-                double s = 0.0;
-                for (int m = c; m < r; ++m) s = fma(a[r * LT + m], wl[m * LT + c], s);
-                v = -s / a[r * LT + r];
+                v = -lds_dot(a + r * LT, 1, wl + c, LT, c, r) / a[r * LT + r];
             }
         }
         wl[r * LT + c] = v;   // only this thread reads column c
