@@ -281,8 +281,10 @@ int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, 
  * logra_offload_rows: copies `rows` rows of `row_bytes` bytes from device
  * memory src (row stride ld_src bytes) to PINNED HOST memory dst
  * (hipHostMalloc; row stride ld_dst bytes), after the work already enqueued
- * on `stream` (an event recorded there is waited for on copy_stream), so the
- * copy runs on copy_stream while the next batch is projected on `stream`.
+ * on `stream` (an event recorded there is waited for on copy_stream; the
+ * library keeps one such event per calling thread and device for the life of
+ * the process), so the copy runs on copy_stream while the next batch is
+ * projected on `stream`.
  * copy_stream NULL: the copy is enqueued on `stream` itself (in order, no
  * overlap on the device, still asynchronous for the host).  The copy is a
  * blit kernel: for a batch's rows on MI355X the in-order form is the cheaper
