@@ -65,6 +65,24 @@ __host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGR
 
 constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
 
+#ifndef LOGRA_PROJ_DMA
+#define LOGRA_PROJ_DMA 1   // bf16, one projection per pass, k <= 32: operands staged by LDS-DMA
+#endif
+constexpr int kDmaStages = 3;    // stages of each wave's LDS ring
+constexpr int kDmaCols = 64;     // columns per step: 128 bytes of a bf16 row
+template <int KT>
+struct DmaShape {
+    static constexpr int kX = TT / 8;                // copies of the x slab (8 token rows of 128 B each)
+    static constexpr int kP = 2 * KT;                // copies of the P slab (8 rows each)
+    static constexpr int kCopies = kX + kP;
+    static constexpr int kStage = kCopies * 1024;    // bytes of one stage
+    static constexpr int kRing = NW * kDmaStages * kStage;   // bytes per workgroup
+};
+template <int KT, int S, typename TIn>
+__host__ __device__ constexpr bool use_dma() {
+    return LOGRA_PROJ_DMA && S == 1 && KT <= 2 && sizeof(TIn) == 2;
+}
+
 struct ChunkLayer {
     const void *x;
     const void *dy;
@@ -132,7 +150,8 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[MB][KT], const u32x4 (&xa)
 // One wave's share of  A'_s[TT x 16KT] = A[TT x nk] * P_s[k x nk]^T for the
 // S projections P_s (s < S) of one operand A (a shared input: one pass over
 // A; a missing P_s reads zeros), A and P_s with row strides lda and ldp.
-// Contraction steps s = wave, wave + NW, ... .  Every load is unconditional
+// Contraction steps are dealt to the waves round-robin (bf16: in adjacent
+// pairs, see step_of).  Every load is unconditional
 // (out-of-range offsets read zeros), and the ST-stage register pipeline
 // keeps ST-1 steps in flight while a step multiplies.  Each wave's step
 // count is rounded up to a multiple of ST with empty steps (no memory access,
@@ -152,8 +171,14 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
 #pragma unroll
         for (int j = 0; j < S * KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int nsteps = (nk + SS - 1) / SS;
-    int s = wave;
-    if (s >= nsteps) return;
+    // the wave's j-th step: for bf16, 32-column steps in adjacent pairs dealt
+    // round-robin (the 64-column steps of project_part_dma, so that both paths
+    // add the same products in the same order); for fp32, single steps
+    constexpr bool kPairs = sizeof(TIn) == 2;
+    auto step_of = [&](int j) { return kPairs ? 2 * (wave + NW * (j >> 1)) + (j & 1) : wave + NW * j; };
+    const int units = kPairs ? (nsteps + 1) / 2 : nsteps;
+    const int count = units > wave ? (units - wave + NW - 1) / NW * (kPairs ? 2 : 1) : 0;
+    if (count == 0) return;
 
     const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * ES);
     __amdgpu_buffer_rsrc_t rp[S];
@@ -181,25 +206,108 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
             for (int j = 0; j < KT; ++j) pb[q * KT + j] = buf_ld128(rp[q], in_k ? poff[j] + koff : kBufOOB);
     };
 
-    const int iters = ((nsteps - wave + NW - 1) / NW + ST - 1) / ST;
+    const int iters = (count + ST - 1) / ST;
     u32x4 xa[ST][MB], pb[ST][S * KT];
 #pragma unroll
-    for (int i = 0; i < ST - 1; ++i) load(s + i * NW, xa[i], pb[i]);
+    for (int i = 0; i < ST - 1; ++i) load(step_of(i), xa[i], pb[i]);
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
         for (int i = 0; i < ST; ++i) {
-            load(s + (i + ST - 1) * NW, xa[(i + ST - 1) % ST], pb[(i + ST - 1) % ST]);
+            load(step_of(it * ST + i + ST - 1), xa[(i + ST - 1) % ST], pb[(i + ST - 1) % ST]);
             mma_step<S * KT>(acc, xa[i], pb[i], TIn{});
         }
-        s += ST * NW;
     }
+}
+
+// project_part for bf16 operands and one projection (k <= 32), staged through
+// the wave's own LDS ring instead of registers.  A step is 64 columns: the x
+// slab (64 tokens x 128 bytes) and the P slab (16 KT rows x 128 bytes), each
+// copy instruction moving 8 whole rows (full 128-byte lines) from memory
+// straight into LDS (gfx950 buffer_load ... lds).  Row r of a slab sits at
+// byte 128 r with its 16-byte chunk c at position c ^ (r & 7); the copies
+// give lane l rows 8 q + l / 8 (so r & 7 = l / 8) and position l & 7, which
+// makes the lane's source chunk (l & 7) ^ (l / 8) the same in every copy.  A
+// fragment read (ds_read_b128) hands lane (row, kg) the 8 elements of chunk
+// 4 h + kg of its row for half-step h.  The ring keeps kDmaStages - 1 steps
+// in flight; the wave waits only on its own copies (s_waitcnt vmcnt) and
+// shares nothing with the other waves, so no barrier is needed.  Masked
+// tokens, rows of P beyond k and columns past the chunk read zeros (an
+// out-of-range offset); steps past the wave's last are all out of range and
+// keep the copy count of every iteration the same.
+template <int KT>
+__device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][KT], const bf16_bits *A, int lda,
+                                                 const bf16_bits *P, int ldp, int nk, int k, int own_ok,
+                                                 int wave, int lane, const uint8_t *ring, uint32_t ring_addr) {
+    using Sh = DmaShape<KT>;
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int j = 0; j < KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nsteps = (nk + kDmaCols - 1) / kDmaCols;
+    const int mine = nsteps > wave ? (nsteps - wave + NW - 1) / NW : 0;
+    if (mine == 0) return;
+    const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * 2u);
+    const auto rp = buf_rsrc(P, (static_cast<uint32_t>(k - 1) * ldp + nk) * 2u);
+    const int sub = lane >> 3;
+    const int lcol = ((lane & 7) ^ sub) * 8;         // the lane's element column within a step
+    uint32_t xo[Sh::kX], po[Sh::kP];
+#pragma unroll
+    for (int q = 0; q < Sh::kX; ++q) {
+        const int t = 8 * q + sub;
+        xo[q] = __shfl(own_ok, t, kWave) ? (static_cast<uint32_t>(t) * lda + lcol) * 2u : kBufOOB;
+    }
+#pragma unroll
+    for (int q = 0; q < Sh::kP; ++q) {
+        const int r = 8 * q + sub;
+        po[q] = r < k ? (static_cast<uint32_t>(r) * ldp + lcol) * 2u : kBufOOB;
+    }
+    auto issue = [&](int i, int stage) {
+        const int st = wave + NW * i;
+        const bool in = st * kDmaCols + lcol < nk;
+        const uint32_t dk = static_cast<uint32_t>(st * kDmaCols) * 2u;
+        const uint32_t lds = ring_addr + static_cast<uint32_t>(stage * Sh::kStage);
+#pragma unroll
+        for (int q = 0; q < Sh::kX; ++q) copy_to_lds(ra, in ? xo[q] + dk : kBufOOB, lds + q * 1024);
+#pragma unroll
+        for (int q = 0; q < Sh::kP; ++q) copy_to_lds(rp, in ? po[q] + dk : kBufOOB, lds + (Sh::kX + q) * 1024);
+    };
+#pragma unroll
+    for (int i = 0; i < kDmaStages - 1; ++i) issue(i, i);
+    const int row = lane & 15, kg = lane >> 4;
+    for (int i = 0; i < mine; ++i) {
+        issue(i + kDmaStages - 1, (i + kDmaStages - 1) % kDmaStages);
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((kDmaStages - 1) * Sh::kCopies) : "memory");
+        const uint8_t *base = ring + (i % kDmaStages) * Sh::kStage;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int c = 4 * h + kg;
+            bf16x8 xf[MB], pf[KT];
+#pragma unroll
+            for (int m = 0; m < MB; ++m) {
+                const int t = 16 * m + row;
+                xf[m] = as_bf16x8(*reinterpret_cast<const u32x4 *>(base + t * 128 + ((c ^ (t & 7)) << 4)));
+            }
+#pragma unroll
+            for (int j = 0; j < KT; ++j) {
+                const int r = 16 * j + row;
+                pf[j] = as_bf16x8(
+                    *reinterpret_cast<const u32x4 *>(base + Sh::kX * 1024 + r * 128 + ((c ^ (r & 7)) << 4)));
+            }
+#pragma unroll
+            for (int m = 0; m < MB; ++m)
+#pragma unroll
+                for (int j = 0; j < KT; ++j) acc[m][j] = mfma16_bf16(xf[m], pf[j], acc[m][j]);
+        }
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the ring is idle when the item ends
 }
 
 // Validity of the MB token rows a lane feeds (tokens t0 + 16m + lane%16):
 // each lane loads the flags of tokens t0 + lane and t0 + 64 + lane (one
 // coalesced load each), and the rows are gathered by lane shuffles.
 // Returns whether any of the lane's rows is valid.
-__device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, int lane, bool (&tok_ok)[MB]) {
+__device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, int lane, bool (&tok_ok)[MB],
+                                            int *own = nullptr) {
     int v[(TT + kWave - 1) / kWave];
 #pragma unroll
     for (int h = 0; h < (TT + kWave - 1) / kWave; ++h) {
@@ -215,6 +323,7 @@ __device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, in
         tok_ok[m] = __shfl(v[r / kWave], r % kWave, kWave) != 0;
         any |= tok_ok[m];
     }
+    if (own) *own = v[0];   // token t0 + lane
     return any;
 }
 
@@ -224,7 +333,7 @@ __device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, in
 // every layer sharing it (S >= share_n).
 template <int KT, int S, typename TIn>
 __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int count, f32x4 *slot, int lane,
-                                           int wave) {
+                                           int wave, const uint8_t *ring, uint32_t ring_addr) {
     const int rank = item / count;              // position of the work slot in processing order
     const int j = item - rank * count;          // listed tile
     const int gslot = a.ordered ? a.slot_order[rank] : rank;   // work slot over all layers
@@ -236,7 +345,8 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     const int b = bt / a.tpe, tile = bt - b * a.tpe;
 
     bool tok_ok[MB];
-    lane_tokens(a, b, tile * TT, lane, tok_ok);  // listed tiles have at least one valid token
+    int own = 0;
+    lane_tokens(a, b, tile * TT, lane, tok_ok, &own);  // listed tiles have at least one valid token
     __syncthreads();   // the previous item's reads of `slot` are done
 
     const bool xside = cs < L.x_items;
@@ -256,7 +366,11 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     }
 
     f32x4 acc[MB][S * KT];
-    project_part<KT, S, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
+    if constexpr (use_dma<KT, S, TIn>())
+        project_part_dma<KT>(acc, reinterpret_cast<const bf16_bits *>(A), n, reinterpret_cast<const bf16_bits *>(P[0]),
+                             n, nk, k, own, wave, lane, ring, ring_addr);
+    else
+        project_part<KT, S, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
 
     // fold the waves in the order ((w3 + w2) + w1) + w0, then write each
     // result in the MFMA layout: element (m, j) of lane l at [(m*KT + j)*64 + l]
@@ -306,14 +420,17 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 template <int KT, int S, typename TIn>
 __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(ProjArgs a) {
     __shared__ f32x4 slot[MB * S * KT * kWave];   // cross-wave fold
+    __shared__ __attribute__((aligned(16))) uint8_t ring[use_dma<KT, S, TIn>() ? DmaShape<KT>::kRing : 16];
     __shared__ int next;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    constexpr int kWaveRing = use_dma<KT, S, TIn>() ? kDmaStages * DmaShape<KT>::kStage : 0;
+    const uint8_t *my_ring = ring + wave * kWaveRing;   // this wave's stages
     const int count = a.tiles ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : a.B * a.tpe;
     const int items = count * a.slots;
     int item = blockIdx.x;
     while (item < items) {
-        chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave);
+        chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave, my_ring, lds_addr(my_ring));
         if (tid == 0) next = static_cast<int>(gridDim.x) + atomicAdd(a.work, 1);
         __syncthreads();
         item = next;
