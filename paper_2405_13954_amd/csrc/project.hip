@@ -68,19 +68,23 @@ constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
 #ifndef LOGRA_PROJ_DMA
 #define LOGRA_PROJ_DMA 1   // bf16, one projection per pass, k <= 32: operands staged by LDS-DMA
 #endif
-constexpr int kDmaStages = 3;    // stages of each wave's LDS ring
 constexpr int kDmaCols = 64;     // columns per step: 128 bytes of a bf16 row
-template <int KT>
+constexpr int kLdsBytes = 160 * 1024;
+template <int KT, int S>
 struct DmaShape {
     static constexpr int kX = TT / 8;                // copies of the x slab (8 token rows of 128 B each)
-    static constexpr int kP = 2 * KT;                // copies of the P slab (8 rows each)
-    static constexpr int kCopies = kX + kP;
+    static constexpr int kPm = 2 * KT;               // copies of one P slab (8 rows each)
+    static constexpr int kCopies = kX + S * kPm;
     static constexpr int kStage = kCopies * 1024;    // bytes of one stage
-    static constexpr int kRing = NW * kDmaStages * kStage;   // bytes per workgroup
+    static constexpr int kFold = MB * S * KT * kWave * 16;   // the cross-wave fold's LDS
+    // ring stages per wave: three when the workgroup's LDS allows, else two
+    static constexpr int kStages = NW * 3 * kStage + kFold <= kLdsBytes ? 3 : 2;
+    static constexpr int kRing = NW * kStages * kStage;      // bytes per workgroup
+    static constexpr bool kFits = kRing + kFold <= kLdsBytes;
 };
 template <int KT, int S, typename TIn>
 __host__ __device__ constexpr bool use_dma() {
-    return LOGRA_PROJ_DMA && S == 1 && KT <= 2 && sizeof(TIn) == 2;
+    return LOGRA_PROJ_DMA && KT <= 2 && sizeof(TIn) == 2 && DmaShape<KT, S>::kFits;
 }
 
 struct ChunkLayer {
@@ -219,45 +223,50 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
     }
 }
 
-// project_part for bf16 operands and one projection (k <= 32), staged through
-// the wave's own LDS ring instead of registers.  A step is 64 columns: the x
-// slab (64 tokens x 128 bytes) and the P slab (16 KT rows x 128 bytes), each
+// project_part for bf16 operands and k <= 32, staged through the wave's own
+// LDS ring instead of registers.  A step is 64 columns: the x slab (64 tokens
+// x 128 bytes) and one P slab (16 KT rows x 128 bytes) per projection, each
 // copy instruction moving 8 whole rows (full 128-byte lines) from memory
 // straight into LDS (gfx950 buffer_load ... lds).  Row r of a slab sits at
 // byte 128 r with its 16-byte chunk c at position c ^ (r & 7); the copies
 // give lane l rows 8 q + l / 8 (so r & 7 = l / 8) and position l & 7, which
 // makes the lane's source chunk (l & 7) ^ (l / 8) the same in every copy.  A
 // fragment read (ds_read_b128) hands lane (row, kg) the 8 elements of chunk
-// 4 h + kg of its row for half-step h.  The ring keeps kDmaStages - 1 steps
-// in flight; the wave waits only on its own copies (s_waitcnt vmcnt) and
+// 4 h + kg of its row for half-step h.  The ring keeps all but one of its
+// stages in flight (three stages where the LDS allows, else two); the wave waits only on its own copies (s_waitcnt vmcnt) and
 // shares nothing with the other waves, so no barrier is needed.  Masked
 // tokens, rows of P beyond k and columns past the chunk read zeros (an
 // out-of-range offset); steps past the wave's last are all out of range and
 // keep the copy count of every iteration the same.
-template <int KT>
-__device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][KT], const bf16_bits *A, int lda,
-                                                 const bf16_bits *P, int ldp, int nk, int k, int own_ok,
-                                                 int wave, int lane, const uint8_t *ring, uint32_t ring_addr) {
-    using Sh = DmaShape<KT>;
+template <int KT, int S>
+__device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const bf16_bits *A, int lda,
+                                                 const bf16_bits *const (&P)[S], int ldp, int nk, int k,
+                                                 int own_ok, int wave, int lane, const uint8_t *ring,
+                                                 uint32_t ring_addr) {
+    using Sh = DmaShape<KT, S>;
+    constexpr int NS = Sh::kStages;
 #pragma unroll
     for (int m = 0; m < MB; ++m)
 #pragma unroll
-        for (int j = 0; j < KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < S * KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int nsteps = (nk + kDmaCols - 1) / kDmaCols;
     const int mine = nsteps > wave ? (nsteps - wave + NW - 1) / NW : 0;
     if (mine == 0) return;
     const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * 2u);
-    const auto rp = buf_rsrc(P, (static_cast<uint32_t>(k - 1) * ldp + nk) * 2u);
+    __amdgpu_buffer_rsrc_t rp[S];
+#pragma unroll
+    for (int q = 0; q < S; ++q)   // a missing projection reads zeros
+        rp[q] = buf_rsrc(P[q] ? P[q] : A, P[q] ? (static_cast<uint32_t>(k - 1) * ldp + nk) * 2u : 0u);
     const int sub = lane >> 3;
     const int lcol = ((lane & 7) ^ sub) * 8;         // the lane's element column within a step
-    uint32_t xo[Sh::kX], po[Sh::kP];
+    uint32_t xo[Sh::kX], po[Sh::kPm];
 #pragma unroll
     for (int q = 0; q < Sh::kX; ++q) {
         const int t = 8 * q + sub;
         xo[q] = __shfl(own_ok, t, kWave) ? (static_cast<uint32_t>(t) * lda + lcol) * 2u : kBufOOB;
     }
 #pragma unroll
-    for (int q = 0; q < Sh::kP; ++q) {
+    for (int q = 0; q < Sh::kPm; ++q) {
         const int r = 8 * q + sub;
         po[q] = r < k ? (static_cast<uint32_t>(r) * ldp + lcol) * 2u : kBufOOB;
     }
@@ -269,34 +278,39 @@ __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][KT], const bf1
 #pragma unroll
         for (int q = 0; q < Sh::kX; ++q) copy_to_lds(ra, in ? xo[q] + dk : kBufOOB, lds + q * 1024);
 #pragma unroll
-        for (int q = 0; q < Sh::kP; ++q) copy_to_lds(rp, in ? po[q] + dk : kBufOOB, lds + (Sh::kX + q) * 1024);
+        for (int m2 = 0; m2 < S; ++m2)
+#pragma unroll
+            for (int q = 0; q < Sh::kPm; ++q)
+                copy_to_lds(rp[m2], in ? po[q] + dk : kBufOOB, lds + (Sh::kX + m2 * Sh::kPm + q) * 1024);
     };
 #pragma unroll
-    for (int i = 0; i < kDmaStages - 1; ++i) issue(i, i);
+    for (int i = 0; i < NS - 1; ++i) issue(i, i);
     const int row = lane & 15, kg = lane >> 4;
     for (int i = 0; i < mine; ++i) {
-        issue(i + kDmaStages - 1, (i + kDmaStages - 1) % kDmaStages);
-        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((kDmaStages - 1) * Sh::kCopies) : "memory");
-        const uint8_t *base = ring + (i % kDmaStages) * Sh::kStage;
+        issue(i + NS - 1, (i + NS - 1) % NS);
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((NS - 1) * Sh::kCopies) : "memory");
+        const uint8_t *base = ring + (i % NS) * Sh::kStage;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int c = 4 * h + kg;
-            bf16x8 xf[MB], pf[KT];
+            bf16x8 xf[MB], pf[S * KT];
 #pragma unroll
             for (int m = 0; m < MB; ++m) {
                 const int t = 16 * m + row;
                 xf[m] = as_bf16x8(*reinterpret_cast<const u32x4 *>(base + t * 128 + ((c ^ (t & 7)) << 4)));
             }
 #pragma unroll
-            for (int j = 0; j < KT; ++j) {
-                const int r = 16 * j + row;
-                pf[j] = as_bf16x8(
-                    *reinterpret_cast<const u32x4 *>(base + Sh::kX * 1024 + r * 128 + ((c ^ (r & 7)) << 4)));
-            }
+            for (int m2 = 0; m2 < S; ++m2)
+#pragma unroll
+                for (int j = 0; j < KT; ++j) {
+                    const int r = 16 * j + row;
+                    pf[m2 * KT + j] = as_bf16x8(*reinterpret_cast<const u32x4 *>(
+                        base + (Sh::kX + m2 * Sh::kPm) * 1024 + r * 128 + ((c ^ (r & 7)) << 4)));
+                }
 #pragma unroll
             for (int m = 0; m < MB; ++m)
 #pragma unroll
-                for (int j = 0; j < KT; ++j) acc[m][j] = mfma16_bf16(xf[m], pf[j], acc[m][j]);
+                for (int j = 0; j < S * KT; ++j) acc[m][j] = mfma16_bf16(xf[m], pf[j], acc[m][j]);
         }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the ring is idle when the item ends
@@ -366,9 +380,13 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     }
 
     f32x4 acc[MB][S * KT];
-    if constexpr (use_dma<KT, S, TIn>())
-        project_part_dma<KT>(acc, reinterpret_cast<const bf16_bits *>(A), n, reinterpret_cast<const bf16_bits *>(P[0]),
-                             n, nk, k, own, wave, lane, ring, ring_addr);
+    if constexpr (use_dma<KT, S, TIn>()) {
+        const bf16_bits *Pb[S];
+#pragma unroll
+        for (int q = 0; q < S; ++q) Pb[q] = reinterpret_cast<const bf16_bits *>(P[q]);
+        project_part_dma<KT, S>(acc, reinterpret_cast<const bf16_bits *>(A), n, Pb, n, nk, k, own, wave, lane, ring,
+                                ring_addr);
+    }
     else
         project_part<KT, S, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
 
@@ -420,11 +438,11 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 template <int KT, int S, typename TIn>
 __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(ProjArgs a) {
     __shared__ f32x4 slot[MB * S * KT * kWave];   // cross-wave fold
-    __shared__ __attribute__((aligned(16))) uint8_t ring[use_dma<KT, S, TIn>() ? DmaShape<KT>::kRing : 16];
+    __shared__ __attribute__((aligned(16))) uint8_t ring[use_dma<KT, S, TIn>() ? DmaShape<KT, S>::kRing : 16];
     __shared__ int next;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    constexpr int kWaveRing = use_dma<KT, S, TIn>() ? kDmaStages * DmaShape<KT>::kStage : 0;
+    constexpr int kWaveRing = use_dma<KT, S, TIn>() ? DmaShape<KT, S>::kStages * DmaShape<KT, S>::kStage : 0;
     const uint8_t *my_ring = ring + wave * kWaveRing;   // this wave's stages
     const int count = a.tiles ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : a.B * a.tpe;
     const int items = count * a.slots;
