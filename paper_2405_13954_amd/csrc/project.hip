@@ -66,7 +66,7 @@ __host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGR
 constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
 
 #ifndef LOGRA_PROJ_DMA
-#define LOGRA_PROJ_DMA 1   // bf16, one projection per pass, k <= 32: operands staged by LDS-DMA
+#define LOGRA_PROJ_DMA 1   // bf16 operands staged by LDS-DMA wherever the rings fit in LDS
 #endif
 constexpr int kDmaCols = 64;     // columns per step: 128 bytes of a bf16 row
 constexpr int kLdsBytes = 160 * 1024;
@@ -84,7 +84,7 @@ struct DmaShape {
 };
 template <int KT, int S, typename TIn>
 __host__ __device__ constexpr bool use_dma() {
-    return LOGRA_PROJ_DMA && KT <= 2 && sizeof(TIn) == 2 && DmaShape<KT, S>::kFits;
+    return LOGRA_PROJ_DMA && sizeof(TIn) == 2 && DmaShape<KT, S>::kFits;
 }
 
 struct ChunkLayer {
@@ -223,7 +223,7 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
     }
 }
 
-// project_part for bf16 operands and k <= 32, staged through the wave's own
+// project_part for bf16 operands, staged through the wave's own
 // LDS ring instead of registers.  A step is 64 columns: the x slab (64 tokens
 // x 128 bytes) and one P slab (16 KT rows x 128 bytes) per projection, each
 // copy instruction moving 8 whole rows (full 128-byte lines) from memory
