@@ -22,13 +22,26 @@ FLAGS = [
 ]
 
 
+# Per-source additions.  project.hip: its one atomic is a single lane's claim
+# of the next work item, whose result is needed only when the current item
+# ends; the atomic optimizer would rewrite it into a wave-level form that
+# waits for the result at once.
+FILE_FLAGS = {
+    "project.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
+}
+
+
+def flags_for(src: str) -> list:
+    return [*FLAGS, *FILE_FLAGS.get(os.path.basename(src), [])]
+
+
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ_DIR, os.path.basename(src) + ".o")
-    cmd = ["hipcc", *FLAGS, "-c", src, "-o", obj]
+    cmd = ["hipcc", *flags_for(src), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")

@@ -8,7 +8,8 @@
 // tiles of a ragged batch are empty):
 //
 //  0. k_project_prep: clears the work counter and, for masked inputs, builds
-//     the ordered list of 64-token tiles holding at least one valid token.
+//     the ordered list of 64-token tiles holding at least one valid token,
+//     each with the 64-bit set of its valid tokens.
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
 //     = one contraction chunk (<= 4096 columns) of one side (x or dy) of one
 //     listed tile.  Layers given the same x tensor (q/k/v, gate/up of a
@@ -23,7 +24,9 @@
 //     of P beyond k and lanes past the chunk end get an out-of-range offset:
 //     they read zeros without a memory access or a branch, so NaN/Inf in
 //     padding cannot leak.  The waves' partial x'/dy' are folded in a fixed
-//     order and written, in the MFMA result layout, to the workspace.
+//     order and written, in the MFMA result layout, to the workspace.  A
+//     workgroup claims its next item when it starts one, so the claim's
+//     round trip is hidden behind the stream.
 //  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
 //     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
 //     formed in fp32 from LDS (KT x KT outputs per thread).  Empty tiles give 0.
@@ -54,8 +57,10 @@ namespace {
 #endif
 constexpr int MB = LOGRA_PROJ_ROWBLOCKS;  // 16-token row blocks per tile
 constexpr int TT = 16 * MB;               // tokens per tile
+static_assert(TT == 64, "a tile's valid-token set is one 64-bit word");
 constexpr int NW = 4;                     // waves per workgroup
 constexpr int kMaxSlots = 1024;           // chunk slots a group can order by width
+static_assert(kMaxSlots <= 4096 && kMaxGroup <= 16, "an ordered slot packs its layer into 4 bits");
 constexpr int NT = NW * kWave;            // threads per workgroup
 
 // Contraction columns per work item, and register pipeline depth, by
@@ -76,11 +81,13 @@ struct DmaShape {
     static constexpr int kPm = 2 * KT;               // copies of one P slab (8 rows each)
     static constexpr int kCopies = kX + S * kPm;
     static constexpr int kStage = kCopies * 1024;    // bytes of one stage
-    static constexpr int kFold = MB * S * KT * kWave * 16;   // the cross-wave fold's LDS
+    static constexpr int kFold = MB * S * KT * kWave * 16;   // one wave's results (f32x4 per lane)
     // ring stages per wave: three when the workgroup's LDS allows, else two
-    static constexpr int kStages = NW * 3 * kStage + kFold <= kLdsBytes ? 3 : 2;
-    static constexpr int kRing = NW * kStages * kStage;      // bytes per workgroup
-    static constexpr bool kFits = kRing + kFold <= kLdsBytes;
+    static constexpr int kStages = NW * 3 * kStage <= kLdsBytes ? 3 : 2;
+    static constexpr int kWaveRing = kStages * kStage;       // bytes per wave
+    static constexpr int kRing = NW * kWaveRing;             // bytes per workgroup
+    // a wave's fold fits its ring, and 1 KB is left for the workgroup's other LDS
+    static constexpr bool kFits = kRing + 1024 <= kLdsBytes && kFold <= kWaveRing;
 };
 template <int KT, int S, typename TIn>
 __host__ __device__ constexpr bool use_dma() {
@@ -106,9 +113,11 @@ struct ProjArgs {
     int n_layers;
     int slots;      // chunk slots of all layers
     int ordered;    // slot_order holds the processing order of the slots
-    uint16_t slot_order[kMaxSlots];
+    // processing order: entry = layer << 12 | work slot (over all layers)
+    alignas(4) uint16_t slot_order[kMaxSlots];
     const uint8_t *mask;
     const int *tiles;     // non-empty tiles (b * tpe + tile) in index order; NULL = all
+    const uint64_t *bits; // their valid tokens (bit i = token 64 tile + i), beside tiles
     const int *n_tiles;   // their count (device), read when tiles != NULL
     int *work;            // items handed out beyond the first gridDim.x (device counter)
     float *part;    // chunk partials, MFMA result layout, TT x 16KT floats each
@@ -241,7 +250,7 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
 template <int KT, int S>
 __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const bf16_bits *A, int lda,
                                                  const bf16_bits *const (&P)[S], int ldp, int nk, int k,
-                                                 int own_ok, int wave, int lane, const uint8_t *ring,
+                                                 uint64_t valid, int wave, int lane, const uint8_t *ring,
                                                  uint32_t ring_addr) {
     using Sh = DmaShape<KT, S>;
     constexpr int NS = Sh::kStages;
@@ -263,7 +272,7 @@ __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const
 #pragma unroll
     for (int q = 0; q < Sh::kX; ++q) {
         const int t = 8 * q + sub;
-        xo[q] = __shfl(own_ok, t, kWave) ? (static_cast<uint32_t>(t) * lda + lcol) * 2u : kBufOOB;
+        xo[q] = (valid >> t) & 1 ? (static_cast<uint32_t>(t) * lda + lcol) * 2u : kBufOOB;
     }
 #pragma unroll
     for (int q = 0; q < Sh::kPm; ++q) {
@@ -316,6 +325,22 @@ __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the ring is idle when the item ends
 }
 
+// A load at a uniform address of data that an earlier launch wrote and this
+// kernel only reads: through the scalar cache.
+template <typename T>
+__device__ __forceinline__ T load_uniform(const T *p) {
+    return *(const __attribute__((address_space(4))) T *)p;
+}
+
+// Valid tokens of tile `tile` of example b as a 64-bit set (bit i = token
+// 64 tile + i): the listed set when the tiles were listed, else the tokens
+// before T.
+__device__ __forceinline__ uint64_t tile_valid(const ProjArgs &a, int j, int tile) {
+    if (a.tiles) return load_uniform(a.bits + j);
+    const int n = a.T - tile * TT;
+    return n >= 64 ? ~0ull : (1ull << n) - 1;
+}
+
 // Validity of the MB token rows a lane feeds (tokens t0 + 16m + lane%16):
 // each lane loads the flags of tokens t0 + lane and t0 + 64 + lane (one
 // coalesced load each), and the rows are gathered by lane shuffles.
@@ -341,27 +366,34 @@ __device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, in
     return any;
 }
 
-// One chunk item (see the file comment).  Returns without a barrier when the
-// tile is fully masked; every thread of the workgroup takes the same path.
-// An x-side item of a layer whose x is shared produces the x' partials of
-// every layer sharing it (S >= share_n).
+// One chunk item (see the file comment).  Every listed tile (and, without a
+// mask, every tile) has at least one valid token.  An x-side item of a layer
+// whose x is shared produces the x' partials of every layer sharing it
+// (S >= share_n).  The item's indices are uniform across the workgroup.
+// With `ahead`, `claim` is thread 0's pending claim of the next item; after
+// the last fold barrier, before any store, every wave reads it (so that the
+// wait for it never waits for stores), and thread 0 publishes it in `next`.
 template <int KT, int S, typename TIn>
 __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int count, f32x4 *slot, int lane,
-                                           int wave, const uint8_t *ring, uint32_t ring_addr) {
+                                           int wave, uint8_t *ring, uint32_t ring_addr, bool ahead, int claim,
+                                           int *next) {
     const int rank = item / count;              // position of the work slot in processing order
     const int j = item - rank * count;          // listed tile
-    const int gslot = a.ordered ? a.slot_order[rank] : rank;   // work slot over all layers
-    int l = 0;
-    while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
+    int gslot = rank, l = 0;                    // work slot over all layers, and its layer
+    if (a.ordered) {   // whole dwords of the argument block: scalar loads
+        const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
+        gslot = e & 0xfff;
+        l = (e >> 12) & 0xf;
+    } else {
+        while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
+    }
     const ChunkLayer &L = a.layer[l];
     const int cs = gslot - L.slot_begin;        // work slot of the layer: x items, then dy chunks
-    const int bt = a.tiles ? a.tiles[j] : j;
+    const int bt = a.tiles ? load_uniform(a.tiles + j) : j;
     const int b = bt / a.tpe, tile = bt - b * a.tpe;
-
-    bool tok_ok[MB];
-    int own = 0;
-    lane_tokens(a, b, tile * TT, lane, tok_ok, &own);  // listed tiles have at least one valid token
-    __syncthreads();   // the previous item's reads of `slot` are done
+    const uint64_t valid = tile_valid(a, j, tile);
+    constexpr bool kDma = use_dma<KT, S, TIn>();
+    if constexpr (!kDma) __syncthreads();   // the previous item's reads of `slot` are done
 
     const bool xside = cs < L.x_items;
     const int c = xside ? cs : cs - L.x_items;
@@ -378,90 +410,148 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
         const void *pm = q >= nmem ? nullptr : xside ? a.layer[L.share[q]].p_in : L.p_out;
         P[q] = pm ? static_cast<const TIn *>(pm) + col0 : nullptr;
     }
+    auto member_dst = [&](int q) {   // member q's partial slot; element (m, jj) at [(m KT + jj) 64 + lane]
+        const ChunkLayer &M = xside ? a.layer[L.share[q]] : L;
+        const int pslot = xside ? c : M.c_in + c;
+        return reinterpret_cast<f32x4 *>(a.part + M.part_begin +
+                                         (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) * (TT * 16 * KT)) +
+               lane;
+    };
+    auto publish = [&]() {   // the read is unconditional, so that no path leaves the claim pending
+        const int claimed = __builtin_amdgcn_readfirstlane(claim);
+        if (ahead && threadIdx.x == 0) *next = static_cast<int>(gridDim.x) + claimed;
+    };
 
     f32x4 acc[MB][S * KT];
-    if constexpr (use_dma<KT, S, TIn>()) {
+    if constexpr (kDma) {
         const bf16_bits *Pb[S];
 #pragma unroll
         for (int q = 0; q < S; ++q) Pb[q] = reinterpret_cast<const bf16_bits *>(P[q]);
-        project_part_dma<KT, S>(acc, reinterpret_cast<const bf16_bits *>(A), n, Pb, n, nk, k, own, wave, lane, ring,
-                                ring_addr);
-    }
-    else
-        project_part<KT, S, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
-
-    // fold the waves in the order ((w3 + w2) + w1) + w0, then write each
-    // result in the MFMA layout: element (m, j) of lane l at [(m*KT + j)*64 + l]
-    // of the partial slot of its layer
-    f32x4 *my = slot + lane;
-    if (wave == NW - 1) {
-#pragma unroll
-        for (int m = 0; m < MB; ++m)
-#pragma unroll
-            for (int j = 0; j < S * KT; ++j) my[(m * S * KT + j) * kWave] = acc[m][j];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int w = NW - 2; w >= 1; --w) {
-        if (wave == w) {
+        project_part_dma<KT, S>(acc, reinterpret_cast<const bf16_bits *>(A), n, Pb, n, nk, k, valid, wave, lane,
+                                ring, ring_addr);
+        // Waves 1..3 park their results in their own (now idle) ring; after
+        // one barrier wave 0 forms ((w3 + w2) + w1) + w0 and writes it.
+        constexpr int kWaveRing = DmaShape<KT, S>::kWaveRing;
+        if (wave > 0) {
+            f32x4 *park = reinterpret_cast<f32x4 *>(ring) + lane;
 #pragma unroll
             for (int m = 0; m < MB; ++m)
 #pragma unroll
-                for (int j = 0; j < S * KT; ++j)
-                    my[(m * S * KT + j) * kWave] = my[(m * S * KT + j) * kWave] + acc[m][j];
+                for (int jj = 0; jj < S * KT; ++jj) park[(m * S * KT + jj) * kWave] = acc[m][jj];
         }
         __syncthreads();
-    }
-    if (wave == 0) {
+        publish();
+        if (wave == 0) {
+            const f32x4 *w1 = reinterpret_cast<const f32x4 *>(ring + kWaveRing) + lane;
+            const f32x4 *w2 = reinterpret_cast<const f32x4 *>(ring + 2 * kWaveRing) + lane;
+            const f32x4 *w3 = reinterpret_cast<const f32x4 *>(ring + 3 * kWaveRing) + lane;
+            static_assert(NW == 4, "the fold names waves 1..3");
 #pragma unroll
-        for (int q = 0; q < S; ++q) {
-            if (q >= nmem) break;
-            const ChunkLayer &M = xside ? a.layer[L.share[q]] : L;
-            const int pslot = xside ? c : M.c_in + c;
-            f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + M.part_begin +
-                                                   (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) *
-                                                       (TT * 16 * KT));
+            for (int q = 0; q < S; ++q) {
+                if (q >= nmem) break;
+                f32x4 *dst = member_dst(q);
+#pragma unroll
+                for (int m = 0; m < MB; ++m)
+#pragma unroll
+                    for (int jj = 0; jj < KT; ++jj) {
+                        const int e = (m * S * KT + q * KT + jj) * kWave;
+                        dst[(m * KT + jj) * kWave] = ((w3[e] + w2[e]) + w1[e]) + acc[m][q * KT + jj];
+                    }
+            }
+        }
+    } else {
+        bool tok_ok[MB];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) tok_ok[m] = (valid >> (16 * m + (lane & 15))) & 1;
+        project_part<KT, S, TIn, stages_for(KT)>(acc, A, n, P, n, nk, k, tok_ok, wave, lane);
+        // fold the waves in the order ((w3 + w2) + w1) + w0 through `slot`
+        f32x4 *my = slot + lane;
+        if (wave == NW - 1) {
 #pragma unroll
             for (int m = 0; m < MB; ++m)
 #pragma unroll
-                for (int jj = 0; jj < KT; ++jj)
-                    dst[(m * KT + jj) * kWave + lane] = my[(m * S * KT + q * KT + jj) * kWave] + acc[m][q * KT + jj];
+                for (int jj = 0; jj < S * KT; ++jj) my[(m * S * KT + jj) * kWave] = acc[m][jj];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int w = NW - 2; w >= 1; --w) {
+            if (wave == w) {
+#pragma unroll
+                for (int m = 0; m < MB; ++m)
+#pragma unroll
+                    for (int jj = 0; jj < S * KT; ++jj)
+                        my[(m * S * KT + jj) * kWave] = my[(m * S * KT + jj) * kWave] + acc[m][jj];
+            }
+            __syncthreads();
+        }
+        publish();
+        if (wave == 0) {
+#pragma unroll
+            for (int q = 0; q < S; ++q) {
+                if (q >= nmem) break;
+                f32x4 *dst = member_dst(q);
+#pragma unroll
+                for (int m = 0; m < MB; ++m)
+#pragma unroll
+                    for (int jj = 0; jj < KT; ++jj)
+                        dst[(m * KT + jj) * kWave] = my[(m * S * KT + q * KT + jj) * kWave] + acc[m][q * KT + jj];
+            }
         }
     }
 }
 
 // Persistent: the grid is sized to the resident capacity of the GPU.  Each
-// workgroup starts on item blockIdx.x and, when done, takes the next
-// unclaimed item from the work counter.  Claiming only when free keeps the
-// tail to at most one item per workgroup.  The loop ends once the counter
-// passes the item count, which every workgroup reaches.
+// workgroup starts on item blockIdx.x and takes further items from the work
+// counter.  While more than one round of items (one per workgroup) lies
+// beyond its current item, it claims the next one when it starts the current
+// one, so the counter's round trip overlaps the stream; in the last round it
+// claims only when free, which keeps the tail to at most one item.  The loop
+// ends once a claim passes the item count, which every workgroup reaches.
+// One barrier per item hands the claim to the workgroup; the next write of
+// `next` comes after the following item's fold barrier, by which time every
+// thread has read it.
 template <int KT, int S, typename TIn>
 __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(ProjArgs a) {
-    __shared__ f32x4 slot[MB * S * KT * kWave];   // cross-wave fold
-    __shared__ __attribute__((aligned(16))) uint8_t ring[use_dma<KT, S, TIn>() ? DmaShape<KT, S>::kRing : 16];
+    constexpr bool kDma = use_dma<KT, S, TIn>();
+    __shared__ f32x4 slot[kDma ? 1 : MB * S * KT * kWave];   // cross-wave fold of the register path
+    __shared__ __attribute__((aligned(16))) uint8_t ring[kDma ? DmaShape<KT, S>::kRing : 16];
     __shared__ int next;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    constexpr int kWaveRing = use_dma<KT, S, TIn>() ? DmaShape<KT, S>::kStages * DmaShape<KT, S>::kStage : 0;
-    const uint8_t *my_ring = ring + wave * kWaveRing;   // this wave's stages
-    const int count = a.tiles ? __builtin_amdgcn_readfirstlane(*a.n_tiles) : a.B * a.tpe;
+    constexpr int kWaveRing = kDma ? DmaShape<KT, S>::kWaveRing : 0;
+    uint8_t *my_ring = ring + wave * kWaveRing;   // this wave's stages
+    const int count = a.tiles ? load_uniform(a.n_tiles) : a.B * a.tpe;
     const int items = count * a.slots;
     int item = blockIdx.x;
     while (item < items) {
-        chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave, my_ring, lds_addr(my_ring));
-        if (tid == 0) next = static_cast<int>(gridDim.x) + atomicAdd(a.work, 1);
+        const bool ahead = item + static_cast<int>(gridDim.x) < items;
+        int claim = 0;
+        if (ahead && tid == 0) claim = atomicAdd(a.work, 1);
+        chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave, my_ring, lds_addr(my_ring), ahead, claim, &next);
+        if (!ahead) {
+            int late = 0;
+            if (tid == 0) late = atomicAdd(a.work, 1);
+            late = __builtin_amdgcn_readfirstlane(late);   // waited for in every wave
+            if (tid == 0) next = static_cast<int>(gridDim.x) + late;
+        }
         __syncthreads();
-        item = next;
-        __syncthreads();   // every thread has read `next` before it is rewritten
+        item = __builtin_amdgcn_readfirstlane(next);
     }
 }
 
+// Bit i set where byte i of w is non-zero (i < 4).
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
+    return ((w & 0xffu) != 0) | (((w >> 8) & 0xffu) != 0) << 1 | (((w >> 16) & 0xffu) != 0) << 2 |
+           ((w >> 24) != 0) << 3;
+}
+
 // Clears the work counter and, with a mask, lists the tiles that hold at
-// least one valid token, in tile order (one workgroup; block-wide prefix
-// counts keep the order).  A full tile's 64 mask bytes are read as four
-// 128-bit loads when the mask rows are 16-byte aligned.
+// least one valid token, in tile order, each with its set of valid tokens
+// (one workgroup; block-wide prefix counts keep the order).  A full tile's
+// 64 mask bytes are read as four 128-bit loads when the mask rows are
+// 16-byte aligned.
 __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int B, int T, int tpe, int *tiles,
-                                                        int *n_tiles, int *work) {
+                                                        uint64_t *bits, int *n_tiles, int *work) {
     __shared__ int wsum[16];
     __shared__ int base;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -475,20 +565,23 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
     const int total = B * tpe;
     for (int t0 = 0; t0 < total; t0 += 1024) {
         const int bt = t0 + tid;
-        int any = 0;
+        uint64_t set = 0;
         if (bt < total) {
             const int b = bt / tpe, tile = bt - b * tpe;
             const uint8_t *m = mask + static_cast<size_t>(b) * T + static_cast<size_t>(tile) * TT;
             const int n = min(TT, T - tile * TT);
             if (vec && n == TT) {
-                u32x4 v = ld128(m);
 #pragma unroll
-                for (int q = 1; q < TT / 16; ++q) v |= ld128(m + 16 * q);
-                any = (v[0] | v[1] | v[2] | v[3]) != 0;
+                for (int q = 0; q < TT / 16; ++q) {
+                    const u32x4 v = ld128(m + 16 * q);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) set |= static_cast<uint64_t>(nonzero_bytes(v[e])) << (16 * q + 4 * e);
+                }
             } else {
-                for (int i = 0; i < n && !any; ++i) any = m[i] != 0;
+                for (int i = 0; i < n; ++i) set |= static_cast<uint64_t>(m[i] != 0) << i;
             }
         }
+        const int any = set != 0;
         int x = any;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
@@ -502,7 +595,10 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
             before += w < wave ? wsum[w] : 0;
             all += wsum[w];
         }
-        if (any) tiles[base + before + x - 1] = bt;
+        if (any) {
+            tiles[base + before + x - 1] = bt;
+            bits[base + before + x - 1] = set;
+        }
         __syncthreads();
         if (tid == 0) base += all;
         __syncthreads();
@@ -717,7 +813,7 @@ size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, 
     const Plan p = plan_group(n_in, n_out, n_layers, B, T, k_in, k_out, nullptr);
     const size_t tiles = static_cast<size_t>(B) * ((T + TT - 1) / TT);
     return align256(p.part_floats * sizeof(float)) + align256(p.gpart_floats * sizeof(float)) +
-           align256((tiles + 2) * sizeof(int));
+           align256((tiles + 2) * sizeof(int)) + align256(tiles * sizeof(uint64_t));
 }
 
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
@@ -742,20 +838,21 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     // narrow ones and the tail after the last claim is short.
     a.ordered = a.slots <= kMaxSlots;
     if (a.ordered) {
-        int width[kMaxSlots];
+        int width[kMaxSlots], layer_of[kMaxSlots];
         for (int l = 0; l < grp.n_layers; ++l) {
             const ChunkLayer &L = a.layer[l];
             for (int c = 0; c < L.x_items + L.c_out; ++c) {
                 const int n = c < L.x_items ? L.n_in : L.n_out;
                 const int col0 = (c < L.x_items ? c : c - L.x_items) * chunk_cols(KT);
                 width[L.slot_begin + c] = min(chunk_cols(KT), n - col0);
+                layer_of[L.slot_begin + c] = l;
             }
         }
         int n = 0;
         for (int w = chunk_cols(KT); w > 0; ) {   // descending distinct widths
             int next = 0;
             for (int sl = 0; sl < a.slots; ++sl) {
-                if (width[sl] == w) a.slot_order[n++] = static_cast<uint16_t>(sl);
+                if (width[sl] == w) a.slot_order[n++] = static_cast<uint16_t>(layer_of[sl] << 12 | sl);
                 else if (width[sl] < w && width[sl] > next) next = width[sl];
             }
             w = next;
@@ -773,12 +870,15 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     a.k_in = k_in;
     a.k_out = k_out;
     a.ck = chunk_cols(KT);
+    const size_t ntiles = static_cast<size_t>(B) * a.tpe;
     int *list = reinterpret_cast<int *>(w);
-    int *count = list + static_cast<size_t>(B) * a.tpe;
+    int *count = list + ntiles;
+    uint64_t *bits = reinterpret_cast<uint64_t *>(w + align256((ntiles + 2) * sizeof(int)));
     a.work = count + 1;
     a.tiles = mask ? list : nullptr;
+    a.bits = mask ? bits : nullptr;
     a.n_tiles = mask ? count : nullptr;
-    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, count, a.work);
+    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, bits, count, a.work);
     const int max_items = a.slots * B * a.tpe;
     switch (KT) {
         case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, smax, s) : launch_chunks<1, float>(a, max_items, smax, s); break;
