@@ -65,19 +65,34 @@ constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100,
 
 // Epilogue of a 256 x 256 tile: the fp32 scores, times the optional row and
 // column scales (s * row_scale[q] * col_scale[j], for normalised scores), go
-// to s (rows past Q and columns past N are skipped).  With a filter, scores at or above the row's
-// threshold are also appended to the row's top-k candidate list (order
-// arbitrary; the count keeps growing past the capacity so that an overflow is
-// visible).  `ths` is 1 KB of free LDS for the tile's thresholds.
-__device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *ths, float *__restrict__ s,
+// to s (rows past Q and columns past N are skipped).  With a filter, scores at
+// or above the row's threshold are also appended to the row's top-k candidate
+// list; the count keeps growing past the capacity so that an overflow is
+// visible.  Each half-wave of one (i, r) step holds one row, so candidates
+// are counted with ballots: a first pass writes the scores and each (row,
+// column half)'s count to LDS, one global atomic per row reserves the tile's
+// space, and a second pass places each candidate at its reserved base plus its
+// ballot prefix (in column order within a column half).  `lds` is 5 KB of free
+// LDS (thresholds, counts and bases).
+__device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *lds, float *__restrict__ s,
                                              int64_t ld_s, int m0, int64_t n0, int rows_a, int rows_b,
                                              int wm, int wn, int tid, int lane, const ScoreFilter &filt,
                                              const ScoreScale &scale) {
     const bool filter = filt.thr != nullptr;
+    float *ths = lds;                                        // [256] row thresholds
+    int *cnt = reinterpret_cast<int *>(lds + 256);           // [2][256] candidates per column half
+    int *base = reinterpret_cast<int *>(lds + 768);          // [2][256] first slot per column half
     if (filter) {
         ths[tid] = tid < rows_a ? filt.thr[m0 + tid] : __builtin_inff();
         __syncthreads();
     }
+    const uint64_t half = lane < 32 ? 0xffffffffull : 0xffffffff00000000ull;   // the lanes of this row
+    auto value = [&](int i, int r, int j, float rs, int col) {   // the same in both passes
+        float v = acc[i][j][r];
+        if (scale.row) v *= rs;
+        if (scale.col && col < rows_b) v *= scale.col[n0 + col];
+        return v;
+    };
     // result register r of block (i, j): row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -89,22 +104,51 @@ __device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *t
             float *srow_p = s + q * ld_s + n0;
             const float t = filter ? ths[row] : 0.f;
             const float rs = scale.row ? scale.row[q] : 1.f;
+            int hits = 0;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int col = wn * 128 + j * 32 + (lane & 31);
-                float v = acc[i][j][r];
-                if (scale.row) v *= rs;
-                if (scale.col && col < rows_b) v *= scale.col[n0 + col];
-                if (col < rows_b) {
-                    srow_p[col] = v;
-                    if (filter && v >= t) {
-                        const int pos = atomicAdd(filt.cnt + q, 1);
-                        if (pos < filt.cap) {
-                            filt.val[q * filt.cap + pos] = v;
-                            filt.idx[q * filt.cap + pos] = static_cast<int>(n0) + col;
-                        }
+                const float v = value(i, r, j, rs, col);
+                if (col < rows_b) srow_p[col] = v;
+                if (filter) hits += __popcll(__builtin_amdgcn_ballot_w64(col < rows_b && v >= t) & half);
+            }
+            if (filter && (lane & 31) == 0) cnt[wn * 256 + row] = hits;
+        }
+    if (!filter) return;
+    __syncthreads();
+    if (tid < rows_a) {
+        const int c0 = cnt[tid], c1 = cnt[256 + tid];
+        const int b = c0 + c1 > 0 ? atomicAdd(filt.cnt + m0 + tid, c0 + c1) : 0;
+        base[tid] = b;
+        base[256 + tid] = b + c0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row >= rows_a) continue;
+            const int64_t q = m0 + row;
+            const float t = ths[row];
+            const float rs = scale.row ? scale.row[q] : 1.f;
+            int pos = base[wn * 256 + row];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int col = wn * 128 + j * 32 + (lane & 31);
+                const float v = value(i, r, j, rs, col);
+                const bool hit = col < rows_b && v >= t;
+                const uint64_t m = __builtin_amdgcn_ballot_w64(hit) & half;
+                if (hit) {
+                    const int p = pos + static_cast<int>(__builtin_amdgcn_mbcnt_hi(
+                                            static_cast<uint32_t>(m >> 32),
+                                            __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)));
+                    if (p < filt.cap) {
+                        filt.val[q * filt.cap + p] = v;
+                        filt.idx[q * filt.cap + p] = static_cast<int>(n0) + col;
                     }
                 }
+                pos += __popcll(m);
             }
         }
 }
