@@ -126,6 +126,14 @@ __device__ __forceinline__ double load_in_d<bf16_bits>(const bf16_bits *p) {
 // selected by l / 16; the result holds rows 4*(l/16) + r, r < 4, of column
 // l % 16.  Any assignment of contraction indices to (l/16, element) is valid
 // as long as A and B use the same one.
+// A double from lane `src` (a compile-time lane), as two 32-bit readlanes.
+__device__ __forceinline__ double readlane_d(double v, int src) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), src));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u >> 32), src));
+    return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 __device__ __forceinline__ f32x4 mfma16_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }

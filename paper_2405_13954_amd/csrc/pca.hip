@@ -650,14 +650,6 @@ __device__ __forceinline__ void sum_partials(const double *__restrict__ part, in
     }
 }
 
-// A double from lane `src` (a compile-time lane), as two 32-bit readlanes.
-__device__ __forceinline__ double readlane_d(double v, int src) {
-    const uint64_t u = __builtin_bit_cast(uint64_t, v);
-    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), src));
-    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u >> 32), src));
-    return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
-}
-
 // p <= PM (32 or 64).  One workgroup sums the partials into G; wave 0 then,
 // in registers, forms the shifted Cholesky G + eps (tr G / p) I = R^T R
 // (R upper) and R^{-1}, lane r holding row r of the matrix padded to PM

@@ -87,23 +87,13 @@ __global__ __launch_bounds__(256) void k_form(const float *S, int D, int64_t N, 
     if (i == 0 && threadIdx.x == 0) info[blk] = 0;
 }
 
-// sum over m in [m0, m1) of x[m sx] y[m sy] from LDS, in four interleaved
-// partial sums ((s0 + s1) + (s2 + s3)): eight loads in flight instead of one
-// LDS round trip per term.
-__device__ __forceinline__ double lds_dot(const double *x, int sx, const double *y, int sy, int m0, int m1) {
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    int m = m0;
-    for (; m + 4 <= m1; m += 4) {
-        s0 = fma(x[m * sx], y[m * sy], s0);
-        s1 = fma(x[(m + 1) * sx], y[(m + 1) * sy], s1);
-        s2 = fma(x[(m + 2) * sx], y[(m + 2) * sy], s2);
-        s3 = fma(x[(m + 3) * sx], y[(m + 3) * sy], s3);
-    }
-    for (; m < m1; ++m) s0 = fma(x[m * sx], y[m * sy], s0);
-    return (s0 + s1) + (s2 + s3);
-}
-
 // Unblocked Cholesky of the nb x nb diagonal block at (k0, k0); one wave.
+// Lane t holds row t in registers; at step j the pivot and then column j of
+// the rows below come from their lanes by readlane, so no step needs LDS or
+// a barrier.  Each row's update A_tk -= L_tj L_kj is the same fused operation
+// in the same order as a textbook right-looking factorisation.  Entries above
+// the diagonal collect meaningless values and are never read; rows past nb
+// are identity rows, so every step runs (unit pivots there).
 __global__ __launch_bounds__(64) void k_potrf_diag(double *A_all, int D, int k0, int *info) {
     __shared__ double a[NB * LT];
     const int blk = blockIdx.x, t = threadIdx.x;
@@ -112,40 +102,56 @@ __global__ __launch_bounds__(64) void k_potrf_diag(double *A_all, int D, int k0,
     for (int i = 0; i < nb; ++i)
         if (t <= i) a[i * LT + t] = A[static_cast<size_t>(k0 + i) * D + k0 + t];
     __syncthreads();
-    for (int j = 0; j < nb; ++j) {
-        if (t == 0) {
-            double piv = a[j * LT + j];
-            if (!(piv > 0.0)) {
-                if (info[blk] == 0) info[blk] = k0 + j + 1;
-                piv = 1.0;   // keep going; the result is reported as not PD
-            }
-            a[j * LT + j] = sqrt(piv);
-        }
-        __syncthreads();
-        if (t > j && t < nb) a[t * LT + j] /= a[j * LT + j];
-        __syncthreads();
-        if (t > j && t < nb) {   // row t: independent updates, four at a time (loads before stores)
-            const double lij = a[t * LT + j];
-            int k = j + 1;
-            for (; k + 4 <= t + 1; k += 4) {
-                double u[4], w[4];
+    double r[NB];
+    const int tl = t < nb ? t : nb - 1;   // clamped: every lane reads, padding is selected afterwards
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    u[q] = a[t * LT + k + q];
-                    w[q] = a[(k + q) * LT + j];
-                }
-#pragma unroll
-                for (int q = 0; q < 4; ++q) a[t * LT + k + q] = u[q] - lij * w[q];
-            }
-            for (; k <= t; ++k) a[t * LT + k] -= lij * a[k * LT + j];
-        }
-        __syncthreads();
+    for (int k = 0; k < NB; ++k) {
+        const double v = a[tl * LT + (k < tl ? k : tl)];
+        r[k] = t < nb ? (k <= t ? v : 0.0) : (k == t ? 1.0 : 0.0);
     }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        double piv = readlane_d(r[j], j);
+        if (!(piv > 0.0)) {
+            if (t == 0 && info[blk] == 0) info[blk] = k0 + j + 1;
+            piv = 1.0;   // keep going; the result is reported as not PD
+        }
+        const double d = sqrt(piv);
+        r[j] = t == j ? d : t > j ? r[j] / d : r[j];
+#pragma unroll
+        for (int k = j + 1; k < NB; ++k) {
+            r[k] = fma(-r[j], readlane_d(r[j], k), r[k]);
+            if ((k - j) % 8 == 0) __builtin_amdgcn_sched_barrier(0);   // at most 8 readlane pairs live
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k)
+        if (k <= t) a[t * LT + k] = r[k];
+    __syncthreads();
     for (int i = 0; i < nb; ++i)
         if (t <= i) A[static_cast<size_t>(k0 + i) * D + k0 + t] = a[i * LT + t];
 }
 
-// Rows below the diagonal block: L21 = A21 L11^{-T}; one row per thread.
+// Forward substitution L x = b for one right-hand side per lane, x in
+// registers (b on entry), L the lower-triangular 64 x 64 tile in LDS (row
+// stride LT; past the valid rows an identity), read at wave-uniform
+// addresses so that every read is a broadcast: x_j = x_j / L_jj, then
+// x_k -= L_kj x_j for k > j.
+__device__ __forceinline__ void fwd_subst(double (&x)[NB], const double *l) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        x[j] = x[j] / l[j * LT + j];
+#pragma unroll
+        for (int k = j + 1; k < NB; ++k) {
+            x[k] = fma(-l[k * LT + j], x[j], x[k]);
+            if ((k - j) % 8 == 0) __builtin_amdgcn_sched_barrier(0);   // at most 8 broadcast reads live
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// Rows below the diagonal block: L21 = A21 L11^{-T}; one row per lane.
 __global__ __launch_bounds__(64) void k_trsm_panel(double *A_all, int D, int k0) {
     __shared__ double l11[NB * LT];
     __shared__ double x[NB * LT];
@@ -154,13 +160,17 @@ __global__ __launch_bounds__(64) void k_trsm_panel(double *A_all, int D, int k0)
     const int nb = min(NB, D - k0);
     const int r0 = k0 + nb + blockIdx.x * NB;
     const int nr = min(NB, D - r0);
-    for (int i = 0; i < nb; ++i) l11[i * LT + t] = (t <= i && t < nb) ? A[static_cast<size_t>(k0 + i) * D + k0 + t] : 0.0;
+    for (int i = 0; i < NB; ++i)   // identity past nb
+        l11[i * LT + t] = i < nb ? (t <= i ? A[static_cast<size_t>(k0 + i) * D + k0 + t] : 0.0) : (t == i ? 1.0 : 0.0);
     for (int i = 0; i < nr; ++i) x[i * LT + t] = (t < nb) ? A[static_cast<size_t>(r0 + i) * D + k0 + t] : 0.0;
     __syncthreads();
-    if (t < nr) {
-        double *xr = x + t * LT;
-        for (int j = 0; j < nb; ++j) xr[j] = (xr[j] - lds_dot(xr, 1, l11 + j * LT, 1, 0, j)) / l11[j * LT + j];
-    }
+    // row t solves x L11^T = a, i.e. L11 x^T = a^T
+    double r[NB];
+#pragma unroll
+    for (int k = 0; k < NB; ++k) r[k] = t < nr ? x[t * LT + k] : 0.0;
+    fwd_subst(r, l11);
+#pragma unroll
+    for (int k = 0; k < NB; ++k) x[t * LT + k] = r[k];   // each lane rewrites only its own row
     __syncthreads();
     for (int i = 0; i < nr; ++i)
         if (t < nb) A[static_cast<size_t>(r0 + i) * D + k0 + t] = x[i * LT + t];
@@ -216,29 +226,22 @@ __global__ __launch_bounds__(256) void k_syrk_update(double *A_all, int D, int k
 }
 
 // Inverse of the lower-triangular 64x64 diagonal tile t of L (zero padded
-// past D): thread c computes column c by substitution, L_tt w = e_c.
+// past D): lane c solves L_tt w = e_c in registers, giving column c.
 __global__ __launch_bounds__(64) void k_diag_inv(const double *A_all, int D, double *Linv_all) {
     __shared__ double a[NB * LT];
-    __shared__ double wl[NB * LT];
     const int t = blockIdx.x, blk = blockIdx.y, c = threadIdx.x;
     const double *A = A_all + static_cast<size_t>(blk) * D * D;
     const int r0 = t * NB, nb = min(NB, D - r0);
-    for (int i = 0; i < NB; ++i)
-        a[i * LT + c] = (i < nb && c <= i) ? A[static_cast<size_t>(r0 + i) * D + r0 + c] : 0.0;
+    for (int i = 0; i < NB; ++i)   // identity past nb
+        a[i * LT + c] = i < nb ? (c <= i ? A[static_cast<size_t>(r0 + i) * D + r0 + c] : 0.0) : (c == i ? 1.0 : 0.0);
     __syncthreads();
+    double w[NB];   // e_c for the valid columns; padded columns of the inverse are zero
+#pragma unroll
+    for (int k = 0; k < NB; ++k) w[k] = (k == c && c < nb) ? 1.0 : 0.0;
+    fwd_subst(w, a);
     double *W = Linv_all + (static_cast<size_t>(blk) * gridDim.x + t) * NB * NB;
-    for (int r = 0; r < NB; ++r) {
-        double v = 0.0;
-        if (c < nb && r < nb && r >= c) {
-            if (r == c) {
-                v = 1.0 / a[r * LT + r];
-            } else {
-                v = -lds_dot(a + r * LT, 1, wl + c, LT, c, r) / a[r * LT + r];
-            }
-        }
-        wl[r * LT + c] = v;   // only this thread reads column c
-        W[r * NB + c] = v;
-    }
+#pragma unroll
+    for (int r = 0; r < NB; ++r) W[r * NB + c] = w[r];
 }
 
 // Blocked substitution on the matrix cores for 64 right-hand sides (queries
