@@ -178,6 +178,51 @@ def test_project_grouped_multichunk_vs_oracle():
         assert err <= 1e-3
 
 
+def test_project_scattered_mask_vs_oracle():
+    """Masks that are not length prefixes: random holes, a fully masked tile
+    between valid ones, tiles whose only valid token is the first or the last
+    of the tile, and a ragged last tile holding one valid token.  NaN and -Inf
+    in every masked slot must not reach the result, and a layer spans two
+    chunks on the x side.  Grouped launch, fp32 out, against the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say("[project] scattered masks with poisoned masked slots vs oracle")
+    B, T = 3, 300                                     # five tiles, the last one 44 tokens
+    mask_np = (W.rng(3, 41, 0).random((B, T)) < 0.6).astype(np.uint8)
+    mask_np[0, 64:128] = 0                            # fully masked tile between valid ones
+    mask_np[1, :] = 0
+    mask_np[1, 64] = 1                                # first token of tile 1 only
+    mask_np[1, 255] = 1                               # last token of tile 3 only
+    mask_np[2, 256:] = 0
+    mask_np[2, 299] = 1                               # last token of the ragged tile only
+    shapes = [(4352, 96), (200, 328)]
+    k_in, k_out = 12, 20
+    D = k_in * k_out
+    store = torch.zeros((B, len(shapes) * D), dtype=torch.float32, device="cuda")
+    layers, data = [], []
+    bad = mask_np == 0
+    for i, (ni, no) in enumerate(shapes):
+        d = W.layer_inputs(13, i, B, T, ni, no, k_in, k_out, 1.0, 0.5, "bf16")
+        data.append(d)
+        x, dy = d["x"].copy(), d["dy"].copy()
+        x[bad] = 0x7FC0                               # NaN
+        dy[bad] = 0xFF80                              # -Inf
+        layers.append(dict(x=dev(x), dy=dev(dy), p_in=dev(d["p_in"]), p_out=dev(d["p_out"]),
+                           g_out=store[:, i * D:(i + 1) * D]))
+    P.logra_project_layers(layers, mask=dev(mask_np))
+    torch.cuda.synchronize()
+    got = host(store).astype(np.float64)
+    assert np.all(np.isfinite(got))
+    for i, d in enumerate(data):
+        want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], mask_np)
+        g = got[:, i * D:(i + 1) * D]
+        for b in range(B):
+            err = np.linalg.norm(g[b] - want[b]) / np.linalg.norm(want[b])
+            say(f"  layer {i} {shapes[i]} example {b} ({int(mask_np[b].sum())} tokens): normwise err {err:.2e}")
+            assert err <= 1e-3
+
+
 def test_project_shared_inputs_bitwise_equal():
     """Layers given the same x tensor (q/k/v and gate/up of a transformer
     block) are projected from one pass over x; every output must equal, bit
