@@ -17,8 +17,9 @@
 //     up to three projections P_in (k <= 32), each with the same per-element
 //     sums as a pass of its own.  Workgroups take items from an atomic counter as they
 //     finish (items differ up to 4x in columns and workgroups in speed, so a
-//     static assignment leaves a long tail).  The four waves deal the chunk's 32-wide steps
-//     round-robin; each lane feeds a 128-bit buffer load straight into its
+//     static assignment leaves a long tail).  Each of the four waves streams
+//     a contiguous band of the chunk's columns (whole bands read HBM faster
+//     than steps dealt round-robin); each lane feeds a 128-bit buffer load straight into its
 //     MFMA operand (row = token for x/dy, row = projection dimension for P;
 //     16x16x32 bf16 or 16x16x4 fp32, fp32 accumulation).  Masked tokens, rows
 //     of P beyond k and lanes past the chunk end get an out-of-range offset:
@@ -163,8 +164,8 @@ __device__ __forceinline__ void mma_step(f32x4 (&acc)[MB][KT], const u32x4 (&xa)
 // One wave's share of  A'_s[TT x 16KT] = A[TT x nk] * P_s[k x nk]^T for the
 // S projections P_s (s < S) of one operand A (a shared input: one pass over
 // A; a missing P_s reads zeros), A and P_s with row strides lda and ldp.
-// Contraction steps are dealt to the waves round-robin (bf16: in adjacent
-// pairs, see step_of).  Every load is unconditional
+// Each wave takes a contiguous band of the contraction steps (bf16: of
+// 64-column units, two steps each, see step_of).  Every load is unconditional
 // (out-of-range offsets read zeros), and the ST-stage register pipeline
 // keeps ST-1 steps in flight while a step multiplies.  Each wave's step
 // count is rounded up to a multiple of ST with empty steps (no memory access,
@@ -184,13 +185,19 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
 #pragma unroll
         for (int j = 0; j < S * KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int nsteps = (nk + SS - 1) / SS;
-    // the wave's j-th step: for bf16, 32-column steps in adjacent pairs dealt
-    // round-robin (the 64-column steps of project_part_dma, so that both paths
-    // add the same products in the same order); for fp32, single steps
+    // the wave's j-th step, in its band of units: for bf16 a unit is two
+    // 32-column steps (a 64-column step of project_part_dma, so that both
+    // paths add the same products in the same order); for fp32 one step.
+    // Steps past the wave's count (the rounding of the pipeline) read zeros.
     constexpr bool kPairs = sizeof(TIn) == 2;
-    auto step_of = [&](int j) { return kPairs ? 2 * (wave + NW * (j >> 1)) + (j & 1) : wave + NW * j; };
+    constexpr int kNone = 1 << 24;   // a step index past any chunk
     const int units = kPairs ? (nsteps + 1) / 2 : nsteps;
-    const int count = units > wave ? (units - wave + NW - 1) / NW * (kPairs ? 2 : 1) : 0;
+    const int per = (units + NW - 1) / NW;
+    const int first = wave * per;
+    const int count = max(0, min(per, units - first)) * (kPairs ? 2 : 1);
+    auto step_of = [&](int j) {
+        return j >= count ? kNone : kPairs ? 2 * (first + (j >> 1)) + (j & 1) : first + j;
+    };
     if (count == 0) return;
 
     const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * ES);
@@ -245,8 +252,9 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
 // stages in flight (three stages where the LDS allows, else two); the wave waits only on its own copies (s_waitcnt vmcnt) and
 // shares nothing with the other waves, so no barrier is needed.  Masked
 // tokens, rows of P beyond k and columns past the chunk read zeros (an
-// out-of-range offset); steps past the wave's last are all out of range and
-// keep the copy count of every iteration the same.
+// out-of-range offset).  The wave's steps are a contiguous band of the
+// chunk; prefetches past the band are all out of range and keep the copy
+// count of every iteration the same.
 template <int KT, int S>
 __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const bf16_bits *A, int lda,
                                                  const bf16_bits *const (&P)[S], int ldp, int nk, int k,
@@ -259,7 +267,9 @@ __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const
 #pragma unroll
         for (int j = 0; j < S * KT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int nsteps = (nk + kDmaCols - 1) / kDmaCols;
-    const int mine = nsteps > wave ? (nsteps - wave + NW - 1) / NW : 0;
+    const int per = (nsteps + NW - 1) / NW;   // each wave streams a contiguous band of steps
+    const int first = wave * per;
+    const int mine = max(0, min(per, nsteps - first));
     if (mine == 0) return;
     const auto ra = buf_rsrc(A, (static_cast<uint32_t>(TT - 1) * lda + nk) * 2u);
     __amdgpu_buffer_rsrc_t rp[S];
@@ -279,9 +289,9 @@ __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const
         const int r = 8 * q + sub;
         po[q] = r < k ? (static_cast<uint32_t>(r) * ldp + lcol) * 2u : kBufOOB;
     }
-    auto issue = [&](int i, int stage) {
-        const int st = wave + NW * i;
-        const bool in = st * kDmaCols + lcol < nk;
+    auto issue = [&](int i, int stage) {   // past the band: all out of range
+        const int st = first + i;
+        const bool in = i < mine && st * kDmaCols + lcol < nk;
         const uint32_t dk = static_cast<uint32_t>(st * kDmaCols) * 2u;
         const uint32_t lds = ring_addr + static_cast<uint32_t>(stage * Sh::kStage);
 #pragma unroll
