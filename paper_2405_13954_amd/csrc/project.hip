@@ -11,7 +11,7 @@
 //     the ordered list of 64-token tiles holding at least one valid token,
 //     each with the 64-bit set of its valid tokens.
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
-//     = one contraction chunk (<= 4096 columns) of one side (x or dy) of one
+//     = one contraction chunk (<= 6144 columns at k <= 32, <= 4096 above) of one side (x or dy) of one
 //     listed tile.  Layers given the same x tensor (q/k/v, gate/up of a
 //     transformer block) share their x items: one pass over the chunk feeds
 //     up to three projections P_in (k <= 32), each with the same per-element
@@ -48,7 +48,7 @@ namespace {
 #define LOGRA_PROJ_ROWBLOCKS 4
 #endif
 #ifndef LOGRA_PROJ_CHUNK
-#define LOGRA_PROJ_CHUNK 4096
+#define LOGRA_PROJ_CHUNK 6144   // k <= 32 (14,336 = 6,144 + 6,144 + 2,048); measured best of 2,048..8,192
 #endif
 #ifndef LOGRA_PROJ_NT
 #define LOGRA_PROJ_NT 0
@@ -73,6 +73,9 @@ constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
 
 #ifndef LOGRA_PROJ_DMA
 #define LOGRA_PROJ_DMA 1   // bf16 operands staged by LDS-DMA wherever the rings fit in LDS
+#endif
+#ifndef LOGRA_PROJ_AHEAD_ROUNDS
+#define LOGRA_PROJ_AHEAD_ROUNDS 2   // rounds of items at the end claimed only when free
 #endif
 #ifndef LOGRA_PROJ_DMA_NT_KT
 // The streamed x / dy copies of the DMA path carry the non-temporal hint up
@@ -521,10 +524,10 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 
 // Persistent: the grid is sized to the resident capacity of the GPU.  Each
 // workgroup starts on item blockIdx.x and takes further items from the work
-// counter.  While more than one round of items (one per workgroup) lies
-// beyond its current item, it claims the next one when it starts the current
-// one, so the counter's round trip overlaps the stream; in the last round it
-// claims only when free, which keeps the tail to at most one item.  The loop
+// counter.  While more than LOGRA_PROJ_AHEAD_ROUNDS rounds of items (one per
+// workgroup) lie beyond its current item, it claims the next one when it
+// starts the current one, so the counter's round trip overlaps the stream;
+// in the last rounds it claims only when free, which keeps the tail short.  The loop
 // ends once a claim passes the item count, which every workgroup reaches.
 // One barrier per item hands the claim to the workgroup; the next write of
 // `next` comes after the following item's fold barrier, by which time every
@@ -543,7 +546,7 @@ __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(Proj
     const int items = count * a.slots;
     int item = blockIdx.x;
     while (item < items) {
-        const bool ahead = item + static_cast<int>(gridDim.x) < items;
+        const bool ahead = item + LOGRA_PROJ_AHEAD_ROUNDS * static_cast<int>(gridDim.x) < items;
         int claim = 0;
         if (ahead && tid == 0) claim = atomicAdd(a.work, 1);
         chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave, my_ring, lds_addr(my_ring), ahead, claim, &next);

@@ -40,7 +40,7 @@ def test_version(L):
 
 def test_workspace_sizes(L):
     # chunk partials (one 64 x 16 fp32 block per side per 64-token tile at k <= 16, chunks of
-    # 4096 columns), per-tile k_out x k_in sums, the list of non-empty tiles (+ its count) and
+    # 6144 columns at k <= 32), per-tile k_out x k_in sums, the list of non-empty tiles (+ its count) and
     # their 64-bit valid-token sets, each rounded up to 256 bytes
     assert P.logra_project_ws_size(2, 100, 64, 48, 8, 12) == 2 * 2 * 2 * 64 * 16 * 4 + 1536 + 256 + 256
     assert P.logra_project_ws_size(0, 100, 64, 48, 8, 8) == 0

@@ -147,14 +147,14 @@ def test_project_grouped_equals_single():
 
 
 def test_project_grouped_multichunk_vs_oracle():
-    """A group whose layers span several 4096-column chunks per side, with
+    """A group whose layers span several column chunks per side, with
     partial last chunks of different widths (the launch processes the chunk
     slots widest first), against the oracle layer by layer."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import dev, host, say
     say("[project] grouped multi-chunk layers vs oracle")
-    shapes = [(6144, 1024), (1024, 9000), (4096, 4096)]
+    shapes = [(13000, 1024), (1024, 9000), (4096, 4096)]
     B, T, k = 2, 70, 16
     lens = np.array([70, 41])
     mask_np = W.mask_from_lengths(lens, T)
@@ -196,7 +196,7 @@ def test_project_scattered_mask_vs_oracle():
     mask_np[1, 255] = 1                               # last token of tile 3 only
     mask_np[2, 256:] = 0
     mask_np[2, 299] = 1                               # last token of the ragged tile only
-    shapes = [(4352, 96), (200, 328)]
+    shapes = [(6400, 96), (200, 328)]
     k_in, k_out = 12, 20
     D = k_in * k_out
     store = torch.zeros((B, len(shapes) * D), dtype=torch.float32, device="cuda")
