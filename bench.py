@@ -692,7 +692,8 @@ def main():
         write_traffic(*args.write_traffic)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (see DESIGN.md on sharding)",
+        print("bench.py measures one GPU: the library has no multi-GPU path; a data-parallel run would "
+              "give each GPU its own slice of the batches and of the gradient store",
               file=sys.stderr)
         sys.exit(2)
     import torch
