@@ -11,7 +11,7 @@
 //     the ordered list of 64-token tiles holding at least one valid token,
 //     each with the 64-bit set of its valid tokens.
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
-//     = one contraction chunk (<= 6144 columns at k <= 32, <= 4096 above) of one side (x or dy) of one
+//     = one contraction chunk (<= 6144 columns at k <= 32, <= 14336 above) of one side (x or dy) of one
 //     listed tile.  Layers given the same x tensor (q/k/v, gate/up of a
 //     transformer block) share their x items: one pass over the chunk feeds
 //     up to three projections P_in (k <= 32), each with the same per-element
@@ -66,7 +66,10 @@ constexpr int NT = NW * kWave;            // threads per workgroup
 
 // Contraction columns per work item, and register pipeline depth, by
 // projection width (KT = ceil(k / 16)).
-__host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? 4096 : LOGRA_PROJ_CHUNK; }
+#ifndef LOGRA_PROJ_CHUNK_WIDE
+#define LOGRA_PROJ_CHUNK_WIDE 14336   // k > 32: one item per layer side up to 14,336 (measured best of 2,048..14,336)
+#endif
+__host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? LOGRA_PROJ_CHUNK_WIDE : LOGRA_PROJ_CHUNK; }
 __host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGRA_PROJ_STAGES; }
 
 constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x

@@ -46,8 +46,8 @@ def test_workspace_sizes(L):
     assert P.logra_project_ws_size(0, 100, 64, 48, 8, 8) == 0
     shapes = [(4096, 4096), (4096, 1024), (4096, 1024), (4096, 4096), (4096, 14336), (4096, 14336), (14336, 4096)]
     descs = (P.LayerDesc * 7)(*[P.LayerDesc(0, 0, 0, 0, 0, a, b) for a, b in shapes])
-    # k = 64: chunks of 4096 columns -> 23 chunk blocks of 64 x 64 floats per tile
-    want = 23 * 16 * 16 * 64 * 64 * 4 + 7 * 16 * 16 * 4096 * 4 + 1280 + 2048
+    # k = 64: chunks of up to 14336 columns -> 14 chunk blocks of 64 x 64 floats per tile
+    want = 14 * 16 * 16 * 64 * 64 * 4 + 7 * 16 * 16 * 4096 * 4 + 1280 + 2048
     assert P.logra_project_layers_ws_size(descs, 7, 16, 1024, 64, 64) == want
     assert P.logra_precondition_ws_size(256, 224, 1024) >= 224 * 256 * 256 * 8
     assert P.logra_influence_ws_size(4, 10, 3, 0) == 256
