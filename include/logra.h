@@ -48,7 +48,10 @@ typedef enum {
     LOGRA_ERR_WORKSPACE = -5    /* workspace missing or smaller than *_ws_size */
 } logra_status;
 
-typedef enum { LOGRA_F32 = 0, LOGRA_BF16 = 1 } logra_dtype;
+/* Element types.  LOGRA_F64 is accepted only where a call says so: the
+ * float64 statistics path of fp32 workloads (covariance, preconditioned test
+ * gradients and the scores against them). */
+typedef enum { LOGRA_F32 = 0, LOGRA_BF16 = 1, LOGRA_F64 = 2 } logra_dtype;
 
 /* Compiled limits. */
 #define LOGRA_MAX_K 128          /* k_in, k_out of one projection */
@@ -135,6 +138,18 @@ int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, f
 int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, int D,
                                 int n_blocks, float *S, void *stream);
 
+/* The same statistic kept in float64, for fp32 workloads whose downstream
+ * solve is ill-conditioned (the damped inverse of App. C amplifies the
+ * rounding of an fp32 S by up to the condition number of C + lambda I):
+ *   g   B rows of n_blocks * D elements at stride ld, g_dtype F32 or F64
+ *   S   [n_blocks][D][D] fp64, caller-initialised, updated in place, kept
+ *       exactly symmetric.
+ * Every product and sum is formed in float64 (a product of two fp32 values
+ * is exact there).  Errors as logra_cov_accumulate_blocks; a bf16 g is
+ * INVALID_ARG. */
+int logra_cov_accumulate_f64(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks,
+                             double *S, void *stream);
+
 /* ------------------------------------------------------------------------
  * Damped inverse applied to test gradients, for one layer block (the iHVP
  * step (1) of Sec. 2 Eq. (2) in the projected space of Eq. (3)):
@@ -149,7 +164,8 @@ int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, i
  *   S       [D][D] fp32 covariance from logra_cov_accumulate (lower triangle
  *           is read); N > 0 the number of examples accumulated into it
  *   g_test  Q rows of D at stride ld_in, in_dtype;  g_out Q rows of D at
- *           stride ld_out, out_dtype (may not alias g_test)
+ *           stride ld_out, out_dtype (may not alias g_test); each of F32,
+ *           BF16 or F64
  *   ws      workspace of logra_precondition_ws_size(D, 1, Q) bytes
  * SYNCHRONOUS: waits for `stream`, so that a non-positive pivot can be
  * returned as LOGRA_ERR_NOT_PD (g_out is then unspecified).
@@ -168,6 +184,13 @@ int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, do
                               int out_dtype, int64_t ld_out, void *ws, size_t ws_bytes,
                               void *stream);
 
+/* logra_precondition_blocks with S in float64 (from logra_cov_accumulate_f64);
+ * same workspace size, semantics and errors.  With fp64 g_out the float64
+ * solution is stored unrounded. */
+int logra_precondition_f64(const double *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                           const void *g_test, int in_dtype, int64_t ld_in, int Q, void *g_out,
+                           int out_dtype, int64_t ld_out, void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------------
  * Influence scores and per-query top-k (Sec. 2 Eq. (2) step (2): the dot
  * product of each preconditioned test gradient with every stored training
@@ -177,7 +200,11 @@ int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, do
  *     s[q][j] = sum_{d < D} g_test_pre[q][d] * g_train[j][d]
  *
  *   g_test_pre  Q rows at stride ld_te;  g_train N_chunk rows at stride ld_tr.
- *               Both BF16 (bf16 MFMA, fp32 accumulation) or both F32.
+ *               Both BF16 (bf16 MFMA, fp32 accumulation), or each F32 or
+ *               F64: then every product and sum is formed in float64 and the
+ *               score rounded once to fp32 (the path of fp32 workloads, whose
+ *               scores can cancel by orders of magnitude).  A bf16 operand
+ *               with a non-bf16 one is UNSUPPORTED.
  *   scores      optional [Q][ld_s] fp32 output (NULL = not materialised by
  *               the caller; it then lives in the workspace).
  *   topk        0 = no selection; else 1..LOGRA_MAX_TOPK entries per query

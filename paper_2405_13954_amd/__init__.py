@@ -12,19 +12,19 @@ import ctypes
 import os
 
 __all__ = [
-    "LograError", "lib", "F32", "BF16",
+    "LograError", "lib", "F32", "BF16", "F64",
     "logra_version", "logra_last_error",
     "logra_project_ws_size", "logra_project_layer",
     "logra_project_layers_ws_size", "logra_project_layers",
-    "logra_cov_accumulate", "logra_cov_accumulate_blocks",
-    "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
+    "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_f64",
+    "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks", "logra_precondition_f64",
     "logra_influence_ws_size", "logra_influence_scores",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpaper_logra.so")
 
-F32, BF16 = 0, 1
+F32, BF16, F64 = 0, 1, 2
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NOT_PD, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
 MAX_GROUP = 16
 
@@ -32,8 +32,8 @@ EXPORTED = (
     "logra_last_error", "logra_version",
     "logra_project_ws_size", "logra_project_layer",
     "logra_project_layers_ws_size", "logra_project_layers",
-    "logra_cov_accumulate", "logra_cov_accumulate_blocks",
-    "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks",
+    "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_f64",
+    "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks", "logra_precondition_f64",
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
     "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_pca_ws_size", "logra_pca_topk",
@@ -76,6 +76,8 @@ def lib():
                                            i32, i64, vp, sz, vp]
         L.logra_cov_accumulate.argtypes = [vp, i32, i64, i32, i32, vp, vp]
         L.logra_cov_accumulate_blocks.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
+        L.logra_cov_accumulate_f64.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
+        L.logra_precondition_f64.argtypes = [vp, i32, i32, i64, f64, vp, i32, i64, i32, vp, i32, i64, vp, sz, vp]
         L.logra_precondition_ws_size.argtypes = [i32, i32, i32]
         L.logra_precondition_ws_size.restype = sz
         L.logra_precondition.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp, i32, i64, vp, sz, vp]
@@ -104,6 +106,7 @@ def lib():
         L.logra_offload_rows.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, vp]
         for name in ("logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
+                     "logra_cov_accumulate_f64", "logra_precondition_f64",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
@@ -122,7 +125,9 @@ def _dtype_code(t) -> int:
         return BF16
     if t.dtype == torch.float32:
         return F32
-    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+    if t.dtype == torch.float64:
+        return F64
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16, float32 or float64)")
 
 
 def _ptr(t):
@@ -222,6 +227,16 @@ def logra_cov_accumulate_blocks(g, S, D: int, stream=None):
                                              _stream(stream)))
 
 
+def logra_cov_accumulate_f64(g, S, D: int = None, stream=None):
+    """float64 statistic: S [D, D] or [n_blocks, D, D] fp64 += block-wise g^T g for g [B, n_blocks*D]
+    (fp32 or fp64 rows)."""
+    B = g.shape[0]
+    n_blocks = 1 if S.dim() == 2 else S.shape[0]
+    D = S.shape[-1] if D is None else D
+    ld = _rows(g, D * n_blocks) if B > 0 else D * n_blocks
+    _check(lib().logra_cov_accumulate_f64(_ptr(g), _dtype_code(g), ld, B, D, n_blocks, _ptr(S), _stream(stream)))
+
+
 def logra_precondition_ws_size(D, n_blocks, Q) -> int:
     return int(lib().logra_precondition_ws_size(D, n_blocks, Q))
 
@@ -248,6 +263,20 @@ def logra_precondition_blocks(S, N: int, damp_ratio: float, g_test, g_out, ws=No
     _check(lib().logra_precondition_blocks(_ptr(S), D, n_blocks, int(N), float(damp_ratio), _ptr(g_test),
                                            _dtype_code(g_test), ld_in, Q, _ptr(g_out), _dtype_code(g_out),
                                            ld_out, _ptr(ws), wsb, _stream(stream)))
+
+
+def logra_precondition_f64(S, N: int, damp_ratio: float, g_test, g_out, ws=None, stream=None):
+    """logra_precondition_blocks with an fp64 S [D, D] or [n_blocks, D, D]; g_test / g_out may be
+    fp32, bf16 or fp64 (synchronous)."""
+    n_blocks = 1 if S.dim() == 2 else S.shape[0]
+    D = S.shape[-1]
+    Q = g_test.shape[0]
+    ld_in = _rows(g_test, D * n_blocks) if Q > 0 else D * n_blocks
+    ld_out = _rows(g_out, D * n_blocks) if Q > 0 else D * n_blocks
+    ws, wsb = _workspace(logra_precondition_ws_size(D, n_blocks, Q) if damp_ratio >= 0 else 0, S.device, ws)
+    _check(lib().logra_precondition_f64(_ptr(S), D, n_blocks, int(N), float(damp_ratio), _ptr(g_test),
+                                        _dtype_code(g_test), ld_in, Q, _ptr(g_out), _dtype_code(g_out), ld_out,
+                                        _ptr(ws), wsb, _stream(stream)))
 
 
 def logra_influence_ws_size(Q, N_chunk, topk, scores_given) -> int:

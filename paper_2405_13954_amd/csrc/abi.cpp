@@ -28,8 +28,19 @@ int ok() {
     return LOGRA_OK;
 }
 
+// Storage types of activations, gradients and stores; fp64 is accepted where
+// a call documents it (fp64 statistics of fp32 workloads).
 bool valid_dtype(int d) { return d == LOGRA_F32 || d == LOGRA_BF16; }
-size_t esize(int d) { return d == LOGRA_BF16 ? 2 : 4; }
+bool valid_dtype64(int d) { return valid_dtype(d) || d == LOGRA_F64; }
+size_t esize(int d) { return d == LOGRA_BF16 ? 2 : d == LOGRA_F64 ? 8 : 4; }
+// A score pair: both bf16 (bf16 MFMA), or any mix of fp32 and fp64 (float64
+// accumulation).
+int check_score_dtypes(int te_dtype, int tr_dtype) {
+    if (!valid_dtype64(te_dtype) || !valid_dtype64(tr_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if ((te_dtype == LOGRA_BF16) != (tr_dtype == LOGRA_BF16))
+        return fail(LOGRA_ERR_UNSUPPORTED, "bf16 scores need both operands in bf16");
+    return LOGRA_OK;
+}
 bool al16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Device-memory check; `align` is the required base alignment in bytes.
@@ -206,6 +217,22 @@ int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, f
     return logra_cov_accumulate_blocks(g, g_dtype, ld, B, D, 1, S, stream);
 }
 
+int logra_cov_accumulate_f64(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks, double *S,
+                             void *stream) {
+    if (g_dtype != LOGRA_F32 && g_dtype != LOGRA_F64)
+        return fail(LOGRA_ERR_INVALID_ARG, "fp64 covariance takes fp32 or fp64 rows");
+    if (B < 0 || D <= 0 || n_blocks <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need B >= 0, D > 0, n_blocks > 0");
+    if (n_blocks > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "n_blocks must be <= 65535");
+    if (ld < static_cast<int64_t>(D) * n_blocks) return fail(LOGRA_ERR_INVALID_ARG, "ld must be >= D * n_blocks");
+    if (B == 0) return ok();
+    TRY(check_dev(g, "g", esize(g_dtype)));
+    TRY(check_dev(S, "S", 8));
+    const hipError_t e = logra::launch_cov_f64(g, g_dtype == LOGRA_F64, ld, B, D, n_blocks, S,
+                                               static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "covariance launch");
+    return ok();
+}
+
 // Waits for `s`, then returns NOT_PD naming the first block whose
 // factorisation met a non-positive pivot (the status words in the workspace).
 static int report_not_pd(void *ws, int D, int n_blocks, hipStream_t s) {
@@ -226,11 +253,10 @@ size_t logra_precondition_ws_size(int D, int n_blocks, int Q) {
     return round256(logra::precond_ws_bytes(D, n_blocks, Q));
 }
 
-int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
-                              const void *g_test, int in_dtype, int64_t ld_in, int Q, void *g_out,
-                              int out_dtype, int64_t ld_out, void *ws, size_t ws_bytes,
-                              void *stream) {
-    if (!valid_dtype(in_dtype) || !valid_dtype(out_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+static int precondition_impl(const void *S, bool s_f64, int D, int n_blocks, int64_t N, double damp_ratio,
+                             const void *g_test, int in_dtype, int64_t ld_in, int Q, void *g_out, int out_dtype,
+                             int64_t ld_out, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype64(in_dtype) || !valid_dtype64(out_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
     if (D <= 0 || n_blocks <= 0 || Q < 0) return fail(LOGRA_ERR_INVALID_ARG, "need D > 0, n_blocks > 0, Q >= 0");
     if (D > LOGRA_MAX_PRECOND_D) return fail(LOGRA_ERR_UNSUPPORTED, "D must be <= %d", LOGRA_MAX_PRECOND_D);
     if (n_blocks > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "n_blocks must be <= 65535");
@@ -245,19 +271,34 @@ int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, do
         TRY(check_dev(g_out, "g_out", esize(out_dtype)));
     }
     if (damp_ratio < 0.0) {
-        hipError_t e = logra::launch_copy_rows(g_test, in_dtype == LOGRA_BF16, ld_in, Q, static_cast<int>(width),
-                                               g_out, out_dtype == LOGRA_BF16, ld_out, s);
+        hipError_t e = logra::launch_copy_rows(g_test, in_dtype, ld_in, Q, static_cast<int>(width), g_out, out_dtype,
+                                               ld_out, s);
         if (e != hipSuccess) return hip_fail(e, "copy launch");
         e = hipStreamSynchronize(s);
         if (e != hipSuccess) return hip_fail(e, "stream synchronize");
         return ok();
     }
-    TRY(check_dev(S, "S", 4));
+    TRY(check_dev(S, "S", s_f64 ? 8 : 4));
     TRY(check_ws(ws, ws_bytes, logra_precondition_ws_size(D, n_blocks, Q)));
-    hipError_t e = logra::launch_precondition(S, D, n_blocks, N, damp_ratio, g_test, in_dtype == LOGRA_BF16,
-                                              ld_in, Q, g_out, out_dtype == LOGRA_BF16, ld_out, ws, s);
+    hipError_t e = logra::launch_precondition(S, s_f64, D, n_blocks, N, damp_ratio, g_test, in_dtype, ld_in, Q,
+                                              g_out, out_dtype, ld_out, ws, s);
     if (e != hipSuccess) return hip_fail(e, "precondition launch");
     return report_not_pd(ws, D, n_blocks, s);
+}
+
+int logra_precondition_blocks(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
+                              const void *g_test, int in_dtype, int64_t ld_in, int Q, void *g_out,
+                              int out_dtype, int64_t ld_out, void *ws, size_t ws_bytes,
+                              void *stream) {
+    return precondition_impl(S, false, D, n_blocks, N, damp_ratio, g_test, in_dtype, ld_in, Q, g_out, out_dtype,
+                             ld_out, ws, ws_bytes, stream);
+}
+
+int logra_precondition_f64(const double *S, int D, int n_blocks, int64_t N, double damp_ratio, const void *g_test,
+                           int in_dtype, int64_t ld_in, int Q, void *g_out, int out_dtype, int64_t ld_out, void *ws,
+                           size_t ws_bytes, void *stream) {
+    return precondition_impl(S, true, D, n_blocks, N, damp_ratio, g_test, in_dtype, ld_in, Q, g_out, out_dtype,
+                             ld_out, ws, ws_bytes, stream);
 }
 
 int logra_precondition(const float *S, int D, int64_t N, double damp_ratio, const void *g_test,
@@ -281,8 +322,7 @@ static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, i
                           float *scores, int64_t ld_s, int topk, float *topk_val, int64_t *topk_idx, int merge,
                           const float *row_scale, const float *col_scale, void *ws, size_t ws_bytes,
                           void *stream) {
-    if (!valid_dtype(te_dtype) || !valid_dtype(tr_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
-    if (te_dtype != tr_dtype) return fail(LOGRA_ERR_UNSUPPORTED, "test and train dtypes must match");
+    TRY(check_score_dtypes(te_dtype, tr_dtype));
     if (Q < 0 || N_chunk < 0 || D <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need Q >= 0, N_chunk >= 0, D > 0");
     if (ld_te < D || ld_tr < D) return fail(LOGRA_ERR_INVALID_ARG, "ld_te and ld_tr must be >= D");
     if (topk < 0 || topk > LOGRA_MAX_TOPK) return fail(topk < 0 ? LOGRA_ERR_INVALID_ARG : LOGRA_ERR_UNSUPPORTED,
@@ -297,7 +337,7 @@ static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, i
         return fail(LOGRA_ERR_INVALID_ARG, "bf16 scores need D, ld_te, ld_tr multiples of 8");
     if (bf16 && (ld_te >= (int64_t{1} << 22) || ld_tr >= (int64_t{1} << 22)))
         return fail(LOGRA_ERR_UNSUPPORTED, "bf16 scores support ld_te, ld_tr < 4194304");
-    if (!bf16 && Q > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "fp32 scores support Q <= 65535");
+    if (!bf16 && Q > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "fp32 / fp64 scores support Q <= 65535");
     if (Q == 0) return ok();
     if (topk > 0) {
         TRY(check_dev(topk_val, "topk_val", 4));
@@ -311,8 +351,8 @@ static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, i
         }
         return ok();
     }
-    TRY(check_dev(g_test_pre, "g_test_pre", bf16 ? 16 : 4));
-    TRY(check_dev(g_train, "g_train", bf16 ? 16 : 4));
+    TRY(check_dev(g_test_pre, "g_test_pre", bf16 ? 16 : esize(te_dtype)));
+    TRY(check_dev(g_train, "g_train", bf16 ? 16 : esize(tr_dtype)));
     if (row_scale) TRY(check_dev(row_scale, "row_scale", 4));
     if (col_scale) TRY(check_dev(col_scale, "col_scale", 4));
     const logra::ScoreScale scale{row_scale, col_scale};
@@ -331,8 +371,8 @@ static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, i
     const hipStream_t s = static_cast<hipStream_t>(stream);
     const int64_t pre = (bf16 && topk > 0) ? logra::topk_prefix_rows(N_chunk, topk) : 0;
     if (pre == 0) {
-        hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, N_chunk, D, bf16, s_buf,
-                                            ld, nullptr, scale, s);
+        hipError_t e = logra::launch_scores(g_test_pre, te_dtype, ld_te, Q, g_train, tr_dtype, ld_tr, N_chunk, D,
+                                            s_buf, ld, nullptr, scale, s);
         if (e != hipSuccess) return hip_fail(e, "score launch");
         if (topk > 0) {
             e = logra::launch_topk(s_buf, ld, Q, N_chunk, train_base, topk, topk_val, topk_idx, merge != 0, s);
@@ -348,8 +388,8 @@ static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, i
     int *cnt = reinterpret_cast<int *>(wp + q4);
     float *cval = reinterpret_cast<float *>(wp + 2 * q4);
     int *cidx = reinterpret_cast<int *>(wp + 2 * q4 + round256(4 * static_cast<size_t>(Q) * logra::kCandCap));
-    hipError_t e = logra::launch_scores(g_test_pre, ld_te, Q, g_train, ld_tr, pre, D, true, s_buf, ld, nullptr,
-                                        scale, s);
+    hipError_t e = logra::launch_scores(g_test_pre, LOGRA_BF16, ld_te, Q, g_train, LOGRA_BF16, ld_tr, pre, D, s_buf,
+                                        ld, nullptr, scale, s);
     if (e != hipSuccess) return hip_fail(e, "score launch");
     e = logra::launch_topk(s_buf, ld, Q, pre, train_base, topk, topk_val, topk_idx, merge != 0, s);
     if (e != hipSuccess) return hip_fail(e, "top-k launch");
@@ -358,8 +398,8 @@ static int influence_impl(const void *g_test_pre, int te_dtype, int64_t ld_te, i
     const logra::ScoreFilter filt{thr, cnt, cval, cidx, logra::kCandCap};
     const void *tr_rest = static_cast<const uint16_t *>(g_train) + pre * ld_tr;
     const logra::ScoreScale scale_rest{row_scale, col_scale ? col_scale + pre : nullptr};
-    e = logra::launch_scores(g_test_pre, ld_te, Q, tr_rest, ld_tr, N_chunk - pre, D, true, s_buf + pre, ld,
-                             &filt, scale_rest, s);
+    e = logra::launch_scores(g_test_pre, LOGRA_BF16, ld_te, Q, tr_rest, LOGRA_BF16, ld_tr, N_chunk - pre, D,
+                             s_buf + pre, ld, &filt, scale_rest, s);
     if (e != hipSuccess) return hip_fail(e, "score launch");
     e = logra::launch_topk_filtered(s_buf + pre, ld, Q, N_chunk - pre, train_base + pre, topk, topk_val, topk_idx,
                                     cnt, cval, cidx, logra::kCandCap, s);
@@ -427,7 +467,7 @@ int logra_self_influence_blocks(const float *S, int D, int n_blocks, int64_t N, 
 // ---------------------------------------------------------------------------
 // Out-of-core scoring: the store in pinned host memory, streamed in chunks.
 size_t logra_influence_stream_ws_size(int Q, int64_t chunk_rows, int D, int tr_dtype, int topk) {
-    if (Q < 0 || chunk_rows <= 0 || D <= 0 || !valid_dtype(tr_dtype) || topk <= 0) return 0;
+    if (Q < 0 || chunk_rows <= 0 || D <= 0 || !valid_dtype64(tr_dtype) || topk <= 0) return 0;
     const size_t stage = round256(static_cast<size_t>(chunk_rows) * D * esize(tr_dtype));
     return 2 * stage + logra_influence_ws_size(Q, chunk_rows, topk, 0);
 }
@@ -436,8 +476,7 @@ int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, 
                            int tr_dtype, int64_t ld_tr, int64_t N, int D, int64_t chunk_rows, int topk,
                            float *topk_val, int64_t *topk_idx, void *ws, size_t ws_bytes, void *stream,
                            void *copy_stream) {
-    if (!valid_dtype(te_dtype) || !valid_dtype(tr_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
-    if (te_dtype != tr_dtype) return fail(LOGRA_ERR_UNSUPPORTED, "test and train dtypes must match");
+    TRY(check_score_dtypes(te_dtype, tr_dtype));
     if (Q < 0 || N < 0 || D <= 0 || chunk_rows <= 0)
         return fail(LOGRA_ERR_INVALID_ARG, "need Q >= 0, N >= 0, D > 0, chunk_rows > 0");
     if (topk <= 0) return fail(LOGRA_ERR_INVALID_ARG, "topk must be > 0");
@@ -448,7 +487,7 @@ int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, 
         return fail(LOGRA_ERR_INVALID_ARG, "bf16 scores need D and ld_te multiples of 8");
     if (Q == 0) return ok();
     const size_t es = esize(tr_dtype);
-    if (N > 0) TRY(check_pinned(g_train_host, "g_train_host", es == 2 ? 16 : 4));
+    if (N > 0) TRY(check_pinned(g_train_host, "g_train_host", es == 2 ? 16 : es));
     TRY(check_dev(topk_val, "topk_val", 4));
     TRY(check_dev(topk_idx, "topk_idx", 8));
     const size_t need = logra_influence_stream_ws_size(Q, chunk_rows, D, tr_dtype, topk);

@@ -111,6 +111,8 @@ template <>
 __device__ __forceinline__ void store_out_d<bf16_bits>(bf16_bits *p, double v) {
     *p = f32_to_bf16_rne(static_cast<float>(v));
 }
+template <>
+__device__ __forceinline__ void store_out_d<double>(double *p, double v) { *p = v; }
 
 template <typename T>
 __device__ __forceinline__ double load_in_d(const T *p);
@@ -120,6 +122,8 @@ template <>
 __device__ __forceinline__ double load_in_d<bf16_bits>(const bf16_bits *p) {
     return static_cast<double>(bf16_to_f32(*p));
 }
+template <>
+__device__ __forceinline__ double load_in_d<double>(const double *p) { return *p; }
 
 // Matrix-core products.  Operand layouts of the 16x16 shapes: lane l holds
 // row (l % 16) of A and column (l % 16) of B, with the contraction slice

@@ -7,7 +7,9 @@
 // are read with 128-bit coalesced loads and written transposed into LDS
 // ([column][example]), from where each lane reads its 8 consecutive examples
 // as one MFMA operand (16x16x32 bf16, fp32 accumulation).  fp32 inputs use a
-// plain fp32 FMA loop.  The tile is then added to S (coalesced
+// plain fp32 FMA loop.  The fp64 form (S in float64, for fp32 or fp64 rows)
+// forms every product and sum in float64: a product of two fp32 values is
+// exact there.  The tile is then added to S (coalesced
 // read-modify-write of the upper tile) and written mirrored to the lower
 // tile through LDS, so S stays exactly symmetric.
 #include "common.h"
@@ -32,14 +34,15 @@ __device__ __forceinline__ void tile_coords(int t, int nt, int &ti, int &tj) {
 
 // Add the computed 64x64 tile c (LDS, row-major with stride CT+1) into S and
 // mirror it.  Diagonal tiles only use entries r <= c of the upper triangle.
-__device__ __forceinline__ void add_and_mirror(float *S, int D, int I, int J, float *ct, bool diag) {
+template <typename TS>
+__device__ __forceinline__ void add_and_mirror(TS *S, int D, int I, int J, TS *ct, bool diag) {
     const int tid = threadIdx.x;
     for (int e = tid; e < CT * CT; e += blockDim.x) {
         const int r = e / CT, c = e - (e / CT) * CT;
         const int i = I + r, j = J + c;
         if (i < D && j < D && (!diag || r <= c)) {
-            float *p = S + static_cast<size_t>(i) * D + j;
-            const float v = *p + ct[r * (CT + 1) + c];
+            TS *p = S + static_cast<size_t>(i) * D + j;
+            const TS v = *p + ct[r * (CT + 1) + c];
             *p = v;
             ct[r * (CT + 1) + c] = v;
         }
@@ -132,6 +135,33 @@ __global__ __launch_bounds__(256) void k_cov_f32(const float *g, int64_t ld, int
     add_and_mirror(S, D, I, J, ct, diag);
 }
 
+// float64 statistics: rows of fp32 or fp64, every product and sum in float64.
+template <typename TG>
+__global__ __launch_bounds__(256) void k_cov_f64(const TG *g, int64_t ld, int B, int D, int nt,
+                                                 double *S_all) {
+    __shared__ double ct[CT * (CT + 1)];
+    const int blk = blockIdx.y;
+    int ti, tj;
+    tile_coords(blockIdx.x, nt, ti, tj);
+    const int I = ti * CT, J = tj * CT;
+    const bool diag = ti == tj;
+    const TG *gb = g + static_cast<size_t>(blk) * D;
+    double *S = S_all + static_cast<size_t>(blk) * D * D;
+    for (int e = threadIdx.x; e < CT * CT; e += blockDim.x) {
+        const int r = e / CT, c = e - (e / CT) * CT;
+        const int i = I + r, j = J + c;
+        double s = 0.0;
+        if (i < D && j < D)
+            for (int b = 0; b < B; ++b) {
+                const TG *rowp = gb + static_cast<int64_t>(b) * ld;
+                s = fma(load_in_d<TG>(rowp + i), load_in_d<TG>(rowp + j), s);
+            }
+        ct[r * (CT + 1) + c] = s;
+    }
+    __syncthreads();
+    add_and_mirror(S, D, I, J, ct, diag);
+}
+
 }  // namespace
 
 hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S,
@@ -144,6 +174,20 @@ hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_
                            D, nt, S);
     else
         hipLaunchKernelGGL(k_cov_f32, grid, dim3(256), 0, s, static_cast<const float *>(g), ld, B, D,
+                           nt, S);
+    return hipGetLastError();
+}
+
+hipError_t launch_cov_f64(const void *g, bool f64_rows, int64_t ld, int B, int D, int n_blocks, double *S,
+                          hipStream_t s) {
+    if (B == 0 || n_blocks == 0) return hipSuccess;
+    const int nt = (D + CT - 1) / CT;
+    const dim3 grid(static_cast<unsigned>(nt * (nt + 1) / 2), static_cast<unsigned>(n_blocks));
+    if (f64_rows)
+        hipLaunchKernelGGL(k_cov_f64<double>, grid, dim3(256), 0, s, static_cast<const double *>(g), ld, B, D,
+                           nt, S);
+    else
+        hipLaunchKernelGGL(k_cov_f64<float>, grid, dim3(256), 0, s, static_cast<const float *>(g), ld, B, D,
                            nt, S);
     return hipGetLastError();
 }

@@ -7,6 +7,7 @@
 namespace logra {
 
 typedef uint16_t bf16_bits_t;   // a bf16 value as its bit pattern
+enum DtypeCode { kF32 = 0, kBF16 = 1, kF64 = 2 };   // element types, numbered as in the C ABI
 constexpr int kMaxGroup = 16;   // layers per grouped projection launch
 constexpr int kMaxK = 128;
 constexpr int kMaxTopk = 1024;
@@ -37,19 +38,23 @@ size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, 
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
                           int k_in, int k_out, bool bf16_out, int64_t g_ld, void *ws, hipStream_t s);
 
-// Covariance S_l += G_l^T G_l for n_blocks column blocks of width D.
+// Covariance S_l += G_l^T G_l for n_blocks column blocks of width D; the
+// _f64 form keeps S in float64 (rows fp32, or fp64 when f64_rows).
 hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S,
                       hipStream_t s);
+hipError_t launch_cov_f64(const void *g, bool f64_rows, int64_t ld, int B, int D, int n_blocks, double *S,
+                          hipStream_t s);
 
 // Damped Cholesky preconditioning of n_blocks blocks.  Writes a per-block
 // status word into the workspace; precond_info_ptr() locates it.
 size_t precond_ws_bytes(int D, int n_blocks, int Q);
 int *precond_info_ptr(void *ws, int D, int n_blocks);
-hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
-                               const void *g_test, bool bf16_in, int64_t ld_in, int Q, void *g_out,
-                               bool bf16_out, int64_t ld_out, void *ws, hipStream_t s);
-hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int rows, int cols,
-                            void *dst, bool bf16_out, int64_t ld_out, hipStream_t s);
+// S is fp32, or fp64 when s_f64; in_dt / out_dt are DtypeCode values.
+hipError_t launch_precondition(const void *S, bool s_f64, int D, int n_blocks, int64_t N, double damp_ratio,
+                               const void *g_test, int in_dt, int64_t ld_in, int Q, void *g_out, int out_dt,
+                               int64_t ld_out, void *ws, hipStream_t s);
+hipError_t launch_copy_rows(const void *src, int in_dt, int64_t ld_in, int rows, int cols,
+                            void *dst, int out_dt, int64_t ld_out, hipStream_t s);
 
 // Self-influence (l-RelatIF's normaliser): per block, W = L^{-1} of the
 // damped covariance's Cholesky factor (identity when damp_ratio < 0), kept as
@@ -99,8 +104,10 @@ struct ScoreScale {
     const float *row;
     const float *col;
 };
-hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
-                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, const ScoreFilter *filt,
+// te_dt / tr_dt: both kBF16 (bf16 MFMA), or each kF32 or kF64 (float64
+// accumulation, no filter).
+hipError_t launch_scores(const void *te, int te_dt, int64_t ld_te, int Q, const void *tr, int tr_dt,
+                         int64_t ld_tr, int64_t N, int D, float *s, int64_t ld_s, const ScoreFilter *filt,
                          const ScoreScale &scale, hipStream_t st);
 // Rows of a chunk scored and selected exactly before candidate filtering
 // starts (their running top-k sets the thresholds); 0 = no filtering.

@@ -4,7 +4,7 @@
 //   C = S / N,  lambda = r * tr(C) / D   (r x mean eigenvalue, App. C)
 //   out_q = (C + lambda I)^{-1} g_q
 //
-// All arithmetic is float64.  Steps, each batched over layer blocks
+// All arithmetic is float64; S may be given in fp32 or fp64.  Steps, each batched over layer blocks
 // (blockIdx.y):
 //   1. lambda per block (fixed-order tree sum of the diagonal);
 //   2. A = S/N + lambda I into the workspace (lower triangle);
@@ -57,13 +57,14 @@ inline WsLayout ws_layout(void *ws, int D, int n_blocks, int Q) {
     return w;
 }
 
-__global__ __launch_bounds__(256) void k_lambda(const float *S, int D, int64_t N, double r,
+template <typename TS>
+__global__ __launch_bounds__(256) void k_lambda(const TS *S, int D, int64_t N, double r,
                                                 double *lam) {
     __shared__ double part[256];
     const int blk = blockIdx.x;
-    const float *Sb = S + static_cast<size_t>(blk) * D * D;
+    const TS *Sb = S + static_cast<size_t>(blk) * D * D;
     double s = 0.0;
-    for (int d = threadIdx.x; d < D; d += 256) s += static_cast<double>(Sb[static_cast<size_t>(d) * D + d]);
+    for (int d = threadIdx.x; d < D; d += 256) s += load_in_d<TS>(Sb + static_cast<size_t>(d) * D + d);
     part[threadIdx.x] = s;
     __syncthreads();
     for (int w = 128; w > 0; w >>= 1) {
@@ -73,14 +74,15 @@ __global__ __launch_bounds__(256) void k_lambda(const float *S, int D, int64_t N
     if (threadIdx.x == 0) lam[blk] = r * (part[0] / static_cast<double>(N)) / static_cast<double>(D);
 }
 
-__global__ __launch_bounds__(256) void k_form(const float *S, int D, int64_t N, const double *lam,
+template <typename TS>
+__global__ __launch_bounds__(256) void k_form(const TS *S, int D, int64_t N, const double *lam,
                                               double *A, int *info) {
     const int blk = blockIdx.y, i = blockIdx.x;
-    const float *Sr = S + (static_cast<size_t>(blk) * D + i) * D;
+    const TS *Sr = S + (static_cast<size_t>(blk) * D + i) * D;
     double *Ar = A + (static_cast<size_t>(blk) * D + i) * D;
     const double inv = 1.0 / static_cast<double>(N);
     for (int j = threadIdx.x; j <= i; j += 256) {
-        double v = static_cast<double>(Sr[j]) * inv;
+        double v = load_in_d<TS>(Sr + j) * inv;
         if (j == i) v += lam[blk];
         Ar[j] = v;
     }
@@ -482,27 +484,48 @@ size_t precond_ws_bytes(int D, int n_blocks, int Q) {
 
 int *precond_info_ptr(void *ws, int D, int n_blocks) { return ws_layout(ws, D, n_blocks, 0).info; }
 
-hipError_t launch_copy_rows(const void *src, bool bf16_in, int64_t ld_in, int rows, int cols,
-                            void *dst, bool bf16_out, int64_t ld_out, hipStream_t s) {
+namespace {
+// Dispatch over the element types of an input and an output (dtype codes).
+template <typename F>
+hipError_t with_types(int in_dt, int out_dt, F &&f) {
+    auto out = [&](auto in_tag) -> hipError_t {
+        using TI = decltype(in_tag);
+        if (out_dt == kBF16) return f(TI{}, bf16_bits{});
+        if (out_dt == kF64) return f(TI{}, double{});
+        return f(TI{}, float{});
+    };
+    if (in_dt == kBF16) return out(bf16_bits{});
+    if (in_dt == kF64) return out(double{});
+    return out(float{});
+}
+}  // namespace
+
+hipError_t launch_copy_rows(const void *src, int in_dt, int64_t ld_in, int rows, int cols,
+                            void *dst, int out_dt, int64_t ld_out, hipStream_t s) {
     if (rows == 0 || cols == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(min((cols + 255) / 256, 64)), static_cast<unsigned>(rows));
-    if (bf16_in && bf16_out)
-        hipLaunchKernelGGL((k_copy_rows<bf16_bits, bf16_bits>), grid, dim3(256), 0, s, static_cast<const bf16_bits *>(src), ld_in, cols, static_cast<bf16_bits *>(dst), ld_out);
-    else if (bf16_in)
-        hipLaunchKernelGGL((k_copy_rows<bf16_bits, float>), grid, dim3(256), 0, s, static_cast<const bf16_bits *>(src), ld_in, cols, static_cast<float *>(dst), ld_out);
-    else if (bf16_out)
-        hipLaunchKernelGGL((k_copy_rows<float, bf16_bits>), grid, dim3(256), 0, s, static_cast<const float *>(src), ld_in, cols, static_cast<bf16_bits *>(dst), ld_out);
-    else
-        hipLaunchKernelGGL((k_copy_rows<float, float>), grid, dim3(256), 0, s, static_cast<const float *>(src), ld_in, cols, static_cast<float *>(dst), ld_out);
-    return hipGetLastError();
+    return with_types(in_dt, out_dt, [&](auto ti, auto to) {
+        using TI = decltype(ti);
+        using TO = decltype(to);
+        hipLaunchKernelGGL((k_copy_rows<TI, TO>), grid, dim3(256), 0, s, static_cast<const TI *>(src), ld_in,
+                           cols, static_cast<TO *>(dst), ld_out);
+        return hipGetLastError();
+    });
 }
 
-hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
-                               const void *g_test, bool bf16_in, int64_t ld_in, int Q, void *g_out,
-                               bool bf16_out, int64_t ld_out, void *ws, hipStream_t s) {
+hipError_t launch_precondition(const void *S, bool s_f64, int D, int n_blocks, int64_t N, double damp_ratio,
+                               const void *g_test, int in_dt, int64_t ld_in, int Q, void *g_out, int out_dt,
+                               int64_t ld_out, void *ws, hipStream_t s) {
     const WsLayout w = ws_layout(ws, D, n_blocks, Q);
-    hipLaunchKernelGGL(k_lambda, dim3(n_blocks), dim3(256), 0, s, S, D, N, damp_ratio, w.lam);
-    hipLaunchKernelGGL(k_form, dim3(D, n_blocks), dim3(256), 0, s, S, D, N, w.lam, w.A, w.info);
+    if (s_f64) {
+        const double *Sd = static_cast<const double *>(S);
+        hipLaunchKernelGGL(k_lambda<double>, dim3(n_blocks), dim3(256), 0, s, Sd, D, N, damp_ratio, w.lam);
+        hipLaunchKernelGGL(k_form<double>, dim3(D, n_blocks), dim3(256), 0, s, Sd, D, N, w.lam, w.A, w.info);
+    } else {
+        const float *Sf = static_cast<const float *>(S);
+        hipLaunchKernelGGL(k_lambda<float>, dim3(n_blocks), dim3(256), 0, s, Sf, D, N, damp_ratio, w.lam);
+        hipLaunchKernelGGL(k_form<float>, dim3(D, n_blocks), dim3(256), 0, s, Sf, D, N, w.lam, w.A, w.info);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     for (int k0 = 0; k0 < D; k0 += NB) {
@@ -517,10 +540,9 @@ hipError_t launch_precondition(const float *S, int D, int n_blocks, int64_t N, d
         if (e != hipSuccess) return e;
     }
     if (Q == 0) return hipSuccess;
-    if (bf16_in && bf16_out) return launch_solve<bf16_bits, bf16_bits>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
-    if (bf16_in) return launch_solve<bf16_bits, float>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
-    if (bf16_out) return launch_solve<float, bf16_bits>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
-    return launch_solve<float, float>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+    return with_types(in_dt, out_dt, [&](auto ti, auto to) {
+        return launch_solve<decltype(ti), decltype(to)>(w, D, n_blocks, g_test, ld_in, Q, g_out, ld_out, s);
+    });
 }
 
 hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N, double damp_ratio,
@@ -530,8 +552,8 @@ hipError_t launch_inverse_factor(const float *S, int D, int n_blocks, int64_t N,
     const bool ident = damp_ratio < 0;
     if (!ident) {
         // factor (status words as for the preconditioner), then L^{-1} = forward solve of I
-        const hipError_t e = launch_precondition(S, D, n_blocks, N, damp_ratio, nullptr, false, D, 0, nullptr,
-                                                 false, D, ws, s);
+        const hipError_t e = launch_precondition(S, false, D, n_blocks, N, damp_ratio, nullptr, kF32, D, 0,
+                                                 nullptr, kF32, D, ws, s);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(k_diag_inv, dim3(tiles_of(D), n_blocks), dim3(64), 0, s, w.A, D, w.Linv);
         const dim3 grid(static_cast<unsigned>(padded_q(D) / NB), static_cast<unsigned>(n_blocks));

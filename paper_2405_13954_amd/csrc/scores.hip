@@ -1,21 +1,18 @@
 // Influence scores and per-query top-k (Sec. 2 Eq. (2) step (2); top-k most
 // valuable training data, Sec. 4.1).
 //
-//   s[q][j] = sum_d te[q][d] * tr[j][d]      (fp32 accumulation)
+//   s[q][j] = sum_d te[q][d] * tr[j][d]      (fp32 result)
 //
-// Score GEMM (bf16): one workgroup per 256 x 256 output tile; 4 waves, each
+// Score GEMM (bf16, fp32 accumulation): one workgroup per 256 x 256 output tile; 4 waves, each
 // owning a 128 x 128 quadrant as 4 x 4 blocks of 32x32x16 bf16 MFMAs (256
 // fp32 accumulators per lane), 64 contraction columns (one slab) per step.
 // Tiles are ordered so that the workgroups sharing one 256-row train slab are
 // dispatched together onto the same XCD (dispatch round-robins workgroups
 // over the 8 XCDs), so the slab is fetched from HBM once into that XCD's L2.
-// Two main loops:
-//  - k_scores_dma (default): operands copied straight from memory into an
-//    LDS ring with gfx950's buffer_load ... lds, no register staging; the
-//    issue order of MFMAs, copies and fragment reads is fixed by hand.
-//  - k_scores_bf16: slabs staged through registers two steps ahead and
-//    stored into two LDS buffers.
-// Both compute the same sums in the same order.
+// Operands are copied straight from memory into an LDS ring with gfx950's
+// buffer_load ... lds (no register staging); the issue order of MFMAs,
+// copies and fragment reads is fixed by hand.  fp32 / fp64 operands take a
+// float64-accumulating tiled kernel.
 //
 // Top-k: one workgroup per query row.  An exact radix select (four 8-bit
 // passes over order-preserving keys) finds the k-th largest score; when more
@@ -34,34 +31,9 @@
 namespace logra {
 namespace {
 
-#ifndef LOGRA_SC_SCHED
-#define LOGRA_SC_SCHED 1   // interleave loads with the MFMA stream (scheduling hints)
-#endif
-#ifndef LOGRA_SC_NT
-#define LOGRA_SC_NT 0      // non-temporal hint on the train-operand loads
-#endif
-#ifndef LOGRA_SC_DMA_NT
-#define LOGRA_SC_DMA_NT 1  // non-temporal hint on k_scores_dma's train-operand copies
-#endif
-#ifndef LOGRA_SC_DMA
-#define LOGRA_SC_DMA 1     // 1: operands copied straight into LDS (k_scores_dma)
-#endif
-
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int LDR = BK + 8;       // padded LDS row (bf16 elements): 144 bytes
 constexpr int GT = 256;           // GEMM threads
-constexpr int kLoads = BM * BK / 8 / GT;   // 128-bit loads per operand and thread per slab
 constexpr int kXcd = 8;
-
-// One slab (BK columns) of both operands in flight, 128 bits per load.
-struct Slab {
-    u32x4 a[kLoads];
-    u32x4 b[kLoads];
-};
-
-// scheduling-group masks of __builtin_amdgcn_sched_group_barrier
-constexpr int kSchedMfma = 0x008, kSchedVmemRead = 0x020, kSchedDsRead = 0x100,
-              kSchedDsWrite = 0x200;
 
 // Epilogue of a 256 x 256 tile: the fp32 scores, times the optional row and
 // column scales (s * row_scale[q] * col_scale[j], for normalised scores), go
@@ -153,154 +125,10 @@ __device__ __forceinline__ void store_scores(const f32x16 (&acc)[4][4], float *l
         }
 }
 
-__global__ __launch_bounds__(GT, 1) void k_scores_bf16(const bf16_bits *__restrict__ te, int64_t ld_te,
-                                                       int Q, const bf16_bits *__restrict__ tr,
-                                                       int64_t ld_tr, int64_t N, int D,
-                                                       float *__restrict__ s, int64_t ld_s,
-                                                       int m_tiles, int n_tiles, ScoreFilter filt,
-                                                       ScoreScale scale) {
-    __shared__ __attribute__((aligned(16))) bf16_bits As[2][BM * LDR];
-    __shared__ __attribute__((aligned(16))) bf16_bits Bs[2][BN * LDR];
-
-    // XCD-aware tile order: consecutive workgroups on one XCD share a train slab.
-    const int bid = blockIdx.x;
-    const int xcd = bid % kXcd, local = bid / kXcd;
-    const int mt = local % m_tiles;
-    const int nt = (local / m_tiles) * kXcd + xcd;
-    if (nt >= n_tiles) return;
-    const int m0 = mt * BM;
-    const int64_t n0 = static_cast<int64_t>(nt) * BN;
-    const int rows_a = Q - m0 < BM ? Q - m0 : BM;
-    const int rows_b = N - n0 < BN ? static_cast<int>(N - n0) : BN;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-
-    // Buffer resources over this tile's rows (the host bounds rows * ld * 2 below
-    // 2^31).  Load i of a thread covers row srow + 32 i, columns scol..scol+7 of
-    // the slab; rows past the operand and columns past D read as zeros.
-    const auto rsa = buf_rsrc_uniform(te + static_cast<int64_t>(m0) * ld_te,
-                                      static_cast<uint32_t>(rows_a * ld_te * 2));
-    const auto rsb = buf_rsrc_uniform(tr + n0 * ld_tr, static_cast<uint32_t>(rows_b * ld_tr * 2));
-    const int srow = tid >> 3, scol = 8 * (tid & 7);
-    uint32_t oa[kLoads], ob[kLoads];
-#pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-        const int r = srow + 32 * i;
-        oa[i] = r < rows_a ? static_cast<uint32_t>((r * ld_te + scol) * 2) : kBufOOB;
-        ob[i] = r < rows_b ? static_cast<uint32_t>((r * ld_tr + scol) * 2) : kBufOOB;
-    }
-    auto gload = [&](Slab &st, int k0) {
-        const bool kin = k0 + scol < D;
-        const uint32_t dk = static_cast<uint32_t>(k0) * 2u;
-#pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
-            st.a[i] = buf_ld128(rsa, kin ? oa[i] + dk : kBufOOB);
-#if LOGRA_SC_NT
-            st.b[i] = buf_ld128_nt(rsb, kin ? ob[i] + dk : kBufOOB);
-#else
-            st.b[i] = buf_ld128(rsb, kin ? ob[i] + dk : kBufOOB);
-#endif
-        }
-    };
-    auto lstore = [&](const Slab &st, int buf) {
-#pragma unroll
-        for (int i = 0; i < kLoads; ++i) {
-            *reinterpret_cast<u32x4 *>(&As[buf][(srow + 32 * i) * LDR + scol]) = st.a[i];
-            *reinterpret_cast<u32x4 *>(&Bs[buf][(srow + 32 * i) * LDR + scol]) = st.b[i];
-        }
-    };
-
-    f32x16 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-    // Operand fragments: lane l reads row l % 32, contraction columns
-    // 8 (l / 32) .. +8 of each 16-wide step.
-    const int frow = lane & 31, fk = 8 * (lane >> 5);
-    bf16x8 fa[2][4], fb[2][4];
-    auto ldfrag = [&](int f, int buf, int ks) {
-        const bf16_bits *Ab = &As[buf][(wm * 128 + frow) * LDR + fk + 16 * ks];
-        const bf16_bits *Bb = &Bs[buf][(wn * 128 + frow) * LDR + fk + 16 * ks];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            fa[f][i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Ab + i * 32 * LDR));
-            fb[f][i] = as_bf16x8(*reinterpret_cast<const u32x4 *>(Bb + i * 32 * LDR));
-        }
-    };
-    auto mfma_step = [&](int f) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[i][j] = mfma32_bf16(fa[f][i], fb[f][j], acc[i][j]);
-    };
-
-    // One slab per half-step.  On entry LDS buffer `buf` holds slab kt and
-    // `next` holds slab kt+1 in flight.  The half-step starts the loads of slab
-    // kt+2 into `fill`, multiplies slab kt out of LDS (four 16-wide steps,
-    // each step's fragments read while the previous step multiplies), stores
-    // slab kt+1 into the other buffer and ends with the barrier.
-    auto half = [&](int buf, Slab &fill, int kfill, const Slab &next) {
-        gload(fill, kfill);
-        ldfrag(0, buf, 0);
-        ldfrag(1, buf, 1);
-        mfma_step(0);
-        ldfrag(0, buf, 2);
-        mfma_step(1);
-        ldfrag(1, buf, 3);
-        mfma_step(0);
-        lstore(next, buf ^ 1);
-        mfma_step(1);
-#if LOGRA_SC_SCHED
-        // first fragments, then the 16 global loads over the first 32 MFMAs,
-        // 8 fragment reads over each of the first three steps and the 16 LDS
-        // stores over the last
-        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 8, 0);
-#pragma unroll
-        for (int ks = 0; ks < 3; ++ks) {
-#pragma unroll
-            for (int g = 0; g < 8; ++g) {
-                __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
-                if (ks < 2) __builtin_amdgcn_sched_group_barrier(kSchedVmemRead, 1, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 8, 0);
-        }
-#pragma unroll
-        for (int g = 0; g < 16; ++g) {
-            __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(kSchedDsWrite, 1, 0);
-        }
-#endif
-        __syncthreads();
-    };
-
-    // The slab count is rounded up to even; slabs past D load as zeros.
-    const int nk = (D + BK - 1) / BK;
-    const int nk2 = nk + (nk & 1);
-    Slab s0, s1;
-    gload(s0, 0);
-    gload(s1, BK);
-    lstore(s0, 0);
-    __syncthreads();
-    for (int kt = 0; kt < nk2; kt += 2) {
-        half(0, s0, (kt + 2) * BK, s1);
-        half(1, s1, (kt + 3) * BK, s0);
-    }
-
-    store_scores(acc, reinterpret_cast<float *>(&As[0][0]), s, ld_s, m0, n0, rows_a, rows_b, wm, wn,
-                 tid, lane, filt, scale);   // LDS is free after the last barrier
-}
-
 // ------------------------------------------------------------------------
 // Score GEMM with asynchronous global->LDS copies (gfx950 buffer_load ... lds).
-// Same tile, waves, MFMA shape and 64-column slabs as above, but the operands
-// travel from memory straight into LDS (no register staging, no LDS store
-// instructions).  The LDS ring holds three slabs of the train operand, which
+// The operands travel from memory straight into LDS (no register staging, no
+// LDS store instructions).  The LDS ring holds three slabs of the train operand, which
 // streams from HBM and is copied two slabs ahead, and two slabs of the test
 // operand, which the L2 mostly serves and is copied one slab ahead
 // (3 x 32 KB + 2 x 32 KB = 160 KB).  The train copies carry the
@@ -439,12 +267,8 @@ __global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restric
                 mfma1(f, 2 * g + 1);
                 if (ks == 0)
                     copy_to_lds(rsa, ((g & 1) ? ka1 : ka0) ? oa[g] + dka : kBufOOB, la + g * 1024);
-                else if (ks == 1) {
-                    if (LOGRA_SC_DMA_NT)
-                        copy_to_lds_nt(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
-                    else
-                        copy_to_lds(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
-                }
+                else if (ks == 1)
+                    copy_to_lds_nt(rsb, ((g & 1) ? kb1 : kb0) ? ob[g] + dkb : kBufOOB, lb + g * 1024);
                 ldfrag1(f ^ 1, abase, bbase, ks + 1, g);
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -469,20 +293,63 @@ __global__ __launch_bounds__(GT, 1) void k_scores_dma(const bf16_bits *__restric
                  lane, filt, scale);
 }
 
-// fp32 scores (small problems): one thread per score, sequential contraction.
-__global__ __launch_bounds__(256) void k_scores_f32(const float *te, int64_t ld_te, int Q,
-                                                    const float *tr, int64_t ld_tr, int64_t N, int D,
-                                                    float *s, int64_t ld_s, ScoreScale scale) {
-    const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    const int q = blockIdx.y;
-    if (j >= N) return;
-    const float *a = te + static_cast<int64_t>(q) * ld_te;
-    const float *b = tr + j * ld_tr;
-    float acc = 0.f;
-    for (int d = 0; d < D; ++d) acc = __builtin_fmaf(a[d], b[d], acc);
-    if (scale.row) acc *= scale.row[q];
-    if (scale.col) acc *= scale.col[j];
-    s[static_cast<int64_t>(q) * ld_s + j] = acc;
+// fp32 / fp64 operands: every product and sum in float64 (a product of two
+// fp32 values is exact there), the result rounded once to fp32.  One 64 x 64
+// output tile per workgroup; 16-column slabs of both operands are staged
+// through LDS as float64 (coalesced row reads, transposed stores), and each
+// thread accumulates a 4 x 4 block over the whole contraction in order d =
+// 0, 1, ..., D-1.  Scales (normalised scores) multiply in float64 before the
+// rounding.
+constexpr int FT = 64, FK = 16;
+template <typename TA, typename TB>
+__global__ __launch_bounds__(256) void k_scores_f64acc(const TA *te, int64_t ld_te, int Q, const TB *tr,
+                                                       int64_t ld_tr, int64_t N, int D, float *s, int64_t ld_s,
+                                                       ScoreScale scale) {
+    __shared__ double As[FK][FT + 1];   // [column][query]
+    __shared__ double Bs[FK][FT + 1];   // [column][train row]
+    const int q0 = blockIdx.y * FT;
+    const int64_t j0 = static_cast<int64_t>(blockIdx.x) * FT;
+    const int tid = threadIdx.x, ta = tid >> 4, tb = tid & 15;
+    double acc[4][4] = {};
+    for (int k0 = 0; k0 < D; k0 += FK) {
+#pragma unroll
+        for (int u = 0; u < FT * FK / 256; ++u) {
+            const int e = tid + 256 * u, r = e / FK, c = e % FK, d = k0 + c;
+            const int q = q0 + r;
+            const int64_t j = j0 + r;
+            As[c][r] = (q < Q && d < D) ? load_in_d<TA>(te + static_cast<int64_t>(q) * ld_te + d) : 0.0;
+            Bs[c][r] = (j < N && d < D) ? load_in_d<TB>(tr + j * ld_tr + d) : 0.0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < FK; ++c) {
+            double x[4], y[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                x[u] = As[c][4 * ta + u];
+                y[u] = Bs[c][tb + 16 * u];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fma(x[u], y[v], acc[u][v]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int q = q0 + 4 * ta + u;
+        if (q >= Q) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t j = j0 + tb + 16 * v;   // consecutive threads: consecutive columns
+            if (j >= N) continue;
+            double val = acc[u][v];
+            if (scale.row) val *= static_cast<double>(scale.row[q]);
+            if (scale.col) val *= static_cast<double>(scale.col[j]);
+            s[static_cast<int64_t>(q) * ld_s + j] = static_cast<float>(val);
+        }
+    }
 }
 
 // ---------------------------------------------------------------- top-k --
@@ -740,27 +607,32 @@ __global__ __launch_bounds__(KT_THREADS) void k_topk_filtered(
 
 }  // namespace
 
-hipError_t launch_scores(const void *te, int64_t ld_te, int Q, const void *tr, int64_t ld_tr,
-                         int64_t N, int D, bool bf16, float *s, int64_t ld_s, const ScoreFilter *filt,
+hipError_t launch_scores(const void *te, int te_dt, int64_t ld_te, int Q, const void *tr, int tr_dt,
+                         int64_t ld_tr, int64_t N, int D, float *s, int64_t ld_s, const ScoreFilter *filt,
                          const ScoreScale &scale, hipStream_t st) {
     if (Q == 0 || N == 0) return hipSuccess;
-    if (bf16) {
+    if (te_dt == kBF16 && tr_dt == kBF16) {
         const int m_tiles = (Q + BM - 1) / BM;
         const int n_tiles = static_cast<int>((N + BN - 1) / BN);
         const int n_groups = (n_tiles + kXcd - 1) / kXcd;
         const unsigned grid = static_cast<unsigned>(kXcd) * n_groups * m_tiles;
         const ScoreFilter none{nullptr, nullptr, nullptr, nullptr, 0};
-        hipLaunchKernelGGL(LOGRA_SC_DMA ? k_scores_dma : k_scores_bf16, dim3(grid), dim3(GT), 0, st,
-                           static_cast<const bf16_bits *>(te), ld_te, Q,
+        hipLaunchKernelGGL(k_scores_dma, dim3(grid), dim3(GT), 0, st, static_cast<const bf16_bits *>(te), ld_te, Q,
                            static_cast<const bf16_bits *>(tr), ld_tr, N, D, s, ld_s, m_tiles, n_tiles,
                            filt ? *filt : none, scale);
-    } else {
-        if (filt) return hipErrorInvalidValue;   // candidate filtering is a bf16-path feature
-        const dim3 grid(static_cast<unsigned>((N + 255) / 256), static_cast<unsigned>(Q));
-        hipLaunchKernelGGL(k_scores_f32, grid, dim3(256), 0, st, static_cast<const float *>(te), ld_te,
-                           Q, static_cast<const float *>(tr), ld_tr, N, D, s, ld_s, scale);
+        return hipGetLastError();
     }
-    return hipGetLastError();
+    if (filt || te_dt == kBF16 || tr_dt == kBF16) return hipErrorInvalidValue;   // bf16 pairs only with bf16
+    const dim3 grid(static_cast<unsigned>((N + FT - 1) / FT), static_cast<unsigned>((Q + FT - 1) / FT));
+    auto go = [&](auto a, auto b) {
+        using TA = decltype(a);
+        using TB = decltype(b);
+        hipLaunchKernelGGL((k_scores_f64acc<TA, TB>), grid, dim3(256), 0, st, static_cast<const TA *>(te), ld_te, Q,
+                           static_cast<const TB *>(tr), ld_tr, N, D, s, ld_s, scale);
+        return hipGetLastError();
+    };
+    if (te_dt == kF64) return tr_dt == kF64 ? go(double{}, double{}) : go(double{}, float{});
+    return tr_dt == kF64 ? go(float{}, double{}) : go(float{}, float{});
 }
 
 int64_t topk_prefix_rows(int64_t N, int k) {

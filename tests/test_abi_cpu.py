@@ -206,3 +206,35 @@ def test_offload_rows_validation(L):
     assert f(*args(ld_dst=63)) == P.ERR_INVALID_ARG
     assert f(*args(rows=0)) == P.OK                       # nothing to copy: no pointer is looked at
     assert f(*args()) == P.ERR_INVALID_ARG                 # NULL src
+
+
+def test_f64_statistics_validation(L):
+    """The float64 statistics path: fp64 S, fp64 preconditioned gradients and
+    float64-accumulated scores are accepted where documented, and refused
+    elsewhere."""
+    assert proj(L, g_dtype=P.F64) == P.ERR_INVALID_ARG        # projections store fp32 or bf16
+    assert proj(L, in_dtype=P.F64) == P.ERR_INVALID_ARG
+    c = L.logra_cov_accumulate_f64
+    assert c(None, P.BF16, 64, 4, 64, 1, None, None) == P.ERR_INVALID_ARG   # fp32 / fp64 rows only
+    assert c(None, P.F32, 100, 4, 64, 2, None, None) == P.ERR_INVALID_ARG   # ld < D * n_blocks
+    assert c(None, P.F32, 64, 4, 64, 0, None, None) == P.ERR_INVALID_ARG
+    assert c(None, P.F64, 64 * 65536, 4, 64, 65536, None, None) == P.ERR_UNSUPPORTED
+    assert c(None, P.F64, 64, 0, 64, 1, None, None) == P.OK                 # B = 0: a no-op
+    assert L.logra_cov_accumulate(None, P.F64, 64, 4, 64, None, None) == P.ERR_INVALID_ARG  # fp32 S
+    p = L.logra_precondition_f64
+    assert p(None, 8193, 1, 4, 0.1, None, P.F32, 8193, 1, None, P.F64, 8193, None, 0, None) == P.ERR_UNSUPPORTED
+    assert p(None, 64, 1, 4, 0.1, None, 3, 64, 1, None, P.F64, 64, None, 0, None) == P.ERR_INVALID_ARG
+    assert p(None, 64, 1, 0, 0.1, None, P.F32, 64, 1, None, P.F64, 64, None, 0, None) == P.ERR_INVALID_ARG
+    assert p(None, 64, 2, 4, 0.1, None, P.F32, 100, 1, None, P.F64, 128, None, 0, None) == P.ERR_INVALID_ARG
+    assert p(None, 64, 1, 4, -1.0, None, P.F64, 64, 0, None, P.F64, 64, None, 0, None) == P.OK
+    f = L.logra_influence_scores
+    args = lambda **kw: [kw.get(k, v) for k, v in dict(
+        te=None, tdt=P.F64, ld_te=64, Q=2, tr=None, rdt=P.F32, ld_tr=64, N=10, D=64, base=0, s=None, ld_s=10,
+        topk=3, tv=None, ti=None, merge=0, ws=None, wsb=0, st=None).items()]
+    assert f(*args(rdt=P.BF16)) == P.ERR_UNSUPPORTED           # bf16 pairs only with bf16
+    assert f(*args(tdt=P.BF16, rdt=P.F64)) == P.ERR_UNSUPPORTED
+    assert f(*args(tdt=3)) == P.ERR_INVALID_ARG
+    assert f(*args(Q=70000)) == P.ERR_UNSUPPORTED
+    assert f(*args(Q=0)) == P.OK
+    assert f(*args()) == P.ERR_INVALID_ARG                     # passes the dtype checks; NULL top-k buffers
+    assert "topk_val" in P.logra_last_error()

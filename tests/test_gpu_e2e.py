@@ -3,10 +3,20 @@ examples of 16 tokens, damping 1e-3 x mean eigenvalue, scores 2 x 4, top-1):
 project -> covariance -> precondition -> scores -> top-1 on the GPU, against
 the same chain in float64.
 
-Stage outputs (G, S) meet 1e-4.  The preconditioned test gradients and the
-scores pass through fp32 S, and a rank-4 covariance with 1e-3 damping is
-ill-conditioned (kappa ~ 1e4), so their bound is derived from the
-conditioning: max(1e-4, 16 * kappa * 2^-24)."""
+The projection runs in fp32 (fp32 inputs, fp32 accumulation); the statistics
+after it run in float64 (logra_cov_accumulate_f64, logra_precondition_f64 with
+an fp64 output, and scores accumulated in float64).  That is what the fp32 bar
+needs here: the damped covariance of 4 examples has a condition number near
+2.6e4 and the scores cancel by 4e4-6e5 (sum of |terms| over |score|), so fp32
+rounding of S, of the preconditioned gradients or of the score sums alone
+gives 4e-4 to 2e-3 relative error, while fp32 projected gradients (about 1e-7
+relative) feed only about 3e-7 into the scores.
+
+Every stage is held to the stated fp32 bound, 1e-4, as a normwise error per
+row (max |got - want| / max |want| over each example's or query's row): G, S,
+the preconditioned test gradients and the scores.  Top-1 must be the oracle's
+wherever the oracle's gap between its first and second score exceeds twice
+that bound of the row's largest score."""
 import numpy as np
 import pytest
 
@@ -14,6 +24,8 @@ import oracle
 import workloads as W
 
 pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
 
 
 def tiny_inputs(seed=0):
@@ -35,10 +47,10 @@ def run_gpu(w, tr, te):
     p_in, p_out = dev(tr["p_in"]), dev(tr["p_out"])
     P.logra_project_layer(dev(tr["x"]), dev(tr["dy"]), p_in, p_out, g_tr)
     P.logra_project_layer(dev(te["x"]), dev(te["dy"]), p_in, p_out, g_te)
-    S = torch.zeros((D, D), dtype=torch.float32, device="cuda")
-    P.logra_cov_accumulate(g_tr, S)
-    pre = torch.zeros_like(g_te)
-    P.logra_precondition(S, w.B, w.extra["damp"], g_te, pre)
+    S = torch.zeros((D, D), dtype=torch.float64, device="cuda")
+    P.logra_cov_accumulate_f64(g_tr, S)
+    pre = torch.zeros((w.extra["Q"], D), dtype=torch.float64, device="cuda")
+    P.logra_precondition_f64(S, w.B, w.extra["damp"], g_te, pre)
     s = torch.zeros((w.extra["Q"], w.B), dtype=torch.float32, device="cuda")
     k = w.extra["topk"]
     tv = torch.zeros((w.extra["Q"], k), dtype=torch.float32, device="cuda")
@@ -59,21 +71,22 @@ def run_oracle(w, tr, te):
     return dict(g_tr=g_tr, g_te=g_te, S=S, pre=pre, s=s, tv=tv, ti=ti, kappa=kappa)
 
 
-def check(got, want):
-    from gpu_util import normwise, rowwise_normwise
-    assert rowwise_normwise(got["g_tr"], want["g_tr"]) <= 1e-4
-    assert rowwise_normwise(got["g_te"], want["g_te"]) <= 1e-4
-    assert normwise(got["S"], want["S"]) <= 1e-4
-    tol = max(1e-4, 16 * want["kappa"] * 2.0 ** -24)
-    assert rowwise_normwise(got["pre"], want["pre"]) <= tol
-    ds = np.abs(got["s"] - want["s"])
-    scale = np.linalg.norm(want["pre"], axis=1)[:, None] * np.linalg.norm(want["g_tr"], axis=1)[None, :]
-    assert np.max(ds / scale) <= tol
+def check(got, want, tol=TOL):
+    """Asserts the bars above; returns the measured errors."""
+    from gpu_util import rowwise_normwise
+    err = {n: rowwise_normwise(got[n], want[n]) for n in ("g_tr", "g_te", "S", "pre", "s")}
+    for n, e in err.items():
+        assert e <= tol, f"{n}: normwise error per row {e:.3e} > {tol:.0e}"
+    top1 = 0
     for q in range(want["s"].shape[0]):
-        srt = np.sort(want["s"][q])[::-1]
-        if srt[0] - srt[1] > 2 * tol * scale[q].max():
-            assert got["ti"][q, 0] == want["ti"][q, 0]
-    return tol
+        row = want["s"][q]
+        srt = np.sort(row)[::-1]
+        if srt[0] - srt[1] > 2 * tol * np.abs(row).max():
+            assert got["ti"][q, 0] == want["ti"][q, 0], f"query {q}: top-1 {got['ti'][q, 0]} != {want['ti'][q, 0]}"
+            top1 += 1
+        assert got["tv"][q, 0] == got["s"][q, got["ti"][q, 0]]   # the value is the score of that index
+    err["top1_checked"] = top1
+    return err
 
 
 def test_tiny_end_to_end():
@@ -82,5 +95,7 @@ def test_tiny_end_to_end():
     w, tr, te = tiny_inputs()
     want = run_oracle(w, tr, te)
     got = run_gpu(w, tr, te)
-    tol = check(got, want)
-    say(f"  kappa {want['kappa']:.3e} -> tolerance {tol:.3e}")
+    err = check(got, want)
+    assert err["top1_checked"] == want["s"].shape[0]   # seed 0: both queries have a clear first
+    say(f"  kappa {want['kappa']:.3e}; errors " + ", ".join(f"{k} {v:.2e}" for k, v in err.items()
+                                                          if k != "top1_checked"))
