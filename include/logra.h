@@ -116,6 +116,22 @@ int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dt
                          const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
                          void *ws, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * logra_project_layers without a workspace argument.  The workspace is a
+ * static device array of the library, LOGRA_NOALLOC_WS_BYTES (64 MiB) on each
+ * GPU it runs on, held until the process ends; the call allocates nothing.
+ * Results are bitwise those of logra_project_layers.  A batch whose
+ * logra_project_layers_ws_size exceeds LOGRA_NOALLOC_WS_BYTES returns
+ * LOGRA_ERR_UNSUPPORTED (e.g. 7 Llama3-8B layers at k = 16 with B = 8,
+ * T = 2048 need 23 MiB; at k = 64 with B = 16, T = 1024 they need 88 MiB).
+ * Calls that overlap on one GPU (other streams or threads) share the array
+ * and race: order them.  Other errors as logra_project_layers. */
+#define LOGRA_NOALLOC_WS_BYTES (64u * 1024u * 1024u)
+int logra_project_layers_noalloc(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
+                                 const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
+                                 void *stream);
+
 /* ------------------------------------------------------------------------
  * Projected Fisher covariance (Sec. 2 Eq. (3) P H P^T; App. D Assumption 1:
  * the empirical Fisher over training examples):

@@ -31,7 +31,7 @@ MAX_GROUP = 16
 EXPORTED = (
     "logra_last_error", "logra_version",
     "logra_project_ws_size", "logra_project_layer",
-    "logra_project_layers_ws_size", "logra_project_layers",
+    "logra_project_layers_ws_size", "logra_project_layers", "logra_project_layers_noalloc",
     "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_f64",
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks", "logra_precondition_f64",
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
@@ -74,6 +74,8 @@ def lib():
         L.logra_project_layers_ws_size.restype = sz
         L.logra_project_layers.argtypes = [ctypes.POINTER(LayerDesc), i32, i32, i32, i32, vp, i32, i32,
                                            i32, i64, vp, sz, vp]
+        L.logra_project_layers_noalloc.argtypes = [ctypes.POINTER(LayerDesc), i32, i32, i32, i32, vp, i32, i32,
+                                                   i32, i64, vp]
         L.logra_cov_accumulate.argtypes = [vp, i32, i64, i32, i32, vp, vp]
         L.logra_cov_accumulate_blocks.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
         L.logra_cov_accumulate_f64.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
@@ -104,7 +106,7 @@ def lib():
         L.logra_influence_stream.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, i32, vp, vp, vp, sz,
                                              vp, vp]
         L.logra_offload_rows.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, vp]
-        for name in ("logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_cov_accumulate",
+        for name in ("logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_project_layers_noalloc", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
                      "logra_cov_accumulate_f64", "logra_precondition_f64",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
@@ -209,6 +211,26 @@ def logra_project_layers(layers, mask=None, ws=None, stream=None):
     ws, wsb = _workspace(logra_project_layers_ws_size(arr, n, B, T, k_in, k_out), x0.device, ws)
     _check(lib().logra_project_layers(arr, n, _dtype_code(x0), B, T, _ptr(mask), k_in, k_out,
                                       _dtype_code(g0), g_ld, _ptr(ws), wsb, _stream(stream)))
+
+
+NOALLOC_WS_BYTES = 64 * 1024 * 1024
+
+
+def logra_project_layers_noalloc(layers, mask=None, stream=None):
+    """logra_project_layers with the library's static device workspace (no allocation;
+    for callers that cannot allocate).  Same layer dicts as logra_project_layers."""
+    n = len(layers)
+    arr = (LayerDesc * n)()
+    x0 = layers[0]["x"]
+    B, T, _ = x0.shape
+    k_in, k_out = layers[0]["p_in"].shape[0], layers[0]["p_out"].shape[0]
+    g0 = layers[0]["g_out"]
+    g_ld = _rows(g0, k_in * k_out) if B > 0 else k_in * k_out
+    for i, L in enumerate(layers):
+        arr[i] = LayerDesc(L["x"].data_ptr(), L["dy"].data_ptr(), L["p_in"].data_ptr(),
+                           L["p_out"].data_ptr(), L["g_out"].data_ptr(), L["x"].shape[2], L["dy"].shape[2])
+    _check(lib().logra_project_layers_noalloc(arr, n, _dtype_code(x0), B, T, _ptr(mask), k_in, k_out,
+                                              _dtype_code(g0), g_ld, _stream(stream)))
 
 
 def logra_cov_accumulate(g, S, stream=None):

@@ -75,9 +75,15 @@ int check_pinned(const void *p, const char *name, size_t align) {
     return LOGRA_OK;
 }
 
-int hip_fail(hipError_t e, const char *what) {
+}  // namespace
+
+int logra::hip_fail(hipError_t e, const char *what) {
     return fail(LOGRA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+int logra::fail_unsupported(const char *msg) { return fail(LOGRA_ERR_UNSUPPORTED, "%s", msg); }
+
+namespace {
+using logra::hip_fail;
 
 #define TRY(expr)                       \
     do {                                \
@@ -138,9 +144,14 @@ size_t logra_project_layers_ws_size(const logra_layer_desc *layers, int n_layers
     return round256(logra::project_ws_bytes(n_in, n_out, n_layers, B, T, k_in, k_out));
 }
 
-int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
-                         const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
-                         void *ws, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+// logra_project_layers; `ws_known` marks a workspace the library owns (the
+// no-allocation entry point's static device array), whose pointer kind needs
+// no check.
+int logra::project_layers_checked(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
+                                  const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld, void *ws,
+                                  size_t ws_bytes, bool ws_known, void *stream) {
     if (layers == nullptr) return fail(LOGRA_ERR_INVALID_ARG, "layers is NULL");
     if (n_layers < 1 || n_layers > LOGRA_MAX_GROUP)
         return fail(n_layers > LOGRA_MAX_GROUP ? LOGRA_ERR_UNSUPPORTED : LOGRA_ERR_INVALID_ARG,
@@ -172,12 +183,28 @@ int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dt
         grp.layer[l] = {d.x, d.dy, d.p_in, d.p_out, d.g_out, d.n_in, d.n_out};
     }
     if (mask) TRY(check_dev(mask, "mask", 1));
-    TRY(check_ws(ws, ws_bytes, logra_project_layers_ws_size(layers, n_layers, B, T, k_in, k_out)));
+    const size_t need = logra_project_layers_ws_size(layers, n_layers, B, T, k_in, k_out);
+    if (ws_known) {
+        if (ws_bytes < need)
+            return fail(LOGRA_ERR_UNSUPPORTED, "the batch needs %zu bytes of workspace, more than the %zu of the "
+                        "no-allocation entry point", need, ws_bytes);
+    } else {
+        TRY(check_ws(ws, ws_bytes, need));
+    }
     const hipError_t e = logra::launch_project(grp, in_dtype == LOGRA_BF16, B, T, mask, k_in, k_out,
                                                g_dtype == LOGRA_BF16, g_ld, ws,
                                                static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "projection launch");
     return ok();
+}
+
+extern "C" {
+
+int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
+                         const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld,
+                         void *ws, size_t ws_bytes, void *stream) {
+    return logra::project_layers_checked(layers, n_layers, in_dtype, B, T, mask, k_in, k_out, g_dtype, g_ld, ws,
+                                         ws_bytes, false, stream);
 }
 
 int logra_project_layer(const void *x, const void *dy, int in_dtype, int B, int T, int n_in,

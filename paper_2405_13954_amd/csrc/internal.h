@@ -4,7 +4,19 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "logra.h"
+
 namespace logra {
+
+// Host-side entry used by both projection entry points (abi.cpp): argument
+// checks, then the launches; ws_known skips the pointer check of a workspace
+// that the library itself owns.
+int project_layers_checked(const logra_layer_desc *layers, int n_layers, int in_dtype, int B, int T,
+                           const uint8_t *mask, int k_in, int k_out, int g_dtype, int64_t g_ld, void *ws,
+                           size_t ws_bytes, bool ws_known, void *stream);
+// Sets the thread's error message; returns LOGRA_ERR_HIP / LOGRA_ERR_UNSUPPORTED.
+int hip_fail(hipError_t e, const char *what);
+int fail_unsupported(const char *msg);
 
 typedef uint16_t bf16_bits_t;   // a bf16 value as its bit pattern
 enum DtypeCode { kF32 = 0, kBF16 = 1, kF64 = 2 };   // element types, numbered as in the C ABI
