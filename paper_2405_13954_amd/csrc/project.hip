@@ -30,7 +30,8 @@
 //     round trip is hidden behind the stream.
 //  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
 //     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
-//     formed in fp32 from LDS (KT x KT outputs per thread).  Empty tiles give 0.
+//     formed by fp32 MFMAs straight from those sums (one wave per 16-row block
+//     of G).  Empty tiles give 0.
 //  C. k_project_reduce: per example, the tile sums are added in tile order
 //     and G_b is written (fp32 or bf16, round to nearest even) to the
 //     caller's store row.
@@ -41,22 +42,7 @@
 namespace logra {
 namespace {
 
-#ifndef LOGRA_PROJ_STAGES
-#define LOGRA_PROJ_STAGES 3
-#endif
-#ifndef LOGRA_PROJ_ROWBLOCKS
-#define LOGRA_PROJ_ROWBLOCKS 4
-#endif
-#ifndef LOGRA_PROJ_CHUNK
-#define LOGRA_PROJ_CHUNK 6144   // k <= 32 (14,336 = 6,144 + 6,144 + 2,048); measured best of 2,048..8,192
-#endif
-#ifndef LOGRA_PROJ_NT
-#define LOGRA_PROJ_NT 0
-#endif
-#ifndef LOGRA_PROJ_MINWAVES
-#define LOGRA_PROJ_MINWAVES 1   // waves per SIMD the chunk kernel's registers must allow
-#endif
-constexpr int MB = LOGRA_PROJ_ROWBLOCKS;  // 16-token row blocks per tile
+constexpr int MB = 4;                     // 16-token row blocks per tile
 constexpr int TT = 16 * MB;               // tokens per tile
 static_assert(TT == 64, "a tile's valid-token set is one 64-bit word");
 constexpr int NW = 4;                     // waves per workgroup
@@ -64,28 +50,25 @@ constexpr int kMaxSlots = 1024;           // chunk slots a group can order by wi
 static_assert(kMaxSlots <= 4096 && kMaxGroup <= 16, "an ordered slot packs its layer into 4 bits");
 constexpr int NT = NW * kWave;            // threads per workgroup
 
-// Contraction columns per work item, and register pipeline depth, by
-// projection width (KT = ceil(k / 16)).
-#ifndef LOGRA_PROJ_CHUNK_WIDE
-#define LOGRA_PROJ_CHUNK_WIDE 14336   // k > 32: one item per layer side up to 14,336 (measured best of 2,048..14,336)
-#endif
-__host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? LOGRA_PROJ_CHUNK_WIDE : LOGRA_PROJ_CHUNK; }
-__host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : LOGRA_PROJ_STAGES; }
+// Contraction columns per work item.  k <= 32: 6,144 (14,336 = 6,144 + 6,144
+// + 2,048), measured best of 2,048..8,192.  k > 32: 14,336 (one item per
+// layer side of a Llama3-8B block), measured best of 2,048..14,336.
+constexpr int kChunkNarrow = 6144;
+constexpr int kChunkWide = 14336;
+__host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? kChunkWide : kChunkNarrow; }
+// Register pipeline depth of the register-staged path.
+__host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : 3; }
 
 constexpr int kMaxShare = 3;   // layers projected from one pass over a shared x
 
-#ifndef LOGRA_PROJ_DMA
-#define LOGRA_PROJ_DMA 1   // bf16 operands staged by LDS-DMA wherever the rings fit in LDS
-#endif
-#ifndef LOGRA_PROJ_AHEAD_ROUNDS
-#define LOGRA_PROJ_AHEAD_ROUNDS 2   // rounds of items at the end claimed only when free
-#endif
-#ifndef LOGRA_PROJ_DMA_NT_KT
-// The streamed x / dy copies of the DMA path carry the non-temporal hint up
-// to this KT (k <= 32 at 2); it leaves the cache to the projection matrices.
-// Measured: the 7-layer k = 16 launch 7% faster, the k = 64 block 2% slower.
-#define LOGRA_PROJ_DMA_NT_KT 2
-#endif
+// Rounds of items (one item per workgroup) at the end of a launch that a
+// workgroup claims only when it is free; before them it claims its next item
+// when it starts one.
+constexpr int kAheadRounds = 2;
+// The streamed x / dy copies of the per-wave DMA path carry the non-temporal
+// hint up to this KT (k <= 32): it leaves the cache to the projection
+// matrices.  Measured: the 7-layer k = 16 launch 7% faster.
+constexpr int kDmaNtMaxKT = 2;
 constexpr int kDmaCols = 64;     // columns per step: 128 bytes of a bf16 row
 constexpr int kLdsBytes = 160 * 1024;
 template <int KT, int S>
@@ -104,7 +87,7 @@ struct DmaShape {
 };
 template <int KT, int S, typename TIn>
 __host__ __device__ constexpr bool use_dma() {
-    return LOGRA_PROJ_DMA && sizeof(TIn) == 2 && DmaShape<KT, S>::kFits;
+    return sizeof(TIn) == 2 && DmaShape<KT, S>::kFits;
 }
 
 struct ChunkLayer {
@@ -230,8 +213,7 @@ __device__ __forceinline__ void project_part(f32x4 (&acc)[MB][S * KT], const TIn
         const uint32_t koff = static_cast<uint32_t>(st * SS) * ES;
 #pragma unroll
         for (int m = 0; m < MB; ++m)
-            xa[m] = LOGRA_PROJ_NT ? buf_ld128_nt(ra, in_k ? aoff[m] + koff : kBufOOB)
-                                  : buf_ld128(ra, in_k ? aoff[m] + koff : kBufOOB);
+            xa[m] = buf_ld128(ra, in_k ? aoff[m] + koff : kBufOOB);
 #pragma unroll
         for (int q = 0; q < S; ++q)
 #pragma unroll
@@ -308,7 +290,7 @@ __device__ __forceinline__ void project_part_dma(f32x4 (&acc)[MB][S * KT], const
         const uint32_t lds = ring_addr + static_cast<uint32_t>(stage * Sh::kStage);
 #pragma unroll
         for (int q = 0; q < Sh::kX; ++q) {
-            if constexpr (KT <= LOGRA_PROJ_DMA_NT_KT) copy_to_lds_nt(ra, in ? xo[q] + dk : kBufOOB, lds + q * 1024);
+            if constexpr (KT <= kDmaNtMaxKT) copy_to_lds_nt(ra, in ? xo[q] + dk : kBufOOB, lds + q * 1024);
             else copy_to_lds(ra, in ? xo[q] + dk : kBufOOB, lds + q * 1024);
         }
 #pragma unroll
@@ -364,31 +346,6 @@ __device__ __forceinline__ uint64_t tile_valid(const ProjArgs &a, int j, int til
     if (a.tiles) return load_uniform(a.bits + j);
     const int n = a.T - tile * TT;
     return n >= 64 ? ~0ull : (1ull << n) - 1;
-}
-
-// Validity of the MB token rows a lane feeds (tokens t0 + 16m + lane%16):
-// each lane loads the flags of tokens t0 + lane and t0 + 64 + lane (one
-// coalesced load each), and the rows are gathered by lane shuffles.
-// Returns whether any of the lane's rows is valid.
-__device__ __forceinline__ bool lane_tokens(const ProjArgs &a, int b, int t0, int lane, bool (&tok_ok)[MB],
-                                            int *own = nullptr) {
-    int v[(TT + kWave - 1) / kWave];
-#pragma unroll
-    for (int h = 0; h < (TT + kWave - 1) / kWave; ++h) {
-        const int t = t0 + h * kWave + lane;
-        int ok = t < a.T && h * kWave + lane < TT;
-        if (a.mask && ok) ok = a.mask[static_cast<size_t>(b) * a.T + t] != 0;
-        v[h] = ok;
-    }
-    bool any = false;
-#pragma unroll
-    for (int m = 0; m < MB; ++m) {
-        const int r = 16 * m + (lane & 15);
-        tok_ok[m] = __shfl(v[r / kWave], r % kWave, kWave) != 0;
-        any |= tok_ok[m];
-    }
-    if (own) *own = v[0];   // token t0 + lane
-    return any;
 }
 
 // One chunk item (see the file comment).  Every listed tile (and, without a
@@ -527,7 +484,7 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 
 // Persistent: the grid is sized to the resident capacity of the GPU.  Each
 // workgroup starts on item blockIdx.x and takes further items from the work
-// counter.  While more than LOGRA_PROJ_AHEAD_ROUNDS rounds of items (one per
+// counter.  While more than kAheadRounds rounds of items (one per
 // workgroup) lie beyond its current item, it claims the next one when it
 // starts the current one, so the counter's round trip overlaps the stream;
 // in the last rounds it claims only when free, which keeps the tail short.  The loop
@@ -536,7 +493,7 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
 // `next` comes after the following item's fold barrier, by which time every
 // thread has read it.
 template <int KT, int S, typename TIn>
-__global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(ProjArgs a) {
+__global__ __launch_bounds__(NT, 1) void k_project_chunks(ProjArgs a) {
     constexpr bool kDma = use_dma<KT, S, TIn>();
     __shared__ f32x4 slot[kDma ? 1 : MB * S * KT * kWave];   // cross-wave fold of the register path
     __shared__ __attribute__((aligned(16))) uint8_t ring[kDma ? DmaShape<KT, S>::kRing : 16];
@@ -549,7 +506,7 @@ __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(Proj
     const int items = count * a.slots;
     int item = blockIdx.x;
     while (item < items) {
-        const bool ahead = item + LOGRA_PROJ_AHEAD_ROUNDS * static_cast<int>(gridDim.x) < items;
+        const bool ahead = item + kAheadRounds * static_cast<int>(gridDim.x) < items;
         int claim = 0;
         if (ahead && tid == 0) claim = atomicAdd(a.work, 1);
         chunk_item<KT, S, TIn>(a, item, count, slot, lane, wave, my_ring, lds_addr(my_ring), ahead, claim, &next);
@@ -561,6 +518,203 @@ __global__ __launch_bounds__(NT, LOGRA_PROJ_MINWAVES) void k_project_chunks(Proj
         }
         __syncthreads();
         item = __builtin_amdgcn_readfirstlane(next);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// bf16, unshared inputs: tile groups sharing one projection slab.
+//
+// At k = 64 a P slab (64 rows x 128 B per 64-column step) is as large as a
+// 64-token x slab, so a ring stage per wave holding both leaves room for only
+// two stages in LDS: about 32 KB of HBM reads in flight per CU.  Here a work
+// item is one contraction chunk of one side of one layer for a GROUP of up
+// to four listed tiles: wave w streams tile w of the group over all of the
+// chunk's 64-column steps, and the four waves share each step's P slab (each
+// wave copies its share of it).  A stage is four x slabs and one P slab
+// (34 KB at k <= 16, 36 KB at k <= 32, 40 KB at k <= 64, 48 KB at k <= 128), so
+// four stages fit at k <= 32 and three above, all but one in flight.  One
+// barrier per step makes every wave's share of the P slab visible and frees
+// the stage the next copies overwrite.  Each wave sums its tile over the
+// whole chunk, so no cross-wave fold is needed; the tile's partial goes to
+// the workspace in the same layout as the per-wave path's.
+//
+// Two measured choices keep the HBM stream fast.  The x / dy copies carry the
+// non-temporal hint (the projection slabs, re-read by every group, keep the
+// cache).  And each group walks the chunk's steps from its own starting
+// step, 37 x group mod steps, so that the groups streaming one chunk at the
+// same time on all CUs read scattered column ranges rather than the same
+// columns of different rows (starts spaced evenly, group x steps / groups,
+// keep groups that run side by side on nearby columns and measured 4% slower).
+// The 7-layer block at k = 64 (B = 16, T = 1024): 570 us with the per-wave
+// path, 581 with tile groups alone, 549 with the scattered start, 559 with the
+// hint, 494-497 with both.
+template <int KT>
+struct TileDma {
+    static constexpr int kX = TT / 8;                    // x slab: 8 copies of 8 token rows
+    static constexpr int kP = 2 * KT;                    // P slab: 16 KT rows, 8 per copy
+    static constexpr int kPw = (kP + NW - 1) / NW;       // P copies issued by each wave (at most)
+    static constexpr int kCopies = kX + kPw;             // copies per wave per stage (at most)
+    static constexpr int kStage = (NW * kX + kP) * 1024; // bytes of one stage
+    static constexpr int kStages = 4 * kStage + 1024 <= 160 * 1024 ? 4 : 3;
+    static constexpr int kRing = kStages * kStage;
+    static_assert(kRing + 1024 <= 160 * 1024, "the ring fits in LDS");
+};
+
+// Wait until at most kCount of this wave's copies are pending (its copies of
+// the later stages), then meet the other waves at the barrier.
+template <int kCount>
+__device__ __forceinline__ void wait_copies_below() {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(kCount) : "memory");
+}
+
+template <int KT>
+__device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int count, int groups, int lane,
+                                                int wave, uint32_t ring_addr, const uint8_t *ring) {
+    using Sh = TileDma<KT>;
+    constexpr int NS = Sh::kStages;
+    const int rank = item / groups;             // position of the work slot in processing order
+    const int grp = item - rank * groups;       // group of listed tiles
+    int gslot = rank, l = 0;
+    if (a.ordered) {
+        const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
+        gslot = e & 0xfff;
+        l = (e >> 12) & 0xf;
+    } else {
+        while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
+    }
+    const ChunkLayer &L = a.layer[l];
+    const int cs = gslot - L.slot_begin;        // x chunks first, then dy chunks
+    const bool xside = cs < L.x_items;
+    const int c = xside ? cs : cs - L.x_items;
+    const int n = xside ? L.n_in : L.n_out;
+    const int k = xside ? a.k_in : a.k_out;
+    const int col0 = c * a.ck;
+    const int nk = min(a.ck, n - col0);
+    // this wave's tile
+    const int j = grp * NW + wave;
+    const bool has = j < count;
+    int bt = 0;
+    uint64_t valid = 0;
+    if (has) {
+        bt = a.tiles ? load_uniform(a.tiles + j) : j;
+        valid = tile_valid(a, j, bt - (bt / a.tpe) * a.tpe);
+    }
+    const int b = bt / a.tpe, tile = bt - b * a.tpe;
+    const size_t tok0 = static_cast<size_t>(b) * a.T + static_cast<size_t>(tile) * TT;
+    const bf16_bits *A = static_cast<const bf16_bits *>(xside ? L.x : L.dy) + tok0 * n + col0;
+    const bf16_bits *Pm = static_cast<const bf16_bits *>(xside ? L.p_in : L.p_out) + col0;
+    const auto ra = buf_rsrc(A, has ? (static_cast<uint32_t>(TT - 1) * n + nk) * 2u : 0u);
+    const auto rp = buf_rsrc(Pm, (static_cast<uint32_t>(k - 1) * n + nk) * 2u);
+    const int sub = lane >> 3;
+    const int lcol = ((lane & 7) ^ sub) * 8;     // the lane's element column within a step
+    // P copies of this wave: kPw, or fewer where the slab has fewer than NW kPw copies
+    constexpr bool kEven = Sh::kPw * NW == Sh::kP;
+    const int pw = kEven ? Sh::kPw : (wave * Sh::kPw < Sh::kP ? Sh::kPw : 0);
+    uint32_t xo[Sh::kX], po[Sh::kPw];
+#pragma unroll
+    for (int q = 0; q < Sh::kX; ++q) {
+        const int t = 8 * q + sub;
+        xo[q] = (valid >> t) & 1 ? (static_cast<uint32_t>(t) * n + lcol) * 2u : kBufOOB;
+    }
+#pragma unroll
+    for (int q = 0; q < Sh::kPw; ++q) {
+        const int r = 8 * (wave * Sh::kPw + q) + sub;
+        po[q] = r < k ? (static_cast<uint32_t>(r) * n + lcol) * 2u : kBufOOB;
+    }
+    const int nsteps = (nk + kDmaCols - 1) / kDmaCols;
+    const int rot = (grp * 37) % nsteps;   // the group's first step: scattered over the chunk
+    // stage layout: x slab of wave 0..3 (8 KB each), then the P slab
+    auto issue = [&](int st, int stage) {   // steps past the chunk's count: all out of range
+        int sr = st + rot;
+        if (sr >= nsteps) sr -= nsteps;
+        const bool in = st < nsteps && sr * kDmaCols + lcol < nk;
+        const uint32_t dk = static_cast<uint32_t>(sr * kDmaCols) * 2u;
+        const uint32_t lds = ring_addr + static_cast<uint32_t>(stage * Sh::kStage);
+#pragma unroll
+        for (int q = 0; q < Sh::kX; ++q)
+            copy_to_lds_nt(ra, in ? xo[q] + dk : kBufOOB, lds + (wave * Sh::kX + q) * 1024);
+#pragma unroll
+        for (int q = 0; q < Sh::kPw; ++q)
+            if (kEven || pw > 0)
+                copy_to_lds(rp, in ? po[q] + dk : kBufOOB, lds + (NW * Sh::kX + wave * Sh::kPw + q) * 1024);
+    };
+    f32x4 acc[MB][KT];
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+        for (int jj = 0; jj < KT; ++jj) acc[m][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NS - 1; ++i) issue(i, i);
+    const int row = lane & 15, kg = lane >> 4;
+    for (int i = 0; i < nsteps; ++i) {
+        // this wave's copies of step i are done when only the NS - 2 later
+        // stages are pending; after the barrier every wave's are, and every
+        // wave has finished reading step i - 1, whose stage the next copies refill
+        if (kEven || pw > 0) wait_copies_below<(NS - 2) * Sh::kCopies>();
+        else wait_copies_below<(NS - 2) * Sh::kX>();
+        issue(i + NS - 1, (i + NS - 1) % NS);
+        if (!has) continue;
+        const uint8_t *base = ring + (i % NS) * Sh::kStage;
+        const uint8_t *xb = base + wave * Sh::kX * 1024;
+        const uint8_t *pbase = base + NW * Sh::kX * 1024;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int cc = 4 * h + kg;
+            bf16x8 xf[MB], pf[KT];
+#pragma unroll
+            for (int m = 0; m < MB; ++m) {
+                const int t = 16 * m + row;
+                xf[m] = as_bf16x8(*reinterpret_cast<const u32x4 *>(xb + t * 128 + ((cc ^ (t & 7)) << 4)));
+            }
+#pragma unroll
+            for (int jj = 0; jj < KT; ++jj) {
+                const int r = 16 * jj + row;
+                pf[jj] = as_bf16x8(*reinterpret_cast<const u32x4 *>(pbase + r * 128 + ((cc ^ (r & 7)) << 4)));
+            }
+#pragma unroll
+            for (int m = 0; m < MB; ++m)
+#pragma unroll
+                for (int jj = 0; jj < KT; ++jj) acc[m][jj] = mfma16_bf16(xf[m], pf[jj], acc[m][jj]);
+        }
+    }
+    // the copies past the chunk (out of range: zeros) are still in flight
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (has) {
+        const int pslot = xside ? c : L.c_in + c;
+        f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + L.part_begin +
+                                               (static_cast<size_t>(bt) * (L.c_in + L.c_out) + pslot) *
+                                                   (TT * 16 * KT)) + lane;
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int jj = 0; jj < KT; ++jj) dst[(m * KT + jj) * kWave] = acc[m][jj];
+    }
+}
+
+// Persistent, like k_project_chunks: items are (work slot, tile group), taken
+// from the work counter, claimed ahead except in the last rounds.  The
+// barrier that hands a claim to the workgroup also keeps the next item's
+// first copies from overwriting a stage another wave is still reading.
+template <int KT>
+__global__ __launch_bounds__(NT, 1) void k_project_tiles(ProjArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t ring[TileDma<KT>::kRing];
+    __shared__ int next;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int count = a.tiles ? load_uniform(a.n_tiles) : a.B * a.tpe;
+    const int groups = (count + NW - 1) / NW;
+    const int items = groups * a.slots;
+    const uint32_t ring_addr = lds_addr(ring);
+    int item = blockIdx.x;
+    while (item < items) {
+        const bool ahead = item + kAheadRounds * static_cast<int>(gridDim.x) < items;
+        int claim = 0;
+        if (ahead && tid == 0) claim = atomicAdd(a.work, 1);
+        tile_group_item<KT>(a, item, count, groups, lane, wave, ring_addr, ring);
+        if (tid == 0) next = static_cast<int>(gridDim.x) + (ahead ? claim : atomicAdd(a.work, 1));
+        __syncthreads();
+        item = __builtin_amdgcn_readfirstlane(next);
+        __syncthreads();   // every wave has read `next` before it is written again
     }
 }
 
@@ -631,72 +785,75 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
     if (tid == 0) *n_tiles = base;
 }
 
+// One wave per (tile, 16-row block jo of G): x' and dy' of the tile are the
+// fixed-order sums of their chunk partials, read straight from the workspace,
+// where they already sit in the operand layout of the fp32 16x16x4 MFMA with
+// the token as the contraction index (lane l of partial block (m, j) holds
+// the rows t = 16 m + 4 (l / 16) + r, r < 4, of column 16 j + l % 16).  So
+// the tile's sum over tokens of dy'_t x'_t^T is, for each 16 x 16 block
+// (jo, ji), 16 MFMAs over (m, r).  Tiles without a valid token get 0.
 template <int KT>
-__global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a) {
+__global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pairs) {
     constexpr int KP = 16 * KT;
     constexpr int NQ = MB * KT * kWave;     // f32x4 per chunk partial
-    __shared__ float xs[TT * KP];            // x'  [token][i]
-    __shared__ float ds[TT * KP];            // dy' [token][o]
+    const int lane = threadIdx.x & (kWave - 1);
+    const int p = blockIdx.x * NW + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    if (p >= pairs) return;
+    const int tix = p / KT, jo = p - tix * KT;   // tile over all layers, row block of G
     const int per_layer = a.B * a.tpe;
-    const int l = blockIdx.x / per_layer;
-    const int bt = blockIdx.x - l * per_layer;
+    const int l = tix / per_layer;
+    const int bt = tix - l * per_layer;
     const int b = bt / a.tpe, tile = bt - b * a.tpe;
-    const int tid = threadIdx.x;
     const int D = a.k_in * a.k_out;
-    float *gdst = a.gpart + static_cast<size_t>(blockIdx.x) * D;
-
-    bool tok_ok[MB];
-    const bool any = lane_tokens(a, b, tile * TT, tid & (kWave - 1), tok_ok);
-    if (!__syncthreads_or(any)) {
-        for (int i = tid; i < D; i += 256) gdst[i] = 0.f;
+    float *gdst = a.gpart + static_cast<size_t>(tix) * D;
+    const int t = tile * TT + lane;
+    bool tok = t < a.T;
+    if (a.mask && tok) tok = a.mask[static_cast<size_t>(b) * a.T + t] != 0;
+    const bool any = __builtin_amdgcn_ballot_w64(tok) != 0;
+    const int row = lane & 15, grp4 = lane >> 4;
+    if (!any) {
+        for (int r = 0; r < 4; ++r) {
+            const int o = 16 * jo + 4 * grp4 + r;
+            if (o >= a.k_out) continue;
+            for (int i = row; i < a.k_in; i += 16) gdst[o * a.k_in + i] = 0.f;
+        }
         return;
     }
     const ChunkLayer &L = a.layer[l];
     const int C = L.c_in + L.c_out;
-    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP));
-    for (int q = tid; q < NQ; q += 256) {
-        f32x4 sx = {0.f, 0.f, 0.f, 0.f}, sd = {0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < L.c_in; ++c) sx += src[static_cast<size_t>(c) * NQ + q];
-        for (int c = L.c_in; c < C; ++c) sd += src[static_cast<size_t>(c) * NQ + q];
-        const int lane = q & (kWave - 1), mj = q / kWave;
-        const int m = mj / KT, j = mj - m * KT;
-        const int row = lane & 15, kg = lane >> 4;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP)) + lane;
+    f32x4 dv[MB], xv[KT][MB];
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+        dv[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ji = 0; ji < KT; ++ji) xv[ji][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int c = 0; c < L.c_in; ++c)
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int ji = 0; ji < KT; ++ji) xv[ji][m] += src[static_cast<size_t>(c) * NQ + (m * KT + ji) * kWave];
+    for (int c = L.c_in; c < C; ++c)
+#pragma unroll
+        for (int m = 0; m < MB; ++m) dv[m] += src[static_cast<size_t>(c) * NQ + (m * KT + jo) * kWave];
+    f32x4 acc[KT];
+#pragma unroll
+    for (int ji = 0; ji < KT; ++ji) {
+        acc[ji] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[ji] = mfma16_f32(dv[m][r], xv[ji][m][r], acc[ji]);
+    }
+    // result register r of lane l: o = 16 jo + 4 (l / 16) + r, i = 16 ji + l % 16
+#pragma unroll
+    for (int ji = 0; ji < KT; ++ji) {
+        const int i = 16 * ji + row;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            xs[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sx[r];
-            ds[(16 * m + 4 * kg + r) * KP + 16 * j + row] = sd[r];
-        }
-    }
-    __syncthreads();
-
-    // Sum over the tile's tokens of dy'_t x'_t^T: thread (ob, ib) of a 16 x 16
-    // grid owns outputs o = KT ob + u, i = KT ib + v for u, v < KT.
-    const int ob = tid >> 4, ib = tid & 15;
-    float c[KT][KT];
-#pragma unroll
-    for (int u = 0; u < KT; ++u)
-#pragma unroll
-        for (int v = 0; v < KT; ++v) c[u][v] = 0.f;
-    for (int t = 0; t < TT; ++t) {
-        float dv[KT], xv[KT];
-#pragma unroll
-        for (int u = 0; u < KT; ++u) {
-            dv[u] = ds[t * KP + KT * ob + u];
-            xv[u] = xs[t * KP + KT * ib + u];
-        }
-#pragma unroll
-        for (int u = 0; u < KT; ++u)
-#pragma unroll
-            for (int v = 0; v < KT; ++v) c[u][v] = __builtin_fmaf(dv[u], xv[v], c[u][v]);
-    }
-#pragma unroll
-    for (int u = 0; u < KT; ++u) {
-        const int o = KT * ob + u;
-        if (o >= a.k_out) break;
-#pragma unroll
-        for (int v = 0; v < KT; ++v) {
-            const int i = KT * ib + v;
-            if (i < a.k_in) gdst[o * a.k_in + i] = c[u][v];
+            const int o = 16 * jo + 4 * grp4 + r;
+            if (o < a.k_out && i < a.k_in) gdst[o * a.k_in + i] = acc[ji][r];
         }
     }
 }
@@ -795,7 +952,7 @@ int plan_shares(ProjArgs &a, int n_layers, int KT, int &smax) {
 
 // Resident workgroups of a kernel on the current device (computed once per
 // device and kernel).
-template <int KT, int S, typename TIn>
+template <void (*K)(ProjArgs)>
 int resident_groups() {
     static int cache[64] = {0};
     int dev = 0;
@@ -804,8 +961,8 @@ int resident_groups() {
         int cus = 0, per_cu = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void *>(k_project_chunks<KT, S, TIn>), NT, 0) != hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(K), NT, 0) !=
+                hipSuccess ||
             per_cu <= 0)
             per_cu = 1;
         cache[dev] = cus * per_cu;
@@ -815,12 +972,24 @@ int resident_groups() {
 
 template <int KT, int S, typename TIn>
 void launch_chunks_s(const ProjArgs &a, int max_items, hipStream_t s) {
-    const int cap = resident_groups<KT, S, TIn>();
+    const int cap = resident_groups<k_project_chunks<KT, S, TIn>>();
     hipLaunchKernelGGL((k_project_chunks<KT, S, TIn>), dim3(max_items < cap ? max_items : cap), dim3(NT), 0, s, a);
 }
 
+template <int KT>
+void launch_tiles(const ProjArgs &a, int max_items, hipStream_t s) {
+    const int cap = resident_groups<k_project_tiles<KT>>();
+    hipLaunchKernelGGL((k_project_tiles<KT>), dim3(max_items < cap ? max_items : cap), dim3(NT), 0, s, a);
+}
+
+// Tile groups sharing the projection slab (launch_tiles) for bf16 inputs at
+// KT >= kTilesMinKT (k > 16) without shared inputs; per-wave chunks otherwise.
+constexpr int kTilesMinKT = 2;
 template <int KT, typename TIn>
 void launch_chunks(const ProjArgs &a, int max_items, int smax, hipStream_t s) {
+    if constexpr (sizeof(TIn) == 2 && KT >= kTilesMinKT) {
+        if (smax == 1) return launch_tiles<KT>(a, a.slots * ((a.B * a.tpe + NW - 1) / NW), s);
+    }
     if constexpr (KT <= 2) {
         if (smax == 3) return launch_chunks_s<KT, 3, TIn>(a, max_items, s);
         if (smax == 2) return launch_chunks_s<KT, 2, TIn>(a, max_items, s);
@@ -908,17 +1077,19 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     switch (KT) {
         case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, smax, s) : launch_chunks<1, float>(a, max_items, smax, s); break;
         case 2: bf16_in ? launch_chunks<2, bf16_bits>(a, max_items, smax, s) : launch_chunks<2, float>(a, max_items, smax, s); break;
+        // k > 32, bf16: tile groups sharing each step's projection slab
         case 4: bf16_in ? launch_chunks<4, bf16_bits>(a, max_items, smax, s) : launch_chunks<4, float>(a, max_items, smax, s); break;
         default: bf16_in ? launch_chunks<8, bf16_bits>(a, max_items, smax, s) : launch_chunks<8, float>(a, max_items, smax, s); break;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const unsigned tiles = static_cast<unsigned>(grp.n_layers) * B * a.tpe;
+    const int pairs = grp.n_layers * B * a.tpe * KT;   // (tile, row block) pairs, one wave each
+    const unsigned fgrid = static_cast<unsigned>((pairs + NW - 1) / NW);
     switch (KT) {
-        case 1: hipLaunchKernelGGL((k_project_tile_finish<1>), dim3(tiles), dim3(256), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((k_project_tile_finish<2>), dim3(tiles), dim3(256), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((k_project_tile_finish<4>), dim3(tiles), dim3(256), 0, s, a); break;
-        default: hipLaunchKernelGGL((k_project_tile_finish<8>), dim3(tiles), dim3(256), 0, s, a); break;
+        case 1: hipLaunchKernelGGL((k_project_tile_finish<1>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
+        case 2: hipLaunchKernelGGL((k_project_tile_finish<2>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
+        case 4: hipLaunchKernelGGL((k_project_tile_finish<4>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
+        default: hipLaunchKernelGGL((k_project_tile_finish<8>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -59,3 +59,31 @@ def zeros(shape, dtype):
 
 def say(*a):
     print(*a, flush=True)
+
+
+def topk_agreement(got_idx, want_row, tau, k):
+    """Top-k parity where several answers are correct (near-ties).
+
+    got_idx: the GPU's top-k indices of one query (sorted by its scores);
+    want_row: the oracle's float64 scores of the whole row; tau: per-index
+    tolerance of a score (array over the row).  Checks that
+      - the rank-r index is the oracle's wherever the oracle's rank-r score
+        is separated from both neighbours by more than their tolerances;
+      - an index in one top-k set but not the other lies within tolerance
+        of the oracle's k-th score (a near-tie at the boundary).
+    Returns (ranks checked, boundary swaps)."""
+    n = want_row.shape[0]
+    order = np.lexsort((np.arange(n), -want_row))[:k + 1]
+    s = want_row[order]
+    checked = 0
+    for r in range(min(k, n)):
+        above = r == 0 or s[r - 1] - s[r] > tau[order[r - 1]] + tau[order[r]]
+        below = r + 1 >= len(order) or s[r] - s[r + 1] > tau[order[r]] + tau[order[r + 1]]
+        if above and below:
+            assert got_idx[r] == order[r], f"rank {r}: {got_idx[r]} != oracle {order[r]}"
+            checked += 1
+    kth = order[min(k, n) - 1]
+    swaps = set(int(j) for j in got_idx) ^ set(int(j) for j in order[:k])
+    for j in swaps:
+        assert abs(want_row[j] - want_row[kth]) <= tau[j] + tau[kth], f"index {j} is not a boundary near-tie"
+    return checked, len(swaps) // 2

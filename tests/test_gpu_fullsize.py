@@ -22,7 +22,10 @@ float64 oracle can compute one by one:
 Inputs are drawn on the device with the same generators bench.py uses; the
 oracle gets host copies of the raw inputs, never a result of the HIP path.
 Tolerances are the ones of the small-size tests: 2e-2 normwise for bf16
-outputs, 1e-3 for fp32 outputs of bf16 inputs, 1e-3 on normalised scores.
+outputs, 1e-3 for fp32 outputs of bf16 inputs.  Scores of the 57,344-dim
+store are held to SCORE_TOL = 2e-5 of |g_te| |g_tr| (the stated 1e-3 bar
+would let a typical score, about 5e-3 of that product here, be 20% off; the
+fp32-accumulated bf16 products measure about 1e-7).
 """
 import numpy as np
 import pytest
@@ -31,6 +34,9 @@ import oracle
 import workloads as W
 
 pytestmark = pytest.mark.gpu
+
+SCORE_TOL = 2e-5
+TIGHT = 1e-6      # near-tie tolerance of the full-row top-k check (measured errors <= 1.1e-7)
 
 
 def _layer_inputs(torch, gen, B, T, n_in, n_out, k, w):
@@ -260,11 +266,61 @@ def test_scores_topk_bench_launch(score_store):
         norm = np.linalg.norm(f64(te_h[qi])) * np.linalg.norm(f64(tr_h), axis=1)
         err = np.max(np.abs(row[js].astype(np.float64) - want) / norm)
         say(f"  query {q}: normalised err on {len(js)} sampled scores {err:.2e}")
-        assert err <= 1e-3
+        assert err <= SCORE_TOL
         # the filtered top-k is exactly the top-k of the full score row
         order = np.lexsort((np.arange(N), -row.astype(np.float64)))[:k]
         assert np.array_equal(ti[q], order)
         assert np.array_equal(tv[q], row[order])
+
+
+def test_scores_topk_full_rows_vs_oracle(score_store):
+    """The top-100 of four queries (0, 511, 1023 and one drawn) over all
+    500,000 store rows against the oracle: the store is copied to the host in
+    slabs of 8,192 rows (0.94 GB), the oracle scores every row, and the GPU's
+    full score rows (every one of the 2 x 10^6 scores, within SCORE_TOL and
+    within TIGHT of |g_te| |g_tr|) and its filtered top-100 (the bench's call)
+    are compared with the oracle's (R13 on near-ties at TIGHT)."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import f64, host, say, topk_agreement
+    w = W.WORKLOADS["llama3_8b_scores"]
+    ex = w.extra
+    N, Q, k = ex["N_train"], ex["Q"], ex["topk"]
+    train, te, _ = score_store
+    qs = [0, 511, 1023, int(W.rng(0, 432).integers(1, 1023))]
+    say(f"[full scores vs oracle] queries {qs}, all {N} rows, top-{k}")
+    tv = torch.empty((Q, k), dtype=torch.float32, device="cuda")
+    ti = torch.empty((Q, k), dtype=torch.int64, device="cuda")
+    P.logra_influence_scores(te, train, scores=None, topk=k, topk_val=tv, topk_idx=ti)   # bench's call
+    qd = torch.tensor(qs, device="cuda")
+    s_q = torch.empty((len(qs), N), dtype=torch.float32, device="cuda")
+    P.logra_influence_scores(te[qd].contiguous(), train, scores=s_q, topk=0)
+    torch.cuda.synchronize()
+    tv, ti, got = host(tv), host(ti), host(s_q).astype(np.float64)
+    te_h = host(te[qd].contiguous())
+    want = np.empty((len(qs), N))
+    tr_norm = np.empty(N)
+    slab = 8192
+    for r0 in range(0, N, slab):
+        r1 = min(N, r0 + slab)
+        tr_h = host(train[r0:r1])
+        want[:, r0:r1] = oracle.scores(te_h, tr_h)
+        tr_norm[r0:r1] = torch.from_numpy(tr_h.view(np.int16)).view(torch.bfloat16).double().norm(dim=1).numpy()
+        if r0 % (16 * slab) == 0:
+            say(f"  oracle rows {r0}..{r1}")
+    for qi, q in enumerate(qs):
+        scale = np.linalg.norm(f64(te_h[qi])) * tr_norm
+        err = float(np.max(np.abs(got[qi] - want[qi]) / scale))
+        assert err <= SCORE_TOL, f"query {q}: normalised err {err:.2e}"
+        # every score of the row is also within TIGHT (about ten times the measured
+        # error), so the near-tie rule may use it: far more ranks become decidable
+        assert err <= TIGHT, f"query {q}: normalised err {err:.2e}"
+        tau = TIGHT * scale
+        checked, swaps = topk_agreement(ti[q], want[qi], tau, k)
+        assert checked >= k // 2
+        assert np.all(np.abs(tv[q].astype(np.float64) - want[qi][ti[q]]) <= tau[ti[q]])
+        say(f"  query {q}: normalised err over all {N} scores {err:.2e}; top-{k}: {checked} ranks "
+            f"checked exactly, {swaps} near-tie swaps at the boundary")
 
 
 def test_relatif_bench_launch(score_store):
@@ -320,7 +376,7 @@ def test_relatif_bench_launch(score_store):
         bound = np.linalg.norm(f64(te_h[qi])) * np.linalg.norm(f64(tr_h), axis=1) / np.sqrt(self_js)
         err = float(np.max(np.abs(row[js].astype(np.float64) - want[qi]) / bound))
         say(f"  query {q}: normalised err on {len(js)} sampled scaled scores {err:.2e}")
-        assert err <= 1e-3
+        assert err <= SCORE_TOL
 
 
 def test_act_cov_gate_bench_launch():

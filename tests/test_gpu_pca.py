@@ -182,7 +182,7 @@ def test_pca_from_masked_activations_end_to_end():
     gaps = np.minimum(full[:k] - full[1:k + 1], np.concatenate([[np.inf], full[:k - 1] - full[1:k]]))
     ok = gaps >= 0.02 * full[:k]
     say(f"  {int(ok.sum())} of {k} rows well separated")
-    assert ok.sum() >= k // 2
+    assert ok.sum() >= k - 1   # this seeded spectrum: 15 of 16 (one neighbour pair is under 2% apart)
     for r in np.nonzero(ok)[0]:
         s = 1.0 if np.dot(got[r], want[r]) >= 0 else -1.0
         sin = np.sqrt(max(0.0, 1.0 - float(np.dot(f64(got[r]), want[r])) ** 2))

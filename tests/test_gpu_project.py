@@ -25,6 +25,11 @@ CASES = {
     "gpt2_qkv": ("bf16", 3, 200, 768, 2304, 16, 16, 1.0, 1e-3, True, "bf16"),
     "llama_gate": ("bf16", 2, 96, 4096, 14336, 16, 16, 1.0, 1e-4, True, "bf16"),
     "llama_down_k64": ("bf16", 2, 65, 14336, 4096, 64, 64, 1.0, 1e-4, False, "f32"),
+    # layers wider than one contraction chunk at k > 32 (chunks of 14,336 columns): the chunk
+    # partials of several slots summed per tile, and P read from each chunk's column offset;
+    # k = 64 takes the LDS-DMA path, k = 128 the register path
+    "wide_in_k64_ragged": ("bf16", 3, 90, 16384, 1024, 64, 64, 1.0, 1e-3, True, "f32"),
+    "wide_out_k128_ragged": ("bf16", 3, 70, 512, 28672, 128, 96, 1.0, 1e-3, True, "f32"),
 }
 
 
@@ -152,7 +157,7 @@ def test_project_grouped_multichunk_vs_oracle():
     slots widest first), against the oracle layer by layer."""
     import torch
     import paper_2405_13954_amd as P
-    from gpu_util import dev, host, say
+    from gpu_util import dev, host, rowwise_normwise, say
     say("[project] grouped multi-chunk layers vs oracle")
     shapes = [(13000, 1024), (1024, 9000), (4096, 4096)]
     B, T, k = 2, 70, 16
@@ -173,8 +178,8 @@ def test_project_grouped_multichunk_vs_oracle():
     for i, d in enumerate(data):
         want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], mask_np)
         g = got[:, i * D:(i + 1) * D]
-        err = np.linalg.norm(g - want) / np.linalg.norm(want)
-        say(f"  layer {i} {shapes[i]}: normwise err {err:.2e}")
+        err = rowwise_normwise(g, want)   # per example: max |diff| / max |oracle|
+        say(f"  layer {i} {shapes[i]}: normwise err per example {err:.2e}")
         assert err <= 1e-3
 
 
@@ -309,7 +314,7 @@ def test_project_reused_workspace_across_masks():
     each result equals the oracle's and a fresh-workspace launch bit for bit."""
     import torch
     import paper_2405_13954_amd as P
-    from gpu_util import dev, host, say
+    from gpu_util import dev, host, rowwise_normwise, say
     say("[project] workspace reused across launches with different masks")
     B, T, k = 4, 200, 16
     shapes = [(512, 256), (256, 4608)]
@@ -334,7 +339,7 @@ def test_project_reused_workspace_across_masks():
         for i, d in enumerate(data):
             want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], mask_np)
             gi = outs[0][:, i * D:(i + 1) * D].astype(np.float64)
-            assert np.linalg.norm(gi - want) <= 1e-3 * np.linalg.norm(want), (trial, i)
+            assert rowwise_normwise(gi[lens > 0], want[lens > 0]) <= 1e-3, (trial, i)
             assert np.all(gi[lens == 0] == 0.0)
 
 

@@ -172,7 +172,10 @@ def test_topk_real_valued_ranks():
     _, tv, ti = _scores_gpu(te, tr, topk=k, materialize=False)
     nte = np.linalg.norm(f64(te), axis=1)
     ntr = np.linalg.norm(f64(tr), axis=1)
-    for rel, min_frac in ((1e-3, 0.0), (2e-5, 0.5)):
+    # min_frac: the share of ranks whose oracle gaps on both sides exceed the tolerance on
+    # this seeded input (a property of the oracle's scores alone: 1,626 of 2,000 = 81% at 2e-5),
+    # so that the rank check cannot pass by checking nothing
+    for rel, min_frac in ((1e-3, 0.0), (2e-5, 0.8)):
         checked = 0
         for q in range(Q):
             tau = rel * nte[q] * ntr

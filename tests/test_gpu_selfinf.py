@@ -217,13 +217,14 @@ def test_relatif_end_to_end():
                              for l in range(nb)], axis=1)
     self_tr = oracle.self_influence_blocks(S64, N_COV, damp, tr)
     want = oracle.normalise_scores(oracle.scores(te_pre, tr), self_tr)
-    # the bf16 rounding of the preconditioned test gradients (2^-9 per element)
-    # dominates; 2e-3 of |g_te,pre| |g_tr| / sqrt(self_tr) bounds it
+    # the bf16 rounding of the preconditioned test gradients (at most 2^-9 per
+    # element, so at most 2^-9 of |g_te,pre| |g_tr| on a score) dominates; held to
+    # the stated 1e-3 of |g_te,pre| |g_tr| / sqrt(self_tr) (measured 6.9e-4)
     base = np.outer(np.linalg.norm(te_pre, axis=1), np.linalg.norm(f64(tr), axis=1) / np.sqrt(self_tr))
     err = float(np.max(np.abs(f64(s) - want) / base))
     say(f"  normalised err {err:.3e}")
-    assert err <= 2e-3
-    tau = 2e-3 * base
+    assert err <= 1e-3
+    tau = 1e-3 * base
     wv, wi = oracle.topk(want, k + 1)
     checked = 0
     for q in range(Q):
@@ -237,3 +238,4 @@ def test_relatif_end_to_end():
                 assert ti[q, r] == wi[q, r], (q, r)
                 checked += 1
     say(f"  {checked} of {Q * k} ranks resolvable, all agree")
+    assert checked > 0
