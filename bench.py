@@ -127,6 +127,9 @@ def write_traffic(fetch_csv, write_csv):
         "projection": ("logra::k_project_chunks<1, 1, unsigned short>", "k_project_chunks<1, 1, bf16>",
                        "7 Llama3-8B layers, B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
                        sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes),
+        "projection_k64": ("logra::k_project_tiles<4>", "k_project_tiles<4>",
+                           "7 Llama3-8B layers, B=16, T=1024, all valid, k=64", PROJ_SOURCES,
+                           16 * 1024 * per_tok + sum(2 * 64 * (a + b) for _, a, b in stream.layers)),
         "scores": ("logra::k_scores_dma", "k_scores_dma", "1,024 x 500,000 x 57,344 bf16", SCORE_SOURCES,
                    (N + Q) * D_tot * 2 + Q * N * 4),
         "self_influence": ("logra::k_self_influence_dma", "k_self_influence_dma",
@@ -180,6 +183,59 @@ class EventTimer:
 
     def mean_ms(self):
         return float(np.mean([a.elapsed_time(b) / n for a, b, n in self.pairs])) if self.pairs else float("nan")
+
+
+# -------------------------------------------------------------------- peaks --
+def peaks_leg(args, torch):
+    """Measured ceilings beside the published peaks: a sustained bf16 MFMA
+    loop on every CU (long enough for the clock to settle) and an HBM read
+    stream of 4 GiB (far above the 256 MB MALL), both timed with HIP events;
+    the MFMA kernel also reports the core clock it ran at."""
+    import paper_2405_13954_amd as P
+    L = ctypes.CDLL(os.path.join(os.path.dirname(P.LIB_PATH), "libpaper_logra_peaks.so"))
+    L.logra_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    L.logra_peak_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    props = torch.cuda.get_device_properties(0)
+    cus = props.multi_processor_count
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    groups = cus * 4                                     # four waves per SIMD
+    flops_per_iter = groups * 4 * 4 * 32768.0            # waves x 4 MFMAs x 32x32x16x2
+    iters = int(args.peak_ms * 1e-3 * BF16_PEAK_TFLOPS * 1e12 / flops_per_iter)
+    sink = torch.empty(max(groups, cus * 8), dtype=torch.float32, device="cuda")
+    cyc = torch.zeros(2, dtype=torch.int64, device="cuda")
+    t = EventTimer(torch)
+    for timed in (False, True, True, True):
+        e0 = t.start() if timed else None
+        assert L.logra_peak_mfma_bf16(groups, iters, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(cyc.data_ptr()),
+                                      stream) == 0
+        if timed:
+            t.stop(e0)
+    torch.cuda.synchronize()
+    mfma_tf = flops_per_iter * iters / (t.mean_ms() * 1e-3) / 1e12
+    cycles, ticks = (int(v) for v in cyc.cpu())
+    khz = ctypes.c_int(0)
+    wall_khz = khz.value if L.logra_peak_wall_clock_khz(ctypes.byref(khz)) == 0 else None
+    clock_ghz = cycles / (ticks / (wall_khz * 1e3)) / 1e9 if wall_khz and ticks > 0 else None
+    nbytes = 4 << 30
+    buf = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    r = EventTimer(torch)
+    for timed in (False, True, True, True, True, True):
+        e0 = r.start() if timed else None
+        assert L.logra_peak_hbm_read(ctypes.c_void_p(buf.data_ptr()), nbytes, cus * 8, ctypes.c_void_p(sink.data_ptr()),
+                                     stream) == 0
+        if timed:
+            r.stop(e0)
+    torch.cuda.synchronize()
+    read_gbs = nbytes / (r.mean_ms() * 1e-3) / 1e9
+    del buf
+    torch.cuda.empty_cache()
+    return {"mfma_bf16_tflops": mfma_tf, "mfma_frac_of_spec": mfma_tf / BF16_PEAK_TFLOPS,
+            "mfma_ms": t.mean_ms(), "mfma_clock_ghz": clock_ghz, "hbm_read_gbs": read_gbs,
+            "hbm_read_frac_of_spec": read_gbs / HBM_PEAK_GBS, "compute_units": cus,
+            "note": "sustained 32x32x16 bf16 MFMA loop on every CU for the time shown, and a 4 GiB read "
+                    "stream with 128-bit loads; published peaks 2,500 TFLOP/s and 8,000 GB/s"}
 
 
 # ------------------------------------------------------------------ logging --
@@ -431,18 +487,39 @@ def host_bf16(t):
     return t.contiguous().to("cpu").view(torch.int16).numpy().view(np.uint16)
 
 
+def host_info(threads_used):
+    """The host the oracle ran on: usable CPUs, OpenMP threads, threads the
+    sample kept busy, CPU model."""
+    import oracle
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count()
+    return {"cores": int(threads_used), "nproc": nproc, "omp_threads": oracle.num_threads(), "cpu_model": model}
+
+
 def cpu_logging_baseline(sample):
     """The oracle on the logging step's work: per-example projection of the 7
-    layers of a block (Eq. (5)) and the covariance update of their blocks,
-    over the sampled batches, repeated until about `seconds` have passed."""
+    layers of a block (Eq. (5)), parallel over (layer, example), and the
+    covariance update of their blocks, over the sampled batches, repeated
+    until about `seconds` have passed."""
     import oracle
     batches, target = sample["batches"], sample["seconds"]
     toks, passes, t0 = 0, 0, time.perf_counter()
+    nl = len(sample["p_in"])
     while True:
         for b in batches:
-            for j in range(len(b["x"])):
-                g = oracle.project_factored(b["x"][j], b["dy"][j], sample["p_in"][j], sample["p_out"][j],
-                                            b["mask"])
+            gs = oracle.project_factored_layers([(b["x"][j], b["dy"][j], sample["p_in"][j], sample["p_out"][j])
+                                                 for j in range(nl)], b["mask"])
+            for g in gs:
                 oracle.cov_accumulate(g)
             toks += int(b["mask"].sum())
         passes += 1
@@ -450,12 +527,270 @@ def cpu_logging_baseline(sample):
             break
     dt = time.perf_counter() - t0
     B, T = batches[0]["mask"].shape
-    # each sampled batch goes through one block; the step runs 32 blocks
-    return {"value": toks / (dt * sample["blocks"]), "unit": "tokens/s",
-            "cores": min(oracle.num_threads(), B), "kind": "oracle",
-            "sample": f"{len(batches)} batches of {B} examples x {T} token slots through the 7 layers "
-                      f"(projection and covariance update) of one block, {passes} passes, {toks} valid "
-                      f"tokens in {dt:.1f} s, scaled to 32 blocks"}
+    # each sampled batch goes through one block; the step runs `blocks` blocks
+    out = {"value": toks / (dt * sample["blocks"]), "unit": "tokens/s", "kind": "oracle"}
+    out.update(host_info(min(oracle.num_threads(), nl * B)))
+    out["sample"] = (f"{len(batches)} batches of {B} examples x {T} token slots through the {nl} layers "
+                     f"(projection, parallel over {nl} layers x {B} examples, and covariance update) of one "
+                     f"block, {passes} passes, {toks} valid tokens in {dt:.1f} s, scaled to {sample['blocks']} blocks")
+    return out
+
+
+# ------------------------------------------------------- k = 64 block leg --
+def block_k64_leg(args, torch, P):
+    """One Llama3-8B block at k = 64: 7 layers, B = 16, T = 1024, every token
+    valid; the fused projection into bf16 rows of 7 x 4,096, then the 7
+    covariance blocks of 4,096 x 4,096 (fp32) updated from those rows.  Two
+    distinct x / dy sets (2.7 GB each, far above the 256 MB MALL) alternate
+    between launches."""
+    w = W.WORKLOADS["llama3_8b_block"]
+    B, T, k = w.B, w.T, w.k_in
+    D, nl = k * k, len(w.layers)
+    log(f"[k64] allocating 2 x/dy sets of one block, B={B} T={T} k={k}")
+    gen = W.torch_generator(args.seed, 150)
+    sets = []
+    for _ in range(2):
+        st = []
+        for (_, ni, no) in w.layers:
+            x = torch.empty((B, T, ni), dtype=torch.bfloat16, device="cuda")
+            dy = torch.empty((B, T, no), dtype=torch.bfloat16, device="cuda")
+            W.device_normal_(x, w.x_std, gen)
+            W.device_normal_(dy, w.dy_std, gen)
+            st.append((x, dy))
+        sets.append(st)
+    projs = []
+    for (_, ni, no) in w.layers:
+        pi = torch.empty((k, ni), dtype=torch.bfloat16, device="cuda")
+        po = torch.empty((k, no), dtype=torch.bfloat16, device="cuda")
+        W.device_normal_(pi, 1.0 / np.sqrt(k), gen)
+        W.device_normal_(po, 1.0 / np.sqrt(k), gen)
+        projs.append((pi, po))
+    store = torch.empty((B, nl * D), dtype=torch.bfloat16, device="cuda")
+    S = torch.zeros((nl, D, D), dtype=torch.float32, device="cuda")
+    descs = []
+    for st in sets:
+        arr = (P.LayerDesc * nl)()
+        for j, (_, ni, no) in enumerate(w.layers):
+            arr[j] = P.LayerDesc(st[j][0].data_ptr(), st[j][1].data_ptr(), projs[j][0].data_ptr(),
+                                 projs[j][1].data_ptr(), store[:, j * D:(j + 1) * D].data_ptr(), ni, no)
+        descs.append(arr)
+    L = P.lib()
+    wsb = P.logra_project_layers_ws_size(descs[0], nl, B, T, k, k)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    def project(i):
+        rc = L.logra_project_layers(descs[i % 2], nl, P.BF16, B, T, None, k, k, P.BF16, store.stride(0),
+                                    ctypes.c_void_p(ws.data_ptr()), wsb, stream)
+        if rc != 0:
+            raise P.LograError(rc, P.logra_last_error())
+
+    def cov():
+        rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(store.data_ptr()), P.BF16, store.stride(0), B, D, nl,
+                                           ctypes.c_void_p(S.data_ptr()), stream)
+        if rc != 0:
+            raise P.LograError(rc, P.logra_last_error())
+
+    reps = args.k64_reps
+    for i in range(3):
+        project(i)
+        cov()
+    torch.cuda.synchronize()
+    pt, ct = EventTimer(torch), EventTimer(torch)
+    e0 = pt.start()
+    for i in range(reps):
+        project(i)
+    pt.stop(e0, reps)
+    e0 = ct.start()
+    for _ in range(reps):
+        cov()
+    ct.stop(e0, reps)
+    torch.cuda.synchronize()
+    tokens = B * T
+    per_tok = sum(2 * (ni + no) for _, ni, no in w.layers)
+    p_bytes = sum(2 * k * (ni + no) for _, ni, no in w.layers)
+    proj_bytes = tokens * per_tok + p_bytes
+    proj_ms = pt.mean_ms()
+    ach = proj_bytes / (proj_ms * 1e-3) / 1e9
+    # covariance: S kept symmetric needs its upper triangle read and all of it written
+    cov_bytes = nl * 4 * (D * (D + 1) // 2 + D * D) + B * nl * D * 2
+    cov_ms = ct.mean_ms()
+    cach = cov_bytes / (cov_ms * 1e-3) / 1e9
+    traffic, ratio = measured_traffic("projection_k64", PROJ_SOURCES)
+    res = {
+        "metric": "projected per-example grads/sec (tokens/s), one Llama3-8B block at k=64",
+        "value": tokens / ((proj_ms + cov_ms) * 1e-3), "unit": "tokens/s",
+        "examples_per_s": B / ((proj_ms + cov_ms) * 1e-3),
+        "proj_launch_ms": proj_ms, "cov_launch_ms": cov_ms,
+        "config": {"workload": "llama3_8b_block", "layers": nl, "B": B, "T": T, "k_in": k, "k_out": k,
+                   "store": "bf16 rows of 7 x 4,096", "covariance": "7 x 4,096 x 4,096 fp32"},
+        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBS, "traffic": traffic, "traffic_over_algorithmic": ratio,
+                     "kernel": "logra_project_layers (7 Llama3-8B layers, B=16, T=1024, k=64)",
+                     "bytes_per_launch": proj_bytes},
+        "cov_roofline": {"bound": "hbm", "achieved": cach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": cach / HBM_PEAK_GBS, "bytes_per_launch": cov_bytes,
+                         "kernel": "logra_cov_accumulate_blocks (7 blocks of 4,096, 16 bf16 rows)"},
+    }
+    sample = None
+    if args.cpu_baseline:
+        nb = args.k64_cpu_examples
+        sample = {"x": [host_bf16(sets[0][j][0][:nb]) for j in range(nl)],
+                  "dy": [host_bf16(sets[0][j][1][:nb]) for j in range(nl)],
+                  "p_in": [host_bf16(p[0]) for p in projs], "p_out": [host_bf16(p[1]) for p in projs],
+                  "seconds": args.cpu_seconds / 2}
+    del sets, store, S, ws
+    torch.cuda.empty_cache()
+    return res, sample
+
+
+def cpu_block_k64_baseline(sample):
+    """The oracle on a bounded sample of the k = 64 block: the projection of
+    the 7 layers for a few examples (parallel over layer x example) and the
+    covariance update of the 7 blocks from those examples' rows."""
+    import oracle
+    nl = len(sample["x"])
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        gs = oracle.project_factored_layers([(sample["x"][j], sample["dy"][j], sample["p_in"][j],
+                                              sample["p_out"][j]) for j in range(nl)])
+        for g in gs:
+            oracle.cov_accumulate(g)
+        passes += 1
+        if time.perf_counter() - t0 >= sample["seconds"]:
+            break
+    dt = time.perf_counter() - t0
+    B, T = sample["x"][0].shape[:2]
+    out = {"value": passes * B * T / dt, "unit": "tokens/s", "kind": "oracle"}
+    out.update(host_info(min(oracle.num_threads(), nl * B)))
+    out["sample"] = (f"{B} examples x {T} tokens through the 7 layers at k=64 (projection, parallel over "
+                     f"layer x example, and the 7 covariance updates of 4,096 x 4,096), {passes} passes in "
+                     f"{dt:.1f} s")
+    return out
+
+
+# ----------------------------------------------------- GPT-2-small leg --
+def gpt2_leg(args, torch, P):
+    """GPT-2-small logging: 12 blocks x {qkv, out, fc, proj}, B = 32, T = 512,
+    lengths U{64..512} (right padding), k = 16, one step = one batch through
+    all 48 layers, grouped 16 layers (4 blocks) per launch, into a bf16 store
+    of 48 x 256 columns, then the 48 covariance blocks of 256 x 256 updated
+    from the step's rows.  Each block has its own x / dy (403 MB per block)."""
+    w = W.WORKLOADS["gpt2_small_log"]
+    B, T, k = w.B, w.T, w.k_in
+    D, nlb = k * k, len(w.layers)
+    nl = w.blocks * nlb
+    log(f"[gpt2] allocating {w.blocks} blocks x {nlb} layers, B={B} T={T} k={k}")
+    gen = W.torch_generator(args.seed, 160)
+    tens = []
+    for blk in range(w.blocks):
+        for (_, ni, no) in w.layers:
+            x = torch.empty((B, T, ni), dtype=torch.bfloat16, device="cuda")
+            dy = torch.empty((B, T, no), dtype=torch.bfloat16, device="cuda")
+            W.device_normal_(x, w.x_std, gen)
+            W.device_normal_(dy, w.dy_std, gen)
+            pi = torch.empty((k, ni), dtype=torch.bfloat16, device="cuda")
+            po = torch.empty((k, no), dtype=torch.bfloat16, device="cuda")
+            W.device_normal_(pi, 1.0 / np.sqrt(k), gen)
+            W.device_normal_(po, 1.0 / np.sqrt(k), gen)
+            tens.append((x, dy, pi, po))
+    steps = args.gpt2_warmup + args.gpt2_steps
+    lens = [W.lengths(W.rng(args.seed, 500, st), B, w.len_lo, w.len_hi) for st in range(steps)]
+    masks = [torch.from_numpy(W.mask_from_lengths(Ls, T)).cuda() for Ls in lens]
+    store = torch.empty((steps * B, nl * D), dtype=torch.bfloat16, device="cuda")
+    S = torch.zeros((nl, D, D), dtype=torch.float32, device="cuda")
+    group = 16
+    L = P.lib()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    def descs(st, g0):
+        n = min(group, nl - g0)
+        arr = (P.LayerDesc * n)()
+        for j in range(n):
+            l = g0 + j
+            x, dy, pi, po = tens[l]
+            arr[j] = P.LayerDesc(x.data_ptr(), dy.data_ptr(), pi.data_ptr(), po.data_ptr(),
+                                 store[st * B:(st + 1) * B, l * D:(l + 1) * D].data_ptr(), x.shape[2], dy.shape[2])
+        return arr, n
+
+    all_d = [[descs(st, g0) for g0 in range(0, nl, group)] for st in range(steps)]
+    wsb = max(P.logra_project_layers_ws_size(d, n, B, T, k, k) for d, n in all_d[0])
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    pt = EventTimer(torch)
+
+    def step(st, timed):
+        e0 = pt.start() if timed else None
+        for d, n in all_d[st]:
+            rc = L.logra_project_layers(d, n, P.BF16, B, T, ctypes.c_void_p(masks[st].data_ptr()), k, k, P.BF16,
+                                        store.stride(0), ctypes.c_void_p(ws.data_ptr()), wsb, stream)
+            if rc != 0:
+                raise P.LograError(rc, P.logra_last_error())
+        if timed:
+            pt.stop(e0, len(all_d[st]))
+        rows = store[st * B:(st + 1) * B]
+        rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(rows.data_ptr()), P.BF16, store.stride(0), B, D, nl,
+                                           ctypes.c_void_p(S.data_ptr()), stream)
+        if rc != 0:
+            raise P.LograError(rc, P.logra_last_error())
+
+    for st in range(args.gpt2_warmup):
+        step(st, False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for st in range(args.gpt2_warmup, steps):
+        step(st, True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    tokens = int(sum(int(Ls.sum()) for Ls in lens[args.gpt2_warmup:]))
+    per_tok = sum(2 * (ni + no) for _, ni, no in w.layers) * (group // nlb)
+    p_bytes = sum(2 * k * (ni + no) for _, ni, no in w.layers) * (group // nlb)
+    launch_bytes = tokens / args.gpt2_steps * per_tok + p_bytes
+    ach = launch_bytes / (pt.mean_ms() * 1e-3) / 1e9
+    res = {
+        "metric": "projected per-example grads/sec (tokens/s), GPT-2-small logging (48 layers, k=16)",
+        "value": tokens / dt, "unit": "tokens/s", "examples_per_s": args.gpt2_steps * B / dt,
+        "ms_per_step": dt * 1e3 / args.gpt2_steps, "proj_launch_ms": pt.mean_ms(), "steps": args.gpt2_steps,
+        "config": {"workload": "gpt2_small_log", "blocks": w.blocks, "layers": nl, "B": B, "T": T,
+                   "len_range": [w.len_lo, w.len_hi], "k_in": k, "k_out": k, "layers_per_launch": group},
+        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "logra_project_layers (16 GPT-2-small layers, B=32 ragged, k=16)",
+                     "bytes_per_launch": launch_bytes},
+    }
+    sample = None
+    if args.cpu_baseline:
+        sample = {"x": [host_bf16(t[0]) for t in tens[:nlb]], "dy": [host_bf16(t[1]) for t in tens[:nlb]],
+                  "p_in": [host_bf16(t[2]) for t in tens[:nlb]], "p_out": [host_bf16(t[3]) for t in tens[:nlb]],
+                  "mask": W.mask_from_lengths(lens[0], T), "blocks": w.blocks, "seconds": args.cpu_seconds / 2}
+    del tens, store, S, ws
+    torch.cuda.empty_cache()
+    return res, sample
+
+
+def cpu_gpt2_baseline(sample):
+    """The oracle on one block of one GPT-2-small batch (the 4 layers,
+    parallel over layer x example, and their covariance updates), repeated for
+    about `seconds`, scaled to the 12 blocks of a step."""
+    import oracle
+    nl = len(sample["x"])
+    toks, passes, t0 = 0, 0, time.perf_counter()
+    while True:
+        gs = oracle.project_factored_layers([(sample["x"][j], sample["dy"][j], sample["p_in"][j],
+                                              sample["p_out"][j]) for j in range(nl)], sample["mask"])
+        for g in gs:
+            oracle.cov_accumulate(g)
+        toks += int(sample["mask"].sum())
+        passes += 1
+        if time.perf_counter() - t0 >= sample["seconds"]:
+            break
+    dt = time.perf_counter() - t0
+    B, T = sample["mask"].shape
+    out = {"value": toks / (dt * sample["blocks"]), "unit": "tokens/s", "kind": "oracle"}
+    out.update(host_info(min(oracle.num_threads(), nl * B)))
+    out["sample"] = (f"one batch of {B} examples x {T} token slots through the {nl} layers of one block "
+                     f"(projection and covariance update), {passes} passes, {toks} valid tokens in {dt:.1f} s, "
+                     f"scaled to {sample['blocks']} blocks")
+    return out
 
 
 # ---------------------------------------------------------------- influence --
@@ -650,9 +985,10 @@ def cpu_influence_baseline(sample):
     oracle.topk(s, sample["topk"])
     dt = time.perf_counter() - t0
     q, n = s.shape
-    return {"value": q * n / dt, "unit": "scores/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": f"{q} queries x {n} stored gradients (224 blocks preconditioned, scores, top-100); "
-                      f"{dt:.1f} s"}
+    out = {"value": q * n / dt, "unit": "scores/s", "kind": "oracle"}
+    out.update(host_info(oracle.num_threads()))
+    out["sample"] = f"{q} queries x {n} stored gradients (224 blocks preconditioned, scores, top-100); {dt:.1f} s"
+    return out
 
 
 # --------------------------------------------------------------------- main --
@@ -664,7 +1000,14 @@ def main():
     ap.add_argument("--inf-passes", type=int, default=3)
     ap.add_argument("--n-train", type=int, default=0, help="override stored-gradient count (testing)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--leg", choices=["all", "log", "influence"], default="all")
+    ap.add_argument("--leg", choices=["all", "log", "influence", "k64", "gpt2"], default="all")
+    ap.add_argument("--k64-reps", type=int, default=20, help="timed launches of the k = 64 block leg")
+    ap.add_argument("--no-peaks", dest="peaks", action="store_false",
+                    help="skip the measured MFMA and HBM ceilings")
+    ap.add_argument("--peak-ms", type=float, default=60.0, help="duration of the MFMA ceiling loop at spec rate")
+    ap.add_argument("--k64-cpu-examples", type=int, default=4, help="examples in the k = 64 oracle sample")
+    ap.add_argument("--gpt2-steps", type=int, default=10, help="timed steps of the GPT-2-small leg")
+    ap.add_argument("--gpt2-warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
     ap.add_argument("--no-relatif", dest="relatif", action="store_false",
                     help="skip the l-RelatIF sub-leg (self-influence + scaled scores)")
@@ -708,6 +1051,11 @@ def main():
            "config": {"workload": "llama3_8b_stream", "blocks": 32, "layers": 224, "B": 8, "T": 2048,
                       "len_range": [128, 2048], "k_in": 16, "k_out": 16, "store": "bf16 rows of 57,344"}}
     log_sample = inf_sample = None
+    peaks = None
+    if args.peaks:
+        log("[peaks] MFMA loop and HBM read stream")
+        peaks = peaks_leg(args, torch)
+        out["peaks"] = peaks
     if args.leg in ("all", "log"):
         r, log_sample = logging_leg(args, torch, P)
         out.update(value=r["tokens_per_s"], ms_per_step=r["ms_per_step"], examples_per_s=r["examples_per_s"],
@@ -715,6 +1063,13 @@ def main():
         for key in ("pca", "shared_inputs", "offload"):
             if key in r:
                 out[key] = r[key]
+    k64_sample = gpt2_sample = None
+    if args.leg in ("all", "k64"):
+        r, k64_sample = block_k64_leg(args, torch, P)
+        out["llama3_8b_block"] = r
+    if args.leg in ("all", "gpt2"):
+        r, gpt2_sample = gpt2_leg(args, torch, P)
+        out["gpt2_small_log"] = r
     if args.leg in ("all", "influence"):
         r, inf_sample = influence_leg(args, torch, P)
         out["influence"] = r
@@ -722,9 +1077,23 @@ def main():
         if log_sample is not None:
             log("[cpu] oracle on the logging sample")
             out["cpu_baseline"] = cpu_logging_baseline(log_sample)
+        if k64_sample is not None:
+            log("[cpu] oracle on the k = 64 block sample")
+            out["llama3_8b_block"]["cpu_baseline"] = cpu_block_k64_baseline(k64_sample)
+        if gpt2_sample is not None:
+            log("[cpu] oracle on the GPT-2-small sample")
+            out["gpt2_small_log"]["cpu_baseline"] = cpu_gpt2_baseline(gpt2_sample)
         if inf_sample is not None:
             log("[cpu] oracle on the influence sample")
             out.setdefault("influence", {})["cpu_baseline"] = cpu_influence_baseline(inf_sample)
+    if peaks is not None:   # each roofline also against the measured ceiling of its bound
+        for r in [out.get("roofline"), out.get("influence", {}).get("roofline"),
+                  out.get("influence", {}).get("relatif", {}).get("roofline"),
+                  out.get("llama3_8b_block", {}).get("roofline"), out.get("llama3_8b_block", {}).get("cov_roofline"),
+                  out.get("gpt2_small_log", {}).get("roofline")]:
+            if r:
+                ceil = peaks["hbm_read_gbs"] if r["bound"] == "hbm" else peaks["mfma_bf16_tflops"]
+                r["frac_of_measured_peak"] = r["achieved"] / ceil
     print(json.dumps(out), flush=True)
 
 

@@ -1,0 +1,43 @@
+/*
+ * logra_peaks.h -- measured ceilings of the GPU the LoGra library runs on
+ * (a separate library, libpaper_logra_peaks.so; not part of the hot path).
+ *
+ * The roofline fractions of the library's kernels are quoted against the
+ * published MI355X peaks (HBM 8 TB/s, dense bf16 MFMA 2.5 PFLOP/s).  These
+ * two kernels measure what the chip sustains under the same kind of load, so
+ * that a fraction can also be read against a measured ceiling:
+ *
+ * logra_peak_mfma_bf16: every wave issues `iters` rounds of four independent
+ *   32x32x16 bf16 MFMAs (fp32 accumulation), 4 x 32,768 flops per round, on a
+ *   grid of `groups` workgroups of 256 threads; the caller times the launch.
+ *   cycles_out (device, 2 x int64, may be NULL) receives, for workgroup 0,
+ *   the core-clock cycles and the constant-rate wall-clock ticks between its
+ *   first and last MFMA round (hipDeviceAttributeWallClockRate gives the
+ *   wall-clock rate in kHz), hence the clock the MFMA loop ran at.
+ *   sink (device, `groups` floats) receives a checksum per workgroup.
+ * logra_peak_hbm_read: streams `bytes` (a multiple of 16) from device memory
+ *   with 128-bit loads, four in flight per thread, on `groups` workgroups of
+ *   256 threads; sink (device, `groups` floats) receives a checksum.
+ *
+ * Both are asynchronous on `stream` and return a logra status code
+ * (0 = OK, -1 = invalid argument, -3 = HIP error).
+ */
+#ifndef LOGRA_PEAKS_H
+#define LOGRA_PEAKS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int64_t *cycles_out, void *stream);
+int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, float *sink, void *stream);
+/* The constant rate of the wall clock read by logra_peak_mfma_bf16, in kHz, of the current device. */
+int logra_peak_wall_clock_khz(int *khz);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LOGRA_PEAKS_H */

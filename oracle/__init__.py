@@ -57,6 +57,7 @@ def lib():
         proj = [vp, vp, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp]
         L.oracle_project_factored.argtypes = proj
         L.oracle_project_dense.argtypes = proj
+        L.oracle_project_factored_layers.argtypes = [i32, vp, vp, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, vp]
         L.oracle_cov_accumulate.argtypes = [vp, i32, i64, i32, i32, vp]
         L.oracle_precondition.argtypes = [vp, i32, i64, f64, vp, i32, i64, i32, vp, i64, vp]
         L.oracle_scores.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, vp, i64]
@@ -65,7 +66,8 @@ def lib():
         L.oracle_normalise_scores.argtypes = [vp, i64, i32, i64, vp, vp]
         L.oracle_act_cov.argtypes = [vp, i32, i32, i32, i32, vp, vp]
         L.oracle_num_threads.argtypes = []
-        for name in ("oracle_project_factored", "oracle_project_dense", "oracle_cov_accumulate",
+        for name in ("oracle_project_factored", "oracle_project_factored_layers", "oracle_project_dense",
+                     "oracle_cov_accumulate",
                      "oracle_precondition", "oracle_scores", "oracle_topk", "oracle_self_influence",
                      "oracle_normalise_scores", "oracle_act_cov", "oracle_num_threads"):
             getattr(L, name).restype = ctypes.c_int
@@ -120,6 +122,34 @@ def project_factored(x, dy, p_in, p_out, mask=None) -> np.ndarray:
     """Eq. (5) right side: G_b = sum_t (P_out dy_t)(P_in x_t)^T over unmasked tokens.
     Returns [B, k_out*k_in] float64, flat index o*k_in + i."""
     return _project(lib().oracle_project_factored, x, dy, p_in, p_out, mask)
+
+
+def project_factored_layers(layers, mask=None) -> list:
+    """project_factored for several layers of one batch, parallel over (layer, example).
+    layers: list of (x, dy, p_in, p_out) of one dtype, shared B, T, k_in, k_out.
+    Returns one [B, k_out*k_in] float64 array per layer."""
+    n = len(layers)
+    layers = [tuple(map(_c, L)) for L in layers]
+    x0, _, pi0, po0 = layers[0]
+    B, T, _ = x0.shape
+    k_in, k_out = pi0.shape[0], po0.shape[0]
+    code = _code(x0)
+    for x, dy, pi, po in layers:
+        assert all(_code(a) == code for a in (x, dy, pi, po))
+        assert x.shape[:2] == (B, T) and dy.shape[:2] == (B, T)
+        assert pi.shape == (k_in, x.shape[2]) and po.shape == (k_out, dy.shape[2])
+    if mask is not None:
+        mask = np.ascontiguousarray(mask.astype(np.uint8, copy=False))
+        assert mask.shape == (B, T)
+    gs = [np.zeros((B, k_out * k_in), dtype=np.float64) for _ in range(n)]
+    ptrs = lambda arrs: (ctypes.c_void_p * n)(*[a.ctypes.data for a in arrs])
+    ints = lambda v: (ctypes.c_int * n)(*v)
+    rc = lib().oracle_project_factored_layers(
+        n, ptrs([L[0] for L in layers]), ptrs([L[1] for L in layers]), code, B, T,
+        ints([L[0].shape[2] for L in layers]), ints([L[1].shape[2] for L in layers]), _ptr(mask),
+        ptrs([L[2] for L in layers]), ptrs([L[3] for L in layers]), k_in, k_out, ptrs(gs))
+    _check(rc, "oracle_project_factored_layers")
+    return gs
 
 
 def project_dense(x, dy, p_in, p_out, mask=None) -> np.ndarray:

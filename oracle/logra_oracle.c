@@ -67,6 +67,36 @@ static int dtype_ok(int d) { return d == OR_F32 || d == OR_BF16 || d == OR_F64; 
 /* p_out: [k_out][n_out] (all of dtype in_dtype); mask: [B][T] or NULL.     */
 /* g: [B][k_out * k_in] doubles, overwritten.                               */
 /* ------------------------------------------------------------------------ */
+/* One example b of the factored projection; g_b (k_out * k_in doubles) is
+ * overwritten.  Scratch: xp (k_in) and dp (k_out) doubles. */
+static void project_example(const void *x, const void *dy, int in_dtype, int b, int T, int n_in,
+                            int n_out, const uint8_t *mask, const void *p_in, const void *p_out,
+                            int k_in, int k_out, double *gb, double *xp, double *dp) {
+    int64_t D = (int64_t)k_in * k_out;
+    for (int64_t d = 0; d < D; ++d) gb[d] = 0.0;
+    for (int t = 0; t < T; ++t) {
+        int64_t bt = (int64_t)b * T + t;
+        if (mask && mask[bt] == 0) continue; /* masked: never read */
+        /* x' = P_in x_t */
+        for (int i = 0; i < k_in; ++i) {
+            double s = 0.0;
+            for (int j = 0; j < n_in; ++j)
+                s += widen(p_in, in_dtype, (int64_t)i * n_in + j) * widen(x, in_dtype, bt * n_in + j);
+            xp[i] = s;
+        }
+        /* dy' = P_out Dx_{o,t} */
+        for (int o = 0; o < k_out; ++o) {
+            double s = 0.0;
+            for (int j = 0; j < n_out; ++j)
+                s += widen(p_out, in_dtype, (int64_t)o * n_out + j) * widen(dy, in_dtype, bt * n_out + j);
+            dp[o] = s;
+        }
+        /* outer product dy' x'^T, accumulated over tokens */
+        for (int o = 0; o < k_out; ++o)
+            for (int i = 0; i < k_in; ++i) gb[(int64_t)o * k_in + i] += dp[o] * xp[i];
+    }
+}
+
 int oracle_project_factored(const void *x, const void *dy, int in_dtype, int B, int T,
                             int n_in, int n_out, const uint8_t *mask, const void *p_in,
                             const void *p_out, int k_in, int k_out, double *g) {
@@ -75,36 +105,39 @@ int oracle_project_factored(const void *x, const void *dy, int in_dtype, int B, 
     int64_t D = (int64_t)k_in * k_out;
 #pragma omp parallel for schedule(dynamic, 1)
     for (int b = 0; b < B; ++b) {
-        double *gb = g + (int64_t)b * D;
         double *xp = (double *)malloc(sizeof(double) * (size_t)k_in);
         double *dp = (double *)malloc(sizeof(double) * (size_t)k_out);
-        for (int64_t d = 0; d < D; ++d) gb[d] = 0.0;
-        for (int t = 0; t < T; ++t) {
-            int64_t bt = (int64_t)b * T + t;
-            if (mask && mask[bt] == 0) continue; /* masked: never read */
-            /* x' = P_in x_t */
-            for (int i = 0; i < k_in; ++i) {
-                double s = 0.0;
-                for (int j = 0; j < n_in; ++j)
-                    s += widen(p_in, in_dtype, (int64_t)i * n_in + j) *
-                         widen(x, in_dtype, bt * n_in + j);
-                xp[i] = s;
-            }
-            /* dy' = P_out Dx_{o,t} */
-            for (int o = 0; o < k_out; ++o) {
-                double s = 0.0;
-                for (int j = 0; j < n_out; ++j)
-                    s += widen(p_out, in_dtype, (int64_t)o * n_out + j) *
-                         widen(dy, in_dtype, bt * n_out + j);
-                dp[o] = s;
-            }
-            /* outer product dy' x'^T, accumulated over tokens */
-            for (int o = 0; o < k_out; ++o)
-                for (int i = 0; i < k_in; ++i) gb[(int64_t)o * k_in + i] += dp[o] * xp[i];
-        }
+        project_example(x, dy, in_dtype, b, T, n_in, n_out, mask, p_in, p_out, k_in, k_out, g + (int64_t)b * D,
+                        xp, dp);
         free(xp);
         free(dp);
     }
+    return OR_OK;
+}
+
+/* The same projection for n_layers layers of one batch (shared B, T, mask,
+ * k_in, k_out, dtype; layer l has its own tensors, widths and output
+ * g[l], [B][k_out * k_in]).  Each (layer, example) is computed exactly as
+ * above; only the parallel loop runs over the pairs. */
+int oracle_project_factored_layers(int n_layers, const void *const *x, const void *const *dy, int in_dtype,
+                                   int B, int T, const int *n_in, const int *n_out, const uint8_t *mask,
+                                   const void *const *p_in, const void *const *p_out, int k_in, int k_out,
+                                   double *const *g) {
+    if (n_layers < 0 || B < 0 || T < 0 || k_in <= 0 || k_out <= 0 || !dtype_ok(in_dtype))
+        return OR_ERR_INVALID_ARG;
+    for (int l = 0; l < n_layers; ++l)
+        if (n_in[l] <= 0 || n_out[l] <= 0) return OR_ERR_INVALID_ARG;
+    int64_t D = (int64_t)k_in * k_out;
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int l = 0; l < n_layers; ++l)
+        for (int b = 0; b < B; ++b) {
+            double *xp = (double *)malloc(sizeof(double) * (size_t)k_in);
+            double *dp = (double *)malloc(sizeof(double) * (size_t)k_out);
+            project_example(x[l], dy[l], in_dtype, b, T, n_in[l], n_out[l], mask, p_in[l], p_out[l], k_in, k_out,
+                            g[l] + (int64_t)b * D, xp, dp);
+            free(xp);
+            free(dp);
+        }
     return OR_OK;
 }
 

@@ -12,6 +12,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJ_DIR = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(HERE, "libpaper_logra.so")
+PEAKS_SRC = os.path.join(HERE, "peaks", "peaks.hip")
+PEAKS_LIB = os.path.join(HERE, "libpaper_logra_peaks.so")
 ARCH = "gfx950"
 
 FLAGS = [
@@ -59,7 +61,18 @@ def build(jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    build_peaks()
     return LIB
+
+
+def build_peaks() -> str:
+    """The measured-ceiling kernels (a library of their own, not the hot path)."""
+    tmp = PEAKS_LIB + ".tmp"
+    r = subprocess.run(["hipcc", *FLAGS, "-shared", PEAKS_SRC, "-o", tmp], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {PEAKS_SRC}:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, PEAKS_LIB)
+    return PEAKS_LIB
 
 
 if __name__ == "__main__":

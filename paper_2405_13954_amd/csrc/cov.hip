@@ -34,9 +34,43 @@ __device__ __forceinline__ void tile_coords(int t, int nt, int &ti, int &tj) {
 
 // Add the computed 64x64 tile c (LDS, row-major with stride CT+1) into S and
 // mirror it.  Diagonal tiles only use entries r <= c of the upper triangle.
+// Off-diagonal tiles of an S whose rows are 16-byte aligned and whose edge is
+// a multiple of 64 take the vector form: thread t owns row t / 4 of the tile
+// and its 16 columns 16 (t % 4) .. +15, loads them as four 128-bit loads all
+// in flight at once, adds, stores, and writes the mirrored tile the same way
+// (row t / 4 of the transposed tile, gathered from LDS).
 template <typename TS>
 __device__ __forceinline__ void add_and_mirror(TS *S, int D, int I, int J, TS *ct, bool diag) {
     const int tid = threadIdx.x;
+    if constexpr (sizeof(TS) == 4) {
+        if (!diag && D % CT == 0 && (reinterpret_cast<uintptr_t>(S) & 15) == 0) {
+            const int r = tid >> 2, c0 = 16 * (tid & 3);
+            f32x4 *row = reinterpret_cast<f32x4 *>(S + static_cast<size_t>(I + r) * D + J + c0);
+            f32x4 v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = row[u];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    v[u][e] += ct[r * (CT + 1) + c0 + 4 * u + e];
+                    ct[r * (CT + 1) + c0 + 4 * u + e] = v[u][e];
+                }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) row[u] = v[u];
+            __syncthreads();
+            // mirrored: S[J + c][I + i] = tile[i][c], thread t writes c = t / 4, i = 16 (t % 4) .. +15
+            f32x4 *mrow = reinterpret_cast<f32x4 *>(S + static_cast<size_t>(J + r) * D + I + c0);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                f32x4 m;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) m[e] = ct[(c0 + 4 * u + e) * (CT + 1) + r];
+                mrow[u] = m;
+            }
+            return;
+        }
+    }
     for (int e = tid; e < CT * CT; e += blockDim.x) {
         const int r = e / CT, c = e - (e / CT) * CT;
         const int i = I + r, j = J + c;

@@ -32,7 +32,7 @@
 //     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
 //     formed by fp32 MFMAs straight from those sums (one wave per 16-row block
 //     of G).  Empty tiles give 0.
-//  C. k_project_reduce: per example, the tile sums are added in tile order
+//  C. k_project_reduce: per example (and 256-wide output slice), the tile sums are added in tile order
 //     and G_b is written (fp32 or bf16, round to nearest even) to the
 //     caller's store row.
 // Every sum has a fixed order, so results are bitwise reproducible.
@@ -861,23 +861,24 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
 template <typename TOut>
 __global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, int B,
                                                         int tpe, int D, int64_t g_ld) {
+    // blockIdx.x: (layer, example); blockIdx.y: a 256-wide slice of the D outputs
     const int l = blockIdx.x / B;
     const int b = blockIdx.x - l * B;
-    const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * D;
+    const int i = blockIdx.y * 256 + threadIdx.x;
+    if (i >= D) return;
+    const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * D + i;
     TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
-    for (int i = threadIdx.x; i < D; i += blockDim.x) {
-        float s = 0.f;
-        int t = 0;
-        for (; t + 8 <= tpe; t += 8) {   // eight loads in flight, summed in tile order
-            float v[8];
+    float s = 0.f;
+    int t = 0;
+    for (; t + 8 <= tpe; t += 8) {   // eight loads in flight, summed in tile order
+        float v[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * D + i];
+        for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * D];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) s += v[u];
-        }
-        for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * D + i];
-        store_out<TOut>(out + i, s);
+        for (int u = 0; u < 8; ++u) s += v[u];
     }
+    for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * D];
+    store_out<TOut>(out + i, s);
 }
 
 inline int kt_for(int k_in, int k_out) {
@@ -1094,11 +1095,12 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned grid = static_cast<unsigned>(grp.n_layers) * B;
+    const unsigned slices = static_cast<unsigned>((k_in * k_out + 255) / 256);
     if (bf16_out)
-        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid, slices), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
                            k_in * k_out, g_ld);
     else
-        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid, slices), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
                            k_in * k_out, g_ld);
     return hipGetLastError();
 }

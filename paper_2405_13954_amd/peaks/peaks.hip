@@ -1,0 +1,84 @@
+// Measured ceilings: a sustained bf16 MFMA loop and an HBM read stream (see
+// include/logra_peaks.h).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "logra_peaks.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void k_peak_mfma(int64_t iters, float *sink, int64_t *cycles) {
+    const int tid = threadIdx.x;
+    // operands that the compiler cannot fold: small values from the thread index
+    bf16x8 a, b;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        a[e] = static_cast<__bf16>(static_cast<float>((tid + e) & 7) * 0.125f);
+        b[e] = static_cast<__bf16>(static_cast<float>((tid * 3 + e) & 7) * 0.0625f);
+    }
+    f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+    const long long t0 = clock64(), w0 = wall_clock64();
+    for (int64_t i = 0; i < iters; ++i) {
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+        c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+    }
+    const long long t1 = clock64(), w1 = wall_clock64();
+    float s = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += c0[r] + c1[r] + c2[r] + c3[r];
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (tid == 0) {
+        sink[blockIdx.x] = s;
+        if (cycles && blockIdx.x == 0) {
+            cycles[0] = t1 - t0;
+            cycles[1] = w1 - w0;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_peak_read(const u32x4 *buf, int64_t n, float *sink) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+    int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    uint32_t x = 0;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const u32x4 v0 = buf[i], v1 = buf[i + stride], v2 = buf[i + 2 * stride], v3 = buf[i + 3 * stride];
+        x ^= v0[0] ^ v0[1] ^ v0[2] ^ v0[3] ^ v1[0] ^ v1[1] ^ v1[2] ^ v1[3];
+        x ^= v2[0] ^ v2[1] ^ v2[2] ^ v2[3] ^ v3[0] ^ v3[1] ^ v3[2] ^ v3[3];
+    }
+    for (; i < n; i += stride) {
+        const u32x4 v = buf[i];
+        x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+    }
+    for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o, 64);
+    if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(x & 0xffff);
+}
+
+}  // namespace
+
+extern "C" int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int64_t *cycles_out, void *stream) {
+    if (groups <= 0 || iters <= 0 || sink == nullptr) return -1;
+    hipLaunchKernelGGL(k_peak_mfma, dim3(groups), dim3(256), 0, static_cast<hipStream_t>(stream), iters, sink,
+                       cycles_out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, float *sink, void *stream) {
+    if (buf == nullptr || sink == nullptr || groups <= 0 || bytes == 0 || bytes % 16 != 0 ||
+        (reinterpret_cast<uintptr_t>(buf) & 15) != 0)
+        return -1;
+    hipLaunchKernelGGL(k_peak_read, dim3(groups), dim3(256), 0, static_cast<hipStream_t>(stream),
+                       static_cast<const u32x4 *>(buf), static_cast<int64_t>(bytes / 16), sink);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int logra_peak_wall_clock_khz(int *khz) {
+    int dev = 0;
+    if (khz == nullptr || hipGetDevice(&dev) != hipSuccess) return -1;
+    return hipDeviceGetAttribute(khz, hipDeviceAttributeWallClockRate, dev) == hipSuccess ? 0 : -3;
+}

@@ -238,3 +238,26 @@ def test_f64_statistics_validation(L):
     assert f(*args(Q=0)) == P.OK
     assert f(*args()) == P.ERR_INVALID_ARG                     # passes the dtype checks; NULL top-k buffers
     assert "topk_val" in P.logra_last_error()
+
+
+def test_peaks_library_exports_and_validation():
+    """The measured-ceiling library (include/logra_peaks.h) loads, exports what
+    its header declares, and refuses bad arguments before any launch."""
+    path = os.path.join(os.path.dirname(P.LIB_PATH), "libpaper_logra_peaks.so")
+    if not os.path.exists(path):
+        pytest.fail("libpaper_logra_peaks.so is not built (run __graft_entry__.build())")
+    src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "logra_peaks.h")).read(), flags=re.S)
+    syms = sorted(set(re.findall(r"\b(logra_[a-z_0-9]+)\s*\(", src)))
+    K = ctypes.CDLL(path)
+    assert syms == ["logra_peak_hbm_read", "logra_peak_mfma_bf16", "logra_peak_wall_clock_khz"]
+    for s in syms:
+        assert hasattr(K, s)
+    K.logra_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    K.logra_peak_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    fake = ctypes.c_void_p(0x1000)
+    assert K.logra_peak_mfma_bf16(0, 10, fake, None, None) == -1
+    assert K.logra_peak_mfma_bf16(4, 10, None, None, None) == -1
+    assert K.logra_peak_hbm_read(fake, 24, 4, fake, None) == -1       # not a multiple of 16
+    assert K.logra_peak_hbm_read(None, 32, 4, fake, None) == -1

@@ -476,3 +476,16 @@ def test_pca_topk_kfac_kronecker_structure():
     assert _rel(PH[0], np.kron(PF[0], PB[0])) < 1e-10
     Pk = np.kron(PF, PB)
     assert _rel(Pk @ H @ Pk.T, np.diag(np.kron(wF, wB))) < 1e-12
+
+
+def test_project_layers_form_equals_per_layer_calls():
+    """The (layer, example)-parallel form computes each layer exactly as its own
+    call (same per-example arithmetic; only the parallel loop differs), with
+    layers of different widths and a ragged mask that empties one example."""
+    lens = np.array([20, 0, 7])
+    ds = [W.layer_inputs(3, j, 3, 20, ni, no, 4, 6, 1.0, 1.0, "bf16", lens)
+          for j, (ni, no) in enumerate([(16, 24), (40, 8), (8, 32)])]
+    gs = oracle.project_factored_layers([(d["x"], d["dy"], d["p_in"], d["p_out"]) for d in ds], ds[0]["mask"])
+    for d, g in zip(ds, gs):
+        assert np.array_equal(g, oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], d["mask"]))
+    assert np.all(gs[1][1] == 0.0)
