@@ -866,6 +866,8 @@ def influence_leg(args, torch, P):
         res["relatif"] = relatif_sub_leg(args, torch, P, S, Nc, ex["damp"], pre, train, topk, sws, tv, ti)
     if args.ooc_rows > 0:
         res["out_of_core"] = out_of_core_sub_leg(args, torch, P, pre, train, topk)
+    if args.ooc_file_rows > 0:
+        res["store_file"] = store_file_sub_leg(args, torch, P, pre, train, topk)
     if args.vendor_gemm:
         # the same operands through torch's library GEMM (hipBLASLt) and through this
         # library's scores-only path, on a 125,000-row slice (context for the roofline)
@@ -974,6 +976,85 @@ def out_of_core_sub_leg(args, torch, P, pre, train, topk):
                          "kernel": "host-to-device stream of the store (copies overlapped with scoring)"}}
 
 
+def store_file_sub_leg(args, torch, P, pre, train, topk):
+    """The disk tier of the out-of-core store: `ooc_file_rows` store rows
+    written from the device to a file with write-behind (logra_offload_rows_file,
+    two pinned buffers of one batch each), flushed to the device, then scored
+    from the file with logra_influence_stream_file (reader thread, pinned
+    double buffer, device double buffer).  The file's pages are evicted from
+    the page cache (posix_fadvise) before each pass, so the reads come from the
+    disk; the bound is the disk's read rate, measured beside it with plain
+    sequential reads of the same file into pinned memory."""
+    import shutil
+    import tempfile
+    n = min(args.ooc_file_rows, train.shape[0])
+    Q, D = pre.shape
+    rb = D * 2
+    nbytes = n * rb
+    tmpdir = os.environ.get("TMPDIR", tempfile.gettempdir())
+    free = shutil.disk_usage(tmpdir).free
+    if free < 2 * nbytes:
+        return {"skipped": f"{free / 1e9:.1f} GB free in {tmpdir}, need {2 * nbytes / 1e9:.1f}"}
+    log(f"[inf] store file: {n} rows ({nbytes / 1e9:.2f} GB) in {tmpdir}")
+    fd_, path = tempfile.mkstemp(prefix="logra_store_", dir=tmpdir)
+    os.close(fd_)
+    batch = args.ooc_file_batch
+    try:
+        fd = os.open(path, os.O_RDWR | os.O_TRUNC)
+        bufs = [torch.empty(batch * rb, dtype=torch.uint8).pin_memory() for _ in range(2)]
+        events, stats = [], []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i, r0 in enumerate(range(0, n, batch)):
+            if i >= 2:
+                events[i - 2].synchronize()
+            st, ev = ctypes.c_int(-7), torch.cuda.Event()
+            P.logra_offload_rows_file(train[r0:min(n, r0 + batch)], fd, r0 * rb, bufs[i % 2], io_status=st, done=ev)
+            events.append(ev)
+            stats.append(st)
+        torch.cuda.synchronize()
+        t_write = time.perf_counter() - t0
+        os.fsync(fd)
+        t_sync = time.perf_counter() - t0
+        os.close(fd)
+        assert all(st.value == P.OK for st in stats), "a store write failed"
+        # evict the file's pages, so that the stream reads the disk, not the page cache
+        fd = os.open(path, os.O_RDONLY)
+        os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+        os.close(fd)
+        chunk = min(args.ooc_file_chunk, n)
+        hb = torch.empty(2 * ((chunk * rb + 255) // 256 * 256), dtype=torch.uint8).pin_memory()
+        tv = torch.empty((Q, topk), dtype=torch.float32, device=train.device)
+        ti = torch.empty((Q, topk), dtype=torch.int64, device=train.device)
+        ws = torch.empty(P.logra_influence_stream_file_ws_size(Q, chunk, D, P.BF16, topk), dtype=torch.uint8,
+                         device=train.device)
+        fd = os.open(path, os.O_RDONLY)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        P.logra_influence_stream_file(pre, fd, 0, n, D, P.BF16, topk, tv, ti, chunk, hb, ws=ws)   # synchronous
+        t_stream = time.perf_counter() - t0
+        os.posix_fadvise(fd, 0, 0, os.POSIX_FADV_DONTNEED)
+        # the disk alone: the same file read sequentially into the same pinned buffer
+        view = hb[: chunk * rb].numpy()
+        t0 = time.perf_counter()
+        for r0 in range(0, n, chunk):
+            rows = min(chunk, n - r0)
+            os.preadv(fd, [memoryview(view[: rows * rb])], r0 * rb)
+        t_read = time.perf_counter() - t0
+        os.close(fd)
+        gbs, read_gbs = nbytes / t_stream / 1e9, nbytes / t_read / 1e9
+        return {"rows": n, "chunk_rows": chunk, "read_mode": "page cache evicted before each pass", "dir": tmpdir,
+                "write_gbs": nbytes / t_write / 1e9, "write_gbs_with_fsync": nbytes / t_sync / 1e9,
+                "ms_per_pass": t_stream * 1e3, "scores_per_s": Q * n / t_stream,
+                "roofline": {"bound": "disk", "achieved": gbs, "peak": read_gbs, "unit": "GB/s",
+                             "frac": gbs / read_gbs,
+                             "kernel": "store file streamed through the reader thread and two pinned buffers "
+                                       "(scoring overlapped)",
+                             "peak_is": "plain sequential reads of the same file into pinned memory"}}
+    finally:
+        os.unlink(path)
+
+
 def cpu_influence_baseline(sample):
     import oracle
     D = sample["D"]
@@ -1021,6 +1102,10 @@ def main():
     ap.add_argument("--ooc-rows", type=int, default=131072,
                     help="rows of the out-of-core sub-leg's pinned host store (0 = skip)")
     ap.add_argument("--ooc-chunk", type=int, default=32768, help="rows per streamed chunk")
+    ap.add_argument("--ooc-file-rows", type=int, default=16384,
+                    help="rows of the store-file sub-leg (written to TMPDIR, then streamed; 0 = skip)")
+    ap.add_argument("--ooc-file-batch", type=int, default=1024, help="rows per write-behind batch")
+    ap.add_argument("--ooc-file-chunk", type=int, default=2048, help="rows per chunk read from the store file")
     ap.add_argument("--no-vendor-gemm", dest="vendor_gemm", action="store_false",
                     help="skip timing torch.matmul (hipBLASLt) on a slice of the score GEMM's operands")
     ap.add_argument("--cpu-batches", type=int, default=2, help="logging batches in the oracle sample")

@@ -45,7 +45,8 @@ typedef enum {
     LOGRA_ERR_UNSUPPORTED = -2, /* valid request beyond a compiled limit */
     LOGRA_ERR_HIP = -3,         /* a HIP runtime call failed */
     LOGRA_ERR_NOT_PD = -4,      /* damped covariance is not positive definite */
-    LOGRA_ERR_WORKSPACE = -5    /* workspace missing or smaller than *_ws_size */
+    LOGRA_ERR_WORKSPACE = -5,   /* workspace missing or smaller than *_ws_size */
+    LOGRA_ERR_IO = -6           /* a store file read or write failed or came up short */
 } logra_status;
 
 /* Element types.  LOGRA_F64 is accepted only where a call says so: the
@@ -342,6 +343,57 @@ int logra_influence_stream(const void *g_test_pre, int te_dtype, int64_t ld_te, 
  * ---------------------------------------------------------------------- */
 int logra_offload_rows(const void *src, int64_t ld_src, void *dst, int64_t ld_dst, int64_t rows, int64_t row_bytes,
                        void *stream, void *copy_stream, void *done);
+
+/* ------------------------------------------------------------------------
+ * Store files.  At the paper's scale the store outgrows host memory as well
+ * (Table 1: 3.5 TB); the paper keeps it on disk and overlaps reading it with
+ * the influence computation (Sec. 4.2, Efficiency; App. E.2, efficient data
+ * IO).  A store file holds rows of row_bytes bytes each, packed, from byte
+ * file_offset of a file descriptor opened by the caller (the raw layout below
+ * writes); row j starts at file_offset + j * row_bytes.  Reads and writes
+ * go through the page cache (the streaming reader announces sequential access
+ * with posix_fadvise).  Direct IO (O_DIRECT) is not usable here: the kernel
+ * cannot pin pages of hipHostMalloc memory for it, and such reads fail with
+ * EFAULT (LOGRA_ERR_IO).
+ *
+ * logra_store_read_rows / logra_store_write_rows: rows row0 .. row0+rows-1 of
+ *   the file from / to host memory (rows at stride ld bytes), blocking, retried
+ *   on interrupted and partial transfers.  A read past the end of the file
+ *   returns LOGRA_ERR_IO.  No device memory is touched.
+ *
+ * logra_influence_stream_file: logra_influence_stream over a store file of N
+ *   rows of D elements of tr_dtype (row_bytes = D * element size): a reader
+ *   thread of the library reads chunk c + 1 into one of the two halves of
+ *   host_buf while chunk c is copied to the device (copy_stream) and chunk
+ *   c - 1 is scored (stream).  host_buf: PINNED host memory of at least
+ *   2 * round_up(chunk_rows * row_bytes, 256) bytes.  ws: as for
+ *   logra_influence_stream (logra_influence_stream_file_ws_size).  The top-k
+ *   (global indices 0..N-1) is exactly that of logra_influence_scores over the
+ *   whole store.  SYNCHRONOUS.  A failed or short read returns LOGRA_ERR_IO
+ *   naming the chunk; the buffers are then idle.
+ *
+ * logra_offload_rows_file: write-behind of store rows.  `rows` device rows of
+ *   row_bytes (stride ld_src bytes) are copied into host_buf (PINNED, packed,
+ *   at least rows * row_bytes bytes) after the work on `stream`, as
+ *   logra_offload_rows does, and a host function enqueued behind the copy on
+ *   the same stream writes them to the file at file_offset (packed rows).
+ *   ASYNCHRONOUS for the caller's thread: *io_status (host, may be NULL) is 1
+ *   while pending, then LOGRA_OK or LOGRA_ERR_IO; `done` (optional hipEvent_t)
+ *   is recorded after the write.  host_buf and io_status must stay valid, and
+ *   host_buf unchanged, until the write has run (wait for `done`).
+ * ---------------------------------------------------------------------- */
+int logra_store_read_rows(int fd, int64_t file_offset, int64_t row0, int64_t rows, int64_t row_bytes, void *dst,
+                          int64_t ld_dst);
+int logra_store_write_rows(int fd, int64_t file_offset, int64_t row0, int64_t rows, int64_t row_bytes,
+                           const void *src, int64_t ld_src);
+size_t logra_influence_stream_file_ws_size(int Q, int64_t chunk_rows, int D, int tr_dtype, int topk);
+int logra_influence_stream_file(const void *g_test_pre, int te_dtype, int64_t ld_te, int Q, int fd,
+                                int64_t file_offset, int tr_dtype, int64_t N, int D, int64_t chunk_rows, int topk,
+                                float *topk_val, int64_t *topk_idx, void *host_buf, size_t host_buf_bytes,
+                                void *ws, size_t ws_bytes, void *stream, void *copy_stream);
+int logra_offload_rows_file(const void *src, int64_t ld_src, int64_t rows, int64_t row_bytes, int fd,
+                            int64_t file_offset, void *host_buf, size_t host_buf_bytes, int *io_status,
+                            void *stream, void *copy_stream, void *done);
 
 /* ------------------------------------------------------------------------
  * PCA initialisation of the projections (Sec. 3.2).  KFAC approximates a

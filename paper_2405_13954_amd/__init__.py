@@ -11,6 +11,8 @@ from __future__ import annotations
 import ctypes
 import os
 
+import numpy as np
+
 __all__ = [
     "LograError", "lib", "F32", "BF16", "F64",
     "logra_version", "logra_last_error",
@@ -25,7 +27,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpaper_logra.so")
 
 F32, BF16, F64 = 0, 1, 2
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NOT_PD, ERR_WORKSPACE = 0, -1, -2, -3, -4, -5
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NOT_PD, ERR_WORKSPACE, ERR_IO = 0, -1, -2, -3, -4, -5, -6
 MAX_GROUP = 16
 
 EXPORTED = (
@@ -38,6 +40,8 @@ EXPORTED = (
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
     "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_pca_ws_size", "logra_pca_topk",
     "logra_influence_stream_ws_size", "logra_influence_stream", "logra_offload_rows",
+    "logra_store_read_rows", "logra_store_write_rows", "logra_influence_stream_file_ws_size",
+    "logra_influence_stream_file", "logra_offload_rows_file",
 )
 
 
@@ -106,7 +110,15 @@ def lib():
         L.logra_influence_stream.argtypes = [vp, i32, i64, i32, vp, i32, i64, i64, i32, i64, i32, vp, vp, vp, sz,
                                              vp, vp]
         L.logra_offload_rows.argtypes = [vp, i64, vp, i64, i64, i64, vp, vp, vp]
-        for name in ("logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_project_layers_noalloc", "logra_cov_accumulate",
+        L.logra_store_read_rows.argtypes = [i32, i64, i64, i64, i64, vp, i64]
+        L.logra_store_write_rows.argtypes = [i32, i64, i64, i64, i64, vp, i64]
+        L.logra_influence_stream_file_ws_size.argtypes = [i32, i64, i32, i32, i32]
+        L.logra_influence_stream_file_ws_size.restype = sz
+        L.logra_influence_stream_file.argtypes = [vp, i32, i64, i32, i32, i64, i32, i64, i32, i64, i32, vp, vp, vp,
+                                                  sz, vp, sz, vp, vp]
+        L.logra_offload_rows_file.argtypes = [vp, i64, i64, i64, i32, i64, vp, sz, vp, vp, vp, vp]
+        for name in ("logra_store_read_rows", "logra_store_write_rows", "logra_influence_stream_file",
+                     "logra_offload_rows_file", "logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_project_layers_noalloc", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
                      "logra_cov_accumulate_f64", "logra_precondition_f64",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
@@ -140,6 +152,15 @@ def _stream(stream):
     if stream is None:
         return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _event(done):
+    """The hipEvent_t of a torch.cuda.Event (created by a first record if torch has not created it yet)."""
+    if done is None:
+        return None
+    if not done.cuda_event:
+        done.record()
+    return ctypes.c_void_p(done.cuda_event)
 
 
 def _check(rc: int):
@@ -411,5 +432,58 @@ def logra_offload_rows(src, dst, stream=None, copy_stream=None, done=None):
     ld_src = (_rows(src, src.shape[1]) if rows > 0 else src.shape[1]) * es
     ld_dst = (_rows(dst, dst.shape[1]) if rows > 0 else dst.shape[1]) * es
     cs = None if copy_stream is None else ctypes.c_void_p(copy_stream.cuda_stream)
-    ev = None if done is None else ctypes.c_void_p(done.cuda_event)
+    ev = _event(done)
     _check(lib().logra_offload_rows(_ptr(src), ld_src, _ptr(dst), ld_dst, rows, row_bytes, _stream(stream), cs, ev))
+
+
+# ------------------------------------------------------------ store files --
+def logra_store_write_rows(fd: int, file_offset: int, row0: int, rows):
+    """Write the rows of a host numpy array (2-D, rows contiguous) as store rows row0.. of the file."""
+    rows = np.ascontiguousarray(rows) if rows.strides[-1] != rows.itemsize else rows
+    n = rows.shape[0]
+    rb = rows.shape[1] * rows.itemsize
+    _check(lib().logra_store_write_rows(int(fd), int(file_offset), int(row0), n, rb,
+                                        rows.ctypes.data_as(ctypes.c_void_p) if n else None, rows.strides[0] if n else rb))
+
+
+def logra_store_read_rows(fd: int, file_offset: int, row0: int, out):
+    """Read store rows row0 .. row0 + len(out) - 1 of the file into the host numpy array out (2-D)."""
+    n = out.shape[0]
+    rb = out.shape[1] * out.itemsize
+    _check(lib().logra_store_read_rows(int(fd), int(file_offset), int(row0), n, rb,
+                                       out.ctypes.data_as(ctypes.c_void_p) if n else None, out.strides[0] if n else rb))
+
+
+def logra_influence_stream_file_ws_size(Q, chunk_rows, D, tr_dtype, topk) -> int:
+    return int(lib().logra_influence_stream_file_ws_size(Q, chunk_rows, D, tr_dtype, topk))
+
+
+def logra_influence_stream_file(g_test_pre, fd: int, file_offset: int, N: int, D: int, tr_dtype: int, topk: int,
+                                topk_val, topk_idx, chunk_rows: int, host_buf, ws=None, stream=None, copy_stream=None):
+    """Running top-k of g_test_pre [Q, D] (device) against a store file of N rows of D elements of tr_dtype
+    (F32, BF16 or F64 code), read by the library's reader thread into host_buf (a pinned uint8 tensor of at
+    least 2 x round_up(chunk_rows x row bytes, 256) bytes).  Synchronous."""
+    Q = g_test_pre.shape[0]
+    ld_te = _rows(g_test_pre, D) if Q > 0 else D
+    ws, wsb = _workspace(logra_influence_stream_file_ws_size(Q, chunk_rows, D, tr_dtype, topk), g_test_pre.device, ws)
+    cs = None if copy_stream is None else ctypes.c_void_p(copy_stream.cuda_stream)
+    _check(lib().logra_influence_stream_file(_ptr(g_test_pre), _dtype_code(g_test_pre), ld_te, Q, int(fd),
+                                             int(file_offset), int(tr_dtype), int(N), int(D), int(chunk_rows),
+                                             int(topk), _ptr(topk_val), _ptr(topk_idx), _ptr(host_buf),
+                                             host_buf.numel() * host_buf.element_size(), _ptr(ws), wsb,
+                                             _stream(stream), cs))
+
+
+def logra_offload_rows_file(src, fd: int, file_offset: int, host_buf, io_status=None, stream=None, copy_stream=None,
+                            done=None):
+    """Write-behind of the device rows src [rows, w] to the store file at file_offset through the pinned
+    host_buf (uint8 tensor); io_status: a ctypes.c_int set to 1, then 0 or ERR_IO once written."""
+    rows = src.shape[0]
+    es = src.element_size()
+    row_bytes = src.shape[1] * es
+    ld_src = (_rows(src, src.shape[1]) if rows > 0 else src.shape[1]) * es
+    cs = None if copy_stream is None else ctypes.c_void_p(copy_stream.cuda_stream)
+    ev = _event(done)
+    st = None if io_status is None else ctypes.byref(io_status)
+    _check(lib().logra_offload_rows_file(_ptr(src), ld_src, rows, row_bytes, int(fd), int(file_offset), _ptr(host_buf),
+                                         host_buf.numel() * host_buf.element_size(), st, _stream(stream), cs, ev))

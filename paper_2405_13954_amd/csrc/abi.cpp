@@ -77,10 +77,20 @@ int check_pinned(const void *p, const char *name, size_t align) {
 
 }  // namespace
 
+int logra::check_pinned_code(const void *p, const char *name, size_t align) { return check_pinned(p, name, align); }
+
 int logra::hip_fail(hipError_t e, const char *what) {
     return fail(LOGRA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 int logra::fail_unsupported(const char *msg) { return fail(LOGRA_ERR_UNSUPPORTED, "%s", msg); }
+int logra::fail_code(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+int logra::ok_code() { return ok(); }
 
 namespace {
 using logra::hip_fail;

@@ -17,6 +17,9 @@ int project_layers_checked(const logra_layer_desc *layers, int n_layers, int in_
 // Sets the thread's error message; returns LOGRA_ERR_HIP / LOGRA_ERR_UNSUPPORTED.
 int hip_fail(hipError_t e, const char *what);
 int fail_unsupported(const char *msg);
+int fail_code(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));   // sets the message
+int ok_code();                                                                         // clears it
+int check_pinned_code(const void *p, const char *name, size_t align);                  // pinned host memory
 
 typedef uint16_t bf16_bits_t;   // a bf16 value as its bit pattern
 enum DtypeCode { kF32 = 0, kBF16 = 1, kF64 = 2 };   // element types, numbered as in the C ABI
