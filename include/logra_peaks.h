@@ -15,9 +15,14 @@
  *   first and last MFMA round (hipDeviceAttributeWallClockRate gives the
  *   wall-clock rate in kHz), hence the clock the MFMA loop ran at.
  *   sink (device, `groups` floats) receives a checksum per workgroup.
- * logra_peak_hbm_read: streams `bytes` (a multiple of 16) from device memory
- *   with 128-bit loads, four in flight per thread, on `groups` workgroups of
- *   256 threads; sink (device, `groups` floats) receives a checksum.
+ * logra_peak_hbm_read: streams `bytes` (a multiple of 1,024; buf 1,024-byte
+ *   aligned) from device memory on `groups` workgroups of 256 threads, in one
+ *   of three ways: mode 0, grid-stride 128-bit loads, four in flight per
+ *   thread; mode 1, a contiguous range per workgroup, eight non-temporal
+ *   128-bit loads in flight per thread; mode 2, a contiguous range per wave
+ *   copied into LDS by asynchronous 1 KB global-to-LDS copies, eight in
+ *   flight (the way the projection streams).  sink (device, `groups` floats)
+ *   receives a checksum.
  *
  * Both are asynchronous on `stream` and return a logra status code
  * (0 = OK, -1 = invalid argument, -3 = HIP error).
@@ -33,7 +38,7 @@ extern "C" {
 #endif
 
 int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int64_t *cycles_out, void *stream);
-int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, float *sink, void *stream);
+int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, int mode, float *sink, void *stream);
 /* The constant rate of the wall clock read by logra_peak_mfma_bf16, in kHz, of the current device. */
 int logra_peak_wall_clock_khz(int *khz);
 

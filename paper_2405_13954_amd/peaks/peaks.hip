@@ -42,6 +42,7 @@ __global__ __launch_bounds__(256) void k_peak_mfma(int64_t iters, float *sink, i
     }
 }
 
+// Mode 0: grid-stride 128-bit loads, four in flight per thread.
 __global__ __launch_bounds__(256) void k_peak_read(const u32x4 *buf, int64_t n, float *sink) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
     int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -59,6 +60,59 @@ __global__ __launch_bounds__(256) void k_peak_read(const u32x4 *buf, int64_t n, 
     if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(x & 0xffff);
 }
 
+// Mode 1: each workgroup streams its own contiguous range, eight
+// non-temporal 128-bit loads in flight per thread.
+__global__ __launch_bounds__(256) void k_peak_read_blocked(const u32x4 *buf, int64_t n, float *sink) {
+    const int64_t per = (n + gridDim.x - 1) / gridDim.x;
+    const int64_t b0 = static_cast<int64_t>(blockIdx.x) * per;
+    const int64_t b1 = b0 + per < n ? b0 + per : n;
+    uint32_t x = 0;
+    int64_t i = b0 + threadIdx.x;
+    for (; i + 7 * 256 < b1; i += 8 * 256) {
+        u32x4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(buf + i + u * 256);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+    }
+    for (; i < b1; i += 256) {
+        const u32x4 v = buf[i];
+        x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+    }
+    for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o, 64);
+    if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(x & 0xffff);
+}
+
+// Mode 2: each wave streams its own contiguous range into an LDS ring with
+// asynchronous global-to-LDS copies of 1 KB (whole 128-byte lines), eight
+// copies in flight, the way the projection streams its operands.
+__global__ __launch_bounds__(256) void k_peak_read_lds(const uint8_t *buf, int64_t bytes, float *sink) {
+    __shared__ __attribute__((aligned(1024))) uint8_t ring[4][16 * 1024];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t waves = static_cast<int64_t>(gridDim.x) * 4;
+    const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + wave;
+    const int64_t kb = bytes / 1024;                       // 1 KB copies in all
+    const int64_t per = (kb + waves - 1) / waves;
+    int64_t c0 = w * per, c1 = c0 + per < kb ? c0 + per : kb;
+    const uint32_t lds = static_cast<uint32_t>(
+        reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t *)&ring[wave][0]));
+    int slot = 0;
+    for (int64_t c = c0; c < c1; ++c) {
+        // a window of the buffer small enough for 32-bit offsets
+        const uint8_t *base = buf + c * 1024;
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint8_t *>(base), static_cast<short>(0), 1024, 0x00020000);
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+                     :: "s"(lds + slot * 1024), "v"(static_cast<uint32_t>(lane * 16)), "s"(r) : "memory");
+        slot = (slot + 1) & 15;
+        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) sink[blockIdx.x] = static_cast<float>(ring[0][0] + ring[3][1023]);
+}
+
 }  // namespace
 
 extern "C" int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int64_t *cycles_out, void *stream) {
@@ -68,12 +122,20 @@ extern "C" int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int6
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
-extern "C" int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, float *sink, void *stream) {
-    if (buf == nullptr || sink == nullptr || groups <= 0 || bytes == 0 || bytes % 16 != 0 ||
-        (reinterpret_cast<uintptr_t>(buf) & 15) != 0)
+extern "C" int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, int mode, float *sink, void *stream) {
+    if (buf == nullptr || sink == nullptr || groups <= 0 || bytes == 0 || bytes % 1024 != 0 ||
+        (reinterpret_cast<uintptr_t>(buf) & 1023) != 0 || mode < 0 || mode > 2)
         return -1;
-    hipLaunchKernelGGL(k_peak_read, dim3(groups), dim3(256), 0, static_cast<hipStream_t>(stream),
-                       static_cast<const u32x4 *>(buf), static_cast<int64_t>(bytes / 16), sink);
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (mode == 0)
+        hipLaunchKernelGGL(k_peak_read, dim3(groups), dim3(256), 0, s, static_cast<const u32x4 *>(buf),
+                           static_cast<int64_t>(bytes / 16), sink);
+    else if (mode == 1)
+        hipLaunchKernelGGL(k_peak_read_blocked, dim3(groups), dim3(256), 0, s, static_cast<const u32x4 *>(buf),
+                           static_cast<int64_t>(bytes / 16), sink);
+    else
+        hipLaunchKernelGGL(k_peak_read_lds, dim3(groups), dim3(256), 0, s, static_cast<const uint8_t *>(buf),
+                           static_cast<int64_t>(bytes), sink);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -254,10 +254,12 @@ def test_peaks_library_exports_and_validation():
         assert hasattr(K, s)
     K.logra_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p]
-    K.logra_peak_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p,
+    K.logra_peak_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                       ctypes.c_void_p]
     fake = ctypes.c_void_p(0x1000)
     assert K.logra_peak_mfma_bf16(0, 10, fake, None, None) == -1
     assert K.logra_peak_mfma_bf16(4, 10, None, None, None) == -1
-    assert K.logra_peak_hbm_read(fake, 24, 4, fake, None) == -1       # not a multiple of 16
-    assert K.logra_peak_hbm_read(None, 32, 4, fake, None) == -1
+    big = ctypes.c_void_p(0x100000)
+    assert K.logra_peak_hbm_read(big, 1000, 4, 0, fake, None) == -1      # not a multiple of 1 KB
+    assert K.logra_peak_hbm_read(None, 1024, 4, 0, fake, None) == -1
+    assert K.logra_peak_hbm_read(big, 1024, 4, 3, fake, None) == -1      # no such method
