@@ -30,7 +30,7 @@
 //     round trip is hidden behind the stream.
 //  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
 //     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
-//     formed by fp32 MFMAs straight from those sums (one wave per 16-row block
+//     formed by fp32 MFMAs straight from those sums (one wave per 16 x 16 block
 //     of G).  Empty tiles give 0.
 //  C. k_project_reduce: per example (and 256-wide output slice), the tile sums are added in tile order
 //     and G_b is written (fp32 or bf16, round to nearest even) to the
@@ -785,13 +785,13 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
     if (tid == 0) *n_tiles = base;
 }
 
-// One wave per (tile, 16-row block jo of G): x' and dy' of the tile are the
-// fixed-order sums of their chunk partials, read straight from the workspace,
-// where they already sit in the operand layout of the fp32 16x16x4 MFMA with
-// the token as the contraction index (lane l of partial block (m, j) holds
-// the rows t = 16 m + 4 (l / 16) + r, r < 4, of column 16 j + l % 16).  So
-// the tile's sum over tokens of dy'_t x'_t^T is, for each 16 x 16 block
-// (jo, ji), 16 MFMAs over (m, r).  Tiles without a valid token get 0.
+// One wave per (tile, 16 x 16 block (jo, ji) of G): x' and dy' of the tile
+// are the fixed-order sums of their chunk partials, read straight from the
+// workspace, where they already sit in the operand layout of the fp32
+// 16x16x4 MFMA with the token as the contraction index (lane l of partial
+// block (m, j) holds the rows t = 16 m + 4 (l / 16) + r, r < 4, of column
+// 16 j + l % 16).  So the block of the tile's sum over tokens of dy'_t x'_t^T
+// is 16 MFMAs over (m, r).  Tiles without a valid token get 0.
 template <int KT>
 __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pairs) {
     constexpr int KP = 16 * KT;
@@ -799,7 +799,8 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
     const int lane = threadIdx.x & (kWave - 1);
     const int p = blockIdx.x * NW + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (p >= pairs) return;
-    const int tix = p / KT, jo = p - tix * KT;   // tile over all layers, row block of G
+    const int tix = p / (KT * KT), blk = p - tix * (KT * KT);   // tile over all layers, block of G
+    const int jo = blk / KT, ji = blk - jo * KT;
     const int per_layer = a.B * a.tpe;
     const int l = tix / per_layer;
     const int bt = tix - l * per_layer;
@@ -811,50 +812,37 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
     if (a.mask && tok) tok = a.mask[static_cast<size_t>(b) * a.T + t] != 0;
     const bool any = __builtin_amdgcn_ballot_w64(tok) != 0;
     const int row = lane & 15, grp4 = lane >> 4;
+    const int i = 16 * ji + row;
     if (!any) {
+#pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int o = 16 * jo + 4 * grp4 + r;
-            if (o >= a.k_out) continue;
-            for (int i = row; i < a.k_in; i += 16) gdst[o * a.k_in + i] = 0.f;
+            if (o < a.k_out && i < a.k_in) gdst[o * a.k_in + i] = 0.f;
         }
         return;
     }
     const ChunkLayer &L = a.layer[l];
     const int C = L.c_in + L.c_out;
     const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP)) + lane;
-    f32x4 dv[MB], xv[KT][MB];
+    f32x4 dv[MB], xv[MB];
 #pragma unroll
-    for (int m = 0; m < MB; ++m) {
-        dv[m] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ji = 0; ji < KT; ++ji) xv[ji][m] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+    for (int m = 0; m < MB; ++m) dv[m] = xv[m] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int c = 0; c < L.c_in; ++c)
 #pragma unroll
-        for (int m = 0; m < MB; ++m)
-#pragma unroll
-            for (int ji = 0; ji < KT; ++ji) xv[ji][m] += src[static_cast<size_t>(c) * NQ + (m * KT + ji) * kWave];
+        for (int m = 0; m < MB; ++m) xv[m] += src[static_cast<size_t>(c) * NQ + (m * KT + ji) * kWave];
     for (int c = L.c_in; c < C; ++c)
 #pragma unroll
         for (int m = 0; m < MB; ++m) dv[m] += src[static_cast<size_t>(c) * NQ + (m * KT + jo) * kWave];
-    f32x4 acc[KT];
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ji = 0; ji < KT; ++ji) {
-        acc[ji] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int m = 0; m < MB; ++m)
 #pragma unroll
-        for (int m = 0; m < MB; ++m)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) acc[ji] = mfma16_f32(dv[m][r], xv[ji][m][r], acc[ji]);
-    }
+        for (int r = 0; r < 4; ++r) acc = mfma16_f32(dv[m][r], xv[m][r], acc);
     // result register r of lane l: o = 16 jo + 4 (l / 16) + r, i = 16 ji + l % 16
 #pragma unroll
-    for (int ji = 0; ji < KT; ++ji) {
-        const int i = 16 * ji + row;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int o = 16 * jo + 4 * grp4 + r;
-            if (o < a.k_out && i < a.k_in) gdst[o * a.k_in + i] = acc[ji][r];
-        }
+    for (int r = 0; r < 4; ++r) {
+        const int o = 16 * jo + 4 * grp4 + r;
+        if (o < a.k_out && i < a.k_in) gdst[o * a.k_in + i] = acc[r];
     }
 }
 
@@ -1084,7 +1072,7 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int pairs = grp.n_layers * B * a.tpe * KT;   // (tile, row block) pairs, one wave each
+    const int pairs = grp.n_layers * B * a.tpe * KT * KT;   // (tile, 16 x 16 block of G), one wave each
     const unsigned fgrid = static_cast<unsigned>((pairs + NW - 1) / NW);
     switch (KT) {
         case 1: hipLaunchKernelGGL((k_project_tile_finish<1>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
