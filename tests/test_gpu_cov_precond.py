@@ -49,6 +49,36 @@ def test_cov_integer_exact_blocks_and_chunks():
         assert np.array_equal(got[l].astype(np.float64), want)
 
 
+@pytest.mark.parametrize("B1,B2,D,nb,pad,s_shift", [
+    (40, 5, 192, 2, 8, 0),     # register tiles: 3 off-diagonal + 3 diagonal per block, 2 chunks then 1
+    (8, 0, 128, 1, 0, 0),      # register tiles, a single short chunk
+    (33, 31, 64, 3, 16, 0),    # diagonal tiles only (one tile per block)
+    (20, 12, 128, 2, 0, 1),    # S not 16-byte aligned: the general kernel
+])
+def test_cov_integer_exact_tile_paths(B1, B2, D, nb, pad, s_shift):
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say(f"[cov] integer exact, B={B1}+{B2}, D={D}, blocks={nb}, row pad={pad}, S shift={s_shift}")
+    ld = D * nb + pad
+    g = W.integer_array(W.rng(24, B1, D), (B1 + B2, ld), -4, 4, "bf16")
+    gd = dev(g)
+    base = torch.zeros(nb * D * D + s_shift, dtype=torch.float32, device="cuda")
+    S0 = W.integer_array(W.rng(25, D), (nb, D, D), -50, 50, "f32")
+    S0 = S0 + S0.transpose(0, 2, 1)   # symmetric, as an accumulated S is
+    base[s_shift:] = torch.from_numpy(S0.reshape(-1)).cuda()
+    S = base[s_shift:].view(nb, D, D)
+    for lo, hi in ((0, B1), (B1, B1 + B2)):
+        if hi > lo:
+            P.logra_cov_accumulate_blocks(gd[lo:hi], S, D)
+    torch.cuda.synchronize()
+    got = host(S)
+    for l in range(nb):
+        want = S0[l].astype(np.float64) + oracle.cov_accumulate(g[:, l * D:(l + 1) * D])
+        assert np.array_equal(got[l].astype(np.float64), want)
+        assert np.array_equal(got[l], got[l].T)
+
+
 def test_cov_deterministic():
     import torch
     import paper_2405_13954_amd as P
