@@ -5,7 +5,7 @@ stream -- per step one batch of B=8 examples of T=2048 padded tokens, valid
 lengths uniform on 128..2048, through all 224 linear layers (k_in = k_out = 16,
 57,344 projected dims per example): fused projection into the bf16 gradient
 store (32 grouped launches of 7 layers) and the 224 per-layer covariance
-updates.
+updates, each kept as its lower triangle (all the preconditioner reads).
 
 The logging leg's "shared_inputs" entry runs the same stream with the
 inputs a transformer block shares (q/k/v one x, gate/up one x), which the
@@ -315,8 +315,8 @@ def logging_leg(args, torch, P):
             ptimer.stop(e0, w.blocks)
         rows = store[s * B:(s + 1) * B]
         e0 = cov_timer.start() if timed else None
-        rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(rows.data_ptr()), P.BF16, g_ld, B, D, n_layers,
-                                           ctypes.c_void_p(S.data_ptr()), stream)
+        rc = L.logra_cov_accumulate_blocks_lower(ctypes.c_void_p(rows.data_ptr()), P.BF16, g_ld, B, D, n_layers,
+                                                 ctypes.c_void_p(S.data_ptr()), stream)
         if rc != 0:
             raise P.LograError(rc, P.logra_last_error())
         if timed:
@@ -589,9 +589,9 @@ def block_k64_leg(args, torch, P):
         if rc != 0:
             raise P.LograError(rc, P.logra_last_error())
 
-    def cov():
-        rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(store.data_ptr()), P.BF16, store.stride(0), B, D, nl,
-                                           ctypes.c_void_p(S.data_ptr()), stream)
+    def cov(fn=L.logra_cov_accumulate_blocks_lower):
+        rc = fn(ctypes.c_void_p(store.data_ptr()), P.BF16, store.stride(0), B, D, nl,
+                ctypes.c_void_p(S.data_ptr()), stream)
         if rc != 0:
             raise P.LograError(rc, P.logra_last_error())
 
@@ -600,7 +600,7 @@ def block_k64_leg(args, torch, P):
         project(i)
         cov()
     torch.cuda.synchronize()
-    pt, ct = EventTimer(torch), EventTimer(torch)
+    pt, ct, st = EventTimer(torch), EventTimer(torch), EventTimer(torch)
     e0 = pt.start()
     for i in range(reps):
         project(i)
@@ -609,6 +609,13 @@ def block_k64_leg(args, torch, P):
     for _ in range(reps):
         cov()
     ct.stop(e0, reps)
+    # the symmetric form of the same update, for reference (not part of the step)
+    S.zero_()
+    cov(L.logra_cov_accumulate_blocks)
+    e0 = st.start()
+    for _ in range(reps):
+        cov(L.logra_cov_accumulate_blocks)
+    st.stop(e0, reps)
     torch.cuda.synchronize()
     tokens = B * T
     per_tok = sum(2 * (ni + no) for _, ni, no in w.layers)
@@ -616,25 +623,32 @@ def block_k64_leg(args, torch, P):
     proj_bytes = tokens * per_tok + p_bytes
     proj_ms = pt.mean_ms()
     ach = proj_bytes / (proj_ms * 1e-3) / 1e9
-    # covariance: S kept symmetric needs its upper triangle read and all of it written
-    cov_bytes = nl * 4 * (D * (D + 1) // 2 + D * D) + B * nl * D * 2
+    # covariance kept as its lower triangle (all the preconditioner reads): that
+    # triangle read and written once, plus the store rows
+    cov_bytes = nl * 4 * 2 * (D * (D + 1) // 2) + B * nl * D * 2
     cov_ms = ct.mean_ms()
     cach = cov_bytes / (cov_ms * 1e-3) / 1e9
+    # the symmetric form reads the upper triangle and writes all of S
+    sym_bytes = nl * 4 * (D * (D + 1) // 2 + D * D) + B * nl * D * 2
+    sym_ms = st.mean_ms()
     traffic, ratio = measured_traffic("projection_k64", PROJ_SOURCES)
     res = {
         "metric": "projected per-example grads/sec (tokens/s), one Llama3-8B block at k=64",
         "value": tokens / ((proj_ms + cov_ms) * 1e-3), "unit": "tokens/s",
         "examples_per_s": B / ((proj_ms + cov_ms) * 1e-3),
         "proj_launch_ms": proj_ms, "cov_launch_ms": cov_ms,
+        "cov_symmetric_launch_ms": sym_ms,
+        "cov_symmetric_gbs": sym_bytes / (sym_ms * 1e-3) / 1e9,
         "config": {"workload": "llama3_8b_block", "layers": nl, "B": B, "T": T, "k_in": k, "k_out": k,
-                   "store": "bf16 rows of 7 x 4,096", "covariance": "7 x 4,096 x 4,096 fp32"},
+                   "store": "bf16 rows of 7 x 4,096",
+                   "covariance": "7 x 4,096 x 4,096 fp32, lower triangles"},
         "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": ach / HBM_PEAK_GBS, "traffic": traffic, "traffic_over_algorithmic": ratio,
                      "kernel": "logra_project_layers (7 Llama3-8B layers, B=16, T=1024, k=64)",
                      "bytes_per_launch": proj_bytes},
         "cov_roofline": {"bound": "hbm", "achieved": cach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": cach / HBM_PEAK_GBS, "bytes_per_launch": cov_bytes,
-                         "kernel": "logra_cov_accumulate_blocks (7 blocks of 4,096, 16 bf16 rows)"},
+                         "kernel": "logra_cov_accumulate_blocks_lower (7 blocks of 4,096, 16 bf16 rows)"},
     }
     sample = None
     if args.cpu_baseline:
@@ -732,8 +746,8 @@ def gpt2_leg(args, torch, P):
         if timed:
             pt.stop(e0, len(all_d[st]))
         rows = store[st * B:(st + 1) * B]
-        rc = L.logra_cov_accumulate_blocks(ctypes.c_void_p(rows.data_ptr()), P.BF16, store.stride(0), B, D, nl,
-                                           ctypes.c_void_p(S.data_ptr()), stream)
+        rc = L.logra_cov_accumulate_blocks_lower(ctypes.c_void_p(rows.data_ptr()), P.BF16, store.stride(0), B, D,
+                                                 nl, ctypes.c_void_p(S.data_ptr()), stream)
         if rc != 0:
             raise P.LograError(rc, P.logra_last_error())
 

@@ -155,6 +155,17 @@ int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, f
 int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, int D,
                                 int n_blocks, float *S, void *stream);
 
+/* The same update applied to the lower triangle alone (the symmetric rank-B
+ * update of a packed-by-convention symmetric matrix, as BLAS SYRK with
+ * uplo = lower): entries S[i][j] with i >= j of each block are read and
+ * written; entries above the diagonal are neither read nor written.  The
+ * preconditioning and inverse-factor entry points below read only the lower
+ * triangle and the diagonal, so a statistic kept this way feeds them
+ * directly, for two thirds of the memory traffic of the symmetric form.
+ * Arguments and errors as logra_cov_accumulate_blocks. */
+int logra_cov_accumulate_blocks_lower(const void *g, int g_dtype, int64_t ld, int B, int D,
+                                      int n_blocks, float *S, void *stream);
+
 /* The same statistic kept in float64, for fp32 workloads whose downstream
  * solve is ill-conditioned (the damped inverse of App. C amplifies the
  * rounding of an fp32 S by up to the condition number of C + lambda I):
@@ -178,8 +189,9 @@ int logra_cov_accumulate_f64(const void *g, int g_dtype, int64_t ld, int B, int 
  * computed by a float64 Cholesky factorisation and two triangular solves.
  * damp_ratio < 0 selects the identity preconditioner (g_out = g_test).
  *
- *   S       [D][D] fp32 covariance from logra_cov_accumulate (lower triangle
- *           is read); N > 0 the number of examples accumulated into it
+ *   S       [D][D] fp32 covariance from logra_cov_accumulate or
+ *           logra_cov_accumulate_blocks_lower (only the lower triangle and the
+ *           diagonal are read); N > 0 the number of examples accumulated into it
  *   g_test  Q rows of D at stride ld_in, in_dtype;  g_out Q rows of D at
  *           stride ld_out, out_dtype (may not alias g_test); each of F32,
  *           BF16 or F64

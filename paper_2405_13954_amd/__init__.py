@@ -18,7 +18,8 @@ __all__ = [
     "logra_version", "logra_last_error",
     "logra_project_ws_size", "logra_project_layer",
     "logra_project_layers_ws_size", "logra_project_layers",
-    "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_f64",
+    "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_blocks_lower",
+    "logra_cov_accumulate_f64",
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks", "logra_precondition_f64",
     "logra_influence_ws_size", "logra_influence_scores",
 ]
@@ -34,7 +35,8 @@ EXPORTED = (
     "logra_last_error", "logra_version",
     "logra_project_ws_size", "logra_project_layer",
     "logra_project_layers_ws_size", "logra_project_layers", "logra_project_layers_noalloc",
-    "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_f64",
+    "logra_cov_accumulate", "logra_cov_accumulate_blocks", "logra_cov_accumulate_blocks_lower",
+    "logra_cov_accumulate_f64",
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks", "logra_precondition_f64",
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
@@ -82,6 +84,7 @@ def lib():
                                                    i32, i64, vp]
         L.logra_cov_accumulate.argtypes = [vp, i32, i64, i32, i32, vp, vp]
         L.logra_cov_accumulate_blocks.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
+        L.logra_cov_accumulate_blocks_lower.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
         L.logra_cov_accumulate_f64.argtypes = [vp, i32, i64, i32, i32, i32, vp, vp]
         L.logra_precondition_f64.argtypes = [vp, i32, i32, i64, f64, vp, i32, i64, i32, vp, i32, i64, vp, sz, vp]
         L.logra_precondition_ws_size.argtypes = [i32, i32, i32]
@@ -119,7 +122,8 @@ def lib():
         L.logra_offload_rows_file.argtypes = [vp, i64, i64, i64, i32, i64, vp, sz, vp, vp, vp, vp]
         for name in ("logra_store_read_rows", "logra_store_write_rows", "logra_influence_stream_file",
                      "logra_offload_rows_file", "logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_project_layers_noalloc", "logra_cov_accumulate",
-                     "logra_cov_accumulate_blocks", "logra_precondition", "logra_precondition_blocks",
+                     "logra_cov_accumulate_blocks", "logra_cov_accumulate_blocks_lower", "logra_precondition",
+                     "logra_precondition_blocks",
                      "logra_cov_accumulate_f64", "logra_precondition_f64",
                      "logra_influence_scores", "logra_influence_scores_scaled", "logra_self_influence_blocks"):
             getattr(L, name).restype = ctypes.c_int
@@ -268,6 +272,16 @@ def logra_cov_accumulate_blocks(g, S, D: int, stream=None):
     ld = _rows(g, D * n_blocks) if B > 0 else D * n_blocks
     _check(lib().logra_cov_accumulate_blocks(_ptr(g), _dtype_code(g), ld, B, D, n_blocks, _ptr(S),
                                              _stream(stream)))
+
+
+def logra_cov_accumulate_blocks_lower(g, S, D: int, stream=None):
+    """S [n_blocks, D, D] fp32; the lower triangle (diagonal included) of block l
+    += G[:, l*D:(l+1)*D]^T G[:, l*D:(l+1)*D]; entries above the diagonal untouched."""
+    B = g.shape[0]
+    n_blocks = S.shape[0]
+    ld = _rows(g, D * n_blocks) if B > 0 else D * n_blocks
+    _check(lib().logra_cov_accumulate_blocks_lower(_ptr(g), _dtype_code(g), ld, B, D, n_blocks, _ptr(S),
+                                                   _stream(stream)))
 
 
 def logra_cov_accumulate_f64(g, S, D: int = None, stream=None):

@@ -233,8 +233,8 @@ int logra_project_layer(const void *x, const void *dy, int in_dtype, int B, int 
                                 stream);
 }
 
-int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks,
-                                float *S, void *stream) {
+static int cov_blocks_impl(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks, float *S, bool lower,
+                           void *stream) {
     if (!valid_dtype(g_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
     if (B < 0 || D <= 0 || n_blocks <= 0) return fail(LOGRA_ERR_INVALID_ARG, "need B >= 0, D > 0, n_blocks > 0");
     if (n_blocks > 65535) return fail(LOGRA_ERR_UNSUPPORTED, "n_blocks must be <= 65535");
@@ -244,10 +244,20 @@ int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, i
     if (B == 0) return ok();
     TRY(check_dev(g, "g", g_dtype == LOGRA_BF16 ? 16 : 4));
     TRY(check_dev(S, "S", 4));
-    const hipError_t e = logra::launch_cov(g, g_dtype == LOGRA_BF16, ld, B, D, n_blocks, S,
+    const hipError_t e = logra::launch_cov(g, g_dtype == LOGRA_BF16, ld, B, D, n_blocks, S, lower,
                                            static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "covariance launch");
     return ok();
+}
+
+int logra_cov_accumulate_blocks(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks,
+                                float *S, void *stream) {
+    return cov_blocks_impl(g, g_dtype, ld, B, D, n_blocks, S, false, stream);
+}
+
+int logra_cov_accumulate_blocks_lower(const void *g, int g_dtype, int64_t ld, int B, int D, int n_blocks,
+                                      float *S, void *stream) {
+    return cov_blocks_impl(g, g_dtype, ld, B, D, n_blocks, S, true, stream);
 }
 
 int logra_cov_accumulate(const void *g, int g_dtype, int64_t ld, int B, int D, float *S, void *stream) {

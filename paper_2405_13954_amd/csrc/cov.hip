@@ -40,8 +40,17 @@ __device__ __forceinline__ void tile_coords(int t, int nt, int &ti, int &tj) {
 // in flight at once, adds, stores, and writes the mirrored tile the same way
 // (row t / 4 of the transposed tile, gathered from LDS).
 template <typename TS>
-__device__ __forceinline__ void add_and_mirror(TS *S, int D, int I, int J, TS *ct, bool diag) {
+__device__ __forceinline__ void add_and_mirror(TS *S, int D, int I, int J, TS *ct, bool diag, bool lower) {
     const int tid = threadIdx.x;
+    if (lower) {
+        // lower triangle only: tile entry (r, c) of the upper tile (I, J) is S(J + c, I + r)
+        for (int e = tid; e < CT * CT; e += blockDim.x) {
+            const int c = e / CT, r = e - (e / CT) * CT;   // consecutive threads: consecutive r
+            const int i = I + r, j = J + c;
+            if (i < D && j < D && (!diag || r <= c)) S[static_cast<size_t>(j) * D + i] += ct[r * (CT + 1) + c];
+        }
+        return;
+    }
     if constexpr (sizeof(TS) == 4) {
         if (!diag && D % CT == 0 && (reinterpret_cast<uintptr_t>(S) & 15) == 0) {
             const int r = tid >> 2, c0 = 16 * (tid & 3);
@@ -90,7 +99,7 @@ __device__ __forceinline__ void add_and_mirror(TS *S, int D, int I, int J, TS *c
 }
 
 __global__ __launch_bounds__(256) void k_cov_bf16(const bf16_bits *g, int64_t ld, int B, int D,
-                                                  int nt, float *S_all) {
+                                                  int nt, float *S_all, bool lower) {
     __shared__ __attribute__((aligned(16))) bf16_bits gi[CT][BK + 8];  // [column][example]
     __shared__ __attribute__((aligned(16))) bf16_bits gj[CT][BK + 8];
     __shared__ float ct[CT * (CT + 1)];
@@ -141,7 +150,7 @@ __global__ __launch_bounds__(256) void k_cov_bf16(const bf16_bits *g, int64_t ld
 #pragma unroll
         for (int r = 0; r < 4; ++r) ct[(16 * wave + 4 * kg + r) * (CT + 1) + 16 * j + row] = acc[j][r];
     __syncthreads();
-    add_and_mirror(S, D, I, J, ct, diag);
+    add_and_mirror(S, D, I, J, ct, diag, lower);
 }
 
 // Strict upper triangle, row by row: (0,1),(0,2)..(0,nt-1),(1,2),...
@@ -213,12 +222,15 @@ __device__ __forceinline__ void st_f32x4(float *base, uint32_t byte_off, f32x4 v
 // Off-diagonal tiles (kDiag false) write the upper tile and its mirror;
 // diagonal tiles (kDiag true, two waves per workgroup) go through the wave's
 // LDS so that every entry below the diagonal is the bit copy of its upper twin.
-template <bool kDiag>
+// With kLower only the lower triangle is read and written: the tile below the
+// diagonal is computed in place of the upper one and nothing is mirrored.
+template <bool kDiag, bool kLower>
 __global__ __launch_bounds__(256, 3) void k_cov_bf16_reg(const bf16_bits *g, int64_t ld, int B, int D, int nt,
                                                       int n_tiles, float *S_all) {
-    constexpr int kWaves = kDiag ? 2 : 4;   // waves (tiles) per workgroup
-    constexpr int kHalf = 32 * (CT + 4);     // half a mirrored tile: 32 rows of 68 floats
-    __shared__ __attribute__((aligned(16))) float tl[kDiag ? kWaves * CT * (CT + 1) : kWaves * kHalf];
+    constexpr int kWaves = kDiag && !kLower ? 2 : 4;   // waves (tiles) per workgroup
+    constexpr int kHalf = 32 * (CT + 4);                // half a mirrored tile: 32 rows of 68 floats
+    constexpr int kLds = kLower ? 1 : kDiag ? kWaves * CT * (CT + 1) : kWaves * kHalf;
+    __shared__ __attribute__((aligned(16))) float tl[kLds];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int t = __builtin_amdgcn_readfirstlane(static_cast<int>(blockIdx.x) * kWaves + wave);
     const bool live = t < n_tiles;   // wave-uniform; every wave still reaches the barrier
@@ -227,7 +239,8 @@ __global__ __launch_bounds__(256, 3) void k_cov_bf16_reg(const bf16_bits *g, int
         if (kDiag) ti = tj = t;
         else strict_upper_coords(t, nt, ti, tj);
     }
-    const int I = ti * CT, J = tj * CT;
+    // the lower triangle alone: the tile below the diagonal, (tj, ti)
+    const int I = (kLower ? tj : ti) * CT, J = (kLower ? ti : tj) * CT;
     const int row = lane & 15, kg = lane >> 4;
     const int blk = blockIdx.y;
     const auto gs = buf_rsrc(g + static_cast<size_t>(blk) * D,
@@ -273,7 +286,27 @@ __global__ __launch_bounds__(256, 3) void k_cov_bf16_reg(const bf16_bits *g, int
             }
         }
     }
-    if constexpr (!kDiag) {
+    if constexpr (kLower) {
+        // the tile itself; on the diagonal only entries (i, c) with c <= i
+        if (live) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = 16 * kg + 4 * r + e;
+                    const f32x4 v = f32x4{acc[e][0][r], acc[e][1][r], acc[e][2][r], acc[e][3][r]};
+                    const uint32_t off = vu + ((I + 4 * r + e) * static_cast<uint32_t>(D) + J) * 4u;
+                    if (!kDiag || 4 * row + 3 <= i) {
+                        st_f32x4(Sb, off, v);
+                    } else if (4 * row <= i) {
+#pragma unroll
+                        for (int f = 0; f < 4; ++f)
+                            if (4 * row + f <= i)
+                                *reinterpret_cast<float *>(reinterpret_cast<char *>(Sb) + off + 4 * f) = v[f];
+                    }
+                }
+        }
+    } else if constexpr (!kDiag) {
         if (live) {
 #pragma unroll
             for (int r = 0; r < 4; ++r)
@@ -332,7 +365,7 @@ __global__ __launch_bounds__(256, 3) void k_cov_bf16_reg(const bf16_bits *g, int
 }
 
 __global__ __launch_bounds__(256) void k_cov_f32(const float *g, int64_t ld, int B, int D, int nt,
-                                                 float *S_all) {
+                                                 float *S_all, bool lower) {
     __shared__ float ct[CT * (CT + 1)];
     const int blk = blockIdx.y;
     int ti, tj;
@@ -353,7 +386,7 @@ __global__ __launch_bounds__(256) void k_cov_f32(const float *g, int64_t ld, int
         ct[r * (CT + 1) + c] = s;
     }
     __syncthreads();
-    add_and_mirror(S, D, I, J, ct, diag);
+    add_and_mirror(S, D, I, J, ct, diag, lower);
 }
 
 // float64 statistics: rows of fp32 or fp64, every product and sum in float64.
@@ -380,12 +413,12 @@ __global__ __launch_bounds__(256) void k_cov_f64(const TG *g, int64_t ld, int B,
         ct[r * (CT + 1) + c] = s;
     }
     __syncthreads();
-    add_and_mirror(S, D, I, J, ct, diag);
+    add_and_mirror(S, D, I, J, ct, diag, false);
 }
 
 }  // namespace
 
-hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S,
+hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S, bool lower,
                       hipStream_t s) {
     if (B == 0 || n_blocks == 0) return hipSuccess;
     const int nt = (D + CT - 1) / CT;
@@ -395,19 +428,31 @@ hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_
     const bool reg = D % CT == 0 && ld % 4 == 0 && (reinterpret_cast<uintptr_t>(g) & 7) == 0 &&
                      (reinterpret_cast<uintptr_t>(S) & 15) == 0 && D <= 16384 &&
                      (static_cast<int64_t>(B) + 32) * ld * 2 < (int64_t{1} << 31);
+    const bf16_bits *gb = static_cast<const bf16_bits *>(g);
     if (bf16 && reg) {
         const int n_off = nt * (nt - 1) / 2;
-        if (n_off > 0)
-            hipLaunchKernelGGL(k_cov_bf16_reg<false>, dim3(static_cast<unsigned>((n_off + 3) / 4), n_blocks),
-                               dim3(256), 0, s, static_cast<const bf16_bits *>(g), ld, B, D, nt, n_off, S);
-        hipLaunchKernelGGL(k_cov_bf16_reg<true>, dim3(static_cast<unsigned>((nt + 1) / 2), n_blocks), dim3(128), 0,
-                           s, static_cast<const bf16_bits *>(g), ld, B, D, nt, nt, S);
-    } else if (bf16)
-        hipLaunchKernelGGL(k_cov_bf16, grid, dim3(256), 0, s, static_cast<const bf16_bits *>(g), ld, B,
-                           D, nt, S);
-    else
-        hipLaunchKernelGGL(k_cov_f32, grid, dim3(256), 0, s, static_cast<const float *>(g), ld, B, D,
-                           nt, S);
+        const dim3 off_grid(static_cast<unsigned>((n_off + 3) / 4), static_cast<unsigned>(n_blocks));
+        if (n_off > 0) {
+            if (lower)
+                hipLaunchKernelGGL((k_cov_bf16_reg<false, true>), off_grid, dim3(256), 0, s, gb, ld, B, D, nt, n_off, S);
+            else
+                hipLaunchKernelGGL((k_cov_bf16_reg<false, false>), off_grid, dim3(256), 0, s, gb, ld, B, D, nt, n_off,
+                                   S);
+        }
+        if (lower)
+            hipLaunchKernelGGL((k_cov_bf16_reg<true, true>),
+                               dim3(static_cast<unsigned>((nt + 3) / 4), static_cast<unsigned>(n_blocks)), dim3(256), 0,
+                               s, gb, ld, B, D, nt, nt, S);
+        else
+            hipLaunchKernelGGL((k_cov_bf16_reg<true, false>),
+                               dim3(static_cast<unsigned>((nt + 1) / 2), static_cast<unsigned>(n_blocks)), dim3(128), 0,
+                               s, gb, ld, B, D, nt, nt, S);
+    } else if (bf16) {
+        hipLaunchKernelGGL(k_cov_bf16, grid, dim3(256), 0, s, gb, ld, B, D, nt, S, lower);
+    } else {
+        hipLaunchKernelGGL(k_cov_f32, grid, dim3(256), 0, s, static_cast<const float *>(g), ld, B, D, nt, S,
+                           lower);
+    }
     return hipGetLastError();
 }
 

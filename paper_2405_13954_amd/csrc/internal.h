@@ -55,7 +55,7 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
 
 // Covariance S_l += G_l^T G_l for n_blocks column blocks of width D; the
 // _f64 form keeps S in float64 (rows fp32, or fp64 when f64_rows).
-hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S,
+hipError_t launch_cov(const void *g, bool bf16, int64_t ld, int B, int D, int n_blocks, float *S, bool lower,
                       hipStream_t s);
 hipError_t launch_cov_f64(const void *g, bool f64_rows, int64_t ld, int B, int D, int n_blocks, double *S,
                           hipStream_t s);

@@ -93,6 +93,12 @@ def test_cov_validation(L):
     assert L.logra_cov_accumulate(None, 1, 32, 4, 64, None, None) == P.ERR_INVALID_ARG   # ld < D
     assert L.logra_cov_accumulate(None, 1, 64, 0, 64, None, None) == P.OK                # B = 0 no-op
     assert L.logra_cov_accumulate_blocks(None, 1, 512, 4, 256, 0, None, None) == P.ERR_INVALID_ARG
+    f = L.logra_cov_accumulate_blocks_lower
+    assert f(None, 1, 512, 4, 256, 0, None, None) == P.ERR_INVALID_ARG                 # n_blocks = 0
+    assert f(None, 1, 508, 4, 254, 2, None, None) == P.ERR_INVALID_ARG                 # bf16 needs D%8==0
+    assert f(None, 1, 256, 4, 256, 2, None, None) == P.ERR_INVALID_ARG                 # ld < D * n_blocks
+    assert f(None, 7, 512, 4, 256, 2, None, None) == P.ERR_INVALID_ARG                 # bad dtype
+    assert f(None, 1, 512, 0, 256, 2, None, None) == P.OK                              # B = 0 no-op
 
 
 def test_precondition_validation(L):

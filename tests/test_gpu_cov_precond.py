@@ -79,6 +79,68 @@ def test_cov_integer_exact_tile_paths(B1, B2, D, nb, pad, s_shift):
         assert np.array_equal(got[l], got[l].T)
 
 
+@pytest.mark.parametrize("B1,B2,D,nb,pad,dtype", [
+    (40, 5, 192, 2, 8, "bf16"),    # register tiles below the diagonal + diagonal tiles, 2 chunks then 1
+    (33, 0, 64, 3, 16, "bf16"),    # diagonal tiles only
+    (25, 15, 72, 3, 0, "bf16"),    # ragged D: the general kernel
+    (9, 4, 100, 2, 3, "f32"),      # fp32 rows: the general kernel
+])
+def test_cov_lower_integer_exact_upper_untouched(B1, B2, D, nb, pad, dtype):
+    """Lower-triangle form (SYRK, uplo = lower): the lower triangle and diagonal
+    equal the oracle's exactly; every entry above the diagonal keeps its bits."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    say(f"[cov lower] integer exact, B={B1}+{B2}, D={D}, blocks={nb}, pad={pad}, {dtype}")
+    ld = D * nb + pad
+    g = W.integer_array(W.rng(26, B1, D), (B1 + B2, ld), -4, 4, dtype)
+    gd = dev(g)
+    S0 = W.integer_array(W.rng(27, D), (nb, D, D), -50, 50, "f32")
+    S0 = S0 + S0.transpose(0, 2, 1)
+    up = np.triu(np.ones((D, D), bool), 1)
+    S0[:, up] = np.nan                      # never read: a NaN there would spread into the result
+    S = dev(S0)
+    for lo, hi in ((0, B1), (B1, B1 + B2)):
+        if hi > lo:
+            P.logra_cov_accumulate_blocks_lower(gd[lo:hi], S, D)
+    torch.cuda.synchronize()
+    got = host(S)
+    assert np.array_equal(got[:, up].view(np.uint32), S0[:, up].view(np.uint32))
+    for l in range(nb):
+        want = S0[l].astype(np.float64) + oracle.cov_accumulate(g[:, l * D:(l + 1) * D])
+        assert np.array_equal(got[l][~up].astype(np.float64), want[~up])
+
+
+def test_precondition_and_self_influence_read_only_the_lower_triangle():
+    """The statistic kept as its lower triangle feeds the preconditioner and the
+    inverse factor to the same bits as the symmetric statistic."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    nb, D, B, Q = 3, 128, 300, 5
+    say(f"[cov lower] preconditioner and self-influence from the lower triangle, {nb} blocks of {D}")
+    g = dev(W.normal(W.rng(28), (B, nb * D), 1.0, "bf16"))
+    S_full = torch.zeros((nb, D, D), dtype=torch.float32, device="cuda")
+    S_low = torch.triu(torch.full((nb, D, D), float("nan"), dtype=torch.float32, device="cuda"), 1)
+    P.logra_cov_accumulate_blocks(g, S_full, D)
+    P.logra_cov_accumulate_blocks_lower(g, S_low, D)
+    torch.cuda.synchronize()
+    lo = np.tril(np.ones((D, D), bool))
+    assert np.array_equal(host(S_full)[:, lo].view(np.uint32), host(S_low)[:, lo].view(np.uint32))
+    gt = dev(W.normal(W.rng(29), (Q, nb * D), 1.0, "f32"))
+    outs = []
+    for S in (S_full, S_low):
+        o = torch.empty((Q, nb * D), dtype=torch.float32, device="cuda")
+        P.logra_precondition_blocks(S, B, 0.1, gt, o)
+        si = torch.empty(B, dtype=torch.float32, device="cuda")
+        P.logra_self_influence_blocks(S, B, 0.1, g, self_out=si)
+        torch.cuda.synchronize()
+        outs.append((host(o), host(si)))
+    assert np.all(np.isfinite(outs[0][0])) and np.all(np.isfinite(outs[0][1]))
+    assert np.array_equal(outs[0][0].view(np.uint32), outs[1][0].view(np.uint32))
+    assert np.array_equal(outs[0][1].view(np.uint32), outs[1][1].view(np.uint32))
+
+
 def test_cov_deterministic():
     import torch
     import paper_2405_13954_amd as P

@@ -163,25 +163,36 @@ def test_llama_block_k64_full():
         assert err <= 1e-5
 
 
-def test_cov_blocks_bench_launch():
+@pytest.mark.parametrize("nb,Db,B,lower", [(224, 256, 8, False), (224, 256, 8, True),
+                                             (7, 4096, 16, False), (7, 4096, 16, True)])
+def test_cov_blocks_bench_launch(nb, Db, B, lower):
+    """The covariance launches the bench times: 224 blocks of 256 from 8 store
+    rows (the logging stream) and 7 blocks of 4,096 from 16 rows (the k = 64
+    block), in the symmetric and in the lower-triangle form, accumulated twice."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import dev, host, normwise, say
-    nb, Db, B = 224, 256, 8
-    say(f"[full cov] {nb} blocks of {Db}, {B} bf16 store rows of {nb * Db}")
+    say(f"[full cov] {nb} blocks of {Db}, {B} bf16 store rows of {nb * Db}, lower={lower}")
     scales = W.block_scales(0, nb, 0.1, 10.0)
     g = W.scaled_gradients(0, 410, B, Db, scales)
     S = torch.zeros((nb, Db, Db), dtype=torch.float32, device="cuda")
-    P.logra_cov_accumulate_blocks(dev(g), S, Db)
-    P.logra_cov_accumulate_blocks(dev(g), S, Db)   # accumulates: twice the same rows
+    if lower:
+        S = torch.triu(torch.full((nb, Db, Db), float("nan"), dtype=torch.float32, device="cuda"), 1)
+    acc = P.logra_cov_accumulate_blocks_lower if lower else P.logra_cov_accumulate_blocks
+    acc(dev(g), S, Db)
+    acc(dev(g), S, Db)   # accumulates: twice the same rows
     torch.cuda.synchronize()
-    got = host(S)
-    for l in (0, 97, 223):
+    lo = np.tril(np.ones((Db, Db), bool))
+    for l in sorted({0, nb // 2 - 1, nb // 2, nb - 1}):
+        got = host(S[l])
         want = 2.0 * oracle.cov_accumulate(g[:, l * Db:(l + 1) * Db])
-        err = normwise(got[l], want)
+        if lower:
+            assert np.all(np.isnan(got[~lo]))
+            got = np.where(lo, got, got.T)
+        err = normwise(got, want)
         say(f"  block {l}: normwise err {err:.2e}")
         assert err <= 1e-5
-        assert np.array_equal(got[l], got[l].T)
+        assert np.array_equal(got, got.T)
 
 
 def test_precondition_blocks_bench_launch():
