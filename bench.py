@@ -124,7 +124,7 @@ def write_traffic(fetch_csv, write_csv):
     sc = W.WORKLOADS["llama3_8b_scores"]
     N, Q, D_tot = sc.extra["N_train"], sc.extra["Q"], sc.n_layers * sc.D
     rows = {
-        "projection": ("logra::k_project_chunks<1, 1, unsigned short>", "k_project_chunks<1, 1, bf16>",
+        "projection": ("logra::k_project_stream", "k_project_stream",
                        "7 Llama3-8B layers, B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
                        sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes),
         "projection_k64": ("logra::k_project_tiles<4>", "k_project_tiles<4>",

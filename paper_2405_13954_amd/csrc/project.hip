@@ -522,6 +522,237 @@ __global__ __launch_bounds__(NT, 1) void k_project_chunks(ProjArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// k <= 16 (KT = 1), bf16 inputs that no two layers share: the per-wave stream
+// of k_project_chunks, with each wave's ring kept busy from one item to the
+// next.
+//
+// In k_project_chunks every item starts with an empty ring and ends with a
+// drained one, so each item pays a memory latency before its first step.  At
+// 768 to 4,096 columns per layer side an item is 3 to 24 steps per wave, and
+// that latency is a large share of it.  Here the ring runs on: during the
+// last two steps of an item a wave issues the copies of the first two steps of
+// its band of the next item.  For that the next item must be known when an
+// item starts, so items are claimed two ahead (the first two of a workgroup
+// are blockIdx.x and blockIdx.x + gridDim.x).  A fifth wave does everything
+// besides the streaming: it claims the items and publishes them through LDS,
+// and it folds the four waves' partials, parked in one of two LDS buffers at
+// each item's end, in the order of k_project_chunks, ((w3 + w2) + w1) + w0,
+// and writes them.  The streaming waves issue no memory operation but their
+// copies, so "at most the two later steps' copies pending" is an exact wait,
+// and one barrier per item (LDS operations only) hands over the partials and
+// the next claim.  A band shorter than two steps is padded with empty steps
+// (out-of-range copies, no products) so that the look-ahead never passes the
+// next item.  Each wave's band, step order and sums are those of
+// k_project_chunks, so the results are the same bits.
+constexpr int kStreamNT = (NW + 1) * kWave;   // four streaming waves and the writer
+using StreamSh = DmaShape<1, 1>;
+constexpr int kStreamNS = StreamSh::kStages;
+static_assert(kStreamNS == 3, "the look-ahead is two steps");
+
+// An unshared item's operands and partial slot (the fields chunk_item uses
+// with S = 1).
+struct StreamItem {
+    const bf16_bits *A, *P;
+    int n, k, nk;
+    uint64_t valid;
+    size_t dst;   // float offset of the chunk partial in a.part
+};
+
+__device__ __forceinline__ StreamItem stream_item(const ProjArgs &a, int item, int count) {
+    const int rank = item / count;
+    const int j = item - rank * count;
+    int gslot = rank, l = 0;
+    if (a.ordered) {
+        const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
+        gslot = e & 0xfff;
+        l = (e >> 12) & 0xf;
+    } else {
+        while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
+    }
+    const ChunkLayer &L = a.layer[l];
+    const int cs = gslot - L.slot_begin;
+    const int bt = a.tiles ? load_uniform(a.tiles + j) : j;
+    const int b = bt / a.tpe, tile = bt - b * a.tpe;
+    const bool xside = cs < L.x_items;
+    const int c = xside ? cs : cs - L.x_items;
+    const ChunkLayer &M = xside ? a.layer[L.share[0]] : L;
+    StreamItem it;
+    it.valid = tile_valid(a, j, tile);
+    it.n = xside ? L.n_in : L.n_out;
+    it.k = xside ? a.k_in : a.k_out;
+    const int col0 = c * a.ck;
+    it.nk = min(a.ck, it.n - col0);
+    const size_t tok0 = static_cast<size_t>(b) * a.T + static_cast<size_t>(tile) * TT;
+    it.A = static_cast<const bf16_bits *>(xside ? L.x : L.dy) + tok0 * it.n + col0;
+    it.P = static_cast<const bf16_bits *>(xside ? M.p_in : L.p_out) + col0;
+    const int pslot = xside ? c : M.c_in + c;
+    it.dst = M.part_begin + (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) * (TT * 16);
+    return it;
+}
+
+// One streaming wave's band of an item: steps first .. first + mine - 1 of
+// the chunk, padded to len >= kStreamNS - 1 steps.
+struct StreamBand {
+    __amdgpu_buffer_rsrc_t ra, rp;
+    uint32_t xo[StreamSh::kX], po[StreamSh::kPm];
+    int first, mine, len, nk;
+};
+
+__device__ __forceinline__ void stream_band(StreamBand &d, const StreamItem &it, int wave, int sub, int lcol) {
+    const int nsteps = (it.nk + kDmaCols - 1) / kDmaCols;
+    const int per = (nsteps + NW - 1) / NW;
+    d.first = wave * per;
+    d.mine = max(0, min(per, nsteps - d.first));
+    d.len = max(d.mine, kStreamNS - 1);
+    d.nk = it.nk;
+    d.ra = buf_rsrc(it.A, (static_cast<uint32_t>(TT - 1) * it.n + it.nk) * 2u);
+    d.rp = buf_rsrc(it.P, (static_cast<uint32_t>(it.k - 1) * it.n + it.nk) * 2u);
+#pragma unroll
+    for (int q = 0; q < StreamSh::kX; ++q) {
+        const int t = 8 * q + sub;
+        d.xo[q] = (it.valid >> t) & 1 ? (static_cast<uint32_t>(t) * it.n + lcol) * 2u : kBufOOB;
+    }
+#pragma unroll
+    for (int q = 0; q < StreamSh::kPm; ++q) {
+        const int r = 8 * q + sub;
+        d.po[q] = r < it.k ? (static_cast<uint32_t>(r) * it.n + lcol) * 2u : kBufOOB;
+    }
+}
+
+// The band of no item (past the last): every copy out of range.
+__device__ __forceinline__ void stream_band_none(StreamBand &d, const bf16_bits *base) {
+    d.first = 0;
+    d.mine = 0;
+    d.len = kStreamNS - 1;
+    d.nk = 0;
+    d.ra = buf_rsrc(base, 0u);
+    d.rp = buf_rsrc(base, 0u);
+#pragma unroll
+    for (int q = 0; q < StreamSh::kX; ++q) d.xo[q] = kBufOOB;
+#pragma unroll
+    for (int q = 0; q < StreamSh::kPm; ++q) d.po[q] = kBufOOB;
+}
+
+// Copies of band position p into the stage at LDS address lds (as the issue of
+// project_part_dma).
+__device__ __forceinline__ void stream_issue(const StreamBand &d, int p, uint32_t lds, int lcol) {
+    const int st = d.first + p;
+    const bool in = p < d.mine && st * kDmaCols + lcol < d.nk;
+    const uint32_t dk = static_cast<uint32_t>(st * kDmaCols) * 2u;
+#pragma unroll
+    for (int q = 0; q < StreamSh::kX; ++q) copy_to_lds_nt(d.ra, in ? d.xo[q] + dk : kBufOOB, lds + q * 1024);
+#pragma unroll
+    for (int q = 0; q < StreamSh::kPm; ++q)
+        copy_to_lds(d.rp, in ? d.po[q] + dk : kBufOOB, lds + (StreamSh::kX + q) * 1024);
+}
+
+// The products of one step (as project_part_dma).
+__device__ __forceinline__ void stream_step(f32x4 (&acc)[MB], const uint8_t *base, int lane) {
+    const int row = lane & 15, kg = lane >> 4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int c = 4 * h + kg;
+        bf16x8 xf[MB];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) {
+            const int t = 16 * m + row;
+            xf[m] = as_bf16x8(*reinterpret_cast<const u32x4 *>(base + t * 128 + ((c ^ (t & 7)) << 4)));
+        }
+        const bf16x8 pf =
+            as_bf16x8(*reinterpret_cast<const u32x4 *>(base + StreamSh::kX * 1024 + row * 128 + ((c ^ (row & 7)) << 4)));
+#pragma unroll
+        for (int m = 0; m < MB; ++m) acc[m] = mfma16_bf16(xf[m], pf, acc[m]);
+    }
+}
+
+// LDS writes done, then the workgroup barrier; no wait for copies in flight.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
+    constexpr int NS = kStreamNS;
+    __shared__ __attribute__((aligned(16))) uint8_t ring[StreamSh::kRing];
+    __shared__ f32x4 fold[2][NW][MB * kWave];
+    __shared__ int queue[4];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
+    const int count = a.tiles ? load_uniform(a.n_tiles) : a.B * a.tpe;
+    const int items = count * a.slots;
+    const int grid = static_cast<int>(gridDim.x);
+    int cur = blockIdx.x, nxt = static_cast<int>(blockIdx.x) + grid;
+
+    if (wave == NW) {   // the writer: claims, publishes, folds and writes
+        auto fold_out = [&](int item, const f32x4 (*w)[MB * kWave]) {
+            f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + stream_item(a, item, count).dst) + lane;
+#pragma unroll
+            for (int m = 0; m < MB; ++m) {
+                const int e = m * kWave + lane;
+                dst[m * kWave] = ((w[3][e] + w[2][e]) + w[1][e]) + w[0][e];
+            }
+        };
+        int prev = -1, n = 0;
+        for (; cur < items; ++n) {
+            int claim = items;   // none
+            if (nxt < items) {
+                int c = 0;
+                if (lane == 0) c = atomicAdd(a.work, 1);
+                claim = 2 * grid + __builtin_amdgcn_readfirstlane(c);
+            }
+            if (lane == 0) queue[(n + 2) & 3] = claim;
+            if (prev >= 0) fold_out(prev, fold[(n - 1) & 1]);
+            lds_barrier();   // B_n: the partials of item n are parked, item n + 2 is published
+            prev = cur;
+            cur = nxt;
+            nxt = claim;
+        }
+        if (prev >= 0) fold_out(prev, fold[(n - 1) & 1]);
+        return;
+    }
+
+    // streaming waves
+    const int sub = lane >> 3;
+    const int lcol = ((lane & 7) ^ sub) * 8;   // the lane's element column within a step
+    uint8_t *my_ring = ring + wave * StreamSh::kWaveRing;
+    const uint32_t ring_addr = lds_addr(my_ring);
+    StreamBand dc, dn;
+    int iss = 0, con = 0;   // stages of the next copy and of the next step
+    if (cur < items) {
+        stream_band(dc, stream_item(a, cur, count), wave, sub, lcol);
+#pragma unroll
+        for (int p = 0; p < NS - 1; ++p) {
+            stream_issue(dc, p, ring_addr + iss * StreamSh::kStage, lcol);
+            iss = iss == NS - 1 ? 0 : iss + 1;
+        }
+    }
+    for (int n = 0; cur < items; ++n) {
+        if (nxt < items) stream_band(dn, stream_item(a, nxt, count), wave, sub, lcol);
+        else stream_band_none(dn, static_cast<const bf16_bits *>(a.layer[0].x));
+        f32x4 acc[MB];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int p = 0; p < dc.len; ++p) {
+            const int q = p + NS - 1;   // the position two steps ahead, in this item or the next
+            const uint32_t lds = ring_addr + iss * StreamSh::kStage;
+            if (q < dc.len) stream_issue(dc, q, lds, lcol);
+            else stream_issue(dn, q - dc.len, lds, lcol);
+            iss = iss == NS - 1 ? 0 : iss + 1;
+            // the copies of position p are done when only the two later positions' are pending
+            asm volatile("s_waitcnt vmcnt(%0)" :: "n"((NS - 1) * StreamSh::kCopies) : "memory");
+            if (p < dc.mine) stream_step(acc, my_ring + con * StreamSh::kStage, lane);
+            con = con == NS - 1 ? 0 : con + 1;
+        }
+        f32x4 *park = fold[n & 1][wave] + lane;
+#pragma unroll
+        for (int m = 0; m < MB; ++m) park[m * kWave] = acc[m];
+        lds_barrier();   // B_n
+        const int after = __builtin_amdgcn_readfirstlane(queue[(n + 2) & 3]);
+        cur = nxt;
+        nxt = after;
+        dc = dn;
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the copies issued for no item
+}
+
+// ---------------------------------------------------------------------------
 // bf16, unshared inputs: tile groups sharing one projection slab.
 //
 // At k = 64 a P slab (64 rows x 128 B per 64-column step) is as large as a
@@ -941,7 +1172,7 @@ int plan_shares(ProjArgs &a, int n_layers, int KT, int &smax) {
 
 // Resident workgroups of a kernel on the current device (computed once per
 // device and kernel).
-template <void (*K)(ProjArgs)>
+template <void (*K)(ProjArgs), int kThreads = NT>
 int resident_groups() {
     static int cache[64] = {0};
     int dev = 0;
@@ -950,7 +1181,7 @@ int resident_groups() {
         int cus = 0, per_cu = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
             cus = 256;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(K), NT, 0) !=
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(K), kThreads, 0) !=
                 hipSuccess ||
             per_cu <= 0)
             per_cu = 1;
@@ -971,13 +1202,22 @@ void launch_tiles(const ProjArgs &a, int max_items, hipStream_t s) {
     hipLaunchKernelGGL((k_project_tiles<KT>), dim3(max_items < cap ? max_items : cap), dim3(NT), 0, s, a);
 }
 
+void launch_stream(const ProjArgs &a, int max_items, hipStream_t s) {
+    const int cap = resident_groups<k_project_stream, kStreamNT>();
+    hipLaunchKernelGGL(k_project_stream, dim3(max_items < cap ? max_items : cap), dim3(kStreamNT), 0, s, a);
+}
+
 // Tile groups sharing the projection slab (launch_tiles) for bf16 inputs at
-// KT >= kTilesMinKT (k > 16) without shared inputs; per-wave chunks otherwise.
+// KT >= kTilesMinKT (k > 16) without shared inputs; the item-pipelined stream
+// at k <= 16 without shared inputs; per-wave chunks otherwise.
 constexpr int kTilesMinKT = 2;
 template <int KT, typename TIn>
 void launch_chunks(const ProjArgs &a, int max_items, int smax, hipStream_t s) {
     if constexpr (sizeof(TIn) == 2 && KT >= kTilesMinKT) {
         if (smax == 1) return launch_tiles<KT>(a, a.slots * ((a.B * a.tpe + NW - 1) / NW), s);
+    }
+    if constexpr (sizeof(TIn) == 2 && KT == 1) {
+        if (smax == 1) return launch_stream(a, max_items, s);
     }
     if constexpr (KT <= 2) {
         if (smax == 3) return launch_chunks_s<KT, 3, TIn>(a, max_items, s);
