@@ -9,7 +9,8 @@
 //
 //  0. k_project_prep: clears the work counter and, for masked inputs, builds
 //     the ordered list of 64-token tiles holding at least one valid token,
-//     each with the 64-bit set of its valid tokens.
+//     each with the 64-bit set of its valid tokens (and every tile's set, by
+//     tile index, for step B).
 //  A. k_project_chunks (persistent, sized to the resident capacity): one item
 //     = one contraction chunk (<= 6144 columns at k <= 32, <= 14336 above) of one side (x or dy) of one
 //     listed tile.  Layers given the same x tensor (q/k/v, gate/up of a
@@ -31,10 +32,11 @@
 //  B. k_project_tile_finish: per tile, x' and dy' are the fixed-order sums of
 //     their chunk partials; the tile's sum over tokens of dy'_t x'_t^T is then
 //     formed by fp32 MFMAs straight from those sums (one wave per 16 x 16 block
-//     of G).  Empty tiles give 0.
-//  C. k_project_reduce: per example (and 256-wide output slice), the tile sums are added in tile order
-//     and G_b is written (fp32 or bf16, round to nearest even) to the
-//     caller's store row.
+//     of G at k <= 16; at k > 16 one workgroup per tile, x' and dy' read once
+//     into LDS).  Empty tiles give 0.
+//  C. k_project_reduce: per example and 16 x 16 block of G, the tile sums are
+//     added in tile order and G_b is written (fp32 or bf16, round to nearest
+//     even) to the caller's store row.
 // Every sum has a fixed order, so results are bitwise reproducible.
 #include "common.h"
 #include "internal.h"
@@ -114,10 +116,11 @@ struct ProjArgs {
     const uint8_t *mask;
     const int *tiles;     // non-empty tiles (b * tpe + tile) in index order; NULL = all
     const uint64_t *bits; // their valid tokens (bit i = token 64 tile + i), beside tiles
+    const uint64_t *tile_bits;   // the valid tokens of every tile b * tpe + tile (masked inputs)
     const int *n_tiles;   // their count (device), read when tiles != NULL
     int *work;            // items handed out beyond the first gridDim.x (device counter)
     float *part;    // chunk partials, MFMA result layout, TT x 16KT floats each
-    float *gpart;   // per-tile sums  [layer][b][tile][k_out * k_in]
+    float *gpart;   // per-tile sums [layer][b][tile][16 KT x 16 KT], 16 x 16 blocks in the MFMA result layout
     int B, T, tpe;  // tpe = tiles per example
     int k_in, k_out, ck;
 };
@@ -961,7 +964,8 @@ __device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
 // 64 mask bytes are read as four 128-bit loads when the mask rows are
 // 16-byte aligned.
 __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int B, int T, int tpe, int *tiles,
-                                                        uint64_t *bits, int *n_tiles, int *work) {
+                                                        uint64_t *bits, uint64_t *tile_bits, int *n_tiles,
+                                                        int *work) {
     __shared__ int wsum[16];
     __shared__ int base;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -991,6 +995,7 @@ __global__ __launch_bounds__(1024) void k_project_prep(const uint8_t *mask, int 
                 for (int i = 0; i < n; ++i) set |= static_cast<uint64_t>(m[i] != 0) << i;
             }
         }
+        if (bt < total) tile_bits[bt] = set;
         const int any = set != 0;
         int x = any;
 #pragma unroll
@@ -1035,23 +1040,14 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
     const int per_layer = a.B * a.tpe;
     const int l = tix / per_layer;
     const int bt = tix - l * per_layer;
-    const int b = bt / a.tpe, tile = bt - b * a.tpe;
-    const int D = a.k_in * a.k_out;
-    float *gdst = a.gpart + static_cast<size_t>(tix) * D;
-    const int t = tile * TT + lane;
-    bool tok = t < a.T;
-    if (a.mask && tok) tok = a.mask[static_cast<size_t>(b) * a.T + t] != 0;
-    const bool any = __builtin_amdgcn_ballot_w64(tok) != 0;
-    const int row = lane & 15, grp4 = lane >> 4;
-    const int i = 16 * ji + row;
-    if (!any) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int o = 16 * jo + 4 * grp4 + r;
-            if (o < a.k_out && i < a.k_in) gdst[o * a.k_in + i] = 0.f;
-        }
-        return;
-    }
+    // the tile's sum, block by block in the MFMA result layout: block (jo, ji)
+    // holds register r of lane l at 256 (jo KT + ji) + 64 r + l
+    float *gdst = a.gpart + static_cast<size_t>(tix) * (KP * KP) + blk * 256 + lane;
+    // every tile below tpe holds a token before T; with a mask, the tile's set from prep
+    const bool any = a.mask == nullptr || load_uniform(a.tile_bits + bt) != 0;
+    // The partials are read whether or not the tile has a valid token (an empty
+    // tile's slots hold stale values, in bounds), so that the read does not wait
+    // for the test; an empty tile's block is then 0.
     const ChunkLayer &L = a.layer[l];
     const int C = L.c_in + L.c_out;
     const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP)) + lane;
@@ -1070,34 +1066,103 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc = mfma16_f32(dv[m][r], xv[m][r], acc);
     // result register r of lane l: o = 16 jo + 4 (l / 16) + r, i = 16 ji + l % 16
+    // (whole 256-byte rows per store; entries past k_out or k_in are never read)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int o = 16 * jo + 4 * grp4 + r;
-        if (o < a.k_out && i < a.k_in) gdst[o * a.k_in + i] = acc[r];
+    for (int r = 0; r < 4; ++r) gdst[64 * r] = any ? acc[r] : 0.f;
+}
+
+// The same sums for KT >= 2, one workgroup per tile: the tile's x' and dy'
+// (the fixed-order sums of their chunk partials) are read once into LDS,
+// rather than once per 16 x 16 block of G that needs them (KT times each),
+// and wave w forms blocks w, w + 4, ... from there with the same MFMAs in the
+// same order, so the results are those of k_project_tile_finish.
+template <int KT>
+__global__ __launch_bounds__(256) void k_project_tile_finish_wg(ProjArgs a) {
+    constexpr int KP = 16 * KT;
+    constexpr int NQ = MB * KT * kWave;     // f32x4 per chunk partial
+    static_assert(NQ == 256 * KT, "thread t sums elements t + 256 u, u < KT");
+    __shared__ f32x4 xs[NQ], ds[NQ];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int tix = blockIdx.x;              // tile over all layers
+    const int per_layer = a.B * a.tpe;
+    const int l = tix / per_layer;
+    const int bt = tix - l * per_layer;
+    const bool any = a.mask == nullptr || load_uniform(a.tile_bits + bt) != 0;
+    float *gdst = a.gpart + static_cast<size_t>(tix) * (KP * KP) + lane;
+    if (!any) {   // no valid token: the tile's sum is 0 (its partial slots were never written)
+        for (int e = tid; e < KP * KP; e += 256) gdst[e - lane] = 0.f;
+        return;
+    }
+    const ChunkLayer &L = a.layer[l];
+    const int C = L.c_in + L.c_out;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP));
+    f32x4 x[KT], d[KT];   // all of a chunk's reads in flight at once
+#pragma unroll
+    for (int u = 0; u < KT; ++u) x[u] = d[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < L.c_in; ++c)
+#pragma unroll
+        for (int u = 0; u < KT; ++u) x[u] += src[static_cast<size_t>(c) * NQ + tid + 256 * u];
+    for (int c = L.c_in; c < C; ++c)
+#pragma unroll
+        for (int u = 0; u < KT; ++u) d[u] += src[static_cast<size_t>(c) * NQ + tid + 256 * u];
+#pragma unroll
+    for (int u = 0; u < KT; ++u) {
+        xs[tid + 256 * u] = x[u];
+        ds[tid + 256 * u] = d[u];
+    }
+    __syncthreads();
+    for (int blk = wave; blk < KT * KT; blk += NW) {
+        const int jo = blk / KT, ji = blk - jo * KT;
+        f32x4 dv[MB], xv[MB];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) {
+            xv[m] = xs[(m * KT + ji) * kWave + lane];
+            dv[m] = ds[(m * KT + jo) * kWave + lane];
+        }
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc = mfma16_f32(dv[m][r], xv[m][r], acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gdst[blk * 256 + 64 * r] = acc[r];
     }
 }
 
 template <typename TOut>
-__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, int B,
-                                                        int tpe, int D, int64_t g_ld) {
-    // blockIdx.x: (layer, example); blockIdx.y: a 256-wide slice of the D outputs
+__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, int B, int tpe, int KT,
+                                                        int k_in, int k_out, int64_t g_ld) {
+    // blockIdx.x: (layer, example); blockIdx.y: a 256-float block of the tile sums (block
+    // (jo, ji) of G in the MFMA result layout: thread = 64 r + lane)
     const int l = blockIdx.x / B;
     const int b = blockIdx.x - l * B;
-    const int i = blockIdx.y * 256 + threadIdx.x;
-    if (i >= D) return;
-    const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * D + i;
-    TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
+    const int KB = 256 * KT * KT;
+    const int blk = blockIdx.y, jo = blk / KT, ji = blk - jo * KT;
+    const int r = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int o = 16 * jo + 4 * (lane >> 4) + r, i = 16 * ji + (lane & 15);
+    const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * KB + blk * 256 + threadIdx.x;
     float s = 0.f;
     int t = 0;
-    for (; t + 8 <= tpe; t += 8) {   // eight loads in flight, summed in tile order
+    for (; t + 32 <= tpe; t += 32) {   // 32 loads in flight, summed in tile order
+        float v[32];
+#pragma unroll
+        for (int u = 0; u < 32; ++u) v[u] = p[static_cast<size_t>(t + u) * KB];
+#pragma unroll
+        for (int u = 0; u < 32; ++u) s += v[u];
+    }
+    for (; t + 8 <= tpe; t += 8) {
         float v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * D];
+        for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * KB];
 #pragma unroll
         for (int u = 0; u < 8; ++u) s += v[u];
     }
-    for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * D];
-    store_out<TOut>(out + i, s);
+    for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * KB];
+    if (o < k_out && i < k_in) {
+        TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
+        store_out<TOut>(out + o * k_in + i, s);
+    }
 }
 
 inline int kt_for(int k_in, int k_out) {
@@ -1131,7 +1196,7 @@ Plan plan_group(const int *n_in, const int *n_out, int n_layers, int B, int T, i
         p.slots += ci + co;
         p.part_floats += static_cast<size_t>(ci + co) * B * tpe * TT * 16 * KT;
     }
-    p.gpart_floats = static_cast<size_t>(n_layers) * B * tpe * k_in * k_out;
+    p.gpart_floats = static_cast<size_t>(n_layers) * B * tpe * (16 * KT) * (16 * KT);
     return p;
 }
 
@@ -1236,7 +1301,7 @@ size_t project_ws_bytes(const int *n_in, const int *n_out, int n_layers, int B, 
     const Plan p = plan_group(n_in, n_out, n_layers, B, T, k_in, k_out, nullptr);
     const size_t tiles = static_cast<size_t>(B) * ((T + TT - 1) / TT);
     return align256(p.part_floats * sizeof(float)) + align256(p.gpart_floats * sizeof(float)) +
-           align256((tiles + 2) * sizeof(int)) + align256(tiles * sizeof(uint64_t));
+           align256((tiles + 2) * sizeof(int)) + 2 * align256(tiles * sizeof(uint64_t));
 }
 
 hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, const uint8_t *mask,
@@ -1297,11 +1362,15 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     int *list = reinterpret_cast<int *>(w);
     int *count = list + ntiles;
     uint64_t *bits = reinterpret_cast<uint64_t *>(w + align256((ntiles + 2) * sizeof(int)));
+    uint64_t *tile_bits = reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(bits) +
+                                                       align256(ntiles * sizeof(uint64_t)));
     a.work = count + 1;
     a.tiles = mask ? list : nullptr;
     a.bits = mask ? bits : nullptr;
+    a.tile_bits = mask ? tile_bits : nullptr;
     a.n_tiles = mask ? count : nullptr;
-    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, bits, count, a.work);
+    hipLaunchKernelGGL(k_project_prep, dim3(1), dim3(1024), 0, s, mask, B, T, a.tpe, list, bits, tile_bits, count,
+                       a.work);
     const int max_items = a.slots * B * a.tpe;
     switch (KT) {
         case 1: bf16_in ? launch_chunks<1, bf16_bits>(a, max_items, smax, s) : launch_chunks<1, float>(a, max_items, smax, s); break;
@@ -1314,22 +1383,23 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     if (e != hipSuccess) return e;
     const int pairs = grp.n_layers * B * a.tpe * KT * KT;   // (tile, 16 x 16 block of G), one wave each
     const unsigned fgrid = static_cast<unsigned>((pairs + NW - 1) / NW);
+    const unsigned tgrid = static_cast<unsigned>(grp.n_layers * B * a.tpe);   // one workgroup per tile
     switch (KT) {
         case 1: hipLaunchKernelGGL((k_project_tile_finish<1>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
-        case 2: hipLaunchKernelGGL((k_project_tile_finish<2>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
-        case 4: hipLaunchKernelGGL((k_project_tile_finish<4>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
-        default: hipLaunchKernelGGL((k_project_tile_finish<8>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
+        case 2: hipLaunchKernelGGL((k_project_tile_finish_wg<2>), dim3(tgrid), dim3(256), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((k_project_tile_finish_wg<4>), dim3(tgrid), dim3(256), 0, s, a); break;
+        default: hipLaunchKernelGGL((k_project_tile_finish_wg<8>), dim3(tgrid), dim3(256), 0, s, a); break;
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const unsigned grid = static_cast<unsigned>(grp.n_layers) * B;
-    const unsigned slices = static_cast<unsigned>((k_in * k_out + 255) / 256);
+    const unsigned blocks = static_cast<unsigned>(KT * KT);   // 16 x 16 blocks of G
     if (bf16_out)
-        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid, slices), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
-                           k_in * k_out, g_ld);
+        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid, blocks), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+                           KT, k_in, k_out, g_ld);
     else
-        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid, slices), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
-                           k_in * k_out, g_ld);
+        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid, blocks), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
+                           KT, k_in, k_out, g_ld);
     return hipGetLastError();
 }
 
