@@ -40,14 +40,15 @@ def test_version(L):
 
 def test_workspace_sizes(L):
     # chunk partials (one 64 x 16 fp32 block per side per 64-token tile at k <= 16, chunks of
-    # 6144 columns at k <= 32), per-tile k_out x k_in sums, the list of non-empty tiles (+ its count) and
-    # their 64-bit valid-token sets, each rounded up to 256 bytes
-    assert P.logra_project_ws_size(2, 100, 64, 48, 8, 12) == 2 * 2 * 2 * 64 * 16 * 4 + 1536 + 256 + 256
+    # 6144 columns at k <= 32), per-tile sums in 16 x 16 blocks ((16 KT)^2 floats a tile), the list
+    # of non-empty tiles (+ its count), their 64-bit valid-token sets and every tile's set, each
+    # rounded up to 256 bytes
+    assert P.logra_project_ws_size(2, 100, 64, 48, 8, 12) == 2 * 2 * 2 * 64 * 16 * 4 + 4 * 256 * 4 + 3 * 256
     assert P.logra_project_ws_size(0, 100, 64, 48, 8, 8) == 0
     shapes = [(4096, 4096), (4096, 1024), (4096, 1024), (4096, 4096), (4096, 14336), (4096, 14336), (14336, 4096)]
     descs = (P.LayerDesc * 7)(*[P.LayerDesc(0, 0, 0, 0, 0, a, b) for a, b in shapes])
     # k = 64: chunks of up to 14336 columns -> 14 chunk blocks of 64 x 64 floats per tile
-    want = 14 * 16 * 16 * 64 * 64 * 4 + 7 * 16 * 16 * 4096 * 4 + 1280 + 2048
+    want = 14 * 16 * 16 * 64 * 64 * 4 + 7 * 16 * 16 * 4096 * 4 + 1280 + 2 * 2048
     assert P.logra_project_layers_ws_size(descs, 7, 16, 1024, 64, 64) == want
     assert P.logra_precondition_ws_size(256, 224, 1024) >= 224 * 256 * 256 * 8
     assert P.logra_influence_ws_size(4, 10, 3, 0) == 256
@@ -83,8 +84,8 @@ def test_project_validation(L):
     assert proj(L, B=0) == P.OK                              # no-op, no device access
     assert proj(L, T=0) == P.OK
     assert L.logra_project_layers(None, 1, 1, 2, 8, None, 8, 8, 0, 64, None, 0, None) == P.ERR_INVALID_ARG
-    descs = (P.LayerDesc * 17)()
-    assert L.logra_project_layers(descs, 17, 1, 2, 8, None, 8, 8, 0, 64, None, 0, None) == P.ERR_UNSUPPORTED
+    descs = (P.LayerDesc * 49)()
+    assert L.logra_project_layers(descs, 49, 1, 2, 8, None, 8, 8, 0, 64, None, 0, None) == P.ERR_UNSUPPORTED
 
 
 def test_cov_validation(L):
