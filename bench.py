@@ -4,7 +4,7 @@ Logging leg (the reported `value`, tokens/s): the 32-block Llama3-8B logging
 stream -- per step one batch of B=8 examples of T=2048 padded tokens, valid
 lengths uniform on 128..2048, through all 224 linear layers (k_in = k_out = 16,
 57,344 projected dims per example): fused projection into the bf16 gradient
-store (32 grouped launches of 7 layers) and the 224 per-layer covariance
+store (8 grouped launches of 28 layers, four blocks each) and the 224 per-layer covariance
 updates, each kept as its lower triangle (all the preconditioner reads).
 
 The logging leg's "shared_inputs" entry runs the same stream with the
@@ -279,40 +279,46 @@ def logging_leg(args, torch, P):
     S = torch.zeros((n_layers, D, D), dtype=torch.float32, device=dev)
     lens = [W.lengths(W.rng(args.seed, 200, s), B, w.len_lo, w.len_hi) for s in range(n_steps)]
     masks = [torch.from_numpy(W.mask_from_lengths(L, T)).to(dev) for L in lens]
-    shape_descs = (P.LayerDesc * nl_block)(*[P.LayerDesc(0, 0, 0, 0, 0, ni, no) for _, ni, no in layers])
-    ws_bytes = P.logra_project_layers_ws_size(shape_descs, nl_block, B, T, k, k)
+    gb = args.log_group_blocks            # blocks per grouped launch
+    n_launch = w.blocks // gb
+    nl_launch = gb * nl_block
+    shape_descs = (P.LayerDesc * nl_launch)(*[P.LayerDesc(0, 0, 0, 0, 0, ni, no) for _ in range(gb)
+                                             for _, ni, no in layers])
+    ws_bytes = P.logra_project_layers_ws_size(shape_descs, nl_launch, B, T, k, k)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     L = P.lib()
     g_ld = store.stride(0)
 
-    # descriptor arrays per (step, block), built once
-    def descs(step, blk):
-        arr = (P.LayerDesc * nl_block)()
+    # descriptor arrays per (step, launch of gb blocks), built once
+    def descs(step, li):
+        arr = (P.LayerDesc * nl_launch)()
         row0 = step * B
-        for j in range(nl_block):
-            l = blk * nl_block + j
-            x, dy = bufs[blk % n_buf][j]
-            pi, po = projs[l]
-            g = store[row0:row0 + B, l * D:(l + 1) * D]
-            arr[j] = P.LayerDesc(x.data_ptr(), dy.data_ptr(), pi.data_ptr(), po.data_ptr(), g.data_ptr(),
-                                 x.shape[2], dy.shape[2])
+        for bb in range(gb):
+            blk = li * gb + bb
+            for j in range(nl_block):
+                l = blk * nl_block + j
+                x, dy = bufs[blk % n_buf][j]
+                pi, po = projs[l]
+                g = store[row0:row0 + B, l * D:(l + 1) * D]
+                arr[bb * nl_block + j] = P.LayerDesc(x.data_ptr(), dy.data_ptr(), pi.data_ptr(), po.data_ptr(),
+                                                     g.data_ptr(), x.shape[2], dy.shape[2])
         return arr
 
-    all_descs = [[descs(s, b) for b in range(w.blocks)] for s in range(n_steps)]
+    all_descs = [[descs(s, li) for li in range(n_launch)] for s in range(n_steps)]
     proj_timer = EventTimer(torch)
     cov_timer = EventTimer(torch)
 
     def step(s, timed, descs_of=all_descs, ptimer=proj_timer):
         m = masks[s]
         e0 = ptimer.start() if timed else None   # one pair over the step's back-to-back launches
-        for b in range(w.blocks):
-            rc = L.logra_project_layers(descs_of[s][b], nl_block, P.BF16, B, T, ctypes.c_void_p(m.data_ptr()),
+        for li in range(n_launch):
+            rc = L.logra_project_layers(descs_of[s][li], nl_launch, P.BF16, B, T, ctypes.c_void_p(m.data_ptr()),
                                         k, k, P.BF16, g_ld, ctypes.c_void_p(ws.data_ptr()), ws_bytes, stream)
             if rc != 0:
                 raise P.LograError(rc, P.logra_last_error())
         if timed:
-            ptimer.stop(e0, w.blocks)
+            ptimer.stop(e0, n_launch)
         rows = store[s * B:(s + 1) * B]
         e0 = cov_timer.start() if timed else None
         rc = L.logra_cov_accumulate_blocks_lower(ctypes.c_void_p(rows.data_ptr()), P.BF16, g_ld, B, D, n_layers,
@@ -334,10 +340,10 @@ def logging_leg(args, torch, P):
     dt = time.perf_counter() - t0
     tokens = int(sum(int(L_.sum()) for L_ in lens[args.warmup:]))
     examples = args.steps * B
-    # algorithmic bytes of one grouped launch (7 layers of a block), averaged over timed steps:
-    # valid tokens x 2 B x (n_in + n_out) summed over the block, plus the projections once.
-    per_tok = sum(2 * (ni + no) for _, ni, no in layers)
-    proj_bytes = sum(2 * k * (ni + no) for _, ni, no in layers)
+    # algorithmic bytes of one grouped launch (gb blocks of 7 layers), averaged over timed steps:
+    # valid tokens x 2 B x (n_in + n_out) summed over the launch's layers, plus the projections once.
+    per_tok = gb * sum(2 * (ni + no) for _, ni, no in layers)
+    proj_bytes = gb * sum(2 * k * (ni + no) for _, ni, no in layers)
     bytes_per_launch = tokens / args.steps * per_tok + proj_bytes
     proj_ms = proj_timer.mean_ms()
     achieved = bytes_per_launch / (proj_ms * 1e-3) / 1e9
@@ -349,20 +355,22 @@ def logging_leg(args, torch, P):
         "proj_launch_ms": proj_ms, "cov_launch_ms": cov_timer.mean_ms(),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "traffic_over_algorithmic": ratio,
-                     "kernel": "logra_project_layers (7 Llama3-8B layers, B=8 ragged, k=16)",
+                     "kernel": f"logra_project_layers ({nl_launch} Llama3-8B layers = {gb} blocks, B=8 ragged, k=16)",
                      "bytes_per_launch": bytes_per_launch},
     }
     res["roofline"]["copy_gbs"] = copy_bandwidth(torch)
     if args.shared_inputs:
         # the same stream with the inputs a transformer block shares: q/k/v read
         # one x, gate/up read one x (x elements per token 38,912 -> 26,624)
-        shared = [[descs(st, b) for b in range(w.blocks)] for st in range(n_steps)]
+        shared = [[descs(st, li) for li in range(n_launch)] for st in range(n_steps)]
         for st in range(n_steps):
-            for b in range(w.blocks):
-                for j in (1, 2, 5):
-                    src = shared[st][b][0 if j < 4 else 4]
-                    d = shared[st][b][j]
-                    shared[st][b][j] = P.LayerDesc(src.x, d.dy, d.p_in, d.p_out, d.g_out, d.n_in, d.n_out)
+            for li in range(n_launch):
+                for bb in range(gb):
+                    for j in (1, 2, 5):
+                        src = shared[st][li][bb * nl_block + (0 if j < 4 else 4)]
+                        d = shared[st][li][bb * nl_block + j]
+                        shared[st][li][bb * nl_block + j] = P.LayerDesc(src.x, d.dy, d.p_in, d.p_out, d.g_out,
+                                                                        d.n_in, d.n_out)
         sh_timer = EventTimer(torch)
         for st in range(args.warmup):
             step(st, False, shared, sh_timer)
@@ -374,7 +382,7 @@ def logging_leg(args, torch, P):
         dt_sh = time.perf_counter() - t1
         x_shared = sum(ni for i, (_, ni, _) in enumerate(layers) if i not in (1, 2, 5))
         per_tok_sh = 2 * (x_shared + sum(no for _, _, no in layers))
-        bytes_sh = tokens / args.steps * per_tok_sh + proj_bytes
+        bytes_sh = tokens / args.steps * per_tok_sh * gb + proj_bytes
         res["shared_inputs"] = {
             "tokens_per_s": tokens / dt_sh, "ms_per_step": dt_sh * 1e3 / args.steps,
             "proj_launch_ms": sh_timer.mean_ms(), "bytes_per_token_per_block": per_tok_sh,
@@ -691,7 +699,7 @@ def cpu_block_k64_baseline(sample):
 def gpt2_leg(args, torch, P):
     """GPT-2-small logging: 12 blocks x {qkv, out, fc, proj}, B = 32, T = 512,
     lengths U{64..512} (right padding), k = 16, one step = one batch through
-    all 48 layers, grouped 16 layers (4 blocks) per launch, into a bf16 store
+    all 48 layers in one grouped launch, into a bf16 store
     of 48 x 256 columns, then the 48 covariance blocks of 256 x 256 updated
     from the step's rows.  Each block has its own x / dy (403 MB per block)."""
     w = W.WORKLOADS["gpt2_small_log"]
@@ -717,7 +725,7 @@ def gpt2_leg(args, torch, P):
     masks = [torch.from_numpy(W.mask_from_lengths(Ls, T)).cuda() for Ls in lens]
     store = torch.empty((steps * B, nl * D), dtype=torch.bfloat16, device="cuda")
     S = torch.zeros((nl, D, D), dtype=torch.float32, device="cuda")
-    group = 16
+    group = min(nl, P.MAX_GROUP)
     L = P.lib()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
@@ -772,7 +780,7 @@ def gpt2_leg(args, torch, P):
                    "len_range": [w.len_lo, w.len_hi], "k_in": k, "k_out": k, "layers_per_launch": group},
         "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": ach / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "logra_project_layers (16 GPT-2-small layers, B=32 ragged, k=16)",
+                     "kernel": f"logra_project_layers ({group} GPT-2-small layers, B=32 ragged, k=16)",
                      "bytes_per_launch": launch_bytes},
     }
     sample = None
@@ -1101,6 +1109,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--leg", choices=["all", "log", "influence", "k64", "gpt2"], default="all")
     ap.add_argument("--k64-reps", type=int, default=20, help="timed launches of the k = 64 block leg")
+    ap.add_argument("--log-group-blocks", type=int, default=4, choices=(1, 2, 4),
+                    help="Llama3-8B blocks (7 layers each) per grouped projection launch of the logging leg")
     ap.add_argument("--no-peaks", dest="peaks", action="store_false",
                     help="skip the measured MFMA and HBM ceilings")
     ap.add_argument("--peak-ms", type=float, default=60.0, help="duration of the MFMA ceiling loop at spec rate")
@@ -1152,7 +1162,8 @@ def main():
            "warmup": args.warmup, "ms_per_step": None, "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
            "config": {"workload": "llama3_8b_stream", "blocks": 32, "layers": 224, "B": 8, "T": 2048,
-                      "len_range": [128, 2048], "k_in": 16, "k_out": 16, "store": "bf16 rows of 57,344"}}
+                      "len_range": [128, 2048], "k_in": 16, "k_out": 16, "store": "bf16 rows of 57,344",
+                      "layers_per_launch": 7 * args.log_group_blocks}}
     log_sample = inf_sample = None
     peaks = None
     if args.peaks:

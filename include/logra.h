@@ -56,7 +56,7 @@ typedef enum { LOGRA_F32 = 0, LOGRA_BF16 = 1, LOGRA_F64 = 2 } logra_dtype;
 
 /* Compiled limits. */
 #define LOGRA_MAX_K 128          /* k_in, k_out of one projection */
-#define LOGRA_MAX_GROUP 16       /* layers in one logra_project_layers call */
+#define LOGRA_MAX_GROUP 48       /* layers in one logra_project_layers call */
 #define LOGRA_MAX_PRECOND_D 8192 /* dimension of one preconditioner block */
 #define LOGRA_MAX_TOPK 1024
 

@@ -29,7 +29,7 @@ LIB_PATH = os.path.join(_HERE, "libpaper_logra.so")
 
 F32, BF16, F64 = 0, 1, 2
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NOT_PD, ERR_WORKSPACE, ERR_IO = 0, -1, -2, -3, -4, -5, -6
-MAX_GROUP = 16
+MAX_GROUP = 48
 
 EXPORTED = (
     "logra_last_error", "logra_version",
@@ -221,7 +221,7 @@ def logra_project_layer(x, dy, p_in, p_out, g_out, mask=None, ws=None, stream=No
 
 
 def logra_project_layers(layers, mask=None, ws=None, stream=None):
-    """Grouped projection of up to 16 layers of one batch.  layers: list of dicts with x, dy,
+    """Grouped projection of up to MAX_GROUP (48) layers of one batch.  layers: list of dicts with x, dy,
     p_in, p_out, g_out (shared B, T, k, dtypes and g_out row stride)."""
     n = len(layers)
     arr = (LayerDesc * n)()

@@ -23,7 +23,7 @@ int check_pinned_code(const void *p, const char *name, size_t align);           
 
 typedef uint16_t bf16_bits_t;   // a bf16 value as its bit pattern
 enum DtypeCode { kF32 = 0, kBF16 = 1, kF64 = 2 };   // element types, numbered as in the C ABI
-constexpr int kMaxGroup = 16;   // layers per grouped projection launch
+constexpr int kMaxGroup = 48;   // layers per grouped projection launch
 constexpr int kMaxK = 128;
 constexpr int kMaxTopk = 1024;
 constexpr int kMaxPrecondD = 8192;

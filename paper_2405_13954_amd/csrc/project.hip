@@ -48,8 +48,8 @@ constexpr int MB = 4;                     // 16-token row blocks per tile
 constexpr int TT = 16 * MB;               // tokens per tile
 static_assert(TT == 64, "a tile's valid-token set is one 64-bit word");
 constexpr int NW = 4;                     // waves per workgroup
-constexpr int kMaxSlots = 1024;           // chunk slots a group can order by width
-static_assert(kMaxSlots <= 4096 && kMaxGroup <= 16, "an ordered slot packs its layer into 4 bits");
+constexpr int kMaxSlots = 256;            // chunk slots a group can order by width
+static_assert(kMaxSlots <= 1024 && kMaxGroup <= 64, "an ordered slot packs its slot into 10 bits, its layer into 6");
 constexpr int NT = NW * kWave;            // threads per workgroup
 
 // Contraction columns per work item.  k <= 32: 6,144 (14,336 = 6,144 + 6,144
@@ -92,26 +92,31 @@ __host__ __device__ constexpr bool use_dma() {
     return sizeof(TIn) == 2 && DmaShape<KT, S>::kFits;
 }
 
-struct ChunkLayer {
+struct ChunkLayer {     // 56 bytes: 48 of them fit the kernel arguments
     const void *x;
     const void *dy;
     const void *p_in;
     const void *p_out;
-    int64_t part_begin;  // first float of this layer's chunk partials
     int n_in, n_out;
-    int c_in, c_out;     // chunks of the x side and of the dy side (partial slots per tile)
-    int x_items;         // x-side work slots: c_in for the first layer of a shared x, else 0
-    int slot_begin;      // work slots of the layers before this one
-    uint8_t share_n;     // layers whose x' this layer's x items produce (itself first)
+    uint32_t part_unit;   // first float of this layer's chunk partials, in units of 1024 floats
+    uint16_t c_in, c_out;  // chunks of the x side and of the dy side (partial slots per tile)
+    uint16_t x_items;      // x-side work slots: c_in for the first layer of a shared x, else 0
+    uint16_t slot_begin;   // work slots of the layers before this one
+    uint8_t share_n;       // layers whose x' this layer's x items produce (itself first)
     uint8_t share[kMaxShare];
 };
+static_assert(sizeof(ChunkLayer) == 56, "the layer table stays within the kernel arguments");
+constexpr int kPartUnit = 1024;   // floats per tile per chunk at KT = 1 (every layer's partials are a multiple)
+__device__ __forceinline__ float *part_of(float *part, const ChunkLayer &L) {
+    return part + static_cast<size_t>(L.part_unit) * kPartUnit;
+}
 
 struct ProjArgs {
     ChunkLayer layer[kMaxGroup];
     int n_layers;
     int slots;      // chunk slots of all layers
     int ordered;    // slot_order holds the processing order of the slots
-    // processing order: entry = layer << 12 | work slot (over all layers)
+    // processing order: entry = layer << 10 | work slot (over all layers)
     alignas(4) uint16_t slot_order[kMaxSlots];
     const uint8_t *mask;
     const int *tiles;     // non-empty tiles (b * tpe + tile) in index order; NULL = all
@@ -367,8 +372,8 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     int gslot = rank, l = 0;                    // work slot over all layers, and its layer
     if (a.ordered) {   // whole dwords of the argument block: scalar loads
         const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
-        gslot = e & 0xfff;
-        l = (e >> 12) & 0xf;
+        gslot = e & 0x3ff;
+        l = (e >> 10) & 0x3f;
     } else {
         while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
     }
@@ -398,7 +403,7 @@ __device__ __forceinline__ void chunk_item(const ProjArgs &a, int item, int coun
     auto member_dst = [&](int q) {   // member q's partial slot; element (m, jj) at [(m KT + jj) 64 + lane]
         const ChunkLayer &M = xside ? a.layer[L.share[q]] : L;
         const int pslot = xside ? c : M.c_in + c;
-        return reinterpret_cast<f32x4 *>(a.part + M.part_begin +
+        return reinterpret_cast<f32x4 *>(part_of(a.part, M) +
                                          (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) * (TT * 16 * KT)) +
                lane;
     };
@@ -567,8 +572,8 @@ __device__ __forceinline__ StreamItem stream_item(const ProjArgs &a, int item, i
     int gslot = rank, l = 0;
     if (a.ordered) {
         const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
-        gslot = e & 0xfff;
-        l = (e >> 12) & 0xf;
+        gslot = e & 0x3ff;
+        l = (e >> 10) & 0x3f;
     } else {
         while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
     }
@@ -589,7 +594,7 @@ __device__ __forceinline__ StreamItem stream_item(const ProjArgs &a, int item, i
     it.A = static_cast<const bf16_bits *>(xside ? L.x : L.dy) + tok0 * it.n + col0;
     it.P = static_cast<const bf16_bits *>(xside ? M.p_in : L.p_out) + col0;
     const int pslot = xside ? c : M.c_in + c;
-    it.dst = M.part_begin + (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) * (TT * 16);
+    it.dst = static_cast<size_t>(M.part_unit) * kPartUnit + (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) * (TT * 16);
     return it;
 }
 
@@ -811,8 +816,8 @@ __device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int
     int gslot = rank, l = 0;
     if (a.ordered) {
         const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
-        gslot = e & 0xfff;
-        l = (e >> 12) & 0xf;
+        gslot = e & 0x3ff;
+        l = (e >> 10) & 0x3f;
     } else {
         while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
     }
@@ -915,7 +920,7 @@ __device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     if (has) {
         const int pslot = xside ? c : L.c_in + c;
-        f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + L.part_begin +
+        f32x4 *dst = reinterpret_cast<f32x4 *>(part_of(a.part, L) +
                                                (static_cast<size_t>(bt) * (L.c_in + L.c_out) + pslot) *
                                                    (TT * 16 * KT)) + lane;
 #pragma unroll
@@ -1050,7 +1055,7 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
     // for the test; an empty tile's block is then 0.
     const ChunkLayer &L = a.layer[l];
     const int C = L.c_in + L.c_out;
-    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP)) + lane;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(part_of(a.part, L) + static_cast<size_t>(bt) * C * (TT * KP)) + lane;
     f32x4 dv[MB], xv[MB];
 #pragma unroll
     for (int m = 0; m < MB; ++m) dv[m] = xv[m] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1096,7 +1101,7 @@ __global__ __launch_bounds__(256) void k_project_tile_finish_wg(ProjArgs a) {
     }
     const ChunkLayer &L = a.layer[l];
     const int C = L.c_in + L.c_out;
-    const f32x4 *src = reinterpret_cast<const f32x4 *>(a.part + L.part_begin + static_cast<size_t>(bt) * C * (TT * KP));
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(part_of(a.part, L) + static_cast<size_t>(bt) * C * (TT * KP));
     f32x4 x[KT], d[KT];   // all of a chunk's reads in flight at once
 #pragma unroll
     for (int u = 0; u < KT; ++u) x[u] = d[u] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1188,10 +1193,10 @@ Plan plan_group(const int *n_in, const int *n_out, int n_layers, int B, int T, i
         if (a) {
             a->layer[l].n_in = n_in[l];
             a->layer[l].n_out = n_out[l];
-            a->layer[l].c_in = ci;
-            a->layer[l].c_out = co;
-            a->layer[l].slot_begin = p.slots;
-            a->layer[l].part_begin = static_cast<int64_t>(p.part_floats);
+            a->layer[l].c_in = static_cast<uint16_t>(ci);
+            a->layer[l].c_out = static_cast<uint16_t>(co);
+            a->layer[l].slot_begin = static_cast<uint16_t>(p.slots);
+            a->layer[l].part_unit = static_cast<uint32_t>(p.part_floats / kPartUnit);
         }
         p.slots += ci + co;
         p.part_floats += static_cast<size_t>(ci + co) * B * tpe * TT * 16 * KT;
@@ -1229,7 +1234,7 @@ int plan_shares(ProjArgs &a, int n_layers, int KT, int &smax) {
     }
     int slots = 0;
     for (int l = 0; l < n_layers; ++l) {
-        a.layer[l].slot_begin = slots;
+        a.layer[l].slot_begin = static_cast<uint16_t>(slots);
         slots += a.layer[l].x_items + a.layer[l].c_out;
     }
     return slots;
@@ -1318,6 +1323,8 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
         a.layer[l].p_out = grp.layer[l].p_out;
     }
     const Plan p = plan_group(n_in, n_out, grp.n_layers, B, T, k_in, k_out, &a);
+    // the compact layer table: partial offsets in 32-bit units, slot indices in 16 bits
+    if (p.part_floats / kPartUnit > 0xffffffffull || p.slots > 0xffff) return hipErrorInvalidValue;
     const int KT = kt_for(k_in, k_out);
     a.n_layers = grp.n_layers;
     int smax = 1;
@@ -1340,7 +1347,7 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
         for (int w = chunk_cols(KT); w > 0; ) {   // descending distinct widths
             int next = 0;
             for (int sl = 0; sl < a.slots; ++sl) {
-                if (width[sl] == w) a.slot_order[n++] = static_cast<uint16_t>(layer_of[sl] << 12 | sl);
+                if (width[sl] == w) a.slot_order[n++] = static_cast<uint16_t>(layer_of[sl] << 10 | sl);
                 else if (width[sl] < w && width[sl] > next) next = width[sl];
             }
             w = next;

@@ -2,9 +2,9 @@
 and at the full sizes of the two other logging workloads, on outputs the
 float64 oracle can compute one by one:
 
-- the grouped projection of one Llama3-8B block (7 layers, B=8, T=2048,
-  lengths U{128..2048}, k=16, bf16 store rows of 57,344) on three sampled
-  layers, all examples;
+- the grouped projection of four Llama3-8B blocks (28 layers, B=8, T=2048,
+  lengths U{128..2048}, k=16, bf16 and fp32 store rows of 57,344) on three
+  sampled layers, all examples;
 - GPT-2-small logging (48 layers, B=32, T=512, ragged) and one Llama3-8B
   block at k = 64 (B=16, T=1024, 4096 x 4096 covariances): sampled layers
   and covariance blocks;
@@ -52,19 +52,24 @@ def _layer_inputs(torch, gen, B, T, n_in, n_out, k, w):
 
 
 def test_project_llama_block_bench_launch():
+    """The grouped launch the logging bench times: four Llama3-8B blocks (28
+    layers), B=8, T=2048, ragged lengths, k=16, into bf16 and fp32 store rows;
+    three sampled layers in different blocks, all examples, against the oracle."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import host, normwise, say
     w = W.WORKLOADS["llama3_8b_stream"]
     B, T, k = w.B, w.T, w.k_in
     D = k * k
+    gb, nlb = 4, len(w.layers)
     lens = W.lengths(W.rng(0, 200, 0), B, w.len_lo, w.len_hi)
     mask_np = W.mask_from_lengths(lens, T)
     mask = torch.from_numpy(mask_np).cuda()
-    say(f"[full project] 7 Llama3-8B layers, B={B} T={T} k={k}, {int(lens.sum())} valid tokens")
+    say(f"[full project] {gb * nlb} Llama3-8B layers ({gb} blocks), B={B} T={T} k={k}, {int(lens.sum())} valid tokens")
     gen = W.torch_generator(0, 400)
-    tensors = [_layer_inputs(torch, gen, B, T, ni, no, k, w) for _, ni, no in w.layers]
+    tensors = [_layer_inputs(torch, gen, B, T, ni, no, k, w) for _ in range(gb) for _, ni, no in w.layers]
     D_tot = w.n_layers * D
+    n = gb * nlb
     results = {}
     for gdt in (torch.bfloat16, torch.float32):
         store = torch.full((B, D_tot), 7.0, dtype=gdt, device="cuda")
@@ -73,24 +78,25 @@ def test_project_llama_block_bench_launch():
         P.logra_project_layers(layers, mask=mask)
         torch.cuda.synchronize()
         results[gdt] = host(store)
-        assert np.all(results[gdt][:, 7 * D:].astype(np.float64) == 7.0) if gdt == torch.float32 else True
-    for j in (1, 4, 6):   # k (4096->1024), gate (4096->14336), down (14336->4096)
-        name, ni, no = w.layers[j]
-        x, dy, pi, po = (host(t) for t in tensors[j])
+        if gdt == torch.float32:
+            assert np.all(results[gdt][:, n * D:].astype(np.float64) == 7.0)
+    for l in (1, 11, 27):   # block 0 k (4096->1024), block 1 gate (4096->14336), block 3 down (14336->4096)
+        name, ni, no = w.layers[l % nlb]
+        x, dy, pi, po = (host(t) for t in tensors[l])
         want = oracle.project_factored(x, dy, pi, po, mask_np)
         for gdt, tol in ((torch.bfloat16, 2e-2), (torch.float32, 1e-3)):
-            got = results[gdt][:, j * D:(j + 1) * D]
+            got = results[gdt][:, l * D:(l + 1) * D]
             errs = [normwise(got[b], want[b]) for b in range(B)]
-            say(f"  {name} ({ni}->{no}) {str(gdt)[6:]}: max normwise err {max(errs):.2e}")
+            say(f"  layer {l} {name} ({ni}->{no}) {str(gdt)[6:]}: max normwise err {max(errs):.2e}")
             assert max(errs) <= tol
 
 
 def test_gpt2_small_logging_full():
     """GPT-2-small logging at its full size: 12 blocks x {qkv, out, fc, proj},
-    B=32, T=512, lengths U{64..512}, k=16, one grouped launch per block into
-    a bf16 store of 48 x 256 columns, then the 48 covariance blocks from the
-    store rows.  Sampled layers (all 32 examples) and covariance blocks
-    against the oracle."""
+    B=32, T=512, lengths U{64..512}, k=16, all 48 layers in one grouped launch
+    (as the bench runs it) into a bf16 store of 48 x 256 columns, then the 48
+    covariance blocks (lower triangles) from the store rows.  Sampled layers
+    (all 32 examples) and covariance blocks against the oracle."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import host, normwise, say
@@ -103,21 +109,22 @@ def test_gpt2_small_logging_full():
     say(f"[full gpt2-small] {w.blocks} blocks x {nl} layers, B={B} T={T} k={k}, {int(lens.sum())} valid tokens")
     store = torch.empty((B, w.blocks * nl * D), dtype=torch.bfloat16, device="cuda")
     sampled = {(0, 0), (0, 3), (5, 2), (11, 1)}           # (block, layer)
-    kept = {}
+    tensors, layers = [], []
     for blk in range(w.blocks):
         gen = W.torch_generator(0, 510, blk)
-        tensors = [_layer_inputs(torch, gen, B, T, ni, no, k, w) for _, ni, no in w.layers]
-        layers = [dict(x=x, dy=dy, p_in=pi, p_out=po, g_out=store[:, (blk * nl + j) * D:(blk * nl + j + 1) * D])
-                  for j, (x, dy, pi, po) in enumerate(tensors)]
-        P.logra_project_layers(layers, mask=mask)
-        for j in range(nl):
-            if (blk, j) in sampled:
-                kept[(blk, j)] = [host(t) for t in tensors[j]]
-        del tensors, layers
-    S = torch.zeros((w.blocks * nl, D, D), dtype=torch.float32, device="cuda")
-    P.logra_cov_accumulate_blocks(store, S, D)
+        for j, (_, ni, no) in enumerate(w.layers):
+            x, dy, pi, po = _layer_inputs(torch, gen, B, T, ni, no, k, w)
+            tensors.append((x, dy, pi, po))
+            layers.append(dict(x=x, dy=dy, p_in=pi, p_out=po,
+                               g_out=store[:, (blk * nl + j) * D:(blk * nl + j + 1) * D]))
+    assert len(layers) <= P.MAX_GROUP
+    P.logra_project_layers(layers, mask=mask)
+    kept = {(blk, j): [host(t) for t in tensors[blk * nl + j]] for blk, j in sampled}
+    S = torch.triu(torch.full((w.blocks * nl, D, D), float("nan"), dtype=torch.float32, device="cuda"), 1)
+    P.logra_cov_accumulate_blocks_lower(store, S, D)
     torch.cuda.synchronize()
     got, S_h = host(store), host(S)
+    lo = np.tril(np.ones((D, D), bool))
     for (blk, j), (x, dy, pi, po) in sorted(kept.items()):
         want = oracle.project_factored(x, dy, pi, po, mask_np)
         c = (blk * nl + j) * D
@@ -125,7 +132,8 @@ def test_gpt2_small_logging_full():
         say(f"  block {blk} {w.layers[j][0]}: max normwise err {err:.2e}")
         assert err <= 2e-2
     for l in (0, 21, 47):
-        err = normwise(S_h[l], oracle.cov_accumulate(got[:, l * D:(l + 1) * D]))
+        assert np.all(np.isnan(S_h[l][~lo]))
+        err = normwise(np.where(lo, S_h[l], S_h[l].T), oracle.cov_accumulate(got[:, l * D:(l + 1) * D]))
         say(f"  covariance block {l}: normwise err {err:.2e}")
         assert err <= 1e-5
 

@@ -1,11 +1,12 @@
 """The whole Llama3-8B logging stream at its full size (Sec. 3.1 Eq. (5) and
 Sec. 2 Eq. (3) over a complete logging run): 65,536 examples in 8,192
 batches of B=8 (T=2048, lengths U{128..2048}), every batch through all 224
-layers (32 grouped launches of 7 layers, k=16) into the bf16 store of
+layers (8 grouped launches of 28 layers, four blocks each, k=16, as the
+bench runs them) into the bf16 store of
 65,536 rows of 57,344, and the 224 covariances (kept as lower triangles)
 accumulated over all 65,536 examples.
 
-x / dy are two device buffer sets cycled over the 32 blocks (drawing 2.7 GB
+x / dy are four device buffer sets cycled over the 32 blocks (drawing 2.7 GB
 per block and batch would be the whole test); the valid lengths, and so the
 masks, differ per batch.  Checks against the float64 oracle: sampled store
 rows (first, middle and last batch; first and last example; three layers)
@@ -36,7 +37,8 @@ def test_full_logging_stream():
     D_tot = n_layers * D
     n_ex = w.extra["examples"]
     n_steps = n_ex // B
-    n_buf = 2
+    n_buf = 4       # x / dy buffer sets: the four blocks of a launch have their own
+    gb = 4          # blocks per grouped launch
     say(f"[full stream] {n_ex} examples in {n_steps} batches of {B}, {n_layers} layers, store {n_ex} x {D_tot} bf16")
     gen = W.torch_generator(0, 600)
     bufs = []
@@ -63,30 +65,33 @@ def test_full_logging_stream():
     masks = torch.from_numpy(np.stack([W.mask_from_lengths(L_, T) for L_ in lens])).cuda()
     L = P.lib()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    shape = (P.LayerDesc * nlb)(*[P.LayerDesc(0, 0, 0, 0, 0, ni, no) for _, ni, no in w.layers])
-    wsb = P.logra_project_layers_ws_size(shape, nlb, B, T, k, k)
+    nll = gb * nlb
+    shape = (P.LayerDesc * nll)(*[P.LayerDesc(0, 0, 0, 0, 0, ni, no) for _ in range(gb) for _, ni, no in w.layers])
+    wsb = P.logra_project_layers_ws_size(shape, nll, B, T, k, k)
     ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
     g_ld = store.stride(0)
     row_bytes = g_ld * 2
-    # one descriptor array per block; only the store rows change from batch to batch
+    # one descriptor array per launch; only the store rows change from batch to batch
     descs = []
-    for blk in range(n_layers // nlb):
-        arr = (P.LayerDesc * nlb)()
-        for j, (_, ni, no) in enumerate(w.layers):
-            x, dy = bufs[blk % n_buf][j]
-            pi, po = projs[blk * nlb + j]
-            arr[j] = P.LayerDesc(x.data_ptr(), dy.data_ptr(), pi.data_ptr(), po.data_ptr(),
-                                 store[0:1, (blk * nlb + j) * D:].data_ptr(), ni, no)
+    for li in range(n_layers // nll):
+        arr = (P.LayerDesc * nll)()
+        for bb in range(gb):
+            blk = li * gb + bb
+            for j, (_, ni, no) in enumerate(w.layers):
+                x, dy = bufs[blk % n_buf][j]
+                pi, po = projs[blk * nlb + j]
+                arr[bb * nlb + j] = P.LayerDesc(x.data_ptr(), dy.data_ptr(), pi.data_ptr(), po.data_ptr(),
+                                                store[0:1, (blk * nlb + j) * D:].data_ptr(), ni, no)
         descs.append(arr)
-    g0 = [[arr[j].g_out for j in range(nlb)] for arr in descs]
+    g0 = [[arr[j].g_out for j in range(nll)] for arr in descs]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(n_steps):
         mp = ctypes.c_void_p(masks[s].data_ptr())
-        for blk, arr in enumerate(descs):
-            for j in range(nlb):
-                arr[j].g_out = g0[blk][j] + s * B * row_bytes
-            rc = L.logra_project_layers(arr, nlb, P.BF16, B, T, mp, k, k, P.BF16, g_ld,
+        for li, arr in enumerate(descs):
+            for j in range(nll):
+                arr[j].g_out = g0[li][j] + s * B * row_bytes
+            rc = L.logra_project_layers(arr, nll, P.BF16, B, T, mp, k, k, P.BF16, g_ld,
                                         ctypes.c_void_p(ws.data_ptr()), wsb, stream)
             assert rc == 0, P.logra_last_error()
         rc = L.logra_cov_accumulate_blocks_lower(ctypes.c_void_p(store[s * B].data_ptr()), P.BF16, g_ld, B, D,
