@@ -125,8 +125,8 @@ def write_traffic(fetch_csv, write_csv):
     N, Q, D_tot = sc.extra["N_train"], sc.extra["Q"], sc.n_layers * sc.D
     rows = {
         "projection": ("logra::k_project_stream", "k_project_stream",
-                       "7 Llama3-8B layers, B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
-                       sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes),
+                       "28 Llama3-8B layers (4 blocks), B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
+                       4 * (sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes)),
         "projection_k64": ("logra::k_project_tiles<4>", "k_project_tiles<4>",
                            "7 Llama3-8B layers, B=16, T=1024, all valid, k=64", PROJ_SOURCES,
                            16 * 1024 * per_tok + sum(2 * 64 * (a + b) for _, a, b in stream.layers)),
