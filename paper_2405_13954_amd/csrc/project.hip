@@ -1048,11 +1048,15 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
     // the tile's sum, block by block in the MFMA result layout: block (jo, ji)
     // holds register r of lane l at 256 (jo KT + ji) + 64 r + l
     float *gdst = a.gpart + static_cast<size_t>(tix) * (KP * KP) + blk * 256 + lane;
-    // every tile below tpe holds a token before T; with a mask, the tile's set from prep
+    // every tile below tpe holds a token before T; with a mask, the tile's set from
+    // prep.  An empty tile's block is 0 and its partial slots (never written) are
+    // not read: with ragged batches that is a third or more of the reads here.
     const bool any = a.mask == nullptr || load_uniform(a.tile_bits + bt) != 0;
-    // The partials are read whether or not the tile has a valid token (an empty
-    // tile's slots hold stale values, in bounds), so that the read does not wait
-    // for the test; an empty tile's block is then 0.
+    if (!any) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gdst[64 * r] = 0.f;
+        return;
+    }
     const ChunkLayer &L = a.layer[l];
     const int C = L.c_in + L.c_out;
     const f32x4 *src = reinterpret_cast<const f32x4 *>(part_of(a.part, L) + static_cast<size_t>(bt) * C * (TT * KP)) + lane;
@@ -1073,7 +1077,7 @@ __global__ __launch_bounds__(256) void k_project_tile_finish(ProjArgs a, int pai
     // result register r of lane l: o = 16 jo + 4 (l / 16) + r, i = 16 ji + l % 16
     // (whole 256-byte rows per store; entries past k_out or k_in are never read)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) gdst[64 * r] = any ? acc[r] : 0.f;
+    for (int r = 0; r < 4; ++r) gdst[64 * r] = acc[r];
 }
 
 // The same sums for KT >= 2, one workgroup per tile: the tile's x' and dy'
