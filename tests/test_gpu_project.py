@@ -228,6 +228,58 @@ def test_project_scattered_mask_vs_oracle():
             assert err <= 1e-3
 
 
+@pytest.mark.parametrize("k,shared", [(16, False), (16, True), (64, False)])
+def test_project_largest_group_equals_single(k, shared):
+    """A grouped launch of the most layers it takes (48: the packed per-layer
+    table, layer indices past 15 in the slot order), with layers of many
+    widths, some of them multi-chunk at k = 16, a ragged mask, and at k = 16
+    groups of layers given the same x (shared passes): every output equals
+    bit for bit the output of the same layer projected in a launch of its
+    own, and sampled layers match the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, normwise, say
+    nl = P.MAX_GROUP
+    g = W.rng(81, k, int(shared))
+    B, T = 3, 130
+    widths = [64, 200, 768, 1000, 6144 + 128, 96]
+    shapes = [(widths[(i // 2) % 6], widths[(i * 5 + 2) % 6]) for i in range(nl)]   # pairs share a width
+    if k == 64:   # the wide layers only in the first half, to keep the test small
+        shapes = [(ni if i < 24 else min(ni, 1000), no if i < 24 else min(no, 1000)) for i, (ni, no) in enumerate(shapes)]
+    say(f"[project] {nl} layers in one launch at k={k}, shared inputs {shared}, B={B} T={T}")
+    lens = W.lengths(g, B, 1, T)
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = dev(mask_np)
+    xs, ins = [], []
+    for i, (ni, no) in enumerate(shapes):
+        if shared and i % 2 == 1:   # the same tensor as the layer before: one shared pass
+            xs.append(xs[-1])
+            ins.append(ins[-1])
+        else:
+            xs.append(W.normal(g, (B, T, ni), 1.0, "bf16"))
+            ins.append(dev(xs[-1]))
+    dys = [W.normal(g, (B, T, no), 1e-2, "bf16") for _, no in shapes]
+    pis = [W.projection(g, k, ni, "bf16") for ni, _ in shapes]
+    pos = [W.projection(g, k, no, "bf16") for _, no in shapes]
+    D = k * k
+    store_g = torch.full((B, nl * D), np.nan, dtype=torch.float32, device="cuda")
+    store_s = torch.full_like(store_g, np.nan)
+    layers = []
+    for i in range(nl):
+        t = dict(x=ins[i], dy=dev(dys[i]), p_in=dev(pis[i]), p_out=dev(pos[i]))
+        layers.append(dict(t, g_out=store_g[:, i * D:(i + 1) * D]))
+        P.logra_project_layer(t["x"], t["dy"], t["p_in"], t["p_out"], store_s[:, i * D:(i + 1) * D], mask=mask)
+    P.logra_project_layers(layers, mask=mask)
+    torch.cuda.synchronize()
+    got_g, got_s = host(store_g), host(store_s)
+    assert np.array_equal(got_g.view(np.uint32), got_s.view(np.uint32))
+    for i in (0, 17, nl - 1):
+        want = oracle.project_factored(xs[i], dys[i], pis[i], pos[i], mask_np)
+        err = max(normwise(got_g[b, i * D:(i + 1) * D], want[b]) for b in range(B))
+        say(f"  layer {i} ({shapes[i][0]}->{shapes[i][1]}): max normwise err {err:.2e}")
+        assert err <= 1e-3
+
+
 def test_project_shared_inputs_bitwise_equal():
     """Layers given the same x tensor (q/k/v and gate/up of a transformer
     block) are projected from one pass over x; every output must equal, bit
