@@ -98,26 +98,34 @@ def write_traffic(fetch_csv, write_csv):
     launches: the scores-only GEMM over all 500,000 rows, the self-influence
     of the store).  Reads = 2 x FETCH_SIZE and writes = 1 x WRITE_SIZE (KiB):
     the factors a plain copy of 1 GiB shows (524,288 KiB fetched, 1,048,576
-    KiB written)."""
+    KiB written).  The stream kernel's grid is the same for every launch (it
+    is sized to the resident workgroups), so its row takes the first launches
+    in dispatch order instead: the logging leg runs first, 4 steps of 8
+    28-layer launches."""
     import collections
     import csv
     import re
+
+    stream = W.WORKLOADS["llama3_8b_stream"]
+    log_launches = 4 * (stream.n_layers // (4 * len(stream.layers)))
 
     def load(path, ctr):
         d = collections.defaultdict(list)
         for r in csv.DictReader(open(path)):
             if r["Counter_Name"] == ctr and "logra" in r["Kernel_Name"]:
                 n = re.sub(r"\(.*", "", r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("void ", ""))
-                d[n].append((int(r["Grid_Size"]), float(r["Counter_Value"])))
+                d[n].append((int(r["Dispatch_Id"]), int(r["Grid_Size"]), float(r["Counter_Value"])))
         out = {}
         for n, v in d.items():
-            gmax = max(g for g, _ in v)
-            vals = [x for g, x in v if g == gmax]
+            if n == "logra::k_project_stream":
+                vals = [x for _, _, x in sorted(v)[:log_launches]]
+            else:
+                gmax = max(g for _, g, _ in v)
+                vals = [x for _, g, x in v if g == gmax]
             out[n] = sum(vals) / len(vals)
         return out
 
     f, w = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
-    stream = W.WORKLOADS["llama3_8b_stream"]
     lens = [W.lengths(W.rng(0, 200, s), stream.B, stream.len_lo, stream.len_hi) for s in range(4)]
     per_tok = sum(2 * (a + b) for _, a, b in stream.layers)
     p_bytes = sum(2 * stream.k_in * (a + b) for _, a, b in stream.layers)
