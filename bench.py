@@ -203,6 +203,8 @@ def peaks_leg(args, torch):
     L = ctypes.CDLL(os.path.join(os.path.dirname(P.LIB_PATH), "libpaper_logra_peaks.so"))
     L.logra_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                        ctypes.c_void_p]
+    L.logra_peak_mfma_bf16_data.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p]
     L.logra_peak_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                       ctypes.c_void_p]
     props = torch.cuda.get_device_properties(0)
@@ -222,10 +224,30 @@ def peaks_leg(args, torch):
             t.stop(e0)
     torch.cuda.synchronize()
     mfma_tf = flops_per_iter * iters / (t.mean_ms() * 1e-3) / 1e12
-    cycles, ticks = (int(v) for v in cyc.cpu())
     khz = ctypes.c_int(0)
     wall_khz = khz.value if L.logra_peak_wall_clock_khz(ctypes.byref(khz)) == 0 else None
-    clock_ghz = cycles / (ticks / (wall_khz * 1e3)) / 1e9 if wall_khz and ticks > 0 else None
+
+    def clock_of(c):
+        cycles, ticks = (int(v) for v in c.cpu())
+        return cycles / (ticks / (wall_khz * 1e3)) / 1e9 if wall_khz and ticks > 0 else None
+
+    clock_ghz = clock_of(cyc)
+    # the same loop with random bf16 operands that change from one MFMA to the next
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+    ops = torch.randn(16 * 16 * 256 * 8, device="cuda", generator=gen).to(torch.bfloat16)   # 1 MiB
+    iters_d = iters - iters % 8
+    td = EventTimer(torch)
+    for timed in (False, True, True, True):
+        e0 = td.start() if timed else None
+        assert L.logra_peak_mfma_bf16_data(groups, iters_d, ctypes.c_void_p(ops.data_ptr()),
+                                           ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(cyc.data_ptr()),
+                                           stream) == 0
+        if timed:
+            td.stop(e0)
+    torch.cuda.synchronize()
+    mfma_data_tf = flops_per_iter * iters_d / (td.mean_ms() * 1e-3) / 1e12
+    data_clock_ghz = clock_of(cyc)
     nbytes = 4 << 30
     buf = torch.empty(nbytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
     modes = {}
@@ -243,11 +265,15 @@ def peaks_leg(args, torch):
     del buf
     torch.cuda.empty_cache()
     return {"mfma_bf16_tflops": mfma_tf, "mfma_frac_of_spec": mfma_tf / BF16_PEAK_TFLOPS,
-            "mfma_ms": t.mean_ms(), "mfma_clock_ghz": clock_ghz, "hbm_read_gbs": read_gbs,
+            "mfma_ms": t.mean_ms(), "mfma_clock_ghz": clock_ghz,
+            "mfma_bf16_data_tflops": mfma_data_tf, "mfma_data_frac_of_spec": mfma_data_tf / BF16_PEAK_TFLOPS,
+            "mfma_data_ms": td.mean_ms(), "mfma_data_clock_ghz": data_clock_ghz, "hbm_read_gbs": read_gbs,
             "hbm_read_frac_of_spec": read_gbs / HBM_PEAK_GBS, "hbm_read_gbs_by_method": modes,
             "compute_units": cus,
-            "note": "sustained 32x32x16 bf16 MFMA loop on every CU for the time shown; a 4 GiB read stream "
-                    "three ways, the best taken as the ceiling; published peaks 2,500 TFLOP/s and 8,000 GB/s"}
+            "note": "sustained 32x32x16 bf16 MFMA loop on every CU for the time shown, once on one constant "
+                    "operand pair (mfma_bf16_*) and once on random operands that change from one MFMA to the "
+                    "next (mfma_bf16_data_*, the ceiling for products of real data); a 4 GiB read stream three "
+                    "ways, the best taken as the ceiling; published peaks 2,500 TFLOP/s and 8,000 GB/s"}
 
 
 # ------------------------------------------------------------------ logging --
@@ -1216,6 +1242,8 @@ def main():
             if r:
                 ceil = peaks["hbm_read_gbs"] if r["bound"] == "hbm" else peaks["mfma_bf16_tflops"]
                 r["frac_of_measured_peak"] = r["achieved"] / ceil
+                if r["bound"] == "mfma":
+                    r["frac_of_measured_data_peak"] = r["achieved"] / peaks["mfma_bf16_data_tflops"]
     print(json.dumps(out), flush=True)
 
 

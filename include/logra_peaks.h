@@ -15,6 +15,14 @@
  *   first and last MFMA round (hipDeviceAttributeWallClockRate gives the
  *   wall-clock rate in kHz), hence the clock the MFMA loop ran at.
  *   sink (device, `groups` floats) receives a checksum per workgroup.
+ * logra_peak_mfma_bf16_data: the same loop (and the same cycles_out and sink)
+ *   with operands that change from one MFMA to the next: ops (device,
+ *   16-byte aligned, 1 MiB = 65,536 fragments of eight bf16 values, filled by
+ *   the caller, e.g. with random normal values) gives each lane 16 fragments,
+ *   taken as a register-tiled GEMM takes them: one A fragment for four MFMAs
+ *   in a row, a different B fragment for each.  The multiplier switching, and
+ *   so the power drawn, is then that of a GEMM on real data rather than of
+ *   one constant operand pair.  iters must be a multiple of 8.
  * logra_peak_hbm_read: streams `bytes` (a multiple of 1,024; buf 1,024-byte
  *   aligned) from device memory on `groups` workgroups of 256 threads, in one
  *   of three ways: mode 0, grid-stride 128-bit loads, four in flight per
@@ -24,7 +32,7 @@
  *   flight (the way the projection streams).  sink (device, `groups` floats)
  *   receives a checksum.
  *
- * Both are asynchronous on `stream` and return a logra status code
+ * All three are asynchronous on `stream` and return a logra status code
  * (0 = OK, -1 = invalid argument, -3 = HIP error).
  */
 #ifndef LOGRA_PEAKS_H
@@ -38,6 +46,8 @@ extern "C" {
 #endif
 
 int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int64_t *cycles_out, void *stream);
+int logra_peak_mfma_bf16_data(int groups, int64_t iters, const void *ops, float *sink, int64_t *cycles_out,
+                              void *stream);
 int logra_peak_hbm_read(const void *buf, size_t bytes, int groups, int mode, float *sink, void *stream);
 /* The constant rate of the wall clock read by logra_peak_mfma_bf16, in kHz, of the current device. */
 int logra_peak_wall_clock_khz(int *khz);

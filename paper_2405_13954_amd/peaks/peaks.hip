@@ -42,6 +42,45 @@ __global__ __launch_bounds__(256) void k_peak_mfma(int64_t iters, float *sink, i
     }
 }
 
+// The same loop on data: each lane holds 16 operand fragments read from
+// `ops` (random bf16 values), and the MFMAs take them in the pattern of a
+// register-tiled GEMM: one A fragment for four MFMAs in a row (one per
+// accumulator), a different B fragment for each.  The multiplier inputs then
+// change from one MFMA to the next as they do in a GEMM on real data.  (The
+// loop above feeds every MFMA the same two fragments of short-mantissa
+// values, which toggles far fewer bits.)
+__global__ __launch_bounds__(256) void k_peak_mfma_data(const u32x4 *ops, int64_t iters, float *sink,
+                                                        int64_t *cycles) {
+    const int tid = threadIdx.x;
+    const u32x4 *src = ops + static_cast<size_t>(blockIdx.x & 15) * (16 * 256) + tid;
+    bf16x8 f[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) f[r] = __builtin_bit_cast(bf16x8, src[r * 256]);
+    f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+    const long long t0 = clock64(), w0 = wall_clock64();
+    for (int64_t i = 0; i < iters; i += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[u], f[8 + u], c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[u], f[8 + ((u + 1) & 7)], c1, 0, 0, 0);
+            c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[u], f[8 + ((u + 2) & 7)], c2, 0, 0, 0);
+            c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f[u], f[8 + ((u + 3) & 7)], c3, 0, 0, 0);
+        }
+    }
+    const long long t1 = clock64(), w1 = wall_clock64();
+    float s = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += c0[r] + c1[r] + c2[r] + c3[r];
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if (tid == 0) {
+        sink[blockIdx.x] = s;
+        if (cycles && blockIdx.x == 0) {
+            cycles[0] = t1 - t0;
+            cycles[1] = w1 - w0;
+        }
+    }
+}
+
 // Mode 0: grid-stride 128-bit loads, four in flight per thread.
 __global__ __launch_bounds__(256) void k_peak_read(const u32x4 *buf, int64_t n, float *sink) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
@@ -119,6 +158,16 @@ extern "C" int logra_peak_mfma_bf16(int groups, int64_t iters, float *sink, int6
     if (groups <= 0 || iters <= 0 || sink == nullptr) return -1;
     hipLaunchKernelGGL(k_peak_mfma, dim3(groups), dim3(256), 0, static_cast<hipStream_t>(stream), iters, sink,
                        cycles_out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int logra_peak_mfma_bf16_data(int groups, int64_t iters, const void *ops, float *sink,
+                                         int64_t *cycles_out, void *stream) {
+    if (groups <= 0 || iters <= 0 || iters % 8 != 0 || ops == nullptr || sink == nullptr ||
+        (reinterpret_cast<uintptr_t>(ops) & 15) != 0)
+        return -1;
+    hipLaunchKernelGGL(k_peak_mfma_data, dim3(groups), dim3(256), 0, static_cast<hipStream_t>(stream),
+                       static_cast<const u32x4 *>(ops), iters, sink, cycles_out);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -256,7 +256,8 @@ def test_peaks_library_exports_and_validation():
     src = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "logra_peaks.h")).read(), flags=re.S)
     syms = sorted(set(re.findall(r"\b(logra_[a-z_0-9]+)\s*\(", src)))
     K = ctypes.CDLL(path)
-    assert syms == ["logra_peak_hbm_read", "logra_peak_mfma_bf16", "logra_peak_wall_clock_khz"]
+    assert syms == ["logra_peak_hbm_read", "logra_peak_mfma_bf16", "logra_peak_mfma_bf16_data",
+                    "logra_peak_wall_clock_khz"]
     for s in syms:
         assert hasattr(K, s)
     K.logra_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
@@ -266,6 +267,13 @@ def test_peaks_library_exports_and_validation():
     fake = ctypes.c_void_p(0x1000)
     assert K.logra_peak_mfma_bf16(0, 10, fake, None, None) == -1
     assert K.logra_peak_mfma_bf16(4, 10, None, None, None) == -1
+    K.logra_peak_mfma_bf16_data.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_void_p]
+    ops = ctypes.c_void_p(0x2000)
+    assert K.logra_peak_mfma_bf16_data(4, 12, ops, fake, None, None) == -1             # not a multiple of 8
+    assert K.logra_peak_mfma_bf16_data(4, 16, None, fake, None, None) == -1
+    assert K.logra_peak_mfma_bf16_data(4, 16, ctypes.c_void_p(0x2008), fake, None, None) == -1   # unaligned
+    assert K.logra_peak_mfma_bf16_data(0, 16, ops, fake, None, None) == -1
     big = ctypes.c_void_p(0x100000)
     assert K.logra_peak_hbm_read(big, 1000, 4, 0, fake, None) == -1      # not a multiple of 1 KB
     assert K.logra_peak_hbm_read(None, 1024, 4, 0, fake, None) == -1
