@@ -324,33 +324,70 @@ __device__ __forceinline__ void act_cov_tile(const bf16_bits *__restrict__ a, in
                     }
         }
         __syncthreads();
-        for (int e = tid; e < 128 * (CT / 4); e += 256) {
-            const int row = e / (CT / 4), c4 = 4 * (e % (CT / 4));
-            const int gi = I + h * 128 + row, gj = J + c4;
-            if (gi >= n) continue;
-            float *p = C + static_cast<size_t>(gi) * n + gj;
-            float *st = ct + row * kCRow + c4;
-            if (gj + 3 < n && (!DIAG || gi <= gj)) {
-                const f32x4 v = *reinterpret_cast<const f32x4 *>(p) + f32x4{st[0], st[1], st[2], st[3]};
-                *reinterpret_cast<f32x4 *>(p) = v;
+        // Read-modify-write in batches of kBatch quads per thread, every load
+        // of a batch issued before its first store: a store to C might alias
+        // a later load, so the compiler would otherwise keep each load behind
+        // the previous store, one memory round trip per quad.
+        constexpr int kQuads = 128 * (CT / 4) / 256, kBatch = 16;
 #pragma unroll
-                for (int u = 0; u < 4; ++u) st[u] = v[u];
-            } else {
+        for (int b0 = 0; b0 < kQuads; b0 += kBatch) {
+            f32x4 old[kBatch];
 #pragma unroll
-                for (int u = 0; u < 4; ++u)
-                    if (gj + u < n && (!DIAG || gi <= gj + u)) {
-                        const float v = p[u] + st[u];
-                        p[u] = v;
-                        st[u] = v;
-                    }
+            for (int u = 0; u < kBatch; ++u) {
+                const int e = tid + 256 * (b0 + u);
+                const int row = e / (CT / 4), c4 = 4 * (e % (CT / 4));
+                const int gi = I + h * 128 + row, gj = J + c4;
+                const float *p = C + static_cast<size_t>(gi) * n + gj;
+                old[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+                if (gi >= n) continue;
+                if (gj + 3 < n && (!DIAG || gi <= gj)) {
+                    old[u] = *reinterpret_cast<const f32x4 *>(p);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (gj + k < n && (!DIAG || gi <= gj + k)) old[u][k] = p[k];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int e = tid + 256 * (b0 + u);
+                const int row = e / (CT / 4), c4 = 4 * (e % (CT / 4));
+                const int gi = I + h * 128 + row, gj = J + c4;
+                if (gi >= n) continue;
+                float *p = C + static_cast<size_t>(gi) * n + gj;
+                float *st = ct + row * kCRow + c4;
+                if (gj + 3 < n && (!DIAG || gi <= gj)) {
+                    const f32x4 v = old[u] + f32x4{st[0], st[1], st[2], st[3]};
+                    *reinterpret_cast<f32x4 *>(p) = v;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) st[k] = v[k];
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        if (gj + k < n && (!DIAG || gi <= gj + k)) {
+                            const float v = old[u][k] + st[k];
+                            p[k] = v;
+                            st[k] = v;
+                        }
+                }
             }
         }
         __syncthreads();
-        for (int e = tid; e < 128 * CT; e += 256) {
-            const int col = e >> 7, row = e & 127;   // consecutive threads: consecutive rows
-            const int gi = I + h * 128 + row, gj = J + col;
-            if (gi < n && gj < n && (DIAG ? gi < gj : true))
-                C[static_cast<size_t>(gj) * n + gi] = ct[row * kCRow + col];
+        // The mirror: four consecutive rows of one column per thread, one
+        // 16-byte store where all four belong below the diagonal and in range.
+        for (int e = tid; e < 32 * CT; e += 256) {
+            const int col = e >> 5, q = e & 31;   // consecutive threads: consecutive row quads
+            const int gi = I + h * 128 + 4 * q, gj = J + col;
+            if (gj >= n) continue;
+            const float *sv = ct + 4 * q * kCRow + col;
+            float *dst = C + static_cast<size_t>(gj) * n + gi;
+            if (gi + 3 < n && (!DIAG || gi + 3 < gj)) {
+                *reinterpret_cast<f32x4 *>(dst) = f32x4{sv[0], sv[kCRow], sv[2 * kCRow], sv[3 * kCRow]};
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (gi + k < n && (!DIAG || gi + k < gj)) dst[k] = sv[k * kCRow];
+            }
         }
         __syncthreads();
     }
