@@ -474,7 +474,9 @@ def pca_sub_leg(args, torch, P, blk, lens, mask, k):
     (n = 4096) and output gradient dy (n = 14,336), timed over back-to-back
     calls with HIP events; then the top-k eigenvectors of each factor (30 subspace
     iterations).  Algorithmic flops of a SYRK call: valid tokens x n (n + 1)
-    (the upper triangle of the symmetric product)."""
+    (the upper triangle of the symmetric product).  Then all eleven KFAC
+    factors of the block in one grouped launch (block_group), beside the same
+    factors as eleven calls."""
     x, dy = blk[4]                      # gate: 4096 -> 14336
     tokens = int(lens.sum())
     out = {"layer": "gate (x: 4096, dy: 14336)", "valid_tokens": tokens, "k": k, "iters": 30}
@@ -506,6 +508,35 @@ def pca_sub_leg(args, torch, P, blk, lens, mask, k):
                                   "traffic_over_algorithmic": ratio,
                                   "kernel": "k_act_cov_dma (masked bf16 SYRK)"}}
         del C, ws, Pk, pws
+    # every KFAC factor of the block in one grouped launch: C_F of the four
+    # distinct inputs (q/k/v share one, gate/up share one; here the q, o,
+    # gate and down inputs) and C_B of the seven layers
+    facts = [blk[0][0], blk[3][0], blk[4][0], blk[6][0]] + [dy_ for _, dy_ in blk]
+    Cs = [torch.zeros((a.shape[2], a.shape[2]), dtype=torch.float32, device="cuda") for a in facts]
+    ws = torch.empty(P.logra_act_cov_ws_size(facts[0].shape[0], facts[0].shape[1]), dtype=torch.uint8,
+                     device="cuda")
+    pairs = list(zip(facts, Cs))
+    tg, tsep = EventTimer(torch), EventTimer(torch)
+    P.logra_act_cov_accumulate_group(pairs, mask=mask, ws=ws)
+    e0 = tg.start()
+    for _ in range(args.pca_reps):
+        P.logra_act_cov_accumulate_group(pairs, mask=mask, ws=ws)
+    tg.stop(e0, args.pca_reps)
+    e0 = tsep.start()
+    for _ in range(args.pca_reps):
+        for a, C in pairs:
+            P.logra_act_cov_accumulate(a, C, mask=mask, ws=ws)
+    tsep.stop(e0, args.pca_reps)
+    torch.cuda.synchronize()
+    flops = float(tokens) * sum(a.shape[2] * (a.shape[2] + 1) for a in facts)
+    tf = flops / (tg.mean_ms() * 1e-3) / 1e12
+    out["block_group"] = {
+        "factors": [("C_F " if i < 4 else "C_B ") + str(a.shape[2]) for i, a in enumerate(facts)],
+        "group_ms": tg.mean_ms(), "separate_calls_ms": tsep.mean_ms(),
+        "roofline": {"bound": "mfma", "achieved": tf, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tf / BF16_PEAK_TFLOPS, "flops_per_launch": flops, "traffic": None,
+                     "kernel": "k_act_cov_dma over the 11 KFAC factors of one Llama3-8B block (one launch)"}}
+    del Cs, ws, pairs
     return out
 
 
@@ -1238,7 +1269,9 @@ def main():
         for r in [out.get("roofline"), out.get("influence", {}).get("roofline"),
                   out.get("influence", {}).get("relatif", {}).get("roofline"),
                   out.get("llama3_8b_block", {}).get("roofline"), out.get("llama3_8b_block", {}).get("cov_roofline"),
-                  out.get("gpt2_small_log", {}).get("roofline")]:
+                  out.get("gpt2_small_log", {}).get("roofline"),
+                  out.get("pca", {}).get("C_F", {}).get("roofline"), out.get("pca", {}).get("C_B", {}).get("roofline"),
+                  out.get("pca", {}).get("block_group", {}).get("roofline")]:
             if r:
                 ceil = peaks["hbm_read_gbs"] if r["bound"] == "hbm" else peaks["mfma_bf16_tflops"]
                 r["frac_of_measured_peak"] = r["achieved"] / ceil

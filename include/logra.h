@@ -425,7 +425,26 @@ int logra_offload_rows_file(const void *src, int64_t ld_src, int64_t rows, int64
  *   ws     workspace of logra_act_cov_ws_size(B, T) bytes (the list of
  *          non-empty 32-token slabs).  B = 0 or T = 0 is a no-op.
  * ---------------------------------------------------------------------- */
+/* logra_act_cov_accumulate_group: the same for up to LOGRA_MAX_ACT_COV_GROUP
+ *   factors of one batch in one launch, e.g. every KFAC factor of a
+ *   transformer block (C_F of each distinct input, C_B of each layer).  The
+ *   factors share B, T, the mask and a_dtype; each has its own activations a
+ *   [B][T][n], n (same rule as above) and C [n][n].  No two C may overlap
+ *   (LOGRA_ERR_INVALID_ARG); the same a may appear in several.  One tile pool
+ *   over all factors, so a small factor no longer leaves most CUs idle.  Each
+ *   C is identical to what logra_act_cov_accumulate gives it.  Workspace:
+ *   logra_act_cov_ws_size(B, T), as for one factor.  n_desc above the maximum
+ *   is LOGRA_ERR_UNSUPPORTED. */
+#define LOGRA_MAX_ACT_COV_GROUP 32
+typedef struct {
+    const void *a;
+    float *C;
+    int n;
+} logra_act_cov_desc;
+
 size_t logra_act_cov_ws_size(int B, int T);
+int logra_act_cov_accumulate_group(const logra_act_cov_desc *factors, int n_desc, int a_dtype, int B, int T,
+                                   const uint8_t *mask, void *ws, size_t ws_bytes, void *stream);
 int logra_act_cov_accumulate(const void *a, int a_dtype, int B, int T, int n, const uint8_t *mask, float *C,
                              void *ws, size_t ws_bytes, void *stream);
 

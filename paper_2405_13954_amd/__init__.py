@@ -30,6 +30,7 @@ LIB_PATH = os.path.join(_HERE, "libpaper_logra.so")
 F32, BF16, F64 = 0, 1, 2
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_NOT_PD, ERR_WORKSPACE, ERR_IO = 0, -1, -2, -3, -4, -5, -6
 MAX_GROUP = 48
+MAX_ACT_COV_GROUP = 32
 
 EXPORTED = (
     "logra_last_error", "logra_version",
@@ -40,7 +41,8 @@ EXPORTED = (
     "logra_precondition_ws_size", "logra_precondition", "logra_precondition_blocks", "logra_precondition_f64",
     "logra_influence_ws_size", "logra_influence_scores", "logra_influence_scores_scaled",
     "logra_self_influence_ws_size", "logra_self_influence_blocks",
-    "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_pca_ws_size", "logra_pca_topk",
+    "logra_act_cov_ws_size", "logra_act_cov_accumulate", "logra_act_cov_accumulate_group",
+    "logra_pca_ws_size", "logra_pca_topk",
     "logra_influence_stream_ws_size", "logra_influence_stream", "logra_offload_rows",
     "logra_store_read_rows", "logra_store_write_rows", "logra_influence_stream_file_ws_size",
     "logra_influence_stream_file", "logra_offload_rows_file",
@@ -57,6 +59,11 @@ class LayerDesc(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("dy", ctypes.c_void_p), ("p_in", ctypes.c_void_p),
                 ("p_out", ctypes.c_void_p), ("g_out", ctypes.c_void_p),
                 ("n_in", ctypes.c_int), ("n_out", ctypes.c_int)]
+
+
+class ActCovDesc(ctypes.Structure):
+    """logra_act_cov_desc: one KFAC factor of a grouped SYRK launch."""
+    _fields_ = [("a", ctypes.c_void_p), ("C", ctypes.c_void_p), ("n", ctypes.c_int)]
 
 
 _lib = None
@@ -105,6 +112,8 @@ def lib():
         L.logra_act_cov_ws_size.argtypes = [i32, i32]
         L.logra_act_cov_ws_size.restype = sz
         L.logra_act_cov_accumulate.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.logra_act_cov_accumulate_group.argtypes = [ctypes.POINTER(ActCovDesc), i32, i32, i32, i32, vp, vp, sz,
+                                                     vp]
         L.logra_pca_ws_size.argtypes = [i32, i32]
         L.logra_pca_ws_size.restype = sz
         L.logra_pca_topk.argtypes = [vp, i32, i32, i32, vp, i32, i64, vp, vp, sz, vp]
@@ -121,7 +130,7 @@ def lib():
                                                   sz, vp, sz, vp, vp]
         L.logra_offload_rows_file.argtypes = [vp, i64, i64, i64, i32, i64, vp, sz, vp, vp, vp, vp]
         for name in ("logra_store_read_rows", "logra_store_write_rows", "logra_influence_stream_file",
-                     "logra_offload_rows_file", "logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_project_layer", "logra_project_layers", "logra_project_layers_noalloc", "logra_cov_accumulate",
+                     "logra_offload_rows_file", "logra_offload_rows", "logra_influence_stream", "logra_pca_topk", "logra_act_cov_accumulate", "logra_act_cov_accumulate_group", "logra_project_layer", "logra_project_layers", "logra_project_layers_noalloc", "logra_cov_accumulate",
                      "logra_cov_accumulate_blocks", "logra_cov_accumulate_blocks_lower", "logra_precondition",
                      "logra_precondition_blocks",
                      "logra_cov_accumulate_f64", "logra_precondition_f64",
@@ -396,6 +405,24 @@ def logra_act_cov_accumulate(a, C, mask=None, ws=None, stream=None):
     ws, wsb = _workspace(logra_act_cov_ws_size(B, T), C.device, ws)
     _check(lib().logra_act_cov_accumulate(_ptr(a), _dtype_code(a), B, T, n, _ptr(mask), _ptr(C), _ptr(ws), wsb,
                                           _stream(stream)))
+
+
+def logra_act_cov_accumulate_group(factors, mask=None, ws=None, stream=None):
+    """Several KFAC factors of one batch in one launch: factors is a list of
+    (a [B, T, n_i], C [n_i, n_i] fp32) pairs sharing B, T, the dtype and the
+    mask; each C += sum over unmasked tokens of a_t a_t^T, as
+    logra_act_cov_accumulate would give it."""
+    assert len(factors) > 0, "no factors"
+    B, T, _ = factors[0][0].shape
+    arr = (ActCovDesc * len(factors))()
+    for i, (a, C) in enumerate(factors):
+        assert a.shape[:2] == (B, T) and a.dtype == factors[0][0].dtype, "factors must share B, T and the dtype"
+        if B > 0 and T > 0:
+            assert a.is_contiguous(), "a must be contiguous [B, T, n]"
+        arr[i] = ActCovDesc(_ptr(a), _ptr(C), a.shape[2])
+    ws, wsb = _workspace(logra_act_cov_ws_size(B, T), factors[0][1].device, ws)
+    _check(lib().logra_act_cov_accumulate_group(arr, len(factors), _dtype_code(factors[0][0]), B, T, _ptr(mask),
+                                                _ptr(ws), wsb, _stream(stream)))
 
 
 def logra_pca_ws_size(n, k) -> int:

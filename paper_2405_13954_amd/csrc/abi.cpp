@@ -660,6 +660,51 @@ int logra_act_cov_accumulate(const void *a, int a_dtype, int B, int T, int n, co
     return ok();
 }
 
+int logra_act_cov_accumulate_group(const logra_act_cov_desc *factors, int n_desc, int a_dtype, int B, int T,
+                                   const uint8_t *mask, void *ws, size_t ws_bytes, void *stream) {
+    static_assert(LOGRA_MAX_ACT_COV_GROUP == logra::kMaxActCovGroup, "one group limit");
+    if (factors == nullptr) return fail(LOGRA_ERR_INVALID_ARG, "factors is NULL");
+    if (n_desc < 1 || n_desc > LOGRA_MAX_ACT_COV_GROUP)
+        return fail(n_desc > LOGRA_MAX_ACT_COV_GROUP ? LOGRA_ERR_UNSUPPORTED : LOGRA_ERR_INVALID_ARG,
+                    "n_desc must be in 1..%d", LOGRA_MAX_ACT_COV_GROUP);
+    if (!valid_dtype(a_dtype)) return fail(LOGRA_ERR_INVALID_ARG, "bad dtype");
+    if (B < 0 || T < 0) return fail(LOGRA_ERR_INVALID_ARG, "need B >= 0, T >= 0");
+    const bool bf16 = a_dtype == LOGRA_BF16;
+    for (int f = 0; f < n_desc; ++f) {
+        const int n = factors[f].n;
+        if (n <= 0) return fail(LOGRA_ERR_INVALID_ARG, "factor %d: need n > 0", f);
+        if (bf16 && n % 8) return fail(LOGRA_ERR_INVALID_ARG, "factor %d: bf16 activations need n a multiple of 8", f);
+        if (n > (1 << 20)) return fail(LOGRA_ERR_UNSUPPORTED, "factor %d: n must be <= 1048576", f);
+    }
+    if (static_cast<int64_t>(B) * T > INT32_MAX) return fail(LOGRA_ERR_UNSUPPORTED, "B * T must be < 2^31");
+    if (B == 0 || T == 0) return ok();
+    const void *a[LOGRA_MAX_ACT_COV_GROUP];
+    float *C[LOGRA_MAX_ACT_COV_GROUP];
+    int n[LOGRA_MAX_ACT_COV_GROUP];
+    for (int f = 0; f < n_desc; ++f) {
+        a[f] = factors[f].a;
+        C[f] = factors[f].C;
+        n[f] = factors[f].n;
+    }
+    // tiles of different factors run at the same time: two C that share bytes would race
+    for (int f = 0; f < n_desc; ++f)
+        for (int h = 0; h < f; ++h) {
+            const uintptr_t f0 = reinterpret_cast<uintptr_t>(C[f]), h0 = reinterpret_cast<uintptr_t>(C[h]);
+            const uintptr_t f1 = f0 + static_cast<uintptr_t>(n[f]) * n[f] * sizeof(float);
+            const uintptr_t h1 = h0 + static_cast<uintptr_t>(n[h]) * n[h] * sizeof(float);
+            if (f0 < h1 && h0 < f1) return fail(LOGRA_ERR_INVALID_ARG, "C of factors %d and %d overlap", h, f);
+        }
+    for (int f = 0; f < n_desc; ++f) {
+        TRY(check_dev(a[f], "a", bf16 ? 16 : 4));
+        TRY(check_dev(C[f], "C", 4));
+    }
+    if (mask) TRY(check_dev(mask, "mask", 1));
+    TRY(check_ws(ws, ws_bytes, logra_act_cov_ws_size(B, T)));
+    hipError_t e = logra::launch_act_cov_group(a, C, n, n_desc, bf16, B, T, mask, ws, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "activation covariance launch");
+    return ok();
+}
+
 size_t logra_pca_ws_size(int n, int k) {
     if (n <= 0 || k <= 0 || k > n || k > LOGRA_MAX_PCA_K) return 0;
     return round256(logra::pca_ws_bytes(n, k));

@@ -94,6 +94,13 @@ hipError_t launch_self_influence(const void *g, bool bf16, int64_t ld, int64_t r
 size_t act_cov_ws_bytes(int B, int T);
 hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const uint8_t *mask, float *C, void *ws,
                           hipStream_t s);
+// The same for `count` (<= kMaxActCovGroup) factors of one batch in one launch:
+// a[i] [B][T][n[i]] into C[i] [n[i]][n[i]]; the factors share B, T, the mask
+// and the dtype, and their C must not overlap.  Each factor's result is
+// identical to launch_act_cov's.
+constexpr int kMaxActCovGroup = 32;
+hipError_t launch_act_cov_group(const void *const *a, float *const *C, const int *n, int count, bool bf16, int B,
+                                int T, const uint8_t *mask, void *ws, hipStream_t s);
 
 // Top-k eigenvectors of a symmetric PSD fp32 C [n][n] (k <= 64) as the rows
 // of P [k][ld_p], by subspace iteration with Rayleigh-Ritz extraction.

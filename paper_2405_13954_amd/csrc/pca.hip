@@ -54,6 +54,9 @@
 //     sign rule, and the rows of P in the output dtype.
 //
 // Every sum has a fixed order, so results are bitwise reproducible.
+#include <algorithm>
+#include <cstdint>
+
 #include "common.h"
 #include "internal.h"
 
@@ -393,19 +396,35 @@ __device__ __forceinline__ void act_cov_tile(const bf16_bits *__restrict__ a, in
     }
 }
 
-__global__ __launch_bounds__(256, 1) void k_act_cov_dma(const bf16_bits *__restrict__ a, int T, int n, int spe,
+// The factors of one launch: factor f owns the workgroup slots
+// [slot_end[f - 1], slot_end[f]) (tile_slots of its tile count, a multiple of
+// 256, so a slot's XCD is the same as in a launch of its own).
+struct ActCovFactor {
+    const bf16_bits *a;
+    float *C;
+    int n, nt, slot_end;
+};
+struct ActCovArgs {
+    ActCovFactor f[kMaxActCovGroup];
+    int count;
+};
+
+__global__ __launch_bounds__(256, 1) void k_act_cov_dma(ActCovArgs g, int T, int spe,
                                                         const int *__restrict__ slabs,
                                                         const uint32_t *__restrict__ bits,
-                                                        const int *__restrict__ n_slabs, int nt,
-                                                        float *__restrict__ C) {
+                                                        const int *__restrict__ n_slabs) {
     __shared__ __attribute__((aligned(1024))) uint8_t smem[kCLds];
+    const int bid = blockIdx.x;
+    int f = 0;
+    while (f + 1 < g.count && bid >= g.f[f].slot_end) ++f;
+    const ActCovFactor &F = g.f[f];
     int ti, tj;
-    if (!tile_of(blockIdx.x, nt, ti, tj)) return;
+    if (!tile_of(bid - (f > 0 ? g.f[f - 1].slot_end : 0), F.nt, ti, tj)) return;
     const int ns = __builtin_amdgcn_readfirstlane(*n_slabs);
     if (ti == tj)
-        act_cov_tile<true>(a, T, n, spe, slabs, bits, ns, ti * CT, tj * CT, C, smem);
+        act_cov_tile<true>(F.a, T, F.n, spe, slabs, bits, ns, ti * CT, tj * CT, F.C, smem);
     else
-        act_cov_tile<false>(a, T, n, spe, slabs, bits, ns, ti * CT, tj * CT, C, smem);
+        act_cov_tile<false>(F.a, T, F.n, spe, slabs, bits, ns, ti * CT, tj * CT, F.C, smem);
 }
 
 // fp32 activations: one thread per upper entry (i <= j) of a 16 x 16 block,
@@ -1132,26 +1151,47 @@ size_t act_cov_ws_bytes(int B, int T) {
     return align256(sizeof(int) * slabs) + align256(sizeof(uint32_t) * slabs) + 256;
 }
 
-hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const uint8_t *mask, float *C, void *ws,
-                          hipStream_t s) {
-    if (B == 0 || T == 0) return hipSuccess;
+hipError_t launch_act_cov_group(const void *const *a, float *const *C, const int *n, int count, bool bf16, int B,
+                                int T, const uint8_t *mask, void *ws, hipStream_t s) {
+    if (B == 0 || T == 0 || count == 0) return hipSuccess;
+    if (count < 0 || count > kMaxActCovGroup) return hipErrorInvalidValue;
     const int spe = (T + ST - 1) / ST;
     const size_t slabs = static_cast<size_t>(B) * spe;
     char *w = static_cast<char *>(ws);
     int *list = reinterpret_cast<int *>(w);
     uint32_t *bits = reinterpret_cast<uint32_t *>(w + align256(sizeof(int) * slabs));
-    int *count = reinterpret_cast<int *>(w + align256(sizeof(int) * slabs) + align256(sizeof(uint32_t) * slabs));
-    hipLaunchKernelGGL(k_slab_prep, dim3(1), dim3(1024), 0, s, mask, B, T, spe, list, bits, count);
+    int *n_slabs = reinterpret_cast<int *>(w + align256(sizeof(int) * slabs) + align256(sizeof(uint32_t) * slabs));
+    hipLaunchKernelGGL(k_slab_prep, dim3(1), dim3(1024), 0, s, mask, B, T, spe, list, bits, n_slabs);
     if (bf16) {
-        const int nt = (n + CT - 1) / CT;
-        hipLaunchKernelGGL(k_act_cov_dma, dim3(static_cast<unsigned>(tile_slots(nt))), dim3(256), 0, s,
-                           static_cast<const bf16_bits *>(a), T, n, spe, list, bits, count, nt, C);
+        // the largest factors first, so that the small ones fill the last rounds
+        int order[kMaxActCovGroup];
+        for (int i = 0; i < count; ++i) order[i] = i;
+        std::stable_sort(order, order + count, [&](int x, int y) { return n[x] > n[y]; });
+        ActCovArgs g;
+        g.count = count;
+        int64_t slots = 0;
+        for (int i = 0; i < count; ++i) {
+            const int f = order[i];
+            const int nt = (n[f] + CT - 1) / CT;
+            slots += tile_slots(nt);
+            if (slots > INT32_MAX) return hipErrorInvalidValue;
+            g.f[i] = {static_cast<const bf16_bits *>(a[f]), C[f], n[f], nt, static_cast<int>(slots)};
+        }
+        hipLaunchKernelGGL(k_act_cov_dma, dim3(static_cast<unsigned>(slots)), dim3(256), 0, s, g, T, spe, list,
+                           bits, n_slabs);
     } else {
-        const unsigned nb = static_cast<unsigned>((n + 15) / 16);
-        hipLaunchKernelGGL(k_act_cov_f32, dim3(nb, nb), dim3(256), 0, s, static_cast<const float *>(a), T, n, spe,
-                           list, bits, count, C);
+        for (int f = 0; f < count; ++f) {
+            const unsigned nb = static_cast<unsigned>((n[f] + 15) / 16);
+            hipLaunchKernelGGL(k_act_cov_f32, dim3(nb, nb), dim3(256), 0, s, static_cast<const float *>(a[f]), T,
+                               n[f], spe, list, bits, n_slabs, C[f]);
+        }
     }
     return hipGetLastError();
+}
+
+hipError_t launch_act_cov(const void *a, bool bf16, int B, int T, int n, const uint8_t *mask, float *C, void *ws,
+                          hipStream_t s) {
+    return launch_act_cov_group(&a, &C, &n, 1, bf16, B, T, mask, ws, s);
 }
 
 }  // namespace logra

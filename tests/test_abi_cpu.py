@@ -174,6 +174,31 @@ def test_pca_entry_points_validation(L):
     assert f(None, 1, 2, 4, 60, None, fake, None, 0, None) == P.ERR_INVALID_ARG     # bf16 n % 8
     assert f(None, 1, -1, 4, 64, None, fake, None, 0, None) == P.ERR_INVALID_ARG
     assert f(None, 1, 0, 4, 64, None, fake, None, 0, None) == P.OK                  # no tokens: a no-op
+    # the grouped form: descriptor limits, per-factor sizes, overlapping outputs
+    grp = L.logra_act_cov_accumulate_group
+    D = P.ActCovDesc
+    two = (D * 2)(D(0x1000, 0x100000, 64), D(0x1000, 0x200000, 64))
+    assert grp(None, 1, 1, 2, 4, None, None, 0, None) == P.ERR_INVALID_ARG          # no descriptors
+    assert grp(two, 0, 1, 2, 4, None, None, 0, None) == P.ERR_INVALID_ARG
+    many = (D * (P.MAX_ACT_COV_GROUP + 1))()
+    assert grp(many, P.MAX_ACT_COV_GROUP + 1, 1, 2, 4, None, None, 0, None) == P.ERR_UNSUPPORTED
+    assert grp(two, 2, 5, 2, 4, None, None, 0, None) == P.ERR_INVALID_ARG           # dtype
+    bad = (D * 2)(D(0x1000, 0x100000, 64), D(0x1000, 0x200000, 60))
+    assert grp(bad, 2, 1, 2, 4, None, None, 0, None) == P.ERR_INVALID_ARG           # bf16 n % 8
+    assert "factor 1" in P.logra_last_error()
+    grp(bad, 2, 0, 2, 4, None, None, 0, None)                                          # fp32: any n
+    assert "multiple of 8" not in P.logra_last_error()
+    big = (D * 1)(D(0x1000, 0x100000, (1 << 20) + 8))
+    assert grp(big, 1, 1, 2, 4, None, None, 0, None) == P.ERR_UNSUPPORTED
+    assert grp(two, 2, 1, 0, 4, None, None, 0, None) == P.OK                          # no tokens: a no-op
+    # C of factor 1 starts inside factor 0's 64 x 64 floats (16 KB): rejected before any launch
+    clash = (D * 2)(D(0x1000, 0x100000, 64), D(0x1000, 0x100000 + 16380, 64))
+    assert grp(clash, 2, 1, 2, 4, None, None, 0, None) == P.ERR_INVALID_ARG
+    assert "overlap" in P.logra_last_error()
+    # back to back is not an overlap (the call then fails on the pointers, which are not device memory)
+    touch = (D * 2)(D(0x1000, 0x100000, 64), D(0x1000, 0x100000 + 16384, 64))
+    assert grp(touch, 2, 1, 2, 4, None, None, 0, None) == P.ERR_INVALID_ARG
+    assert "overlap" not in P.logra_last_error()
     # PCA: k limits, iterations, output stride
     assert P.logra_pca_ws_size(100, 65) == 0 and P.logra_pca_ws_size(10, 11) == 0
     assert P.logra_pca_ws_size(4096, 16) > 2 * 4096 * 32 * 4

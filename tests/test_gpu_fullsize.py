@@ -430,6 +430,43 @@ def test_act_cov_gate_bench_launch():
         del a, C
 
 
+def test_act_cov_block_group_bench_launch():
+    """Every KFAC factor of one Llama3-8B block over one logging batch (B=8,
+    T=2048, lengths U{128..2048}) in one grouped launch, as bench.py times it:
+    C_F of the four distinct inputs (q/k/v share one, gate/up share one) and
+    C_B of the seven layers.  Each of the eleven C equals what a call of its
+    own gives, bit for bit; sampled entries of C_B(k) against the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, normwise, say
+    w = W.WORKLOADS["llama3_8b_stream"]
+    B, T = w.B, w.T
+    lens = W.lengths(W.rng(0, 200, 0), B, w.len_lo, w.len_hi)
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = torch.from_numpy(mask_np).cuda()
+    gen = W.torch_generator(0, 452)
+    widths = [4096, 4096, 4096, 14336] + [no for _, _, no in w.layers]   # C_F inputs, then C_B per layer
+    say(f"[full act cov group] one Llama3-8B block: {len(widths)} factors, n = {widths}")
+    acts = []
+    for i, n in enumerate(widths):
+        a = torch.empty((B, T, n), dtype=torch.bfloat16, device="cuda")
+        W.device_normal_(a, w.x_std if i < 4 else w.dy_std, gen)
+        acts.append(a)
+    Cg = [torch.zeros((n, n), dtype=torch.float32, device="cuda") for n in widths]
+    P.logra_act_cov_accumulate_group(list(zip(acts, Cg)), mask=mask)
+    for i, (a, n) in enumerate(zip(acts, widths)):
+        C = torch.zeros((n, n), dtype=torch.float32, device="cuda")
+        P.logra_act_cov_accumulate(a, C, mask=mask)
+        assert torch.equal(C, Cg[i]), f"factor {i} (n={n})"
+        del C
+    kk = 5   # C_B of the k projection (n = 1024)
+    F = np.sort(W.rng(0, 453).choice(widths[kk], size=48, replace=False))
+    Fd = torch.from_numpy(F).cuda()
+    err = normwise(host(Cg[kk][Fd][:, Fd]), oracle.act_cov(host(acts[kk][:, :, Fd].contiguous()), mask_np))
+    say(f"  all {len(widths)} equal their own calls; C_B(k) 48 x 48 sampled entries: normwise err {err:.2e}")
+    assert err <= 1e-5
+
+
 def test_pca_topk_n4096():
     """The top-16 eigenvectors of a 4096 x 4096 covariance (the gate layer's
     C_F size) with a geometric spectrum (neighbour ratio 0.95), 30

@@ -77,6 +77,76 @@ def test_act_cov_integer_exact_accumulates_and_repeats():
     assert np.array_equal(got.view(np.uint32), again.view(np.uint32))
 
 
+def _sym_start(g, n):
+    """A symmetric fp32 starting C (the group accumulates into it)."""
+    m = W.normal(g, (n, n), 1.0, "f32")
+    return ((m + m.T) * 0.5).astype(np.float32)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_act_cov_group_equals_single_calls(dtype):
+    """Several factors of one batch in one grouped launch (different n, one
+    activation tensor feeding two factors, symmetric non-zero starting C): each
+    C equals, bit for bit, what a call of its own gives, and matches the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, normwise, say
+    g = W.rng(62)
+    B, T = 3, 70
+    ns = [264, 8, 640, 520, 264] if dtype == "bf16" else [36, 20, 36]
+    say(f"[act cov group] {dtype}: B={B} T={T} n={ns}")
+    lens = W.lengths(g, B, 0, T)
+    lens[0], lens[-1] = 0, T                      # a fully masked example and a full one
+    mask = W.mask_from_lengths(lens, T)
+    acts = [W.normal(g, (B, T, n), 1.0, dtype) for n in ns[:-1]]
+    acts.append(acts[0])                          # the same activations into a second C
+    for a in acts[:-1]:
+        a[mask == 0] = np.uint16(0x7FC0) if dtype == "bf16" else np.nan   # never read
+    starts = [_sym_start(g, n) for n in ns]
+    ad = [dev(a) for a in acts[:-1]]
+    ad.append(ad[0])
+    md = dev(mask)
+    Cg = [dev(c) for c in starts]
+    P.logra_act_cov_accumulate_group(list(zip(ad, Cg)), mask=md)
+    Cs = [dev(c) for c in starts]
+    for a, C in zip(ad, Cs):
+        P.logra_act_cov_accumulate(a, C, mask=md)
+    torch.cuda.synchronize()
+    for i, n in enumerate(ns):
+        got, single = host(Cg[i]), host(Cs[i])
+        assert np.array_equal(got.view(np.uint32), single.view(np.uint32)), f"factor {i} (n={n})"
+        assert np.array_equal(got, got.T)
+        err = normwise(got.astype(np.float64) - starts[i], oracle.act_cov(acts[i], mask))
+        say(f"  factor {i} (n={n}): equals its own call; normwise err vs oracle {err:.2e}")
+        assert err <= 1e-5
+
+
+def test_act_cov_group_full_table():
+    """A table of LOGRA_MAX_ACT_COV_GROUP factors (n from 8 to 520, some
+    1-tile, some 3-tile): every factor's workgroup slots decode to the right
+    factor; each C equals its own call bit for bit."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, say
+    g = W.rng(63)
+    B, T = 2, 40
+    ns = [8 * (1 + (7 * i) % 65) for i in range(P.MAX_ACT_COV_GROUP)]
+    say(f"[act cov group] {len(ns)} factors, n in {min(ns)}..{max(ns)}")
+    mask = W.mask_from_lengths(W.lengths(g, B, 1, T), T)
+    md = dev(mask)
+    ad = [dev(W.normal(g, (B, T, n), 1.0, "bf16")) for n in ns]
+    Cg = [torch.zeros((n, n), dtype=torch.float32, device="cuda") for n in ns]
+    Cs = [torch.zeros((n, n), dtype=torch.float32, device="cuda") for n in ns]
+    P.logra_act_cov_accumulate_group(list(zip(ad, Cg)), mask=md)
+    for a, C in zip(ad, Cs):
+        P.logra_act_cov_accumulate(a, C, mask=md)
+    torch.cuda.synchronize()
+    for i in range(len(ns)):
+        assert torch.equal(Cg[i], Cs[i]), f"factor {i} (n={ns[i]})"
+    err = np.max(np.abs(host(Cg[-1]).astype(np.float64) - oracle.act_cov(host(ad[-1]), mask)))
+    assert err <= 1e-5 * max(1.0, float(np.max(np.abs(host(Cs[-1])))))
+
+
 def _pca_gpu(C, k, dtype="f32", iters=30):
     import torch
     import paper_2405_13954_amd as P
