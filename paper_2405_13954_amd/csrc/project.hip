@@ -542,8 +542,10 @@ __global__ __launch_bounds__(NT, 1) void k_project_chunks(ProjArgs a) {
 // its band of the next item.  For that the next item must be known when an
 // item starts, so items are claimed two ahead (the first two of a workgroup
 // are blockIdx.x and blockIdx.x + gridDim.x).  A fifth wave does everything
-// besides the streaming: it claims the items and publishes them through LDS,
-// and it folds the four waves' partials, parked in one of two LDS buffers at
+// besides the streaming: it claims the items, decodes each (its layer, tile,
+// operands, valid-token set and partial slot: a chain of dependent loads that
+// took a streaming wave about 1,800 cycles per item) and publishes it through
+// LDS, and it folds the four waves' partials, parked in one of two LDS buffers at
 // each item's end, in the order of k_project_chunks, ((w3 + w2) + w1) + w0,
 // and writes them.  The streaming waves issue no memory operation but their
 // copies, so "at most the two later steps' copies pending" is an exact wait,
@@ -577,24 +579,29 @@ __device__ __forceinline__ StreamItem stream_item(const ProjArgs &a, int item, i
     } else {
         while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
     }
-    const ChunkLayer &L = a.layer[l];
-    const int cs = gslot - L.slot_begin;
+    // the layer table is indexed by integers (no selects or phis of pointers into
+    // the kernel arguments, which would keep them in a private copy)
+    const int cs = gslot - a.layer[l].slot_begin;
     const int bt = a.tiles ? load_uniform(a.tiles + j) : j;
     const int b = bt / a.tpe, tile = bt - b * a.tpe;
-    const bool xside = cs < L.x_items;
-    const int c = xside ? cs : cs - L.x_items;
-    const ChunkLayer &M = xside ? a.layer[L.share[0]] : L;
+    const bool xside = cs < a.layer[l].x_items;
+    const int c = xside ? cs : cs - a.layer[l].x_items;
+    const int m = xside ? a.layer[l].share[0] : l;   // the layer whose partial slots hold the item
     StreamItem it;
     it.valid = tile_valid(a, j, tile);
-    it.n = xside ? L.n_in : L.n_out;
+    it.n = xside ? a.layer[l].n_in : a.layer[l].n_out;
     it.k = xside ? a.k_in : a.k_out;
     const int col0 = c * a.ck;
     it.nk = min(a.ck, it.n - col0);
     const size_t tok0 = static_cast<size_t>(b) * a.T + static_cast<size_t>(tile) * TT;
-    it.A = static_cast<const bf16_bits *>(xside ? L.x : L.dy) + tok0 * it.n + col0;
-    it.P = static_cast<const bf16_bits *>(xside ? M.p_in : L.p_out) + col0;
-    const int pslot = xside ? c : M.c_in + c;
-    it.dst = static_cast<size_t>(M.part_unit) * kPartUnit + (static_cast<size_t>(bt) * (M.c_in + M.c_out) + pslot) * (TT * 16);
+    const void *src = xside ? a.layer[l].x : a.layer[l].dy;
+    const void *proj = xside ? a.layer[m].p_in : a.layer[l].p_out;
+    it.A = static_cast<const bf16_bits *>(src) + tok0 * it.n + col0;
+    it.P = static_cast<const bf16_bits *>(proj) + col0;
+    const int c_in = a.layer[m].c_in, c_out = a.layer[m].c_out;
+    const int pslot = xside ? c : c_in + c;
+    it.dst = static_cast<size_t>(a.layer[m].part_unit) * kPartUnit +
+             (static_cast<size_t>(bt) * (c_in + c_out) + pslot) * (TT * 16);
     return it;
 }
 
@@ -625,6 +632,50 @@ __device__ __forceinline__ void stream_band(StreamBand &d, const StreamItem &it,
         const int r = 8 * q + sub;
         d.po[q] = r < it.k ? (static_cast<uint32_t>(r) * it.n + lcol) * 2u : kBufOOB;
     }
+}
+
+// A decoded item as the writer wave publishes it in LDS: 12 words (A, P,
+// valid, dst as low / high halves, then n, k, nk) at the start of a 64-word
+// slot.  Lane l writes word l, the lanes past 12 write padding, so the store
+// needs no branch on the lane (a divergent branch around the decode would
+// move the kernel arguments it indexes into scratch memory).
+constexpr int kItemWords = 12;
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+// (The slot pointers carry the LDS address space: through generic pointers
+// the accesses might alias private memory, and the kernel arguments would be
+// kept in a private copy.)
+__device__ __forceinline__ void item_to_lds(lds_u32 *slot, const StreamItem &it, int lane) {
+    const uint64_t A = reinterpret_cast<uintptr_t>(it.A), P = reinterpret_cast<uintptr_t>(it.P);
+    const uint64_t dst = static_cast<uint64_t>(it.dst);
+    const uint32_t w[kItemWords] = {static_cast<uint32_t>(A),         static_cast<uint32_t>(A >> 32),
+                                    static_cast<uint32_t>(P),         static_cast<uint32_t>(P >> 32),
+                                    static_cast<uint32_t>(it.valid),  static_cast<uint32_t>(it.valid >> 32),
+                                    static_cast<uint32_t>(dst),       static_cast<uint32_t>(dst >> 32),
+                                    static_cast<uint32_t>(it.n),      static_cast<uint32_t>(it.k),
+                                    static_cast<uint32_t>(it.nk),     0u};
+    uint32_t v = 0;
+#pragma unroll
+    for (int q = 0; q < kItemWords; ++q) v = lane == q ? w[q] : v;
+    slot[lane] = v;
+}
+
+// The read-back: every lane reads the same words, made wave-uniform.
+__device__ __forceinline__ StreamItem item_from_lds(const lds_u32 *slot) {
+    const u32x4 q0 = reinterpret_cast<const lds_u32x4 *>(slot)[0];
+    const u32x4 q1 = reinterpret_cast<const lds_u32x4 *>(slot)[1];
+    const u32x4 q2 = reinterpret_cast<const lds_u32x4 *>(slot)[2];
+    auto u = [](uint32_t v) { return static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v))); };
+    auto u64 = [&](uint32_t lo, uint32_t hi) { return static_cast<uint64_t>(u(lo)) | static_cast<uint64_t>(u(hi)) << 32; };
+    StreamItem it;
+    it.A = reinterpret_cast<const bf16_bits *>(static_cast<uintptr_t>(u64(q0[0], q0[1])));
+    it.P = reinterpret_cast<const bf16_bits *>(static_cast<uintptr_t>(u64(q0[2], q0[3])));
+    it.valid = u64(q1[0], q1[1]);
+    it.dst = static_cast<size_t>(u64(q1[2], q1[3]));
+    it.n = static_cast<int>(u(q2[0]));
+    it.k = static_cast<int>(u(q2[1]));
+    it.nk = static_cast<int>(u(q2[2]));
+    return it;
 }
 
 // The band of no item (past the last): every copy out of range.
@@ -681,6 +732,7 @@ __global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t ring[StreamSh::kRing];
     __shared__ f32x4 fold[2][NW][MB * kWave];
     __shared__ int queue[4];
+    __shared__ __attribute__((aligned(16))) uint32_t decoded[4][kWave];   // the claimed items, decoded (slots of queue)
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) / kWave);
     const int count = a.tiles ? load_uniform(a.n_tiles) : a.B * a.tpe;
@@ -688,31 +740,44 @@ __global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
     const int grid = static_cast<int>(gridDim.x);
     int cur = blockIdx.x, nxt = static_cast<int>(blockIdx.x) + grid;
 
-    if (wave == NW) {   // the writer: claims, publishes, folds and writes
-        auto fold_out = [&](int item, const f32x4 (*w)[MB * kWave]) {
-            f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + stream_item(a, item, count).dst) + lane;
+    if (wave == NW) {   // the writer: claims, decodes, publishes, folds and writes
+        auto fold_out = [&](size_t part, const f32x4 (*w)[MB * kWave]) {
+            f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + part) + lane;
 #pragma unroll
             for (int m = 0; m < MB; ++m) {
                 const int e = m * kWave + lane;
                 dst[m * kWave] = ((w[3][e] + w[2][e]) + w[1][e]) + w[0][e];
             }
         };
-        int prev = -1, n = 0;
+        // partial offsets of the items in flight: prev (folded now), cur, nxt
+        size_t part_prev = 0, part_cur = cur < items ? stream_item(a, cur, count).dst : 0;
+        size_t part_nxt = nxt < items ? stream_item(a, nxt, count).dst : 0;
+        bool have_prev = false;
+        int n = 0;
         for (; cur < items; ++n) {
             int claim = items;   // none
+            size_t part_claim = 0;
             if (nxt < items) {
                 int c = 0;
                 if (lane == 0) c = atomicAdd(a.work, 1);
                 claim = 2 * grid + __builtin_amdgcn_readfirstlane(c);
             }
             if (lane == 0) queue[(n + 2) & 3] = claim;
-            if (prev >= 0) fold_out(prev, fold[(n - 1) & 1]);
+            if (claim < items) {   // the streaming waves take it decoded
+                const StreamItem it = stream_item(a, claim, count);
+                part_claim = it.dst;
+                item_to_lds((lds_u32 *)decoded[(n + 2) & 3], it, lane);
+            }
+            if (have_prev) fold_out(part_prev, fold[(n - 1) & 1]);
             lds_barrier();   // B_n: the partials of item n are parked, item n + 2 is published
-            prev = cur;
+            have_prev = true;
+            part_prev = part_cur;
             cur = nxt;
+            part_cur = part_nxt;
             nxt = claim;
+            part_nxt = part_claim;
         }
-        if (prev >= 0) fold_out(prev, fold[(n - 1) & 1]);
+        if (have_prev) fold_out(part_prev, fold[(n - 1) & 1]);
         return;
     }
 
@@ -731,9 +796,14 @@ __global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
             iss = iss == NS - 1 ? 0 : iss + 1;
         }
     }
+    // item 1 of the workgroup is decoded here; the later ones, claimed, come decoded from the writer
+    if (nxt < items) stream_band(dn, stream_item(a, nxt, count), wave, sub, lcol);
+    else stream_band_none(dn, static_cast<const bf16_bits *>(a.layer[0].x));
     for (int n = 0; cur < items; ++n) {
-        if (nxt < items) stream_band(dn, stream_item(a, nxt, count), wave, sub, lcol);
-        else stream_band_none(dn, static_cast<const bf16_bits *>(a.layer[0].x));
+        if (n > 0) {
+            if (nxt < items) stream_band(dn, item_from_lds((const lds_u32 *)decoded[(n + 1) & 3]), wave, sub, lcol);
+            else stream_band_none(dn, static_cast<const bf16_bits *>(a.layer[0].x));
+        }
         f32x4 acc[MB];
 #pragma unroll
         for (int m = 0; m < MB; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
