@@ -125,7 +125,8 @@ int logra_project_layers(const logra_layer_desc *layers, int n_layers, int in_dt
  * Results are bitwise those of logra_project_layers.  A batch whose
  * logra_project_layers_ws_size exceeds LOGRA_NOALLOC_WS_BYTES returns
  * LOGRA_ERR_UNSUPPORTED (e.g. 7 Llama3-8B layers at k = 16 with B = 8,
- * T = 2048 need 23 MiB; at k = 64 with B = 16, T = 1024 they need 88 MiB).
+ * T = 2048 need 16 MiB, 28 of them 63 MiB; at k = 64 with B = 16, T = 1024
+ * the 7 layers need 84 MiB).
  * Calls that overlap on one GPU (other streams or threads) share the array
  * and race: order them.  Other errors as logra_project_layers. */
 #define LOGRA_NOALLOC_WS_BYTES (64u * 1024u * 1024u)

@@ -38,6 +38,8 @@
 //     added in tile order and G_b is written (fp32 or bf16, round to nearest
 //     even) to the caller's store row.
 // Every sum has a fixed order, so results are bitwise reproducible.
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 
@@ -52,12 +54,14 @@ constexpr int kMaxSlots = 256;            // chunk slots a group can order by wi
 static_assert(kMaxSlots <= 1024 && kMaxGroup <= 64, "an ordered slot packs its slot into 10 bits, its layer into 6");
 constexpr int NT = NW * kWave;            // threads per workgroup
 
-// Contraction columns per work item.  k <= 32: 6,144 (14,336 = 6,144 + 6,144
-// + 2,048), measured best of 2,048..8,192.  k > 32: 14,336 (one item per
-// layer side of a Llama3-8B block), measured best of 2,048..14,336.
-constexpr int kChunkNarrow = 6144;
-constexpr int kChunkWide = 14336;
-__host__ __device__ constexpr int chunk_cols(int KT) { return KT >= 4 ? kChunkWide : kChunkNarrow; }
+// Contraction columns per work item: 14,336, one item per layer side of a
+// Llama3-8B block.  At k > 32 it measured best of 2,048..14,336.  At k <= 16
+// 6,144 was best while every item wrote chunk partials; with one chunk per
+// side the stream kernel pairs a tile's two sides and writes no partials, and
+// 14,336 took the 28-layer Llama3-8B launch from 782 to 721 us (the
+// shared-input one from 722 to 675 us).
+constexpr int kChunkCols = 14336;
+__host__ __device__ constexpr int chunk_cols(int) { return kChunkCols; }
 // Register pipeline depth of the register-staged path.
 __host__ __device__ constexpr int stages_for(int KT) { return KT >= 4 ? 2 : 3; }
 
@@ -116,6 +120,10 @@ struct ProjArgs {
     int n_layers;
     int slots;      // chunk slots of all layers
     int ordered;    // slot_order holds the processing order of the slots
+    int paired;
+    // paired (the stream kernel, every layer side one chunk): item 2 p + s is side
+    // s (0 = x, 1 = dy) of pair p = (layer, listed tile); slot_order holds each
+    // layer's x slot, widest pair first; the writer forms the tile's sum itself
     // processing order: entry = layer << 10 | work slot (over all layers)
     alignas(4) uint16_t slot_order[kMaxSlots];
     const uint8_t *mask;
@@ -532,7 +540,13 @@ __global__ __launch_bounds__(NT, 1) void k_project_chunks(ProjArgs a) {
 // ---------------------------------------------------------------------------
 // k <= 16 (KT = 1), bf16 inputs that no two layers share: the per-wave stream
 // of k_project_chunks, with each wave's ring kept busy from one item to the
-// next.
+// next.  When every layer side is one chunk (always, up to 14,336 columns) the
+// items come in pairs, a tile's x side then its dy side, both in the same
+// workgroup: the writer keeps the folded x' in registers and, after the dy
+// fold, forms the tile's 16 x 16 sum with the MFMAs of k_project_tile_finish<1>
+// (same operands, same order, so the same bits) straight into gpart.  No chunk
+// partial is written and the tile-sum kernel is not launched; the example sums
+// skip the tiles without a valid token, whose sums were never written.
 //
 // In k_project_chunks every item starts with an empty ring and ends with a
 // drained one, so each item pays a memory latency before its first step.  At
@@ -569,12 +583,13 @@ struct StreamItem {
 };
 
 __device__ __forceinline__ StreamItem stream_item(const ProjArgs &a, int item, int count) {
-    const int rank = item / count;
-    const int j = item - rank * count;
+    const int unit = a.paired ? item >> 1 : item;   // a pair or an item
+    const int rank = unit / count;
+    const int j = unit - rank * count;
     int gslot = rank, l = 0;
     if (a.ordered) {
         const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
-        gslot = e & 0x3ff;
+        gslot = (e & 0x3ff) + (a.paired ? item & 1 : 0);
         l = (e >> 10) & 0x3f;
     } else {
         while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
@@ -600,8 +615,10 @@ __device__ __forceinline__ StreamItem stream_item(const ProjArgs &a, int item, i
     it.P = static_cast<const bf16_bits *>(proj) + col0;
     const int c_in = a.layer[m].c_in, c_out = a.layer[m].c_out;
     const int pslot = xside ? c : c_in + c;
-    it.dst = static_cast<size_t>(a.layer[m].part_unit) * kPartUnit +
-             (static_cast<size_t>(bt) * (c_in + c_out) + pslot) * (TT * 16);
+    // paired: the tile's 16 x 16 sum in gpart; else the chunk partial in part
+    it.dst = a.paired ? (static_cast<size_t>(l) * a.B * a.tpe + bt) * 256
+                      : static_cast<size_t>(a.layer[m].part_unit) * kPartUnit +
+                            (static_cast<size_t>(bt) * (c_in + c_out) + pslot) * (TT * 16);
     return it;
 }
 
@@ -738,29 +755,56 @@ __global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
     const int count = a.tiles ? load_uniform(a.n_tiles) : a.B * a.tpe;
     const int items = count * a.slots;
     const int grid = static_cast<int>(gridDim.x);
-    int cur = blockIdx.x, nxt = static_cast<int>(blockIdx.x) + grid;
+    // the first two items: pair blockIdx.x (paired), else items blockIdx.x and blockIdx.x + gridDim.x
+    int cur = a.paired ? 2 * static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.x);
+    int nxt = a.paired ? cur + 1 : cur + grid;
 
     if (wave == NW) {   // the writer: claims, decodes, publishes, folds and writes
-        auto fold_out = [&](size_t part, const f32x4 (*w)[MB * kWave]) {
-            f32x4 *dst = reinterpret_cast<f32x4 *>(a.part + part) + lane;
+        f32x4 xk[MB];   // paired: the x' of the pair being formed
+        auto fold_out = [&](int item, size_t dst, const f32x4 (*w)[MB * kWave]) {
+            f32x4 v[MB];
 #pragma unroll
             for (int m = 0; m < MB; ++m) {
                 const int e = m * kWave + lane;
-                dst[m * kWave] = ((w[3][e] + w[2][e]) + w[1][e]) + w[0][e];
+                v[m] = ((w[3][e] + w[2][e]) + w[1][e]) + w[0][e];
+            }
+            if (!a.paired) {
+                f32x4 *d = reinterpret_cast<f32x4 *>(a.part + dst) + lane;
+#pragma unroll
+                for (int m = 0; m < MB; ++m) d[m * kWave] = v[m];
+            } else if ((item & 1) == 0) {
+#pragma unroll
+                for (int m = 0; m < MB; ++m) xk[m] = v[m];
+            } else {   // the tile's sum, as k_project_tile_finish<1> forms it from the partials
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int m = 0; m < MB; ++m) {
+                    const f32x4 dv = f32x4{0.f, 0.f, 0.f, 0.f} + v[m], xv = f32x4{0.f, 0.f, 0.f, 0.f} + xk[m];
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) acc = mfma16_f32(dv[r], xv[r], acc);
+                }
+                float *g = a.gpart + dst + lane;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) g[64 * r] = acc[r];
             }
         };
-        // partial offsets of the items in flight: prev (folded now), cur, nxt
+        // output offsets of the items in flight: prev (folded now), cur, nxt
         size_t part_prev = 0, part_cur = cur < items ? stream_item(a, cur, count).dst : 0;
         size_t part_nxt = nxt < items ? stream_item(a, nxt, count).dst : 0;
-        bool have_prev = false;
+        int prev = -1;
         int n = 0;
         for (; cur < items; ++n) {
-            int claim = items;   // none
+            int claim = items;   // none (any value >= items)
             size_t part_claim = 0;
             if (nxt < items) {
-                int c = 0;
-                if (lane == 0) c = atomicAdd(a.work, 1);
-                claim = 2 * grid + __builtin_amdgcn_readfirstlane(c);
+                if (a.paired && (n & 1)) {
+                    claim = nxt + 1;   // the dy side of the pair whose x side is item n + 1
+                } else {   // a claimed pair (paired, n + 2 even) or item
+                    int c = 0;
+                    if (lane == 0) c = atomicAdd(a.work, 1);
+                    c = __builtin_amdgcn_readfirstlane(c);
+                    claim = a.paired ? 2 * (grid + c) : 2 * grid + c;
+                }
             }
             if (lane == 0) queue[(n + 2) & 3] = claim;
             if (claim < items) {   // the streaming waves take it decoded
@@ -768,16 +812,16 @@ __global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
                 part_claim = it.dst;
                 item_to_lds((lds_u32 *)decoded[(n + 2) & 3], it, lane);
             }
-            if (have_prev) fold_out(part_prev, fold[(n - 1) & 1]);
+            if (prev >= 0) fold_out(prev, part_prev, fold[(n - 1) & 1]);
             lds_barrier();   // B_n: the partials of item n are parked, item n + 2 is published
-            have_prev = true;
+            prev = cur;
             part_prev = part_cur;
             cur = nxt;
             part_cur = part_nxt;
             nxt = claim;
             part_nxt = part_claim;
         }
-        if (have_prev) fold_out(part_prev, fold[(n - 1) & 1]);
+        if (prev >= 0) fold_out(prev, part_prev, fold[(n - 1) & 1]);
         return;
     }
 
@@ -1210,8 +1254,8 @@ __global__ __launch_bounds__(256) void k_project_tile_finish_wg(ProjArgs a) {
 }
 
 template <typename TOut>
-__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, int B, int tpe, int KT,
-                                                        int k_in, int k_out, int64_t g_ld) {
+__global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const float *gpart, const uint64_t *tile_bits,
+                                                        int B, int tpe, int KT, int k_in, int k_out, int64_t g_ld) {
     // blockIdx.x: (layer, example); blockIdx.y: a 256-float block of the tile sums (block
     // (jo, ji) of G in the MFMA result layout: thread = 64 r + lane)
     const int l = blockIdx.x / B;
@@ -1221,6 +1265,10 @@ __global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const flo
     const int r = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int o = 16 * jo + 4 * (lane >> 4) + r, i = 16 * ji + (lane & 15);
     const float *p = gpart + static_cast<size_t>(l * B + b) * tpe * KB + blk * 256 + threadIdx.x;
+    // tile_bits (or NULL): an empty tile's sum was never written; it counts as 0
+    // (selected, so whatever the slot holds does not reach the sum)
+    const uint64_t *tb = tile_bits ? tile_bits + static_cast<size_t>(b) * tpe : nullptr;
+    auto kept = [&](int t, float v) { return tb == nullptr || load_uniform(tb + t) != 0 ? v : 0.f; };
     float s = 0.f;
     int t = 0;
     for (; t + 32 <= tpe; t += 32) {   // 32 loads in flight, summed in tile order
@@ -1228,16 +1276,16 @@ __global__ __launch_bounds__(256) void k_project_reduce(ProjGroup grp, const flo
 #pragma unroll
         for (int u = 0; u < 32; ++u) v[u] = p[static_cast<size_t>(t + u) * KB];
 #pragma unroll
-        for (int u = 0; u < 32; ++u) s += v[u];
+        for (int u = 0; u < 32; ++u) s += kept(t + u, v[u]);
     }
     for (; t + 8 <= tpe; t += 8) {
         float v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) v[u] = p[static_cast<size_t>(t + u) * KB];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s += v[u];
+        for (int u = 0; u < 8; ++u) s += kept(t + u, v[u]);
     }
-    for (; t < tpe; ++t) s += p[static_cast<size_t>(t) * KB];
+    for (; t < tpe; ++t) s += kept(t, p[static_cast<size_t>(t) * KB]);
     if (o < k_out && i < k_in) {
         TOut *out = static_cast<TOut *>(grp.layer[l].g_out) + static_cast<int64_t>(b) * g_ld;
         store_out<TOut>(out + o * k_in + i, s);
@@ -1348,7 +1396,8 @@ void launch_tiles(const ProjArgs &a, int max_items, hipStream_t s) {
 
 void launch_stream(const ProjArgs &a, int max_items, hipStream_t s) {
     const int cap = resident_groups<k_project_stream, kStreamNT>();
-    hipLaunchKernelGGL(k_project_stream, dim3(max_items < cap ? max_items : cap), dim3(kStreamNT), 0, s, a);
+    const int units = a.paired ? max_items / 2 : max_items;   // the first unit of each workgroup is fixed
+    hipLaunchKernelGGL(k_project_stream, dim3(units < cap ? units : cap), dim3(kStreamNT), 0, s, a);
 }
 
 // Tile groups sharing the projection slab (launch_tiles) for bf16 inputs at
@@ -1406,7 +1455,20 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     // Slots widest first (stable), so that the last items handed out are the
     // narrow ones and the tail after the last claim is short.
     a.ordered = a.slots <= kMaxSlots;
-    if (a.ordered) {
+    // Paired: the stream kernel (bf16, k <= 16, no shared inputs) with one chunk per
+    // layer side, so a workgroup that streams a tile's x side and then its dy side
+    // forms the tile's sum itself; pairs widest first.
+    a.paired = bf16_in && KT == 1 && smax == 1 && a.ordered;
+    for (int l = 0; l < grp.n_layers && a.paired; ++l) a.paired = a.layer[l].c_in == 1 && a.layer[l].c_out == 1;
+    if (a.paired) {
+        int order[kMaxGroup];
+        for (int l = 0; l < grp.n_layers; ++l) order[l] = l;
+        std::stable_sort(order, order + grp.n_layers, [&](int x, int y) {
+            return a.layer[x].n_in + a.layer[x].n_out > a.layer[y].n_in + a.layer[y].n_out;
+        });
+        for (int r = 0; r < grp.n_layers; ++r)
+            a.slot_order[r] = static_cast<uint16_t>(order[r] << 10 | a.layer[order[r]].slot_begin);
+    } else if (a.ordered) {
         int width[kMaxSlots], layer_of[kMaxSlots];
         for (int l = 0; l < grp.n_layers; ++l) {
             const ChunkLayer &L = a.layer[l];
@@ -1465,7 +1527,8 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     const int pairs = grp.n_layers * B * a.tpe * KT * KT;   // (tile, 16 x 16 block of G), one wave each
     const unsigned fgrid = static_cast<unsigned>((pairs + NW - 1) / NW);
     const unsigned tgrid = static_cast<unsigned>(grp.n_layers * B * a.tpe);   // one workgroup per tile
-    switch (KT) {
+    switch (a.paired ? 0 : KT) {
+        case 0: break;   // the stream kernel wrote the tile sums of the listed tiles
         case 1: hipLaunchKernelGGL((k_project_tile_finish<1>), dim3(fgrid), dim3(256), 0, s, a, pairs); break;
         case 2: hipLaunchKernelGGL((k_project_tile_finish_wg<2>), dim3(tgrid), dim3(256), 0, s, a); break;
         case 4: hipLaunchKernelGGL((k_project_tile_finish_wg<4>), dim3(tgrid), dim3(256), 0, s, a); break;
@@ -1475,12 +1538,14 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     if (e != hipSuccess) return e;
     const unsigned grid = static_cast<unsigned>(grp.n_layers) * B;
     const unsigned blocks = static_cast<unsigned>(KT * KT);   // 16 x 16 blocks of G
+    // paired with a mask: the sums of empty tiles were never written, the reduce skips them
+    const uint64_t *skip = a.paired ? a.tile_bits : nullptr;
     if (bf16_out)
-        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid, blocks), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
-                           KT, k_in, k_out, g_ld);
+        hipLaunchKernelGGL((k_project_reduce<bf16_bits>), dim3(grid, blocks), dim3(256), 0, s, grp, a.gpart, skip, B,
+                           a.tpe, KT, k_in, k_out, g_ld);
     else
-        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid, blocks), dim3(256), 0, s, grp, a.gpart, B, a.tpe,
-                           KT, k_in, k_out, g_ld);
+        hipLaunchKernelGGL((k_project_reduce<float>), dim3(grid, blocks), dim3(256), 0, s, grp, a.gpart, skip, B,
+                           a.tpe, KT, k_in, k_out, g_ld);
     return hipGetLastError();
 }
 

@@ -323,6 +323,44 @@ def test_project_shared_inputs_bitwise_equal():
         assert err <= 1e-3
 
 
+def test_project_paired_equals_unpaired():
+    """At k <= 16 with every layer side in one chunk the stream kernel runs a
+    tile's x and dy items back to back and forms the tile's sum itself (the
+    tile-sum kernel is skipped; the example sums skip empty tiles).  A layer
+    wider than one chunk turns that off for the whole launch.  The narrow
+    layers' outputs must be the same bits either way, and match the oracle."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import dev, host, normwise, say
+    say("[project] paired stream items == unpaired (one wide layer in the launch)")
+    g = W.rng(83)
+    B, T, k = 5, 200, 16
+    narrow = [(768, 2304), (768, 768), (3072, 768)]
+    wide = (512, 7000)            # two chunks on its dy side
+    lens = W.lengths(g, B, 1, T)
+    lens[1], lens[-1] = 0, T      # an empty example and a full one
+    mask_np = W.mask_from_lengths(lens, T)
+    mask = dev(mask_np)
+    data = [W.layer_inputs(84, i, B, T, ni, no, k, k, 1.0, 1e-2, "bf16") for i, (ni, no) in enumerate(narrow + [wide])]
+    t = [{key: dev(d[key]) for key in ("x", "dy", "p_in", "p_out")} for d in data]
+    outs = []
+    for with_wide in (False, True):
+        n = len(narrow) + int(with_wide)
+        store = torch.full((B, n * k * k), np.nan, dtype=torch.float32, device="cuda")
+        layers = [dict(t[i], g_out=store[:, i * k * k:(i + 1) * k * k]) for i in range(n)]
+        P.logra_project_layers(layers, mask=mask)
+        torch.cuda.synchronize()
+        outs.append(host(store)[:, :len(narrow) * k * k])
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    assert np.all(outs[0][1] == 0.0)          # the empty example
+    for i in (0, 2):
+        d = data[i]
+        want = oracle.project_factored(d["x"], d["dy"], d["p_in"], d["p_out"], mask_np)
+        err = max(normwise(outs[0][b, i * k * k:(i + 1) * k * k], want[b]) for b in range(B) if lens[b] > 0)
+        say(f"  layer {narrow[i]}: equal bits paired and unpaired; max normwise err {err:.2e}")
+        assert err <= 1e-3
+
+
 def test_project_all_masked_batch_writes_zeros():
     """No valid token anywhere: no tile is listed and no chunk item runs; every
     output row (pre-filled with 7.0) must still be written as zeros."""
