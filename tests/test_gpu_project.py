@@ -30,6 +30,11 @@ CASES = {
     # k = 64 takes the LDS-DMA path, k = 128 the register path
     "wide_in_k64_ragged": ("bf16", 3, 90, 16384, 1024, 64, 64, 1.0, 1e-3, True, "f32"),
     "wide_out_k128_ragged": ("bf16", 3, 70, 512, 28672, 128, 96, 1.0, 1e-3, True, "f32"),
+    # and at k <= 32: an unpaired stream item per chunk (k = 16, bf16), the per-wave chunk
+    # kernel (k = 16, fp32 inputs) and tile groups (k = 32)
+    "wide_out_k16_ragged": ("bf16", 3, 90, 1024, 16384, 16, 16, 1.0, 1e-3, True, "bf16"),
+    "wide_in_k16_f32": ("f32", 2, 40, 20000, 64, 16, 16, 1.0, 1e-2, True, "f32"),
+    "wide_in_k32_ragged": ("bf16", 2, 70, 15000, 512, 32, 32, 1.0, 1e-3, True, "f32"),
 }
 
 
@@ -152,14 +157,14 @@ def test_project_grouped_equals_single():
 
 
 def test_project_grouped_multichunk_vs_oracle():
-    """A group whose layers span several column chunks per side, with
-    partial last chunks of different widths (the launch processes the chunk
-    slots widest first), against the oracle layer by layer."""
+    """A group whose layers span several column chunks per side (chunks of
+    14,336 columns), with partial last chunks of different widths (the launch
+    processes the chunk slots widest first), against the oracle layer by layer."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import dev, host, rowwise_normwise, say
     say("[project] grouped multi-chunk layers vs oracle")
-    shapes = [(13000, 1024), (1024, 9000), (4096, 4096)]
+    shapes = [(30000, 1024), (1024, 20000), (4096, 4096)]
     B, T, k = 2, 70, 16
     lens = np.array([70, 41])
     mask_np = W.mask_from_lengths(lens, T)
@@ -336,7 +341,7 @@ def test_project_paired_equals_unpaired():
     g = W.rng(83)
     B, T, k = 5, 200, 16
     narrow = [(768, 2304), (768, 768), (3072, 768)]
-    wide = (512, 7000)            # two chunks on its dy side
+    wide = (512, 16384)           # two chunks on its dy side (chunks of 14,336 columns)
     lens = W.lengths(g, B, 1, T)
     lens[1], lens[-1] = 0, T      # an empty example and a full one
     mask_np = W.mask_from_lengths(lens, T)
