@@ -798,8 +798,8 @@ __global__ __launch_bounds__(kStreamNT, 1) void k_project_stream(ProjArgs a) {
             size_t part_claim = 0;
             if (nxt < items) {
                 if (a.paired && (n & 1)) {
-                    claim = nxt + 1;   // the dy side of the pair whose x side is item n + 1
-                } else {   // a claimed pair (paired, n + 2 even) or item
+                    claim = nxt + 1;   // the dy side of the pair whose x side (nxt) is at position n + 1
+                } else {   // a new pair (paired: position n + 2 is even) or a new item
                     int c = 0;
                     if (lane == 0) c = atomicAdd(a.work, 1);
                     c = __builtin_amdgcn_readfirstlane(c);
