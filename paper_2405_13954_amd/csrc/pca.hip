@@ -10,7 +10,9 @@
 //     example) that hold at least one unmasked token, each with the 32-bit
 //     map of its unmasked tokens.
 //  1. k_act_cov_dma (bf16): one workgroup per upper-triangle 256 x 256 tile
-//     (I <= J) of C, tiles grouped per XCD for L2 reuse; 4 waves, each owning a 128 x 128 quadrant as 4 x 4
+//     (I <= J) of C, tiles grouped per XCD for L2 reuse (one launch may hold
+//     several factors of the same batch, each with a range of workgroup
+//     slots); 4 waves, each owning a 128 x 128 quadrant as 4 x 4
 //     blocks of 32x32x16 bf16 MFMAs (fp32 accumulation).  The contraction
 //     runs over the listed slabs.  A slab of the two operands (the tile's
 //     256 features I.. and J.. of 32 tokens, 16 KB each in token-major
