@@ -1204,7 +1204,12 @@ __global__ __launch_bounds__(256) void k_project_tile_finish_wg(ProjArgs a) {
     constexpr int KP = 16 * KT;
     constexpr int NQ = MB * KT * kWave;     // f32x4 per chunk partial
     static_assert(NQ == 256 * KT, "thread t sums elements t + 256 u, u < KT");
-    __shared__ f32x4 xs[NQ], ds[NQ];
+    // Thread (wave w, lane) sums elements 256 u + 64 w + lane, u < KT: block row
+    // 4 u + w of the partial.  From KT = 4 on, w's blocks (jo, ji) all have ji = w
+    // (mod 4), so the x' it sums are the x' it needs and only dy' goes through LDS
+    // (half the LDS, so one round of workgroups fits the CUs at k = 64).
+    constexpr bool kOwnX = KT % 4 == 0;
+    __shared__ f32x4 xs[kOwnX ? 1 : NQ], ds[NQ];
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int tix = blockIdx.x;              // tile over all layers
@@ -1231,16 +1236,20 @@ __global__ __launch_bounds__(256) void k_project_tile_finish_wg(ProjArgs a) {
         for (int u = 0; u < KT; ++u) d[u] += src[static_cast<size_t>(c) * NQ + tid + 256 * u];
 #pragma unroll
     for (int u = 0; u < KT; ++u) {
-        xs[tid + 256 * u] = x[u];
+        if constexpr (!kOwnX) xs[tid + 256 * u] = x[u];
         ds[tid + 256 * u] = d[u];
     }
     __syncthreads();
-    for (int blk = wave; blk < KT * KT; blk += NW) {
+#pragma unroll
+    for (int i = 0; i < KT * KT / NW; ++i) {
+        const int blk = wave + NW * i;
         const int jo = blk / KT, ji = blk - jo * KT;
         f32x4 dv[MB], xv[MB];
 #pragma unroll
         for (int m = 0; m < MB; ++m) {
-            xv[m] = xs[(m * KT + ji) * kWave + lane];
+            // own x': element (m KT + ji) 64 + lane = 256 u + 64 w + lane, u = (m KT + ji - w) / 4
+            if constexpr (kOwnX) xv[m] = x[(m * KT + NW * i % KT) / NW];
+            else xv[m] = xs[(m * KT + ji) * kWave + lane];
             dv[m] = ds[(m * KT + jo) * kWave + lane];
         }
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
