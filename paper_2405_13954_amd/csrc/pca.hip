@@ -37,27 +37,30 @@
 //   largest magnitude (lowest index among equal magnitudes) is positive.
 //
 //  Q and Z are kept in row quads (four rows of a column adjacent).
-//  2. k_cq_part (+ k_cq_sum): Z = C Q; a workgroup owns 64 rows of C (32
-//     for p > 64) and a range of its columns, its waves splitting the range;
-//     128-bit loads of C and Q feed 16x16x4 fp32 MFMAs.  Column ranges
-//     (splits) give about 2048 workgroups; their partials are summed in
-//     split order.
+//  2. k_cq_dma / k_cq_regs (+ k_cq_sum): Z = C Q; a workgroup owns 64 rows
+//     of C (32 for p > 64) and a range of its columns, its waves splitting
+//     the range; 16x16x4 fp32 MFMAs.  p <= 64 (bound by the reads of C):
+//     64-column slabs of C and Q copied into an LDS ring; wider: 128-bit
+//     loads into a register pipeline.  Column ranges (splits) give about
+//     2048 workgroups; their partials are summed in split order.
 //  3. k_gram_part: fp64 partial sums of X^T Y over 256-row chunks (X^T X for
 //     the orthonormalisation, Z^T Q for Rayleigh-Ritz), fixed order.
-//  4. k_chol_inv_reg / k_chol_inv (one workgroup): the chunk sums, a
+//  4. k_chol_inv_reg / k_chol_inv_wide (one workgroup): the chunk sums, a
 //     shifted Cholesky Z^T Z + eps tr/p I = R^T R and R^{-1} in fp64 (p <= 64:
-//     one wave, a column per lane in registers; wider: LDS).
+//     one wave, a row per lane in registers; wider: a column per pair of
+//     threads in registers, one barrier per step).
 //  5. k_apply_rinv: Q = Z R^{-1} (fp64 arithmetic, fp32 result).
-//  6. k_jacobi_lds / k_jacobi (one workgroup): T in LDS, round-robin parallel
-//     cyclic Jacobi (p/2 disjoint rotations per round), eigenvectors
-//     accumulated in W^T (p <= 64: in LDS, each round one pass of 2 x 2
-//     blocks).
+//  6. k_jacobi_rot (one workgroup): T in LDS, round-robin parallel cyclic
+//     Jacobi (m/2 disjoint rotations per round, each round one pass of 2 x 2
+//     blocks), the rotations logged; k_jacobi_replay: W^T = the logged
+//     rotations applied to the identity, one wave per column.
 //  7. k_ritz, k_pca_out: Ritz vectors in the order of decreasing theta, the
 //     sign rule, and the rows of P in the output dtype.
 //
 // Every sum has a fixed order, so results are bitwise reproducible.
 #include <algorithm>
 #include <cstdint>
+#include <utility>
 
 #include "common.h"
 #include "internal.h"
@@ -463,7 +466,8 @@ __global__ __launch_bounds__(256) void k_act_cov_f32(const float *__restrict__ a
 constexpr int kGramRows = 256;   // rows per partial sum of a Gram matrix
 constexpr int kGramChunk = 64;   // rows staged in LDS at a time
 constexpr int kMaxP = 128;       // subspace width (at most 2 k for k <= 64)
-constexpr int kCqStages = 3;     // register pipeline depth of k_cq_part
+constexpr int kCqStages = 3;     // register pipeline depth of k_cq_regs
+constexpr int kJacobiSweeps = 40;   // at most this many Jacobi sweeps
 
 __host__ __device__ constexpr int round4(int n) { return (n + 3) & ~3; }
 __device__ __forceinline__ size_t qidx(int i, int j, int pp) {
@@ -491,21 +495,177 @@ __global__ __launch_bounds__(256) void k_pca_init(float *Q, int n, int p, int pp
     Q[e] = i < n && j < p ? hash_uniform(static_cast<uint32_t>(i), static_cast<uint32_t>(j)) : 0.f;
 }
 
+// The end of both C Q kernels: fold the four waves' sums ((w3 + w2) + w1) +
+// w0 through LDS (`fold`, MR NB 64 128-bit slots) and store the result in row
+// quads to Z (one split) or the split's partial.  Result register r of lane
+// (row, q) is row 4 q + r, column row of its 16 x 16 block: four consecutive
+// rows of one column, one 128-bit store.
+template <int NB, int MR>
+__device__ __forceinline__ void cq_fold_store(const f32x4 (&acc)[MR][NB], f32x4 *fold, int lane, int wave, int m0,
+                                              int n4, float *__restrict__ Zs) {
+    constexpr int pp = 16 * NB;
+    const int row = lane & 15, q = lane >> 4;
+    f32x4 *my = fold + lane;
+    if (wave == 3) {
+#pragma unroll
+        for (int m = 0; m < MR; ++m)
+#pragma unroll
+            for (int b = 0; b < NB; ++b) my[(m * NB + b) * kWave] = acc[m][b];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int w = 2; w >= 1; --w) {
+        if (wave == w) {
+#pragma unroll
+            for (int m = 0; m < MR; ++m)
+#pragma unroll
+                for (int b = 0; b < NB; ++b) my[(m * NB + b) * kWave] = my[(m * NB + b) * kWave] + acc[m][b];
+        }
+        __syncthreads();
+    }
+    if (wave == 0) {
+        float *dst = Zs + static_cast<size_t>(blockIdx.y) * n4 * pp;
+#pragma unroll
+        for (int m = 0; m < MR; ++m) {
+            const int i0 = m0 + 16 * m + 4 * q;
+            if (i0 >= n4) continue;
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                *reinterpret_cast<f32x4 *>(dst + qidx(i0, 16 * b + row, pp)) =
+                    my[(m * NB + b) * kWave] + acc[m][b];
+        }
+    }
+}
+
 // Z_s = C[:, K_s] Q[K_s, :] over the column range K_s = [s kr, (s + 1) kr) of
-// split s = blockIdx.y (kr a multiple of 64).  A workgroup owns 16 MR rows
-// of C; its four waves take the range's 16-column steps round-robin.  Lane
-// (row, q) of a wave streams columns k + 4q .. k + 4q + 3 of its row in each
-// row block (one 128-bit load per block) and rows k + 4q .. k + 4q + 3 of
-// one column of each 16-column block of Q (one 128-bit load), and feeds
-// them to 16x16x4 fp32 MFMAs, element e of both to MFMA e.  A register
-// pipeline keeps kCqStages - 1 steps in flight; every load is unconditional
-// (out-of-range offsets read zeros).  The waves' sums are folded in a fixed
-// order through LDS and written, in row quads, to Z (one split) or to the
-// split's partial.  Rows past n read zeros; columns past n meet the zero
+// split s = blockIdx.y (kr a multiple of 64).  A workgroup owns R = 16 MR
+// rows of C and streams the range in 64-column slabs: each slab's R rows of
+// C (256 bytes per row, whole cache lines) and the 16 row quads of Q it
+// meets are copied straight into an LDS ring by asynchronous global-to-LDS
+// copies, two slabs ahead.  Wave w takes the slab's 16-column step w: lane
+// (row, q) reads columns 4q .. 4q + 3 of that step in each row block and rows
+// 4q .. 4q + 3 of one column of each 16-column block of Q (one 128-bit LDS
+// read each; C's 16-byte chunks sit at chunk ^ (row & 15), so the reads of a
+// row block hit 16 different bank groups), and feeds them to 16x16x4 fp32
+// MFMAs, element e of both to MFMA e.  So wave w sums the range's steps w,
+// w + 4, ... in order.  The waves' sums are folded in a fixed order through
+// LDS and written, in row quads, to Z (one split) or to the split's partial.
+// Rows past n read zeros; so do columns past the range's end; columns past n
+// meet the zero rows of Q past n (a chunk straddling the end of a row reads
+// the next row's first columns, or zeros past the end of C, against those
+// zeros).  Every memory operation in the loop is a copy, so waiting until
+// only the later slabs' copies are pending is exact.
+template <int NB, int MR>
+struct CqDma {
+    static constexpr int R = 16 * MR, PP = 16 * NB;
+    static constexpr int kC = R * 256;              // bytes of a slab's rows of C
+    static constexpr int kQ = 16 * PP * 16;         // bytes of its 16 row quads of Q
+    static constexpr int kStage = kC + kQ;
+    static constexpr int kStages = 3;
+    static constexpr int kCopies = (kC + kQ) / 1024 / 4;   // 1 KB copies per wave per slab (MR + NB)
+    static_assert(kCopies == MR + NB, "each wave copies MR row groups of C and NB kilobytes of Q");
+    static_assert(MR * NB * kWave * 16 <= kStage, "the fold fits in one stage");
+};
+
+template <int NB, int MR>
+__global__ __launch_bounds__(256) void k_cq_dma(const float *__restrict__ C, int n, const float *__restrict__ Q,
+                                                int kr, float *__restrict__ Zs) {
+    using Sh = CqDma<NB, MR>;
+    constexpr int NS = Sh::kStages, pp = Sh::PP;
+    __shared__ __attribute__((aligned(1024))) uint8_t ring[NS * Sh::kStage];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int row = lane & 15, q = lane >> 4;
+    const int m0 = blockIdx.x * Sh::R;
+    const int k0 = blockIdx.y * kr;
+    const int k1 = min(n, k0 + kr);
+    const int n4 = round4(n);
+    const int rows = min(Sh::R, n - m0);
+    const auto rc = buf_rsrc_uniform(C + static_cast<size_t>(m0) * n, static_cast<uint32_t>(rows) * n * 4u);
+    const auto rq = buf_rsrc_uniform(Q, static_cast<uint32_t>(n4) * pp * 4u);
+    const uint32_t lds0 = lds_addr(ring);
+    // copy i of this wave (i < MR) covers slab rows 4 (MR wave + i) .. + 3:
+    // lane l writes position l & 15 of row 4 (MR wave + i) + (l >> 4), which
+    // holds the row's chunk (l & 15) ^ (row & 15)
+    uint32_t coff[MR];
+    int ccol[MR];
+#pragma unroll
+    for (int i = 0; i < MR; ++i) {
+        const int r = 4 * (MR * wave + i) + (lane >> 4);
+        ccol[i] = 4 * ((lane & 15) ^ (r & 15));
+        coff[i] = r < rows ? static_cast<uint32_t>(r * n + ccol[i]) * 4u : kBufOOB;
+    }
+    // copy i of this wave (i < NB) covers kilobyte NB wave + i of the slab's Q quads
+    const uint32_t qoff = static_cast<uint32_t>(NB * wave) * 1024u + static_cast<uint32_t>(lane) * 16u;
+    const int nslabs = (k1 - k0 + 63) / 64;
+    auto issue = [&](int sl, int stage) {   // slabs past the range: all out of range
+        const int k = k0 + 64 * sl;
+        const uint32_t lds = lds0 + static_cast<uint32_t>(stage * Sh::kStage);
+#pragma unroll
+        for (int i = 0; i < MR; ++i) {
+            const bool in = sl < nslabs && k + ccol[i] < k1;
+            copy_to_lds(rc, in ? coff[i] + static_cast<uint32_t>(k) * 4u : kBufOOB,
+                        lds + static_cast<uint32_t>(MR * wave + i) * 1024u);
+        }
+        const uint32_t kq = static_cast<uint32_t>(k) * pp * 4u;   // bytes of row quad k / 4
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            copy_to_lds(rq, sl < nslabs ? kq + qoff + static_cast<uint32_t>(i) * 1024u : kBufOOB,
+                        lds + static_cast<uint32_t>(Sh::kC + (NB * wave + i) * 1024));
+    };
+
+    f32x4 acc[MR][NB];
+#pragma unroll
+    for (int m = 0; m < MR; ++m)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) acc[m][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < NS - 1; ++i) issue(i, i);
+    const int cpos = ((4 * wave + q) ^ row) * 16;   // this lane's chunk within a row of its row blocks
+    for (int sl = 0; sl < nslabs; ++sl) {
+        // this wave's copies of slab sl are done when only the later slab's are
+        // pending; after the barrier every wave's are, and every wave has read
+        // slab sl - 1, whose stage the next copies refill
+        asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"((NS - 2) * Sh::kCopies) : "memory");
+        issue(sl + NS - 1, (sl + NS - 1) % NS);
+        const uint8_t *cb = ring + (sl % NS) * Sh::kStage;
+        const uint8_t *qb = cb + Sh::kC;
+        u32x4 cv[MR], qv[NB];
+#pragma unroll
+        for (int m = 0; m < MR; ++m) cv[m] = *reinterpret_cast<const u32x4 *>(cb + (16 * m + row) * 256 + cpos);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+            qv[b] = *reinterpret_cast<const u32x4 *>(qb + ((4 * wave + q) * pp + 16 * b + row) * 16);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int m = 0; m < MR; ++m)
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    acc[m][b] = mfma16_f32(__uint_as_float(cv[m][e]), __uint_as_float(qv[b][e]), acc[m][b]);
+    }
+    // the copies past the range (zeros) are still in flight; stage 0 then
+    // holds the fold
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    cq_fold_store<NB, MR>(acc, reinterpret_cast<f32x4 *>(ring), lane, wave, m0, n4, Zs);
+}
+
+// Z_s = C[:, K_s] Q[K_s, :] as k_cq_dma computes it (the same steps, sums
+// and fold), for wide subspaces (pp > 64).  There the 16x16x4 fp32 MFMAs,
+// not the reads of C, bound the pass, and an LDS ring would leave room for
+// one workgroup per CU; the waves of several workgroups hide the MFMA and
+// load latencies better.  A workgroup owns 16 MR rows of C; its four waves
+// take the range's 16-column steps round-robin.  Lane (row, q) of a wave
+// streams columns k + 4q .. k + 4q + 3 of its row in each row block (one
+// 128-bit load per block) and rows k + 4q .. k + 4q + 3 of one column of
+// each 16-column block of Q (one 128-bit load), and feeds them to the
+// MFMAs, element e of both to MFMA e.  A register pipeline keeps
+// kCqStages - 1 steps in flight; every load is unconditional (out-of-range
+// offsets read zeros).  Rows past n read zeros; columns past n meet the zero
 // rows of Q past n (a load straddling the end of a row reads the next row's
 // first columns, or zeros past the end of C, against those zeros).
 template <int NB, int MR>
-__global__ __launch_bounds__(256) void k_cq_part(const float *__restrict__ C, int n, const float *__restrict__ Q,
+__global__ __launch_bounds__(256) void k_cq_regs(const float *__restrict__ C, int n, const float *__restrict__ Q,
                                                  int kr, float *__restrict__ Zs) {
     constexpr int pp = 16 * NB;
     constexpr int ST = kCqStages;
@@ -562,39 +722,7 @@ __global__ __launch_bounds__(256) void k_cq_part(const float *__restrict__ C, in
             s += 4 * ST;
         }
     }
-    // fold ((w3 + w2) + w1) + w0; result register r of lane (row, q) is row
-    // 4 q + r, column row of its 16 x 16 block: four consecutive rows of one
-    // column, one 128-bit store in row quads
-    f32x4 *my = fold + lane;
-    if (wave == 3) {
-#pragma unroll
-        for (int m = 0; m < MR; ++m)
-#pragma unroll
-            for (int b = 0; b < NB; ++b) my[(m * NB + b) * kWave] = acc[m][b];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int w = 2; w >= 1; --w) {
-        if (wave == w) {
-#pragma unroll
-            for (int m = 0; m < MR; ++m)
-#pragma unroll
-                for (int b = 0; b < NB; ++b) my[(m * NB + b) * kWave] = my[(m * NB + b) * kWave] + acc[m][b];
-        }
-        __syncthreads();
-    }
-    if (wave == 0) {
-        float *dst = Zs + static_cast<size_t>(blockIdx.y) * n4 * pp;
-#pragma unroll
-        for (int m = 0; m < MR; ++m) {
-            const int i0 = m0 + 16 * m + 4 * q;
-            if (i0 >= n4) continue;
-#pragma unroll
-            for (int b = 0; b < NB; ++b)
-                *reinterpret_cast<f32x4 *>(dst + qidx(i0, 16 * b + row, pp)) =
-                    my[(m * NB + b) * kWave] + acc[m][b];
-        }
-    }
+    cq_fold_store<NB, MR>(acc, fold, lane, wave, m0, n4, Zs);
 }
 
 // Z = sum of the splits' partials, in split order (128-bit elements).
@@ -689,23 +817,57 @@ void launch_gram(const float *X, const float *Y, int n, int p, int pp, double *p
     else hipLaunchKernelGGL(k_gram_part<128>, grid, dim3(256), 0, s, X, Y, n, p, pp, part);
 }
 
-// G = sum of the chunk partials, in chunk order, into A (all threads; eight
-// loads in flight).
+// G = sum of the chunk partials, in chunk order, into A (all threads).  The
+// partials were just written by CUs all over the chip and this workgroup
+// runs alone, so the sum is bound by memory latency: a thread sums four
+// elements at a time with eight chunks of each in flight (32 loads).
 __device__ __forceinline__ void sum_partials(const double *__restrict__ part, int chunks, int np, double *A,
                                              int tid) {
-    for (int e = tid; e < np; e += 256) {
-        double s = 0.0;
+    for (int e0 = tid; e0 < np; e0 += 4 * 256) {
+        double s[4] = {0.0, 0.0, 0.0, 0.0};
         int c = 0;
         for (; c + 8 <= chunks; c += 8) {
-            double v[8];
+            double v[4][8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = part[static_cast<size_t>(c + u) * np + e];
+            for (int u = 0; u < 4; ++u)
 #pragma unroll
-            for (int u = 0; u < 8; ++u) s += v[u];
+                for (int w = 0; w < 8; ++w)
+                    v[u][w] = e0 + 256 * u < np ? part[static_cast<size_t>(c + w) * np + e0 + 256 * u] : 0.0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int w = 0; w < 8; ++w) s[u] += v[u][w];
         }
-        for (; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
-        A[e] = s;
+        for (; c < chunks; ++c)
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (e0 + 256 * u < np) s[u] += part[static_cast<size_t>(c) * np + e0 + 256 * u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (e0 + 256 * u < np) A[e0 + 256 * u] = s[u];
     }
+}
+
+// G = the sum of the chunk partials, in chunk order (the order sum_partials
+// takes), written over chunk 0's slot: a thread reads all of its element's
+// chunks before it writes.  The partials of a wide Gram matrix (p = 128:
+// 7 MB at n = 14336) are too much for one workgroup to gather; spread over
+// the chip they take a few microseconds, and the one-workgroup kernels then
+// read a single chunk.
+__global__ __launch_bounds__(256) void k_sum_parts(double *__restrict__ part, int chunks, int np) {
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e >= np) return;
+    double s = 0.0;
+    int c = 0;
+    for (; c + 16 <= chunks; c += 16) {
+        double v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = part[static_cast<size_t>(c + u) * np + e];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) s += v[u];
+    }
+    for (; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
+    part[e] = s;
 }
 
 // p <= PM (32 or 64).  One workgroup sums the partials into G; wave 0 then,
@@ -775,63 +937,146 @@ __global__ __launch_bounds__(256) void k_chol_inv_reg(const double *__restrict__
         if (r < p && c < p) RinvT[c * p + r] = a[c];
 }
 
-// p > 64: one workgroup, G = sum of the chunk partials, then the shifted
-// Cholesky (right-looking, a barrier per phase of each step) and R^{-1}
-// (thread c solves R x = e_c upwards, x kept below the diagonal), in fp64 in
-// LDS.  Writes R^{-T} [p][p] (R^{-1} transposed: zero above the diagonal).
-__global__ __launch_bounds__(256) void k_chol_inv(const double *__restrict__ part, int chunks, int p,
-                                                  double *__restrict__ RinvT) {
-    __shared__ double A[kMaxP * kMaxP];   // G; then R on and above the diagonal, R^{-1} (transposed) below it
-    __shared__ double red[256];
-    const int tid = threadIdx.x, np = p * p;
-    sum_partials(part, chunks, np, A, tid);
+// f(std::integral_constant<int, I>{}) for I = 0 .. N - 1, expanded by the
+// front end: a register array indexed by I stays in registers however long
+// the body is (the loop unroller gives up on long bodies).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_seq(F &f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// a[i] -= v[i] f for i < 64, v 64 consecutive doubles in LDS (16-byte
+// aligned): read 16 at a time, one group ahead of its FMAs, so that at most
+// two groups are live next to a; a is in registers on return.
+__device__ __forceinline__ void axpy64_lds(double (&a)[64], const double *v, double f) {
+    const double2 *v2 = reinterpret_cast<const double2 *>(v);
+    double2 cur[8], nxt[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) cur[k] = v2[k];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        if (g < 3) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) nxt[k] = v2[8 * (g + 1) + k];
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            a[16 * g + 2 * k] = fma(-cur[k].x, f, a[16 * g + 2 * k]);
+            a[16 * g + 2 * k + 1] = fma(-cur[k].y, f, a[16 * g + 2 * k + 1]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) cur[k] = nxt[k];
+    }
+    // the updated values are materialised here: left to itself the compiler
+    // sinks each step's FMAs towards the step that reads the row, keeping
+    // every loaded value live until then
+#pragma unroll
+    for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(a[i]));
+}
+
+// 64 < p <= 128: one workgroup.  Thread (c, h), c = 64 (wave & 1) + lane and
+// h = wave >> 1, keeps rows 64 h .. 64 h + 63 of column c of the matrix in
+// registers (padded to 128 with the identity, whose factor and inverse are
+// the identity).  The shifted Cholesky G + eps (tr G / p) I = R^T R runs in
+// outer-product form: step j passes row j through LDS (zeros left of the
+// diagonal) and every thread updates its entries below it, A_rc -= A_jr
+// (A_jc / A_jj), one barrier per step (two row buffers alternate); each
+// step is the same 64 FMAs in every thread, the zeros leaving the rows above
+// it unchanged.  Row r of R is then row r of
+// the updated matrix over sqrt(A_rr) (a non-positive pivot, which cannot
+// follow the shift, is taken as 1).  X = R^{-1} solves R X = I by back
+// substitution in the same form with R in LDS: steps j = 127 .. 0 finish
+// row j of X, X_jc = B_jc / R_jj, pass it through LDS and update the rows
+// above it, B_rc -= R_rj X_jc.  All fp64.  Writes R^{-T} [p][p] (R^{-1}
+// transposed: zero above the diagonal), through LDS so that the stores are
+// coalesced.
+__global__ __launch_bounds__(256) void k_chol_inv_wide(const double *__restrict__ part, int chunks, int p,
+                                                       double *__restrict__ RinvT) {
+    constexpr int PM = kMaxP;
+    constexpr int RS = PM + 2;   // stride of the column-major copies of R and R^{-T} (even: 16-byte pairs)
+    __shared__ __attribute__((aligned(16))) double A[PM * RS];   // G [p][p]; then R by columns; then R^{-T} by rows
+    __shared__ __attribute__((aligned(16))) double buf[2][PM];
+    __shared__ double rdiag[PM];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = 64 * (wave & 1) + lane;
+    const int h = wave >> 1;
+    sum_partials(part, chunks, p * p, A, tid);
     __syncthreads();
     double tr = 0.0;
-    for (int a = tid; a < p; a += 256) tr += A[a * p + a];
-    red[tid] = tr;
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-        if (tid < w) red[tid] += red[tid + w];
-        __syncthreads();
+    for (int r = 0; r < p; ++r) tr += A[r * p + r];   // the same order in every thread
+    const double shift = 1e-12 * (tr > 0.0 ? tr / p : 1.0);
+    double a[64];
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+        const int r = 64 * h + i;
+        const double g = A[min(r, p - 1) * p + min(c, p - 1)];   // clamped: padding is selected below
+        a[i] = r < p && c < p ? (r == c ? g + shift : g) : r == c ? 1.0 : 0.0;
     }
-    const double shift = 1e-12 * (red[0] > 0.0 ? red[0] / p : 1.0);
-    for (int a = tid; a < p; a += 256) A[a * p + a] += shift;
-    __syncthreads();
-    for (int j = 0; j < p; ++j) {
-        if (tid == 0) {
-            const double d = A[j * p + j];
-            A[j * p + j] = d > 0.0 ? sqrt(d) : 1.0;
-        }
-        __syncthreads();
-        const double rjj = A[j * p + j];
-        for (int c = j + 1 + tid; c < p; c += 256) A[j * p + c] /= rjj;
-        __syncthreads();
-        for (int e = tid; e < (p - j - 1) * (p - j - 1); e += 256) {
-            const int r = j + 1 + e / (p - j - 1), c = j + 1 + e % (p - j - 1);
-            if (c >= r) A[r * p + c] -= A[j * p + r] * A[j * p + c];
-        }
-        __syncthreads();
+    __syncthreads();   // G is overwritten below
+    {
+        static_for<PM>([&](auto step) __attribute__((always_inline)) {
+            constexpr int j = decltype(step)::value;
+            constexpr int hj = j / 64, jj = j % 64;
+            double *row = buf[jj & 1];
+            if (h == hj) row[c] = c >= j ? a[jj] : 0.0;   // zeros left of the diagonal: no update there
+            __syncthreads();
+            const double d = row[j];
+            const double e = d > 0.0 ? d : 1.0;
+            if (tid == 0) rdiag[j] = e;
+            const double f = c > j ? row[c] / e : 0.0;
+            const double keep = a[jj];   // row j itself is final
+            axpy64_lds(a, row + 64 * h, f);
+            a[jj] = h == hj ? keep : a[jj];
+        });
     }
-    for (int c = tid; c < p; c += 256) {
-        const double xc = 1.0 / A[c * p + c];
-        for (int r = c - 1; r >= 0; --r) {
-            double s = A[r * p + c] * xc;
-            for (int m = r + 1; m < c; ++m) s = fma(A[r * p + m], A[c * p + m], s);
-            A[c * p + r] = -s / A[r * p + r];
-        }
+    __syncthreads();   // the pivots are complete
+    if (tid < PM) rdiag[tid] = sqrt(rdiag[tid]);   // R_rr
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 64; ++i) {
+        const int r = 64 * h + i;
+        const double rr = rdiag[r];
+        A[c * RS + r] = r < c ? a[i] / rr : r == c ? rr : 0.0;   // R_rc, column c contiguous
+        a[i] = r == c ? 1.0 : 0.0;
     }
     __syncthreads();
-    for (int e = tid; e < np; e += 256) {
-        const int r = e / p, c = e - (e / p) * p;
-        // element e of R^{-T} is (R^{-1})[c][r]: nonzero for c <= r
-        RinvT[e] = c < r ? A[r * p + c] : r == c ? 1.0 / A[r * p + r] : 0.0;
+    {
+        static_for<PM>([&](auto step) __attribute__((always_inline)) {
+            constexpr int j = PM - 1 - decltype(step)::value;
+            constexpr int hj = j / 64, jj = j % 64;
+            double *row = buf[jj & 1];
+            const double *Rj = A + j * RS;   // column j of R
+            if (h == hj) {
+                a[jj] = a[jj] / Rj[j];
+                row[c] = a[jj];
+            }
+            __syncthreads();
+            const double x = row[c];
+            const double keep = a[jj];   // row j of X is final; R is zero below its diagonal
+            axpy64_lds(a, Rj + 64 * h, x);
+            a[jj] = h == hj ? keep : a[jj];
+        });
+    }
+    __syncthreads();   // every read of R is done
+#pragma unroll
+    for (int i = 0; i < 64; ++i) A[c * RS + 64 * h + i] = a[i];   // row c of R^{-T} is column c of R^{-1}
+    __syncthreads();
+    for (int e = tid; e < p * p; e += 256) {
+        const int r = e / p;
+        RinvT[e] = A[r * RS + (e - r * p)];
     }
 }
 
 void launch_chol_inv(const double *part, int chunks, int p, double *RinvT, hipStream_t s) {
     if (p <= 32) hipLaunchKernelGGL(k_chol_inv_reg<32>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
     else if (p <= 64) hipLaunchKernelGGL(k_chol_inv_reg<64>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
-    else hipLaunchKernelGGL(k_chol_inv, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
+    else hipLaunchKernelGGL(k_chol_inv_wide, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
 }
 
 // Q = Z R^{-1} in row quads: a thread forms one column j of four rows, each
@@ -860,130 +1105,23 @@ __global__ __launch_bounds__(256) void k_apply_rinv(const float *__restrict__ Z,
 }
 
 // One workgroup: T = (sum of the chunk partials of Q^T Z), symmetrised, is
-// diagonalised by round-robin parallel cyclic Jacobi in fp64: each round
-// applies p'/2 disjoint plane rotations (p' = p rounded up to even; a pair
-// with the padding index p is skipped), each zeroing T[a][b] (the symmetric
-// 2 x 2 Schur decomposition).  Sweeps stop when the off-diagonal mass is
-// below 1e-30 of the total, or after 40.  Writes theta [p] and the
-// eigenvectors as the rows of Wt [p][p].
-__global__ __launch_bounds__(256) void k_jacobi(const double *__restrict__ part, int chunks, int p,
-                                                double *__restrict__ Wt, double *__restrict__ theta) {
-    __shared__ double T[kMaxP * kMaxP];
-    __shared__ double cs[64], sn[64];
-    __shared__ int pa[64], pb[64];
-    __shared__ double red[256];
-    const int tid = threadIdx.x, np = p * p;
-    for (int e = tid; e < np; e += 256) {
-        double s = 0.0;
-        for (int c = 0; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
-        T[e] = s;
-    }
-    __syncthreads();
-    for (int e = tid; e < np; e += 256) {
-        const int a = e / p, b = e - (e / p) * p;
-        if (a < b) {
-            const double v = 0.5 * (T[a * p + b] + T[b * p + a]);
-            T[a * p + b] = v;
-            T[b * p + a] = v;
-        }
-        Wt[e] = a == b ? 1.0 : 0.0;
-    }
-    __syncthreads();
-    const int m = p + (p & 1);   // players of the round-robin schedule
-    const int half = m / 2;
-    for (int sweep = 0; sweep < 40; ++sweep) {
-        double off = 0.0, all = 0.0;
-        for (int e = tid; e < np; e += 256) {
-            const int a = e / p, b = e - (e / p) * p;
-            const double v = T[e] * T[e];
-            all += v;
-            if (a != b) off += v;
-        }
-        red[tid] = off;
-        __syncthreads();
-        for (int w = 128; w > 0; w >>= 1) {
-            if (tid < w) red[tid] += red[tid + w];
-            __syncthreads();
-        }
-        const double off_sum = red[0];
-        __syncthreads();
-        red[tid] = all;
-        __syncthreads();
-        for (int w = 128; w > 0; w >>= 1) {
-            if (tid < w) red[tid] += red[tid + w];
-            __syncthreads();
-        }
-        const double all_sum = red[0];
-        __syncthreads();
-        if (!(off_sum > 1e-30 * all_sum)) break;   // uniform: every thread read the same sums
-        for (int rnd = 0; rnd < m - 1; ++rnd) {
-            if (tid < half) {
-                // circle method: position 0 fixed, positions 1..m-1 rotate by rnd
-                auto player = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + rnd) % (m - 1); };
-                int a = player(tid), b = player(m - 1 - tid);
-                if (a > b) {
-                    const int t = a;
-                    a = b;
-                    b = t;
-                }
-                double c = 1.0, s = 0.0;
-                if (b < p) {
-                    const double apq = T[a * p + b];
-                    if (apq != 0.0) {
-                        const double tau = (T[b * p + b] - T[a * p + a]) / (2.0 * apq);
-                        const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-                        c = 1.0 / sqrt(1.0 + t * t);
-                        s = t * c;
-                    }
-                }
-                pa[tid] = a;
-                pb[tid] = b;
-                cs[tid] = c;
-                sn[tid] = s;
-            }
-            __syncthreads();
-            // rows a, b of T (all columns), then columns a, b (all rows), and rows a, b of W^T
-            for (int e = tid; e < half * p; e += 256) {
-                const int q = e / p, j = e - (e / p) * p;
-                const int a = pa[q], b = pb[q];
-                if (b < p) {
-                    const double c = cs[q], s = sn[q];
-                    const double ta = T[a * p + j], tb = T[b * p + j];
-                    T[a * p + j] = c * ta - s * tb;
-                    T[b * p + j] = s * ta + c * tb;
-                }
-            }
-            __syncthreads();
-            for (int e = tid; e < half * p; e += 256) {
-                const int q = e / p, i = e - (e / p) * p;
-                const int a = pa[q], b = pb[q];
-                if (b < p) {
-                    const double c = cs[q], s = sn[q];
-                    const double ta = T[i * p + a], tb = T[i * p + b];
-                    T[i * p + a] = c * ta - s * tb;
-                    T[i * p + b] = s * ta + c * tb;
-                    const double wa = Wt[static_cast<size_t>(a) * p + i], wb = Wt[static_cast<size_t>(b) * p + i];
-                    Wt[static_cast<size_t>(a) * p + i] = c * wa - s * wb;
-                    Wt[static_cast<size_t>(b) * p + i] = s * wa + c * wb;
-                }
-            }
-            __syncthreads();
-        }
-    }
-    for (int a = tid; a < p; a += 256) theta[a] = T[a * p + a];
-}
-
-// p <= 64: the same iteration with T and W^T both in LDS, and each round in
-// one pass.  A round's pairs partition the indices, so the block of T on the
-// rows of pair P and the columns of pair Q becomes G_P T_PQ G_Q^T with
-// G = [[c, -s], [s, c]] (the identity for a pair with the padding index):
-// the same products as rotating the rows and then the columns, formed by one
-// thread per block in place.  Rows a, b of W^T turn by G_P.  Two barriers
-// per round; the convergence sums reduce by wave butterflies.
-__global__ __launch_bounds__(256) void k_jacobi_lds(const double *__restrict__ part, int chunks, int p,
-                                                    double *__restrict__ Wt, double *__restrict__ theta) {
-    constexpr int PM = 64;
-    __shared__ double T[PM * PM], W[PM * PM];
+// diagonalised by round-robin parallel cyclic Jacobi in fp64.  Each round
+// applies m/2 disjoint plane rotations (m = p rounded up to even; a pair
+// with the padding index p is the identity), each zeroing T[a][b] (the
+// symmetric 2 x 2 Schur decomposition).  A round's pairs partition the
+// indices, so the block of T on the rows of pair P and the columns of pair
+// Q becomes G_P T_PQ G_Q^T with G = [[c, -s], [s, c]]: the same products as
+// rotating the rows and then the columns, formed by one thread per block in
+// place, two barriers per round.  Sweeps stop when the off-diagonal mass is
+// below 1e-30 of the total, or after kJacobiSweeps.  The eigenvectors are
+// not formed here: each round's (c, s) go to `rot` [round][m/2] and the
+// number of rounds to *rounds, and k_jacobi_replay applies them to W^T.
+// Writes theta [p].  T stays in LDS (PM = 64 or 128).
+template <int PM>
+__global__ __launch_bounds__(256) void k_jacobi_rot(const double *__restrict__ part, int chunks, int p,
+                                                    double2 *__restrict__ rot, int *__restrict__ rounds,
+                                                    double *__restrict__ theta) {
+    __shared__ double T[PM * PM];
     __shared__ double cs[PM / 2], sn[PM / 2];
     __shared__ int pa[PM / 2], pb[PM / 2];
     __shared__ double red[8];
@@ -997,12 +1135,12 @@ __global__ __launch_bounds__(256) void k_jacobi_lds(const double *__restrict__ p
             T[a * p + b] = v;
             T[b * p + a] = v;
         }
-        W[e] = a == b ? 1.0 : 0.0;
     }
     __syncthreads();
     const int m = p + (p & 1);   // players of the round-robin schedule
     const int half = m / 2;
-    for (int sweep = 0; sweep < 40; ++sweep) {
+    int done = 0;   // rounds applied
+    for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
         double off = 0.0, all = 0.0;
         for (int e = tid; e < np; e += 256) {
             const int a = e / p, b = e - (e / p) * p;
@@ -1023,8 +1161,9 @@ __global__ __launch_bounds__(256) void k_jacobi_lds(const double *__restrict__ p
         const double off_sum = ((red[0] + red[2]) + red[4]) + red[6];
         const double all_sum = ((red[1] + red[3]) + red[5]) + red[7];
         if (!(off_sum > 1e-30 * all_sum)) break;   // uniform: every thread read the same sums
-        for (int rnd = 0; rnd < m - 1; ++rnd) {   // red is rewritten only after this round's barriers
+        for (int rnd = 0; rnd < m - 1; ++rnd, ++done) {   // red is rewritten only after this round's barriers
             if (tid < half) {
+                // circle method: position 0 fixed, positions 1 .. m - 1 turn by one each round
                 auto player = [&](int pos) { return pos == 0 ? 0 : 1 + (pos - 1 + rnd) % (m - 1); };
                 int a = player(tid), b = player(m - 1 - tid);
                 if (a > b) {
@@ -1046,6 +1185,7 @@ __global__ __launch_bounds__(256) void k_jacobi_lds(const double *__restrict__ p
                 pb[tid] = b;
                 cs[tid] = c;
                 sn[tid] = sv;
+                rot[static_cast<size_t>(done) * half + tid] = double2{c, sv};
             }
             __syncthreads();
             for (int e = tid; e < half * half; e += 256) {
@@ -1062,51 +1202,123 @@ __global__ __launch_bounds__(256) void k_jacobi_lds(const double *__restrict__ p
                 if (bp) T[b * p + c2] = cq * u10 - sq * u11;
                 if (bp && bq) T[b * p + d] = sq * u10 + cq * u11;
             }
-            for (int e = tid; e < half * p; e += 256) {
-                const int P = e / p, i = e - (e / p) * p;
-                const int a = pa[P], b = pb[P];
-                if (b < p) {
-                    const double c = cs[P], sv = sn[P];
-                    const double wa = W[a * p + i], wb = W[b * p + i];
-                    W[a * p + i] = c * wa - sv * wb;
-                    W[b * p + i] = sv * wa + c * wb;
-                }
-            }
             __syncthreads();
         }
     }
-    for (int e = tid; e < np; e += 256) Wt[e] = W[e];
+    if (tid == 0) *rounds = done;
     for (int a = tid; a < p; a += 256) theta[a] = T[a * p + a];
 }
 
+// W^T (rows: the eigenvectors of T) = the product of the logged rotations
+// applied to the identity.  A rotation of pair (a, b) turns rows a and b of
+// W^T, so every column evolves on its own: workgroup i (one wave) keeps
+// column i in LDS and takes the rounds in order, lane q turning entries a, b
+// of the round's pair q by its (c, s), with the pairs found by the same
+// circle method.  The LDS operations of one wave take effect in program
+// order, so a round reads what the one before it wrote.  The rotations'
+// (c, s) are loaded eight rounds ahead.  Writes Wt [p][p].
+__global__ __launch_bounds__(64) void k_jacobi_replay(const double2 *__restrict__ rot, const int *__restrict__ rounds,
+                                                      int p, double *__restrict__ Wt) {
+    constexpr int kAhead = 8;
+    __shared__ double col[kMaxP];
+    const int i = blockIdx.x, lane = threadIdx.x;
+    for (int a = lane; a < p; a += kWave) col[a] = a == i ? 1.0 : 0.0;
+    const int m = p + (p & 1), half = m / 2;
+    const int nr = *rounds;
+    const bool active = lane < half;
+    // circle positions of this lane's pair, advanced by one (mod m - 1) each round
+    int ta = lane == 0 ? -1 : lane - 1;        // -1: the fixed position 0
+    int tb = m - 1 - lane - 1;
+    double2 g[kAhead], gn[kAhead];
+#pragma unroll
+    for (int u = 0; u < kAhead; ++u)
+        g[u] = active && u < nr ? rot[static_cast<size_t>(u) * half + lane] : double2{1.0, 0.0};
+    for (int r0 = 0; r0 < nr; r0 += kAhead) {
+#pragma unroll
+        for (int u = 0; u < kAhead; ++u) {
+            const int r = r0 + kAhead + u;
+            gn[u] = active && r < nr ? rot[static_cast<size_t>(r) * half + lane] : double2{1.0, 0.0};
+        }
+#pragma unroll
+        for (int u = 0; u < kAhead; ++u) {
+            if (r0 + u < nr && active) {
+                int a = ta < 0 ? 0 : 1 + ta, b = 1 + tb;
+                if (a > b) {
+                    const int t = a;
+                    a = b;
+                    b = t;
+                }
+                if (b < p) {
+                    const double c = g[u].x, sv = g[u].y;
+                    const double wa = col[a], wb = col[b];
+                    col[a] = c * wa - sv * wb;
+                    col[b] = sv * wa + c * wb;
+                }
+            }
+            ta = ta < 0 ? ta : ta + 1 == m - 1 ? 0 : ta + 1;
+            tb = tb + 1 == m - 1 ? 0 : tb + 1;
+        }
+#pragma unroll
+        for (int u = 0; u < kAhead; ++u) g[u] = gn[u];
+    }
+    for (int a = lane; a < p; a += kWave) Wt[static_cast<size_t>(a) * p + i] = col[a];
+}
+
 // Ritz vectors of the k largest theta (decreasing; equal values in index
-// order): V[e][i] = sum_j Q[i][j] Wt[order_e][j] (fp64 sums; Q in row
-// quads), eigvals[e].
-// The order is found by every thread from theta (p <= 128).
+// order): V[e][i] = sum_j Q[i][j] Wt[order_e][j] (fp64 sums in j order, fp32
+// result; Q in row quads), and eigvals[e].  Workgroup (x, y) forms Ritz
+// vectors kRitzE y .. kRitzE y + kRitzE - 1 on 1024 rows: a thread takes one
+// row quad, one 128-bit load of Q per j feeding 4 kRitzE fp64 FMAs, with the
+// selected rows of Wt in LDS.  Each theta's rank is counted by its own
+// thread.
+constexpr int kRitzE = 16;
 __global__ __launch_bounds__(256) void k_ritz(const float *__restrict__ Q, int n, int p, int pp, int k,
                                               const double *__restrict__ Wt, const double *__restrict__ theta,
                                               float *__restrict__ V, float *__restrict__ eigvals) {
-    __shared__ int order[64];
-    __shared__ double w[128];
-    const int e = blockIdx.y;
-    if (threadIdx.x == 0) {
-        // rank of each theta among all (larger first, lower index first): the e-th is order[e]
-        for (int a = 0; a < p; ++a) {
-            int rank = 0;
-            for (int b = 0; b < p; ++b) rank += theta[b] > theta[a] || (theta[b] == theta[a] && b < a);
-            if (rank < k) order[rank] = a;
-        }
+    __shared__ double th[kMaxP];
+    __shared__ int order[kRitzE];
+    __shared__ double w[kRitzE * kMaxP];
+    const int tid = threadIdx.x, e0 = blockIdx.y * kRitzE;
+    const int ne = min(kRitzE, k - e0);
+    for (int a = tid; a < p; a += 256) th[a] = theta[a];
+    __syncthreads();
+    for (int a = tid; a < p; a += 256) {
+        int rank = 0;   // larger first, lower index first among equals
+        for (int b = 0; b < p; ++b) rank += th[b] > th[a] || (th[b] == th[a] && b < a);
+        if (rank >= e0 && rank < e0 + ne) order[rank - e0] = a;
     }
     __syncthreads();
-    const int col = order[e];
-    for (int j = threadIdx.x; j < p; j += 256) w[j] = Wt[static_cast<size_t>(col) * p + j];
+    for (int x = tid; x < kRitzE * p; x += 256) {
+        const int e = x / p, j = x - (x / p) * p;
+        w[e * kMaxP + j] = e < ne ? Wt[static_cast<size_t>(order[e]) * p + j] : 0.0;
+    }
+    if (blockIdx.x == 0 && tid < ne && eigvals) eigvals[e0 + tid] = static_cast<float>(th[order[tid]]);
     __syncthreads();
-    if (blockIdx.x == 0 && threadIdx.x == 0 && eigvals) eigvals[e] = static_cast<float>(theta[col]);
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    double s = 0.0;
-    for (int j = 0; j < p; ++j) s = fma(static_cast<double>(Q[qidx(i, j, pp)]), w[j], s);
-    V[static_cast<size_t>(e) * n + i] = static_cast<float>(s);
+    const int quad = blockIdx.x * 256 + tid;   // rows 4 quad .. 4 quad + 3
+    if (4 * quad >= n) return;
+    const f32x4 *Q4 = reinterpret_cast<const f32x4 *>(Q) + static_cast<size_t>(quad) * pp;
+    double acc[4][kRitzE];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int e = 0; e < kRitzE; ++e) acc[r][e] = 0.0;
+    for (int j = 0; j < p; ++j) {
+        const f32x4 q = Q4[j];
+#pragma unroll
+        for (int e = 0; e < kRitzE; ++e) {
+            const double we = w[e * kMaxP + j];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[r][e] = fma(static_cast<double>(q[r]), we, acc[r][e]);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int i = 4 * quad + r;
+        if (i >= n) break;
+#pragma unroll
+        for (int e = 0; e < kRitzE; ++e)
+            if (e < ne) V[static_cast<size_t>(e0 + e) * n + i] = static_cast<float>(acc[r][e]);
+    }
 }
 
 // One workgroup per Ritz vector: the index of its largest magnitude (lowest
@@ -1204,6 +1416,8 @@ namespace {
 struct PcaLayout {
     float *Q, *Z, *Zs;
     double *part, *RinvT, *Wt, *theta;
+    double2 *rot;   // the Jacobi rotations, [round][m/2]
+    int *rounds;
 };
 
 inline int pca_p(int n, int k) {
@@ -1213,6 +1427,10 @@ inline int pca_p(int n, int k) {
 inline int pca_pp(int n, int k) { return (pca_p(n, k) + 15) / 16 * 16; }
 inline int gram_chunks(int n) { return (round4(n) + kGramRows - 1) / kGramRows; }
 inline size_t block_floats(int n, int pp) { return static_cast<size_t>(round4(n)) * pp; }
+inline size_t rot_bytes(int p) {
+    const int m = p + (p & 1);
+    return sizeof(double2) * static_cast<size_t>(kJacobiSweeps) * (m - 1) * (m / 2);
+}
 
 // Z = C Q: row blocks of 16 MR rows per workgroup, and the columns of C cut
 // into splits of kr (a multiple of 64, at least 512 unless n is smaller) so
@@ -1245,6 +1463,10 @@ PcaLayout pca_layout(void *ws, int n, int k) {
     L.Wt = reinterpret_cast<double *>(w);
     w += align256(sizeof(double) * static_cast<size_t>(p) * p);
     L.theta = reinterpret_cast<double *>(w);
+    w += align256(sizeof(double) * p);
+    L.rot = reinterpret_cast<double2 *>(w);
+    w += align256(rot_bytes(p));
+    L.rounds = reinterpret_cast<int *>(w);
     return L;
 }
 
@@ -1253,7 +1475,10 @@ void launch_cq_nb(const float *C, int n, const float *Q, float *Zs, hipStream_t 
     constexpr int MR = NB <= 4 ? 4 : 2;
     const int kr = cq_kr(n, 16 * NB);
     const dim3 grid(static_cast<unsigned>((n + 16 * MR - 1) / (16 * MR)), static_cast<unsigned>((n + kr - 1) / kr));
-    hipLaunchKernelGGL((k_cq_part<NB, MR>), grid, dim3(256), 0, s, C, n, Q, kr, Zs);
+    if constexpr (NB <= 4)
+        hipLaunchKernelGGL((k_cq_dma<NB, MR>), grid, dim3(256), 0, s, C, n, Q, kr, Zs);
+    else
+        hipLaunchKernelGGL((k_cq_regs<NB, MR>), grid, dim3(256), 0, s, C, n, Q, kr, Zs);
 }
 
 hipError_t launch_cq(const PcaLayout &L, const float *C, int n, int pp, const float *Q, float *Z, hipStream_t s) {
@@ -1277,11 +1502,19 @@ hipError_t launch_cq(const PcaLayout &L, const float *C, int n, int pp, const fl
     return hipGetLastError();
 }
 
+// Sums the Gram partials on the chip when there are many of them (p > 64);
+// returns the chunk count left for the one-workgroup kernel that follows.
+int sum_parts(double *part, int chunks, int p, hipStream_t s) {
+    if (p <= 64 || chunks == 1) return chunks;
+    hipLaunchKernelGGL(k_sum_parts, dim3(static_cast<unsigned>((p * p + 255) / 256)), dim3(256), 0, s, part, chunks,
+                       p * p);
+    return 1;
+}
+
 // Q = orthonormalised Z (shifted CholQR)
 void cholqr(const PcaLayout &L, int n, int p, int pp, const float *Z, float *Q, hipStream_t s) {
-    const int chunks = gram_chunks(n);
     launch_gram(Z, Z, n, p, pp, L.part, s);
-    launch_chol_inv(L.part, chunks, p, L.RinvT, s);
+    launch_chol_inv(L.part, sum_parts(L.part, gram_chunks(n), p, s), p, L.RinvT, s);
     const unsigned g = static_cast<unsigned>((static_cast<int64_t>(block_floats(n, pp) / 4) + 255) / 256);
     hipLaunchKernelGGL(k_apply_rinv, dim3(g), dim3(256), 0, s, Z, n, p, pp, L.RinvT, Q);
 }
@@ -1294,7 +1527,8 @@ size_t pca_ws_bytes(int n, int k) {
     return 2 * align256(sizeof(float) * block_floats(n, pp)) +
            (sp > 1 ? align256(sizeof(float) * block_floats(n, pp) * sp) : 0) +
            align256(sizeof(double) * static_cast<size_t>(gram_chunks(n)) * p * p) +
-           2 * align256(sizeof(double) * static_cast<size_t>(p) * p) + align256(sizeof(double) * p);
+           2 * align256(sizeof(double) * static_cast<size_t>(p) * p) + align256(sizeof(double) * p) +
+           align256(rot_bytes(p)) + align256(sizeof(int));
 }
 
 hipError_t launch_pca_topk(const float *C, int n, int k, int iters, void *P, bool bf16_out, int64_t ld_p,
@@ -1313,13 +1547,17 @@ hipError_t launch_pca_topk(const float *C, int n, int k, int iters, void *P, boo
     cholqr(L, n, p, pp, L.Q, L.Z, s);
     hipError_t e = launch_cq(L, C, n, pp, L.Z, L.Q, s);
     if (e != hipSuccess) return e;
-    const int chunks = gram_chunks(n);
     launch_gram(L.Z, L.Q, n, p, pp, L.part, s);
-    if (p <= 64) hipLaunchKernelGGL(k_jacobi_lds, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
-    else hipLaunchKernelGGL(k_jacobi, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.Wt, L.theta);
+    const int chunks = sum_parts(L.part, gram_chunks(n), p, s);
+    if (p <= 64)
+        hipLaunchKernelGGL(k_jacobi_rot<64>, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.rot, L.rounds, L.theta);
+    else
+        hipLaunchKernelGGL(k_jacobi_rot<kMaxP>, dim3(1), dim3(256), 0, s, L.part, chunks, p, L.rot, L.rounds,
+                           L.theta);
+    hipLaunchKernelGGL(k_jacobi_replay, dim3(static_cast<unsigned>(p)), dim3(kWave), 0, s, L.rot, L.rounds, p, L.Wt);
     // the Ritz vectors [k][n] overwrite Q (k <= pp)
-    hipLaunchKernelGGL(k_ritz, dim3(static_cast<unsigned>((n + 255) / 256), static_cast<unsigned>(k)), dim3(256), 0,
-                       s, L.Z, n, p, pp, k, L.Wt, L.theta, L.Q, eigvals);
+    const dim3 ritz_grid(static_cast<unsigned>((n + 1023) / 1024), static_cast<unsigned>((k + kRitzE - 1) / kRitzE));
+    hipLaunchKernelGGL(k_ritz, ritz_grid, dim3(256), 0, s, L.Z, n, p, pp, k, L.Wt, L.theta, L.Q, eigvals);
     if (bf16_out)
         hipLaunchKernelGGL(k_pca_out<bf16_bits>, dim3(static_cast<unsigned>(k)), dim3(256), 0, s, L.Q, n,
                            static_cast<bf16_bits *>(P), ld_p);

@@ -186,6 +186,10 @@ PCA_CASES = {
     "n20_k12_full_width": (20, 12, 0.7, "f32"),
     "n1000_k64_widest": (1000, 64, 0.95, "f32"),
     "n17_k1": (17, 1, 0.6, "f32"),
+    # two column splits, n not a multiple of 4 (the last 4-column chunk of a
+    # row runs past its end), subspace widths 48 and 80
+    "n1101_k24_ragged_two_splits": (1101, 24, 0.9, "f32"),
+    "n1500_k40_two_splits": (1500, 40, 0.95, "f32"),
 }
 
 
