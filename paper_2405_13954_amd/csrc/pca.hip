@@ -1079,29 +1079,49 @@ void launch_chol_inv(const double *part, int chunks, int p, double *RinvT, hipSt
     else hipLaunchKernelGGL(k_chol_inv_wide, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
 }
 
-// Q = Z R^{-1} in row quads: a thread forms one column j of four rows, each
-// entry sum over m <= j of Z[i][m] R^{-1}[m][j] in fp64 (fp32 result), with
-// R^{-1} given transposed (column j is a contiguous row); the padding
-// columns j >= p are zero.
+// Q = Z R^{-1} in row quads.  Lane = one row quad, wave = four consecutive
+// columns j0 .. j0 + 3: entry (i, j) = sum over m <= j of Z[i][m]
+// R^{-1}[m][j] in fp64 (fp32 result), m ascending.  R^{-1} comes transposed
+// (column j a contiguous row, zero past the diagonal), so the four columns
+// share one loop to j0 + 3, the entries past a column's diagonal adding exact
+// zeros; its entries are the same across the wave (scalar loads), and each
+// 128-bit load of Z feeds 16 FMAs.  The padding columns j >= p are zero.
 __global__ __launch_bounds__(256) void k_apply_rinv(const float *__restrict__ Z, int n, int p, int pp,
                                                     const double *__restrict__ RinvT, float *__restrict__ Q) {
-    const int64_t v = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;   // 128-bit element of Q
-    if (v >= static_cast<int64_t>(round4(n) / 4) * pp) return;
-    const int64_t quad = v / pp;
-    const int j = static_cast<int>(v - quad * pp);
-    const f32x4 *Z4 = reinterpret_cast<const f32x4 *>(Z) + quad * pp;
-    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-    if (j < p)
-        for (int m = 0; m <= j; ++m) {
+    const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    const int j0 = 4 * (4 * static_cast<int>(blockIdx.y) + wave);
+    const int64_t nq = round4(n) / 4;
+    const int64_t quad = static_cast<int64_t>(blockIdx.x) * kWave + lane;
+    const bool qin = quad < nq;
+    double acc[4][4];   // [column j0 + u][row 4 quad + r]
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[u][r] = 0.0;
+    if (j0 < p) {
+        const f32x4 *Z4 = reinterpret_cast<const f32x4 *>(Z) + (qin ? quad : 0) * pp;
+        const int mend = min(j0 + 4, p);
+        const double *R[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) R[u] = RinvT + static_cast<size_t>(min(j0 + u, p - 1)) * p;
+#pragma unroll 4
+        for (int m = 0; m < mend; ++m) {
             const f32x4 z = Z4[m];
-            const double r = RinvT[static_cast<size_t>(j) * p + m];
-            s0 = fma(static_cast<double>(z[0]), r, s0);
-            s1 = fma(static_cast<double>(z[1]), r, s1);
-            s2 = fma(static_cast<double>(z[2]), r, s2);
-            s3 = fma(static_cast<double>(z[3]), r, s3);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const double rv = j0 + u < p ? R[u][m] : 0.0;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[u][r] = fma(static_cast<double>(z[r]), rv, acc[u][r]);
+            }
         }
-    reinterpret_cast<f32x4 *>(Q)[v] =
-        f32x4{static_cast<float>(s0), static_cast<float>(s1), static_cast<float>(s2), static_cast<float>(s3)};
+    }
+    if (!qin) return;
+    f32x4 *Q4 = reinterpret_cast<f32x4 *>(Q) + quad * pp + j0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        Q4[u] = f32x4{static_cast<float>(acc[u][0]), static_cast<float>(acc[u][1]), static_cast<float>(acc[u][2]),
+                      static_cast<float>(acc[u][3])};
 }
 
 // One workgroup: T = (sum of the chunk partials of Q^T Z), symmetrised, is
@@ -1515,8 +1535,8 @@ int sum_parts(double *part, int chunks, int p, hipStream_t s) {
 void cholqr(const PcaLayout &L, int n, int p, int pp, const float *Z, float *Q, hipStream_t s) {
     launch_gram(Z, Z, n, p, pp, L.part, s);
     launch_chol_inv(L.part, sum_parts(L.part, gram_chunks(n), p, s), p, L.RinvT, s);
-    const unsigned g = static_cast<unsigned>((static_cast<int64_t>(block_floats(n, pp) / 4) + 255) / 256);
-    hipLaunchKernelGGL(k_apply_rinv, dim3(g), dim3(256), 0, s, Z, n, p, pp, L.RinvT, Q);
+    const dim3 grid(static_cast<unsigned>((round4(n) / 4 + kWave - 1) / kWave), static_cast<unsigned>(pp / 16));
+    hipLaunchKernelGGL(k_apply_rinv, grid, dim3(256), 0, s, Z, n, p, pp, L.RinvT, Q);
 }
 
 }  // namespace
