@@ -45,10 +45,11 @@
 //     2048 workgroups; their partials are summed in split order.
 //  3. k_gram_part: fp64 partial sums of X^T Y over 256-row chunks (X^T X for
 //     the orthonormalisation, Z^T Q for Rayleigh-Ritz), fixed order.
-//  4. k_chol_inv_reg / k_chol_inv_wide (one workgroup): the chunk sums, a
-//     shifted Cholesky Z^T Z + eps tr/p I = R^T R and R^{-1} in fp64 (p <= 64:
-//     one wave, a row per lane in registers; wider: a column per pair of
-//     threads in registers, one barrier per step).
+//  4. k_chol_inv_cols (one workgroup): the chunk sums (for p > 64 summed on
+//     the chip first by k_sum_parts), a shifted Cholesky Z^T Z + eps tr/p I =
+//     R^T R and R^{-1} in fp64, columns in registers and each step's row
+//     broadcast through LDS (p <= 64: one wave; wider: four waves, one
+//     barrier per step).
 //  5. k_apply_rinv: Q = Z R^{-1} (fp64 arithmetic, fp32 result).
 //  6. k_jacobi_rot (one workgroup): T in LDS, round-robin parallel cyclic
 //     Jacobi (m/2 disjoint rotations per round, each round one pass of 2 x 2
@@ -870,73 +871,6 @@ __global__ __launch_bounds__(256) void k_sum_parts(double *__restrict__ part, in
     part[e] = s;
 }
 
-// p <= PM (32 or 64).  One workgroup sums the partials into G; wave 0 then,
-// in registers, forms the shifted Cholesky G + eps (tr G / p) I = R^T R
-// (R upper) and R^{-1}, lane r holding row r of the matrix padded to PM
-// with the identity (whose factor and inverse are the identity).  Step j of
-// the right-looking factorisation takes row j from lane j (readlanes) and,
-// the trailing matrix being kept whole and symmetric, each lane's own entry
-// of column j from its own row.  Then lane r solves x R = e_r for row r of
-// X = R^{-1} column by column, x_c = (delta_rc - sum over m < c of
-// x_m R_mc) / R_cc, with column c of R read from lanes m <= c; x_c replaces
-// the row's entry c, whose last reader was that column.  All in fp64.
-// Writes R^{-T} [p][p] (R^{-1} transposed: zero above the diagonal).
-template <int PM>
-__global__ __launch_bounds__(256) void k_chol_inv_reg(const double *__restrict__ part, int chunks, int p,
-                                                      double *__restrict__ RinvT) {
-    __shared__ double A[PM * PM];
-    const int tid = threadIdx.x, np = p * p;
-    sum_partials(part, chunks, np, A, tid);
-    __syncthreads();
-    if (tid >= kWave) return;
-    const int r = tid;                // the lane's row (lanes >= PM carry an unused identity row)
-    double a[PM];
-    const int rr = r < p ? r : p - 1;   // clamped: every lane loads, padding is selected afterwards
-#pragma unroll
-    for (int c = 0; c < PM; ++c) {
-        const double g = A[rr * p + (c < p ? c : p - 1)];
-        a[c] = r < p && c < p ? g : r == c ? 1.0 : 0.0;
-    }
-    double tr = r < p ? A[r * p + r] : 0.0;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) tr += __shfl_xor(tr, o, kWave);   // the same butterfly in every lane
-    const double shift = 1e-12 * (tr > 0.0 ? tr / p : 1.0);
-#pragma unroll
-    for (int c = 0; c < PM; ++c)
-        if (c == r && r < p) a[c] += shift;
-#pragma unroll
-    for (int j = 0; j < PM; ++j) {
-        const double d = readlane_d(a[j], j);
-        const double rjj = d > 0.0 ? sqrt(d) : 1.0;   // a non-positive pivot (cannot follow the shift) keeps R invertible
-        const double inv = 1.0 / rjj;
-        const double rjr = a[j] * inv;                // R_jr (lanes r > j)
-#pragma unroll
-        for (int c = j + 1; c < PM; ++c) {
-            const double rjc = readlane_d(a[c], j) * inv;   // R_jc
-            const double upd = fma(-rjr, rjc, a[c]);
-            a[c] = r > j ? upd : r == j ? rjc : a[c];
-            if ((c - j) % 8 == 0) __builtin_amdgcn_sched_barrier(0);   // at most 8 readlane pairs live
-        }
-        a[j] = r == j ? rjj : a[j];
-        __builtin_amdgcn_sched_barrier(0);   // a step's readlanes stay in the step (scalar registers)
-    }
-#pragma unroll
-    for (int c = 0; c < PM; ++c) {
-        double s = c == r ? 1.0 : 0.0;
-#pragma unroll
-        for (int m = 0; m < c; ++m) {
-            s = fma(-a[m], readlane_d(a[c], m), s);
-            if (m % 8 == 7) __builtin_amdgcn_sched_barrier(0);
-        }
-        a[c] = s / readlane_d(a[c], c);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    // R^{-T}: lane r's row of R^{-1} is column r, so each store is coalesced
-#pragma unroll
-    for (int c = 0; c < PM; ++c)
-        if (r < p && c < p) RinvT[c * p + r] = a[c];
-}
-
 // f(std::integral_constant<int, I>{}) for I = 0 .. N - 1, expanded by the
 // front end: a register array indexed by I stays in registers however long
 // the body is (the loop unroller gives up on long bodies).
@@ -949,17 +883,20 @@ __device__ __forceinline__ void static_for(F &&f) {
     static_for_seq(f, std::make_integer_sequence<int, N>{});
 }
 
-// a[i] -= v[i] f for i < 64, v 64 consecutive doubles in LDS (16-byte
+// a[i] -= v[i] f for i < RPT, v RPT consecutive doubles in LDS (16-byte
 // aligned): read 16 at a time, one group ahead of its FMAs, so that at most
 // two groups are live next to a; a is in registers on return.
-__device__ __forceinline__ void axpy64_lds(double (&a)[64], const double *v, double f) {
+template <int RPT>
+__device__ __forceinline__ void axpy_lds(double (&a)[RPT], const double *v, double f) {
+    static_assert(RPT % 16 == 0, "groups of 16");
+    constexpr int G = RPT / 16;
     const double2 *v2 = reinterpret_cast<const double2 *>(v);
     double2 cur[8], nxt[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) cur[k] = v2[k];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        if (g < 3) {
+    for (int g = 0; g < G; ++g) {
+        if (g + 1 < G) {
 #pragma unroll
             for (int k = 0; k < 8; ++k) nxt[k] = v2[8 * (g + 1) + k];
         }
@@ -976,107 +913,115 @@ __device__ __forceinline__ void axpy64_lds(double (&a)[64], const double *v, dou
     // sinks each step's FMAs towards the step that reads the row, keeping
     // every loaded value live until then
 #pragma unroll
-    for (int i = 0; i < 64; ++i) asm volatile("" : "+v"(a[i]));
+    for (int i = 0; i < RPT; ++i) asm volatile("" : "+v"(a[i]));
 }
 
-// 64 < p <= 128: one workgroup.  Thread (c, h), c = 64 (wave & 1) + lane and
-// h = wave >> 1, keeps rows 64 h .. 64 h + 63 of column c of the matrix in
-// registers (padded to 128 with the identity, whose factor and inverse are
-// the identity).  The shifted Cholesky G + eps (tr G / p) I = R^T R runs in
-// outer-product form: step j passes row j through LDS (zeros left of the
-// diagonal) and every thread updates its entries below it, A_rc -= A_jr
-// (A_jc / A_jj), one barrier per step (two row buffers alternate); each
-// step is the same 64 FMAs in every thread, the zeros leaving the rows above
-// it unchanged.  Row r of R is then row r of
-// the updated matrix over sqrt(A_rr) (a non-positive pivot, which cannot
-// follow the shift, is taken as 1).  X = R^{-1} solves R X = I by back
-// substitution in the same form with R in LDS: steps j = 127 .. 0 finish
-// row j of X, X_jc = B_jc / R_jj, pass it through LDS and update the rows
-// above it, B_rc -= R_rj X_jc.  All fp64.  Writes R^{-T} [p][p] (R^{-1}
-// transposed: zero above the diagonal), through LDS so that the stores are
-// coalesced.
-__global__ __launch_bounds__(256) void k_chol_inv_wide(const double *__restrict__ part, int chunks, int p,
+// One workgroup; the matrix is padded to PM (32, 64 or 128) with the
+// identity, whose factor and inverse are the identity.  Thread (c, h) keeps
+// rows RPT h .. RPT h + RPT - 1 of column c in registers (RPT = min(PM, 64)):
+// for PM <= 64 one wave, lane c holding the whole column; for PM = 128 four
+// waves, c = 64 (wave & 1) + lane and h = wave >> 1.  The shifted Cholesky
+// G + eps (tr G / p) I = R^T R runs in outer-product form: step j passes row
+// j through LDS (zeros left of the diagonal) and every thread updates its
+// entries below it, A_rc -= A_jr (A_jc / A_jj); each step is the same RPT
+// FMAs in every thread, the zeros leaving the rows above it unchanged.  Row
+// r of R is then row r of the updated matrix over sqrt(A_rr) (a non-positive
+// pivot, which cannot follow the shift, is taken as 1).  X = R^{-1} solves
+// R X = I by back substitution in the same form with R in LDS: steps
+// j = PM - 1 .. 0 finish row j of X, X_jc = B_jc / R_jj, pass it through LDS
+// and update the rows above it, B_rc -= R_rj X_jc.  With four waves a
+// barrier follows each step's row (two row buffers alternate); one wave
+// needs none, its LDS operations taking effect in program order.  All fp64.
+// Writes R^{-T} [p][p] (R^{-1} transposed: zero above the diagonal),
+// through LDS so that the stores are coalesced.
+template <int PM>
+__global__ __launch_bounds__(256) void k_chol_inv_cols(const double *__restrict__ part, int chunks, int p,
                                                        double *__restrict__ RinvT) {
-    constexpr int PM = kMaxP;
+    constexpr int RPT = PM < 64 ? PM : 64;
+    constexpr int NW = PM <= 64 ? 1 : 4;   // waves that factorise
     constexpr int RS = PM + 2;   // stride of the column-major copies of R and R^{-T} (even: 16-byte pairs)
     __shared__ __attribute__((aligned(16))) double A[PM * RS];   // G [p][p]; then R by columns; then R^{-T} by rows
     __shared__ __attribute__((aligned(16))) double buf[2][PM];
     __shared__ double rdiag[PM];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int c = 64 * (wave & 1) + lane;
-    const int h = wave >> 1;
+    const int c = NW == 4 ? 64 * (wave & 1) + lane : lane;
+    const int h = NW == 4 ? wave >> 1 : 0;
+    const bool col = c < PM;   // lanes past PM (PM = 32) hold no column
     sum_partials(part, chunks, p * p, A, tid);
     __syncthreads();
+    if (wave >= NW) return;
+    auto sync = [] {
+        if constexpr (NW > 1) __syncthreads();
+    };
     double tr = 0.0;
     for (int r = 0; r < p; ++r) tr += A[r * p + r];   // the same order in every thread
     const double shift = 1e-12 * (tr > 0.0 ? tr / p : 1.0);
-    double a[64];
+    double a[RPT];
 #pragma unroll
-    for (int i = 0; i < 64; ++i) {
-        const int r = 64 * h + i;
+    for (int i = 0; i < RPT; ++i) {
+        const int r = RPT * h + i;
         const double g = A[min(r, p - 1) * p + min(c, p - 1)];   // clamped: padding is selected below
         a[i] = r < p && c < p ? (r == c ? g + shift : g) : r == c ? 1.0 : 0.0;
     }
-    __syncthreads();   // G is overwritten below
-    {
-        static_for<PM>([&](auto step) __attribute__((always_inline)) {
-            constexpr int j = decltype(step)::value;
-            constexpr int hj = j / 64, jj = j % 64;
-            double *row = buf[jj & 1];
-            if (h == hj) row[c] = c >= j ? a[jj] : 0.0;   // zeros left of the diagonal: no update there
-            __syncthreads();
-            const double d = row[j];
-            const double e = d > 0.0 ? d : 1.0;
-            if (tid == 0) rdiag[j] = e;
-            const double f = c > j ? row[c] / e : 0.0;
-            const double keep = a[jj];   // row j itself is final
-            axpy64_lds(a, row + 64 * h, f);
-            a[jj] = h == hj ? keep : a[jj];
-        });
-    }
-    __syncthreads();   // the pivots are complete
+    if constexpr (NW > 1) __syncthreads();   // G is overwritten below
+    else __builtin_amdgcn_wave_barrier();
+    static_for<PM>([&](auto step) __attribute__((always_inline)) {
+        constexpr int j = decltype(step)::value;
+        constexpr int hj = j / RPT, jj = j % RPT;
+        double *row = buf[j & 1];
+        if (h == hj && col) row[c] = c >= j ? a[jj] : 0.0;   // zeros left of the diagonal: no update there
+        sync();
+        const double d = row[j];
+        const double e = d > 0.0 ? d : 1.0;
+        if (tid == 0) rdiag[j] = e;
+        const double f = col && c > j ? row[c] / e : 0.0;
+        const double keep = a[jj];   // row j itself is final
+        axpy_lds<RPT>(a, row + RPT * h, f);
+        a[jj] = h == hj ? keep : a[jj];
+    });
+    sync();   // the pivots are complete
     if (tid < PM) rdiag[tid] = sqrt(rdiag[tid]);   // R_rr
-    __syncthreads();
+    sync();
 #pragma unroll
-    for (int i = 0; i < 64; ++i) {
-        const int r = 64 * h + i;
+    for (int i = 0; i < RPT; ++i) {
+        const int r = RPT * h + i;
         const double rr = rdiag[r];
-        A[c * RS + r] = r < c ? a[i] / rr : r == c ? rr : 0.0;   // R_rc, column c contiguous
+        if (col) A[c * RS + r] = r < c ? a[i] / rr : r == c ? rr : 0.0;   // R_rc, column c contiguous
         a[i] = r == c ? 1.0 : 0.0;
     }
-    __syncthreads();
-    {
-        static_for<PM>([&](auto step) __attribute__((always_inline)) {
-            constexpr int j = PM - 1 - decltype(step)::value;
-            constexpr int hj = j / 64, jj = j % 64;
-            double *row = buf[jj & 1];
-            const double *Rj = A + j * RS;   // column j of R
-            if (h == hj) {
-                a[jj] = a[jj] / Rj[j];
-                row[c] = a[jj];
-            }
-            __syncthreads();
-            const double x = row[c];
-            const double keep = a[jj];   // row j of X is final; R is zero below its diagonal
-            axpy64_lds(a, Rj + 64 * h, x);
-            a[jj] = h == hj ? keep : a[jj];
-        });
-    }
-    __syncthreads();   // every read of R is done
+    sync();
+    static_for<PM>([&](auto step) __attribute__((always_inline)) {
+        constexpr int j = PM - 1 - decltype(step)::value;
+        constexpr int hj = j / RPT, jj = j % RPT;
+        double *row = buf[j & 1];
+        const double *Rj = A + j * RS;   // column j of R
+        if (h == hj) {
+            a[jj] = a[jj] / Rj[j];
+            if (col) row[c] = a[jj];
+        }
+        sync();
+        const double x = col ? row[c] : 0.0;
+        const double keep = a[jj];   // row j of X is final; R is zero below its diagonal
+        axpy_lds<RPT>(a, Rj + RPT * h, x);
+        a[jj] = h == hj ? keep : a[jj];
+    });
+    sync();   // every read of R is done
+    if (col) {
 #pragma unroll
-    for (int i = 0; i < 64; ++i) A[c * RS + 64 * h + i] = a[i];   // row c of R^{-T} is column c of R^{-1}
-    __syncthreads();
-    for (int e = tid; e < p * p; e += 256) {
+        for (int i = 0; i < RPT; ++i) A[c * RS + RPT * h + i] = a[i];   // row c of R^{-T} is column c of R^{-1}
+    }
+    sync();
+    for (int e = tid; e < p * p; e += kWave * NW) {
         const int r = e / p;
         RinvT[e] = A[r * RS + (e - r * p)];
     }
 }
 
 void launch_chol_inv(const double *part, int chunks, int p, double *RinvT, hipStream_t s) {
-    if (p <= 32) hipLaunchKernelGGL(k_chol_inv_reg<32>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
-    else if (p <= 64) hipLaunchKernelGGL(k_chol_inv_reg<64>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
-    else hipLaunchKernelGGL(k_chol_inv_wide, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
+    if (p <= 32) hipLaunchKernelGGL(k_chol_inv_cols<32>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
+    else if (p <= 64) hipLaunchKernelGGL(k_chol_inv_cols<64>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
+    else hipLaunchKernelGGL(k_chol_inv_cols<kMaxP>, dim3(1), dim3(256), 0, s, part, chunks, p, RinvT);
 }
 
 // Q = Z R^{-1} in row quads.  Lane = one row quad, wave = four consecutive
