@@ -190,6 +190,8 @@ PCA_CASES = {
     # row runs past its end), subspace widths 48 and 80
     "n1101_k24_ragged_two_splits": (1101, 24, 0.9, "f32"),
     "n1500_k40_two_splits": (1500, 40, 0.95, "f32"),
+    # odd subspace width p = n = 21: the Jacobi schedule pairs one index with padding
+    "n21_k12_odd_width": (21, 12, 0.7, "f32"),
 }
 
 
