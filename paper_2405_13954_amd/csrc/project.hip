@@ -920,17 +920,34 @@ __device__ __forceinline__ void wait_copies_below() {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(kCount) : "memory");
 }
 
+// Paired units in the tile-group kernel up to KT = 4 (at KT = 8 the kept x
+// side would be 128 more registers per lane).
+constexpr int kMaxPairedKT = 4;
 template <int KT>
+constexpr bool kTilePairs = KT <= kMaxPairedKT;
+
+// What a tile-group item does with each wave's projection of its tile:
+// write it as the chunk partial (the tile-sum kernel reads it), keep it in
+// registers (the x side of a paired unit), or form the tile's sum from it
+// (the dy side) and the kept x side.
+enum TileFold { kFoldPart, kFoldKeepX, kFoldTileSum };
+
+template <int KT, TileFold F>
 __device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int count, int groups, int lane,
-                                                int wave, uint32_t ring_addr, const uint8_t *ring) {
+                                                int wave, uint32_t ring_addr, const uint8_t *ring,
+                                                f32x4 (&xk)[MB][KT]) {
     using Sh = TileDma<KT>;
     constexpr int NS = Sh::kStages;
-    const int rank = item / groups;             // position of the work slot in processing order
-    const int grp = item - rank * groups;       // group of listed tiles
+    // paired: item 2 u is unit u's x side, item 2 u + 1 its dy side (the layer's
+    // x slot and the slot after it, one chunk each)
+    const int unit = F == kFoldPart ? item : item >> 1;
+    const int side = F == kFoldPart ? 0 : item & 1;
+    const int rank = unit / groups;             // position of the work slot (paired: layer) in processing order
+    const int grp = unit - rank * groups;       // group of listed tiles
     int gslot = rank, l = 0;
     if (a.ordered) {
         const uint32_t e = reinterpret_cast<const uint32_t *>(a.slot_order)[rank >> 1] >> (16 * (rank & 1));
-        gslot = e & 0x3ff;
+        gslot = (e & 0x3ff) + side;
         l = (e >> 10) & 0x3f;
     } else {
         while (l + 1 < a.n_layers && gslot >= a.layer[l + 1].slot_begin) ++l;
@@ -1032,7 +1049,8 @@ __device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int
     }
     // the copies past the chunk (out of range: zeros) are still in flight
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (has) {
+    if (!has) return;
+    if constexpr (F == kFoldPart) {
         const int pslot = xside ? c : L.c_in + c;
         f32x4 *dst = reinterpret_cast<f32x4 *>(part_of(a.part, L) +
                                                (static_cast<size_t>(bt) * (L.c_in + L.c_out) + pslot) *
@@ -1041,6 +1059,30 @@ __device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int
         for (int m = 0; m < MB; ++m)
 #pragma unroll
             for (int jj = 0; jj < KT; ++jj) dst[(m * KT + jj) * kWave] = acc[m][jj];
+    } else if constexpr (F == kFoldKeepX) {
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int jj = 0; jj < KT; ++jj) xk[m][jj] = acc[m][jj];
+    } else {
+        // The tile's sum over tokens of dy'_t x'_t^T, block (jo, ji) as the
+        // tile-sum kernel forms it from the partials (which hold x' and dy' in
+        // this lane layout): the same fp32 16x16x4 MFMAs in the same order,
+        // on the same operands (0 + v, as its sum over one chunk gives).
+        const int per_layer = a.B * a.tpe;
+        float *gdst = a.gpart + static_cast<size_t>(l * per_layer + bt) * (16 * KT * 16 * KT) + lane;
+#pragma unroll
+        for (int jo = 0; jo < KT; ++jo)
+#pragma unroll
+            for (int ji = 0; ji < KT; ++ji) {
+                f32x4 g = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int m = 0; m < MB; ++m)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) g = mfma16_f32(0.f + acc[m][jo][r], 0.f + xk[m][ji][r], g);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) gdst[(jo * KT + ji) * 256 + 64 * r] = g[r];
+            }
     }
 }
 
@@ -1048,7 +1090,7 @@ __device__ __forceinline__ void tile_group_item(const ProjArgs &a, int item, int
 // from the work counter, claimed ahead except in the last rounds.  The
 // barrier that hands a claim to the workgroup also keeps the next item's
 // first copies from overwriting a stage another wave is still reading.
-template <int KT>
+template <int KT, bool kPaired>
 __global__ __launch_bounds__(NT, 1) void k_project_tiles(ProjArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t ring[TileDma<KT>::kRing];
     __shared__ int next;
@@ -1058,15 +1100,24 @@ __global__ __launch_bounds__(NT, 1) void k_project_tiles(ProjArgs a) {
     const int groups = (count + NW - 1) / NW;
     const int items = groups * a.slots;
     const uint32_t ring_addr = lds_addr(ring);
-    int item = blockIdx.x;
-    while (item < items) {
-        const bool ahead = item + kAheadRounds * static_cast<int>(gridDim.x) < items;
+    f32x4 xk[MB][KT];   // paired: this wave's x side of the unit's tile
+    // paired: units of two items (a tile group's x side, then its dy side)
+    const int units = kPaired ? items / 2 : items;
+    int u = blockIdx.x;
+    while (u < units) {
+        const bool ahead = u + kAheadRounds * static_cast<int>(gridDim.x) < units;
         int claim = 0;
         if (ahead && tid == 0) claim = atomicAdd(a.work, 1);
-        tile_group_item<KT>(a, item, count, groups, lane, wave, ring_addr, ring);
+        if constexpr (kPaired) {
+            tile_group_item<KT, kFoldKeepX>(a, 2 * u, count, groups, lane, wave, ring_addr, ring, xk);
+            __syncthreads();   // the dy side's first copies refill stages the x side read
+            tile_group_item<KT, kFoldTileSum>(a, 2 * u + 1, count, groups, lane, wave, ring_addr, ring, xk);
+        } else {
+            tile_group_item<KT, kFoldPart>(a, u, count, groups, lane, wave, ring_addr, ring, xk);
+        }
         if (tid == 0) next = static_cast<int>(gridDim.x) + (ahead ? claim : atomicAdd(a.work, 1));
         __syncthreads();
-        item = __builtin_amdgcn_readfirstlane(next);
+        u = __builtin_amdgcn_readfirstlane(next);
         __syncthreads();   // every wave has read `next` before it is written again
     }
 }
@@ -1399,8 +1450,16 @@ void launch_chunks_s(const ProjArgs &a, int max_items, hipStream_t s) {
 
 template <int KT>
 void launch_tiles(const ProjArgs &a, int max_items, hipStream_t s) {
-    const int cap = resident_groups<k_project_tiles<KT>>();
-    hipLaunchKernelGGL((k_project_tiles<KT>), dim3(max_items < cap ? max_items : cap), dim3(NT), 0, s, a);
+    if constexpr (kTilePairs<KT>) {
+        if (a.paired) {   // a unit is two items
+            const int cap = resident_groups<k_project_tiles<KT, true>>();
+            const int units = max_items / 2;
+            hipLaunchKernelGGL((k_project_tiles<KT, true>), dim3(units < cap ? units : cap), dim3(NT), 0, s, a);
+            return;
+        }
+    }
+    const int cap = resident_groups<k_project_tiles<KT, false>>();
+    hipLaunchKernelGGL((k_project_tiles<KT, false>), dim3(max_items < cap ? max_items : cap), dim3(NT), 0, s, a);
 }
 
 void launch_stream(const ProjArgs &a, int max_items, hipStream_t s) {
@@ -1464,10 +1523,11 @@ hipError_t launch_project(const ProjGroup &grp, bool bf16_in, int B, int T, cons
     // Slots widest first (stable), so that the last items handed out are the
     // narrow ones and the tail after the last claim is short.
     a.ordered = a.slots <= kMaxSlots;
-    // Paired: the stream kernel (bf16, k <= 16, no shared inputs) with one chunk per
-    // layer side, so a workgroup that streams a tile's x side and then its dy side
-    // forms the tile's sum itself; pairs widest first.
-    a.paired = bf16_in && KT == 1 && smax == 1 && a.ordered;
+    // Paired: the stream kernel (bf16, k <= 16) or the tile-group kernel (bf16,
+    // 16 < k <= 64), no shared inputs, one chunk per layer side, so a workgroup that
+    // streams a tile's (or tile group's) x side and then its dy side forms the
+    // tile sums itself and the tile-sum kernel is not launched; pairs widest first.
+    a.paired = bf16_in && (KT == 1 || (KT >= kTilesMinKT && KT <= kMaxPairedKT)) && smax == 1 && a.ordered;
     for (int l = 0; l < grp.n_layers && a.paired; ++l) a.paired = a.layer[l].c_in == 1 && a.layer[l].c_out == 1;
     if (a.paired) {
         int order[kMaxGroup];

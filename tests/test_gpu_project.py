@@ -328,18 +328,20 @@ def test_project_shared_inputs_bitwise_equal():
         assert err <= 1e-3
 
 
-def test_project_paired_equals_unpaired():
-    """At k <= 16 with every layer side in one chunk the stream kernel runs a
-    tile's x and dy items back to back and forms the tile's sum itself (the
-    tile-sum kernel is skipped; the example sums skip empty tiles).  A layer
-    wider than one chunk turns that off for the whole launch.  The narrow
-    layers' outputs must be the same bits either way, and match the oracle."""
+@pytest.mark.parametrize("k", [16, 32, 64])
+def test_project_paired_equals_unpaired(k):
+    """With every layer side in one chunk, a workgroup runs a tile's (k <= 16,
+    stream kernel) or a tile group's (16 < k <= 64, tile-group kernel) x and dy
+    items back to back and forms the tile sums itself (the tile-sum kernel is
+    skipped; the example sums skip empty tiles).  A layer wider than one chunk
+    turns that off for the whole launch.  The narrow layers' outputs must be
+    the same bits either way, and match the oracle."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import dev, host, normwise, say
-    say("[project] paired stream items == unpaired (one wide layer in the launch)")
+    say(f"[project] paired items == unpaired (one wide layer in the launch), k={k}")
     g = W.rng(83)
-    B, T, k = 5, 200, 16
+    B, T = 5, 200
     narrow = [(768, 2304), (768, 768), (3072, 768)]
     wide = (512, 16384)           # two chunks on its dy side (chunks of 14,336 columns)
     lens = W.lengths(g, B, 1, T)
