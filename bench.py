@@ -142,7 +142,7 @@ def write_traffic(fetch_csv, write_csv):
         "projection": ("logra::k_project_stream", "k_project_stream",
                        "28 Llama3-8B layers (4 blocks), B=8, T=2048, lengths of steps 0-3, k=16", PROJ_SOURCES,
                        4 * (sum(int(x.sum()) for x in lens) / 4 * per_tok + p_bytes)),
-        "projection_k64": ("logra::k_project_tiles<4>", "k_project_tiles<4>",
+        "projection_k64": ("logra::k_project_tiles<4, true>", "k_project_tiles<4, true> (paired units)",
                            "7 Llama3-8B layers, B=16, T=1024, all valid, k=64", PROJ_SOURCES,
                            16 * 1024 * per_tok + sum(2 * 64 * (a + b) for _, a, b in stream.layers)),
         "scores": ("logra::k_scores_dma", "k_scores_dma", "1,024 x 500,000 x 57,344 bf16", SCORE_SOURCES,
