@@ -368,14 +368,16 @@ def test_project_paired_equals_unpaired(k):
         assert err <= 1e-3
 
 
-def test_project_all_masked_batch_writes_zeros():
-    """No valid token anywhere: no tile is listed and no chunk item runs; every
-    output row (pre-filled with 7.0) must still be written as zeros."""
+@pytest.mark.parametrize("k", [16, 64])
+def test_project_all_masked_batch_writes_zeros(k):
+    """No valid token anywhere: no tile is listed and no item runs (k = 16: the
+    paired stream kernel; k = 64: the paired tile-group kernel); every output
+    row (pre-filled with 7.0) must still be written as zeros."""
     import torch
     import paper_2405_13954_amd as P
     from gpu_util import dev, host, say
-    say("[project] fully masked batch")
-    B, T, k = 3, 130, 16
+    say(f"[project] fully masked batch, k={k}")
+    B, T = 3, 130
     d = W.layer_inputs(12, 0, B, T, 256, 320, k, k, 1.0, 1.0, "bf16", np.zeros(B, dtype=np.int64))
     for out in (torch.float32, torch.bfloat16):
         store = torch.full((B, k * k + 5), 7.0, dtype=out, device="cuda")
