@@ -490,3 +490,60 @@ def test_pca_topk_n4096():
     eerr = float(np.max(np.abs(ev - wev) / wev))
     say(f"  max entry err {err:.2e}, eigenvalue err {eerr:.2e}")
     assert err <= 1e-4 and eerr <= 1e-5
+
+
+def test_pca_topk_n14336_k64_known_eigenpairs():
+    """The top-64 eigenvectors at the largest factor size (n = 14,336; p = 128:
+    the four-wave column Cholesky, the chunk sums on the chip, the logged
+    rotations and their replay, the register C Q pipeline, four Ritz-vector
+    groups).  C = H_u H_v D H_v H_u, two Householder reflections H_w = I - 2 w
+    w^T (random unit u, v) of a diagonal with a geometric spectrum (1e3 0.95^r,
+    in random order), so the eigenpairs are known in closed form: eigenvalue
+    D_ii with eigenvector H_u H_v e_i.  C is built in float64 and rounded to
+    fp32 (which moves the top-64 eigenvalues by about 1e-9 relative and the
+    eigenvector entries by about 1e-6).  Entries to 1e-4 (fp32 products,
+    neighbour gaps of 5%), Ritz values to 1e-5 relative, and the sign rule."""
+    import torch
+    import paper_2405_13954_amd as P
+    from gpu_util import host, say
+    n, k = 14336, 64
+    say(f"[full pca] n={n} k={k}, closed-form eigenpairs")
+    g = W.rng(67)
+    d = 1e3 * 0.95 ** np.arange(n)
+    perm = g.permutation(n)
+    D = np.empty(n)
+    D[perm] = d
+    u = g.standard_normal(n)
+    u /= np.linalg.norm(u)
+    v = g.standard_normal(n)
+    v /= np.linalg.norm(v)
+    # H M H = M - 2 w (M w)^T - 2 (M w) w^T + 4 (w^T M w) w w^T for symmetric M
+    M = np.diag(D)
+    for w in (v, u):
+        Mw = M @ w
+        c = float(w @ Mw)
+        M -= 2.0 * np.outer(w, Mw)
+        M -= 2.0 * np.outer(Mw, w)
+        M += 4.0 * c * np.outer(w, w)
+        del Mw
+    C = torch.from_numpy(M.astype(np.float32)).cuda()
+    del M
+    Pt = torch.empty((k, n), dtype=torch.float32, device="cuda")
+    ev = torch.empty(k, dtype=torch.float32, device="cuda")
+    P.logra_pca_topk(C, k, Pt, eigvals=ev, iters=30)
+    torch.cuda.synchronize()
+    got, ev = host(Pt).astype(np.float64), host(ev).astype(np.float64)
+    err = 0.0
+    for e in range(k):
+        i = perm[e]   # D[perm[e]] is the e-th largest
+        x = np.zeros(n)
+        x[i] = 1.0
+        x -= 2.0 * v * v[i]
+        x -= 2.0 * u * (u @ x)
+        s = 1.0 if np.dot(got[e], x) >= 0 else -1.0
+        err = max(err, float(np.max(np.abs(s * got[e] - x))))
+        piv = int(np.argmax(np.abs(got[e])))
+        assert got[e, piv] > 0, f"row {e}: the sign rule"
+    eerr = float(np.max(np.abs(ev - d[:k]) / d[:k]))
+    say(f"  max entry err {err:.2e}, Ritz value err {eerr:.2e}")
+    assert err <= 1e-4 and eerr <= 1e-5
