@@ -480,7 +480,8 @@ def pca_sub_leg(args, torch, P, blk, lens, mask, k):
     SYRK over one batch of B=8 ragged sequences for the gate layer's input x
     (n = 4096) and output gradient dy (n = 14,336), timed over back-to-back
     calls with HIP events; then the top-k eigenvectors of each factor (30 subspace
-    iterations).  Algorithmic flops of a SYRK call: valid tokens x n (n + 1)
+    iterations), and for dy also its top-64 (the projection width of the k = 64
+    block).  Algorithmic flops of a SYRK call: valid tokens x n (n + 1)
     (the upper triangle of the symmetric product).  Then all eleven KFAC
     factors of the block in one grouped launch (block_group), beside the same
     factors as eleven calls."""
@@ -505,11 +506,24 @@ def pca_sub_leg(args, torch, P, blk, lens, mask, k):
             P.logra_pca_topk(C, k, Pk, iters=30, ws=pws)
             if timed:
                 te.stop(e0)
+        k64_ms = None
+        if n == 14336:   # the top-64 at the widest factor
+            P64 = torch.empty((64, n), dtype=torch.bfloat16, device="cuda")
+            pws64 = torch.empty(P.logra_pca_ws_size(n, 64), dtype=torch.uint8, device="cuda")
+            t64 = EventTimer(torch)
+            for timed in (False, True):
+                e0 = t64.start() if timed else None
+                P.logra_pca_topk(C, 64, P64, iters=30, ws=pws64)
+                if timed:
+                    t64.stop(e0)
+            torch.cuda.synchronize()
+            k64_ms = t64.mean_ms()
+            del P64, pws64
         torch.cuda.synchronize()
         flops = float(tokens) * n * (n + 1)
         tf = flops / (t.mean_ms() * 1e-3) / 1e12
         traffic, ratio = measured_traffic("act_cov", PCA_SOURCES) if n == 14336 else (None, None)
-        out[name] = {"n": n, "syrk_ms": t.mean_ms(), "pca_topk_ms": te.mean_ms(),
+        out[name] = {"n": n, "syrk_ms": t.mean_ms(), "pca_topk_ms": te.mean_ms(), "pca_topk_k64_ms": k64_ms,
                      "roofline": {"bound": "mfma", "achieved": tf, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                   "frac": tf / BF16_PEAK_TFLOPS, "flops_per_launch": flops, "traffic": traffic,
                                   "traffic_over_algorithmic": ratio,
