@@ -43,10 +43,10 @@
 //     64-column slabs of C and Q copied into an LDS ring; wider: 128-bit
 //     loads into a register pipeline.  Column ranges (splits) give about
 //     2048 workgroups; their partials are summed in split order.
-//  3. k_gram_part: fp64 partial sums of X^T Y over 256-row chunks (X^T X for
+//  3. k_gram_part: fp64 partial sums of X^T Y over 64-row chunks (X^T X for
 //     the orthonormalisation, Z^T Q for Rayleigh-Ritz), fixed order.
-//  4. k_chol_inv_cols (one workgroup): the chunk sums (for p > 64 summed on
-//     the chip first by k_sum_parts), a shifted Cholesky Z^T Z + eps tr/p I =
+//  4. k_chol_inv_cols (one workgroup): the chunk sums (summed on the chip
+//     first by k_sum_parts), a shifted Cholesky Z^T Z + eps tr/p I =
 //     R^T R and R^{-1} in fp64, columns in registers and each step's row
 //     broadcast through LDS (p <= 64: one wave; wider: four waves, one
 //     barrier per step).
@@ -464,7 +464,7 @@ __global__ __launch_bounds__(256) void k_act_cov_f32(const float *__restrict__ a
 // n4 = n rounded up to 4 and every element past n or p zero.  Four
 // consecutive rows of one column (the B operand of a 16x16x4 MFMA) are then
 // one 128-bit load, and a run of rows is one contiguous range.
-constexpr int kGramRows = 256;   // rows per partial sum of a Gram matrix
+constexpr int kGramRows = 64;    // rows per partial sum of a Gram matrix
 constexpr int kGramChunk = 64;   // rows staged in LDS at a time
 constexpr int kMaxP = 128;       // subspace width (at most 2 k for k <= 64)
 constexpr int kCqStages = 3;     // register pipeline depth of k_cq_regs
@@ -737,12 +737,13 @@ __global__ __launch_bounds__(256) void k_cq_sum(const f32x4 *__restrict__ Zs, in
 }
 
 // Partial Gram sums G_c[a][b] = sum over rows r of chunk c of X[r][a] Y[r][b]
-// (fp64), a, b < p, for X, Y in row quads (n4 rows, zero past n).  Rows are
-// staged through LDS 64 at a time, the next 64 loaded into registers while
-// the current ones are summed; an LDS read of 128 bits gives one column's
-// values in four consecutive rows.  PMAX (32, 64 or 128) bounds p; a
-// workgroup forms at most 4096 of the p x p sums (16 per thread), the
-// blockIdx.y-th group of them.
+// (fp64), a, b < p, for X, Y in row quads (n4 rows, zero past n), one
+// workgroup per chunk of kGramRows rows (64: 224 workgroups at n = 14336).
+// Rows are staged through LDS kGramChunk at a time (a longer chunk loads the
+// next rows into registers while the current ones are summed); an LDS read
+// of 128 bits gives one column's values in four consecutive rows.  PMAX (32,
+// 64 or 128) bounds p; a workgroup forms at most 4096 of the p x p sums (16
+// per thread), the blockIdx.y-th group of them.
 template <int PMAX>
 __global__ __launch_bounds__(256) void k_gram_part(const float *__restrict__ X, const float *__restrict__ Y, int n,
                                                    int p, int pp, double *__restrict__ part) {
@@ -851,10 +852,10 @@ __device__ __forceinline__ void sum_partials(const double *__restrict__ part, in
 
 // G = the sum of the chunk partials, in chunk order (the order sum_partials
 // takes), written over chunk 0's slot: a thread reads all of its element's
-// chunks before it writes.  The partials of a wide Gram matrix (p = 128:
-// 7 MB at n = 14336) are too much for one workgroup to gather; spread over
-// the chip they take a few microseconds, and the one-workgroup kernels then
-// read a single chunk.
+// chunks before it writes.  The Gram partials come in 64-row chunks (224 at
+// n = 14336: 1.8 MB at p = 32, 29 MB at p = 128), too many for one workgroup
+// to gather; spread over the chip they take a few microseconds, and the
+// one-workgroup kernels then read a single chunk.
 __global__ __launch_bounds__(256) void k_sum_parts(double *__restrict__ part, int chunks, int np) {
     const int e = blockIdx.x * 256 + threadIdx.x;
     if (e >= np) return;
@@ -1467,10 +1468,10 @@ hipError_t launch_cq(const PcaLayout &L, const float *C, int n, int pp, const fl
     return hipGetLastError();
 }
 
-// Sums the Gram partials on the chip when there are many of them (p > 64);
-// returns the chunk count left for the one-workgroup kernel that follows.
+// Sums the Gram partials on the chip; returns the chunk count left for the
+// one-workgroup kernel that follows.
 int sum_parts(double *part, int chunks, int p, hipStream_t s) {
-    if (p <= 64 || chunks == 1) return chunks;
+    if (chunks == 1) return chunks;
     hipLaunchKernelGGL(k_sum_parts, dim3(static_cast<unsigned>((p * p + 255) / 256)), dim3(256), 0, s, part, chunks,
                        p * p);
     return 1;
