@@ -543,7 +543,10 @@ __device__ __forceinline__ void cq_fold_store(const f32x4 (&acc)[MR][NB], f32x4 
 // rows of C and streams the range in 64-column slabs: each slab's R rows of
 // C (256 bytes per row, whole cache lines) and the 16 row quads of Q it
 // meets are copied straight into an LDS ring by asynchronous global-to-LDS
-// copies, two slabs ahead.  Wave w takes the slab's 16-column step w: lane
+// copies, one slab ahead: two stages (48 KB at p = 32) let three workgroups
+// share a CU, whose copies overlap one another's MFMAs (at n = 14336, p = 32:
+// 154 us per pass; three stages and two workgroups 170 us; four stages and
+// one workgroup slower still).  Wave w takes the slab's 16-column step w: lane
 // (row, q) reads columns 4q .. 4q + 3 of that step in each row block and rows
 // 4q .. 4q + 3 of one column of each 16-column block of Q (one 128-bit LDS
 // read each; C's 16-byte chunks sit at chunk ^ (row & 15), so the reads of a
@@ -562,7 +565,7 @@ struct CqDma {
     static constexpr int kC = R * 256;              // bytes of a slab's rows of C
     static constexpr int kQ = 16 * PP * 16;         // bytes of its 16 row quads of Q
     static constexpr int kStage = kC + kQ;
-    static constexpr int kStages = 3;
+    static constexpr int kStages = 2;
     static constexpr int kCopies = (kC + kQ) / 1024 / 4;   // 1 KB copies per wave per slab (MR + NB)
     static_assert(kCopies == MR + NB, "each wave copies MR row groups of C and NB kilobytes of Q");
     static_assert(MR * NB * kWave * 16 <= kStage, "the fold fits in one stage");
@@ -624,9 +627,9 @@ __global__ __launch_bounds__(256) void k_cq_dma(const float *__restrict__ C, int
     for (int i = 0; i < NS - 1; ++i) issue(i, i);
     const int cpos = ((4 * wave + q) ^ row) * 16;   // this lane's chunk within a row of its row blocks
     for (int sl = 0; sl < nslabs; ++sl) {
-        // this wave's copies of slab sl are done when only the later slab's are
-        // pending; after the barrier every wave's are, and every wave has read
-        // slab sl - 1, whose stage the next copies refill
+        // this wave's copies of slab sl are done when at most the NS - 2 later
+        // slabs' copies are pending; after the barrier every wave's are, and
+        // every wave has read slab sl - 1, whose stage the next copies refill
         asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"((NS - 2) * Sh::kCopies) : "memory");
         issue(sl + NS - 1, (sl + NS - 1) % NS);
         const uint8_t *cb = ring + (sl % NS) * Sh::kStage;
