@@ -853,26 +853,34 @@ __device__ __forceinline__ void sum_partials(const double *__restrict__ part, in
     }
 }
 
-// G = the sum of the chunk partials, in chunk order (the order sum_partials
-// takes), written over chunk 0's slot: a thread reads all of its element's
-// chunks before it writes.  The Gram partials come in 64-row chunks (224 at
-// n = 14336: 1.8 MB at p = 32, 29 MB at p = 128), too many for one workgroup
-// to gather; spread over the chip they take a few microseconds, and the
-// one-workgroup kernels then read a single chunk.
+// G = the sum of the chunk partials, written over chunk 0's slot.  The Gram
+// partials come in 64-row chunks (224 at n = 14336: 1.8 MB at p = 32, 29 MB
+// at p = 128), too many for one workgroup to gather; spread over the chip
+// they take a few microseconds, and the one-workgroup kernels then read a
+// single chunk.  A workgroup takes 64 elements; wave w sums the w-th quarter
+// of the chunks of each, in chunk order, and the quarters are added in a
+// fixed order, ((q0 + q1) + q2) + q3, after every chunk has been read.
 __global__ __launch_bounds__(256) void k_sum_parts(double *__restrict__ part, int chunks, int np) {
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    if (e >= np) return;
+    __shared__ double q[4][kWave];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int e = blockIdx.x * kWave + lane;
+    const int per = (chunks + 3) / 4;
+    const int c0 = min(chunks, w * per), c1 = min(chunks, c0 + per);
     double s = 0.0;
-    int c = 0;
-    for (; c + 16 <= chunks; c += 16) {
-        double v[16];
+    if (e < np) {
+        int c = c0;
+        for (; c + 8 <= c1; c += 8) {
+            double v[8];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = part[static_cast<size_t>(c + u) * np + e];
+            for (int u = 0; u < 8; ++u) v[u] = part[static_cast<size_t>(c + u) * np + e];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) s += v[u];
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; c < c1; ++c) s += part[static_cast<size_t>(c) * np + e];
     }
-    for (; c < chunks; ++c) s += part[static_cast<size_t>(c) * np + e];
-    part[e] = s;
+    q[w][lane] = s;
+    __syncthreads();
+    if (w == 0 && e < np) part[e] = ((q[0][lane] + q[1][lane]) + q[2][lane]) + q[3][lane];
 }
 
 // f(std::integral_constant<int, I>{}) for I = 0 .. N - 1, expanded by the
@@ -1475,8 +1483,8 @@ hipError_t launch_cq(const PcaLayout &L, const float *C, int n, int pp, const fl
 // one-workgroup kernel that follows.
 int sum_parts(double *part, int chunks, int p, hipStream_t s) {
     if (chunks == 1) return chunks;
-    hipLaunchKernelGGL(k_sum_parts, dim3(static_cast<unsigned>((p * p + 255) / 256)), dim3(256), 0, s, part, chunks,
-                       p * p);
+    hipLaunchKernelGGL(k_sum_parts, dim3(static_cast<unsigned>((p * p + kWave - 1) / kWave)), dim3(256), 0, s, part,
+                       chunks, p * p);
     return 1;
 }
 
