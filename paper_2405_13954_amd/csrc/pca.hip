@@ -984,10 +984,12 @@ __global__ __launch_bounds__(256) void k_chol_inv_cols(const double *__restrict_
         double *row = buf[j & 1];
         if (h == hj && col) row[c] = c >= j ? a[jj] : 0.0;   // zeros left of the diagonal: no update there
         sync();
-        const double d = row[j];
+        // one wave: the pivot from lane j's register and f from the lane's own
+        // (the values the row holds), so the reciprocal need not wait for LDS
+        const double d = NW == 1 ? readlane_d(a[jj], j) : row[j];
         const double e = d > 0.0 ? d : 1.0;
         if (tid == 0) rdiag[j] = e;
-        const double f = col && c > j ? row[c] / e : 0.0;
+        const double f = col && c > j ? (NW == 1 ? a[jj] : row[c]) / e : 0.0;
         const double keep = a[jj];   // row j itself is final
         axpy_lds<RPT>(a, row + RPT * h, f);
         a[jj] = h == hj ? keep : a[jj];
@@ -1010,10 +1012,11 @@ __global__ __launch_bounds__(256) void k_chol_inv_cols(const double *__restrict_
         const double *Rj = A + j * RS;   // column j of R
         if (h == hj) {
             a[jj] = a[jj] / Rj[j];
-            if (col) row[c] = a[jj];
+            if (NW > 1 && col) row[c] = a[jj];
         }
         sync();
-        const double x = col ? row[c] : 0.0;
+        // one wave: row j of X is the lane's own register
+        const double x = col ? (NW == 1 ? a[jj] : row[c]) : 0.0;
         const double keep = a[jj];   // row j of X is final; R is zero below its diagonal
         axpy_lds<RPT>(a, Rj + RPT * h, x);
         a[jj] = h == hj ? keep : a[jj];
